@@ -1,0 +1,240 @@
+/*
+ * hardkv.h -- C ABI of the Hard-KV decoding-time KV-compression step on MI355X (gfx950).
+ *
+ * Paper: "Hard-KV: Head-Adaptive Regularization for Decoding-time KV Compression".
+ * The step (Sec. 3.1, continuous compression pipeline, Steps 1-3) is
+ *   hk_score          importance of every cached key against an observation window
+ *   hk_calibrate      Logits Calibration into one probability space (Sec. 3.2, Solution 2)
+ *   hk_calibrate_solve_T  per-head temperature for Problem 1 (App. D.1, binary search)
+ *   hk_topp_select    head-adaptive Top-p budget (Sec. 3.2, Problem 1)
+ *   hk_compact        Cascade-Cache rewrite into dense / sparse / condensed tiers
+ *                     (Sec. 3.1 Step 3; Sec. 3.3.1 Rewrite Cache and Sparse Loading)
+ *   hk_decode_attn    paged decode attention over the variable-budget cache with the
+ *                     attention-state merge (App. F)
+ *   hk_append_kv      append-only dense-tier write of one decode step (Sec. 3.1 Step 1)
+ *
+ * Conventions shared by every entry point
+ *   - Every tensor pointer is a DEVICE pointer owned by the caller.  The library never
+ *     allocates, frees or synchronises; it only enqueues kernels on `stream`.
+ *   - Scratch memory is a caller-provided device `workspace` of at least
+ *     hk_workspace_size(op, ...) bytes, 256-byte aligned.
+ *   - Shapes are static: no entry point changes a tensor's size; counts that change
+ *     (pages per head, free-list top) live in device memory and are updated in place.
+ *   - The return value reports argument validation and launch errors synchronously.
+ *     Conditions found while running (page pool exhausted, NaN inputs) are OR-ed as
+ *     HK_FLAG_* bits into a caller-provided device int32 `status` word, which the
+ *     caller clears and reads after its own synchronisation.
+ *   - Calls on one stream run in order; calls that touch the same cache from
+ *     different streams without ordering race.
+ *
+ * Paged Cascade Cache (head-flattened block table, Sec. 3.3.2 P2; App. B.1):
+ *   one "head" = (sequence, KV head); with NS sequences and Hkv KV heads there are
+ *   n_heads = NS * Hkv rows.  Logical slot j of head h lives in physical page
+ *   page_table[h][j / 16], slot j % 16, and is valid when bit (j % 16) of
+ *   page_mask[h][j / 16] is set.  Pages are ordered oldest first; rows hold
+ *   n_pages[h] pages and -1 past them.  S_max = 16 * max_pages logical slots per head.
+ *   Page contents: k_pool / v_pool [num_pages][16][D] in `dtype`.
+ *
+ * Window queries (observation window of the W most recent queries) are window-major:
+ *   q_obs[W][NS][Hq][D].  Query head g belongs to KV head g / G, G = Hq / Hkv.
+ *   The R = G * W rows of a KV head are its G query heads at every window position.
+ */
+#ifndef HARDKV_H_
+#define HARDKV_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ------------------------------------------------------------------ status */
+typedef int32_t hk_status;
+enum {
+  HK_OK = 0,
+  HK_ERR_ARG = 1,        /* null pointer, non-positive size, scalar out of range      */
+  HK_ERR_DTYPE = 2,      /* dtype is not HK_F32 or HK_BF16                             */
+  HK_ERR_SHAPE = 3,      /* unsupported shape: D not 64/128, Hq % Hkv != 0,
+                            G*W > 256, S_max > 32768, ...                              */
+  HK_ERR_ALIGN = 4,      /* a pointer is not 16-byte aligned (256 for workspace)       */
+  HK_ERR_WORKSPACE = 5,  /* workspace smaller than hk_workspace_size()                 */
+  HK_ERR_HIP = 6         /* a kernel launch failed                                     */
+};
+/* bits OR-ed into the device status word */
+enum {
+  HK_FLAG_NOSPACE = 1,   /* hk_compact / hk_append_kv: free list too short; cache left unchanged */
+  HK_FLAG_NAN = 2,       /* a NaN probability was met and given weight 0               */
+  HK_FLAG_RANGE = 4      /* a probability outside [0,1] was clamped                    */
+};
+
+typedef enum { HK_F32 = 0, HK_BF16 = 1 } hk_dtype;
+
+/* One paged Cascade Cache (any number of heads; layers may share one pool). */
+typedef struct {
+  void* k_pool;          /* [num_pages][16][D]                                          */
+  void* v_pool;          /* [num_pages][16][D]                                          */
+  int32_t* page_table;   /* [n_heads][max_pages] physical ids, -1 past n_pages          */
+  uint16_t* page_mask;   /* [n_heads][max_pages] bit t = slot t valid                   */
+  int32_t* n_pages;      /* [n_heads] pages in use                                      */
+  int32_t num_pages;     /* pool capacity (pages)                                       */
+  int32_t max_pages;     /* table width                                                 */
+  hk_dtype dtype;
+} hk_paged_kv;
+
+/* Device page allocator: a stack of free page ids. */
+typedef struct {
+  int32_t* free_ids;     /* [capacity] device; entries [0, *free_top) are free          */
+  int32_t* free_top;     /* device int32                                                */
+  int32_t capacity;
+} hk_allocator;
+
+typedef struct {
+  int32_t NS;            /* sequences in this call (batch x layers)                     */
+  int32_t Hq;            /* query heads per sequence                                    */
+  int32_t Hkv;           /* KV heads per sequence                                       */
+  int32_t D;             /* head dimension: 64 or 128                                   */
+  int32_t W;             /* observation-window length                                   */
+} hk_dims;
+
+enum { HK_OP_SCORE = 0, HK_OP_COMPACT = 1, HK_OP_DECODE = 2, HK_OP_APPEND = 3 };
+
+/* Bytes of workspace entry point `op` needs for these dims and table width. */
+size_t hk_workspace_size(int32_t op, const hk_dims* dims, int32_t max_pages);
+
+/* Name of a hk_status code (flags = 0) or of a single HK_FLAG_* bit (flags = 1). */
+const char* hk_status_string(int32_t code, int32_t flags);
+
+/* ------------------------------------------------------------------ a1: score
+ * Importance of every candidate slot of every KV head against its observation window
+ * (Reduce step of the three-step selection framework, App. E, applied to the raw
+ * attention distribution S of Problem 1, Sec. 3.2; Vanilla/H2O-style attention mass,
+ * Sec. 4 baseline adaptations):
+ *   z[r][j]  = sm_scale * <q_r, k_j>                     (App. F standard attention)
+ *   LSE_r    = log sum_{j valid} exp z[r][j]             computed here, or row_lse_in
+ *   s[h][j]  = log( (1/R) sum_r exp(z[r][j] - LSE_r) )   for candidate slots j
+ *            = -inf for every other slot
+ * Candidates of head h are valid slots older than the dense tier: j < cand_len[h] with
+ * cand_len[h] = 16 * max(0, n_pages[h] - ceil(L_dense / 16)).
+ * Optional redundancy metric (R-KV style pairwise key similarity as a logit-level
+ * transform, Sec. 4; Solution 2 form): with n_ref reference slots ref_slots[h][0..n_ref)
+ * (valid logical slots of head h),
+ *   x_red[h][j] = -max_{i in ref, i != j} cos(k_i, k_j)  for candidates (-inf elsewhere);
+ *   a zero-norm key has cosine 0; an empty reference set gives +1.
+ * Arguments
+ *   q_obs        [W][NS][Hq][D] in kv->dtype
+ *   row_lse_in   [W][NS][Hq] fp32 or NULL (then computed: two passes over K)
+ *   row_lse_out  [W][NS][Hq] fp32 or NULL
+ *   s_attn       [n_heads][S_max] fp32 (written in full)
+ *   cand_len_out [n_heads] int32
+ *   ref_slots    [n_heads][n_ref] int32 or NULL; n_ref in [0, 256]; x_red likewise
+ * Errors: HK_ERR_SHAPE unless D in {64,128}, Hq % Hkv == 0 and G*W <= 256.
+ */
+hk_status hk_score(const hk_dims* dims, const void* q_obs, const hk_paged_kv* kv,
+                   int32_t L_dense, float sm_scale, const float* row_lse_in,
+                   float* row_lse_out, float* s_attn, int32_t* cand_len_out,
+                   const int32_t* ref_slots, int32_t n_ref, float* x_red,
+                   void* workspace, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------ a2: calibrate
+ * Logits Calibration, Solution 2 (Sec. 3.2): each metric m is mapped to a distribution
+ * over the candidates of head h,
+ *   c_m[j] = exp(x_m[j] / T_m[h] - lse_m[h]),  lse_m[h] = log sum_{cand} exp(x_m / T_m[h]),
+ * and the output is the mixture c = sum_m w_m c_m (0 outside candidates).
+ * Candidates: j < cand_len[h] and (page_mask == NULL or bit j%16 of page_mask[h][j/16]).
+ * Arguments
+ *   x[m]    host array of n_metrics device pointers, each [n_heads][S_max] fp32
+ *   T[m]    host array of n_metrics device pointers to [n_heads] fp32, or T == NULL /
+ *           T[m] == NULL for T = 1; every T must be > 0
+ *   w       host array of n_metrics mixture weights
+ *   c_out   [n_heads][S_max] fp32;  lse_out [n_heads][n_metrics] fp32 or NULL
+ * n_metrics in [1, 2].  All -inf candidates give c = 0 and lse = -inf.
+ */
+hk_status hk_calibrate(int32_t n_heads, int32_t S_max, const int32_t* cand_len,
+                       const uint16_t* page_mask, int32_t n_metrics,
+                       const float* const* x, const float* const* T, const float* w,
+                       float* c_out, float* lse_out, hipStream_t stream);
+
+/* ------------------------------------------------------------------ a3: Top-p
+ * Head-adaptive Top-p budget (Sec. 3.2, Problem 1): per head, the smallest prefix of the
+ * candidates ordered by c descending -- ties to the larger slot index, i.e. the more
+ * recent token -- whose mass reaches p.  Fixed-point rule (exact, order-free):
+ *   w_j = floor(c_j * 2^40), Total = sum w, p_q = round(p * 1e6),
+ *   target = ceil(p_q * Total / 1e6), k = min{k : mass of the first k >= target}
+ *   (k = 0 if target = 0), then clamped to [min(k_min, n_cand), min(k_max, n_cand)]
+ *   (k_max <= 0: no cap).  NaN c counts as 0 (HK_FLAG_NAN); c outside [0,1] is clamped
+ *   (HK_FLAG_RANGE).
+ * Outputs
+ *   sel_bits [n_heads][S_max/32] uint32, bit j%32 of word j/32 = slot j selected
+ *   k_out    [n_heads] int32
+ *   sel_mass_out [n_heads] fp32 = (mass of the selected set) / 2^40, or NULL
+ * p in [0, 1].  S_max must be a multiple of 32 and at most 32768.
+ */
+hk_status hk_topp_select(int32_t n_heads, int32_t S_max, const int32_t* cand_len,
+                         const uint16_t* page_mask, const float* c, double p,
+                         int32_t k_min, int32_t k_max, uint32_t* sel_bits, int32_t* k_out,
+                         float* sel_mass_out, int32_t* status, hipStream_t stream);
+
+/* ------------------------------------------------------------------ a2': temperature
+ * Temperature of Problem 1 (Sec. 3.2) by bisection (App. D.1, binary search on T):
+ *   f(T) = M_k(Softmax(x / T)) - target_mass[h], M_k = mass of the Top-k set of x
+ *   (order c desc, ties to the larger slot; invariant in T, App. D.2 theorem).
+ *   Search on log T in [T_lo, T_hi] for `iters` halvings: f(T_mid) > 0 raises the lower
+ *   end, otherwise the upper end comes down; T_out = exp(midpoint of the final bracket).
+ * Arguments: x [n_heads][S_max] fp32; k [n_heads] int32 (the Top-p count of the target
+ * distribution); target_mass [n_heads] fp32; T_out [n_heads] fp32.
+ * 0 < T_lo < T_hi; iters in [1, 64].
+ */
+hk_status hk_calibrate_solve_T(int32_t n_heads, int32_t S_max, const int32_t* cand_len,
+                               const uint16_t* page_mask, const float* x, const int32_t* k,
+                               const float* target_mass, float T_lo, float T_hi,
+                               int32_t iters, float* T_out, hipStream_t stream);
+
+/* ------------------------------------------------------------------ a4: compact
+ * Cascade-Cache rewrite (Sec. 3.1 Step 3; Sec. 3.3.1).  Per head, page positions are
+ * split into age bands: dense = the newest ceil(L_dense/16) pages, sparse = the
+ * floor(L_sparse/16) pages before them, condensed = all older pages.
+ *   condensed: every selected valid slot is copied (K and V rows, bit-exact), in
+ *              ascending logical order, into freshly popped pages filled 16 at a time
+ *              (all full except the last) -- Rewrite Cache; the old pages are pushed back;
+ *   sparse:    pages stay in place with mask &= selection -- Sparse Loading; a page left
+ *              empty is pushed back;
+ *   dense:     untouched.
+ * The new row is [condensed][sparse][dense], still oldest first; n_pages is updated.
+ * Page ids are popped in head order before any is pushed, so the rewrite is out of place
+ * and deterministic.  If the free list is too short, HK_FLAG_NOSPACE is raised and the
+ * cache is left exactly as it was.
+ */
+hk_status hk_compact(const hk_dims* dims, const hk_paged_kv* kv, const uint32_t* sel_bits,
+                     int32_t L_dense, int32_t L_sparse, const hk_allocator* alloc,
+                     int32_t* status, void* workspace, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------ a5: decode
+ * One decode step of attention for every query head over its KV head's valid slots
+ * (App. F):  o = sum_j Softmax_j(sm_scale q.k_j) v_j,  lse = log sum_j exp(sm_scale q.k_j).
+ * Split-K partial states over page ranges are combined with the merge operator of App. F.
+ * q [NS][Hq][D] in kv->dtype; o [NS][Hq][D] fp32; lse [NS][Hq] fp32 (may point into a
+ * window ring).  A head with no valid slot gives o = 0, lse = -inf.
+ */
+hk_status hk_decode_attn(const hk_dims* dims, const void* q, const hk_paged_kv* kv,
+                         float sm_scale, float* o, float* lse, void* workspace,
+                         size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------ a6: append
+ * Append-only write of one decode step's K and V into the dense tier (Sec. 3.1 Step 1):
+ * for each head the new token goes one past the highest valid slot of its newest page,
+ * or into slot 0 of a page popped from the allocator when that page is full (or the
+ * row is empty).  k_new, v_new [NS][Hkv][D] in kv->dtype.  Pops happen in head order.
+ * If the free list is too short or a row is full (n_pages == max_pages) the step is
+ * skipped for every head and HK_FLAG_NOSPACE is raised.
+ */
+hk_status hk_append_kv(const hk_dims* dims, const hk_paged_kv* kv, const void* k_new,
+                       const void* v_new, const hk_allocator* alloc, int32_t* status,
+                       void* workspace, size_t ws_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HARDKV_H_ */

@@ -1,0 +1,212 @@
+"""Python binding of libhardkv (Hard-KV decoding-time compression step on MI355X).
+
+Argument marshalling only: every step runs in the HIP kernels of libhardkv.so.
+Torch tensors provide device memory and the current stream; each wrapper passes
+their device pointers to the C entry point of the same name (include/hardkv.h)
+and raises HardKVError on a non-zero status.  There is no fallback: if the
+library is missing, importing the entry points raises.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import torch
+
+__all__ = ["HardKVError", "lib", "PagedKV", "Allocator", "hk_score", "hk_calibrate",
+           "hk_calibrate_solve_T", "hk_topp_select", "hk_compact", "hk_decode_attn",
+           "hk_append_kv", "hk_workspace_size", "hk_status_string", "OP_SCORE", "OP_COMPACT",
+           "OP_DECODE", "OP_APPEND", "FLAG_NOSPACE", "FLAG_NAN", "FLAG_RANGE", "LIB_PATH"]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhardkv.so")
+
+HK_F32, HK_BF16 = 0, 1
+OP_SCORE, OP_COMPACT, OP_DECODE, OP_APPEND = 0, 1, 2, 3
+FLAG_NOSPACE, FLAG_NAN, FLAG_RANGE = 1, 2, 4
+EXPORTED = ["hk_score", "hk_calibrate", "hk_calibrate_solve_T", "hk_topp_select", "hk_compact",
+            "hk_decode_attn", "hk_append_kv", "hk_workspace_size", "hk_status_string"]
+
+
+class HardKVError(RuntimeError):
+    pass
+
+
+class hk_dims(C.Structure):
+    _fields_ = [("NS", C.c_int32), ("Hq", C.c_int32), ("Hkv", C.c_int32), ("D", C.c_int32),
+                ("W", C.c_int32)]
+
+
+class hk_paged_kv(C.Structure):
+    _fields_ = [("k_pool", C.c_void_p), ("v_pool", C.c_void_p), ("page_table", C.c_void_p),
+                ("page_mask", C.c_void_p), ("n_pages", C.c_void_p), ("num_pages", C.c_int32),
+                ("max_pages", C.c_int32), ("dtype", C.c_int32)]
+
+
+class hk_allocator(C.Structure):
+    _fields_ = [("free_ids", C.c_void_p), ("free_top", C.c_void_p), ("capacity", C.c_int32)]
+
+
+_lib = None
+
+
+def lib():
+    """Load libhardkv.so (built in-tree by paper_2606_28831_amd.build)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise HardKVError(f"{LIB_PATH} is missing: build it with "
+                              "`python -m paper_2606_28831_amd.build` (no fallback exists)")
+        L = C.CDLL(LIB_PATH)
+        P, I32, SZ, F, D = C.c_void_p, C.c_int32, C.c_size_t, C.c_float, C.c_double
+        L.hk_workspace_size.restype = SZ
+        L.hk_workspace_size.argtypes = [I32, C.POINTER(hk_dims), I32]
+        L.hk_status_string.restype = C.c_char_p
+        L.hk_status_string.argtypes = [I32, I32]
+        L.hk_score.restype = I32
+        L.hk_score.argtypes = [C.POINTER(hk_dims), P, C.POINTER(hk_paged_kv), I32, F, P, P, P, P,
+                               P, I32, P, P, SZ, P]
+        L.hk_calibrate.restype = I32
+        L.hk_calibrate.argtypes = [I32, I32, P, P, I32, C.POINTER(C.c_void_p),
+                                   C.POINTER(C.c_void_p), C.POINTER(C.c_float), P, P, P]
+        L.hk_topp_select.restype = I32
+        L.hk_topp_select.argtypes = [I32, I32, P, P, P, D, I32, I32, P, P, P, P, P]
+        L.hk_calibrate_solve_T.restype = I32
+        L.hk_calibrate_solve_T.argtypes = [I32, I32, P, P, P, P, P, F, F, I32, P, P]
+        L.hk_compact.restype = I32
+        L.hk_compact.argtypes = [C.POINTER(hk_dims), C.POINTER(hk_paged_kv), P, I32, I32,
+                                 C.POINTER(hk_allocator), P, P, SZ, P]
+        L.hk_decode_attn.restype = I32
+        L.hk_decode_attn.argtypes = [C.POINTER(hk_dims), P, C.POINTER(hk_paged_kv), F, P, P, P,
+                                     SZ, P]
+        L.hk_append_kv.restype = I32
+        L.hk_append_kv.argtypes = [C.POINTER(hk_dims), C.POINTER(hk_paged_kv), P, P,
+                                   C.POINTER(hk_allocator), P, P, SZ, P]
+        _lib = L
+    return _lib
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("expected a torch.Tensor")
+    if not t.is_contiguous():
+        raise HardKVError("tensor arguments must be contiguous")
+    return C.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return C.c_void_p(stream.cuda_stream)
+
+
+def _check(code: int, name: str):
+    if code != 0:
+        msg = lib().hk_status_string(code, 0).decode()
+        raise HardKVError(f"{name}: {msg}")
+
+
+def hk_status_string(code: int, flags: bool = False) -> str:
+    return lib().hk_status_string(int(code), int(bool(flags))).decode()
+
+
+def dims(NS, Hq, Hkv, D, W=0) -> hk_dims:
+    return hk_dims(int(NS), int(Hq), int(Hkv), int(D), int(W))
+
+
+class PagedKV:
+    """Device tensors of one paged Cascade Cache plus its C descriptor."""
+
+    def __init__(self, k_pool, v_pool, page_table, page_mask, n_pages):
+        self.k_pool, self.v_pool = k_pool, v_pool
+        self.page_table, self.page_mask, self.n_pages = page_table, page_mask, n_pages
+        if k_pool.dtype == torch.bfloat16:
+            dt = HK_BF16
+        elif k_pool.dtype == torch.float32:
+            dt = HK_F32
+        else:
+            raise HardKVError("cache dtype must be bfloat16 or float32")
+        self.desc = hk_paged_kv(k_pool.data_ptr(), v_pool.data_ptr() if v_pool is not None else None,
+                                page_table.data_ptr(), page_mask.data_ptr(), n_pages.data_ptr(),
+                                k_pool.shape[0], page_table.shape[1], dt)
+
+    def rows(self, first_head: int, n_heads: int) -> "PagedKV":
+        """A view of heads [first_head, first_head + n_heads) (e.g. one layer)."""
+        sl = slice(first_head, first_head + n_heads)
+        return PagedKV(self.k_pool, self.v_pool, self.page_table[sl], self.page_mask[sl],
+                       self.n_pages[sl])
+
+    @property
+    def max_pages(self):
+        return self.page_table.shape[1]
+
+
+class Allocator:
+    def __init__(self, free_ids, free_top):
+        self.free_ids, self.free_top = free_ids, free_top
+        self.desc = hk_allocator(free_ids.data_ptr(), free_top.data_ptr(), free_ids.shape[0])
+
+
+def hk_workspace_size(op: int, d: hk_dims, max_pages: int) -> int:
+    return int(lib().hk_workspace_size(int(op), C.byref(d), int(max_pages)))
+
+
+def workspace(op: int, d: hk_dims, max_pages: int, device) -> torch.Tensor:
+    n = max(256, hk_workspace_size(op, d, max_pages))
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def hk_score(d: hk_dims, q_obs, kv: PagedKV, L_dense: int, sm_scale: float, s_attn, cand_len,
+             row_lse_in=None, row_lse_out=None, ref_slots=None, n_ref: int = 0, x_red=None,
+             ws=None, stream=None):
+    _check(lib().hk_score(C.byref(d), _ptr(q_obs), C.byref(kv.desc), int(L_dense),
+                          float(sm_scale), _ptr(row_lse_in), _ptr(row_lse_out), _ptr(s_attn),
+                          _ptr(cand_len), _ptr(ref_slots), int(n_ref), _ptr(x_red), _ptr(ws),
+                          ws.numel() if ws is not None else 0, _stream(stream)), "hk_score")
+
+
+def hk_calibrate(n_heads: int, S_max: int, cand_len, page_mask, xs, Ts, weights, c_out,
+                 lse_out=None, stream=None):
+    m = len(xs)
+    xa = (C.c_void_p * m)(*[t.data_ptr() for t in xs])
+    Ta = None
+    if Ts is not None:
+        Ta = (C.c_void_p * m)(*[(t.data_ptr() if t is not None else None) for t in Ts])
+    wa = (C.c_float * m)(*[float(w) for w in weights])
+    _check(lib().hk_calibrate(int(n_heads), int(S_max), _ptr(cand_len), _ptr(page_mask), m, xa,
+                              Ta, wa, _ptr(c_out), _ptr(lse_out), _stream(stream)), "hk_calibrate")
+
+
+def hk_topp_select(n_heads: int, S_max: int, cand_len, page_mask, c, p: float, sel_bits, k_out,
+                   k_min: int = 1, k_max: int = 0, sel_mass=None, status=None, stream=None):
+    _check(lib().hk_topp_select(int(n_heads), int(S_max), _ptr(cand_len), _ptr(page_mask), _ptr(c),
+                                float(p), int(k_min), int(k_max), _ptr(sel_bits), _ptr(k_out),
+                                _ptr(sel_mass), _ptr(status), _stream(stream)), "hk_topp_select")
+
+
+def hk_calibrate_solve_T(n_heads: int, S_max: int, cand_len, page_mask, x, k, target_mass, T_out,
+                         T_lo: float = 1e-4, T_hi: float = 1e4, iters: int = 40, stream=None):
+    _check(lib().hk_calibrate_solve_T(int(n_heads), int(S_max), _ptr(cand_len), _ptr(page_mask),
+                                      _ptr(x), _ptr(k), _ptr(target_mass), float(T_lo),
+                                      float(T_hi), int(iters), _ptr(T_out), _stream(stream)),
+           "hk_calibrate_solve_T")
+
+
+def hk_compact(d: hk_dims, kv: PagedKV, sel_bits, L_dense: int, L_sparse: int, alloc: Allocator,
+               status, ws, stream=None):
+    _check(lib().hk_compact(C.byref(d), C.byref(kv.desc), _ptr(sel_bits), int(L_dense),
+                            int(L_sparse), C.byref(alloc.desc), _ptr(status), _ptr(ws), ws.numel(),
+                            _stream(stream)), "hk_compact")
+
+
+def hk_decode_attn(d: hk_dims, q, kv: PagedKV, sm_scale: float, o, lse, ws, stream=None):
+    _check(lib().hk_decode_attn(C.byref(d), _ptr(q), C.byref(kv.desc), float(sm_scale), _ptr(o),
+                                _ptr(lse), _ptr(ws), ws.numel(), _stream(stream)), "hk_decode_attn")
+
+
+def hk_append_kv(d: hk_dims, kv: PagedKV, k_new, v_new, alloc: Allocator, status, ws=None,
+                 stream=None):
+    _check(lib().hk_append_kv(C.byref(d), C.byref(kv.desc), _ptr(k_new), _ptr(v_new),
+                              C.byref(alloc.desc), _ptr(status), _ptr(ws),
+                              ws.numel() if ws is not None else 0, _stream(stream)), "hk_append_kv")

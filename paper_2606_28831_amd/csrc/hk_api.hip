@@ -1,0 +1,216 @@
+// C ABI of libhardkv: argument validation and dispatch to the HIP launchers.
+// Declarations, argument meaning and error behaviour: include/hardkv.h.
+#include <cmath>
+#include <cstdint>
+
+#include "hk_internal.h"
+
+bool hk_decode_supports_group(int G);
+
+namespace {
+
+constexpr int kMaxSlots = 32768;   // per-head logical slots held in registers by the selectors
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned256(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 255u) == 0; }
+
+hk_status check_dims(const hk_dims* d, bool need_w) {
+  if (!d) return HK_ERR_ARG;
+  if (d->NS <= 0 || d->Hq <= 0 || d->Hkv <= 0 || d->D <= 0) return HK_ERR_ARG;
+  if (need_w && d->W <= 0) return HK_ERR_ARG;
+  if (d->D != 64 && d->D != 128) return HK_ERR_SHAPE;
+  if (d->Hq % d->Hkv != 0) return HK_ERR_SHAPE;
+  if ((long long)d->NS * d->Hkv > 65535) return HK_ERR_SHAPE;
+  return HK_OK;
+}
+
+hk_status check_kv(const hk_paged_kv* kv, bool need_v) {
+  if (!kv || !kv->k_pool || !kv->page_table || !kv->page_mask || !kv->n_pages) return HK_ERR_ARG;
+  if (need_v && !kv->v_pool) return HK_ERR_ARG;
+  if (kv->dtype != HK_F32 && kv->dtype != HK_BF16) return HK_ERR_DTYPE;
+  if (kv->num_pages <= 0 || kv->max_pages <= 0) return HK_ERR_ARG;
+  if (kv->max_pages % 2 != 0) return HK_ERR_SHAPE;                 // S_max multiple of 32
+  if (!aligned16(kv->k_pool) || (need_v && !aligned16(kv->v_pool))) return HK_ERR_ALIGN;
+  if (!aligned16(kv->page_table) || !aligned16(kv->page_mask) || !aligned16(kv->n_pages))
+    return HK_ERR_ALIGN;
+  return HK_OK;
+}
+
+hk_status check_rows(int n_heads, int S_max, const int32_t* cand_len) {
+  if (n_heads <= 0 || S_max <= 0 || !cand_len) return HK_ERR_ARG;
+  if (S_max % 32 != 0 || S_max > kMaxSlots) return HK_ERR_SHAPE;
+  if (n_heads > 1 << 20) return HK_ERR_SHAPE;
+  return HK_OK;
+}
+
+hk_status launched(hipError_t e) { return e == hipSuccess ? HK_OK : HK_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+size_t hk_workspace_size(int32_t op, const hk_dims* d, int32_t max_pages) {
+  if (!d || max_pages <= 0) return 0;
+  switch (op) {
+    case HK_OP_SCORE: return hk_score_ws(d->NS, d->Hq, d->Hkv, d->D, d->W, max_pages);
+    case HK_OP_COMPACT: return hk_compact_ws(d->NS * d->Hkv, max_pages);
+    case HK_OP_DECODE: return hk_decode_ws(d->NS, d->Hq, d->Hkv, d->D, max_pages);
+    case HK_OP_APPEND: return hk_append_ws(d->NS, d->Hkv);
+    default: return 0;
+  }
+}
+
+const char* hk_status_string(int32_t code, int32_t flags) {
+  if (flags) {
+    switch (code) {
+      case HK_FLAG_NOSPACE: return "HK_FLAG_NOSPACE: page pool exhausted, cache left unchanged";
+      case HK_FLAG_NAN: return "HK_FLAG_NAN: NaN probability given weight 0";
+      case HK_FLAG_RANGE: return "HK_FLAG_RANGE: probability outside [0,1] clamped";
+      default: return "unknown flag";
+    }
+  }
+  switch (code) {
+    case HK_OK: return "HK_OK";
+    case HK_ERR_ARG: return "HK_ERR_ARG: null pointer or size/scalar out of range";
+    case HK_ERR_DTYPE: return "HK_ERR_DTYPE: dtype must be HK_F32 or HK_BF16";
+    case HK_ERR_SHAPE: return "HK_ERR_SHAPE: unsupported shape";
+    case HK_ERR_ALIGN: return "HK_ERR_ALIGN: pointer not 16-byte (workspace: 256-byte) aligned";
+    case HK_ERR_WORKSPACE: return "HK_ERR_WORKSPACE: workspace smaller than hk_workspace_size()";
+    case HK_ERR_HIP: return "HK_ERR_HIP: kernel launch failed";
+    default: return "unknown status";
+  }
+}
+
+hk_status hk_score(const hk_dims* dims, const void* q_obs, const hk_paged_kv* kv, int32_t L_dense,
+                   float sm_scale, const float* row_lse_in, float* row_lse_out, float* s_attn,
+                   int32_t* cand_len_out, const int32_t* ref_slots, int32_t n_ref, float* x_red,
+                   void* workspace, size_t ws_bytes, hipStream_t stream) {
+  hk_status e = check_dims(dims, true);
+  if (e) return e;
+  if ((e = check_kv(kv, false))) return e;
+  if (!q_obs || !s_attn || !cand_len_out) return HK_ERR_ARG;
+  if (L_dense < 0 || !(sm_scale > 0.f) || !std::isfinite(sm_scale)) return HK_ERR_ARG;
+  const int G = dims->Hq / dims->Hkv;
+  if (G * dims->W > 256) return HK_ERR_SHAPE;
+  if ((x_red != nullptr) != (ref_slots != nullptr)) return HK_ERR_ARG;
+  if (x_red && (n_ref < 0 || n_ref > 256)) return HK_ERR_ARG;
+  if (!aligned16(q_obs)) return HK_ERR_ALIGN;
+  if (hk_score_lds_bytes(dims->Hq / dims->Hkv * dims->W, dims->D, kv->dtype == HK_BF16 ? 2 : 4,
+                         x_red != nullptr) > 160 * 1024)
+    return HK_ERR_SHAPE;
+  const size_t need = hk_score_ws(dims->NS, dims->Hq, dims->Hkv, dims->D, dims->W, kv->max_pages);
+  if (!row_lse_in) {
+    if (!workspace || ws_bytes < need) return HK_ERR_WORKSPACE;
+    if (!aligned256(workspace)) return HK_ERR_ALIGN;
+  }
+  hk_score_args a;
+  a.q_obs = q_obs;
+  a.kv = kv;
+  a.NS = dims->NS;
+  a.Hq = dims->Hq;
+  a.Hkv = dims->Hkv;
+  a.D = dims->D;
+  a.W = dims->W;
+  a.L_dense = L_dense;
+  a.sm_scale = sm_scale;
+  a.row_lse_in = row_lse_in;
+  a.row_lse_out = row_lse_out;
+  a.s_attn = s_attn;
+  a.cand_len = cand_len_out;
+  a.ref_slots = ref_slots;
+  a.n_ref = x_red ? n_ref : 0;
+  a.x_red = x_red;
+  a.ws = workspace;
+  return launched(hk_launch_score(a, stream));
+}
+
+hk_status hk_calibrate(int32_t n_heads, int32_t S_max, const int32_t* cand_len,
+                       const uint16_t* page_mask, int32_t n_metrics, const float* const* x,
+                       const float* const* T, const float* w, float* c_out, float* lse_out,
+                       hipStream_t stream) {
+  hk_status e = check_rows(n_heads, S_max, cand_len);
+  if (e) return e;
+  if (n_metrics < 1 || n_metrics > 2 || !x || !w || !c_out) return HK_ERR_ARG;
+  for (int m = 0; m < n_metrics; ++m)
+    if (!x[m] || !std::isfinite(w[m])) return HK_ERR_ARG;
+  const float* T0 = T ? T[0] : nullptr;
+  const float* T1 = (T && n_metrics > 1) ? T[1] : nullptr;
+  return launched(hk_launch_calibrate(n_heads, S_max, cand_len, page_mask, n_metrics, x[0],
+                                      n_metrics > 1 ? x[1] : nullptr, T0, T1, w[0],
+                                      n_metrics > 1 ? w[1] : 0.f, c_out, lse_out, stream));
+}
+
+hk_status hk_topp_select(int32_t n_heads, int32_t S_max, const int32_t* cand_len,
+                         const uint16_t* page_mask, const float* c, double p, int32_t k_min,
+                         int32_t k_max, uint32_t* sel_bits, int32_t* k_out, float* sel_mass_out,
+                         int32_t* status, hipStream_t stream) {
+  hk_status e = check_rows(n_heads, S_max, cand_len);
+  if (e) return e;
+  if (!c || !sel_bits || !k_out) return HK_ERR_ARG;
+  if (!(p >= 0.0 && p <= 1.0)) return HK_ERR_ARG;
+  if (!aligned16(sel_bits)) return HK_ERR_ALIGN;
+  const int p_q = (int)std::nearbyint(p * 1e6);
+  return launched(hk_launch_topp(n_heads, S_max, cand_len, page_mask, c, p_q, k_min, k_max,
+                                 sel_bits, k_out, sel_mass_out, status, stream));
+}
+
+hk_status hk_calibrate_solve_T(int32_t n_heads, int32_t S_max, const int32_t* cand_len,
+                               const uint16_t* page_mask, const float* x, const int32_t* k,
+                               const float* target_mass, float T_lo, float T_hi, int32_t iters,
+                               float* T_out, hipStream_t stream) {
+  hk_status e = check_rows(n_heads, S_max, cand_len);
+  if (e) return e;
+  if (!x || !k || !target_mass || !T_out) return HK_ERR_ARG;
+  if (!(T_lo > 0.f) || !(T_hi > T_lo) || !std::isfinite(T_hi) || iters < 1 || iters > 64)
+    return HK_ERR_ARG;
+  return launched(hk_launch_solve_T(n_heads, S_max, cand_len, page_mask, x, k, target_mass, T_lo,
+                                    T_hi, iters, T_out, stream));
+}
+
+hk_status hk_compact(const hk_dims* dims, const hk_paged_kv* kv, const uint32_t* sel_bits,
+                     int32_t L_dense, int32_t L_sparse, const hk_allocator* alloc, int32_t* status,
+                     void* workspace, size_t ws_bytes, hipStream_t stream) {
+  hk_status e = check_dims(dims, false);
+  if (e) return e;
+  if ((e = check_kv(kv, true))) return e;
+  if (!sel_bits || !alloc || !alloc->free_ids || !alloc->free_top || alloc->capacity <= 0)
+    return HK_ERR_ARG;
+  if (L_dense < 0 || L_sparse < 0) return HK_ERR_ARG;
+  if ((long long)kv->max_pages * 6 > 160 * 1024) return HK_ERR_SHAPE;   // table row staged in LDS
+  const int n_heads = dims->NS * dims->Hkv;
+  if (!workspace || ws_bytes < hk_compact_ws(n_heads, kv->max_pages)) return HK_ERR_WORKSPACE;
+  if (!aligned256(workspace)) return HK_ERR_ALIGN;
+  return launched(hk_launch_compact(n_heads, dims->D, kv, sel_bits, L_dense, L_sparse, alloc,
+                                    status, workspace, stream));
+}
+
+hk_status hk_decode_attn(const hk_dims* dims, const void* q, const hk_paged_kv* kv, float sm_scale,
+                         float* o, float* lse, void* workspace, size_t ws_bytes, hipStream_t stream) {
+  hk_status e = check_dims(dims, false);
+  if (e) return e;
+  if ((e = check_kv(kv, true))) return e;
+  if (!q || !o || !lse) return HK_ERR_ARG;
+  if (!(sm_scale > 0.f) || !std::isfinite(sm_scale)) return HK_ERR_ARG;
+  if (!hk_decode_supports_group(dims->Hq / dims->Hkv)) return HK_ERR_SHAPE;
+  if (!aligned16(q)) return HK_ERR_ALIGN;
+  if (!workspace || ws_bytes < hk_decode_ws(dims->NS, dims->Hq, dims->Hkv, dims->D, kv->max_pages))
+    return HK_ERR_WORKSPACE;
+  if (!aligned256(workspace)) return HK_ERR_ALIGN;
+  return launched(hk_launch_decode(dims->NS, dims->Hq, dims->Hkv, dims->D, q, kv, sm_scale, o, lse,
+                                   workspace, stream));
+}
+
+hk_status hk_append_kv(const hk_dims* dims, const hk_paged_kv* kv, const void* k_new,
+                       const void* v_new, const hk_allocator* alloc, int32_t* status,
+                       void* workspace, size_t ws_bytes, hipStream_t stream) {
+  (void)ws_bytes;
+  hk_status e = check_dims(dims, false);
+  if (e) return e;
+  if ((e = check_kv(kv, true))) return e;
+  if (!k_new || !v_new || !alloc || !alloc->free_ids || !alloc->free_top) return HK_ERR_ARG;
+  if (!aligned16(k_new) || !aligned16(v_new)) return HK_ERR_ALIGN;
+  return launched(hk_launch_append(dims->NS, dims->Hkv, dims->D, kv, k_new, v_new, alloc, status,
+                                   workspace, stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,370 @@
+// a5 / a6: paged decode attention over the variable-budget Cascade Cache, and the
+// append-only dense-tier write of one decode step (gfx950).
+//
+// Decode (App. F): every (sequence, KV head) is split into ranges of pages; a workgroup
+// computes the attention state (o, m, l) of the G query heads of that KV head over its
+// range (each K/V page is read once for all G heads: head expansion), and a merge kernel
+// combines the ranges with the merge operator
+//   o(I u J) = (o(I) SE(I) + o(J) SE(J)) / (SE(I) + SE(J)),  SE(I u J) = SE(I) + SE(J).
+// Only pages below n_pages are visited and page masks drop invalid slots, so the work
+// follows each head's own budget.
+//
+// Lane mapping inside a wave, for one 16-slot page:
+//   scores  lane = 4 * t + c: slot t, quarter c of the head dimension; partial dot
+//           products are summed over the 4 lanes of a slot with two xor-shuffles;
+//   values  lane = LPR * kg + dc: 16-byte chunk dc of the row, slots kg*KPL .. +KPL;
+//           the probabilities reach those lanes by shuffles.
+#include "hk_internal.h"
+
+namespace hk {
+
+constexpr int DEC_NT = 256;
+constexpr int DEC_NW = DEC_NT / 64;
+
+template <typename T, int D, int G>
+__global__ __launch_bounds__(DEC_NT) void decode_split_kernel(
+    const T* __restrict__ q, const T* __restrict__ k_pool, const T* __restrict__ v_pool,
+    const int32_t* __restrict__ table, const uint16_t* __restrict__ masks,
+    const int32_t* __restrict__ n_pages_arr, int Hq, int Hkv, int max_pages, int pps, float c2,
+    float* __restrict__ part, int n_split) {
+  constexpr int ES = sizeof(T);
+  constexpr int DQ = D / 4;                 // dims per quarter
+  constexpr int VEC = 16 / ES;              // elements per 16-byte chunk
+  constexpr int LPR = D / VEC;              // lanes per value row
+  constexpr int KG = 64 / LPR;              // slot groups
+  constexpr int KPL = HK_PAGE / KG;         // slots per lane (values)
+  constexpr int QW = DQ * ES / 4;           // 32-bit words of the query quarter
+  __shared__ float s_m[DEC_NW][G], s_l[DEC_NW][G];
+  __shared__ float s_o[DEC_NW][G][D];
+
+  const int h = blockIdx.y, split = blockIdx.x;
+  const int s = h / Hkv, kv = h % Hkv;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n = n_pages_arr[h];
+  const int p_begin = split * pps, p_end = min(p_begin + pps, n);
+  const int t = lane >> 2, c = lane & 3;
+  const int kg = lane / LPR, dc = lane % LPR;
+
+  uint32_t qw[G][QW];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const uint4* src = reinterpret_cast<const uint4*>(q + ((size_t)s * Hq + kv * G + g) * D + c * DQ);
+#pragma unroll
+    for (int i = 0; i < QW / 4; ++i) {
+      const uint4 u = src[i];
+      qw[g][4 * i + 0] = u.x;
+      qw[g][4 * i + 1] = u.y;
+      qw[g][4 * i + 2] = u.z;
+      qw[g][4 * i + 3] = u.w;
+    }
+  }
+  float m_run[G], l_part[G], o[G][VEC];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    m_run[g] = -INFINITY;
+    l_part[g] = 0.f;
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) o[g][e] = 0.f;
+  }
+  const int32_t* trow = table + (size_t)h * max_pages;
+  const uint16_t* mrow = masks + (size_t)h * max_pages;
+
+  for (int p = p_begin + wave; p < p_end; p += DEC_NW) {
+    const uint32_t m16 = mrow[p];
+    if (m16 == 0u) continue;
+    const size_t page = (size_t)trow[p] * HK_PAGE;
+    uint32_t kw[QW];
+    {
+      const uint4* src = reinterpret_cast<const uint4*>(k_pool + (page + t) * D + c * DQ);
+#pragma unroll
+      for (int i = 0; i < QW / 4; ++i) {
+        const uint4 u = src[i];
+        kw[4 * i + 0] = u.x;
+        kw[4 * i + 1] = u.y;
+        kw[4 * i + 2] = u.z;
+        kw[4 * i + 3] = u.w;
+      }
+    }
+    uint4 vw[KPL];
+#pragma unroll
+    for (int i = 0; i < KPL; ++i)
+      vw[i] = *reinterpret_cast<const uint4*>(v_pool + (page + kg * KPL + i) * D + dc * VEC);
+
+    const bool valid = (m16 >> t) & 1u;
+    float zl[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      float z = 0.f;
+      if constexpr (ES == 2) {
+        typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+#pragma unroll
+        for (int i = 0; i < QW; ++i)
+          z = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, qw[g][i]),
+                                              __builtin_bit_cast(bf16x2, kw[i]), z, false);
+      } else {
+#pragma unroll
+        for (int i = 0; i < QW; ++i) z = fmaf(__uint_as_float(qw[g][i]), __uint_as_float(kw[i]), z);
+      }
+      z += __shfl_xor(z, 1, 64);
+      z += __shfl_xor(z, 2, 64);
+      zl[g] = valid ? z * c2 : -INFINITY;      // log2 units
+    }
+    float pr[G], alpha[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      float pm = zl[g];
+      pm = fmaxf(pm, __shfl_xor(pm, 4, 64));
+      pm = fmaxf(pm, __shfl_xor(pm, 8, 64));
+      pm = fmaxf(pm, __shfl_xor(pm, 16, 64));
+      pm = fmaxf(pm, __shfl_xor(pm, 32, 64));
+      const float mn = fmaxf(m_run[g], pm);     // finite: the page has a valid slot
+      alpha[g] = exp2f(m_run[g] - mn);
+      pr[g] = exp2f(zl[g] - mn);
+      m_run[g] = mn;
+      l_part[g] = l_part[g] * alpha[g] + (c == 0 ? pr[g] : 0.f);
+    }
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) o[g][e] *= alpha[g];
+#pragma unroll
+    for (int i = 0; i < KPL; ++i) {
+      const int src_lane = 4 * (kg * KPL + i);
+      float vf[VEC];
+      const uint32_t vv[4] = {vw[i].x, vw[i].y, vw[i].z, vw[i].w};
+      if constexpr (ES == 2) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          vf[2 * e] = bf16_lo(vv[e]);
+          vf[2 * e + 1] = bf16_hi(vv[e]);
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) vf[e] = __uint_as_float(vv[e]);
+      }
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const float pg = __shfl(pr[g], src_lane, 64);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) o[g][e] = fmaf(pg, vf[e], o[g][e]);
+      }
+    }
+  }
+  // reduce over slot groups (lanes with the same value chunk) and over all lanes for l
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+#pragma unroll
+    for (int x = LPR; x < 64; x <<= 1)
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) o[g][e] += __shfl_xor(o[g][e], x, 64);
+    l_part[g] = wave_sum(l_part[g]);
+    if (lane == 0) {
+      s_m[wave][g] = m_run[g];
+      s_l[wave][g] = l_part[g];
+    }
+    if (lane < LPR)
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) s_o[wave][g][dc * VEC + e] = o[g][e];
+  }
+  __syncthreads();
+  // combine the waves -> one partial state per (head, split, g): [o(D) unnormalised, m, l]
+  for (int idx = threadIdx.x; idx < G * D; idx += DEC_NT) {
+    const int g = idx / D, d = idx % D;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < DEC_NW; ++w) M = fmaxf(M, s_m[w][g]);
+    float L = 0.f, O = 0.f;
+    if (M != -INFINITY)
+#pragma unroll
+      for (int w = 0; w < DEC_NW; ++w) {
+        const float a = exp2f(s_m[w][g] - M);
+        L += s_l[w][g] * a;
+        O += s_o[w][g][d] * a;
+      }
+    float* dst = part + (((size_t)h * n_split + split) * G + g) * (D + 2);
+    dst[d] = O;
+    if (d == 0) {
+      dst[D] = M;
+      dst[D + 1] = L;
+    }
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(D) void decode_merge_kernel(const float* __restrict__ part, int n_split,
+                                                         int G, int Hq, int Hkv, float* __restrict__ o,
+                                                         float* __restrict__ lse) {
+  const int hg = blockIdx.x, h = hg / G, g = hg % G;
+  const int s = h / Hkv, kv = h % Hkv;
+  const float* p = part + ((size_t)h * n_split * G + g) * (D + 2);
+  const size_t stride = (size_t)G * (D + 2);
+  float M = -INFINITY;
+  for (int i = 0; i < n_split; ++i) M = fmaxf(M, p[i * stride + D]);
+  float L = 0.f, O = 0.f;
+  if (M != -INFINITY)
+    for (int i = 0; i < n_split; ++i) {
+      const float a = exp2f(p[i * stride + D] - M);
+      L += p[i * stride + D + 1] * a;
+      O += p[i * stride + threadIdx.x] * a;
+    }
+  const size_t row = (size_t)s * Hq + kv * G + g;
+  o[row * D + threadIdx.x] = (L > 0.f) ? O / L : 0.f;
+  if (threadIdx.x == 0) lse[row] = (L > 0.f) ? (M + __log2f(L)) * kLn2 : -INFINITY;
+}
+
+// ------------------------------------------------------------------ a6: append
+constexpr int AP_NT = 1024;
+
+template <int ROW_BYTES>
+__global__ __launch_bounds__(AP_NT) void append_kernel(
+    int n_heads, int Hkv, char* __restrict__ k_pool, char* __restrict__ v_pool,
+    int32_t* __restrict__ table, uint16_t* __restrict__ masks, int32_t* __restrict__ n_pages,
+    int max_pages, const char* __restrict__ k_new, const char* __restrict__ v_new,
+    int32_t* __restrict__ free_ids, int32_t* __restrict__ free_top, int32_t* __restrict__ status) {
+  __shared__ int lds[AP_NT / 64];
+  __shared__ int s_ok, s_base;
+  const int per = (n_heads + AP_NT - 1) / AP_NT;
+  const int h0 = threadIdx.x * per, h1 = min(h0 + per, n_heads);
+  int need = 0, full = 0;
+  for (int h = h0; h < h1; ++h) {
+    const int n = n_pages[h];
+    const uint32_t m = n > 0 ? masks[(size_t)h * max_pages + n - 1] : 0xffffu;
+    if (m & 0x8000u || n == 0) {
+      need += 1;
+      if (n >= max_pages) full = 1;
+    }
+  }
+  full = __syncthreads_or(full);
+  // exclusive scan of needs in head order
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int x = need;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) lds[wave] = x;
+  __syncthreads();
+  int before = 0, total = 0;
+  for (int w = 0; w < AP_NT / 64; ++w) {
+    if (w < wave) before += lds[w];
+    total += lds[w];
+  }
+  int off = before + x - need;
+  if (threadIdx.x == 0) {
+    const int top = *free_top;
+    s_ok = (!full && total <= top) ? 1 : 0;
+    s_base = top - total;
+    if (!s_ok && status) atomicOr(status, HK_FLAG_NOSPACE);
+    if (s_ok) *free_top = top - total;
+  }
+  __syncthreads();
+  if (!s_ok) return;
+  for (int h = h0; h < h1; ++h) {
+    int n = n_pages[h];
+    const uint32_t m = n > 0 ? masks[(size_t)h * max_pages + n - 1] : 0xffffu;
+    int page, slot;
+    if (m & 0x8000u || n == 0) {
+      page = free_ids[s_base + off];
+      ++off;
+      table[(size_t)h * max_pages + n] = page;
+      masks[(size_t)h * max_pages + n] = 1;
+      n_pages[h] = n + 1;
+      slot = 0;
+    } else {
+      page = table[(size_t)h * max_pages + n - 1];
+      slot = 32 - __clz(m);               // one past the highest valid slot
+      masks[(size_t)h * max_pages + n - 1] = (uint16_t)(m | (1u << slot));
+    }
+    const int s = h / Hkv, kv = h % Hkv;
+    const size_t src = ((size_t)s * Hkv + kv) * ROW_BYTES;
+    const size_t dst = ((size_t)page * HK_PAGE + slot) * ROW_BYTES;
+#pragma unroll
+    for (int i = 0; i < ROW_BYTES / 16; ++i) {
+      *reinterpret_cast<uint4*>(k_pool + dst + 16 * i) = *reinterpret_cast<const uint4*>(k_new + src + 16 * i);
+      *reinterpret_cast<uint4*>(v_pool + dst + 16 * i) = *reinterpret_cast<const uint4*>(v_new + src + 16 * i);
+    }
+  }
+}
+
+template <typename T, int D, int G>
+static void launch_split(dim3 grid, hipStream_t st, const void* q, const hk_paged_kv* kv, int Hq,
+                         int Hkv, int pps, float c2, float* part, int n_split) {
+  hipLaunchKernelGGL((decode_split_kernel<T, D, G>), grid, dim3(DEC_NT), 0, st,
+                     static_cast<const T*>(q), static_cast<const T*>(kv->k_pool),
+                     static_cast<const T*>(kv->v_pool), kv->page_table, kv->page_mask, kv->n_pages,
+                     Hq, Hkv, kv->max_pages, pps, c2, part, n_split);
+}
+
+template <typename T, int D>
+static bool launch_split_g(int G, dim3 grid, hipStream_t st, const void* q, const hk_paged_kv* kv,
+                           int Hq, int Hkv, int pps, float c2, float* part, int n_split) {
+  switch (G) {
+    case 1: launch_split<T, D, 1>(grid, st, q, kv, Hq, Hkv, pps, c2, part, n_split); return true;
+    case 2: launch_split<T, D, 2>(grid, st, q, kv, Hq, Hkv, pps, c2, part, n_split); return true;
+    case 4: launch_split<T, D, 4>(grid, st, q, kv, Hq, Hkv, pps, c2, part, n_split); return true;
+    case 7: launch_split<T, D, 7>(grid, st, q, kv, Hq, Hkv, pps, c2, part, n_split); return true;
+    case 8: launch_split<T, D, 8>(grid, st, q, kv, Hq, Hkv, pps, c2, part, n_split); return true;
+    default: return false;
+  }
+}
+
+constexpr int DEC_PPS = 16;   // pages per split
+
+}  // namespace hk
+
+using namespace hk;
+
+bool hk_decode_supports_group(int G) { return G == 1 || G == 2 || G == 4 || G == 7 || G == 8; }
+
+size_t hk_decode_ws(int NS, int Hq, int Hkv, int D, int max_pages) {
+  const int G = Hq / Hkv, n_split = (max_pages + DEC_PPS - 1) / DEC_PPS;
+  return (size_t)NS * Hkv * n_split * G * (D + 2) * sizeof(float);
+}
+
+hipError_t hk_launch_decode(int NS, int Hq, int Hkv, int D, const void* q, const hk_paged_kv* kv,
+                            float sm_scale, float* o, float* lse, void* ws, hipStream_t st) {
+  const int G = Hq / Hkv, n_heads = NS * Hkv;
+  const int n_split = (kv->max_pages + DEC_PPS - 1) / DEC_PPS;
+  const float c2 = sm_scale * kLog2e;
+  float* part = static_cast<float*>(ws);
+  dim3 grid(n_split, n_heads);
+  const bool bf = kv->dtype == HK_BF16;
+  bool ok;
+  if (bf && D == 128) ok = launch_split_g<uint16_t, 128>(G, grid, st, q, kv, Hq, Hkv, DEC_PPS, c2, part, n_split);
+  else if (bf) ok = launch_split_g<uint16_t, 64>(G, grid, st, q, kv, Hq, Hkv, DEC_PPS, c2, part, n_split);
+  else if (D == 128) ok = launch_split_g<float, 128>(G, grid, st, q, kv, Hq, Hkv, DEC_PPS, c2, part, n_split);
+  else ok = launch_split_g<float, 64>(G, grid, st, q, kv, Hq, Hkv, DEC_PPS, c2, part, n_split);
+  if (!ok) return hipErrorInvalidValue;
+  if (D == 128)
+    hipLaunchKernelGGL(decode_merge_kernel<128>, dim3(n_heads * G), dim3(128), 0, st, part, n_split, G,
+                       Hq, Hkv, o, lse);
+  else
+    hipLaunchKernelGGL(decode_merge_kernel<64>, dim3(n_heads * G), dim3(64), 0, st, part, n_split, G,
+                       Hq, Hkv, o, lse);
+  return hipGetLastError();
+}
+
+size_t hk_append_ws(int NS, int Hkv) {
+  (void)NS;
+  (void)Hkv;
+  return 0;
+}
+
+hipError_t hk_launch_append(int NS, int Hkv, int D, const hk_paged_kv* kv, const void* k_new,
+                            const void* v_new, const hk_allocator* alloc, int32_t* status, void* ws,
+                            hipStream_t st) {
+  (void)ws;
+  const int n_heads = NS * Hkv;
+  const int row_bytes = D * (kv->dtype == HK_BF16 ? 2 : 4);
+  char* kp = static_cast<char*>(kv->k_pool);
+  char* vp = static_cast<char*>(kv->v_pool);
+  const char* kn = static_cast<const char*>(k_new);
+  const char* vn = static_cast<const char*>(v_new);
+  switch (row_bytes) {
+    case 128: hipLaunchKernelGGL((append_kernel<128>), dim3(1), dim3(AP_NT), 0, st, n_heads, Hkv, kp, vp, kv->page_table, kv->page_mask, kv->n_pages, kv->max_pages, kn, vn, alloc->free_ids, alloc->free_top, status); break;
+    case 256: hipLaunchKernelGGL((append_kernel<256>), dim3(1), dim3(AP_NT), 0, st, n_heads, Hkv, kp, vp, kv->page_table, kv->page_mask, kv->n_pages, kv->max_pages, kn, vn, alloc->free_ids, alloc->free_top, status); break;
+    default: hipLaunchKernelGGL((append_kernel<512>), dim3(1), dim3(AP_NT), 0, st, n_heads, Hkv, kp, vp, kv->page_table, kv->page_mask, kv->n_pages, kv->max_pages, kn, vn, alloc->free_ids, alloc->free_top, status); break;
+  }
+  return hipGetLastError();
+}

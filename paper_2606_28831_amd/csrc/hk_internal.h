@@ -1,0 +1,155 @@
+// Internal helpers shared by the HIP kernels of libhardkv (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "hardkv.h"
+
+#define HK_PAGE 16
+#define HK_WAVE 64
+
+namespace hk {
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// bf16 bits -> fp32 (exact)
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ int wave_sum_i(int v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ unsigned long long wave_sum_u64(unsigned long long v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// Block-wide reductions for blockDim.x = NT threads (multiple of 64).  `red` is LDS
+// scratch of at least NT/64 elements; every thread gets the result.
+template <int NT>
+__device__ __forceinline__ float block_max(float v, float* red) {
+  v = wave_max(v);
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  __syncthreads();
+  if (l == 0) red[w] = v;
+  __syncthreads();
+  float r = red[0];
+#pragma unroll
+  for (int i = 1; i < NT / 64; ++i) r = fmaxf(r, red[i]);
+  return r;
+}
+template <int NT>
+__device__ __forceinline__ float block_sum(float v, float* red) {
+  v = wave_sum(v);
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  __syncthreads();
+  if (l == 0) red[w] = v;
+  __syncthreads();
+  float r = 0.f;
+#pragma unroll
+  for (int i = 0; i < NT / 64; ++i) r += red[i];
+  return r;
+}
+template <int NT>
+__device__ __forceinline__ unsigned long long block_sum_u64(unsigned long long v,
+                                                            unsigned long long* red) {
+  v = wave_sum_u64(v);
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  __syncthreads();
+  if (l == 0) red[w] = v;
+  __syncthreads();
+  unsigned long long r = 0;
+#pragma unroll
+  for (int i = 0; i < NT / 64; ++i) r += red[i];
+  return r;
+}
+template <int NT>
+__device__ __forceinline__ int block_sum_int(int v, int* red) {
+  v = wave_sum_i(v);
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  __syncthreads();
+  if (l == 0) red[w] = v;
+  __syncthreads();
+  int r = 0;
+#pragma unroll
+  for (int i = 0; i < NT / 64; ++i) r += red[i];
+  return r;
+}
+
+// Candidate predicate: slot j of a head is a candidate when j < cand_len and its page
+// mask bit is set (mask row may be null: all slots valid).
+__device__ __forceinline__ bool is_cand(const uint16_t* mask_row, int cand_len, int j) {
+  if (j >= cand_len) return false;
+  if (mask_row == nullptr) return true;
+  return (mask_row[j >> 4] >> (j & 15)) & 1;
+}
+
+__device__ __forceinline__ int dense_pages(int L_dense) { return (L_dense + HK_PAGE - 1) / HK_PAGE; }
+
+}  // namespace hk
+
+// ---------------------------------------------------------------- launchers
+// Each returns hipGetLastError() of its launches; arguments are validated by the C ABI.
+struct hk_score_args {
+  const void* q_obs;
+  const hk_paged_kv* kv;
+  int NS, Hq, Hkv, D, W;
+  int L_dense;
+  float sm_scale;
+  const float* row_lse_in;
+  float* row_lse_out;
+  float* s_attn;
+  int32_t* cand_len;
+  const int32_t* ref_slots;
+  int n_ref;
+  float* x_red;
+  void* ws;
+};
+hipError_t hk_launch_score(const hk_score_args& a, hipStream_t st);
+size_t hk_score_ws(int NS, int Hq, int Hkv, int D, int W, int max_pages);
+size_t hk_score_lds_bytes(int R, int D, int esize, bool redundancy);
+
+hipError_t hk_launch_calibrate(int n_heads, int S_max, const int32_t* cand_len,
+                               const uint16_t* mask, int n_metrics, const float* x0,
+                               const float* x1, const float* T0, const float* T1, float w0,
+                               float w1, float* c_out, float* lse_out, hipStream_t st);
+hipError_t hk_launch_topp(int n_heads, int S_max, const int32_t* cand_len, const uint16_t* mask,
+                          const float* c, int p_q, int k_min, int k_max, uint32_t* sel_bits,
+                          int32_t* k_out, float* sel_mass, int32_t* status, hipStream_t st);
+hipError_t hk_launch_solve_T(int n_heads, int S_max, const int32_t* cand_len,
+                             const uint16_t* mask, const float* x, const int32_t* k,
+                             const float* target, float T_lo, float T_hi, int iters,
+                             float* T_out, hipStream_t st);
+
+hipError_t hk_launch_compact(int n_heads, int D, const hk_paged_kv* kv, const uint32_t* sel_bits,
+                             int L_dense, int L_sparse, const hk_allocator* alloc,
+                             int32_t* status, void* ws, hipStream_t st);
+size_t hk_compact_ws(int n_heads, int max_pages);
+
+hipError_t hk_launch_decode(int NS, int Hq, int Hkv, int D, const void* q, const hk_paged_kv* kv,
+                            float sm_scale, float* o, float* lse, void* ws, hipStream_t st);
+size_t hk_decode_ws(int NS, int Hq, int Hkv, int D, int max_pages);
+
+hipError_t hk_launch_append(int NS, int Hkv, int D, const hk_paged_kv* kv, const void* k_new,
+                            const void* v_new, const hk_allocator* alloc, int32_t* status,
+                            void* ws, hipStream_t st);
+size_t hk_append_ws(int NS, int Hkv);

@@ -1,0 +1,364 @@
+// a2 / a2' / a3: Logits Calibration, temperature solve and head-adaptive Top-p (gfx950).
+//
+// One workgroup of 1024 threads per head.  Slot j of the head is owned by thread
+// j % 1024 as its element j / 1024, so a wave's 64 lanes always cover 64 consecutive
+// slots (coalesced loads, and one ballot gives two words of the selection bitmap).
+// Every head's candidates stay in registers (S_max <= 32768 -> <= 32 per thread).
+#include "hk_internal.h"
+
+namespace hk {
+
+constexpr int SEL_NT = 1024;
+constexpr int SEL_NW = SEL_NT / 64;
+constexpr unsigned long long kMassOne = 1ull << 40;   // fixed-point unit of the Top-p mass
+
+// ------------------------------------------------------------------ a2: calibrate
+// c = sum_m w_m Softmax(x_m / T_m) over the candidates (Solution 2, Sec. 3.2).
+template <int EPT>
+__global__ __launch_bounds__(SEL_NT) void calibrate_kernel(
+    int S_max, const int32_t* __restrict__ cand_len, const uint16_t* __restrict__ mask, int n_metrics,
+    const float* __restrict__ x0, const float* __restrict__ x1, const float* __restrict__ T0,
+    const float* __restrict__ T1, float w0, float w1, float* __restrict__ c_out,
+    float* __restrict__ lse_out) {
+  __shared__ float red[SEL_NW];
+  const int h = blockIdx.x, tid = threadIdx.x;
+  const int cl = cand_len[h];
+  const uint16_t* mrow = mask ? mask + (size_t)h * (S_max / HK_PAGE) : nullptr;
+  uint32_t cbits = 0;
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) {
+    const int j = tid + SEL_NT * i;
+    if (j < S_max && is_cand(mrow, cl, j)) cbits |= 1u << i;
+  }
+  float c[EPT];
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) c[i] = 0.f;
+  for (int m = 0; m < n_metrics; ++m) {
+    const float* x = (m == 0 ? x0 : x1) + (size_t)h * S_max;
+    const float* Tp = (m == 0 ? T0 : T1);
+    const float T = Tp ? Tp[h] : 1.0f;
+    const float wm = (m == 0 ? w0 : w1);
+    float y[EPT];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < EPT; ++i) {
+      y[i] = -INFINITY;
+      if ((cbits >> i) & 1u) y[i] = x[tid + SEL_NT * i] / T;
+      mx = fmaxf(mx, y[i]);
+    }
+    mx = block_max<SEL_NT>(mx, red);
+    float lse = -INFINITY;
+    if (mx != -INFINITY) {
+      float sm = 0.f;
+#pragma unroll
+      for (int i = 0; i < EPT; ++i)
+        if ((cbits >> i) & 1u) sm += expf(y[i] - mx);
+      sm = block_sum<SEL_NT>(sm, red);
+      lse = mx + logf(sm);
+#pragma unroll
+      for (int i = 0; i < EPT; ++i)
+        if ((cbits >> i) & 1u) c[i] = fmaf(wm, expf(y[i] - lse), c[i]);
+    }
+    if (lse_out && tid == 0) lse_out[(size_t)h * n_metrics + m] = lse;
+  }
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) {
+    const int j = tid + SEL_NT * i;
+    if (j < S_max) c_out[(size_t)h * S_max + j] = c[i];
+  }
+}
+
+// Threshold searches run most-significant bit first: the answer v is the largest key
+// with mass(key >= v) >= target (or count(key >= v) >= k); both are monotone in v.
+template <int EPT>
+__device__ __forceinline__ unsigned long long mass_ge(const uint32_t* key, const unsigned long long* w,
+                                                      uint32_t cbits, uint32_t t) {
+  unsigned long long m = 0;
+#pragma unroll
+  for (int i = 0; i < EPT; ++i)
+    if (((cbits >> i) & 1u) && key[i] >= t) m += w[i];
+  return m;
+}
+template <int EPT>
+__device__ __forceinline__ int count_ge(const uint32_t* key, uint32_t cbits, uint32_t t) {
+  int n = 0;
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) n += (((cbits >> i) & 1u) && key[i] >= t) ? 1 : 0;
+  return n;
+}
+
+// Select, among elements with key == v (flags in `tie`), the `take` with the largest slot
+// index.  Returns the per-element selection bits for the ties.
+template <int EPT>
+__device__ uint32_t take_top_ties(uint32_t tie, int take, int* cnt /* LDS [EPT][SEL_NW] */) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  unsigned long long bal[EPT];
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) {
+    bal[i] = __ballot((tie >> i) & 1u);
+    if (lane == 0) cnt[i * SEL_NW + wave] = __popcll(bal[i]);
+  }
+  __syncthreads();
+  uint32_t out = 0;
+  // ties with a larger slot index: later rows, later waves of this row, higher lanes
+  int above_rows = 0;
+  for (int i = EPT - 1; i >= 0; --i) {
+    int above = above_rows;
+    for (int w = wave + 1; w < SEL_NW; ++w) above += cnt[i * SEL_NW + w];
+    const unsigned long long hi = (lane == 63) ? 0ull : (bal[i] >> (lane + 1));
+    above += __popcll(hi);
+    if (((tie >> i) & 1u) && above < take) out |= 1u << i;
+    int row = 0;
+    for (int w = 0; w < SEL_NW; ++w) row += cnt[i * SEL_NW + w];
+    above_rows += row;
+  }
+  return out;
+}
+
+// ------------------------------------------------------------------ a3: Top-p
+template <int EPT>
+__global__ __launch_bounds__(SEL_NT) void topp_kernel(
+    int S_max, const int32_t* __restrict__ cand_len, const uint16_t* __restrict__ mask,
+    const float* __restrict__ c, int p_q, int k_min, int k_max, uint32_t* __restrict__ sel_bits,
+    int32_t* __restrict__ k_out, float* __restrict__ sel_mass, int32_t* __restrict__ status) {
+  __shared__ unsigned long long red64[SEL_NW];
+  __shared__ int redi[SEL_NW];
+  __shared__ int tiecnt[EPT * SEL_NW];
+  const int h = blockIdx.x, tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int cl = cand_len[h];
+  const uint16_t* mrow = mask ? mask + (size_t)h * (S_max / HK_PAGE) : nullptr;
+  const float* crow = c + (size_t)h * S_max;
+
+  uint32_t cbits = 0, key[EPT];
+  unsigned long long w[EPT];
+  int flags = 0;
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) {
+    const int j = tid + SEL_NT * i;
+    key[i] = 0;
+    w[i] = 0;
+    if (j < S_max && is_cand(mrow, cl, j)) {
+      cbits |= 1u << i;
+      float v = crow[j];
+      if (v != v) { v = 0.f; flags |= HK_FLAG_NAN; }
+      if (v > 1.f) { v = 1.f; flags |= HK_FLAG_RANGE; }
+      if (v < 0.f) { v = 0.f; flags |= HK_FLAG_RANGE; }
+      if (v == 0.f) v = 0.f;                      // canonical +0
+      key[i] = __float_as_uint(v);                // non-negative floats order as integers
+      w[i] = (unsigned long long)(v * (float)kMassOne);   // exact scaling, truncation = floor
+    }
+  }
+  flags = __syncthreads_or(flags);
+  if (tid == 0 && flags && status) atomicOr(status, flags);
+
+  const int n_cand = block_sum_int<SEL_NT>(__popc(cbits), redi);
+  unsigned long long tot = 0;
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) tot += ((cbits >> i) & 1u) ? w[i] : 0ull;
+  tot = block_sum_u64<SEL_NT>(tot, red64);
+  const unsigned long long pq = (unsigned long long)p_q;
+  const unsigned long long target = pq * (tot / 1000000ull) + (pq * (tot % 1000000ull) + 999999ull) / 1000000ull;
+
+  // k from the mass rule
+  int k = 0;
+  uint32_t v = 0;
+  int take = 0;
+  if (target > 0) {
+    for (int b = 29; b >= 0; --b) {
+      const uint32_t t = v | (1u << b);
+      const unsigned long long m = block_sum_u64<SEL_NT>(mass_ge<EPT>(key, w, cbits, t), red64);
+      if (m >= target) v = t;
+    }
+    // v = value of the crossing element; elements above it are all taken
+    const int cnt_gt = block_sum_int<SEL_NT>(count_ge<EPT>(key, cbits, v + 1), redi);
+    const unsigned long long mass_gt = block_sum_u64<SEL_NT>(mass_ge<EPT>(key, w, cbits, v + 1), red64);
+    const unsigned long long wv = (unsigned long long)(__uint_as_float(v) * (float)kMassOne);
+    take = wv ? (int)((target - mass_gt + wv - 1) / wv) : 0;   // wv > 0 whenever target > 0
+    k = cnt_gt + take;
+  }
+  const int lo = min(max(k_min, 0), n_cand);
+  const int hi = (k_max > 0) ? min(k_max, n_cand) : n_cand;
+  const int kf = max(lo, min(k, hi));
+  if (kf != k || target == 0) {
+    if (kf == 0) {
+      v = 0xffffffffu;
+      take = 0;
+    } else {
+      v = 0;
+      for (int b = 29; b >= 0; --b) {
+        const uint32_t t = v | (1u << b);
+        if (block_sum_int<SEL_NT>(count_ge<EPT>(key, cbits, t), redi) >= kf) v = t;
+      }
+      const int cnt_gt = block_sum_int<SEL_NT>(count_ge<EPT>(key, cbits, v + 1), redi);
+      take = kf - cnt_gt;
+    }
+  }
+  // selection: keys above v, plus the `take` most recent slots equal to v
+  uint32_t sel = 0, tie = 0;
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) {
+    if ((cbits >> i) & 1u) {
+      if (v != 0xffffffffu && key[i] > v) sel |= 1u << i;
+      if (key[i] == v) tie |= 1u << i;
+    }
+  }
+  const int n_tie = block_sum_int<SEL_NT>(__popc(tie), redi);
+  if (take >= n_tie) sel |= tie;
+  else if (take > 0) sel |= take_top_ties<EPT>(tie, take, tiecnt);
+
+  unsigned long long msel = 0;
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) msel += ((sel >> i) & 1u) ? w[i] : 0ull;
+  msel = block_sum_u64<SEL_NT>(msel, red64);
+
+  uint32_t* brow = sel_bits + (size_t)h * (S_max / 32);
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) {
+    const unsigned long long b = __ballot((sel >> i) & 1u);
+    const int j0 = SEL_NT * i + 64 * wave;
+    if (lane == 0 && j0 < S_max) {
+      brow[j0 / 32] = (uint32_t)b;
+      if (j0 + 32 < S_max) brow[j0 / 32 + 1] = (uint32_t)(b >> 32);
+    }
+  }
+  if (tid == 0) {
+    k_out[h] = kf;
+    if (sel_mass) sel_mass[h] = (float)((double)msel / (double)kMassOne);
+  }
+}
+
+// ------------------------------------------------------------------ a2': temperature
+// Bisection on log T for M_k(Softmax(x/T)) = target (App. D.1; order invariance App. D.2).
+__device__ __forceinline__ uint32_t ordered_key(float x) {
+  uint32_t b = __float_as_uint(x);
+  if (x != x) return 0u;                         // NaN below everything
+  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+template <int EPT>
+__global__ __launch_bounds__(SEL_NT) void solve_T_kernel(
+    int S_max, const int32_t* __restrict__ cand_len, const uint16_t* __restrict__ mask,
+    const float* __restrict__ x, const int32_t* __restrict__ k_arr, const float* __restrict__ target,
+    float T_lo, float T_hi, int iters, float* __restrict__ T_out) {
+  __shared__ float red[SEL_NW];
+  __shared__ int redi[SEL_NW];
+  __shared__ int tiecnt[EPT * SEL_NW];
+  const int h = blockIdx.x, tid = threadIdx.x;
+  const int cl = cand_len[h];
+  const uint16_t* mrow = mask ? mask + (size_t)h * (S_max / HK_PAGE) : nullptr;
+  const float* xrow = x + (size_t)h * S_max;
+  uint32_t cbits = 0, key[EPT];
+  float xv[EPT];
+  float mx = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) {
+    const int j = tid + SEL_NT * i;
+    key[i] = 0;
+    xv[i] = -INFINITY;
+    if (j < S_max && is_cand(mrow, cl, j)) {
+      cbits |= 1u << i;
+      xv[i] = xrow[j];
+      key[i] = ordered_key(xv[i]);
+      mx = fmaxf(mx, xv[i]);
+    }
+  }
+  mx = block_max<SEL_NT>(mx, red);
+  const int n_cand = block_sum_int<SEL_NT>(__popc(cbits), redi);
+  const int kk = min(max(k_arr[h], 0), n_cand);
+  // Top-k set of x: keys above v plus the most recent ties
+  uint32_t top = 0;
+  if (kk > 0) {
+    uint32_t v = 0;
+    for (int b = 31; b >= 0; --b) {
+      const uint32_t t = v | (1u << b);
+      if (block_sum_int<SEL_NT>(count_ge<EPT>(key, cbits, t), redi) >= kk) v = t;
+    }
+    const int cnt_gt = (v == 0xffffffffu) ? 0 : block_sum_int<SEL_NT>(count_ge<EPT>(key, cbits, v + 1), redi);
+    const int take = kk - cnt_gt;
+    uint32_t tie = 0;
+#pragma unroll
+    for (int i = 0; i < EPT; ++i)
+      if ((cbits >> i) & 1u) {
+        if (v != 0xffffffffu && key[i] > v) top |= 1u << i;
+        if (key[i] == v) tie |= 1u << i;
+      }
+    const int n_tie = block_sum_int<SEL_NT>(__popc(tie), redi);
+    if (take >= n_tie) top |= tie;
+    else if (take > 0) top |= take_top_ties<EPT>(tie, take, tiecnt);
+  }
+  const float tgt = target[h];
+  float a = logf(T_lo), b = logf(T_hi);
+  for (int it = 0; it < iters; ++it) {
+    const float mid = 0.5f * (a + b);
+    const float invT = expf(-mid);
+    float s_all = 0.f, s_top = 0.f;
+    if (mx != -INFINITY) {
+#pragma unroll
+      for (int i = 0; i < EPT; ++i)
+        if ((cbits >> i) & 1u) {
+          const float e = expf((xv[i] - mx) * invT);
+          s_all += e;
+          if ((top >> i) & 1u) s_top += e;
+        }
+    }
+    s_all = block_sum<SEL_NT>(s_all, red);
+    s_top = block_sum<SEL_NT>(s_top, red);
+    const float mass = (s_all > 0.f) ? s_top / s_all : 0.f;
+    if (mass - tgt > 0.f) a = mid;
+    else b = mid;
+  }
+  if (tid == 0) T_out[h] = expf(0.5f * (a + b));
+}
+
+static int ept_for(int S_max) {
+  const int e = (S_max + SEL_NT - 1) / SEL_NT;
+  if (e <= 1) return 1;
+  if (e <= 2) return 2;
+  if (e <= 4) return 4;
+  if (e <= 8) return 8;
+  if (e <= 16) return 16;
+  return 32;
+}
+
+#define HK_EPT_SWITCH(S_max, CALL)        \
+  switch (ept_for(S_max)) {               \
+    case 1: { constexpr int E = 1; CALL; break; } \
+    case 2: { constexpr int E = 2; CALL; break; } \
+    case 4: { constexpr int E = 4; CALL; break; } \
+    case 8: { constexpr int E = 8; CALL; break; } \
+    case 16: { constexpr int E = 16; CALL; break; } \
+    default: { constexpr int E = 32; CALL; break; } \
+  }
+
+}  // namespace hk
+
+using namespace hk;
+
+hipError_t hk_launch_calibrate(int n_heads, int S_max, const int32_t* cand_len, const uint16_t* mask,
+                               int n_metrics, const float* x0, const float* x1, const float* T0,
+                               const float* T1, float w0, float w1, float* c_out, float* lse_out,
+                               hipStream_t st) {
+  HK_EPT_SWITCH(S_max, hipLaunchKernelGGL((calibrate_kernel<E>), dim3(n_heads), dim3(SEL_NT), 0, st,
+                                          S_max, cand_len, mask, n_metrics, x0, x1, T0, T1, w0, w1,
+                                          c_out, lse_out));
+  return hipGetLastError();
+}
+
+hipError_t hk_launch_topp(int n_heads, int S_max, const int32_t* cand_len, const uint16_t* mask,
+                          const float* c, int p_q, int k_min, int k_max, uint32_t* sel_bits,
+                          int32_t* k_out, float* sel_mass, int32_t* status, hipStream_t st) {
+  HK_EPT_SWITCH(S_max, hipLaunchKernelGGL((topp_kernel<E>), dim3(n_heads), dim3(SEL_NT), 0, st, S_max,
+                                          cand_len, mask, c, p_q, k_min, k_max, sel_bits, k_out,
+                                          sel_mass, status));
+  return hipGetLastError();
+}
+
+hipError_t hk_launch_solve_T(int n_heads, int S_max, const int32_t* cand_len, const uint16_t* mask,
+                             const float* x, const int32_t* k, const float* target, float T_lo,
+                             float T_hi, int iters, float* T_out, hipStream_t st) {
+  HK_EPT_SWITCH(S_max, hipLaunchKernelGGL((solve_T_kernel<E>), dim3(n_heads), dim3(SEL_NT), 0, st,
+                                          S_max, cand_len, mask, x, k, target, T_lo, T_hi, iters,
+                                          T_out));
+  return hipGetLastError();
+}

@@ -1,0 +1,129 @@
+"""Chaining of the C entry points into one compression step and one decode step.
+
+Marshalling only: buffers are allocated once (static shapes) and every call goes to
+libhardkv.  The compression step is Steps 2-3 of the continuous compression pipeline
+(Sec. 3.1): score -> calibrate -> Top-p -> rewrite.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass
+
+import torch
+
+from . import (Allocator, PagedKV, OP_COMPACT, OP_DECODE, OP_SCORE, dims, hk_append_kv,
+               hk_calibrate, hk_calibrate_solve_T, hk_compact, hk_decode_attn, hk_score,
+               hk_topp_select, workspace)
+
+
+@dataclass
+class CompressBuffers:
+    s_attn: torch.Tensor
+    x_red: torch.Tensor | None
+    c: torch.Tensor
+    c_attn: torch.Tensor | None
+    cand_len: torch.Tensor
+    row_lse: torch.Tensor
+    sel_bits: torch.Tensor
+    k: torch.Tensor
+    sel_mass: torch.Tensor
+    k_attn: torch.Tensor | None
+    mass_attn: torch.Tensor | None
+    T_red: torch.Tensor | None
+    status: torch.Tensor
+    ws_score: torch.Tensor
+    ws_compact: torch.Tensor
+
+
+class Compressor:
+    """One compression step over every head of a paged cache.
+
+    metric "attn": attention mass over the window, calibrated with T = 1.
+    metric "attn+red": attention mass and key redundancy, each calibrated (the
+    redundancy temperature solved once per head, on the first call), mixed 0.5/0.5.
+    """
+
+    def __init__(self, NS, Hq, Hkv, D, W, kv: PagedKV, alloc: Allocator, p: float,
+                 L_dense: int = 0, L_sparse: int = 0, metric: str = "attn", n_ref: int = 0,
+                 k_max: int = 0):
+        self.d = dims(NS, Hq, Hkv, D, W)
+        self.kv, self.alloc, self.p = kv, alloc, p
+        self.L_dense, self.L_sparse = L_dense, L_sparse
+        self.metric, self.n_ref, self.k_max = metric, n_ref, k_max
+        self.sm_scale = 1.0 / math.sqrt(D)
+        dev = kv.k_pool.device
+        H = NS * Hkv
+        S = kv.max_pages * 16
+        self.n_heads, self.S_max = H, S
+        f32, i32 = torch.float32, torch.int32
+        red = metric == "attn+red"
+        self.buf = CompressBuffers(
+            s_attn=torch.empty(H, S, dtype=f32, device=dev),
+            x_red=torch.empty(H, S, dtype=f32, device=dev) if red else None,
+            c=torch.empty(H, S, dtype=f32, device=dev),
+            c_attn=torch.empty(H, S, dtype=f32, device=dev) if red else None,
+            cand_len=torch.empty(H, dtype=i32, device=dev),
+            row_lse=torch.empty(W, NS, Hq, dtype=f32, device=dev),
+            sel_bits=torch.empty(H, S // 32, dtype=i32, device=dev),
+            k=torch.empty(H, dtype=i32, device=dev),
+            sel_mass=torch.empty(H, dtype=f32, device=dev),
+            k_attn=torch.empty(H, dtype=i32, device=dev) if red else None,
+            mass_attn=torch.empty(H, dtype=f32, device=dev) if red else None,
+            T_red=None,
+            status=torch.zeros(1, dtype=i32, device=dev),
+            ws_score=workspace(OP_SCORE, self.d, kv.max_pages, dev),
+            ws_compact=workspace(OP_COMPACT, self.d, kv.max_pages, dev),
+        )
+
+    def score(self, q_obs, ref_slots=None, row_lse_in=None, stream=None):
+        b = self.buf
+        hk_score(self.d, q_obs, self.kv, self.L_dense, self.sm_scale, b.s_attn, b.cand_len,
+                 row_lse_in=row_lse_in, row_lse_out=b.row_lse if row_lse_in is None else None,
+                 ref_slots=ref_slots, n_ref=self.n_ref if ref_slots is not None else 0,
+                 x_red=b.x_red if ref_slots is not None else None, ws=b.ws_score, stream=stream)
+
+    def select(self, stream=None):
+        b, H, S, pm = self.buf, self.n_heads, self.S_max, self.kv.page_mask
+        if self.metric == "attn":
+            hk_calibrate(H, S, b.cand_len, pm, [b.s_attn], None, [1.0], b.c, stream=stream)
+        else:
+            if b.T_red is None:
+                # temperature of the redundancy metric, solved at the first compression only
+                hk_calibrate(H, S, b.cand_len, pm, [b.s_attn], None, [1.0], b.c_attn, stream=stream)
+                hk_topp_select(H, S, b.cand_len, pm, b.c_attn, self.p, b.sel_bits, b.k_attn,
+                               sel_mass=b.mass_attn, status=b.status, stream=stream)
+                b.T_red = torch.empty(H, dtype=torch.float32, device=b.c.device)
+                hk_calibrate_solve_T(H, S, b.cand_len, pm, b.x_red, b.k_attn, b.mass_attn, b.T_red,
+                                     stream=stream)
+            hk_calibrate(H, S, b.cand_len, pm, [b.s_attn, b.x_red], [None, b.T_red], [0.5, 0.5],
+                         b.c, stream=stream)
+        hk_topp_select(H, S, b.cand_len, pm, b.c, self.p, b.sel_bits, b.k, k_max=self.k_max,
+                       sel_mass=b.sel_mass, status=b.status, stream=stream)
+
+    def compact(self, stream=None):
+        b = self.buf
+        hk_compact(self.d, self.kv, b.sel_bits, self.L_dense, self.L_sparse, self.alloc, b.status,
+                   b.ws_compact, stream=stream)
+
+    def step(self, q_obs, ref_slots=None, row_lse_in=None, stream=None):
+        self.score(q_obs, ref_slots=ref_slots, row_lse_in=row_lse_in, stream=stream)
+        self.select(stream=stream)
+        self.compact(stream=stream)
+
+
+class Decoder:
+    """One decode step of one layer: append the step's K/V, then attend."""
+
+    def __init__(self, NS, Hq, Hkv, D, kv: PagedKV, alloc: Allocator):
+        self.d = dims(NS, Hq, Hkv, D, 0)
+        self.kv, self.alloc = kv, alloc
+        self.sm_scale = 1.0 / math.sqrt(D)
+        dev = kv.k_pool.device
+        self.ws = workspace(OP_DECODE, self.d, kv.max_pages, dev)
+        self.status = torch.zeros(1, dtype=torch.int32, device=dev)
+
+    def append(self, k_new, v_new, stream=None):
+        hk_append_kv(self.d, self.kv, k_new, v_new, self.alloc, self.status, stream=stream)
+
+    def attend(self, q, o, lse, stream=None):
+        hk_decode_attn(self.d, q, self.kv, self.sm_scale, o, lse, self.ws, stream=stream)

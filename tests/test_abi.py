@@ -1,0 +1,92 @@
+"""The C ABI library loads, exports every symbol include/hardkv.h declares, and rejects
+invalid arguments on the host (no GPU needed: validation happens before any launch)."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "hardkv.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:hk_status|size_t|const char\*)\s+(hk_\w+)\s*\(", text,
+                                 flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def hk():
+    import paper_2606_28831_amd as hk
+    if not os.path.exists(hk.LIB_PATH):
+        from paper_2606_28831_amd.build import build
+        build()
+    return hk
+
+
+def test_header_declares_the_boundary():
+    names = _declared()
+    for n in ["hk_score", "hk_calibrate", "hk_calibrate_solve_T", "hk_topp_select", "hk_compact",
+              "hk_decode_attn", "hk_append_kv", "hk_workspace_size", "hk_status_string"]:
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(hk):
+    L = C.CDLL(hk.LIB_PATH)
+    for n in _declared():
+        assert hasattr(L, n), n
+    assert sorted(_declared()) == sorted(hk.EXPORTED)
+
+
+def test_status_strings(hk):
+    for code in range(7):
+        assert hk.hk_status_string(code).startswith("HK_")
+    for f in (1, 2, 4):
+        assert hk.hk_status_string(f, True).startswith("HK_FLAG")
+
+
+def test_workspace_sizes(hk):
+    d = hk.dims(32, 28, 4, 128, 32)
+    assert hk.hk_workspace_size(hk.OP_SCORE, d, 2048) >= 128 * 32 * 224 * 8
+    assert hk.hk_workspace_size(hk.OP_COMPACT, d, 2048) >= 2 * 128 * 2048 * 4
+    assert hk.hk_workspace_size(hk.OP_DECODE, d, 2048) > 0
+    assert hk.hk_workspace_size(99, d, 2048) == 0
+
+
+def _kv(hk, dtype=1, max_pages=4, D=128, addr=1 << 20):
+    return hk.hk_paged_kv(addr, addr, addr, addr, addr, 64, max_pages, dtype)
+
+
+def test_validation_errors_without_gpu(hk):
+    L = hk.lib()
+    d = hk.dims(1, 8, 2, 128, 16)
+    kv = _kv(hk)
+    P = 1 << 20
+    ws = 1 << 24
+    score = lambda d_, kv_, **kw: L.hk_score(C.byref(d_), kw.get("q", P), C.byref(kv_), 0,
+                                             kw.get("scale", 0.125), None, None, P, P, None, 0,
+                                             None, kw.get("ws", ws), 1 << 30, None)
+    assert score(hk.dims(1, 8, 2, 96, 16), kv) == 3          # D not 64/128 -> SHAPE
+    assert score(hk.dims(1, 9, 2, 128, 16), kv) == 3         # Hq % Hkv -> SHAPE
+    assert score(hk.dims(1, 8, 2, 128, 128), kv) == 3        # G*W > 256 -> SHAPE
+    assert score(d, _kv(hk, dtype=7)) == 2                   # dtype
+    assert score(d, _kv(hk, max_pages=3)) == 3               # odd table width
+    assert score(d, kv, scale=-1.0) == 1                     # scale
+    assert score(d, kv, q=P + 4) == 4                        # alignment
+    assert score(d, kv, ws=P + 16) == 4                      # workspace alignment
+    assert L.hk_topp_select(4, 100, P, None, P, 0.9, 1, 0, P, P, None, None, None) == 3
+    assert L.hk_topp_select(4, 65536, P, None, P, 0.9, 1, 0, P, P, None, None, None) == 3
+    assert L.hk_topp_select(4, 128, P, None, P, 1.5, 1, 0, P, P, None, None, None) == 1
+    assert L.hk_topp_select(4, 128, None, None, P, 0.9, 1, 0, P, P, None, None, None) == 1
+    assert L.hk_calibrate_solve_T(4, 128, P, None, P, P, P, 1.0, 0.5, 40, P, None) == 1
+    assert L.hk_calibrate_solve_T(4, 128, P, None, P, P, P, 1e-4, 1e4, 0, P, None) == 1
+    alloc = hk.hk_allocator(P, P, 64)
+    assert L.hk_compact(C.byref(d), C.byref(kv), P, -1, 0, C.byref(alloc), P, P, 1 << 30, None) == 1
+    assert L.hk_compact(C.byref(d), C.byref(kv), P, 0, 0, C.byref(alloc), P, P, 16, None) == 5
+    assert L.hk_decode_attn(C.byref(hk.dims(1, 12, 2, 128)), P, C.byref(kv), 0.1, P, P, P,
+                            1 << 30, None) == 3              # group of 6 unsupported
+    assert L.hk_decode_attn(C.byref(d), P, C.byref(kv), 0.1, P, P, P, 16, None) == 5
+    assert L.hk_append_kv(C.byref(d), C.byref(kv), None, P, C.byref(alloc), P, None, 0, None) == 1
+    kvnull = hk.hk_paged_kv(None, P, P, P, P, 64, 4, 1)
+    assert L.hk_decode_attn(C.byref(d), P, C.byref(kvnull), 0.1, P, P, P, 1 << 30, None) == 1

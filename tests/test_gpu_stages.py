@@ -1,0 +1,480 @@
+"""GPU parity of every stage against the CPU oracle, fed the GPU's own stage inputs.
+
+Selections, counts and compacted layouts must match bit for bit; scores, calibrated
+probabilities, LSEs, attention outputs and temperatures within rtol 2e-3 (bf16 caches)
+or 1e-5 (fp32 caches).  Shapes span several tiles with ragged tails, masked slots,
+GQA groups of 1..8, head dims 64/128 and both cache dtypes.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import workload as WL
+from hk_testlib import (RTOL, HostCache, check_lse, check_log_scores, check_prob, np64, np_i,
+                        q_rows, unpack_bits)
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+CASES = {
+    "cfg1_f32_d64_g4": (WL.config(1), {}),
+    "bf16_d128_g4_ragged_holes": (dict(L=1, B=2, Hq=8, Hkv=2, D=128, N=1000, dtype="bf16", W=32,
+                                       seed=11, recipe="normal"), dict(hole_prob=0.1)),
+    "bf16_d128_g7_tempered": (dict(L=1, B=2, Hq=28, Hkv=4, D=128, N=700, dtype="bf16", W=32,
+                                   seed=12, recipe="tempered"), {}),
+    "bf16_d64_g2_w8_planted": (dict(L=1, B=3, Hq=4, Hkv=2, D=64, N=333, dtype="bf16", W=8,
+                                    seed=13, recipe="planted"), {}),
+    "f32_d128_g8_w16": (dict(L=1, B=1, Hq=8, Hkv=1, D=128, N=520, dtype="f32", W=16, seed=14,
+                             recipe="normal"), dict(hole_prob=0.3)),
+    "bf16_d128_g1_w32_tail1": (dict(L=1, B=2, Hq=2, Hkv=2, D=128, N=1, dtype="bf16", W=32,
+                                    seed=15, recipe="normal"), dict(max_pages=40)),
+}
+
+
+def _setup(name, **extra):
+    import paper_2606_28831_amd as hk
+    cfg, kw = CASES[name]
+    kw = dict(kw)
+    kw.update(extra)
+    w = WL.make_workload(cfg, DEV, **kw)
+    kv = hk.PagedKV(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)
+    return hk, cfg, w, kv
+
+
+@pytest.mark.parametrize("name", list(CASES))
+@pytest.mark.parametrize("L_dense", [0, 48])
+def test_score_attention_mass(name, L_dense):
+    hk, cfg, w, kv = _setup(name)
+    G = cfg["Hq"] // cfg["Hkv"]
+    d = hk.dims(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"], cfg["W"])
+    H, S = w.n_heads, w.S_max
+    s = torch.full((H, S), 7.0, device=DEV)
+    cl = torch.empty(H, dtype=torch.int32, device=DEV)
+    lse = torch.empty(cfg["W"], w.NS, cfg["Hq"], device=DEV)
+    ws = hk.workspace(hk.OP_SCORE, d, w.max_pages, DEV)
+    scale = 1 / math.sqrt(cfg["D"])
+    hk.hk_score(d, w.q_obs, kv, L_dense, scale, s, cl, row_lse_out=lse, ws=ws)
+    torch.cuda.synchronize()
+    host = HostCache(w.k_pool, None, w.page_table, w.page_mask, w.n_pages)
+    qn = np64(w.q_obs)
+    s_np, cl_np, lse_np = np64(s), np_i(cl), np64(lse)
+    rtol = RTOL[cfg["dtype"]]
+    for h in range(H):
+        rows, valid = host.head(h)
+        n = int(host.n[h])
+        cand_len = 16 * max(0, n - O.tier_pages(n, L_dense, 0)[2])
+        assert cl_np[h] == cand_len
+        sr, lr = O.score_head(q_rows(qn, h, cfg["Hkv"], G), rows, valid, cand_len, scale)
+        full = np.full(S, -np.inf)
+        full[:len(sr)] = sr
+        check_log_scores(s_np[h], full, rtol, f"s head {h}")
+        sq, kvh = divmod(h, cfg["Hkv"])
+        check_lse(lse_np[:, sq, kvh * G:(kvh + 1) * G].reshape(-1), lr, rtol, f"row_lse head {h}")
+
+
+@pytest.mark.parametrize("name", ["cfg1_f32_d64_g4", "bf16_d128_g4_ragged_holes",
+                                  "bf16_d128_g7_tempered"])
+def test_score_with_given_row_lse(name):
+    """Single-pass score: the row LSEs come from the caller (the decode step's own)."""
+    hk, cfg, w, kv = _setup(name)
+    G = cfg["Hq"] // cfg["Hkv"]
+    d = hk.dims(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"], cfg["W"])
+    H, S = w.n_heads, w.S_max
+    scale = 1 / math.sqrt(cfg["D"])
+    host = HostCache(w.k_pool, None, w.page_table, w.page_mask, w.n_pages)
+    qn = np64(w.q_obs)
+    lse_in = np.zeros((cfg["W"], w.NS, cfg["Hq"]), np.float32)
+    refs = {}
+    for h in range(H):
+        rows, valid = host.head(h)
+        _, lr = O.score_head(q_rows(qn, h, cfg["Hkv"], G), rows, valid, 0, scale)
+        lr = lr + 0.25    # any normaliser works: the score is defined relative to it
+        sq, kvh = divmod(h, cfg["Hkv"])
+        lse_in[:, sq, kvh * G:(kvh + 1) * G] = lr.astype(np.float32).reshape(cfg["W"], G)
+        refs[h] = (rows, valid)
+    lse_t = torch.tensor(lse_in, device=DEV)
+    s = torch.empty(H, S, device=DEV)
+    cl = torch.empty(H, dtype=torch.int32, device=DEV)
+    hk.hk_score(d, w.q_obs, kv, 0, scale, s, cl, row_lse_in=lse_t)
+    torch.cuda.synchronize()
+    s_np = np64(s)
+    for h in range(H):
+        rows, valid = refs[h]
+        sq, kvh = divmod(h, cfg["Hkv"])
+        lr = lse_in[:, sq, kvh * G:(kvh + 1) * G].reshape(-1).astype(np.float64)
+        sr, _ = O.score_head(q_rows(qn, h, cfg["Hkv"], G), rows, valid, len(valid), scale,
+                             row_lse_in=lr)
+        full = np.full(S, -np.inf)
+        full[:len(sr)] = sr
+        check_log_scores(s_np[h], full, RTOL[cfg["dtype"]], f"s head {h}")
+
+
+@pytest.mark.parametrize("name", ["bf16_d128_g4_ragged_holes", "bf16_d64_g2_w8_planted",
+                                  "cfg1_f32_d64_g4"])
+@pytest.mark.parametrize("n_ref", [1, 37, 256])
+def test_score_redundancy(name, n_ref):
+    hk, cfg, w, kv = _setup(name)
+    G = cfg["Hq"] // cfg["Hkv"]
+    d = hk.dims(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"], cfg["W"])
+    H, S = w.n_heads, w.S_max
+    host = HostCache(w.k_pool, None, w.page_table, w.page_mask, w.n_pages)
+    rng = np.random.default_rng(n_ref)
+    refs = np.zeros((H, n_ref), np.int32)
+    for h in range(H):
+        _, valid = host.head(h)
+        vidx = np.nonzero(valid)[0]
+        refs[h] = rng.choice(vidx, size=n_ref, replace=len(vidx) < n_ref)
+    ref_t = torch.tensor(refs, device=DEV)
+    s = torch.empty(H, S, device=DEV)
+    xr = torch.empty(H, S, device=DEV)
+    cl = torch.empty(H, dtype=torch.int32, device=DEV)
+    ws = hk.workspace(hk.OP_SCORE, d, w.max_pages, DEV)
+    L_dense = 32
+    hk.hk_score(d, w.q_obs, kv, L_dense, 1 / math.sqrt(cfg["D"]), s, cl, ref_slots=ref_t,
+                n_ref=n_ref, x_red=xr, ws=ws)
+    torch.cuda.synchronize()
+    xr_np = np64(xr)
+    rtol = RTOL[cfg["dtype"]]
+    for h in range(H):
+        rows, valid = host.head(h)
+        n = int(host.n[h])
+        cand_len = 16 * max(0, n - O.tier_pages(n, L_dense, 0)[2])
+        want = O.redundancy_head(rows, valid, cand_len, refs[h])
+        full = np.full(S, -np.inf)
+        full[:len(want)] = want
+        fin = np.isfinite(full)
+        assert np.all(np.isneginf(xr_np[h][~fin]))
+        err = np.abs(xr_np[h][fin] - full[fin])
+        assert err.max(initial=0) <= rtol, f"x_red head {h}: {err.max():.3g}"
+
+
+def _calib_inputs(name):
+    hk, cfg, w, kv = _setup(name)
+    d = hk.dims(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"], cfg["W"])
+    H, S = w.n_heads, w.S_max
+    s = torch.empty(H, S, device=DEV)
+    cl = torch.empty(H, dtype=torch.int32, device=DEV)
+    ws = hk.workspace(hk.OP_SCORE, d, w.max_pages, DEV)
+    hk.hk_score(d, w.q_obs, kv, 0, 1 / math.sqrt(cfg["D"]), s, cl, ws=ws)
+    return hk, cfg, w, kv, s, cl
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_calibrate_and_topp(name):
+    hk, cfg, w, kv, s, cl = _calib_inputs(name)
+    H, S = w.n_heads, w.S_max
+    c = torch.empty(H, S, device=DEV)
+    lse = torch.empty(H, 1, device=DEV)
+    T = torch.tensor(np.linspace(0.3, 3.0, H), dtype=torch.float32, device=DEV)
+    hk.hk_calibrate(H, S, cl, w.page_mask, [s], [T], [1.0], c, lse)
+    torch.cuda.synchronize()
+    rtol = RTOL[cfg["dtype"]]
+    s_np, c_np, lse_np, cl_np = np64(s), np64(c), np64(lse), np_i(cl)
+    mask = np_i(w.page_mask).astype(np.int64) & 0xFFFF
+    for h in range(H):
+        valid = ((mask[h][:, None] >> np.arange(16)) & 1).reshape(-1).astype(bool)
+        cand = O.candidate_mask(valid, int(cl_np[h]))
+        cr, lr = O.calibrate_head(s_np[h], cand, float(T[h]))
+        check_prob(c_np[h], cr, rtol, f"c head {h}")
+        check_lse(lse_np[h], [lr], rtol, f"lse head {h}")
+        assert abs(c_np[h].sum() - 1.0) <= 1e-5 * max(1, cand.sum() / 1000)
+    for p in (cfg["p"] if "p" in cfg else 0.9, 0.5, 0.999, 1.0):
+        sel = torch.empty(H, S // 32, dtype=torch.int32, device=DEV)
+        k = torch.empty(H, dtype=torch.int32, device=DEV)
+        m = torch.empty(H, device=DEV)
+        st = torch.zeros(1, dtype=torch.int32, device=DEV)
+        hk.hk_topp_select(H, S, cl, w.page_mask, c, p, sel, k, sel_mass=m, status=st)
+        torch.cuda.synchronize()
+        sel_np, k_np, m_np = np_i(sel), np_i(k), np64(m)
+        c32 = c.cpu().numpy()
+        for h in range(H):
+            valid = ((mask[h][:, None] >> np.arange(16)) & 1).reshape(-1).astype(bool)
+            cand = O.candidate_mask(valid, int(cl_np[h]))
+            r = O.topp_head(c32[h], cand, p)
+            got = unpack_bits(sel_np[h], S)
+            assert k_np[h] == r.k, f"k head {h} p {p}: {k_np[h]} vs {r.k}"
+            assert np.array_equal(got, r.sel), f"selection head {h} p {p}"
+            assert m_np[h] == np.float32(r.sel_mass / 2.0 ** 40)
+        assert int(st.item()) == 0
+
+
+@pytest.mark.parametrize("kind", ["uniform", "ties", "onehot", "nan_range", "zeros", "clamp"])
+def test_topp_edge_cases(kind):
+    import paper_2606_28831_amd as hk
+    H, S = 6, 2048
+    rng = np.random.default_rng(7)
+    c = np.zeros((H, S), np.float32)
+    cand_len = np.array([S, 1000, 1, 0, 33, 2047 // 32 * 32], np.int32)
+    kmin, kmax, p = 1, 0, 0.9
+    for h in range(H):
+        n = cand_len[h]
+        if kind == "uniform":
+            c[h, :n] = np.float32(1.0 / max(n, 1))
+        elif kind == "ties":
+            c[h, :n] = rng.choice(np.float32([0.5, 0.25, 0.125]), n) / max(n, 1)
+        elif kind == "onehot":
+            if n:
+                c[h, rng.integers(0, n)] = 1.0
+        elif kind == "nan_range":
+            c[h, :n] = rng.random(n).astype(np.float32) / max(n, 1)
+            if n > 3:
+                c[h, 1] = np.nan
+                c[h, 2] = 3.0
+                c[h, 3] = -0.5
+        elif kind == "zeros":
+            pass
+        elif kind == "clamp":
+            c[h, :n] = rng.dirichlet(np.ones(max(n, 1)))[:n].astype(np.float32)
+            kmin, kmax, p = 5, 40, 0.99
+    ct = torch.tensor(c, device=DEV)
+    clt = torch.tensor(cand_len, device=DEV)
+    sel = torch.empty(H, S // 32, dtype=torch.int32, device=DEV)
+    k = torch.empty(H, dtype=torch.int32, device=DEV)
+    st = torch.zeros(1, dtype=torch.int32, device=DEV)
+    hk.hk_topp_select(H, S, clt, None, ct, p, sel, k, k_min=kmin, k_max=kmax, status=st)
+    torch.cuda.synchronize()
+    for h in range(H):
+        cand = np.arange(S) < cand_len[h]
+        r = O.topp_head(c[h], cand, p, k_min=kmin, k_max=kmax)
+        assert int(k[h]) == r.k, (kind, h)
+        assert np.array_equal(unpack_bits(np_i(sel[h]), S), r.sel), (kind, h)
+    flag = int(st.item())
+    if kind == "nan_range":
+        assert flag & hk.FLAG_NAN and flag & hk.FLAG_RANGE
+    else:
+        assert flag == 0
+
+
+@pytest.mark.parametrize("case", range(4))
+def test_solve_T(case):
+    import paper_2606_28831_amd as hk
+    H, S = 8, 1024
+    rng = np.random.default_rng(case)
+    x = np.full((H, S), -np.inf, np.float32)
+    cand_len = rng.integers(16, S // 32 + 1, H).astype(np.int32) * 32
+    ks = np.zeros(H, np.int32)
+    tg = np.zeros(H, np.float32)
+    for h in range(H):
+        n = cand_len[h]
+        if case == 0:     # two-level closed form
+            a, b, k = 1.0, 0.0, max(1, n // 10)
+            x[h, :n] = b
+            x[h, rng.permutation(n)[:k]] = a
+            tg[h], ks[h] = 0.5, k
+        else:
+            x[h, :n] = -rng.random(n).astype(np.float32) * (case * 0.7)
+            ks[h] = rng.integers(1, n)
+            tg[h] = rng.uniform(ks[h] / n * 1.05, 0.99)
+    T = torch.empty(H, device=DEV)
+    hk.hk_calibrate_solve_T(H, S, torch.tensor(cand_len, device=DEV), None,
+                            torch.tensor(x, device=DEV), torch.tensor(ks, device=DEV),
+                            torch.tensor(tg, device=DEV), T)
+    torch.cuda.synchronize()
+    for h in range(H):
+        cand = np.arange(S) < cand_len[h]
+        want = O.solve_T_head(x[h].astype(np.float64), cand, int(ks[h]), float(tg[h]))
+        assert float(T[h]) == pytest.approx(want, rel=2e-3), h
+        if case == 0:
+            n, k = cand_len[h], ks[h]
+            closed = 1.0 / math.log(0.5 * (n - k) / (k * 0.5))
+            assert float(T[h]) == pytest.approx(closed, rel=2e-3)
+
+
+def _snapshot(w):
+    return dict(table=np_i(w.page_table).copy(), mask=np_i(w.page_mask).astype(np.int64) & 0xFFFF,
+                n=np_i(w.n_pages).copy(), free=np_i(w.free_ids).copy(), top=int(w.free_top.item()),
+                k=w.k_pool.detach().clone(), v=w.v_pool.detach().clone())
+
+
+def _check_compaction(w, before, sel_np, L_dense, L_sparse, S):
+    table, mask, n_new = np_i(w.page_table), np_i(w.page_mask).astype(np.int64) & 0xFFFF, np_i(w.n_pages)
+    top = int(w.free_top.item())
+    free = set(np_i(w.free_ids)[:top].tolist())
+    live = set()
+    new_ids = []
+    for h in range(table.shape[0]):
+        sel = unpack_bits(sel_np[h], S)
+        r = O.compact_head(before["table"][h], before["mask"][h], int(before["n"][h]), sel,
+                           L_dense, L_sparse)
+        assert n_new[h] == len(r.pages), f"n_pages head {h}"
+        for pos, e in enumerate(r.pages):
+            pid = int(table[h, pos])
+            assert mask[h, pos] == e.mask, f"mask head {h} pos {pos}"
+            assert pid not in live
+            live.add(pid)
+            if e.kind == "new":
+                new_ids.append(pid)
+                src = torch.tensor([ph * 16 + t for ph, t in e.src], device=w.k_pool.device)
+                got_k = w.k_pool.view(-1, w.k_pool.shape[-1])[pid * 16: pid * 16 + len(e.src)]
+                got_v = w.v_pool.view(-1, w.v_pool.shape[-1])[pid * 16: pid * 16 + len(e.src)]
+                want_k = before["k"].view(-1, w.k_pool.shape[-1]).index_select(0, src)
+                want_v = before["v"].view(-1, w.v_pool.shape[-1]).index_select(0, src)
+                assert torch.equal(got_k.view(torch.int16) if got_k.dtype == torch.bfloat16 else got_k.view(torch.int32),
+                                   want_k.view(torch.int16) if want_k.dtype == torch.bfloat16 else want_k.view(torch.int32)), \
+                    f"K bytes head {h} pos {pos}"
+                assert torch.equal(got_v.view(torch.int16) if got_v.dtype == torch.bfloat16 else got_v.view(torch.int32),
+                                   want_v.view(torch.int16) if want_v.dtype == torch.bfloat16 else want_v.view(torch.int32)), \
+                    f"V bytes head {h} pos {pos}"
+            else:
+                assert pid == e.phys, f"kept page head {h} pos {pos}"
+        assert np.all(table[h, len(r.pages):] == -1)
+        assert np.all(mask[h, len(r.pages):] == 0)
+    assert live.isdisjoint(free)
+    assert len(live) + len(free) == len(before["free"]), "pages lost or duplicated"
+    assert set(new_ids) <= set(before["free"][:before["top"]].tolist())
+
+
+@pytest.mark.parametrize("name", list(CASES))
+@pytest.mark.parametrize("tiers", [(0, 0), (32, 64), (512, 2048)])
+def test_compact(name, tiers):
+    hk, cfg, w, kv = _setup(name, max_pages=None)
+    L_dense, L_sparse = tiers
+    H, S = w.n_heads, w.S_max
+    d = hk.dims(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"], cfg["W"])
+    rng = np.random.default_rng(5)
+    sel_np = rng.integers(-2 ** 31, 2 ** 31, size=(H, S // 32), dtype=np.int64).astype(np.int32)
+    sel_np[0] = 0                               # a head whose bands select nothing
+    sel = torch.tensor(sel_np, device=DEV)
+    before = _snapshot(w)
+    alloc = hk.Allocator(w.free_ids, w.free_top)
+    st = torch.zeros(1, dtype=torch.int32, device=DEV)
+    ws = hk.workspace(hk.OP_COMPACT, d, w.max_pages, DEV)
+    hk.hk_compact(d, kv, sel, L_dense, L_sparse, alloc, st, ws)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    _check_compaction(w, before, sel_np, L_dense, L_sparse, S)
+
+
+def test_compact_nospace_leaves_cache_unchanged():
+    hk, cfg, w, kv = _setup("bf16_d128_g4_ragged_holes")
+    H, S = w.n_heads, w.S_max
+    d = hk.dims(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"], cfg["W"])
+    w.free_top.fill_(1)                        # almost no free page
+    sel = torch.full((H, S // 32), -1, dtype=torch.int32, device=DEV)
+    before = _snapshot(w)
+    st = torch.zeros(1, dtype=torch.int32, device=DEV)
+    hk.hk_compact(d, kv, sel, 0, 0, hk.Allocator(w.free_ids, w.free_top), st,
+                  hk.workspace(hk.OP_COMPACT, d, w.max_pages, DEV))
+    torch.cuda.synchronize()
+    assert int(st.item()) & hk.FLAG_NOSPACE
+    assert np.array_equal(np_i(w.page_table), before["table"])
+    assert np.array_equal(np_i(w.n_pages), before["n"])
+    assert int(w.free_top.item()) == 1
+    assert torch.equal(w.k_pool, before["k"])
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_decode(name):
+    hk, cfg, w, kv = _setup(name)
+    G = cfg["Hq"] // cfg["Hkv"]
+    if G not in (1, 2, 4, 7, 8):
+        pytest.skip("group size")
+    d = hk.dims(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"])
+    gen = torch.Generator(device=DEV).manual_seed(3)
+    q = (torch.randn(w.NS, cfg["Hq"], cfg["D"], generator=gen, device=DEV) * 2).to(w.k_pool.dtype)
+    o = torch.empty(w.NS, cfg["Hq"], cfg["D"], device=DEV)
+    lse = torch.empty(w.NS, cfg["Hq"], device=DEV)
+    ws = hk.workspace(hk.OP_DECODE, d, w.max_pages, DEV)
+    scale = 1 / math.sqrt(cfg["D"])
+    hk.hk_decode_attn(d, q, kv, scale, o, lse, ws)
+    torch.cuda.synchronize()
+    host = HostCache(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)
+    qn, on, ln = np64(q), np64(o), np64(lse)
+    rtol = RTOL[cfg["dtype"]]
+    for h in range(w.n_heads):
+        K, valid = host.head(h)
+        V, _ = host.head_v(h)
+        s, kvh = divmod(h, cfg["Hkv"])
+        ref_o, ref_l = O.decode_head(qn[s, kvh * G:(kvh + 1) * G], K, V, valid, scale)
+        for g in range(G):
+            check_prob(on[s, kvh * G + g], ref_o[g], rtol, f"o head {h} g {g}")
+        check_lse(ln[s, kvh * G:(kvh + 1) * G], ref_l, rtol, f"lse head {h}")
+
+
+def test_decode_after_compaction_equals_masked_original():
+    """Tier equivalence (Sec. 3.3.1 HA-Max vs HA-Sparse): attention over the rewritten
+    cache equals attention over the original pages restricted to the kept slots."""
+    hk, cfg, w, kv = _setup("bf16_d128_g4_ragged_holes")
+    H, S = w.n_heads, w.S_max
+    d = hk.dims(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"], cfg["W"])
+    rng = np.random.default_rng(9)
+    sel_np = rng.integers(-2 ** 31, 2 ** 31, size=(H, S // 32), dtype=np.int64).astype(np.int32)
+    sel = torch.tensor(sel_np, device=DEV)
+    q = torch.randn(w.NS, cfg["Hq"], cfg["D"], device=DEV).to(w.k_pool.dtype)
+    masked = w.page_mask.clone()
+    bits = torch.tensor(sel_np.view(np.uint16).reshape(H, -1).astype(np.int32), device=DEV)
+    masked = (masked.to(torch.int32) & bits[:, :w.max_pages]).to(torch.int16)
+    kv_sparse = hk.PagedKV(w.k_pool, w.v_pool, w.page_table.clone(), masked, w.n_pages.clone())
+    dd = hk.dims(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"])
+    ws = hk.workspace(hk.OP_DECODE, dd, w.max_pages, DEV)
+    o1 = torch.empty(w.NS, cfg["Hq"], cfg["D"], device=DEV)
+    l1 = torch.empty(w.NS, cfg["Hq"], device=DEV)
+    hk.hk_decode_attn(dd, q, kv_sparse, 0.1, o1, l1, ws)
+    st = torch.zeros(1, dtype=torch.int32, device=DEV)
+    hk.hk_compact(d, kv, sel, 0, 0, hk.Allocator(w.free_ids, w.free_top), st,
+                  hk.workspace(hk.OP_COMPACT, d, w.max_pages, DEV))
+    o2 = torch.empty_like(o1)
+    l2 = torch.empty_like(l1)
+    hk.hk_decode_attn(dd, q, kv, 0.1, o2, l2, ws)
+    torch.cuda.synchronize()
+    check_prob(np64(o2).reshape(-1), np64(o1).reshape(-1), 2e-3, "o")
+    check_lse(np64(l2).reshape(-1), np64(l1).reshape(-1), 2e-3, "lse")
+
+
+@pytest.mark.parametrize("name", ["bf16_d128_g4_ragged_holes", "cfg1_f32_d64_g4",
+                                  "bf16_d128_g1_w32_tail1"])
+def test_append(name):
+    hk, cfg, w, kv = _setup(name, max_pages=256)
+    d = hk.dims(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"])
+    alloc = hk.Allocator(w.free_ids, w.free_top)
+    st = torch.zeros(1, dtype=torch.int32, device=DEV)
+    for step in range(20):
+        before = HostCache(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)
+        top0 = int(w.free_top.item())
+        kn = torch.randn(w.NS, cfg["Hkv"], cfg["D"], device=DEV).to(w.k_pool.dtype)
+        vn = torch.randn(w.NS, cfg["Hkv"], cfg["D"], device=DEV).to(w.k_pool.dtype)
+        hk.hk_append_kv(d, kv, kn, vn, alloc, st)
+        torch.cuda.synchronize()
+        after = HostCache(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)
+        pops = 0
+        for h in range(w.n_heads):
+            K0, v0 = before.head(h)
+            K1, v1 = after.head(h)
+            pp, slot, new = O.append_position(before.mask[h], int(before.n[h]))
+            pops += int(new)
+            j = pp * 16 + slot
+            exp_valid = np.zeros(max(len(v0), j + 1), bool)
+            exp_valid[:len(v0)] = v0
+            exp_valid[j] = True
+            assert np.array_equal(v1[:len(exp_valid)], exp_valid), (step, h)
+            s, kvh = divmod(h, cfg["Hkv"])
+            assert np.array_equal(K1[j], np64(kn[s, kvh])), (step, h)
+            assert np.array_equal(after.head_v(h)[0][j], np64(vn[s, kvh]))
+            assert np.array_equal(K1[:len(v0)][v0], K0[v0])
+        assert int(w.free_top.item()) == top0 - pops
+    assert int(st.item()) == 0
+
+
+def test_determinism_bitwise():
+    outs = []
+    for _ in range(2):
+        hk, cfg, w, kv, s, cl = _calib_inputs("bf16_d128_g7_tempered")
+        H, S = w.n_heads, w.S_max
+        c = torch.empty(H, S, device=DEV)
+        hk.hk_calibrate(H, S, cl, w.page_mask, [s], None, [1.0], c)
+        sel = torch.empty(H, S // 32, dtype=torch.int32, device=DEV)
+        k = torch.empty(H, dtype=torch.int32, device=DEV)
+        hk.hk_topp_select(H, S, cl, w.page_mask, c, 0.9, sel, k)
+        d = hk.dims(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"], cfg["W"])
+        st = torch.zeros(1, dtype=torch.int32, device=DEV)
+        hk.hk_compact(d, kv, sel, 0, 0, hk.Allocator(w.free_ids, w.free_top), st,
+                      hk.workspace(hk.OP_COMPACT, d, w.max_pages, DEV))
+        torch.cuda.synchronize()
+        outs.append([t.cpu().clone() for t in (s, c, sel, k, w.page_table, w.page_mask, w.n_pages,
+                                               w.free_ids, w.k_pool.view(torch.int16))])
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)

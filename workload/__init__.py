@@ -19,7 +19,7 @@ Layouts (shared by every entry point):
 from __future__ import annotations
 
 import math
-from dataclasses import dataclass, field, replace
+from dataclasses import dataclass, field
 
 import torch
 
@@ -105,6 +105,7 @@ def make_workload(cfg: dict, device="cpu", pool_slack: float = 2.0, max_pages: i
     dt = TORCH_DTYPE[cfg["dtype"]]
     n_used = -(-N // PAGE)
     mp = max(n_used, max_pages or 0)
+    mp += mp % 2                    # even table width: S_max is a multiple of 32
     used = H * n_used
     num_pages = int(pool_pages) if pool_pages else max(int(math.ceil(used * pool_slack)), used + 1)
 
@@ -138,8 +139,8 @@ def make_workload(cfg: dict, device="cpu", pool_slack: float = 2.0, max_pages: i
     n_pages = torch.full((H,), n_used, dtype=torch.int32, device=dev)
 
     # K/V pools: every page holds N(0,1) draws; live pages are (re)written per head
-    k_pool = torch.empty(num_pages, PAGE, D, dtype=dt, device=dev)
-    v_pool = torch.empty(num_pages, PAGE, D, dtype=dt, device=dev)
+    k_pool = torch.zeros(num_pages, PAGE, D, dtype=dt, device=dev)
+    v_pool = torch.zeros(num_pages, PAGE, D, dtype=dt, device=dev)
     chunk = max(1, (1 << 28) // max(1, n_used * PAGE * D * 4))
     plant = cfg.get("recipe") == "planted"
     n_plant = int(round(0.02 * N))
@@ -157,12 +158,6 @@ def make_workload(cfg: dict, device="cpu", pool_slack: float = 2.0, max_pages: i
         ids = table[h0:h1, :n_used].reshape(-1).long()
         k_pool[ids] = kl.to(dt).view(-1, PAGE, D)
         v_pool[ids] = vl.to(dt).view(-1, PAGE, D)
-    free_pages = free_ids[:n_free].long()
-    if n_free:
-        for f0 in range(0, n_free, 1 << 16):
-            f = free_pages[f0:f0 + (1 << 16)]
-            k_pool[f] = torch.randn(len(f), PAGE, D, generator=g, device=dev).to(dt)
-            v_pool[f] = torch.randn(len(f), PAGE, D, generator=g, device=dev).to(dt)
 
     ref = None
     n_ref = cfg.get("n_ref", 0)

@@ -235,7 +235,9 @@ def topp_head(c, cand, p: float, k_min: int = 1, k_max: int = 0) -> ToppResult:
     c = np.asarray(c)
     idx = np.nonzero(cand)[0]
     n = len(idx)
-    order = order_desc(np.where(np.isnan(c), 0.0, c), idx)
+    # inputs are probabilities: NaN counts as 0 and values are clamped to [0, 1]
+    # before both the ordering and the fixed-point weights
+    order = order_desc(np.clip(np.where(np.isnan(c), 0.0, c), 0.0, 1.0), idx)
     w = {j: fixed_weight(float(c[j])) for j in idx}
     total = sum(w.values())
     pq = quantise_p(p)

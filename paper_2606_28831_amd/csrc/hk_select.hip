@@ -149,7 +149,10 @@ __global__ __launch_bounds__(SEL_NT) void topp_kernel(
       w[i] = (unsigned long long)(v * (float)kMassOne);   // exact scaling, truncation = floor
     }
   }
-  flags = __syncthreads_or(flags);
+  // __syncthreads_or returns a predicate, so each flag bit is reduced on its own
+  const int any_nan = __syncthreads_or(flags & HK_FLAG_NAN);
+  const int any_range = __syncthreads_or(flags & HK_FLAG_RANGE);
+  flags = (any_nan ? HK_FLAG_NAN : 0) | (any_range ? HK_FLAG_RANGE : 0);
   if (tid == 0 && flags && status) atomicOr(status, flags);
 
   const int n_cand = block_sum_int<SEL_NT>(__popc(cbits), redi);

@@ -279,6 +279,10 @@ def test_topp_clamps_and_empty():
     cn = np.array([np.nan, 0.5, 0.5], np.float32)
     r = O.topp_head(cn, np.ones(3, bool), 1.0)
     assert r.k == 2 and not r.sel[0]
+    # values above 1 clamp to 1 and then tie: the more recent slot ranks first
+    cc = np.array([3.0, 2.0, 0.0, 0.0], np.float32)
+    r = O.topp_head(cc, np.ones(4, bool), 0.5)
+    assert r.k == 1 and r.sel[1] and not r.sel[0]
 
 
 # ---------------------------------------------------------------- T solve (a2')

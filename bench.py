@@ -1,0 +1,288 @@
+#!/usr/bin/env python3
+"""Benchmark of the Hard-KV decoding-time compression step on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--config {1,2,3,4,5}]
+
+A step (configs 1-4) is one pass of the whole hot path over every head of the
+workload: score -> calibrate -> Top-p -> Cascade-Cache rewrite.  The rewrite
+mutates the cache, so before each step the small metadata (tables, masks, page
+counts, free list) is restored to its pristine copy -- the K/V pages themselves
+are never overwritten by a rewrite (it writes only freshly popped pages), so the
+pristine cache is whole again.  The restore (a few MB of device copies) stays
+inside the timed region, which makes the reported rate slightly conservative.
+
+Config 5 runs the end-to-end decode loop (append + paged decode attention per
+layer per step, compression every 128 steps) and reports decode tokens/s.
+
+Prints ONE JSON line (rank 0).  value = compressed KV tokens/s = candidate
+(head, slot) pairs processed per second.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+METRIC = "compressed KV tokens/s (score+Top-p+compact) & % HBM peak; decode tok/s"
+
+
+def _events(n):
+    return [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+
+
+def _esize(cfg):
+    return 2 if cfg["dtype"] == "bf16" else 4
+
+
+def _cand_tokens(w, L_dense):
+    """Candidate (head, slot) pairs of the pristine cache: valid slots older than the dense tier."""
+    m = w.page_mask.to(torch.int32) & 0xFFFF
+    bits = ((m[:, :, None] >> torch.arange(16, device=m.device, dtype=torch.int32)) & 1)
+    n = w.n_pages.long()
+    nd = torch.clamp(n, max=-(-L_dense // 16))
+    pos = torch.arange(w.max_pages, device=m.device)[None, :]
+    cand_pages = pos < (n - nd)[:, None]
+    return int((bits.sum(-1) * cand_pages).sum().item())
+
+
+def run_compression(args):
+    import paper_2606_28831_amd as hk
+    import workload as WL
+    from paper_2606_28831_amd.pipeline import Compressor
+
+    c = args.config
+    cfg = WL.config(c)
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    t_gen = time.perf_counter()
+    w = WL.make_workload(cfg, dev)
+    torch.cuda.synchronize()
+    t_gen = time.perf_counter() - t_gen
+    kv = hk.PagedKV(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)
+    alloc = hk.Allocator(w.free_ids, w.free_top)
+    metric = "attn+red" if cfg.get("n_ref") else "attn"
+    comp = Compressor(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"], cfg["W"], kv, alloc, cfg["p"],
+                      L_dense=cfg["L_dense"], L_sparse=cfg["L_sparse"], metric=metric,
+                      n_ref=cfg.get("n_ref", 0))
+    pristine = WL.clone_state(w)
+    ref = w.ref_slots
+    tokens = _cand_tokens(w, cfg["L_dense"])
+    positions = w.NS * cfg["N"]
+
+    def restore():
+        WL.restore_state(w, pristine)
+
+    for _ in range(args.warmup):
+        restore()
+        comp.step(w.q_obs, ref_slots=ref)
+    torch.cuda.synchronize()
+
+    # ---------------- timed region: exactly K steps
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        restore()
+        comp.step(w.q_obs, ref_slots=ref)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    status = int(comp.buf.status.item())
+
+    # ---------------- per-stage timing (HIP events on the launch stream), outside the timed loop
+    reps = max(3, min(args.steps, 10))
+    ev = _events(8 * reps)
+    lse_given = comp.buf.row_lse.clone()
+    for r in range(reps):
+        restore()
+        e = ev[8 * r:8 * r + 8]
+        e[0].record()
+        comp.score(w.q_obs, ref_slots=ref)
+        e[1].record()
+        comp.select()
+        e[2].record()
+        comp.compact()
+        e[3].record()
+        restore()
+        e[4].record()
+        comp.score(w.q_obs, ref_slots=ref, row_lse_in=lse_given)     # pass 2 alone: one kernel
+        e[5].record()
+    torch.cuda.synchronize()
+
+    def avg(a, b):
+        return sum(ev[8 * r + a].elapsed_time(ev[8 * r + b]) for r in range(reps)) / reps
+
+    st = {"score": avg(0, 1), "select": avg(1, 2), "compact": avg(2, 3), "score_pass2": avg(4, 5)}
+    st["score_pass1_merge"] = st["score"] - st["score_pass2"]
+    step_ms_events = st["score"] + st["select"] + st["compact"]
+
+    # ---------------- budget statistics of the last step
+    restore()
+    comp.step(w.q_obs, ref_slots=ref)
+    torch.cuda.synchronize()
+    k = comp.buf.k.float()
+    cl = comp.buf.cand_len.float()
+    nc_valid = tokens / max(1, w.n_heads)
+    frac = (k / torch.clamp(cl, min=1)).cpu()
+    kept_mean = float(k.mean())
+
+    # ---------------- algorithmic bytes (K read once, scores written+read, selection bits,
+    # condensed K and V read + written); flops of the score contraction per pass
+    D, e = cfg["D"], _esize(cfg)
+    S = w.S_max
+    G = cfg["Hq"] // cfg["Hkv"]
+    R = G * cfg["W"]
+    H = w.n_heads
+    n_metric = 2 if metric == "attn+red" else 1
+    k_cond_total = float(k.sum())
+    bytes_k = tokens * D * e
+    bytes_scores = H * S * 4 * 2 * n_metric
+    bytes_sel = H * S / 8 * 2
+    bytes_rewrite = 4 * k_cond_total * D * e
+    bytes_q = cfg["W"] * w.NS * cfg["Hq"] * D * e
+    alg_bytes = bytes_k + bytes_scores + bytes_sel + bytes_rewrite + bytes_q
+    step_s = ms_per_step / 1e3
+    pass2_bytes = bytes_k + H * S * 4 + bytes_q
+    pass2_flops = 2.0 * R * tokens * D
+    if metric == "attn+red":
+        pass2_flops += 2.0 * cfg["n_ref"] * tokens * D
+
+    roof_kernel = {
+        "kernel": "score_pass2_kernel",
+        "bound": "hbm",
+        "achieved": pass2_bytes / (st["score_pass2"] / 1e3) / 1e9,
+        "peak": HBM_PEAK_GBS,
+        "unit": "GB/s",
+        "traffic": None,
+        "mfma_tflops": pass2_flops / (st["score_pass2"] / 1e3) / 1e12,
+        "bytes_per_launch": pass2_bytes,
+    }
+    roof_kernel["frac"] = roof_kernel["achieved"] / roof_kernel["peak"]
+
+    out = {
+        "metric": METRIC,
+        "value": tokens / step_s,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg["dtype"],
+        "data": "synthetic",
+        "config": {"workload": cfg["name"], "sequences": w.NS, "q_heads": cfg["Hq"],
+                   "kv_heads": cfg["Hkv"], "head_dim": D, "cache_len": cfg["N"],
+                   "window": cfg["W"], "top_p": cfg["p"], "page": 16,
+                   "L_dense": cfg["L_dense"], "L_sparse": cfg["L_sparse"], "metric": metric},
+        "hbm_frac_step": alg_bytes / step_s / 1e9 / HBM_PEAK_GBS,
+        "alg_bytes_per_step": alg_bytes,
+        "positions_per_s": positions / step_s,
+        "stage_ms": st,
+        "step_ms_events": step_ms_events,
+        "budget": {"mean_kept": kept_mean, "min_frac": float(frac.min()),
+                   "mean_frac": float(frac.mean()), "max_frac": float(frac.max()),
+                   "SU": float(frac.mean() / max(1e-9, float(frac.max())))},
+        "status_flags": status,
+        "gen_s": t_gen,
+        "roofline": roof_kernel,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, cfg, comp, args)
+    return out
+
+
+def cpu_baseline(w, cfg, comp, args):
+    """The oracle, as it stands, on a bounded sample of heads of the same workload."""
+    import numpy as np
+
+    import oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    G = cfg["Hq"] // cfg["Hkv"]
+    D = cfg["D"]
+    scale = 1 / math.sqrt(D)
+    pristine_table = w.page_table.cpu().numpy()
+    masks = w.page_mask.cpu().numpy().astype(np.int64) & 0xFFFF
+    n = w.n_pages.cpu().numpy()
+    budget_s = args.cpu_seconds
+    heads = list(range(0, w.n_heads, max(1, w.n_heads // 64)))
+    done_tokens, spent, used = 0, 0.0, []
+    for h in heads:
+        ids = torch.tensor(pristine_table[h, :n[h]], dtype=torch.long, device=w.k_pool.device)
+        kh = w.k_pool.index_select(0, ids).float().cpu().numpy()
+        vh = w.v_pool.index_select(0, ids).float().cpu().numpy()
+        s_, kv = divmod(h, cfg["Hkv"])
+        q = w.q_obs[:, s_, kv * G:(kv + 1) * G].float().cpu().numpy().reshape(-1, D)
+        local = np.arange(n[h])
+        refs = w.ref_slots[h].cpu().numpy() if w.ref_slots is not None else None
+        t0 = time.perf_counter()
+        rows, valid = O.read_head(kh, local, masks[h], int(n[h]))
+        nc, ns, nd = O.tier_pages(int(n[h]), cfg["L_dense"], cfg["L_sparse"])
+        cand_len = 16 * (int(n[h]) - nd)
+        s, _ = O.score_head(q, rows, valid, cand_len, scale)
+        cand = O.candidate_mask(valid, cand_len)
+        c, _ = O.calibrate_head(s, cand)
+        if refs is not None:
+            xr = O.redundancy_head(rows, valid, cand_len, refs)
+            r0 = O.topp_head(c.astype(np.float32), cand, cfg["p"])
+            T = O.solve_T_head(xr, cand, r0.k, r0.sel_mass / 2.0 ** 40)
+            c = O.mix([c, O.calibrate_head(xr, cand, T)[0]], [0.5, 0.5])
+        r = O.topp_head(c.astype(np.float32), cand, cfg["p"])
+        res = O.compact_head(local, masks[h], int(n[h]), r.sel, cfg["L_dense"], cfg["L_sparse"])
+        for ent in res.pages:
+            if ent.kind == "new":
+                src = [ph * 16 + t for ph, t in ent.src]
+                _ = kh.reshape(-1, D)[src].copy(), vh.reshape(-1, D)[src].copy()
+        spent += time.perf_counter() - t0
+        done_tokens += int(cand.sum())
+        used.append(h)
+        if spent >= budget_s:
+            break
+    return {"value": done_tokens / spent, "unit": "tokens/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{len(used)} of {w.n_heads} heads ({done_tokens} candidate slots), "
+                      f"full chain score->calibrate->Top-p->rewrite, {spent:.1f} s"}
+
+
+def run_decode(args):
+    from decode_loop import run
+    return run(args)
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the compression step is independent per (sequence, KV "
+              "head) and is benchmarked on a single MI355X; --gpus above 1 is not supported.",
+              file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    out = run_decode(args) if args.config == 5 else run_compression(args)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -118,8 +118,8 @@ __global__ __launch_bounds__(DEC_NT) void decode_split_kernel(
       pm = fmaxf(pm, __shfl_xor(pm, 16, 64));
       pm = fmaxf(pm, __shfl_xor(pm, 32, 64));
       const float mn = fmaxf(m_run[g], pm);     // finite: the page has a valid slot
-      alpha[g] = exp2f(m_run[g] - mn);
-      pr[g] = exp2f(zl[g] - mn);
+      alpha[g] = fast_exp2(m_run[g] - mn);
+      pr[g] = fast_exp2(zl[g] - mn);
       m_run[g] = mn;
       l_part[g] = l_part[g] * alpha[g] + (c == 0 ? pr[g] : 0.f);
     }
@@ -177,7 +177,7 @@ __global__ __launch_bounds__(DEC_NT) void decode_split_kernel(
     if (M != -INFINITY)
 #pragma unroll
       for (int w = 0; w < DEC_NW; ++w) {
-        const float a = exp2f(s_m[w][g] - M);
+        const float a = fast_exp2(s_m[w][g] - M);
         L += s_l[w][g] * a;
         O += s_o[w][g][d] * a;
       }

@@ -18,6 +18,13 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
+// Hardware base-2 exponential and logarithm (v_exp_f32 / v_log_f32, ~1 ulp).  Unlike the
+// library exp2f/log2f they skip the denormal range fix-ups: results below 2^-126 come out
+// as 0 and log of a denormal input as -inf, which is harmless where they are used (sums of
+// probabilities whose terms below 2^-126 carry no weight).
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
+
 // bf16 bits -> fp32 (exact)
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }

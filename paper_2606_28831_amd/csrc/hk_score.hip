@@ -136,20 +136,211 @@ __device__ __forceinline__ void stage_rows(char* lds, int R, int R_pad, RowFn ro
   }
 }
 
-constexpr int QB_MAX = 8;   // R_pad <= 256
-constexpr int SCORE_NT = 256;
+#ifndef HK_SCORE_NT
+#define HK_SCORE_NT 512
+#endif
+#ifndef HK_SCORE_PPW
+#define HK_SCORE_PPW 128
+#endif
+#ifndef HK_SCORE_PREFETCH
+#define HK_SCORE_PREFETCH 0
+#endif
+#ifndef HK_SCORE_WPE
+#define HK_SCORE_WPE 0
+#endif
+#ifndef HK_SCORE_KT
+#define HK_SCORE_KT 1
+#endif
+#if HK_SCORE_WPE > 0
+#define HK_SCORE_ATTR __launch_bounds__(SCORE_NT) __attribute__((amdgpu_waves_per_eu(HK_SCORE_WPE, HK_SCORE_WPE)))
+#else
+#define HK_SCORE_ATTR __launch_bounds__(SCORE_NT)
+#endif
+
+constexpr int SCORE_NT = HK_SCORE_NT;      // threads per workgroup
+constexpr int SCORE_NW = SCORE_NT / 64;
+constexpr int SCORE_PPW = HK_SCORE_PPW;    // pages per workgroup
+constexpr int SCORE_KT = HK_SCORE_KT;      // 32-key tiles a wave holds at once
+constexpr int SCORE_WPP = 2 * SCORE_KT;    // pages per wave iteration
+constexpr int NREF_MAX = 256;
+
+// Query blocks of 32 rows are a compile-time count; other counts round up to the next
+// instantiated one (the extra rows are zero and carry no weight).
+__host__ __device__ constexpr int qb_eff(int qb) {
+  return qb <= 1 ? 1 : qb <= 2 ? 2 : qb <= 4 ? 4 : qb <= 7 ? 7 : 8;
+}
+__host__ __device__ constexpr int score_rpad(int R) { return 32 * qb_eff((R + 31) / 32); }
+
+// MFMA chain of one 32x32 output block over the whole head dimension.  LDS_IS_A: the
+// LDS block is the A operand (rows of C), the register fragment the B operand.
+template <typename F, bool LDS_IS_A>
+__device__ __forceinline__ f32x16 mma_chain(const F& kf, const char* lds, int blk, int lane) {
+  f32x16 acc = {};
+#pragma unroll
+  for (int kk = 0; kk < F::KSTEPS; ++kk) {
+    if constexpr (LDS_IS_A) acc = F::mma(F::lds(lds, blk, kk, lane), kf.v[kk], acc);
+    else acc = F::mma(kf.v[kk], F::lds(lds, blk, kk, lane), acc);
+  }
+  return acc;
+}
+
+// KT interleaved chains sharing each LDS operand read (KT register fragments).
+template <typename F, bool LDS_IS_A, int KT>
+__device__ __forceinline__ void mma_chains(const F* kf, const char* lds, int blk, int lane,
+                                           f32x16* acc) {
+#pragma unroll
+  for (int t = 0; t < KT; ++t) acc[t] = f32x16{};
+#pragma unroll
+  for (int kk = 0; kk < F::KSTEPS; ++kk) {
+    const auto op = F::lds(lds, blk, kk, lane);
+#pragma unroll
+    for (int t = 0; t < KT; ++t) {
+      if constexpr (LDS_IS_A) acc[t] = F::mma(op, kf[t].v[kk], acc[t]);
+      else acc[t] = F::mma(kf[t].v[kk], op, acc[t]);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------------
+// Software-pipelined full tiles (KT = 1).  Within one wave the MFMAs of query block qb
+// are interleaved with the VALU work on block qb-1 (independent data), and each LDS
+// fragment is read two MFMA steps before its use.  MFMA and VALU work of one wave overlap
+// on the SIMD; split across different waves they do not, which is why the interleave is
+// made explicit here and pinned with scheduling-group barriers.
+template <typename F>
+using lds_frag_t = decltype(F::lds(nullptr, 0, 0, 0));
+
+template <int N_VALU>
+__device__ __forceinline__ void sched_step() {
+  __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);        // one MFMA
+  __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);        // one LDS read
+  __builtin_amdgcn_sched_group_barrier(0x002, N_VALU, 0);   // VALU work
+}
+
+// pass 2: returns this lane's partial column sum  sum_r exp2(c2*z[r][key] - lse2[r])
+template <typename F, int QB>
+__device__ __forceinline__ float p2_tile_pipelined(const F& kf, const char* qlds, const float* lse2,
+                                                   float c2, int lane) {
+  constexpr int KS = F::KSTEPS;
+  constexpr int NF = QB * KS;
+  lds_frag_t<F> qf[3];
+  qf[0] = F::lds(qlds, 0, 0, lane);
+  if constexpr (NF > 1) qf[1] = F::lds(qlds, 1 / KS, 1 % KS, lane);
+  f32x16 acc[2];
+  float col = 0.f;
+#pragma unroll
+  for (int qb = 0; qb <= QB; ++qb) {
+    f32x4 l4[4];
+    if (qb >= 1) {
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4)
+        l4[r4] = *reinterpret_cast<const f32x4*>(lse2 + (qb - 1) * 32 + 8 * r4 + 4 * (lane >> 5));
+    }
+    if (qb < QB) acc[qb & 1] = f32x16{};
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      const int g = qb * KS + kk;
+      if (qb < QB) {
+        acc[qb & 1] = F::mma(qf[g % 3], kf.v[kk], acc[qb & 1]);
+        if (g + 2 < NF) qf[(g + 2) % 3] = F::lds(qlds, (g + 2) / KS, (g + 2) % KS, lane);
+      }
+      if (qb >= 1) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          if (e * KS / 16 == kk) col += fast_exp2(fmaf(acc[(qb - 1) & 1][e], c2, -l4[e >> 2][e & 3]));
+      }
+    }
+    if constexpr (sizeof(lds_frag_t<F>) == 16) {
+      if (qb >= 1 && qb < QB) {
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) sched_step<3 * 16 / KS>();
+      }
+    }
+  }
+  return col;
+}
+
+// pass 1: online (max, sum exp2) update of the lane's query column for every block
+template <typename F, int QB>
+__device__ __forceinline__ void p1_tile_pipelined(const F& kf, const char* qlds, float c2, int lane,
+                                                  float* M, float* L) {
+  constexpr int KS = F::KSTEPS;
+  constexpr int NF = QB * KS;
+  lds_frag_t<F> qf[3];
+  qf[0] = F::lds(qlds, 0, 0, lane);
+  if constexpr (NF > 1) qf[1] = F::lds(qlds, 1 / KS, 1 % KS, lane);
+  f32x16 acc[2];
+#pragma unroll
+  for (int qb = 0; qb <= QB; ++qb) {
+    if (qb < QB) {
+      acc[qb & 1] = f32x16{};
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) {
+        const int g = qb * KS + kk;
+        acc[qb & 1] = F::mma(kf.v[kk], qf[g % 3], acc[qb & 1]);
+        if (g + 2 < NF) qf[(g + 2) % 3] = F::lds(qlds, (g + 2) / KS, (g + 2) % KS, lane);
+      }
+    }
+    if (qb >= 1) {
+      const f32x16& a = acc[(qb - 1) & 1];
+      float m0 = fmaxf(a[0], a[1]), m1 = fmaxf(a[2], a[3]), m2 = fmaxf(a[4], a[5]), m3 = fmaxf(a[6], a[7]);
+      m0 = fmaxf(m0, fmaxf(a[8], a[9]));
+      m1 = fmaxf(m1, fmaxf(a[10], a[11]));
+      m2 = fmaxf(m2, fmaxf(a[12], a[13]));
+      m3 = fmaxf(m3, fmaxf(a[14], a[15]));
+      const float m = fmaxf(fmaxf(m0, m1), fmaxf(m2, m3));
+      const float mn = fmaxf(M[qb - 1], m);
+      const float mc = mn * c2;
+      float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+      for (int r = 0; r < 16; r += 2) {
+        s0 += fast_exp2(fmaf(a[r], c2, -mc));
+        s1 += fast_exp2(fmaf(a[r + 1], c2, -mc));
+      }
+      L[qb - 1] = fmaf(L[qb - 1], fast_exp2((M[qb - 1] - mn) * c2), s0 + s1);
+      M[qb - 1] = mn;
+    }
+    if constexpr (sizeof(lds_frag_t<F>) == 16) {
+      if (qb >= 1 && qb < QB) {
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) sched_step<(16 * 3 + 22) / KS>();
+      }
+    }
+  }
+}
+
+// K fragment of the tile at page p0 (2 pages = 32 keys); lanes past p_end get zeros.
+template <typename T, int D>
+__device__ __forceinline__ void load_tile(Frag<T, D>& kf, const T* __restrict__ k_pool,
+                                          const int32_t* __restrict__ trow, int p0, int p_end,
+                                          int lane) {
+  const int kl = lane & 31, pg = p0 + (kl >> 4);
+  if (pg < p_end) {
+    const int phys = trow[pg];
+    kf.load(k_pool + ((size_t)phys * HK_PAGE + (kl & 15)) * D + (lane >> 5) * (D / 2));
+  } else {
+    kf.zero();
+  }
+}
+
+// validity of the 16 accumulator rows a lane holds, from the tile's 32-slot mask
+__device__ __forceinline__ uint32_t lane_rows(uint32_t tmask, int lane) {
+  const uint32_t t = tmask >> (4 * (lane >> 5));
+  return (t & 0xfu) | ((t >> 4) & 0xf0u) | ((t >> 8) & 0xf00u) | ((t >> 12) & 0xf000u);
+}
 
 // ------------------------------------------------------------------ pass 1
-template <typename T, int D>
-__global__ __launch_bounds__(SCORE_NT) void score_pass1_kernel(
+template <typename T, int D, int QB>
+__global__ HK_SCORE_ATTR void score_pass1_kernel(
     const T* __restrict__ q_obs, const T* __restrict__ k_pool, const int32_t* __restrict__ table,
     const uint16_t* __restrict__ masks, const int32_t* __restrict__ n_pages_arr, int NS, int Hq,
-    int Hkv, int W, int max_pages, int ppw, float c2, float2* __restrict__ part, int n_chunks) {
+    int Hkv, int W, int max_pages, float c2, float2* __restrict__ part, int n_chunks) {
   using F = Frag<T, D>;
+  constexpr int R_pad = 32 * QB;
   extern __shared__ __align__(16) char smem[];
   const int h = blockIdx.y, chunk = blockIdx.x;
   const int s = h / Hkv, kv = h % Hkv, G = Hq / Hkv;
-  const int R = G * W, R_pad = (R + 31) & ~31, QB = R_pad >> 5;
+  const int R = G * W;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 
   stage_rows<T, D>(smem, R, R_pad, [&](int r) -> const T* {
@@ -160,79 +351,94 @@ __global__ __launch_bounds__(SCORE_NT) void score_pass1_kernel(
   __syncthreads();
 
   const int n = n_pages_arr[h];
-  const int p_begin = chunk * ppw, p_end = min(p_begin + ppw, n);
-  float M[QB_MAX], L[QB_MAX];
+  const int p_begin = chunk * SCORE_PPW, p_end = min(p_begin + SCORE_PPW, n);
+  float M[QB], L[QB];
 #pragma unroll
-  for (int q = 0; q < QB_MAX; ++q) { M[q] = -INFINITY; L[q] = 0.f; }
+  for (int q = 0; q < QB; ++q) { M[q] = -INFINITY; L[q] = 0.f; }
 
   const int32_t* trow = table + (size_t)h * max_pages;
   const uint16_t* mrow = masks + (size_t)h * max_pages;
-  for (int p0 = p_begin + 2 * wave; p0 < p_end; p0 += 2 * (SCORE_NT / 64)) {
-    const int p1 = p0 + 1;
-    const uint32_t m0 = mrow[p0], m1 = (p1 < p_end) ? mrow[p1] : 0u;
-    const uint32_t tmask = m0 | (m1 << 16);
-    if (tmask == 0) continue;
-    const int kl = lane & 31, pg = p0 + (kl >> 4);
-    F kf;
-    if (pg < p_end) {
-      const int phys = trow[pg];
-      kf.load(k_pool + ((size_t)phys * HK_PAGE + (kl & 15)) * D + (lane >> 5) * (D / 2));
-    } else {
-      kf.zero();
+  for (int p0 = p_begin + SCORE_WPP * wave; p0 < p_end; p0 += SCORE_WPP * SCORE_NW) {
+    F kf[SCORE_KT];
+    uint32_t tm[SCORE_KT];
+    bool all_full = true, any = false;
+#pragma unroll
+    for (int t = 0; t < SCORE_KT; ++t) {
+      const int pa = p0 + 2 * t, pb = pa + 1;
+      load_tile<T, D>(kf[t], k_pool, trow, pa, p_end, lane);
+      tm[t] = (pa < p_end ? (uint32_t)mrow[pa] : 0u) | ((pb < p_end) ? (uint32_t)mrow[pb] << 16 : 0u);
+      all_full = all_full && (tm[t] == 0xffffffffu);
+      any = any || (tm[t] != 0u);
     }
-    const bool full = (tmask == 0xffffffffu);
+    if (all_full && SCORE_KT == 1) {
+      p1_tile_pipelined<F, QB>(kf[0], smem, c2, lane, M, L);
+    } else if (all_full) {
 #pragma unroll
-    for (int qb = 0; qb < QB_MAX; ++qb) {
-      if (qb < QB) {
-        f32x16 acc = {};
+      for (int qb = 0; qb < QB; ++qb) {
+        f32x16 acc[SCORE_KT];
+        mma_chains<F, false, SCORE_KT>(kf, smem, qb, lane, acc);
+        float m = acc[0][0];
 #pragma unroll
-        for (int kk = 0; kk < F::KSTEPS; ++kk) acc = F::mma(kf.v[kk], F::lds(smem, qb, kk, lane), acc);
-        float m = -INFINITY;
-        if (full) {
+        for (int t = 0; t < SCORE_KT; ++t)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) m = fmaxf(m, acc[r]);
-        } else {
-#pragma unroll
-          for (int r = 0; r < 16; ++r)
-            if ((tmask >> acc_row(r, lane)) & 1u) m = fmaxf(m, acc[r]);
-        }
+          for (int r = 0; r < 16; ++r) m = fmaxf(m, acc[t][r]);
         const float mn = fmaxf(M[qb], m);
-        if (mn == -INFINITY) continue;   // nothing valid seen yet in this column
         const float mc = mn * c2;
         float sum = 0.f;
-        if (full) {
 #pragma unroll
-          for (int r = 0; r < 16; ++r) sum += exp2f(fmaf(acc[r], c2, -mc));
-        } else {
+        for (int t = 0; t < SCORE_KT; ++t)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) sum += fast_exp2(fmaf(acc[t][r], c2, -mc));
+        L[qb] = fmaf(L[qb], fast_exp2((M[qb] - mn) * c2), sum);
+        M[qb] = mn;
+      }
+    } else if (any) {
+      uint32_t rows[SCORE_KT];
+#pragma unroll
+      for (int t = 0; t < SCORE_KT; ++t) rows[t] = lane_rows(tm[t], lane);
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        f32x16 acc[SCORE_KT];
+        mma_chains<F, false, SCORE_KT>(kf, smem, qb, lane, acc);
+        float m = -INFINITY;
+#pragma unroll
+        for (int t = 0; t < SCORE_KT; ++t)
 #pragma unroll
           for (int r = 0; r < 16; ++r)
-            if ((tmask >> acc_row(r, lane)) & 1u) sum += exp2f(fmaf(acc[r], c2, -mc));
+            if ((rows[t] >> r) & 1u) m = fmaxf(m, acc[t][r]);
+        const float mn = fmaxf(M[qb], m);
+        if (mn != -INFINITY) {           // this column has seen a valid key
+          const float mc = mn * c2;
+          float sum = 0.f;
+#pragma unroll
+          for (int t = 0; t < SCORE_KT; ++t)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+              if ((rows[t] >> r) & 1u) sum += fast_exp2(fmaf(acc[t][r], c2, -mc));
+          L[qb] = fmaf(L[qb], fast_exp2((M[qb] - mn) * c2), sum);
+          M[qb] = mn;
         }
-        L[qb] = L[qb] * exp2f((M[qb] - mn) * c2) + sum;
-        M[qb] = mn;
       }
     }
   }
   // merge lane halves (same query column), then waves
 #pragma unroll
-  for (int qb = 0; qb < QB_MAX; ++qb) {
-    if (qb < QB) {
-      const float Mo = __shfl_xor(M[qb], 32, 64), Lo = __shfl_xor(L[qb], 32, 64);
-      const float mn = fmaxf(M[qb], Mo);
-      float Ln = 0.f;
-      if (mn != -INFINITY) Ln = L[qb] * exp2f((M[qb] - mn) * c2) + Lo * exp2f((Mo - mn) * c2);
-      if (lane < 32) red[wave * R_pad + qb * 32 + lane] = make_float2(mn, Ln);
-    }
+  for (int qb = 0; qb < QB; ++qb) {
+    const float Mo = __shfl_xor(M[qb], 32, 64), Lo = __shfl_xor(L[qb], 32, 64);
+    const float mn = fmaxf(M[qb], Mo);
+    float Ln = 0.f;
+    if (mn != -INFINITY) Ln = L[qb] * fast_exp2((M[qb] - mn) * c2) + Lo * fast_exp2((Mo - mn) * c2);
+    if (lane < 32) red[wave * R_pad + qb * 32 + lane] = make_float2(mn, Ln);
   }
   __syncthreads();
   for (int r = threadIdx.x; r < R; r += SCORE_NT) {
     float mn = -INFINITY;
-    for (int w = 0; w < SCORE_NT / 64; ++w) mn = fmaxf(mn, red[w * R_pad + r].x);
+    for (int w = 0; w < SCORE_NW; ++w) mn = fmaxf(mn, red[w * R_pad + r].x);
     float Ln = 0.f;
     if (mn != -INFINITY)
-      for (int w = 0; w < SCORE_NT / 64; ++w) {
+      for (int w = 0; w < SCORE_NW; ++w) {
         const float2 v = red[w * R_pad + r];
-        Ln += v.y * exp2f((v.x - mn) * c2);
+        Ln += v.y * fast_exp2((v.x - mn) * c2);
       }
     part[((size_t)h * n_chunks + chunk) * R_pad + r] = make_float2(mn, Ln);
   }
@@ -240,11 +446,11 @@ __global__ __launch_bounds__(SCORE_NT) void score_pass1_kernel(
 
 // merge chunk partials into natural-log row LSE, layout [W][NS][Hq]
 __global__ __launch_bounds__(256) void score_lse_merge_kernel(const float2* __restrict__ part,
-                                                               int n_chunks, int NS, int Hq,
-                                                               int Hkv, int W, float c2,
+                                                               int n_chunks, int R_pad, int NS,
+                                                               int Hq, int Hkv, int W, float c2,
                                                                float sm_scale, float* lse_out) {
   const int h = blockIdx.x, s = h / Hkv, kv = h % Hkv, G = Hq / Hkv;
-  const int R = G * W, R_pad = (R + 31) & ~31;
+  const int R = G * W;
   for (int r = threadIdx.x; r < R; r += blockDim.x) {
     const float2* p = part + (size_t)h * n_chunks * R_pad + r;
     float mn = -INFINITY;
@@ -261,21 +467,20 @@ __global__ __launch_bounds__(256) void score_lse_merge_kernel(const float2* __re
   }
 }
 
-constexpr int NREF_MAX = 256;
-
 // ------------------------------------------------------------------ pass 2
-template <typename T, int D, bool RED>
-__global__ __launch_bounds__(SCORE_NT) void score_pass2_kernel(
+template <typename T, int D, int QB, bool RED>
+__global__ HK_SCORE_ATTR void score_pass2_kernel(
     const T* __restrict__ q_obs, const T* __restrict__ k_pool, const int32_t* __restrict__ table,
     const uint16_t* __restrict__ masks, const int32_t* __restrict__ n_pages_arr, int NS, int Hq,
-    int Hkv, int W, int max_pages, int ppw, int L_dense, float c2, float lnR,
+    int Hkv, int W, int max_pages, int L_dense, float c2, float lnR,
     const float* __restrict__ row_lse, float* __restrict__ s_out, int32_t* __restrict__ cand_len_out,
     const int32_t* __restrict__ ref_slots, int n_ref, float* __restrict__ x_red) {
   using F = Frag<T, D>;
+  constexpr int R_pad = 32 * QB;
   extern __shared__ __align__(16) char smem[];
   const int h = blockIdx.y, chunk = blockIdx.x;
   const int s = h / Hkv, kv = h % Hkv, G = Hq / Hkv;
-  const int R = G * W, R_pad = (R + 31) & ~31, QB = R_pad >> 5;
+  const int R = G * W;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const size_t S_max = (size_t)max_pages * HK_PAGE;
   const int n = n_pages_arr[h];
@@ -284,7 +489,7 @@ __global__ __launch_bounds__(SCORE_NT) void score_pass2_kernel(
 
   const int32_t* trow = table + (size_t)h * max_pages;
   const uint16_t* mrow = masks + (size_t)h * max_pages;
-  const int p_begin = chunk * ppw, p_end_all = min(p_begin + ppw, max_pages);
+  const int p_begin = chunk * SCORE_PPW, p_end_all = min(p_begin + SCORE_PPW, max_pages);
   const int p_cand_end = min(p_end_all, cand_len / HK_PAGE);
 
   // slots of this chunk that hold no candidate: -inf
@@ -314,12 +519,14 @@ __global__ __launch_bounds__(SCORE_NT) void score_pass2_kernel(
   char* ref_lds = after_q + (size_t)R_pad * sizeof(float);
   float* rn_ref = nullptr;
   int32_t* ref_slot = nullptr;
+  uint32_t* ref_bits = nullptr;
   int RB = 0;
   if constexpr (RED) {
     const int nr_pad = (n_ref + 31) & ~31;
     RB = nr_pad >> 5;
     rn_ref = reinterpret_cast<float*>(ref_lds + (size_t)NREF_MAX * D * sizeof(T));
     ref_slot = reinterpret_cast<int32_t*>(rn_ref + NREF_MAX);
+    ref_bits = reinterpret_cast<uint32_t*>(ref_slot + NREF_MAX);   // [SCORE_PPW / 2] words
     const int32_t* rs = ref_slots + (size_t)h * n_ref;
     auto ref_row = [&](int i) -> const T* {
       const int j = rs[i];
@@ -328,6 +535,7 @@ __global__ __launch_bounds__(SCORE_NT) void score_pass2_kernel(
       return k_pool + ((size_t)trow[pp] * HK_PAGE + (j & 15)) * D;
     };
     stage_rows<T, D>(ref_lds, n_ref, nr_pad, ref_row);
+    for (int i = threadIdx.x; i < SCORE_PPW / 2; i += SCORE_NT) ref_bits[i] = 0u;
     __syncthreads();
     for (int i = threadIdx.x; i < nr_pad; i += SCORE_NT) {
       // squared norm of reference row i, read back from its fragment-major LDS image
@@ -353,152 +561,187 @@ __global__ __launch_bounds__(SCORE_NT) void score_pass2_kernel(
           }
         }
       }
-      rn_ref[i] = ss > 0.f ? 1.0f / sqrtf(ss) : 0.f;
-      ref_slot[i] = (i < n_ref) ? rs[i] : -1;
+      // padding rows (i >= n_ref) carry NaN, which fmaxf ignores; a zero-norm
+      // reference has cosine 0 with every key
+      rn_ref[i] = (i >= n_ref) ? __builtin_nanf("") : (ss > 0.f ? 1.0f / sqrtf(ss) : 0.f);
+      const int slot = (i < n_ref) ? rs[i] : -1;
+      ref_slot[i] = slot;
+      const int rel = slot - p_begin * HK_PAGE;    // reference slots inside this chunk
+      if (i < n_ref && rel >= 0 && rel < SCORE_PPW * HK_PAGE)
+        atomicOr(&ref_bits[rel >> 5], 1u << (rel & 31));
     }
   }
   __syncthreads();
 
-  for (int p0 = p_begin + 2 * wave; p0 < p_cand_end; p0 += 2 * (SCORE_NT / 64)) {
-    const int p1 = p0 + 1;
-    const uint32_t m0 = mrow[p0], m1 = (p1 < p_cand_end) ? mrow[p1] : 0u;
-    const int kl = lane & 31, pg = p0 + (kl >> 4);
-    const int slot = pg * HK_PAGE + (kl & 15);
-    const bool cand = (pg < p_cand_end) && (((kl < 16 ? m0 : m1) >> (kl & 15)) & 1u);
-    if ((m0 | m1) == 0) {
-      if (lane < 32 && pg < p_cand_end) {
-        s_out[(size_t)h * S_max + slot] = -INFINITY;
-        if (RED) x_red[(size_t)h * S_max + slot] = -INFINITY;
-      }
-      continue;
-    }
-    F kf;
-    if (pg < p_cand_end) {
-      const int phys = trow[pg];
-      kf.load(k_pool + ((size_t)phys * HK_PAGE + (kl & 15)) * D + (lane >> 5) * (D / 2));
-    } else {
-      kf.zero();
-    }
-    float col = 0.f;
+  for (int p0 = p_begin + SCORE_WPP * wave; p0 < p_cand_end; p0 += SCORE_WPP * SCORE_NW) {
+    F kf[SCORE_KT];
+    uint32_t m0[SCORE_KT], m1[SCORE_KT];
+    bool any = false;
 #pragma unroll
-    for (int qb = 0; qb < QB_MAX; ++qb) {
-      if (qb < QB) {
-        f32x16 acc = {};
+    for (int t = 0; t < SCORE_KT; ++t) {
+      const int pa = p0 + 2 * t, pb = pa + 1;
+      load_tile<T, D>(kf[t], k_pool, trow, pa, p_cand_end, lane);
+      m0[t] = (pa < p_cand_end) ? (uint32_t)mrow[pa] : 0u;
+      m1[t] = (pb < p_cand_end) ? (uint32_t)mrow[pb] : 0u;
+      any = any || ((m0[t] | m1[t]) != 0u);
+    }
+    const int kl = lane & 31;
+    float col[SCORE_KT];
 #pragma unroll
-        for (int kk = 0; kk < F::KSTEPS; ++kk) acc = F::mma(F::lds(smem, qb, kk, lane), kf.v[kk], acc);
+    for (int t = 0; t < SCORE_KT; ++t) col[t] = 0.f;
+    if (any && SCORE_KT == 1) {
+      col[0] = p2_tile_pipelined<F, QB>(kf[0], smem, lse2, c2, lane);
+    } else if (any) {
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        f32x16 acc[SCORE_KT];
+        mma_chains<F, true, SCORE_KT>(kf, smem, qb, lane, acc);
 #pragma unroll
         for (int r4 = 0; r4 < 4; ++r4) {
           const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse2 + qb * 32 + 8 * r4 + 4 * (lane >> 5));
 #pragma unroll
-          for (int i = 0; i < 4; ++i) col += exp2f(fmaf(acc[4 * r4 + i], c2, -l4[i]));
+          for (int t = 0; t < SCORE_KT; ++t)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) col[t] += fast_exp2(fmaf(acc[t][4 * r4 + i], c2, -l4[i]));
         }
       }
     }
-    col += __shfl_xor(col, 32, 64);
-    if constexpr (RED) {
-      const float ss = kf.sumsq();
-      const float nrm2 = ss + __shfl_xor(ss, 32, 64);
-      const float rn = nrm2 > 0.f ? 1.0f / sqrtf(nrm2) : 0.f;
-      float cmax = -INFINITY;
-      int self = 0;
-      for (int rb = 0; rb < RB; ++rb) {
-        f32x16 acc = {};
 #pragma unroll
-        for (int kk = 0; kk < F::KSTEPS; ++kk) acc = F::mma(F::lds(ref_lds, rb, kk, lane), kf.v[kk], acc);
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int i = rb * 32 + acc_row(r, lane);
-          if (i < n_ref) {
-            if (ref_slot[i] == slot) self = 1;
-            else cmax = fmaxf(cmax, acc[r] * rn_ref[i]);
-          }
-        }
-      }
-      cmax = fmaxf(cmax, __shfl_xor(cmax, 32, 64));
-      self |= __shfl_xor(self, 32, 64);
-      if (lane < 32 && pg < p_cand_end) {
+    for (int t = 0; t < SCORE_KT; ++t) {
+      const int pg = p0 + 2 * t + (kl >> 4);
+      const int slot = pg * HK_PAGE + (kl & 15);
+      const bool cand = (pg < p_cand_end) && (((kl < 16 ? m0[t] : m1[t]) >> (kl & 15)) & 1u);
+      const bool write = (lane < 32) && (pg < p_cand_end);
+      const float c_all = col[t] + __shfl_xor(col[t], 32, 64);
+      if constexpr (RED) {
         float x = -INFINITY;
-        if (cand) x = (n_ref - self > 0) ? -(cmax * rn) : 1.0f;
-        x_red[(size_t)h * S_max + slot] = x;
+        if ((m0[t] | m1[t]) != 0u) {
+          const float ss = kf[t].sumsq();
+          const float nrm2 = ss + __shfl_xor(ss, 32, 64);
+          const float rn = nrm2 > 0.f ? 1.0f / sqrtf(nrm2) : 0.f;
+          const uint32_t self_word = ref_bits[(p0 + 2 * t - p_begin) >> 1];
+          float cmax = -INFINITY;
+          int self = 0;
+          for (int rb = 0; rb < RB; ++rb) {
+            f32x16 ra[1];
+            mma_chains<F, true, 1>(&kf[t], ref_lds, rb, lane, ra);
+#pragma unroll
+            for (int r4 = 0; r4 < 4; ++r4) {
+              const int i0 = rb * 32 + 8 * r4 + 4 * (lane >> 5);
+              const f32x4 rn4 = *reinterpret_cast<const f32x4*>(rn_ref + i0);
+              if (self_word == 0u) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) cmax = fmaxf(cmax, ra[0][4 * r4 + i] * rn4[i]);
+              } else {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                  if (ref_slot[i0 + i] == slot) self = 1;
+                  else cmax = fmaxf(cmax, ra[0][4 * r4 + i] * rn4[i]);
+                }
+              }
+            }
+          }
+          cmax = fmaxf(cmax, __shfl_xor(cmax, 32, 64));
+          self |= __shfl_xor(self, 32, 64);
+          if (cand) x = (n_ref - self > 0) ? -(cmax * rn) : 1.0f;
+        }
+        if (write) x_red[(size_t)h * S_max + slot] = x;
       }
+      if (write) s_out[(size_t)h * S_max + slot] = cand ? fmaf(fast_log2(c_all), kLn2, -lnR) : -INFINITY;
     }
-    if (lane < 32 && pg < p_cand_end)
-      s_out[(size_t)h * S_max + slot] = cand ? fmaf(__log2f(col), kLn2, -lnR) : -INFINITY;
   }
 }
 
 template <typename K>
 static void allow_lds(K kernel, size_t bytes) {
-  if (bytes > 65536) hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+  if (bytes > 65536)
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
 }
 
-template <typename T, int D>
-hipError_t launch_score_t(const hk_score_args& a, hipStream_t st) {
+static size_t pass1_lds(int R_pad, int D, int es) {
+  return (size_t)R_pad * D * es + (size_t)SCORE_NW * R_pad * sizeof(float2);
+}
+static size_t pass2_lds(int R_pad, int D, int es, bool red) {
+  size_t b = (size_t)R_pad * D * es + (size_t)R_pad * sizeof(float);
+  if (red) b += (size_t)NREF_MAX * D * es + (size_t)NREF_MAX * 8 + (SCORE_PPW / 2) * 4;
+  return b;
+}
+
+template <typename T, int D, int QB>
+hipError_t launch_score_q(const hk_score_args& a, hipStream_t st) {
   const hk_paged_kv* kv = a.kv;
-  const int G = a.Hq / a.Hkv, R = G * a.W, R_pad = (R + 31) & ~31;
+  constexpr int R_pad = 32 * QB;
   const int n_heads = a.NS * a.Hkv;
-  const int ppw = 64;
-  const int n_chunks = (kv->max_pages + ppw - 1) / ppw;
+  const int n_chunks = (kv->max_pages + SCORE_PPW - 1) / SCORE_PPW;
   const float c2 = a.sm_scale * kLog2e;
   char* ws = static_cast<char*>(a.ws);
   float2* part = reinterpret_cast<float2*>(ws);
   float* lse_buf = a.row_lse_out;
-  size_t off = ((size_t)n_heads * n_chunks * R_pad * sizeof(float2) + 255) & ~(size_t)255;
+  const size_t off = ((size_t)n_heads * n_chunks * R_pad * sizeof(float2) + 255) & ~(size_t)255;
   if (!lse_buf) lse_buf = reinterpret_cast<float*>(ws + off);
   const float* lse_use = a.row_lse_in;
   dim3 grid(n_chunks, n_heads);
   if (!lse_use) {
-    const size_t lds1 = (size_t)R_pad * D * sizeof(T) + (size_t)(SCORE_NT / 64) * R_pad * sizeof(float2);
-    allow_lds(score_pass1_kernel<T, D>, lds1);
-    hipLaunchKernelGGL((score_pass1_kernel<T, D>), grid, dim3(SCORE_NT), lds1, st,
+    const size_t lds1 = pass1_lds(R_pad, D, sizeof(T));
+    allow_lds(score_pass1_kernel<T, D, QB>, lds1);
+    hipLaunchKernelGGL((score_pass1_kernel<T, D, QB>), grid, dim3(SCORE_NT), lds1, st,
                        static_cast<const T*>(a.q_obs), static_cast<const T*>(kv->k_pool),
                        kv->page_table, kv->page_mask, kv->n_pages, a.NS, a.Hq, a.Hkv, a.W,
-                       kv->max_pages, ppw, c2, part, n_chunks);
+                       kv->max_pages, c2, part, n_chunks);
     hipLaunchKernelGGL(score_lse_merge_kernel, dim3(n_heads), dim3(256), 0, st, part, n_chunks,
-                       a.NS, a.Hq, a.Hkv, a.W, c2, a.sm_scale, lse_buf);
+                       R_pad, a.NS, a.Hq, a.Hkv, a.W, c2, a.sm_scale, lse_buf);
     lse_use = lse_buf;
   } else if (a.row_lse_out && a.row_lse_out != a.row_lse_in) {
-    hipMemcpyAsync(a.row_lse_out, a.row_lse_in, sizeof(float) * (size_t)a.W * a.NS * a.Hq,
-                   hipMemcpyDeviceToDevice, st);
+    (void)hipMemcpyAsync(a.row_lse_out, a.row_lse_in, sizeof(float) * (size_t)a.W * a.NS * a.Hq,
+                         hipMemcpyDeviceToDevice, st);
   }
-  const float lnR = logf((float)R);
-  size_t lds2 = (size_t)R_pad * D * sizeof(T) + (size_t)R_pad * sizeof(float);
+  const float lnR = logf((float)(a.Hq / a.Hkv * a.W));
+  const size_t lds2 = pass2_lds(R_pad, D, sizeof(T), a.x_red != nullptr);
   if (a.x_red) {
-    lds2 += (size_t)NREF_MAX * D * sizeof(T) + (size_t)NREF_MAX * (sizeof(float) + sizeof(int32_t));
-    allow_lds(score_pass2_kernel<T, D, true>, lds2);
-    hipLaunchKernelGGL((score_pass2_kernel<T, D, true>), grid, dim3(SCORE_NT), lds2, st,
+    allow_lds(score_pass2_kernel<T, D, QB, true>, lds2);
+    hipLaunchKernelGGL((score_pass2_kernel<T, D, QB, true>), grid, dim3(SCORE_NT), lds2, st,
                        static_cast<const T*>(a.q_obs), static_cast<const T*>(kv->k_pool),
                        kv->page_table, kv->page_mask, kv->n_pages, a.NS, a.Hq, a.Hkv, a.W,
-                       kv->max_pages, ppw, a.L_dense, c2, lnR, lse_use, a.s_attn, a.cand_len,
+                       kv->max_pages, a.L_dense, c2, lnR, lse_use, a.s_attn, a.cand_len,
                        a.ref_slots, a.n_ref, a.x_red);
   } else {
-    allow_lds(score_pass2_kernel<T, D, false>, lds2);
-    hipLaunchKernelGGL((score_pass2_kernel<T, D, false>), grid, dim3(SCORE_NT), lds2, st,
+    allow_lds(score_pass2_kernel<T, D, QB, false>, lds2);
+    hipLaunchKernelGGL((score_pass2_kernel<T, D, QB, false>), grid, dim3(SCORE_NT), lds2, st,
                        static_cast<const T*>(a.q_obs), static_cast<const T*>(kv->k_pool),
                        kv->page_table, kv->page_mask, kv->n_pages, a.NS, a.Hq, a.Hkv, a.W,
-                       kv->max_pages, ppw, a.L_dense, c2, lnR, lse_use, a.s_attn, a.cand_len,
+                       kv->max_pages, a.L_dense, c2, lnR, lse_use, a.s_attn, a.cand_len,
                        nullptr, 0, nullptr);
   }
   return hipGetLastError();
+}
+
+template <typename T, int D>
+hipError_t launch_score_t(const hk_score_args& a, hipStream_t st) {
+  switch (qb_eff((a.Hq / a.Hkv * a.W + 31) / 32)) {
+    case 1: return launch_score_q<T, D, 1>(a, st);
+    case 2: return launch_score_q<T, D, 2>(a, st);
+    case 4: return launch_score_q<T, D, 4>(a, st);
+    case 7: return launch_score_q<T, D, 7>(a, st);
+    default: return launch_score_q<T, D, 8>(a, st);
+  }
 }
 
 }  // namespace hk
 
 size_t hk_score_ws(int NS, int Hq, int Hkv, int D, int W, int max_pages) {
   (void)D;
-  const int G = Hq / Hkv, R_pad = (G * W + 31) & ~31;
-  const int n_chunks = (max_pages + 63) / 64;
+  const int R_pad = hk::score_rpad(Hq / Hkv * W);
+  const int n_chunks = (max_pages + hk::SCORE_PPW - 1) / hk::SCORE_PPW;
   const size_t part = ((size_t)NS * Hkv * n_chunks * R_pad * sizeof(float2) + 255) & ~(size_t)255;
   const size_t lse = ((size_t)W * NS * Hq * sizeof(float) + 255) & ~(size_t)255;
   return part + lse;
 }
 
 size_t hk_score_lds_bytes(int R, int D, int esize, bool redundancy) {
-  const size_t R_pad = (size_t)((R + 31) & ~31);
-  const size_t p1 = R_pad * D * esize + (size_t)(hk::SCORE_NT / 64) * R_pad * 8;
-  size_t p2 = R_pad * D * esize + R_pad * 4;
-  if (redundancy) p2 += (size_t)hk::NREF_MAX * D * esize + (size_t)hk::NREF_MAX * 8;
+  const int R_pad = hk::score_rpad(R);
+  const size_t p1 = hk::pass1_lds(R_pad, D, esize);
+  const size_t p2 = hk::pass2_lds(R_pad, D, esize, redundancy);
   return p1 > p2 ? p1 : p2;
 }
 

@@ -48,7 +48,9 @@ def test_status_strings(hk):
 
 def test_workspace_sizes(hk):
     d = hk.dims(32, 28, 4, 128, 32)
-    assert hk.hk_workspace_size(hk.OP_SCORE, d, 2048) >= 128 * 32 * 224 * 8
+    # row-LSE partials: at least one (max, sum) pair per window row and head, plus the LSEs
+    assert hk.hk_workspace_size(hk.OP_SCORE, d, 2048) >= 128 * 224 * 8 + 32 * 32 * 28 * 4
+    assert hk.hk_workspace_size(hk.OP_SCORE, d, 4096) > hk.hk_workspace_size(hk.OP_SCORE, d, 2048)
     assert hk.hk_workspace_size(hk.OP_COMPACT, d, 2048) >= 2 * 128 * 2048 * 4
     assert hk.hk_workspace_size(hk.OP_DECODE, d, 2048) > 0
     assert hk.hk_workspace_size(99, d, 2048) == 0

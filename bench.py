@@ -259,19 +259,83 @@ def cpu_baseline(w, cfg, comp, args):
 
 
 def run_decode(args):
-    from decode_loop import run
-    return run(args)
+    """Config 5: end-to-end decode loop.  One timed "step" = one segment of
+    `compress_every` decode steps (append + per-layer paged decode attention) followed by
+    one compression of every layer; the segment's random q/k/v are drawn into HBM before
+    its timed region starts."""
+    import paper_2606_28831_amd as hk
+    import workload as WL
+    from paper_2606_28831_amd.pipeline import DecodeLoop
+
+    cfg = WL.config(5)
+    L, B, Hq, Hkv, D, W = (cfg[k] for k in ("L", "B", "Hq", "Hkv", "D", "W"))
+    T = cfg["compress_every"]
+    n_seg = args.steps if args.steps_given else cfg["decode_steps"] // T
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    max_pages = (cfg["N"] + cfg["decode_steps"]) // 16
+    H = L * B * Hkv
+    t_gen = time.perf_counter()
+    w = WL.make_workload(cfg, dev, max_pages=max_pages, pool_pages=H * max_pages + H * 256)
+    torch.cuda.synchronize()
+    t_gen = time.perf_counter() - t_gen
+    kv = hk.PagedKV(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)
+    alloc = hk.Allocator(w.free_ids, w.free_top)
+    loop = DecodeLoop(L, B, Hq, Hkv, D, W, kv, alloc, cfg["p"], cfg["L_dense"])
+    NS = L * B
+    dt = WL.TORCH_DTYPE[cfg["dtype"]]
+    seg_ms, seg_tokens_kv, kept = [], [], []
+    for seg in range(n_seg):
+        g = torch.Generator(device=dev).manual_seed(cfg["seed"] * 7919 + seg + 1)
+        q_seg = torch.randn(T, NS, Hq, D, generator=g, device=dev).to(dt)
+        k_seg = torch.randn(T, NS, Hkv, D, generator=g, device=dev).to(dt)
+        v_seg = torch.randn(T, NS, Hkv, D, generator=g, device=dev).to(dt)
+        lse_seg = torch.empty(T, NS, Hq, device=dev)
+        m = w.page_mask.to(torch.int32) & 0xFFFF
+        valid = int(sum(bin(i).count("1") * c for i, c in zip(*torch.unique(m, return_counts=True))))
+        seg_tokens_kv.append(valid)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for t in range(T):
+            loop.step(q_seg[t], k_seg[t], v_seg[t], lse_seg[t])
+        loop.compress(q_seg[T - W:], lse_seg[T - W:])
+        e1.record()
+        torch.cuda.synchronize()
+        seg_ms.append(e0.elapsed_time(e1))
+        kept.append(float(loop.comp.buf.k.float().mean()))
+        del q_seg, k_seg, v_seg, lse_seg
+    status = int(loop.status.item()) | int(loop.comp.buf.status.item())
+    total_s = sum(seg_ms) / 1e3
+    tokens = B * T * n_seg
+    # decode attention bytes: every valid K and V row read once per step per layer
+    dec_bytes = sum(v * 2 * D * 2 * T for v in seg_tokens_kv)
+    return {
+        "metric": METRIC, "value": tokens / total_s, "unit": "decode tokens/s",
+        "n_gpus": 1, "steps": n_seg, "warmup": 0, "ms_per_step": sum(seg_ms) / n_seg,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": cfg["dtype"],
+        "data": "synthetic",
+        "config": {"workload": cfg["name"], "layers": L, "batch": B, "q_heads": Hq, "kv_heads": Hkv,
+                   "head_dim": D, "prompt": cfg["N"], "decode_steps": T * n_seg,
+                   "compress_every": T, "window": W, "top_p": cfg["p"], "L_dense": cfg["L_dense"]},
+        "decode_attn_hbm_frac_lower_bound": dec_bytes / total_s / 1e9 / HBM_PEAK_GBS,
+        "segment_ms": seg_ms, "valid_kv_slots_per_segment": seg_tokens_kv, "mean_kept_per_head": kept,
+        "status_flags": status, "gen_s": t_gen,
+    }
 
 
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=None)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     args = ap.parse_args()
+    args.steps_given = args.steps is not None
+    if args.steps is None:
+        args.steps = 20
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the compression step is independent per (sequence, KV "
               "head) and is benchmarked on a single MI355X; --gpus above 1 is not supported.",

@@ -127,3 +127,42 @@ class Decoder:
 
     def attend(self, q, o, lse, stream=None):
         hk_decode_attn(self.d, q, self.kv, self.sm_scale, o, lse, self.ws, stream=stream)
+
+
+class DecodeLoop:
+    """End-to-end decode loop over L independent attention layers sharing one page pool
+    and one allocator (config-5 style).
+
+    step():     append this step's K/V for every layer (Step 1, dense tier), then one paged
+                decode-attention launch per layer, writing o and the row LSE.
+    compress(): Steps 2-3 over every layer at once, with the window queries and the decode
+                step's own LSEs (single-pass score).
+    Heads are ordered (layer, sequence, KV head); sequence index = layer * B + b.
+    """
+
+    def __init__(self, L, B, Hq, Hkv, D, W, kv: PagedKV, alloc: Allocator, p: float,
+                 L_dense: int, L_sparse: int = 0):
+        self.L, self.B, self.Hq, self.Hkv, self.D, self.W = L, B, Hq, Hkv, D, W
+        self.kv, self.alloc = kv, alloc
+        self.NS = L * B
+        dev = kv.k_pool.device
+        self.d_all = dims(self.NS, Hq, Hkv, D, W)
+        self.d_layer = dims(B, Hq, Hkv, D, W)
+        self.layers = [kv.rows(l * B * Hkv, B * Hkv) for l in range(L)]
+        self.sm_scale = 1.0 / math.sqrt(D)
+        self.ws_dec = workspace(OP_DECODE, self.d_layer, kv.max_pages, dev)
+        self.status = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.o = torch.empty(self.NS, Hq, D, dtype=torch.float32, device=dev)
+        self.comp = Compressor(self.NS, Hq, Hkv, D, W, kv, alloc, p, L_dense=L_dense,
+                               L_sparse=L_sparse, metric="attn")
+
+    def step(self, q_t, k_t, v_t, lse_t, stream=None):
+        hk_append_kv(self.d_all, self.kv, k_t, v_t, self.alloc, self.status, stream=stream)
+        B = self.B
+        for l, kv_l in enumerate(self.layers):
+            hk_decode_attn(self.d_layer, q_t[l * B:(l + 1) * B], kv_l, self.sm_scale,
+                           self.o[l * B:(l + 1) * B], lse_t[l * B:(l + 1) * B], self.ws_dec,
+                           stream=stream)
+
+    def compress(self, q_win, lse_win, stream=None):
+        self.comp.step(q_win, row_lse_in=lse_win, stream=stream)

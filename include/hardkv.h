@@ -229,6 +229,8 @@ hk_status hk_decode_attn(const hk_dims* dims, const void* q, const hk_paged_kv* 
  * row is empty).  k_new, v_new [NS][Hkv][D] in kv->dtype.  Pops happen in head order.
  * If the free list is too short or a row is full (n_pages == max_pages) the step is
  * skipped for every head and HK_FLAG_NOSPACE is raised.
+ * workspace: device, 256-B aligned, >= hk_workspace_size(HK_OP_APPEND) bytes (a few int32
+ * per 64 heads), caller-owned, overwritten by the call.
  */
 hk_status hk_append_kv(const hk_dims* dims, const hk_paged_kv* kv, const void* k_new,
                        const void* v_new, const hk_allocator* alloc, int32_t* status,

@@ -205,7 +205,7 @@ def hk_decode_attn(d: hk_dims, q, kv: PagedKV, sm_scale: float, o, lse, ws, stre
                                 _ptr(lse), _ptr(ws), ws.numel(), _stream(stream)), "hk_decode_attn")
 
 
-def hk_append_kv(d: hk_dims, kv: PagedKV, k_new, v_new, alloc: Allocator, status, ws=None,
+def hk_append_kv(d: hk_dims, kv: PagedKV, k_new, v_new, alloc: Allocator, status, ws,
                  stream=None):
     _check(lib().hk_append_kv(C.byref(d), C.byref(kv.desc), _ptr(k_new), _ptr(v_new),
                               C.byref(alloc.desc), _ptr(status), _ptr(ws),

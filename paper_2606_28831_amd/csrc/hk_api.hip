@@ -203,12 +203,13 @@ hk_status hk_decode_attn(const hk_dims* dims, const void* q, const hk_paged_kv* 
 hk_status hk_append_kv(const hk_dims* dims, const hk_paged_kv* kv, const void* k_new,
                        const void* v_new, const hk_allocator* alloc, int32_t* status,
                        void* workspace, size_t ws_bytes, hipStream_t stream) {
-  (void)ws_bytes;
   hk_status e = check_dims(dims, false);
   if (e) return e;
   if ((e = check_kv(kv, true))) return e;
   if (!k_new || !v_new || !alloc || !alloc->free_ids || !alloc->free_top) return HK_ERR_ARG;
   if (!aligned16(k_new) || !aligned16(v_new)) return HK_ERR_ALIGN;
+  if (!workspace || ws_bytes < hk_append_ws(dims->NS, dims->Hkv)) return HK_ERR_WORKSPACE;
+  if (!aligned256(workspace)) return HK_ERR_ALIGN;
   return launched(hk_launch_append(dims->NS, dims->Hkv, dims->D, kv, k_new, v_new, alloc, status,
                                    workspace, stream));
 }

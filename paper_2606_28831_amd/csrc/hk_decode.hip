@@ -18,14 +18,22 @@
 
 namespace hk {
 
+#ifndef HK_DEC_PPS
+#define HK_DEC_PPS 64         // pages per split (one workgroup)
+#endif
+#ifndef HK_DEC_PREFETCH
+#define HK_DEC_PREFETCH 0     // 1: load the wave's next page while computing the current one
+#endif
+
 constexpr int DEC_NT = 256;
 constexpr int DEC_NW = DEC_NT / 64;
+constexpr int DEC_PPS = HK_DEC_PPS;
 
 template <typename T, int D, int G>
 __global__ __launch_bounds__(DEC_NT) void decode_split_kernel(
     const T* __restrict__ q, const T* __restrict__ k_pool, const T* __restrict__ v_pool,
     const int32_t* __restrict__ table, const uint16_t* __restrict__ masks,
-    const int32_t* __restrict__ n_pages_arr, int Hq, int Hkv, int max_pages, int pps, float c2,
+    const int32_t* __restrict__ n_pages_arr, int Hq, int Hkv, int max_pages, float c2,
     float* __restrict__ part, int n_split) {
   constexpr int ES = sizeof(T);
   constexpr int DQ = D / 4;                 // dims per quarter
@@ -41,7 +49,7 @@ __global__ __launch_bounds__(DEC_NT) void decode_split_kernel(
   const int s = h / Hkv, kv = h % Hkv;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n = n_pages_arr[h];
-  const int p_begin = split * pps, p_end = min(p_begin + pps, n);
+  const int p_begin = split * DEC_PPS, p_end = min(p_begin + DEC_PPS, n);
   const int t = lane >> 2, c = lane & 3;
   const int kg = lane / LPR, dc = lane % LPR;
 
@@ -69,27 +77,32 @@ __global__ __launch_bounds__(DEC_NT) void decode_split_kernel(
   const int32_t* trow = table + (size_t)h * max_pages;
   const uint16_t* mrow = masks + (size_t)h * max_pages;
 
-  for (int p = p_begin + wave; p < p_end; p += DEC_NW) {
-    const uint32_t m16 = mrow[p];
-    if (m16 == 0u) continue;
+  struct PageRegs {
+    uint4 k[QW / 4];
+    uint4 v[KPL];
+    uint32_t m16;
+  };
+  auto load_page = [&](PageRegs& r, int p) {
+    r.m16 = mrow[p];
     const size_t page = (size_t)trow[p] * HK_PAGE;
-    uint32_t kw[QW];
-    {
-      const uint4* src = reinterpret_cast<const uint4*>(k_pool + (page + t) * D + c * DQ);
+    const uint4* ks = reinterpret_cast<const uint4*>(k_pool + (page + t) * D + c * DQ);
 #pragma unroll
-      for (int i = 0; i < QW / 4; ++i) {
-        const uint4 u = src[i];
-        kw[4 * i + 0] = u.x;
-        kw[4 * i + 1] = u.y;
-        kw[4 * i + 2] = u.z;
-        kw[4 * i + 3] = u.w;
-      }
-    }
-    uint4 vw[KPL];
+    for (int i = 0; i < QW / 4; ++i) r.k[i] = ks[i];
 #pragma unroll
     for (int i = 0; i < KPL; ++i)
-      vw[i] = *reinterpret_cast<const uint4*>(v_pool + (page + kg * KPL + i) * D + dc * VEC);
-
+      r.v[i] = *reinterpret_cast<const uint4*>(v_pool + (page + kg * KPL + i) * D + dc * VEC);
+  };
+  auto process_page = [&](const PageRegs& r) {
+    const uint32_t m16 = r.m16;
+    if (m16 == 0u) return;
+    uint32_t kw[QW];
+#pragma unroll
+    for (int i = 0; i < QW / 4; ++i) {
+      kw[4 * i + 0] = r.k[i].x;
+      kw[4 * i + 1] = r.k[i].y;
+      kw[4 * i + 2] = r.k[i].z;
+      kw[4 * i + 3] = r.k[i].w;
+    }
     const bool valid = (m16 >> t) & 1u;
     float zl[G];
 #pragma unroll
@@ -131,7 +144,7 @@ __global__ __launch_bounds__(DEC_NT) void decode_split_kernel(
     for (int i = 0; i < KPL; ++i) {
       const int src_lane = 4 * (kg * KPL + i);
       float vf[VEC];
-      const uint32_t vv[4] = {vw[i].x, vw[i].y, vw[i].z, vw[i].w};
+      const uint32_t vv[4] = {r.v[i].x, r.v[i].y, r.v[i].z, r.v[i].w};
       if constexpr (ES == 2) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -148,6 +161,29 @@ __global__ __launch_bounds__(DEC_NT) void decode_split_kernel(
 #pragma unroll
         for (int e = 0; e < VEC; ++e) o[g][e] = fmaf(pg, vf[e], o[g][e]);
       }
+    }
+  };
+
+  int p = p_begin + wave;
+  if constexpr (HK_DEC_PREFETCH) {
+    PageRegs ra, rb;
+    if (p < p_end) load_page(ra, p);
+    while (p < p_end) {
+      int pn = p + DEC_NW;
+      if (pn < p_end) load_page(rb, pn);
+      process_page(ra);
+      p = pn;
+      if (p >= p_end) break;
+      pn = p + DEC_NW;
+      if (pn < p_end) load_page(ra, pn);
+      process_page(rb);
+      p = pn;
+    }
+  } else {
+    for (; p < p_end; p += DEC_NW) {
+      PageRegs r;
+      load_page(r, p);
+      process_page(r);
     }
   }
   // reduce over slot groups (lanes with the same value chunk) and over all lanes for l
@@ -190,126 +226,180 @@ __global__ __launch_bounds__(DEC_NT) void decode_split_kernel(
   }
 }
 
+// one workgroup per KV head merges the split states of all its G query heads (App. F)
 template <int D>
-__global__ __launch_bounds__(D) void decode_merge_kernel(const float* __restrict__ part, int n_split,
-                                                         int G, int Hq, int Hkv, float* __restrict__ o,
-                                                         float* __restrict__ lse) {
-  const int hg = blockIdx.x, h = hg / G, g = hg % G;
-  const int s = h / Hkv, kv = h % Hkv;
-  const float* p = part + ((size_t)h * n_split * G + g) * (D + 2);
-  const size_t stride = (size_t)G * (D + 2);
-  float M = -INFINITY;
-  for (int i = 0; i < n_split; ++i) M = fmaxf(M, p[i * stride + D]);
-  float L = 0.f, O = 0.f;
-  if (M != -INFINITY)
-    for (int i = 0; i < n_split; ++i) {
-      const float a = exp2f(p[i * stride + D] - M);
-      L += p[i * stride + D + 1] * a;
-      O += p[i * stride + threadIdx.x] * a;
-    }
-  const size_t row = (size_t)s * Hq + kv * G + g;
-  o[row * D + threadIdx.x] = (L > 0.f) ? O / L : 0.f;
-  if (threadIdx.x == 0) lse[row] = (L > 0.f) ? (M + __log2f(L)) * kLn2 : -INFINITY;
+__global__ __launch_bounds__(256) void decode_merge_kernel(const float* __restrict__ part, int n_split,
+                                                           int G, int Hq, int Hkv, float* __restrict__ o,
+                                                           float* __restrict__ lse) {
+  const int h = blockIdx.x, s = h / Hkv, kv = h % Hkv;
+  for (int idx = threadIdx.x; idx < G * D; idx += blockDim.x) {
+    const int g = idx / D, d = idx % D;
+    const float* p = part + ((size_t)h * n_split * G + g) * (D + 2);
+    const size_t stride = (size_t)G * (D + 2);
+    float M = -INFINITY;
+    for (int i = 0; i < n_split; ++i) M = fmaxf(M, p[i * stride + D]);
+    float L = 0.f, O = 0.f;
+    if (M != -INFINITY)
+      for (int i = 0; i < n_split; ++i) {
+        const float a = exp2f(p[i * stride + D] - M);
+        L += p[i * stride + D + 1] * a;
+        O += p[i * stride + d] * a;
+      }
+    const size_t row = (size_t)s * Hq + kv * G + g;
+    o[row * D + d] = (L > 0.f) ? O / L : 0.f;
+    if (d == 0) lse[row] = (L > 0.f) ? (M + __log2f(L)) * kLn2 : -INFINITY;
+  }
 }
 
 // ------------------------------------------------------------------ a6: append
-constexpr int AP_NT = 1024;
+// Two launches.  Count: one wave per 64 heads records how many of its heads need a fresh
+// page (row empty, or newest page full) and whether any such row is already at max_pages,
+// and block 0 snapshots the free-list top.  Write: every workgroup re-derives its heads'
+// needs, takes the exclusive prefix over the preceding workgroups' counts (head order, so
+// the pops are the same as a sequential scan), decides success from the global totals,
+// and writes its heads.  Only block 0 updates free_top; every block reads the snapshot.
+// Workspace (int32): [0] top snapshot, [1, 1+nblk) counts, [1+nblk, 1+2*nblk) full flags.
+constexpr int AP_HPB = 64;     // heads per workgroup
+constexpr int AP_NT = 256;
+
+__device__ inline void append_need(int h, int n_heads, const int32_t* n_pages, const uint16_t* masks,
+                                   int max_pages, int& n, uint32_t& m, int& need, int& full) {
+  n = 0;
+  m = 0;
+  need = 0;
+  full = 0;
+  if (h >= n_heads) return;
+  n = n_pages[h];
+  m = n > 0 ? masks[(size_t)h * max_pages + n - 1] : 0xffffu;
+  if ((m & 0x8000u) || n == 0) {
+    need = 1;
+    full = n >= max_pages;
+  }
+}
+
+__global__ __launch_bounds__(64) void append_count_kernel(int n_heads, const int32_t* __restrict__ n_pages,
+                                                          const uint16_t* __restrict__ masks, int max_pages,
+                                                          const int32_t* __restrict__ free_top,
+                                                          int32_t* __restrict__ ws) {
+  const int nblk = gridDim.x;
+  int n, need, full;
+  uint32_t m;
+  append_need(blockIdx.x * AP_HPB + threadIdx.x, n_heads, n_pages, masks, max_pages, n, m, need, full);
+  need = wave_sum(need);
+  full = __any(full) ? 1 : 0;
+  if (threadIdx.x == 0) {
+    ws[1 + blockIdx.x] = need;
+    ws[1 + nblk + blockIdx.x] = full;
+    if (blockIdx.x == 0) ws[0] = *free_top;
+  }
+}
 
 template <int ROW_BYTES>
-__global__ __launch_bounds__(AP_NT) void append_kernel(
-    int n_heads, int Hkv, char* __restrict__ k_pool, char* __restrict__ v_pool,
-    int32_t* __restrict__ table, uint16_t* __restrict__ masks, int32_t* __restrict__ n_pages,
-    int max_pages, const char* __restrict__ k_new, const char* __restrict__ v_new,
-    int32_t* __restrict__ free_ids, int32_t* __restrict__ free_top, int32_t* __restrict__ status) {
-  __shared__ int lds[AP_NT / 64];
-  __shared__ int s_ok, s_base;
-  const int per = (n_heads + AP_NT - 1) / AP_NT;
-  const int h0 = threadIdx.x * per, h1 = min(h0 + per, n_heads);
-  int need = 0, full = 0;
-  for (int h = h0; h < h1; ++h) {
-    const int n = n_pages[h];
-    const uint32_t m = n > 0 ? masks[(size_t)h * max_pages + n - 1] : 0xffffu;
-    if (m & 0x8000u || n == 0) {
-      need += 1;
-      if (n >= max_pages) full = 1;
-    }
-  }
-  full = __syncthreads_or(full);
-  // exclusive scan of needs in head order
+__global__ __launch_bounds__(AP_NT) void append_write_kernel(
+    int n_heads, char* __restrict__ k_pool, char* __restrict__ v_pool, int32_t* __restrict__ table,
+    uint16_t* __restrict__ masks, int32_t* __restrict__ n_pages, int max_pages,
+    const char* __restrict__ k_new, const char* __restrict__ v_new, const int32_t* __restrict__ free_ids,
+    int32_t* __restrict__ free_top, int32_t* __restrict__ status, const int32_t* __restrict__ ws) {
+  constexpr int CH = ROW_BYTES / 16;
+  __shared__ int s_red[3][AP_NT / 64];
+  __shared__ int64_t s_dst[AP_HPB];
+  const int nblk = gridDim.x, blk = blockIdx.x;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  int x = need;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(x, o, 64);
-    if (lane >= o) x += y;
+  // global totals and this block's offset, from the counts of the first launch
+  int before = 0, total = 0, anyfull = 0;
+  for (int b = threadIdx.x; b < nblk; b += AP_NT) {
+    const int c = ws[1 + b];
+    total += c;
+    if (b < blk) before += c;
+    anyfull |= ws[1 + nblk + b];
   }
-  if (lane == 63) lds[wave] = x;
+  before = wave_sum(before);
+  total = wave_sum(total);
+  anyfull = __any(anyfull) ? 1 : 0;
+  if (lane == 0) {
+    s_red[0][wave] = before;
+    s_red[1][wave] = total;
+    s_red[2][wave] = anyfull;
+  }
   __syncthreads();
-  int before = 0, total = 0;
+  before = total = anyfull = 0;
+#pragma unroll
   for (int w = 0; w < AP_NT / 64; ++w) {
-    if (w < wave) before += lds[w];
-    total += lds[w];
+    before += s_red[0][w];
+    total += s_red[1][w];
+    anyfull |= s_red[2][w];
   }
-  int off = before + x - need;
-  if (threadIdx.x == 0) {
-    const int top = *free_top;
-    s_ok = (!full && total <= top) ? 1 : 0;
-    s_base = top - total;
-    if (!s_ok && status) atomicOr(status, HK_FLAG_NOSPACE);
-    if (s_ok) *free_top = top - total;
+  const int top = ws[0];
+  const bool ok = !anyfull && total <= top;
+  if (blk == 0 && threadIdx.x == 0) {
+    if (ok) *free_top = top - total;
+    else if (status) atomicOr(status, HK_FLAG_NOSPACE);
+  }
+  if (!ok) return;
+  if (wave == 0) {
+    const int h = blk * AP_HPB + lane;
+    int n, need, full;
+    uint32_t m;
+    append_need(h, n_heads, n_pages, masks, max_pages, n, m, need, full);
+    int x = need;   // inclusive scan over the wave
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(x, o, 64);
+      if (lane >= o) x += y;
+    }
+    int64_t dst = -1;
+    if (h < n_heads) {
+      int page, slot;
+      if (need) {
+        page = free_ids[top - total + before + x - 1];
+        table[(size_t)h * max_pages + n] = page;
+        masks[(size_t)h * max_pages + n] = 1;
+        n_pages[h] = n + 1;
+        slot = 0;
+      } else {
+        page = table[(size_t)h * max_pages + n - 1];
+        slot = 32 - __clz(m);               // one past the highest valid slot
+        masks[(size_t)h * max_pages + n - 1] = (uint16_t)(m | (1u << slot));
+      }
+      dst = ((int64_t)page * HK_PAGE + slot) * ROW_BYTES;
+    }
+    s_dst[lane] = dst;
   }
   __syncthreads();
-  if (!s_ok) return;
-  for (int h = h0; h < h1; ++h) {
-    int n = n_pages[h];
-    const uint32_t m = n > 0 ? masks[(size_t)h * max_pages + n - 1] : 0xffffu;
-    int page, slot;
-    if (m & 0x8000u || n == 0) {
-      page = free_ids[s_base + off];
-      ++off;
-      table[(size_t)h * max_pages + n] = page;
-      masks[(size_t)h * max_pages + n] = 1;
-      n_pages[h] = n + 1;
-      slot = 0;
-    } else {
-      page = table[(size_t)h * max_pages + n - 1];
-      slot = 32 - __clz(m);               // one past the highest valid slot
-      masks[(size_t)h * max_pages + n - 1] = (uint16_t)(m | (1u << slot));
-    }
-    const int s = h / Hkv, kv = h % Hkv;
-    const size_t src = ((size_t)s * Hkv + kv) * ROW_BYTES;
-    const size_t dst = ((size_t)page * HK_PAGE + slot) * ROW_BYTES;
-#pragma unroll
-    for (int i = 0; i < ROW_BYTES / 16; ++i) {
-      *reinterpret_cast<uint4*>(k_pool + dst + 16 * i) = *reinterpret_cast<const uint4*>(k_new + src + 16 * i);
-      *reinterpret_cast<uint4*>(v_pool + dst + 16 * i) = *reinterpret_cast<const uint4*>(v_new + src + 16 * i);
-    }
+  // rows of the workgroup's heads: K then V, 16-byte chunks, consecutive threads on one row
+  const int h0 = blk * AP_HPB;
+  for (int i = threadIdx.x; i < 2 * AP_HPB * CH; i += AP_NT) {
+    const int kv = i / (AP_HPB * CH), r = i % (AP_HPB * CH);
+    const int hl = r / CH, ch = r % CH;
+    const int64_t dst = s_dst[hl];
+    if (dst < 0) continue;
+    const size_t src = (size_t)(h0 + hl) * ROW_BYTES + ch * 16;
+    const uint4 u = *reinterpret_cast<const uint4*>((kv ? v_new : k_new) + src);
+    *reinterpret_cast<uint4*>((kv ? v_pool : k_pool) + dst + ch * 16) = u;
   }
 }
 
 template <typename T, int D, int G>
 static void launch_split(dim3 grid, hipStream_t st, const void* q, const hk_paged_kv* kv, int Hq,
-                         int Hkv, int pps, float c2, float* part, int n_split) {
+                         int Hkv, float c2, float* part, int n_split) {
   hipLaunchKernelGGL((decode_split_kernel<T, D, G>), grid, dim3(DEC_NT), 0, st,
                      static_cast<const T*>(q), static_cast<const T*>(kv->k_pool),
                      static_cast<const T*>(kv->v_pool), kv->page_table, kv->page_mask, kv->n_pages,
-                     Hq, Hkv, kv->max_pages, pps, c2, part, n_split);
+                     Hq, Hkv, kv->max_pages, c2, part, n_split);
 }
 
 template <typename T, int D>
 static bool launch_split_g(int G, dim3 grid, hipStream_t st, const void* q, const hk_paged_kv* kv,
-                           int Hq, int Hkv, int pps, float c2, float* part, int n_split) {
+                           int Hq, int Hkv, float c2, float* part, int n_split) {
   switch (G) {
-    case 1: launch_split<T, D, 1>(grid, st, q, kv, Hq, Hkv, pps, c2, part, n_split); return true;
-    case 2: launch_split<T, D, 2>(grid, st, q, kv, Hq, Hkv, pps, c2, part, n_split); return true;
-    case 4: launch_split<T, D, 4>(grid, st, q, kv, Hq, Hkv, pps, c2, part, n_split); return true;
-    case 7: launch_split<T, D, 7>(grid, st, q, kv, Hq, Hkv, pps, c2, part, n_split); return true;
-    case 8: launch_split<T, D, 8>(grid, st, q, kv, Hq, Hkv, pps, c2, part, n_split); return true;
+    case 1: launch_split<T, D, 1>(grid, st, q, kv, Hq, Hkv, c2, part, n_split); return true;
+    case 2: launch_split<T, D, 2>(grid, st, q, kv, Hq, Hkv, c2, part, n_split); return true;
+    case 4: launch_split<T, D, 4>(grid, st, q, kv, Hq, Hkv, c2, part, n_split); return true;
+    case 7: launch_split<T, D, 7>(grid, st, q, kv, Hq, Hkv, c2, part, n_split); return true;
+    case 8: launch_split<T, D, 8>(grid, st, q, kv, Hq, Hkv, c2, part, n_split); return true;
     default: return false;
   }
 }
-
-constexpr int DEC_PPS = 16;   // pages per split
 
 }  // namespace hk
 
@@ -331,40 +421,46 @@ hipError_t hk_launch_decode(int NS, int Hq, int Hkv, int D, const void* q, const
   dim3 grid(n_split, n_heads);
   const bool bf = kv->dtype == HK_BF16;
   bool ok;
-  if (bf && D == 128) ok = launch_split_g<uint16_t, 128>(G, grid, st, q, kv, Hq, Hkv, DEC_PPS, c2, part, n_split);
-  else if (bf) ok = launch_split_g<uint16_t, 64>(G, grid, st, q, kv, Hq, Hkv, DEC_PPS, c2, part, n_split);
-  else if (D == 128) ok = launch_split_g<float, 128>(G, grid, st, q, kv, Hq, Hkv, DEC_PPS, c2, part, n_split);
-  else ok = launch_split_g<float, 64>(G, grid, st, q, kv, Hq, Hkv, DEC_PPS, c2, part, n_split);
+  if (bf && D == 128) ok = launch_split_g<uint16_t, 128>(G, grid, st, q, kv, Hq, Hkv, c2, part, n_split);
+  else if (bf) ok = launch_split_g<uint16_t, 64>(G, grid, st, q, kv, Hq, Hkv, c2, part, n_split);
+  else if (D == 128) ok = launch_split_g<float, 128>(G, grid, st, q, kv, Hq, Hkv, c2, part, n_split);
+  else ok = launch_split_g<float, 64>(G, grid, st, q, kv, Hq, Hkv, c2, part, n_split);
   if (!ok) return hipErrorInvalidValue;
   if (D == 128)
-    hipLaunchKernelGGL(decode_merge_kernel<128>, dim3(n_heads * G), dim3(128), 0, st, part, n_split, G,
+    hipLaunchKernelGGL(decode_merge_kernel<128>, dim3(n_heads), dim3(256), 0, st, part, n_split, G,
                        Hq, Hkv, o, lse);
   else
-    hipLaunchKernelGGL(decode_merge_kernel<64>, dim3(n_heads * G), dim3(64), 0, st, part, n_split, G,
+    hipLaunchKernelGGL(decode_merge_kernel<64>, dim3(n_heads), dim3(256), 0, st, part, n_split, G,
                        Hq, Hkv, o, lse);
   return hipGetLastError();
 }
 
 size_t hk_append_ws(int NS, int Hkv) {
-  (void)NS;
-  (void)Hkv;
-  return 0;
+  const int nblk = (NS * Hkv + AP_HPB - 1) / AP_HPB;
+  return (size_t)(1 + 2 * nblk) * sizeof(int32_t);
 }
 
 hipError_t hk_launch_append(int NS, int Hkv, int D, const hk_paged_kv* kv, const void* k_new,
                             const void* v_new, const hk_allocator* alloc, int32_t* status, void* ws,
                             hipStream_t st) {
-  (void)ws;
-  const int n_heads = NS * Hkv;
+  const int n_heads = NS * Hkv, nblk = (n_heads + AP_HPB - 1) / AP_HPB;
   const int row_bytes = D * (kv->dtype == HK_BF16 ? 2 : 4);
   char* kp = static_cast<char*>(kv->k_pool);
   char* vp = static_cast<char*>(kv->v_pool);
   const char* kn = static_cast<const char*>(k_new);
   const char* vn = static_cast<const char*>(v_new);
+  int32_t* w = static_cast<int32_t*>(ws);
+  hipLaunchKernelGGL(append_count_kernel, dim3(nblk), dim3(64), 0, st, n_heads, kv->n_pages,
+                     kv->page_mask, kv->max_pages, alloc->free_top, w);
+#define HK_APPEND_WRITE(RB)                                                                       \
+  hipLaunchKernelGGL((append_write_kernel<RB>), dim3(nblk), dim3(AP_NT), 0, st, n_heads, kp, vp, \
+                     kv->page_table, kv->page_mask, kv->n_pages, kv->max_pages, kn, vn,           \
+                     alloc->free_ids, alloc->free_top, status, w)
   switch (row_bytes) {
-    case 128: hipLaunchKernelGGL((append_kernel<128>), dim3(1), dim3(AP_NT), 0, st, n_heads, Hkv, kp, vp, kv->page_table, kv->page_mask, kv->n_pages, kv->max_pages, kn, vn, alloc->free_ids, alloc->free_top, status); break;
-    case 256: hipLaunchKernelGGL((append_kernel<256>), dim3(1), dim3(AP_NT), 0, st, n_heads, Hkv, kp, vp, kv->page_table, kv->page_mask, kv->n_pages, kv->max_pages, kn, vn, alloc->free_ids, alloc->free_top, status); break;
-    default: hipLaunchKernelGGL((append_kernel<512>), dim3(1), dim3(AP_NT), 0, st, n_heads, Hkv, kp, vp, kv->page_table, kv->page_mask, kv->n_pages, kv->max_pages, kn, vn, alloc->free_ids, alloc->free_top, status); break;
+    case 128: HK_APPEND_WRITE(128); break;
+    case 256: HK_APPEND_WRITE(256); break;
+    default: HK_APPEND_WRITE(512); break;
   }
+#undef HK_APPEND_WRITE
   return hipGetLastError();
 }

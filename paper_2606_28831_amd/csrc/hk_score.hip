@@ -14,12 +14,13 @@
 //           C[ref][key] = Kref K^T for the cosine-redundancy metric.
 //
 // Operand mapping.  For the 32-row MFMA operands (32x32x16 bf16, 32x32x2 f32) lane l
-// supplies row (l % 32) and one half of the contraction range.  The contraction index
-// is permuted so that lane l always works on dims [ (l/32) * D/2, (l/32+1) * D/2 ) of its
-// row: step kk uses the next 8 (bf16) or 1 (f32) of them.  Q and K use the same
-// permutation, so the dot products are unchanged, every lane reads one contiguous half
-// row of its key (D/2 elements, 16-byte loads), and one fragment serves as either the
-// A or the B operand.
+// supplies row (l % 32) and one half of each contraction step.  bf16 keeps the natural
+// k-order: step kk covers dims [16 kk, 16 kk + 16), lanes l < 32 the first 8 and lanes
+// l >= 32 the next 8, so the two lanes of a row read adjacent 16-byte pieces.  f32
+// permutes the contraction index so that lane l works on dims [ (l/32) * D/2,
+// (l/32+1) * D/2 ) of its row, one per step, and reads one contiguous half row.  Q and
+// K use the same order, so the dot products are unchanged and one fragment serves as
+// either the A or the B operand.
 // Accumulator layout of the 32x32 MFMA: register r of lane l holds row
 // 8*(r/4) + 4*(l/32) + (r%4), column l % 32.
 #include "hk_internal.h"
@@ -35,11 +36,13 @@ struct Frag<uint16_t, D> {
   static constexpr int KSTEPS = D / 16;
   static constexpr int BYTES_PER_STEP = 16;
   bf16x8 v[KSTEPS];
-  __device__ __forceinline__ void load(const uint16_t* row_half) {
-    const uint4* p = reinterpret_cast<const uint4*>(row_half);
+  // natural MFMA k-order: step kk covers dims [16 kk, 16 kk + 16), lanes l < 32 the first
+  // 8 and lanes l >= 32 the next 8, so the two lanes of a key read 32 contiguous bytes
+  __device__ __forceinline__ void load(const uint16_t* row, int half) {
+    const uint4* p = reinterpret_cast<const uint4*>(row + half * 8);
 #pragma unroll
     for (int kk = 0; kk < KSTEPS; ++kk) {
-      uint4 u = p[kk];
+      uint4 u = p[2 * kk];
       v[kk] = __builtin_bit_cast(bf16x8, u);
     }
   }
@@ -77,8 +80,10 @@ struct Frag<float, D> {
   static constexpr int KSTEPS = D / 2;
   static constexpr int BYTES_PER_STEP = 4;
   float v[KSTEPS];
-  __device__ __forceinline__ void load(const float* row_half) {
-    const float4* p = reinterpret_cast<const float4*>(row_half);
+  // permuted k-order: lane l covers dims [(l/32) D/2, (l/32 + 1) D/2), one element per
+  // step, so each lane loads its half row with 16-byte loads
+  __device__ __forceinline__ void load(const float* row, int half) {
+    const float4* p = reinterpret_cast<const float4*>(row + half * (D / 2));
 #pragma unroll
     for (int i = 0; i < KSTEPS / 4; ++i) {
       float4 u = p[i];
@@ -122,12 +127,13 @@ __device__ __forceinline__ void stage_rows(char* lds, int R, int R_pad, RowFn ro
     uint4 u = make_uint4(0, 0, 0, 0);
     if (src) u = *reinterpret_cast<const uint4*>(src + ch * VEC);
     const int e0 = ch * VEC;
-    const int half = e0 / HALF, off = e0 % HALF;
-    const int lane = half * 32 + (r & 31), blk = r >> 5;
+    const int blk = r >> 5;
     if constexpr (sizeof(T) == 2) {
-      const int kk = off / 8;
+      const int kk = e0 / 16, lane = ((e0 / 8) & 1) * 32 + (r & 31);     // natural k-order
       *reinterpret_cast<uint4*>(lds + ((size_t)(blk * F::KSTEPS + kk) * 64 + lane) * 16) = u;
     } else {
+      const int half = e0 / HALF, off = e0 % HALF;                       // permuted k-order
+      const int lane = half * 32 + (r & 31);
       const uint32_t w[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
       for (int i = 0; i < 4; ++i)
@@ -150,6 +156,9 @@ __device__ __forceinline__ void stage_rows(char* lds, int R, int R_pad, RowFn ro
 #endif
 #ifndef HK_SCORE_KT
 #define HK_SCORE_KT 1
+#endif
+#ifndef HK_SCORE_PIPE
+#define HK_SCORE_PIPE 1
 #endif
 #if HK_SCORE_WPE > 0
 #define HK_SCORE_ATTR __launch_bounds__(SCORE_NT) __attribute__((amdgpu_waves_per_eu(HK_SCORE_WPE, HK_SCORE_WPE)))
@@ -317,7 +326,7 @@ __device__ __forceinline__ void load_tile(Frag<T, D>& kf, const T* __restrict__ 
   const int kl = lane & 31, pg = p0 + (kl >> 4);
   if (pg < p_end) {
     const int phys = trow[pg];
-    kf.load(k_pool + ((size_t)phys * HK_PAGE + (kl & 15)) * D + (lane >> 5) * (D / 2));
+    kf.load(k_pool + ((size_t)phys * HK_PAGE + (kl & 15)) * D, lane >> 5);
   } else {
     kf.zero();
   }
@@ -327,6 +336,36 @@ __device__ __forceinline__ void load_tile(Frag<T, D>& kf, const T* __restrict__ 
 __device__ __forceinline__ uint32_t lane_rows(uint32_t tmask, int lane) {
   const uint32_t t = tmask >> (4 * (lane >> 5));
   return (t & 0xfu) | ((t >> 4) & 0xf0u) | ((t >> 8) & 0xf00u) | ((t >> 12) & 0xf000u);
+}
+
+
+// Walk a wave's tiles p0, p0 + step, ...  With prefetch, the next tile's K fragments are
+// loaded (into a second register set) before the current tile is processed; the loop is
+// unrolled by two so both sets stay in registers.
+template <typename F, typename LoadFn, typename ProcFn>
+__device__ __forceinline__ void tile_loop(LoadFn load_group, ProcFn process, int p0, int p_end,
+                                          int step) {
+  if constexpr (HK_SCORE_PREFETCH) {
+    F ka[SCORE_KT], kb[SCORE_KT];
+    if (p0 < p_end) load_group(ka, p0);
+    while (p0 < p_end) {
+      int pn = p0 + step;
+      if (pn < p_end) load_group(kb, pn);
+      process(ka, p0);
+      p0 = pn;
+      if (p0 >= p_end) break;
+      pn = p0 + step;
+      if (pn < p_end) load_group(ka, pn);
+      process(kb, p0);
+      p0 = pn;
+    }
+  } else {
+    for (; p0 < p_end; p0 += step) {
+      F kf[SCORE_KT];
+      load_group(kf, p0);
+      process(kf, p0);
+    }
+  }
 }
 
 // ------------------------------------------------------------------ pass 1
@@ -358,19 +397,21 @@ __global__ HK_SCORE_ATTR void score_pass1_kernel(
 
   const int32_t* trow = table + (size_t)h * max_pages;
   const uint16_t* mrow = masks + (size_t)h * max_pages;
-  for (int p0 = p_begin + SCORE_WPP * wave; p0 < p_end; p0 += SCORE_WPP * SCORE_NW) {
-    F kf[SCORE_KT];
+  auto load_group = [&](F* kf, int p0) {
+#pragma unroll
+    for (int t = 0; t < SCORE_KT; ++t) load_tile<T, D>(kf[t], k_pool, trow, p0 + 2 * t, p_end, lane);
+  };
+  auto process = [&](F* kf, int p0) {
     uint32_t tm[SCORE_KT];
     bool all_full = true, any = false;
 #pragma unroll
     for (int t = 0; t < SCORE_KT; ++t) {
       const int pa = p0 + 2 * t, pb = pa + 1;
-      load_tile<T, D>(kf[t], k_pool, trow, pa, p_end, lane);
       tm[t] = (pa < p_end ? (uint32_t)mrow[pa] : 0u) | ((pb < p_end) ? (uint32_t)mrow[pb] << 16 : 0u);
       all_full = all_full && (tm[t] == 0xffffffffu);
       any = any || (tm[t] != 0u);
     }
-    if (all_full && SCORE_KT == 1) {
+    if (all_full && SCORE_KT == 1 && HK_SCORE_PIPE) {
       p1_tile_pipelined<F, QB>(kf[0], smem, c2, lane, M, L);
     } else if (all_full) {
 #pragma unroll
@@ -420,7 +461,8 @@ __global__ HK_SCORE_ATTR void score_pass1_kernel(
         }
       }
     }
-  }
+  };
+  tile_loop<F>(load_group, process, p_begin + SCORE_WPP * wave, p_end, SCORE_WPP * SCORE_NW);
   // merge lane halves (same query column), then waves
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
@@ -573,14 +615,16 @@ __global__ HK_SCORE_ATTR void score_pass2_kernel(
   }
   __syncthreads();
 
-  for (int p0 = p_begin + SCORE_WPP * wave; p0 < p_cand_end; p0 += SCORE_WPP * SCORE_NW) {
-    F kf[SCORE_KT];
+  auto load_group = [&](F* kf, int p0) {
+#pragma unroll
+    for (int t = 0; t < SCORE_KT; ++t) load_tile<T, D>(kf[t], k_pool, trow, p0 + 2 * t, p_cand_end, lane);
+  };
+  auto process = [&](F* kf, int p0) {
     uint32_t m0[SCORE_KT], m1[SCORE_KT];
     bool any = false;
 #pragma unroll
     for (int t = 0; t < SCORE_KT; ++t) {
       const int pa = p0 + 2 * t, pb = pa + 1;
-      load_tile<T, D>(kf[t], k_pool, trow, pa, p_cand_end, lane);
       m0[t] = (pa < p_cand_end) ? (uint32_t)mrow[pa] : 0u;
       m1[t] = (pb < p_cand_end) ? (uint32_t)mrow[pb] : 0u;
       any = any || ((m0[t] | m1[t]) != 0u);
@@ -589,7 +633,7 @@ __global__ HK_SCORE_ATTR void score_pass2_kernel(
     float col[SCORE_KT];
 #pragma unroll
     for (int t = 0; t < SCORE_KT; ++t) col[t] = 0.f;
-    if (any && SCORE_KT == 1) {
+    if (any && SCORE_KT == 1 && HK_SCORE_PIPE) {
       col[0] = p2_tile_pipelined<F, QB>(kf[0], smem, lse2, c2, lane);
     } else if (any) {
 #pragma unroll
@@ -649,7 +693,8 @@ __global__ HK_SCORE_ATTR void score_pass2_kernel(
       }
       if (write) s_out[(size_t)h * S_max + slot] = cand ? fmaf(fast_log2(c_all), kLn2, -lnR) : -INFINITY;
     }
-  }
+  };
+  tile_loop<F>(load_group, process, p_begin + SCORE_WPP * wave, p_cand_end, SCORE_WPP * SCORE_NW);
 }
 
 template <typename K>

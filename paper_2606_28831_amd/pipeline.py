@@ -11,7 +11,7 @@ from dataclasses import dataclass
 
 import torch
 
-from . import (Allocator, PagedKV, OP_COMPACT, OP_DECODE, OP_SCORE, dims, hk_append_kv,
+from . import (Allocator, PagedKV, OP_APPEND, OP_COMPACT, OP_DECODE, OP_SCORE, dims, hk_append_kv,
                hk_calibrate, hk_calibrate_solve_T, hk_compact, hk_decode_attn, hk_score,
                hk_topp_select, workspace)
 
@@ -120,10 +120,12 @@ class Decoder:
         self.sm_scale = 1.0 / math.sqrt(D)
         dev = kv.k_pool.device
         self.ws = workspace(OP_DECODE, self.d, kv.max_pages, dev)
+        self.ws_app = workspace(OP_APPEND, self.d, kv.max_pages, dev)
         self.status = torch.zeros(1, dtype=torch.int32, device=dev)
 
     def append(self, k_new, v_new, stream=None):
-        hk_append_kv(self.d, self.kv, k_new, v_new, self.alloc, self.status, stream=stream)
+        hk_append_kv(self.d, self.kv, k_new, v_new, self.alloc, self.status, self.ws_app,
+                     stream=stream)
 
     def attend(self, q, o, lse, stream=None):
         hk_decode_attn(self.d, q, self.kv, self.sm_scale, o, lse, self.ws, stream=stream)
@@ -151,13 +153,15 @@ class DecodeLoop:
         self.layers = [kv.rows(l * B * Hkv, B * Hkv) for l in range(L)]
         self.sm_scale = 1.0 / math.sqrt(D)
         self.ws_dec = workspace(OP_DECODE, self.d_layer, kv.max_pages, dev)
+        self.ws_app = workspace(OP_APPEND, self.d_all, kv.max_pages, dev)
         self.status = torch.zeros(1, dtype=torch.int32, device=dev)
         self.o = torch.empty(self.NS, Hq, D, dtype=torch.float32, device=dev)
         self.comp = Compressor(self.NS, Hq, Hkv, D, W, kv, alloc, p, L_dense=L_dense,
                                L_sparse=L_sparse, metric="attn")
 
     def step(self, q_t, k_t, v_t, lse_t, stream=None):
-        hk_append_kv(self.d_all, self.kv, k_t, v_t, self.alloc, self.status, stream=stream)
+        hk_append_kv(self.d_all, self.kv, k_t, v_t, self.alloc, self.status, self.ws_app,
+                     stream=stream)
         B = self.B
         for l, kv_l in enumerate(self.layers):
             hk_decode_attn(self.d_layer, q_t[l * B:(l + 1) * B], kv_l, self.sm_scale,

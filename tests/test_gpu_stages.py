@@ -425,26 +425,47 @@ def test_decode_after_compaction_equals_masked_original():
     check_lse(np64(l2).reshape(-1), np64(l1).reshape(-1), 2e-3, "lse")
 
 
+APPEND_MANY = dict(L=1, B=37, Hq=8, Hkv=4, D=128, N=40, dtype="bf16", W=8, seed=16,
+                   recipe="normal")
+
+
 @pytest.mark.parametrize("name", ["bf16_d128_g4_ragged_holes", "cfg1_f32_d64_g4",
-                                  "bf16_d128_g1_w32_tail1"])
+                                  "bf16_d128_g1_w32_tail1", "many_heads_ragged"])
 def test_append(name):
-    hk, cfg, w, kv = _setup(name, max_pages=256)
+    import paper_2606_28831_amd as hk
+    if name == "many_heads_ragged":
+        # 148 heads: three workgroups of the write launch, the last one partial; holes in
+        # the newest pages make the fill level differ per head, so pops are scattered
+        cfg = APPEND_MANY
+        w = WL.make_workload(cfg, DEV, max_pages=64, hole_prob=0.3)
+        kv = hk.PagedKV(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)
+    else:
+        hk, cfg, w, kv = _setup(name, max_pages=256)
     d = hk.dims(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"])
     alloc = hk.Allocator(w.free_ids, w.free_top)
     st = torch.zeros(1, dtype=torch.int32, device=DEV)
+    ws = hk.workspace(hk.OP_APPEND, d, w.max_pages, DEV)
     for step in range(20):
         before = HostCache(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)
         top0 = int(w.free_top.item())
+        free0 = np_i(w.free_ids).copy()
         kn = torch.randn(w.NS, cfg["Hkv"], cfg["D"], device=DEV).to(w.k_pool.dtype)
         vn = torch.randn(w.NS, cfg["Hkv"], cfg["D"], device=DEV).to(w.k_pool.dtype)
-        hk.hk_append_kv(d, kv, kn, vn, alloc, st)
+        hk.hk_append_kv(d, kv, kn, vn, alloc, st, ws)
         torch.cuda.synchronize()
         after = HostCache(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)
+        pos = [O.append_position(before.mask[h], int(before.n[h])) for h in range(w.n_heads)]
+        total = sum(int(p[2]) for p in pos)
         pops = 0
         for h in range(w.n_heads):
             K0, v0 = before.head(h)
             K1, v1 = after.head(h)
-            pp, slot, new = O.append_position(before.mask[h], int(before.n[h]))
+            pp, slot, new = pos[h]
+            if new:
+                # pops in head order from the top of the free stack
+                assert int(after.table[h][pp]) == int(free0[top0 - total + pops]), (step, h)
+            else:
+                assert int(after.table[h][pp]) == int(before.table[h][pp]), (step, h)
             pops += int(new)
             j = pp * 16 + slot
             exp_valid = np.zeros(max(len(v0), j + 1), bool)
@@ -457,6 +478,37 @@ def test_append(name):
             assert np.array_equal(K1[:len(v0)][v0], K0[v0])
         assert int(w.free_top.item()) == top0 - pops
     assert int(st.item()) == 0
+
+
+@pytest.mark.parametrize("why", ["short_free_list", "row_full"])
+def test_append_nospace(why):
+    """A step that cannot be placed leaves every head untouched and raises NOSPACE."""
+    import paper_2606_28831_amd as hk
+    cfg = dict(APPEND_MANY, N=48)     # every newest page is full: each head pops
+    w = WL.make_workload(cfg, DEV, max_pages=64)
+    kv = hk.PagedKV(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)
+    host = HostCache(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)
+    need = sum(int(O.append_position(host.mask[h], int(host.n[h]))[2]) for h in range(w.n_heads))
+    assert need > 0
+    if why == "short_free_list":
+        w.free_top.fill_(need - 1)
+    else:
+        # the last head's row: full pages up to max_pages
+        h = w.n_heads - 1
+        w.n_pages[h] = w.max_pages
+        w.page_mask[h, :] = -1
+        w.page_table[h, :] = w.page_table[h, 0]
+    d = hk.dims(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"])
+    snap = [t.clone() for t in (w.page_table, w.page_mask, w.n_pages, w.free_top, w.k_pool)]
+    st = torch.zeros(1, dtype=torch.int32, device=DEV)
+    kn = torch.randn(w.NS, cfg["Hkv"], cfg["D"], device=DEV).to(w.k_pool.dtype)
+    vn = torch.randn(w.NS, cfg["Hkv"], cfg["D"], device=DEV).to(w.k_pool.dtype)
+    hk.hk_append_kv(d, kv, kn, vn, hk.Allocator(w.free_ids, w.free_top), st,
+                    hk.workspace(hk.OP_APPEND, d, w.max_pages, DEV))
+    torch.cuda.synchronize()
+    assert int(st.item()) & hk.FLAG_NOSPACE
+    for a, b in zip(snap, (w.page_table, w.page_mask, w.n_pages, w.free_top, w.k_pool)):
+        assert torch.equal(a, b)
 
 
 def test_determinism_bitwise():

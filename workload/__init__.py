@@ -124,7 +124,9 @@ def make_workload(cfg: dict, device="cpu", pool_slack: float = 2.0, max_pages: i
     table[:, :n_used] = perm[:used].view(H, n_used)
     free_ids = torch.zeros(num_pages, dtype=torch.int32, device=dev)
     n_free = num_pages - used
-    free_ids[:n_free] = perm[used:]
+    # a fresh pool's free pages are kept in address order, so a run of pops returns a
+    # run of consecutive page ids (live pages stay scattered)
+    free_ids[:n_free] = torch.sort(perm[used:]).values
     free_top = torch.tensor([n_free], dtype=torch.int32, device=dev)
 
     masks = torch.zeros((H, mp), dtype=torch.int32, device=dev)

@@ -55,6 +55,78 @@ def _cand_tokens(w, L_dense):
     return int((bits.sum(-1) * cand_pages).sum().item())
 
 
+def _condensed_kept(w, sel_bits, L_dense, L_sparse):
+    """Selected slots inside the condensed tier (the rows the rewrite copies), per the
+    pristine page counts: dense = newest ceil(L_dense/16) pages, sparse = the
+    floor(L_sparse/16) pages before them, condensed = the rest."""
+    n = w.n_pages.long()
+    nd = torch.clamp(n, max=-(-L_dense // 16))
+    ns = torch.minimum(n - nd, torch.full_like(n, L_sparse // 16))
+    nc = n - nd - ns
+    words = sel_bits.to(torch.int64) & 0xFFFFFFFF
+    bits = (words[:, :, None] >> torch.arange(32, device=words.device)) & 1
+    bits = bits.reshape(words.shape[0], -1)
+    pos = torch.arange(bits.shape[1], device=bits.device)[None, :]
+    return int((bits * (pos < 16 * nc[:, None])).sum().item())
+
+
+# source file of each timed kernel (a stored counter reading is only valid for that source)
+ROOFLINE_KERNELS = ("score_pass1", "score_pass2", "compact_gather", "decode_split")
+KERNEL_SOURCE = {"score_pass1": "hk_score.hip", "score_pass2": "hk_score.hip",
+                 "compact_gather": "hk_compact.hip", "decode_split": "hk_decode.hip"}
+
+
+def _source_sha(kernel):
+    """sha256 over the kernel's source file and the shared device helpers it includes."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2606_28831_amd", "csrc")
+    for f in (KERNEL_SOURCE[kernel], "hk_internal.h"):
+        h.update(open(os.path.join(csrc, f), "rb").read())
+    return h.hexdigest()
+
+
+def _traffic(kernel, workload):
+    """HBM bytes per launch from the stored rocprofv3 counter summary of this kernel and
+    workload (FETCH_SIZE and WRITE_SIZE, scaled by the plain-copy calibration), or None when
+    there is none or the kernel's source has changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.txt")
+    src = os.path.join(ROOT, "paper_2606_28831_amd", "csrc", KERNEL_SOURCE.get(kernel, ""))
+    if not os.path.isfile(path) or not os.path.isfile(src):
+        return None, "no stored counter summary"
+    kv = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("source_sha256") != _source_sha(kernel):
+        return None, "kernel source changed since the counters were taken"
+    try:
+        return float(kv["hbm_bytes_per_launch"]), path
+    except (KeyError, ValueError):
+        return None, "malformed counter summary"
+
+
+def _roofline(ktime, per_launch, workload):
+    """Roofline entry for the kernel with the largest share of the timed region."""
+    timed = {k: v for k, v in ktime.items() if k in per_launch}
+    if not timed:
+        return None
+    name = max(timed, key=lambda k: timed[k]["ms_per_step"])
+    nbytes, flops = per_launch[name]
+    dur_s = timed[name]["avg_ms"] / 1e3
+    achieved = nbytes / dur_s / 1e9
+    traffic, note = _traffic(name, workload)
+    out = {"kernel": name, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
+           "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+           "traffic_source": note, "bytes_per_launch": nbytes, "avg_launch_ms": timed[name]["avg_ms"],
+           "launches_per_step": timed[name]["launches_per_step"]}
+    if flops:
+        out["mfma_tflops"] = flops / dur_s / 1e12
+        out["mfma_frac_bf16"] = out["mfma_tflops"] / BF16_PEAK_TFLOPS
+    return out
+
+
 def run_compression(args):
     import paper_2606_28831_amd as hk
     import workload as WL
@@ -82,12 +154,25 @@ def run_compression(args):
     def restore():
         WL.restore_state(w, pristine)
 
-    for _ in range(args.warmup):
+    # warmup, with every kernel timed: finds the kernel with the largest share of a step
+    for name in hk.TIMED_KERNELS:
+        hk.hk_timing_read(name)
+    hk.hk_timing_enable()
+    for _ in range(max(1, args.warmup)):
         restore()
         comp.step(w.q_obs, ref_slots=ref)
     torch.cuda.synchronize()
+    hk.hk_timing_enable([])
+    kwarm = {}
+    for name in hk.TIMED_KERNELS:
+        tot, n = hk.hk_timing_read(name)
+        if n:
+            kwarm[name] = tot
+    dominant = max((k for k in kwarm if k in ROOFLINE_KERNELS), key=lambda k: kwarm[k])
 
-    # ---------------- timed region: exactly K steps
+    # ---------------- timed region: exactly K steps.  The library records HIP events around
+    # each launch of the dominant kernel, on its launch stream.
+    hk.hk_timing_enable([dominant])
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
@@ -95,8 +180,23 @@ def run_compression(args):
         comp.step(w.q_obs, ref_slots=ref)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    hk.hk_timing_enable([])
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     status = int(comp.buf.status.item())
+    tot, n = hk.hk_timing_read(dominant)
+    ktime = {dominant: {"avg_ms": tot / n, "launches_per_step": n / args.steps,
+                        "ms_per_step": tot / args.steps}}
+    warm_steps = max(1, args.warmup)
+    kernels_warmup = {k: v / warm_steps for k, v in kwarm.items()}
+
+    # the same K steps with kernel timing off (event records cost a little launch time)
+    torch.cuda.synchronize()
+    t2 = time.perf_counter()
+    for _ in range(args.steps):
+        restore()
+        comp.step(w.q_obs, ref_slots=ref)
+    torch.cuda.synchronize()
+    ms_per_step_plain = (time.perf_counter() - t2) * 1e3 / args.steps
 
     # ---------------- per-stage timing (HIP events on the launch stream), outside the timed loop
     reps = max(3, min(args.steps, 10))
@@ -136,14 +236,16 @@ def run_compression(args):
     kept_mean = float(k.mean())
 
     # ---------------- algorithmic bytes (K read once, scores written+read, selection bits,
-    # condensed K and V read + written); flops of the score contraction per pass
+    # condensed K and V read + written); per-kernel bytes and flops per launch
     D, e = cfg["D"], _esize(cfg)
     S = w.S_max
     G = cfg["Hq"] // cfg["Hkv"]
     R = G * cfg["W"]
     H = w.n_heads
     n_metric = 2 if metric == "attn+red" else 1
-    k_cond_total = float(k.sum())
+    restore()
+    valid_tokens = _cand_tokens(w, 0)
+    k_cond_total = _condensed_kept(w, comp.buf.sel_bits, cfg["L_dense"], cfg["L_sparse"])
     bytes_k = tokens * D * e
     bytes_scores = H * S * 4 * 2 * n_metric
     bytes_sel = H * S / 8 * 2
@@ -151,22 +253,18 @@ def run_compression(args):
     bytes_q = cfg["W"] * w.NS * cfg["Hq"] * D * e
     alg_bytes = bytes_k + bytes_scores + bytes_sel + bytes_rewrite + bytes_q
     step_s = ms_per_step / 1e3
-    pass2_bytes = bytes_k + H * S * 4 + bytes_q
-    pass2_flops = 2.0 * R * tokens * D
-    if metric == "attn+red":
-        pass2_flops += 2.0 * cfg["n_ref"] * tokens * D
-
-    roof_kernel = {
-        "kernel": "score_pass2_kernel",
-        "bound": "hbm",
-        "achieved": pass2_bytes / (st["score_pass2"] / 1e3) / 1e9,
-        "peak": HBM_PEAK_GBS,
-        "unit": "GB/s",
-        "traffic": None,
-        "mfma_tflops": pass2_flops / (st["score_pass2"] / 1e3) / 1e12,
-        "bytes_per_launch": pass2_bytes,
+    n_ref = cfg.get("n_ref", 0) if metric == "attn+red" else 0
+    per_launch = {
+        # every valid key against the window (row LSE), the window queries
+        "score_pass1": (valid_tokens * D * e + bytes_q, 2.0 * R * valid_tokens * D),
+        # candidate keys, window queries and reference keys; score rows written (one per metric)
+        "score_pass2": (tokens * D * e + bytes_q + H * n_ref * D * e + H * S * 4 * n_metric,
+                        2.0 * (R + n_ref) * tokens * D),
+        # condensed rows: K and V, each read once and written once
+        "compact_gather": (bytes_rewrite, 0.0),
     }
-    roof_kernel["frac"] = roof_kernel["achieved"] / roof_kernel["peak"]
+    roof_kernel = _roofline(ktime, per_launch, cfg["name"])
+    roof_kernel["share_of_step"] = ktime[dominant]["ms_per_step"] / ms_per_step
 
     out = {
         "metric": METRIC,
@@ -190,6 +288,8 @@ def run_compression(args):
         "positions_per_s": positions / step_s,
         "stage_ms": st,
         "step_ms_events": step_ms_events,
+        "ms_per_step_no_kernel_events": ms_per_step_plain,
+        "kernel_ms_per_step_warmup": kernels_warmup,
         "budget": {"mean_kept": kept_mean, "min_frac": float(frac.min()),
                    "mean_frac": float(frac.mean()), "max_frac": float(frac.max()),
                    "SU": float(frac.mean() / max(1e-9, float(frac.max())))},
@@ -285,6 +385,9 @@ def run_decode(args):
     NS = L * B
     dt = WL.TORCH_DTYPE[cfg["dtype"]]
     seg_ms, seg_tokens_kv, kept = [], [], []
+    for name in hk.TIMED_KERNELS:
+        hk.hk_timing_read(name)
+    hk.hk_timing_enable(["decode_split"])    # the dominant kernel of the loop
     for seg in range(n_seg):
         g = torch.Generator(device=dev).manual_seed(cfg["seed"] * 7919 + seg + 1)
         q_seg = torch.randn(T, NS, Hq, D, generator=g, device=dev).to(dt)
@@ -305,11 +408,21 @@ def run_decode(args):
         seg_ms.append(e0.elapsed_time(e1))
         kept.append(float(loop.comp.buf.k.float().mean()))
         del q_seg, k_seg, v_seg, lse_seg
+    hk.hk_timing_enable([])
+    tot, n = hk.hk_timing_read("decode_split")
+    ktime = {"decode_split": {"avg_ms": tot / n, "launches_per_step": n / n_seg,
+                              "ms_per_step": tot / n_seg}}
     status = int(loop.status.item()) | int(loop.comp.buf.status.item())
     total_s = sum(seg_ms) / 1e3
     tokens = B * T * n_seg
-    # decode attention bytes: every valid K and V row read once per step per layer
-    dec_bytes = sum(v * 2 * D * 2 * T for v in seg_tokens_kv)
+    e = 2 if cfg["dtype"] == "bf16" else 4
+    # decode attention bytes: every valid K and V row read once per step per layer (the
+    # append adds one row per head per step), the step's queries read, outputs written
+    dec_bytes = sum(2 * D * e * (T * v + H * T * (T + 1) // 2) for v in seg_tokens_kv)
+    dec_bytes += n_seg * T * NS * Hq * (D * e + D * 4 + 4)
+    per_launch = {"decode_split": (dec_bytes / max(1, n_seg * T * L), 0.0)}
+    roof = _roofline(ktime, per_launch, cfg["name"])
+    roof["share_of_step"] = ktime["decode_split"]["ms_per_step"] / (sum(seg_ms) / n_seg)
     return {
         "metric": METRIC, "value": tokens / total_s, "unit": "decode tokens/s",
         "n_gpus": 1, "steps": n_seg, "warmup": 0, "ms_per_step": sum(seg_ms) / n_seg,
@@ -319,9 +432,78 @@ def run_decode(args):
                    "head_dim": D, "prompt": cfg["N"], "decode_steps": T * n_seg,
                    "compress_every": T, "window": W, "top_p": cfg["p"], "L_dense": cfg["L_dense"]},
         "decode_attn_hbm_frac_lower_bound": dec_bytes / total_s / 1e9 / HBM_PEAK_GBS,
+        "kernels": ktime, "roofline": roof,
         "segment_ms": seg_ms, "valid_kv_slots_per_segment": seg_tokens_kv, "mean_kept_per_head": kept,
         "status_flags": status, "gen_s": t_gen,
     }
+
+
+def copy_calibration():
+    """A plain 1 GiB device-to-device copy, three times: the reference the FETCH_SIZE and
+    WRITE_SIZE counters are scaled by (each copy reads and writes exactly 1 GiB)."""
+    a = torch.empty(1 << 28, dtype=torch.float32, device="cuda").fill_(1.0)
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    return {"copy_calibration_bytes": a.numel() * 4, "copies": 3}
+
+
+def _pmc_mean(run_dir, counter, match):
+    """Mean per-dispatch value (KiB) of one counter over the dispatches of kernels whose
+    name contains `match`, from a rocprofv3 --pmc output directory."""
+    import csv
+    import glob
+    vals = []
+    for f in glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True):
+        for row in csv.DictReader(open(f)):
+            if row["Counter_Name"] == counter and match in row["Kernel_Name"]:
+                vals.append(float(row["Counter_Value"]))
+    if not vals:
+        raise SystemExit(f"no {counter} dispatches of '{match}' under {run_dir}")
+    return sum(vals) / len(vals), len(vals)
+
+
+KERNEL_SYMBOL = {"score_pass1": "score_pass1_kernel", "score_pass2": "score_pass2_kernel",
+                 "compact_gather": "compact_gather_kernel", "decode_split": "decode_split_kernel"}
+
+
+def summarize_pmc(a):
+    """Write profiles/traffic_<kernel>_<workload>.txt from four rocprofv3 --pmc runs: the
+    benchmark with FETCH_SIZE, with WRITE_SIZE, and the copy calibration with each."""
+    fetch_dir, write_dir, cal_fetch_dir, cal_write_dir = a.summarize_pmc
+    sym = KERNEL_SYMBOL[a.kernel]
+    cal_bytes = float(1 << 30)
+    cf, _ = _pmc_mean(cal_fetch_dir, "FETCH_SIZE", "copyBuffer")
+    cw, _ = _pmc_mean(cal_write_dir, "WRITE_SIZE", "copyBuffer")
+    f_scale, w_scale = cal_bytes / (cf * 1024), cal_bytes / (cw * 1024)
+    kf, nf = _pmc_mean(fetch_dir, "FETCH_SIZE", sym)
+    kw, nw = _pmc_mean(write_dir, "WRITE_SIZE", sym)
+    hbm = kf * 1024 * f_scale + kw * 1024 * w_scale
+    sha = _source_sha(a.kernel)
+    path = os.path.join(ROOT, "profiles", f"traffic_{a.kernel}_{a.workload}.txt")
+    with open(path, "w") as f:
+        f.write(f"# HBM traffic of {sym} on workload {a.workload}, per dispatch\n")
+        f.write(f"# made by: {a.command}\n")
+        f.write("# FETCH_SIZE and WRITE_SIZE are KiB per dispatch; each is scaled by what the same\n")
+        f.write("# counter reads for a plain 1 GiB device copy (__amd_rocclr_copyBuffer).\n")
+        f.write(f"kernel: {sym}\n")
+        f.write(f"workload: {a.workload}\n")
+        f.write(f"dispatches_fetch: {nf}\n")
+        f.write(f"dispatches_write: {nw}\n")
+        f.write(f"fetch_size_kib_per_dispatch: {kf:.1f}\n")
+        f.write(f"write_size_kib_per_dispatch: {kw:.1f}\n")
+        f.write(f"copy_fetch_kib_per_GiB: {cf:.1f}\n")
+        f.write(f"copy_write_kib_per_GiB: {cw:.1f}\n")
+        f.write(f"fetch_scale: {f_scale:.4f}\n")
+        f.write(f"write_scale: {w_scale:.4f}\n")
+        f.write(f"hbm_read_bytes_per_launch: {kf * 1024 * f_scale:.0f}\n")
+        f.write(f"hbm_write_bytes_per_launch: {kw * 1024 * w_scale:.0f}\n")
+        f.write(f"hbm_bytes_per_launch: {hbm:.0f}\n")
+        f.write(f"source: paper_2606_28831_amd/csrc/{KERNEL_SOURCE[a.kernel]} + hk_internal.h\n")
+        f.write(f"source_sha256: {sha}\n")
+    return {"traffic_summary": path, "hbm_bytes_per_launch": hbm}
 
 
 def main():
@@ -332,7 +514,18 @@ def main():
     ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run the 1 GiB plain copy the byte counters are scaled by")
+    ap.add_argument("--summarize-pmc", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "CAL_FETCH_DIR",
+                                                          "CAL_WRITE_DIR"),
+                    help="write a profiles/traffic_*.txt summary from rocprofv3 --pmc outputs")
+    ap.add_argument("--kernel", default="compact_gather", choices=sorted(KERNEL_SYMBOL))
+    ap.add_argument("--workload", default=None)
+    ap.add_argument("--command", default="", help="the profiling command, recorded in the summary")
     args = ap.parse_args()
+    if args.summarize_pmc:
+        print(json.dumps(summarize_pmc(args)), flush=True)
+        return
     args.steps_given = args.steps is not None
     if args.steps is None:
         args.steps = 20
@@ -344,6 +537,9 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
+    if args.copy_calibration:
+        print(json.dumps(copy_calibration()), flush=True)
+        return
     out = run_decode(args) if args.config == 5 else run_compression(args)
     print(json.dumps(out), flush=True)
 

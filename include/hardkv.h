@@ -236,6 +236,33 @@ hk_status hk_append_kv(const hk_dims* dims, const hk_paged_kv* kv, const void* k
                        const void* v_new, const hk_allocator* alloc, int32_t* status,
                        void* workspace, size_t ws_bytes, hipStream_t stream);
 
+/* ------------------------------------------------------------------ kernel timing
+ * Optional HIP-event timing of individual kernels, for measurement harnesses (not part of
+ * the method).  hk_timing_enable(mask) selects the kernels to time: bit k of mask stands
+ * for kernel id k below (0 turns timing off, the default).  Every launch of a selected
+ * kernel is then bracketed by two events recorded on its launch stream.  hk_timing_read
+ * waits for the events of one kernel, returns their summed duration (ms) and the number
+ * of timed launches since the previous read, and clears them.  Events are recycled
+ * between reads.  Thread-safe.  Errors: HK_ERR_ARG for an unknown kernel id or a null
+ * output, HK_ERR_HIP if an event could not be read (the sum then omits it).
+ */
+enum {
+  HK_TK_SCORE_PASS1 = 0,   /* hk_score: LSE pass over the window                        */
+  HK_TK_SCORE_MERGE = 1,   /* hk_score: chunk partials -> row LSE                        */
+  HK_TK_SCORE_PASS2 = 2,   /* hk_score: attention-mass (and redundancy) pass             */
+  HK_TK_CALIBRATE = 3,     /* hk_calibrate                                               */
+  HK_TK_TOPP = 4,          /* hk_topp_select                                             */
+  HK_TK_SOLVE_T = 5,       /* hk_calibrate_solve_T                                       */
+  HK_TK_COMPACT_GATHER = 6,/* hk_compact: condensed-row gather into fresh pages          */
+  HK_TK_COMPACT_META = 7,  /* hk_compact: plan, alloc, table, push (four launches)       */
+  HK_TK_DECODE_SPLIT = 8,  /* hk_decode_attn: split-K partial states                     */
+  HK_TK_DECODE_MERGE = 9,  /* hk_decode_attn: merge of the partial states                */
+  HK_TK_APPEND = 10,       /* hk_append_kv: count + write, timed together                */
+  HK_TK_COUNT = 11
+};
+hk_status hk_timing_enable(uint32_t kernel_mask);
+hk_status hk_timing_read(int32_t kernel, double* total_ms, int64_t* launches);
+
 #ifdef __cplusplus
 }
 #endif

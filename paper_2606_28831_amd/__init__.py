@@ -16,7 +16,8 @@ import torch
 __all__ = ["HardKVError", "lib", "PagedKV", "Allocator", "hk_score", "hk_calibrate",
            "hk_calibrate_solve_T", "hk_topp_select", "hk_compact", "hk_decode_attn",
            "hk_append_kv", "hk_workspace_size", "hk_status_string", "OP_SCORE", "OP_COMPACT",
-           "OP_DECODE", "OP_APPEND", "FLAG_NOSPACE", "FLAG_NAN", "FLAG_RANGE", "LIB_PATH"]
+           "OP_DECODE", "OP_APPEND", "FLAG_NOSPACE", "FLAG_NAN", "FLAG_RANGE", "LIB_PATH",
+           "hk_timing_enable", "hk_timing_read", "TIMED_KERNELS"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhardkv.so")
 
@@ -24,7 +25,11 @@ HK_F32, HK_BF16 = 0, 1
 OP_SCORE, OP_COMPACT, OP_DECODE, OP_APPEND = 0, 1, 2, 3
 FLAG_NOSPACE, FLAG_NAN, FLAG_RANGE = 1, 2, 4
 EXPORTED = ["hk_score", "hk_calibrate", "hk_calibrate_solve_T", "hk_topp_select", "hk_compact",
-            "hk_decode_attn", "hk_append_kv", "hk_workspace_size", "hk_status_string"]
+            "hk_decode_attn", "hk_append_kv", "hk_workspace_size", "hk_status_string",
+            "hk_timing_enable", "hk_timing_read"]
+# kernel ids of hk_timing_read, in header order
+TIMED_KERNELS = ["score_pass1", "score_merge", "score_pass2", "calibrate", "topp", "solve_T",
+                 "compact_gather", "compact_meta", "decode_split", "decode_merge", "append"]
 
 
 class HardKVError(RuntimeError):
@@ -81,6 +86,10 @@ def lib():
         L.hk_append_kv.restype = I32
         L.hk_append_kv.argtypes = [C.POINTER(hk_dims), C.POINTER(hk_paged_kv), P, P,
                                    C.POINTER(hk_allocator), P, P, SZ, P]
+        L.hk_timing_enable.restype = I32
+        L.hk_timing_enable.argtypes = [C.c_uint32]
+        L.hk_timing_read.restype = I32
+        L.hk_timing_read.argtypes = [I32, C.POINTER(C.c_double), C.POINTER(C.c_int64)]
         _lib = L
     return _lib
 
@@ -210,3 +219,21 @@ def hk_append_kv(d: hk_dims, kv: PagedKV, k_new, v_new, alloc: Allocator, status
     _check(lib().hk_append_kv(C.byref(d), C.byref(kv.desc), _ptr(k_new), _ptr(v_new),
                               C.byref(alloc.desc), _ptr(status), _ptr(ws),
                               ws.numel() if ws is not None else 0, _stream(stream)), "hk_append_kv")
+
+
+def hk_timing_enable(kernels=None):
+    """Time the launches of the named kernels (all of them for kernels=None; [] turns
+    timing off)."""
+    names = TIMED_KERNELS if kernels is None else kernels
+    mask = 0
+    for k in names:
+        mask |= 1 << TIMED_KERNELS.index(k)
+    _check(lib().hk_timing_enable(mask), "hk_timing_enable")
+
+
+def hk_timing_read(kernel: str):
+    """(summed ms, launches) of one timed kernel since the previous read; clears them."""
+    ms, n = C.c_double(0.0), C.c_int64(0)
+    _check(lib().hk_timing_read(TIMED_KERNELS.index(kernel), C.byref(ms), C.byref(n)),
+           "hk_timing_read")
+    return ms.value, n.value

@@ -397,10 +397,16 @@ hipError_t hk_launch_compact(int n_heads, int D, const hk_paged_kv* kv, const ui
                              void* ws, hipStream_t st) {
   const CompactWs w = carve(ws, n_heads, kv->max_pages);
   const int mp = kv->max_pages;
-  hipLaunchKernelGGL(compact_plan_kernel, dim3(n_heads), dim3(CP_NT), 0, st, kv->n_pages,
-                     kv->page_mask, sel_bits, mp, L_dense, L_sparse, w);
-  hipLaunchKernelGGL(compact_alloc_kernel, dim3(1), dim3(AL_NT), 0, st, n_heads, alloc->free_top,
-                     status, w);
+  {
+    TimedLaunch t(HK_TK_COMPACT_META, st);
+    hipLaunchKernelGGL(compact_plan_kernel, dim3(n_heads), dim3(CP_NT), 0, st, kv->n_pages,
+                       kv->page_mask, sel_bits, mp, L_dense, L_sparse, w);
+  }
+  {
+    TimedLaunch t(HK_TK_COMPACT_META, st);
+    hipLaunchKernelGGL(compact_alloc_kernel, dim3(1), dim3(AL_NT), 0, st, n_heads, alloc->free_top,
+                       status, w);
+  }
   const int row_bytes = D * (kv->dtype == HK_BF16 ? 2 : 4);
   dim3 gg((mp + 3) / 4, n_heads);
   char* kp = static_cast<char*>(kv->k_pool);
@@ -410,18 +416,27 @@ hipError_t hk_launch_compact(int n_heads, int D, const hk_paged_kv* kv, const ui
 #else
 #define HK_GATHER_K compact_gather_kernel
 #endif
+  {
+  TimedLaunch t(HK_TK_COMPACT_GATHER, st);
   switch (row_bytes) {
     case 128: hipLaunchKernelGGL((HK_GATHER_K<128>), gg, dim3(256), 0, st, kp, vp, kv->page_table, kv->page_mask, sel_bits, alloc->free_ids, mp, w); break;
     case 256: hipLaunchKernelGGL((HK_GATHER_K<256>), gg, dim3(256), 0, st, kp, vp, kv->page_table, kv->page_mask, sel_bits, alloc->free_ids, mp, w); break;
     default: hipLaunchKernelGGL((HK_GATHER_K<512>), gg, dim3(256), 0, st, kp, vp, kv->page_table, kv->page_mask, sel_bits, alloc->free_ids, mp, w); break;
   }
+  }
   const size_t lds = (size_t)mp * (sizeof(int32_t) + sizeof(uint16_t));
   if (lds > 65536)
     (void)hipFuncSetAttribute(reinterpret_cast<const void*>(compact_table_kernel),
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  hipLaunchKernelGGL(compact_table_kernel, dim3(n_heads), dim3(CP_NT), lds, st, kv->page_table,
-                     kv->page_mask, kv->n_pages, sel_bits, alloc->free_ids, mp, w);
-  hipLaunchKernelGGL(compact_push_kernel, dim3(256), dim3(256), 0, st, alloc->free_ids,
-                     alloc->free_top, w);
+  {
+    TimedLaunch t(HK_TK_COMPACT_META, st);
+    hipLaunchKernelGGL(compact_table_kernel, dim3(n_heads), dim3(CP_NT), lds, st, kv->page_table,
+                       kv->page_mask, kv->n_pages, sel_bits, alloc->free_ids, mp, w);
+  }
+  {
+    TimedLaunch t(HK_TK_COMPACT_META, st);
+    hipLaunchKernelGGL(compact_push_kernel, dim3(256), dim3(256), 0, st, alloc->free_ids,
+                       alloc->free_top, w);
+  }
   return hipGetLastError();
 }

@@ -226,25 +226,59 @@ __global__ __launch_bounds__(DEC_NT) void decode_split_kernel(
   }
 }
 
-// one workgroup per KV head merges the split states of all its G query heads (App. F)
+// One workgroup per KV head merges the split states of its G query heads (App. F).  A
+// 32-lane group per query head finds the running maximum and the rescaled sum over the
+// splits; then each (query head, dim) thread sums its rescaled outputs with independent
+// loads.  Any number of splits.
 template <int D>
 __global__ __launch_bounds__(256) void decode_merge_kernel(const float* __restrict__ part, int n_split,
                                                            int G, int Hq, int Hkv, float* __restrict__ o,
                                                            float* __restrict__ lse) {
+  __shared__ float s_M[8], s_L[8];
   const int h = blockIdx.x, s = h / Hkv, kv = h % Hkv;
+  const size_t stride = (size_t)G * (D + 2);
+  const float* base = part + (size_t)h * n_split * stride;
+  {
+    const int g = threadIdx.x >> 5, l32 = threadIdx.x & 31;
+    float M = -INFINITY, L = 0.f;
+    if (g < G) {
+      for (int i = l32; i < n_split; i += 32) M = fmaxf(M, base[i * stride + g * (D + 2) + D]);
+    }
+#pragma unroll
+    for (int x = 1; x < 32; x <<= 1) M = fmaxf(M, __shfl_xor(M, x, 32));
+    if (g < G && M != -INFINITY) {
+      for (int i = l32; i < n_split; i += 32) {
+        const float* p = base + i * stride + g * (D + 2);
+        L += p[D + 1] * exp2f(p[D] - M);
+      }
+    }
+#pragma unroll
+    for (int x = 1; x < 32; x <<= 1) L += __shfl_xor(L, x, 32);
+    if (g < G && l32 == 0) {
+      s_M[g] = M;
+      s_L[g] = L;
+    }
+  }
+  __syncthreads();
   for (int idx = threadIdx.x; idx < G * D; idx += blockDim.x) {
     const int g = idx / D, d = idx % D;
-    const float* p = part + ((size_t)h * n_split * G + g) * (D + 2);
-    const size_t stride = (size_t)G * (D + 2);
-    float M = -INFINITY;
-    for (int i = 0; i < n_split; ++i) M = fmaxf(M, p[i * stride + D]);
-    float L = 0.f, O = 0.f;
-    if (M != -INFINITY)
-      for (int i = 0; i < n_split; ++i) {
-        const float a = exp2f(p[i * stride + D] - M);
-        L += p[i * stride + D + 1] * a;
-        O += p[i * stride + d] * a;
+    const float M = s_M[g], L = s_L[g];
+    const float* p = base + g * (D + 2);
+    float O0 = 0.f, O1 = 0.f, O2 = 0.f, O3 = 0.f;
+    if (M != -INFINITY) {
+      int i = 0;
+      for (; i + 4 <= n_split; i += 4) {
+        const float* q0 = p + i * stride;
+        const float m0 = q0[D], m1 = q0[stride + D], m2 = q0[2 * stride + D], m3 = q0[3 * stride + D];
+        const float v0 = q0[d], v1 = q0[stride + d], v2 = q0[2 * stride + d], v3 = q0[3 * stride + d];
+        O0 = fmaf(v0, exp2f(m0 - M), O0);
+        O1 = fmaf(v1, exp2f(m1 - M), O1);
+        O2 = fmaf(v2, exp2f(m2 - M), O2);
+        O3 = fmaf(v3, exp2f(m3 - M), O3);
       }
+      for (; i < n_split; ++i) O0 = fmaf(p[i * stride + d], exp2f(p[i * stride + D] - M), O0);
+    }
+    const float O = (O0 + O1) + (O2 + O3);
     const size_t row = (size_t)s * Hq + kv * G + g;
     o[row * D + d] = (L > 0.f) ? O / L : 0.f;
     if (d == 0) lse[row] = (L > 0.f) ? (M + __log2f(L)) * kLn2 : -INFINITY;
@@ -421,11 +455,15 @@ hipError_t hk_launch_decode(int NS, int Hq, int Hkv, int D, const void* q, const
   dim3 grid(n_split, n_heads);
   const bool bf = kv->dtype == HK_BF16;
   bool ok;
+  {
+  TimedLaunch t(HK_TK_DECODE_SPLIT, st);
   if (bf && D == 128) ok = launch_split_g<uint16_t, 128>(G, grid, st, q, kv, Hq, Hkv, c2, part, n_split);
   else if (bf) ok = launch_split_g<uint16_t, 64>(G, grid, st, q, kv, Hq, Hkv, c2, part, n_split);
   else if (D == 128) ok = launch_split_g<float, 128>(G, grid, st, q, kv, Hq, Hkv, c2, part, n_split);
   else ok = launch_split_g<float, 64>(G, grid, st, q, kv, Hq, Hkv, c2, part, n_split);
+  }
   if (!ok) return hipErrorInvalidValue;
+  TimedLaunch t(HK_TK_DECODE_MERGE, st);
   if (D == 128)
     hipLaunchKernelGGL(decode_merge_kernel<128>, dim3(n_heads), dim3(256), 0, st, part, n_split, G,
                        Hq, Hkv, o, lse);
@@ -450,6 +488,7 @@ hipError_t hk_launch_append(int NS, int Hkv, int D, const hk_paged_kv* kv, const
   const char* kn = static_cast<const char*>(k_new);
   const char* vn = static_cast<const char*>(v_new);
   int32_t* w = static_cast<int32_t*>(ws);
+  TimedLaunch t(HK_TK_APPEND, st);
   hipLaunchKernelGGL(append_count_kernel, dim3(nblk), dim3(64), 0, st, n_heads, kv->n_pages,
                      kv->page_mask, kv->max_pages, alloc->free_top, w);
 #define HK_APPEND_WRITE(RB)                                                                       \

@@ -112,6 +112,21 @@ __device__ __forceinline__ bool is_cand(const uint16_t* mask_row, int cand_len, 
 
 __device__ __forceinline__ int dense_pages(int L_dense) { return (L_dense + HK_PAGE - 1) / HK_PAGE; }
 
+// Records HIP events around one kernel launch on its stream while kernel timing is on
+// (hk_timing_enable); construct right before the launch, let it go out of scope after.
+class TimedLaunch {
+ public:
+  TimedLaunch(int kernel, hipStream_t st);
+  ~TimedLaunch();
+  TimedLaunch(const TimedLaunch&) = delete;
+  TimedLaunch& operator=(const TimedLaunch&) = delete;
+
+ private:
+  int kernel_;
+  hipStream_t st_;
+  bool active_;
+};
+
 }  // namespace hk
 
 // ---------------------------------------------------------------- launchers

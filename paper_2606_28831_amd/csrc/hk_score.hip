@@ -730,12 +730,18 @@ hipError_t launch_score_q(const hk_score_args& a, hipStream_t st) {
   if (!lse_use) {
     const size_t lds1 = pass1_lds(R_pad, D, sizeof(T));
     allow_lds(score_pass1_kernel<T, D, QB>, lds1);
-    hipLaunchKernelGGL((score_pass1_kernel<T, D, QB>), grid, dim3(SCORE_NT), lds1, st,
-                       static_cast<const T*>(a.q_obs), static_cast<const T*>(kv->k_pool),
-                       kv->page_table, kv->page_mask, kv->n_pages, a.NS, a.Hq, a.Hkv, a.W,
-                       kv->max_pages, c2, part, n_chunks);
-    hipLaunchKernelGGL(score_lse_merge_kernel, dim3(n_heads), dim3(256), 0, st, part, n_chunks,
-                       R_pad, a.NS, a.Hq, a.Hkv, a.W, c2, a.sm_scale, lse_buf);
+    {
+      TimedLaunch t(HK_TK_SCORE_PASS1, st);
+      hipLaunchKernelGGL((score_pass1_kernel<T, D, QB>), grid, dim3(SCORE_NT), lds1, st,
+                         static_cast<const T*>(a.q_obs), static_cast<const T*>(kv->k_pool),
+                         kv->page_table, kv->page_mask, kv->n_pages, a.NS, a.Hq, a.Hkv, a.W,
+                         kv->max_pages, c2, part, n_chunks);
+    }
+    {
+      TimedLaunch t(HK_TK_SCORE_MERGE, st);
+      hipLaunchKernelGGL(score_lse_merge_kernel, dim3(n_heads), dim3(256), 0, st, part, n_chunks,
+                         R_pad, a.NS, a.Hq, a.Hkv, a.W, c2, a.sm_scale, lse_buf);
+    }
     lse_use = lse_buf;
   } else if (a.row_lse_out && a.row_lse_out != a.row_lse_in) {
     (void)hipMemcpyAsync(a.row_lse_out, a.row_lse_in, sizeof(float) * (size_t)a.W * a.NS * a.Hq,
@@ -743,6 +749,7 @@ hipError_t launch_score_q(const hk_score_args& a, hipStream_t st) {
   }
   const float lnR = logf((float)(a.Hq / a.Hkv * a.W));
   const size_t lds2 = pass2_lds(R_pad, D, sizeof(T), a.x_red != nullptr);
+  TimedLaunch t(HK_TK_SCORE_PASS2, st);
   if (a.x_red) {
     allow_lds(score_pass2_kernel<T, D, QB, true>, lds2);
     hipLaunchKernelGGL((score_pass2_kernel<T, D, QB, true>), grid, dim3(SCORE_NT), lds2, st,

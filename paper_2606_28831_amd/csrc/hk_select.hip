@@ -342,6 +342,7 @@ hipError_t hk_launch_calibrate(int n_heads, int S_max, const int32_t* cand_len, 
                                int n_metrics, const float* x0, const float* x1, const float* T0,
                                const float* T1, float w0, float w1, float* c_out, float* lse_out,
                                hipStream_t st) {
+  TimedLaunch t(HK_TK_CALIBRATE, st);
   HK_EPT_SWITCH(S_max, hipLaunchKernelGGL((calibrate_kernel<E>), dim3(n_heads), dim3(SEL_NT), 0, st,
                                           S_max, cand_len, mask, n_metrics, x0, x1, T0, T1, w0, w1,
                                           c_out, lse_out));
@@ -351,6 +352,7 @@ hipError_t hk_launch_calibrate(int n_heads, int S_max, const int32_t* cand_len, 
 hipError_t hk_launch_topp(int n_heads, int S_max, const int32_t* cand_len, const uint16_t* mask,
                           const float* c, int p_q, int k_min, int k_max, uint32_t* sel_bits,
                           int32_t* k_out, float* sel_mass, int32_t* status, hipStream_t st) {
+  TimedLaunch t(HK_TK_TOPP, st);
   HK_EPT_SWITCH(S_max, hipLaunchKernelGGL((topp_kernel<E>), dim3(n_heads), dim3(SEL_NT), 0, st, S_max,
                                           cand_len, mask, c, p_q, k_min, k_max, sel_bits, k_out,
                                           sel_mass, status));
@@ -360,6 +362,7 @@ hipError_t hk_launch_topp(int n_heads, int S_max, const int32_t* cand_len, const
 hipError_t hk_launch_solve_T(int n_heads, int S_max, const int32_t* cand_len, const uint16_t* mask,
                              const float* x, const int32_t* k, const float* target, float T_lo,
                              float T_hi, int iters, float* T_out, hipStream_t st) {
+  TimedLaunch t(HK_TK_SOLVE_T, st);
   HK_EPT_SWITCH(S_max, hipLaunchKernelGGL((solve_T_kernel<E>), dim3(n_heads), dim3(SEL_NT), 0, st,
                                           S_max, cand_len, mask, x, k, target, T_lo, T_hi, iters,
                                           T_out));

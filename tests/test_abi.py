@@ -92,3 +92,18 @@ def test_validation_errors_without_gpu(hk):
     assert L.hk_append_kv(C.byref(d), C.byref(kv), None, P, C.byref(alloc), P, None, 0, None) == 1
     kvnull = hk.hk_paged_kv(None, P, P, P, P, 64, 4, 1)
     assert L.hk_decode_attn(C.byref(d), P, C.byref(kvnull), 0.1, P, P, P, 1 << 30, None) == 1
+
+
+def test_kernel_timing_host_side(hk):
+    """Timing off by default: nothing recorded, reads are empty; bad ids are rejected."""
+    L = C.CDLL(hk.LIB_PATH)
+    ms, n = C.c_double(1.0), C.c_int64(7)
+    for k in range(len(hk.TIMED_KERNELS)):
+        assert L.hk_timing_read(k, C.byref(ms), C.byref(n)) == 0
+        assert ms.value == 0.0 and n.value == 0
+    assert L.hk_timing_read(len(hk.TIMED_KERNELS), C.byref(ms), C.byref(n)) == 1
+    assert L.hk_timing_read(-1, C.byref(ms), C.byref(n)) == 1
+    assert L.hk_timing_read(0, None, C.byref(n)) == 1
+    assert L.hk_timing_enable(C.c_uint32(0xFFFFFFFF)) == 0 and L.hk_timing_enable(C.c_uint32(0)) == 0
+    text = open(HEADER).read()
+    assert int(re.search(r"HK_TK_COUNT = (\d+)", text).group(1)) == len(hk.TIMED_KERNELS)

@@ -151,6 +151,9 @@ __device__ __forceinline__ void stage_rows(char* lds, int R, int R_pad, RowFn ro
 #ifndef HK_SCORE_PREFETCH
 #define HK_SCORE_PREFETCH 0
 #endif
+#ifndef HK_SCORE_P2_REVERSE
+#define HK_SCORE_P2_REVERSE 0
+#endif
 #ifndef HK_SCORE_WPE
 #define HK_SCORE_WPE 0
 #endif
@@ -219,24 +222,30 @@ __device__ __forceinline__ void mma_chains(const F* kf, const char* lds, int blk
 template <typename F>
 using lds_frag_t = decltype(F::lds(nullptr, 0, 0, 0));
 
-template <int N_VALU>
+// Maximum of MFMA results.  fmaxf must quiet signalling NaNs first, which costs one
+// canonicalising v_max per operand that the compiler cannot prove canonical (every MFMA
+// result); the NaN-propagating maximum (v_maximum3_f32 on gfx950) needs none.  A NaN
+// score propagates either way, through the exponential sum.
+__device__ __forceinline__ float vmax(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+
+template <int N_MFMA, int N_VALU>
 __device__ __forceinline__ void sched_step() {
-  __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);        // one MFMA
+  __builtin_amdgcn_sched_group_barrier(0x008, N_MFMA, 0);   // MFMA
   __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);        // one LDS read
   __builtin_amdgcn_sched_group_barrier(0x002, N_VALU, 0);   // VALU work
 }
 
-// pass 2: returns this lane's partial column sum  sum_r exp2(c2*z[r][key] - lse2[r])
-template <typename F, int QB>
-__device__ __forceinline__ float p2_tile_pipelined(const F& kf, const char* qlds, const float* lse2,
-                                                   float c2, int lane) {
+// pass 2: adds to col[t] this lane's partial column sum  sum_r exp2(c2*z[r][key] - lse2[r])
+// for each of the KT key tiles; every Q fragment read from LDS feeds KT MFMAs.
+template <typename F, int QB, int KT>
+__device__ __forceinline__ void p2_tile_pipelined(const F* kf, const char* qlds, const float* lse2,
+                                                  float c2, int lane, float* col) {
   constexpr int KS = F::KSTEPS;
   constexpr int NF = QB * KS;
   lds_frag_t<F> qf[3];
   qf[0] = F::lds(qlds, 0, 0, lane);
   if constexpr (NF > 1) qf[1] = F::lds(qlds, 1 / KS, 1 % KS, lane);
-  f32x16 acc[2];
-  float col = 0.f;
+  f32x16 acc[2][KT];
 #pragma unroll
   for (int qb = 0; qb <= QB; ++qb) {
     f32x4 l4[4];
@@ -245,74 +254,93 @@ __device__ __forceinline__ float p2_tile_pipelined(const F& kf, const char* qlds
       for (int r4 = 0; r4 < 4; ++r4)
         l4[r4] = *reinterpret_cast<const f32x4*>(lse2 + (qb - 1) * 32 + 8 * r4 + 4 * (lane >> 5));
     }
-    if (qb < QB) acc[qb & 1] = f32x16{};
+    if (qb < QB) {
+#pragma unroll
+      for (int t = 0; t < KT; ++t) acc[qb & 1][t] = f32x16{};
+    }
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) {
       const int g = qb * KS + kk;
       if (qb < QB) {
-        acc[qb & 1] = F::mma(qf[g % 3], kf.v[kk], acc[qb & 1]);
+#pragma unroll
+        for (int t = 0; t < KT; ++t) acc[qb & 1][t] = F::mma(qf[g % 3], kf[t].v[kk], acc[qb & 1][t]);
         if (g + 2 < NF) qf[(g + 2) % 3] = F::lds(qlds, (g + 2) / KS, (g + 2) % KS, lane);
       }
       if (qb >= 1) {
 #pragma unroll
         for (int e = 0; e < 16; ++e)
-          if (e * KS / 16 == kk) col += fast_exp2(fmaf(acc[(qb - 1) & 1][e], c2, -l4[e >> 2][e & 3]));
+          if (e * KS / 16 == kk) {
+#pragma unroll
+            for (int t = 0; t < KT; ++t)
+              col[t] += fast_exp2(fmaf(acc[(qb - 1) & 1][t][e], c2, -l4[e >> 2][e & 3]));
+          }
       }
     }
     if constexpr (sizeof(lds_frag_t<F>) == 16) {
       if (qb >= 1 && qb < QB) {
 #pragma unroll
-        for (int kk = 0; kk < KS; ++kk) sched_step<3 * 16 / KS>();
+        for (int kk = 0; kk < KS; ++kk) sched_step<KT, 3 * 16 * KT / KS>();
       }
     }
   }
-  return col;
 }
 
-// pass 1: online (max, sum exp2) update of the lane's query column for every block
-template <typename F, int QB>
-__device__ __forceinline__ void p1_tile_pipelined(const F& kf, const char* qlds, float c2, int lane,
+// pass 1: online (max, sum exp2) update of the lane's query column for every block, over
+// KT key tiles; every Q fragment read from LDS feeds KT MFMAs.
+template <typename F, int QB, int KT>
+__device__ __forceinline__ void p1_tile_pipelined(const F* kf, const char* qlds, float c2, int lane,
                                                   float* M, float* L) {
   constexpr int KS = F::KSTEPS;
   constexpr int NF = QB * KS;
   lds_frag_t<F> qf[3];
   qf[0] = F::lds(qlds, 0, 0, lane);
   if constexpr (NF > 1) qf[1] = F::lds(qlds, 1 / KS, 1 % KS, lane);
-  f32x16 acc[2];
+  f32x16 acc[2][KT];
 #pragma unroll
   for (int qb = 0; qb <= QB; ++qb) {
     if (qb < QB) {
-      acc[qb & 1] = f32x16{};
+#pragma unroll
+      for (int t = 0; t < KT; ++t) acc[qb & 1][t] = f32x16{};
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) {
         const int g = qb * KS + kk;
-        acc[qb & 1] = F::mma(kf.v[kk], qf[g % 3], acc[qb & 1]);
+#pragma unroll
+        for (int t = 0; t < KT; ++t) acc[qb & 1][t] = F::mma(kf[t].v[kk], qf[g % 3], acc[qb & 1][t]);
         if (g + 2 < NF) qf[(g + 2) % 3] = F::lds(qlds, (g + 2) / KS, (g + 2) % KS, lane);
       }
     }
     if (qb >= 1) {
-      const f32x16& a = acc[(qb - 1) & 1];
-      float m0 = fmaxf(a[0], a[1]), m1 = fmaxf(a[2], a[3]), m2 = fmaxf(a[4], a[5]), m3 = fmaxf(a[6], a[7]);
-      m0 = fmaxf(m0, fmaxf(a[8], a[9]));
-      m1 = fmaxf(m1, fmaxf(a[10], a[11]));
-      m2 = fmaxf(m2, fmaxf(a[12], a[13]));
-      m3 = fmaxf(m3, fmaxf(a[14], a[15]));
-      const float m = fmaxf(fmaxf(m0, m1), fmaxf(m2, m3));
-      const float mn = fmaxf(M[qb - 1], m);
-      const float mc = mn * c2;
-      float s0 = 0.f, s1 = 0.f;
+      const f32x16* a = acc[(qb - 1) & 1];
+      // maximum over the KT * 16 values, three at a time
+      float mt[KT];
 #pragma unroll
-      for (int r = 0; r < 16; r += 2) {
-        s0 += fast_exp2(fmaf(a[r], c2, -mc));
-        s1 += fast_exp2(fmaf(a[r + 1], c2, -mc));
+      for (int t = 0; t < KT; ++t) {
+        float m0 = vmax(vmax(a[t][0], a[t][1]), a[t][2]), m1 = vmax(vmax(a[t][3], a[t][4]), a[t][5]);
+        float m2 = vmax(vmax(a[t][6], a[t][7]), a[t][8]), m3 = vmax(vmax(a[t][9], a[t][10]), a[t][11]);
+        float m4 = vmax(vmax(a[t][12], a[t][13]), a[t][14]);
+        m0 = vmax(vmax(m0, m1), m2);
+        m3 = vmax(vmax(m3, m4), a[t][15]);
+        mt[t] = vmax(m0, m3);
       }
+      float mn = M[qb - 1];
+#pragma unroll
+      for (int t = 0; t < KT; ++t) mn = vmax(mn, mt[t]);
+      const float mc = mn * c2;
+      float s0 = fast_exp2(fmaf(a[0][0], c2, -mc)), s1 = fast_exp2(fmaf(a[0][1], c2, -mc));
+#pragma unroll
+      for (int t = 0; t < KT; ++t)
+#pragma unroll
+        for (int r = (t == 0 ? 2 : 0); r < 16; r += 2) {
+          s0 += fast_exp2(fmaf(a[t][r], c2, -mc));
+          s1 += fast_exp2(fmaf(a[t][r + 1], c2, -mc));
+        }
       L[qb - 1] = fmaf(L[qb - 1], fast_exp2((M[qb - 1] - mn) * c2), s0 + s1);
       M[qb - 1] = mn;
     }
     if constexpr (sizeof(lds_frag_t<F>) == 16) {
       if (qb >= 1 && qb < QB) {
 #pragma unroll
-        for (int kk = 0; kk < KS; ++kk) sched_step<(16 * 3 + 22) / KS>();
+        for (int kk = 0; kk < KS; ++kk) sched_step<KT, (16 * 3 * KT + 22) / KS>();
       }
     }
   }
@@ -411,8 +439,8 @@ __global__ HK_SCORE_ATTR void score_pass1_kernel(
       all_full = all_full && (tm[t] == 0xffffffffu);
       any = any || (tm[t] != 0u);
     }
-    if (all_full && SCORE_KT == 1 && HK_SCORE_PIPE) {
-      p1_tile_pipelined<F, QB>(kf[0], smem, c2, lane, M, L);
+    if (all_full && HK_SCORE_PIPE) {
+      p1_tile_pipelined<F, QB, SCORE_KT>(kf, smem, c2, lane, M, L);
     } else if (all_full) {
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) {
@@ -422,8 +450,8 @@ __global__ HK_SCORE_ATTR void score_pass1_kernel(
 #pragma unroll
         for (int t = 0; t < SCORE_KT; ++t)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) m = fmaxf(m, acc[t][r]);
-        const float mn = fmaxf(M[qb], m);
+          for (int r = 0; r < 16; ++r) m = vmax(m, acc[t][r]);
+        const float mn = vmax(M[qb], m);
         const float mc = mn * c2;
         float sum = 0.f;
 #pragma unroll
@@ -446,8 +474,8 @@ __global__ HK_SCORE_ATTR void score_pass1_kernel(
         for (int t = 0; t < SCORE_KT; ++t)
 #pragma unroll
           for (int r = 0; r < 16; ++r)
-            if ((rows[t] >> r) & 1u) m = fmaxf(m, acc[t][r]);
-        const float mn = fmaxf(M[qb], m);
+            if ((rows[t] >> r) & 1u) m = vmax(m, acc[t][r]);
+        const float mn = vmax(M[qb], m);
         if (mn != -INFINITY) {           // this column has seen a valid key
           const float mc = mn * c2;
           float sum = 0.f;
@@ -510,8 +538,19 @@ __global__ __launch_bounds__(256) void score_lse_merge_kernel(const float2* __re
 }
 
 // ------------------------------------------------------------------ pass 2
+// Waves per SIMD the register allocator must leave room for: 4 lets two 512-thread
+// workgroups share a CU; asked only where it fits without spilling.
 template <typename T, int D, int QB, bool RED>
-__global__ HK_SCORE_ATTR void score_pass2_kernel(
+constexpr int pass2_min_waves() {
+  if (HK_SCORE_WPE > 0) return HK_SCORE_WPE;
+  if (HK_SCORE_KT > 1) return 1;
+  return (sizeof(T) == 2 && D == 128 && (QB == 7 || (QB == 4 && !RED))) ? 4 : 1;
+}
+
+template <typename T, int D, int QB, bool RED>
+__global__ __launch_bounds__(SCORE_NT) __attribute__((amdgpu_waves_per_eu(
+    pass2_min_waves<T, D, QB, RED>(), pass2_min_waves<T, D, QB, RED>() > 1 ? pass2_min_waves<T, D, QB, RED>() : 8)))
+void score_pass2_kernel(
     const T* __restrict__ q_obs, const T* __restrict__ k_pool, const int32_t* __restrict__ table,
     const uint16_t* __restrict__ masks, const int32_t* __restrict__ n_pages_arr, int NS, int Hq,
     int Hkv, int W, int max_pages, int L_dense, float c2, float lnR,
@@ -520,7 +559,11 @@ __global__ HK_SCORE_ATTR void score_pass2_kernel(
   using F = Frag<T, D>;
   constexpr int R_pad = 32 * QB;
   extern __shared__ __align__(16) char smem[];
+#if HK_SCORE_P2_REVERSE
+  const int h = gridDim.y - 1 - blockIdx.y, chunk = blockIdx.x;
+#else
   const int h = blockIdx.y, chunk = blockIdx.x;
+#endif
   const int s = h / Hkv, kv = h % Hkv, G = Hq / Hkv;
   const int R = G * W;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -633,8 +676,8 @@ __global__ HK_SCORE_ATTR void score_pass2_kernel(
     float col[SCORE_KT];
 #pragma unroll
     for (int t = 0; t < SCORE_KT; ++t) col[t] = 0.f;
-    if (any && SCORE_KT == 1 && HK_SCORE_PIPE) {
-      col[0] = p2_tile_pipelined<F, QB>(kf[0], smem, lse2, c2, lane);
+    if (any && HK_SCORE_PIPE) {
+      p2_tile_pipelined<F, QB, SCORE_KT>(kf, smem, lse2, c2, lane, col);
     } else if (any) {
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) {

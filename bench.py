@@ -145,7 +145,7 @@ def run_compression(args):
     metric = "attn+red" if cfg.get("n_ref") else "attn"
     comp = Compressor(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"], cfg["W"], kv, alloc, cfg["p"],
                       L_dense=cfg["L_dense"], L_sparse=cfg["L_sparse"], metric=metric,
-                      n_ref=cfg.get("n_ref", 0))
+                      n_ref=cfg.get("n_ref", 0), keep_c=False)
     pristine = WL.clone_state(w)
     ref = w.ref_slots
     tokens = _cand_tokens(w, cfg["L_dense"])
@@ -381,7 +381,7 @@ def run_decode(args):
     t_gen = time.perf_counter() - t_gen
     kv = hk.PagedKV(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)
     alloc = hk.Allocator(w.free_ids, w.free_top)
-    loop = DecodeLoop(L, B, Hq, Hkv, D, W, kv, alloc, cfg["p"], cfg["L_dense"])
+    loop = DecodeLoop(L, B, Hq, Hkv, D, W, kv, alloc, cfg["p"], cfg["L_dense"], keep_c=False)
     NS = L * B
     dt = WL.TORCH_DTYPE[cfg["dtype"]]
     seg_ms, seg_tokens_kv, kept = [], [], []

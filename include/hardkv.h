@@ -7,6 +7,7 @@
  *   hk_calibrate      Logits Calibration into one probability space (Sec. 3.2, Solution 2)
  *   hk_calibrate_solve_T  per-head temperature for Problem 1 (App. D.1, binary search)
  *   hk_topp_select    head-adaptive Top-p budget (Sec. 3.2, Problem 1)
+ *   hk_calibrate_topp hk_calibrate followed by hk_topp_select in one launch
  *   hk_compact        Cascade-Cache rewrite into dense / sparse / condensed tiers
  *                     (Sec. 3.1 Step 3; Sec. 3.3.1 Rewrite Cache and Sparse Loading)
  *   hk_decode_attn    paged decode attention over the variable-budget cache with the
@@ -177,6 +178,20 @@ hk_status hk_topp_select(int32_t n_heads, int32_t S_max, const int32_t* cand_len
                          int32_t k_min, int32_t k_max, uint32_t* sel_bits, int32_t* k_out,
                          float* sel_mass_out, int32_t* status, hipStream_t stream);
 
+/* ------------------------------------------------------------------ a2 + a3 fused
+ * hk_calibrate followed by hk_topp_select on its output, in one launch: the calibrated
+ * values stay on chip, and c_out, lse_out, sel_bits, k_out and sel_mass_out receive
+ * exactly what the two separate calls would write (same arithmetic, bit for bit).
+ * c_out and lse_out may be NULL (then nothing is written there); sel_mass_out and status
+ * may be NULL.  Arguments and limits as for hk_calibrate and hk_topp_select.
+ */
+hk_status hk_calibrate_topp(int32_t n_heads, int32_t S_max, const int32_t* cand_len,
+                            const uint16_t* page_mask, int32_t n_metrics,
+                            const float* const* x, const float* const* T, const float* w,
+                            double p, int32_t k_min, int32_t k_max, float* c_out,
+                            float* lse_out, uint32_t* sel_bits, int32_t* k_out,
+                            float* sel_mass_out, int32_t* status, hipStream_t stream);
+
 /* ------------------------------------------------------------------ a2': temperature
  * Temperature of Problem 1 (Sec. 3.2) by bisection (App. D.1, binary search on T):
  *   f(T) = M_k(Softmax(x / T)) - target_mass[h], M_k = mass of the Top-k set of x
@@ -258,7 +273,8 @@ enum {
   HK_TK_DECODE_SPLIT = 8,  /* hk_decode_attn: split-K partial states                     */
   HK_TK_DECODE_MERGE = 9,  /* hk_decode_attn: merge of the partial states                */
   HK_TK_APPEND = 10,       /* hk_append_kv: count + write, timed together                */
-  HK_TK_COUNT = 11
+  HK_TK_CALIB_TOPP = 11,   /* hk_calibrate_topp                                          */
+  HK_TK_COUNT = 12
 };
 hk_status hk_timing_enable(uint32_t kernel_mask);
 hk_status hk_timing_read(int32_t kernel, double* total_ms, int64_t* launches);

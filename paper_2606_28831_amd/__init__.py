@@ -17,7 +17,7 @@ __all__ = ["HardKVError", "lib", "PagedKV", "Allocator", "hk_score", "hk_calibra
            "hk_calibrate_solve_T", "hk_topp_select", "hk_compact", "hk_decode_attn",
            "hk_append_kv", "hk_workspace_size", "hk_status_string", "OP_SCORE", "OP_COMPACT",
            "OP_DECODE", "OP_APPEND", "FLAG_NOSPACE", "FLAG_NAN", "FLAG_RANGE", "LIB_PATH",
-           "hk_timing_enable", "hk_timing_read", "TIMED_KERNELS"]
+           "hk_timing_enable", "hk_timing_read", "TIMED_KERNELS", "hk_calibrate_topp"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhardkv.so")
 
@@ -26,10 +26,11 @@ OP_SCORE, OP_COMPACT, OP_DECODE, OP_APPEND = 0, 1, 2, 3
 FLAG_NOSPACE, FLAG_NAN, FLAG_RANGE = 1, 2, 4
 EXPORTED = ["hk_score", "hk_calibrate", "hk_calibrate_solve_T", "hk_topp_select", "hk_compact",
             "hk_decode_attn", "hk_append_kv", "hk_workspace_size", "hk_status_string",
-            "hk_timing_enable", "hk_timing_read"]
+            "hk_timing_enable", "hk_timing_read", "hk_calibrate_topp"]
 # kernel ids of hk_timing_read, in header order
 TIMED_KERNELS = ["score_pass1", "score_merge", "score_pass2", "calibrate", "topp", "solve_T",
-                 "compact_gather", "compact_meta", "decode_split", "decode_merge", "append"]
+                 "compact_gather", "compact_meta", "decode_split", "decode_merge", "append",
+                 "calib_topp"]
 
 
 class HardKVError(RuntimeError):
@@ -86,6 +87,10 @@ def lib():
         L.hk_append_kv.restype = I32
         L.hk_append_kv.argtypes = [C.POINTER(hk_dims), C.POINTER(hk_paged_kv), P, P,
                                    C.POINTER(hk_allocator), P, P, SZ, P]
+        L.hk_calibrate_topp.restype = I32
+        L.hk_calibrate_topp.argtypes = [I32, I32, P, P, I32, C.POINTER(C.c_void_p),
+                                        C.POINTER(C.c_void_p), C.POINTER(C.c_float), D, I32, I32,
+                                        P, P, P, P, P, P, P]
         L.hk_timing_enable.restype = I32
         L.hk_timing_enable.argtypes = [C.c_uint32]
         L.hk_timing_read.restype = I32
@@ -192,6 +197,21 @@ def hk_topp_select(n_heads: int, S_max: int, cand_len, page_mask, c, p: float, s
     _check(lib().hk_topp_select(int(n_heads), int(S_max), _ptr(cand_len), _ptr(page_mask), _ptr(c),
                                 float(p), int(k_min), int(k_max), _ptr(sel_bits), _ptr(k_out),
                                 _ptr(sel_mass), _ptr(status), _stream(stream)), "hk_topp_select")
+
+
+def hk_calibrate_topp(n_heads: int, S_max: int, cand_len, page_mask, xs, Ts, weights, p: float,
+                      sel_bits, k_out, c_out=None, lse_out=None, k_min: int = 1, k_max: int = 0,
+                      sel_mass=None, status=None, stream=None):
+    m = len(xs)
+    xa = (C.c_void_p * m)(*[t.data_ptr() for t in xs])
+    Ta = None
+    if Ts is not None:
+        Ta = (C.c_void_p * m)(*[(t.data_ptr() if t is not None else None) for t in Ts])
+    wa = (C.c_float * m)(*[float(w) for w in weights])
+    _check(lib().hk_calibrate_topp(int(n_heads), int(S_max), _ptr(cand_len), _ptr(page_mask), m,
+                                   xa, Ta, wa, float(p), int(k_min), int(k_max), _ptr(c_out),
+                                   _ptr(lse_out), _ptr(sel_bits), _ptr(k_out), _ptr(sel_mass),
+                                   _ptr(status), _stream(stream)), "hk_calibrate_topp")
 
 
 def hk_calibrate_solve_T(n_heads: int, S_max: int, cand_len, page_mask, x, k, target_mass, T_out,

@@ -154,6 +154,28 @@ hk_status hk_topp_select(int32_t n_heads, int32_t S_max, const int32_t* cand_len
                                  sel_bits, k_out, sel_mass_out, status, stream));
 }
 
+hk_status hk_calibrate_topp(int32_t n_heads, int32_t S_max, const int32_t* cand_len,
+                            const uint16_t* page_mask, int32_t n_metrics, const float* const* x,
+                            const float* const* T, const float* w, double p, int32_t k_min,
+                            int32_t k_max, float* c_out, float* lse_out, uint32_t* sel_bits,
+                            int32_t* k_out, float* sel_mass_out, int32_t* status,
+                            hipStream_t stream) {
+  hk_status e = check_rows(n_heads, S_max, cand_len);
+  if (e) return e;
+  if (n_metrics < 1 || n_metrics > 2 || !x || !w || !sel_bits || !k_out) return HK_ERR_ARG;
+  for (int m = 0; m < n_metrics; ++m)
+    if (!x[m] || !std::isfinite(w[m])) return HK_ERR_ARG;
+  if (!(p >= 0.0 && p <= 1.0)) return HK_ERR_ARG;
+  if (!aligned16(sel_bits)) return HK_ERR_ALIGN;
+  const int p_q = (int)std::nearbyint(p * 1e6);
+  const float* T0 = T ? T[0] : nullptr;
+  const float* T1 = (T && n_metrics > 1) ? T[1] : nullptr;
+  return launched(hk_launch_calib_topp(n_heads, S_max, cand_len, page_mask, n_metrics, x[0],
+                                       n_metrics > 1 ? x[1] : nullptr, T0, T1, w[0],
+                                       n_metrics > 1 ? w[1] : 0.f, p_q, k_min, k_max, c_out,
+                                       lse_out, sel_bits, k_out, sel_mass_out, status, stream));
+}
+
 hk_status hk_calibrate_solve_T(int32_t n_heads, int32_t S_max, const int32_t* cand_len,
                                const uint16_t* page_mask, const float* x, const int32_t* k,
                                const float* target_mass, float T_lo, float T_hi, int32_t iters,

@@ -29,25 +29,57 @@ __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_lo
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
+// Wave-wide reductions on DPP lane moves (no LDS round trip): pairs within quads, the
+// two halves of each 8-lane group, of each 16-lane row, then rows 0->1, 2->3 and 1->2,3
+// by row broadcasts; lane 63 ends with the total, which is read back as a scalar so every
+// lane returns it.  `id` is the identity filled into the rows a broadcast does not reach.
+template <int CTRL, int ROW_MASK = 0xf>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v, uint32_t id) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)id, (int)v, CTRL, ROW_MASK, 0xf, false);
+}
+template <typename Op>
+__device__ __forceinline__ uint32_t wave_reduce_u32(uint32_t v, uint32_t id, Op op) {
+  v = op(v, dpp_u32<0xb1>(v, id));          // quad_perm [1,0,3,2]
+  v = op(v, dpp_u32<0x4e>(v, id));          // quad_perm [2,3,0,1]
+  v = op(v, dpp_u32<0x141>(v, id));         // row_half_mirror
+  v = op(v, dpp_u32<0x140>(v, id));         // row_mirror
+  v = op(v, dpp_u32<0x142, 0xa>(v, id));    // row_bcast:15
+  v = op(v, dpp_u32<0x143, 0xc>(v, id));    // row_bcast:31
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
+}
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
+  return __uint_as_float(wave_reduce_u32(__float_as_uint(v), 0xff800000u, [](uint32_t a, uint32_t b) {
+    return __float_as_uint(fmaxf(__uint_as_float(a), __uint_as_float(b)));
+  }));
 }
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
+  return __uint_as_float(wave_reduce_u32(__float_as_uint(v), 0u, [](uint32_t a, uint32_t b) {
+    return __float_as_uint(__uint_as_float(a) + __uint_as_float(b));
+  }));
 }
 __device__ __forceinline__ int wave_sum_i(int v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
+  return (int)wave_reduce_u32((uint32_t)v, 0u, [](uint32_t a, uint32_t b) { return a + b; });
 }
 __device__ __forceinline__ unsigned long long wave_sum_u64(unsigned long long v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
+  uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
+#define HK_U64_STEP(CTRL, RM)                                                                     \
+  {                                                                                               \
+    const unsigned long long t = ((unsigned long long)dpp_u32<CTRL, RM>(hi, 0u) << 32) |          \
+                                 dpp_u32<CTRL, RM>(lo, 0u);                                       \
+    const unsigned long long r = (((unsigned long long)hi << 32) | lo) + t;                       \
+    lo = (uint32_t)r;                                                                             \
+    hi = (uint32_t)(r >> 32);                                                                     \
+  }
+  HK_U64_STEP(0xb1, 0xf)
+  HK_U64_STEP(0x4e, 0xf)
+  HK_U64_STEP(0x141, 0xf)
+  HK_U64_STEP(0x140, 0xf)
+  HK_U64_STEP(0x142, 0xa)
+  HK_U64_STEP(0x143, 0xc)
+#undef HK_U64_STEP
+  lo = (uint32_t)__builtin_amdgcn_readlane((int)lo, 63);
+  hi = (uint32_t)__builtin_amdgcn_readlane((int)hi, 63);
+  return ((unsigned long long)hi << 32) | lo;
 }
 
 // Block-wide reductions for blockDim.x = NT threads (multiple of 64).  `red` is LDS
@@ -157,6 +189,11 @@ hipError_t hk_launch_calibrate(int n_heads, int S_max, const int32_t* cand_len,
 hipError_t hk_launch_topp(int n_heads, int S_max, const int32_t* cand_len, const uint16_t* mask,
                           const float* c, int p_q, int k_min, int k_max, uint32_t* sel_bits,
                           int32_t* k_out, float* sel_mass, int32_t* status, hipStream_t st);
+hipError_t hk_launch_calib_topp(int n_heads, int S_max, const int32_t* cand_len, const uint16_t* mask,
+                                int n_metrics, const float* x0, const float* x1, const float* T0,
+                                const float* T1, float w0, float w1, int p_q, int k_min, int k_max,
+                                float* c_out, float* lse_out, uint32_t* sel_bits, int32_t* k_out,
+                                float* sel_mass, int32_t* status, hipStream_t st);
 hipError_t hk_launch_solve_T(int n_heads, int S_max, const int32_t* cand_len,
                              const uint16_t* mask, const float* x, const int32_t* k,
                              const float* target, float T_lo, float T_hi, int iters,

@@ -13,7 +13,60 @@ constexpr int SEL_NW = SEL_NT / 64;
 constexpr unsigned long long kMassOne = 1ull << 40;   // fixed-point unit of the Top-p mass
 
 // ------------------------------------------------------------------ a2: calibrate
-// c = sum_m w_m Softmax(x_m / T_m) over the candidates (Solution 2, Sec. 3.2).
+// c = sum_m w_m Softmax(x_m / T_m) over the candidates (Solution 2, Sec. 3.2), for the
+// thread's EPT slots; the fused select kernel runs the same code, so both paths produce
+// identical values.
+template <int EPT>
+__device__ __forceinline__ void calib_values(int h, int S_max, uint32_t cbits, int n_metrics,
+                                             const float* __restrict__ x0, const float* __restrict__ x1,
+                                             const float* __restrict__ T0, const float* __restrict__ T1,
+                                             float w0, float w1, float* __restrict__ lse_out, float* red,
+                                             float* c) {
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) c[i] = 0.f;
+  for (int m = 0; m < n_metrics; ++m) {
+    const float* x = (m == 0 ? x0 : x1) + (size_t)h * S_max;
+    const float* Tp = (m == 0 ? T0 : T1);
+    const float T = Tp ? Tp[h] : 1.0f;
+    const float wm = (m == 0 ? w0 : w1);
+    // x / T is recomputed from memory (cache-resident) in each of the three sweeps
+    // rather than kept: EPT more registers would spill next to c
+    float mx = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < EPT; ++i)
+      if ((cbits >> i) & 1u) mx = fmaxf(mx, x[tid + SEL_NT * i] / T);
+    mx = block_max<SEL_NT>(mx, red);
+    float lse = -INFINITY;
+    if (mx != -INFINITY) {
+      float sm = 0.f;
+#pragma unroll
+      for (int i = 0; i < EPT; ++i)
+        if ((cbits >> i) & 1u) sm += expf(x[tid + SEL_NT * i] / T - mx);
+      sm = block_sum<SEL_NT>(sm, red);
+      lse = mx + logf(sm);
+#pragma unroll
+      for (int i = 0; i < EPT; ++i)
+        if ((cbits >> i) & 1u) c[i] = fmaf(wm, expf(x[tid + SEL_NT * i] / T - lse), c[i]);
+    }
+    if (lse_out && tid == 0) lse_out[(size_t)h * n_metrics + m] = lse;
+  }
+}
+
+template <int EPT>
+__device__ __forceinline__ uint32_t cand_bits(int h, int S_max, const int32_t* __restrict__ cand_len,
+                                              const uint16_t* __restrict__ mask) {
+  const int cl = cand_len[h];
+  const uint16_t* mrow = mask ? mask + (size_t)h * (S_max / HK_PAGE) : nullptr;
+  uint32_t cbits = 0;
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) {
+    const int j = threadIdx.x + SEL_NT * i;
+    if (j < S_max && is_cand(mrow, cl, j)) cbits |= 1u << i;
+  }
+  return cbits;
+}
+
 template <int EPT>
 __global__ __launch_bounds__(SEL_NT) void calibrate_kernel(
     int S_max, const int32_t* __restrict__ cand_len, const uint16_t* __restrict__ mask, int n_metrics,
@@ -22,45 +75,9 @@ __global__ __launch_bounds__(SEL_NT) void calibrate_kernel(
     float* __restrict__ lse_out) {
   __shared__ float red[SEL_NW];
   const int h = blockIdx.x, tid = threadIdx.x;
-  const int cl = cand_len[h];
-  const uint16_t* mrow = mask ? mask + (size_t)h * (S_max / HK_PAGE) : nullptr;
-  uint32_t cbits = 0;
-#pragma unroll
-  for (int i = 0; i < EPT; ++i) {
-    const int j = tid + SEL_NT * i;
-    if (j < S_max && is_cand(mrow, cl, j)) cbits |= 1u << i;
-  }
+  const uint32_t cbits = cand_bits<EPT>(h, S_max, cand_len, mask);
   float c[EPT];
-#pragma unroll
-  for (int i = 0; i < EPT; ++i) c[i] = 0.f;
-  for (int m = 0; m < n_metrics; ++m) {
-    const float* x = (m == 0 ? x0 : x1) + (size_t)h * S_max;
-    const float* Tp = (m == 0 ? T0 : T1);
-    const float T = Tp ? Tp[h] : 1.0f;
-    const float wm = (m == 0 ? w0 : w1);
-    float y[EPT];
-    float mx = -INFINITY;
-#pragma unroll
-    for (int i = 0; i < EPT; ++i) {
-      y[i] = -INFINITY;
-      if ((cbits >> i) & 1u) y[i] = x[tid + SEL_NT * i] / T;
-      mx = fmaxf(mx, y[i]);
-    }
-    mx = block_max<SEL_NT>(mx, red);
-    float lse = -INFINITY;
-    if (mx != -INFINITY) {
-      float sm = 0.f;
-#pragma unroll
-      for (int i = 0; i < EPT; ++i)
-        if ((cbits >> i) & 1u) sm += expf(y[i] - mx);
-      sm = block_sum<SEL_NT>(sm, red);
-      lse = mx + logf(sm);
-#pragma unroll
-      for (int i = 0; i < EPT; ++i)
-        if ((cbits >> i) & 1u) c[i] = fmaf(wm, expf(y[i] - lse), c[i]);
-    }
-    if (lse_out && tid == 0) lse_out[(size_t)h * n_metrics + m] = lse;
-  }
+  calib_values<EPT>(h, S_max, cbits, n_metrics, x0, x1, T0, T1, w0, w1, lse_out, red, c);
 #pragma unroll
   for (int i = 0; i < EPT; ++i) {
     const int j = tid + SEL_NT * i;
@@ -68,19 +85,31 @@ __global__ __launch_bounds__(SEL_NT) void calibrate_kernel(
   }
 }
 
+// Fixed-point weight of a Top-p value v in [0, 1] given by its bits: floor(v * 2^40).
+// The product is exact in fp32 (a power-of-two scale) and keeps at most 24 significant
+// bits, so the truncated float is that integer exactly; a thread's sum of up to 32 of
+// them stays below 2^46 and is exact in fp64.
+__device__ __forceinline__ float fixed_weight(uint32_t key) {
+  return truncf(__uint_as_float(key) * (float)kMassOne);
+}
+
 // Threshold searches run most-significant bit first: the answer v is the largest key
 // with mass(key >= v) >= target (or count(key >= v) >= k); both are monotone in v.
-template <int EPT>
-__device__ __forceinline__ unsigned long long mass_ge(const uint32_t* key, const unsigned long long* w,
-                                                      uint32_t cbits, uint32_t t) {
-  unsigned long long m = 0;
+// (The empty asm keeps the compiler from hoisting the EPT weights out of a search loop
+// into registers of their own, which would spill.)
+template <int EPT, typename K>
+__device__ __forceinline__ unsigned long long mass_ge(const K& key, uint32_t cbits, uint32_t t) {
+  double m = 0.0;
 #pragma unroll
-  for (int i = 0; i < EPT; ++i)
-    if (((cbits >> i) & 1u) && key[i] >= t) m += w[i];
-  return m;
+  for (int i = 0; i < EPT; ++i) {
+    uint32_t k = key[i];
+    asm volatile("" : "+v"(k));
+    if (((cbits >> i) & 1u) && k >= t) m += (double)fixed_weight(k);
+  }
+  return (unsigned long long)m;
 }
-template <int EPT>
-__device__ __forceinline__ int count_ge(const uint32_t* key, uint32_t cbits, uint32_t t) {
+template <int EPT, typename K>
+__device__ __forceinline__ int count_ge(const K& key, uint32_t cbits, uint32_t t) {
   int n = 0;
 #pragma unroll
   for (int i = 0; i < EPT; ++i) n += (((cbits >> i) & 1u) && key[i] >= t) ? 1 : 0;
@@ -92,20 +121,22 @@ __device__ __forceinline__ int count_ge(const uint32_t* key, uint32_t cbits, uin
 template <int EPT>
 __device__ uint32_t take_top_ties(uint32_t tie, int take, int* cnt /* LDS [EPT][SEL_NW] */) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  unsigned long long bal[EPT];
 #pragma unroll
   for (int i = 0; i < EPT; ++i) {
-    bal[i] = __ballot((tie >> i) & 1u);
-    if (lane == 0) cnt[i * SEL_NW + wave] = __popcll(bal[i]);
+    const unsigned long long b = __ballot((tie >> i) & 1u);
+    if (lane == 0) cnt[i * SEL_NW + wave] = __popcll(b);
   }
   __syncthreads();
   uint32_t out = 0;
-  // ties with a larger slot index: later rows, later waves of this row, higher lanes
+  // ties with a larger slot index: later rows, later waves of this row, higher lanes (the
+  // ballots are taken again rather than kept: EPT 64-bit registers would spill)
   int above_rows = 0;
+#pragma unroll
   for (int i = EPT - 1; i >= 0; --i) {
     int above = above_rows;
     for (int w = wave + 1; w < SEL_NW; ++w) above += cnt[i * SEL_NW + w];
-    const unsigned long long hi = (lane == 63) ? 0ull : (bal[i] >> (lane + 1));
+    const unsigned long long b = __ballot((tie >> i) & 1u);
+    const unsigned long long hi = (lane == 63) ? 0ull : (b >> (lane + 1));
     above += __popcll(hi);
     if (((tie >> i) & 1u) && above < take) out |= 1u << i;
     int row = 0;
@@ -116,50 +147,102 @@ __device__ uint32_t take_top_ties(uint32_t tie, int take, int* cnt /* LDS [EPT][
 }
 
 // ------------------------------------------------------------------ a3: Top-p
-template <int EPT>
-__global__ __launch_bounds__(SEL_NT) void topp_kernel(
-    int S_max, const int32_t* __restrict__ cand_len, const uint16_t* __restrict__ mask,
-    const float* __restrict__ c, int p_q, int k_min, int k_max, uint32_t* __restrict__ sel_bits,
-    int32_t* __restrict__ k_out, float* __restrict__ sel_mass, int32_t* __restrict__ status) {
-  __shared__ unsigned long long red64[SEL_NW];
-  __shared__ int redi[SEL_NW];
-  __shared__ int tiecnt[EPT * SEL_NW];
-  const int h = blockIdx.x, tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
-  const int cl = cand_len[h];
-  const uint16_t* mrow = mask ? mask + (size_t)h * (S_max / HK_PAGE) : nullptr;
-  const float* crow = c + (size_t)h * S_max;
+// Exclusive prefix (thread order) of one int per thread (.x) and the block sum (.y).
+__device__ __forceinline__ int2 block_exscan_int(int v, int* red) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  __syncthreads();
+  if (lane == 63) red[wave] = x;
+  __syncthreads();
+  int before = 0, all = 0;
+#pragma unroll
+  for (int w = 0; w < SEL_NW; ++w) {
+    if (w < wave) before += red[w];
+    all += red[w];
+  }
+  return make_int2(before + x - v, all);
+}
 
-  uint32_t cbits = 0, key[EPT];
-  unsigned long long w[EPT];
+// Below the bits all candidates share, SEL_COARSE bits are searched with every candidate
+// in registers; the candidates that still share the prefix found are then packed into LDS
+// (`list`, room for S_max keys) and the remaining low bits are searched over that list.
+constexpr int SEL_COARSE = 9;
+
+template <bool MAX>
+__device__ __forceinline__ uint32_t block_minmax_u32(uint32_t v, int* red) {
+  v = wave_reduce_u32(v, MAX ? 0u : 0xffffffffu,
+                      [](uint32_t a, uint32_t b) { return MAX ? (a > b ? a : b) : (a < b ? a : b); });
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  __syncthreads();
+  if (l == 0) red[w] = (int)v;
+  __syncthreads();
+  uint32_t r = (uint32_t)red[0];
+#pragma unroll
+  for (int i = 1; i < SEL_NW; ++i) r = MAX ? max(r, (uint32_t)red[i]) : min(r, (uint32_t)red[i]);
+  return r;
+}
+__device__ __forceinline__ uint32_t block_min_u32(uint32_t v, int* red) { return block_minmax_u32<false>(v, red); }
+__device__ __forceinline__ uint32_t block_max_u32(uint32_t v, int* red) { return block_minmax_u32<true>(v, red); }
+
+// Block-uniform values (results of block reductions) moved to scalar registers, so the
+// 64-bit divisions of the mass rule run on the scalar unit.
+__device__ __forceinline__ unsigned long long uniform_u64(unsigned long long x) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(x >> 32));
+  return ((unsigned long long)hi << 32) | lo;
+}
+
+struct SelLds {
+  unsigned long long red64[SEL_NW];
+  int redi[SEL_NW];
+};
+
+// Head-adaptive Top-p (Sec. 3.3) on the thread's EPT values: the smallest set whose
+// fixed-point mass reaches ceil(p_q * Total / 10^6), ties at the threshold broken toward
+// the larger slot index; the count is clamped to [k_min, k_max].
+// Read-only view of a thread's values as ordering keys (their bit patterns).
+template <int EPT>
+struct KeyView {
+  const float* v;
+  __device__ __forceinline__ uint32_t operator[](int i) const { return __float_as_uint(v[i]); }
+};
+
+// `val` holds the thread's EPT values; they are clamped in place, and their bit patterns
+// (non-negative floats order as integers) are the ordering keys.
+template <int EPT>
+__device__ __forceinline__ void topp_core(float* val, uint32_t cbits, int p_q, int k_min, int k_max,
+                          uint32_t* __restrict__ brow, int S_max, int32_t* __restrict__ k_out,
+                          float* __restrict__ sel_mass, int32_t* __restrict__ status, int h,
+                          uint32_t* list, SelLds& sh, int* tiecnt) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int flags = 0;
 #pragma unroll
   for (int i = 0; i < EPT; ++i) {
-    const int j = tid + SEL_NT * i;
-    key[i] = 0;
-    w[i] = 0;
-    if (j < S_max && is_cand(mrow, cl, j)) {
-      cbits |= 1u << i;
-      float v = crow[j];
+    float v = val[i];
+    if ((cbits >> i) & 1u) {
       if (v != v) { v = 0.f; flags |= HK_FLAG_NAN; }
       if (v > 1.f) { v = 1.f; flags |= HK_FLAG_RANGE; }
       if (v < 0.f) { v = 0.f; flags |= HK_FLAG_RANGE; }
       if (v == 0.f) v = 0.f;                      // canonical +0
-      key[i] = __float_as_uint(v);                // non-negative floats order as integers
-      w[i] = (unsigned long long)(v * (float)kMassOne);   // exact scaling, truncation = floor
+    } else {
+      v = 0.f;
     }
+    val[i] = v;
   }
+  const KeyView<EPT> key{val};
   // __syncthreads_or returns a predicate, so each flag bit is reduced on its own
   const int any_nan = __syncthreads_or(flags & HK_FLAG_NAN);
   const int any_range = __syncthreads_or(flags & HK_FLAG_RANGE);
   flags = (any_nan ? HK_FLAG_NAN : 0) | (any_range ? HK_FLAG_RANGE : 0);
   if (tid == 0 && flags && status) atomicOr(status, flags);
 
-  const int n_cand = block_sum_int<SEL_NT>(__popc(cbits), redi);
-  unsigned long long tot = 0;
-#pragma unroll
-  for (int i = 0; i < EPT; ++i) tot += ((cbits >> i) & 1u) ? w[i] : 0ull;
-  tot = block_sum_u64<SEL_NT>(tot, red64);
+  const int n_cand = block_sum_int<SEL_NT>(__popc(cbits), sh.redi);
+  const unsigned long long tot = uniform_u64(block_sum_u64<SEL_NT>(mass_ge<EPT>(key, cbits, 0u), sh.red64));
   const unsigned long long pq = (unsigned long long)p_q;
   const unsigned long long target = pq * (tot / 1000000ull) + (pq * (tot % 1000000ull) + 999999ull) / 1000000ull;
 
@@ -168,15 +251,52 @@ __global__ __launch_bounds__(SEL_NT) void topp_kernel(
   uint32_t v = 0;
   int take = 0;
   if (target > 0) {
-    for (int b = 29; b >= 0; --b) {
+    // the bits above the first one where the candidates' keys differ are common to all of
+    // them, hence to v (a candidate's key): the search starts below them
+    uint32_t kmin = 0xffffffffu, kmax = 0u;
+#pragma unroll
+    for (int i = 0; i < EPT; ++i)
+      if ((cbits >> i) & 1u) {
+        kmin = min(kmin, key[i]);
+        kmax = max(kmax, key[i]);
+      }
+    kmin = block_min_u32(kmin, sh.redi);
+    kmax = block_max_u32(kmax, sh.redi);
+    const int top = (kmin == kmax) ? -1 : 31 - __clz(kmin ^ kmax);   // highest differing bit
+    v = (top < 0) ? kmin : (kmin & ~((2u << top) - 1u));
+    const int b_lo = max(top - SEL_COARSE + 1, 0);                      // last full-register bit
+    for (int b = top; b >= b_lo; --b) {
       const uint32_t t = v | (1u << b);
-      const unsigned long long m = block_sum_u64<SEL_NT>(mass_ge<EPT>(key, w, cbits, t), red64);
-      if (m >= target) v = t;
+      if (block_sum_u64<SEL_NT>(mass_ge<EPT>(key, cbits, t), sh.red64) >= target) v = t;
+    }
+    const int LB = b_lo;                           // low bits left for the packed list
+    const uint32_t hi_end = v + (1u << LB);        // keys >= hi_end: above the prefix
+    const unsigned long long above = uniform_u64(block_sum_u64<SEL_NT>(mass_ge<EPT>(key, cbits, hi_end), sh.red64));
+    uint32_t inb = 0;
+#pragma unroll
+    for (int i = 0; i < EPT; ++i)
+      if (((cbits >> i) & 1u) && key[i] >= v && key[i] < hi_end) inb |= 1u << i;
+    const int2 scan = block_exscan_int(__popc(inb), sh.redi);
+    const int n_list = scan.y;
+    int off = scan.x;
+#pragma unroll
+    for (int i = 0; i < EPT; ++i)
+      if ((inb >> i) & 1u) list[off++] = key[i];
+    __syncthreads();
+    for (int b = LB - 1; b >= 0; --b) {
+      const uint32_t t = v | (1u << b);
+      double m = 0.0;
+      for (int j = tid; j < n_list; j += SEL_NT) {
+        const uint32_t kj = list[j];
+        if (kj >= t) m += (double)fixed_weight(kj);
+      }
+      if (above + block_sum_u64<SEL_NT>((unsigned long long)m, sh.red64) >= target) v = t;
     }
     // v = value of the crossing element; elements above it are all taken
-    const int cnt_gt = block_sum_int<SEL_NT>(count_ge<EPT>(key, cbits, v + 1), redi);
-    const unsigned long long mass_gt = block_sum_u64<SEL_NT>(mass_ge<EPT>(key, w, cbits, v + 1), red64);
-    const unsigned long long wv = (unsigned long long)(__uint_as_float(v) * (float)kMassOne);
+    const int cnt_gt = block_sum_int<SEL_NT>(count_ge<EPT>(key, cbits, v + 1), sh.redi);
+    const unsigned long long mass_gt = uniform_u64(block_sum_u64<SEL_NT>(mass_ge<EPT>(key, cbits, v + 1), sh.red64));
+    v = __builtin_amdgcn_readfirstlane(v);
+    const unsigned long long wv = uniform_u64((unsigned long long)fixed_weight(v));
     take = wv ? (int)((target - mass_gt + wv - 1) / wv) : 0;   // wv > 0 whenever target > 0
     k = cnt_gt + take;
   }
@@ -191,9 +311,9 @@ __global__ __launch_bounds__(SEL_NT) void topp_kernel(
       v = 0;
       for (int b = 29; b >= 0; --b) {
         const uint32_t t = v | (1u << b);
-        if (block_sum_int<SEL_NT>(count_ge<EPT>(key, cbits, t), redi) >= kf) v = t;
+        if (block_sum_int<SEL_NT>(count_ge<EPT>(key, cbits, t), sh.redi) >= kf) v = t;
       }
-      const int cnt_gt = block_sum_int<SEL_NT>(count_ge<EPT>(key, cbits, v + 1), redi);
+      const int cnt_gt = block_sum_int<SEL_NT>(count_ge<EPT>(key, cbits, v + 1), sh.redi);
       take = kf - cnt_gt;
     }
   }
@@ -206,16 +326,16 @@ __global__ __launch_bounds__(SEL_NT) void topp_kernel(
       if (key[i] == v) tie |= 1u << i;
     }
   }
-  const int n_tie = block_sum_int<SEL_NT>(__popc(tie), redi);
+  const int n_tie = block_sum_int<SEL_NT>(__popc(tie), sh.redi);
   if (take >= n_tie) sel |= tie;
   else if (take > 0) sel |= take_top_ties<EPT>(tie, take, tiecnt);
 
-  unsigned long long msel = 0;
+  double msel_d = 0.0;
 #pragma unroll
-  for (int i = 0; i < EPT; ++i) msel += ((sel >> i) & 1u) ? w[i] : 0ull;
-  msel = block_sum_u64<SEL_NT>(msel, red64);
+  for (int i = 0; i < EPT; ++i)
+    if ((sel >> i) & 1u) msel_d += (double)fixed_weight(key[i]);
+  const unsigned long long msel = block_sum_u64<SEL_NT>((unsigned long long)msel_d, sh.red64);
 
-  uint32_t* brow = sel_bits + (size_t)h * (S_max / 32);
 #pragma unroll
   for (int i = 0; i < EPT; ++i) {
     const unsigned long long b = __ballot((sel >> i) & 1u);
@@ -229,6 +349,51 @@ __global__ __launch_bounds__(SEL_NT) void topp_kernel(
     k_out[h] = kf;
     if (sel_mass) sel_mass[h] = (float)((double)msel / (double)kMassOne);
   }
+}
+
+template <int EPT>
+__global__ __launch_bounds__(SEL_NT) void topp_kernel(
+    int S_max, const int32_t* __restrict__ cand_len, const uint16_t* __restrict__ mask,
+    const float* __restrict__ c, int p_q, int k_min, int k_max, uint32_t* __restrict__ sel_bits,
+    int32_t* __restrict__ k_out, float* __restrict__ sel_mass, int32_t* __restrict__ status) {
+  extern __shared__ uint32_t list[];
+  __shared__ SelLds sh;
+  __shared__ int tiecnt[EPT * SEL_NW];
+  const int h = blockIdx.x, tid = threadIdx.x;
+  const uint32_t cbits = cand_bits<EPT>(h, S_max, cand_len, mask);
+  const float* crow = c + (size_t)h * S_max;
+  float val[EPT];
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) val[i] = ((cbits >> i) & 1u) ? crow[tid + SEL_NT * i] : 0.f;
+  topp_core<EPT>(val, cbits, p_q, k_min, k_max, sel_bits + (size_t)h * (S_max / 32), S_max, k_out,
+                 sel_mass, status, h, list, sh, tiecnt);
+}
+
+// a2 + a3 in one launch: calibrate, then Top-p on the calibrated values in registers
+template <int EPT>
+__global__ __launch_bounds__(SEL_NT) void calib_topp_kernel(
+    int S_max, const int32_t* __restrict__ cand_len, const uint16_t* __restrict__ mask, int n_metrics,
+    const float* __restrict__ x0, const float* __restrict__ x1, const float* __restrict__ T0,
+    const float* __restrict__ T1, float w0, float w1, int p_q, int k_min, int k_max,
+    float* __restrict__ c_out, float* __restrict__ lse_out, uint32_t* __restrict__ sel_bits,
+    int32_t* __restrict__ k_out, float* __restrict__ sel_mass, int32_t* __restrict__ status) {
+  extern __shared__ uint32_t list[];
+  __shared__ SelLds sh;
+  __shared__ float red[SEL_NW];
+  __shared__ int tiecnt[EPT * SEL_NW];
+  const int h = blockIdx.x, tid = threadIdx.x;
+  const uint32_t cbits = cand_bits<EPT>(h, S_max, cand_len, mask);
+  float c[EPT];
+  calib_values<EPT>(h, S_max, cbits, n_metrics, x0, x1, T0, T1, w0, w1, lse_out, red, c);
+  if (c_out) {
+#pragma unroll
+    for (int i = 0; i < EPT; ++i) {
+      const int j = tid + SEL_NT * i;
+      if (j < S_max) c_out[(size_t)h * S_max + j] = c[i];
+    }
+  }
+  topp_core<EPT>(c, cbits, p_q, k_min, k_max, sel_bits + (size_t)h * (S_max / 32), S_max, k_out,
+                 sel_mass, status, h, list, sh, tiecnt);
 }
 
 // ------------------------------------------------------------------ a2': temperature
@@ -349,13 +514,40 @@ hipError_t hk_launch_calibrate(int n_heads, int S_max, const int32_t* cand_len, 
   return hipGetLastError();
 }
 
+// dynamic LDS of the Top-p kernels: the packed key list of the low-bit search
+template <typename K>
+static void sel_allow_lds(K kernel, size_t bytes) {
+  if (bytes > 65536)
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+}
+
 hipError_t hk_launch_topp(int n_heads, int S_max, const int32_t* cand_len, const uint16_t* mask,
                           const float* c, int p_q, int k_min, int k_max, uint32_t* sel_bits,
                           int32_t* k_out, float* sel_mass, int32_t* status, hipStream_t st) {
+  const size_t lds = (size_t)S_max * sizeof(uint32_t);
   TimedLaunch t(HK_TK_TOPP, st);
-  HK_EPT_SWITCH(S_max, hipLaunchKernelGGL((topp_kernel<E>), dim3(n_heads), dim3(SEL_NT), 0, st, S_max,
-                                          cand_len, mask, c, p_q, k_min, k_max, sel_bits, k_out,
-                                          sel_mass, status));
+  HK_EPT_SWITCH(S_max, {
+    sel_allow_lds(topp_kernel<E>, lds);
+    hipLaunchKernelGGL((topp_kernel<E>), dim3(n_heads), dim3(SEL_NT), lds, st, S_max, cand_len, mask,
+                       c, p_q, k_min, k_max, sel_bits, k_out, sel_mass, status);
+  });
+  return hipGetLastError();
+}
+
+hipError_t hk_launch_calib_topp(int n_heads, int S_max, const int32_t* cand_len, const uint16_t* mask,
+                                int n_metrics, const float* x0, const float* x1, const float* T0,
+                                const float* T1, float w0, float w1, int p_q, int k_min, int k_max,
+                                float* c_out, float* lse_out, uint32_t* sel_bits, int32_t* k_out,
+                                float* sel_mass, int32_t* status, hipStream_t st) {
+  const size_t lds = (size_t)S_max * sizeof(uint32_t);
+  TimedLaunch t(HK_TK_CALIB_TOPP, st);
+  HK_EPT_SWITCH(S_max, {
+    sel_allow_lds(calib_topp_kernel<E>, lds);
+    hipLaunchKernelGGL((calib_topp_kernel<E>), dim3(n_heads), dim3(SEL_NT), lds, st, S_max, cand_len,
+                       mask, n_metrics, x0, x1, T0, T1, w0, w1, p_q, k_min, k_max, c_out, lse_out,
+                       sel_bits, k_out, sel_mass, status);
+  });
   return hipGetLastError();
 }
 

@@ -12,8 +12,8 @@ from dataclasses import dataclass
 import torch
 
 from . import (Allocator, PagedKV, OP_APPEND, OP_COMPACT, OP_DECODE, OP_SCORE, dims, hk_append_kv,
-               hk_calibrate, hk_calibrate_solve_T, hk_compact, hk_decode_attn, hk_score,
-               hk_topp_select, workspace)
+               hk_calibrate_solve_T, hk_calibrate_topp, hk_compact, hk_decode_attn, hk_score,
+               workspace)
 
 
 @dataclass
@@ -41,15 +41,17 @@ class Compressor:
     metric "attn": attention mass over the window, calibrated with T = 1.
     metric "attn+red": attention mass and key redundancy, each calibrated (the
     redundancy temperature solved once per head, on the first call), mixed 0.5/0.5.
+    Calibration and Top-p run as one launch; keep_c=False leaves the calibrated
+    probabilities on chip (buf.c / buf.c_attn are then not written).
     """
 
     def __init__(self, NS, Hq, Hkv, D, W, kv: PagedKV, alloc: Allocator, p: float,
                  L_dense: int = 0, L_sparse: int = 0, metric: str = "attn", n_ref: int = 0,
-                 k_max: int = 0):
+                 k_max: int = 0, keep_c: bool = True):
         self.d = dims(NS, Hq, Hkv, D, W)
         self.kv, self.alloc, self.p = kv, alloc, p
         self.L_dense, self.L_sparse = L_dense, L_sparse
-        self.metric, self.n_ref, self.k_max = metric, n_ref, k_max
+        self.metric, self.n_ref, self.k_max, self.keep_c = metric, n_ref, k_max, keep_c
         self.sm_scale = 1.0 / math.sqrt(D)
         dev = kv.k_pool.device
         H = NS * Hkv
@@ -85,20 +87,20 @@ class Compressor:
     def select(self, stream=None):
         b, H, S, pm = self.buf, self.n_heads, self.S_max, self.kv.page_mask
         if self.metric == "attn":
-            hk_calibrate(H, S, b.cand_len, pm, [b.s_attn], None, [1.0], b.c, stream=stream)
+            xs, Ts, ws = [b.s_attn], None, [1.0]
         else:
             if b.T_red is None:
                 # temperature of the redundancy metric, solved at the first compression only
-                hk_calibrate(H, S, b.cand_len, pm, [b.s_attn], None, [1.0], b.c_attn, stream=stream)
-                hk_topp_select(H, S, b.cand_len, pm, b.c_attn, self.p, b.sel_bits, b.k_attn,
-                               sel_mass=b.mass_attn, status=b.status, stream=stream)
+                hk_calibrate_topp(H, S, b.cand_len, pm, [b.s_attn], None, [1.0], self.p, b.sel_bits,
+                                  b.k_attn, c_out=b.c_attn if self.keep_c else None,
+                                  sel_mass=b.mass_attn, status=b.status, stream=stream)
                 b.T_red = torch.empty(H, dtype=torch.float32, device=b.c.device)
                 hk_calibrate_solve_T(H, S, b.cand_len, pm, b.x_red, b.k_attn, b.mass_attn, b.T_red,
                                      stream=stream)
-            hk_calibrate(H, S, b.cand_len, pm, [b.s_attn, b.x_red], [None, b.T_red], [0.5, 0.5],
-                         b.c, stream=stream)
-        hk_topp_select(H, S, b.cand_len, pm, b.c, self.p, b.sel_bits, b.k, k_max=self.k_max,
-                       sel_mass=b.sel_mass, status=b.status, stream=stream)
+            xs, Ts, ws = [b.s_attn, b.x_red], [None, b.T_red], [0.5, 0.5]
+        hk_calibrate_topp(H, S, b.cand_len, pm, xs, Ts, ws, self.p, b.sel_bits, b.k,
+                          c_out=b.c if self.keep_c else None, k_max=self.k_max,
+                          sel_mass=b.sel_mass, status=b.status, stream=stream)
 
     def compact(self, stream=None):
         b = self.buf
@@ -143,7 +145,7 @@ class DecodeLoop:
     """
 
     def __init__(self, L, B, Hq, Hkv, D, W, kv: PagedKV, alloc: Allocator, p: float,
-                 L_dense: int, L_sparse: int = 0):
+                 L_dense: int, L_sparse: int = 0, keep_c: bool = True):
         self.L, self.B, self.Hq, self.Hkv, self.D, self.W = L, B, Hq, Hkv, D, W
         self.kv, self.alloc = kv, alloc
         self.NS = L * B
@@ -157,7 +159,7 @@ class DecodeLoop:
         self.status = torch.zeros(1, dtype=torch.int32, device=dev)
         self.o = torch.empty(self.NS, Hq, D, dtype=torch.float32, device=dev)
         self.comp = Compressor(self.NS, Hq, Hkv, D, W, kv, alloc, p, L_dense=L_dense,
-                               L_sparse=L_sparse, metric="attn")
+                               L_sparse=L_sparse, metric="attn", keep_c=keep_c)
 
     def step(self, q_t, k_t, v_t, lse_t, stream=None):
         hk_append_kv(self.d_all, self.kv, k_t, v_t, self.alloc, self.status, self.ws_app,

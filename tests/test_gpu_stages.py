@@ -202,17 +202,26 @@ def test_calibrate_and_topp(name):
         assert int(st.item()) == 0
 
 
-@pytest.mark.parametrize("kind", ["uniform", "ties", "onehot", "nan_range", "zeros", "clamp"])
-def test_topp_edge_cases(kind):
+@pytest.mark.parametrize("kind,S", [("uniform", 2048), ("ties", 2048), ("onehot", 2048),
+                                    ("nan_range", 2048), ("zeros", 2048), ("clamp", 2048),
+                                    ("crowded", 2048), ("crowded", 32768), ("spread", 32768),
+                                    ("uniform", 32768)])
+def test_topp_edge_cases(kind, S):
     import paper_2606_28831_amd as hk
-    H, S = 6, 2048
+    H = 6
     rng = np.random.default_rng(7)
     c = np.zeros((H, S), np.float32)
-    cand_len = np.array([S, 1000, 1, 0, 33, 2047 // 32 * 32], np.int32)
+    cand_len = np.array([S, S // 2 - 24, 1, 0, 33, (S - 1) // 32 * 32], np.int32)
     kmin, kmax, p = 1, 0, 0.9
     for h in range(H):
         n = cand_len[h]
-        if kind == "uniform":
+        if kind == "crowded":
+            # one binade, distinct low mantissa bits: the search's low-bit phase sees them all
+            c[h, :n] = ((1.0 + rng.integers(0, 1 << 12, n) * 2.0 ** -12) / (2 * max(n, 1))).astype(np.float32)
+        elif kind == "spread":
+            # log-uniform over ~30 binades
+            c[h, :n] = np.exp2(-rng.random(n) * 30.0).astype(np.float32) / max(n, 1)
+        elif kind == "uniform":
             c[h, :n] = np.float32(1.0 / max(n, 1))
         elif kind == "ties":
             c[h, :n] = rng.choice(np.float32([0.5, 0.25, 0.125]), n) / max(n, 1)
@@ -247,6 +256,41 @@ def test_topp_edge_cases(kind):
         assert flag & hk.FLAG_NAN and flag & hk.FLAG_RANGE
     else:
         assert flag == 0
+
+
+@pytest.mark.parametrize("name", ["cfg1_f32_d64_g4", "bf16_d128_g7_tempered", "bf16_d128_g4_ragged_holes",
+                                  "bf16_d128_g1_w32_tail1"])
+@pytest.mark.parametrize("two_metrics", [False, True])
+def test_calibrate_topp_fused(name, two_metrics):
+    """The fused launch writes exactly what hk_calibrate + hk_topp_select write."""
+    hk, cfg, w, kv, s, cl = _calib_inputs(name)
+    H, S = w.n_heads, w.S_max
+    pm = w.page_mask
+    xs, Ts, ws_ = [s], None, [1.0]
+    if two_metrics:
+        g = torch.Generator(device=DEV).manual_seed(5)
+        x2 = torch.randn(H, S, generator=g, device=DEV)
+        T2 = torch.tensor(np.linspace(0.5, 2.0, H), dtype=torch.float32, device=DEV)
+        xs, Ts, ws_ = [s, x2], [None, T2], [0.5, 0.5]
+    n = len(xs)
+    c1, l1 = torch.empty(H, S, device=DEV), torch.empty(H, n, device=DEV)
+    sel1, k1 = torch.empty(H, S // 32, dtype=torch.int32, device=DEV), torch.empty(H, dtype=torch.int32, device=DEV)
+    m1, st1 = torch.empty(H, device=DEV), torch.zeros(1, dtype=torch.int32, device=DEV)
+    hk.hk_calibrate(H, S, cl, pm, xs, Ts, ws_, c1, l1)
+    p = cfg.get("p", 0.9)
+    hk.hk_topp_select(H, S, cl, pm, c1, p, sel1, k1, sel_mass=m1, status=st1)
+    c2, l2 = torch.full((H, S), 5.0, device=DEV), torch.empty(H, n, device=DEV)
+    sel2, k2 = torch.empty_like(sel1), torch.empty_like(k1)
+    m2, st2 = torch.empty_like(m1), torch.zeros_like(st1)
+    hk.hk_calibrate_topp(H, S, cl, pm, xs, Ts, ws_, p, sel2, k2, c_out=c2, lse_out=l2,
+                         sel_mass=m2, status=st2)
+    sel3, k3 = torch.empty_like(sel1), torch.empty_like(k1)
+    hk.hk_calibrate_topp(H, S, cl, pm, xs, Ts, ws_, p, sel3, k3)
+    torch.cuda.synchronize()
+    assert torch.equal(c1, c2) and torch.equal(l1, l2)
+    assert torch.equal(sel1, sel2) and torch.equal(k1, k2) and torch.equal(m1, m2)
+    assert torch.equal(sel1, sel3) and torch.equal(k1, k3)
+    assert int(st1.item()) == int(st2.item()) == 0
 
 
 @pytest.mark.parametrize("case", range(4))

@@ -19,18 +19,33 @@
 namespace hk {
 
 #ifndef HK_DEC_PPS
-#define HK_DEC_PPS 64         // pages per split (one workgroup)
+#define HK_DEC_PPS 128        // pages per split (one workgroup)
+#endif
+#ifndef HK_DEC_QLDS
+#define HK_DEC_QLDS 1         // 0: the G query rows live in registers instead of LDS
 #endif
 #ifndef HK_DEC_PREFETCH
-#define HK_DEC_PREFETCH 0     // 1: load the wave's next page while computing the current one
+#define HK_DEC_PREFETCH 1     // load the wave's next page while computing the current one
 #endif
 
-constexpr int DEC_NT = 256;
+#ifndef HK_DEC_NT
+#define HK_DEC_NT 256
+#endif
+constexpr int DEC_NT = HK_DEC_NT;
 constexpr int DEC_NW = DEC_NT / 64;
 constexpr int DEC_PPS = HK_DEC_PPS;
 
+#ifndef HK_DEC_WPE
+#define HK_DEC_WPE 0
+#endif
+#if HK_DEC_WPE > 0
+#define HK_DEC_ATTR __launch_bounds__(DEC_NT) __attribute__((amdgpu_waves_per_eu(HK_DEC_WPE, HK_DEC_WPE)))
+#else
+#define HK_DEC_ATTR __launch_bounds__(DEC_NT)
+#endif
+
 template <typename T, int D, int G>
-__global__ __launch_bounds__(DEC_NT) void decode_split_kernel(
+__global__ HK_DEC_ATTR void decode_split_kernel(
     const T* __restrict__ q, const T* __restrict__ k_pool, const T* __restrict__ v_pool,
     const int32_t* __restrict__ table, const uint16_t* __restrict__ masks,
     const int32_t* __restrict__ n_pages_arr, int Hq, int Hkv, int max_pages, float c2,
@@ -53,6 +68,19 @@ __global__ __launch_bounds__(DEC_NT) void decode_split_kernel(
   const int t = lane >> 2, c = lane & 3;
   const int kg = lane / LPR, dc = lane % LPR;
 
+#if HK_DEC_QLDS
+  // the G query rows of this KV head (contiguous in q), 16 bytes per thread
+  __shared__ uint4 s_q[G * D * ES / 16];
+  {
+    const uint4* src = reinterpret_cast<const uint4*>(q + ((size_t)s * Hq + kv * G) * D);
+    for (int i = threadIdx.x; i < G * D * ES / 16; i += DEC_NT) s_q[i] = src[i];
+  }
+  __syncthreads();
+  auto q_word = [&](int g, int i) -> uint32_t {
+    const uint4 u = s_q[(g * D * ES + c * DQ * ES) / 16 + i / 4];
+    return (i & 3) == 0 ? u.x : (i & 3) == 1 ? u.y : (i & 3) == 2 ? u.z : u.w;
+  };
+#else
   uint32_t qw[G][QW];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
@@ -66,6 +94,8 @@ __global__ __launch_bounds__(DEC_NT) void decode_split_kernel(
       qw[g][4 * i + 3] = u.w;
     }
   }
+  auto q_word = [&](int g, int i) -> uint32_t { return qw[g][i]; };
+#endif
   float m_run[G], l_part[G], o[G][VEC];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
@@ -112,11 +142,11 @@ __global__ __launch_bounds__(DEC_NT) void decode_split_kernel(
         typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 #pragma unroll
         for (int i = 0; i < QW; ++i)
-          z = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, qw[g][i]),
+          z = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, q_word(g, i)),
                                               __builtin_bit_cast(bf16x2, kw[i]), z, false);
       } else {
 #pragma unroll
-        for (int i = 0; i < QW; ++i) z = fmaf(__uint_as_float(qw[g][i]), __uint_as_float(kw[i]), z);
+        for (int i = 0; i < QW; ++i) z = fmaf(__uint_as_float(q_word(g, i)), __uint_as_float(kw[i]), z);
       }
       z += __shfl_xor(z, 1, 64);
       z += __shfl_xor(z, 2, 64);

@@ -151,9 +151,6 @@ __device__ __forceinline__ void stage_rows(char* lds, int R, int R_pad, RowFn ro
 #ifndef HK_SCORE_PREFETCH
 #define HK_SCORE_PREFETCH 0
 #endif
-#ifndef HK_SCORE_P2_REVERSE
-#define HK_SCORE_P2_REVERSE 0
-#endif
 #ifndef HK_SCORE_WPE
 #define HK_SCORE_WPE 0
 #endif
@@ -343,6 +340,49 @@ __device__ __forceinline__ void p1_tile_pipelined(const F* kf, const char* qlds,
         for (int kk = 0; kk < KS; ++kk) sched_step<KT, (16 * 3 * KT + 22) / KS>();
       }
     }
+  }
+}
+
+// Redundancy of one 32-key tile: the lane's running maximum over the reference blocks of
+// cos-numerator * 1/|ref| (C[ref][key], refs as rows).  The MFMA chain of block rb+1 is
+// interleaved with the maximum over block rb.  check_self: some reference of this tile's
+// pages is one of its keys; that reference is then skipped for that key and `self` set.
+template <typename F>
+__device__ __forceinline__ void red_tile_max(const F& kf, const char* ref_lds, const float* rn_ref,
+                                             const int32_t* ref_slot, int RB, int lane, int slot,
+                                             bool check_self, float& cmax, int& self) {
+  constexpr int KS = F::KSTEPS;
+  if (RB <= 0) return;
+  f32x16 cur = mma_chain<F, true>(kf, ref_lds, 0, lane);
+  for (int rb = 0; rb < RB; ++rb) {
+    const bool more = rb + 1 < RB;
+    f32x16 nxt = {};
+    f32x4 rn4[4];
+#pragma unroll
+    for (int r4 = 0; r4 < 4; ++r4)
+      rn4[r4] = *reinterpret_cast<const f32x4*>(rn_ref + rb * 32 + 8 * r4 + 4 * (lane >> 5));
+    if (!check_self) {
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) {
+        if (more) nxt = F::mma(F::lds(ref_lds, rb + 1, kk, lane), kf.v[kk], nxt);
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          if (e * KS / 16 == kk) cmax = vmax(cmax, cur[e] * rn4[e >> 2][e & 3]);
+      }
+      if constexpr (sizeof(lds_frag_t<F>) == 16) {
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) sched_step<1, 2 * 16 / KS>();
+      }
+    } else {
+      if (more) nxt = mma_chain<F, true>(kf, ref_lds, rb + 1, lane);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int i = rb * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+        if (ref_slot[i] == slot) self = 1;
+        else cmax = vmax(cmax, cur[e] * rn4[e >> 2][e & 3]);
+      }
+    }
+    cur = nxt;
   }
 }
 
@@ -540,15 +580,26 @@ __global__ __launch_bounds__(256) void score_lse_merge_kernel(const float2* __re
 // ------------------------------------------------------------------ pass 2
 // Waves per SIMD the register allocator must leave room for: 4 lets two 512-thread
 // workgroups share a CU; asked only where it fits without spilling.
+// (The 1024-thread redundancy shape already caps registers at 128.)
 template <typename T, int D, int QB, bool RED>
 constexpr int pass2_min_waves() {
   if (HK_SCORE_WPE > 0) return HK_SCORE_WPE;
-  if (HK_SCORE_KT > 1) return 1;
-  return (sizeof(T) == 2 && D == 128 && (QB == 7 || (QB == 4 && !RED))) ? 4 : 1;
+  if (HK_SCORE_KT > 1 || RED) return 1;
+  return (sizeof(T) == 2 && D == 128 && (QB == 7 || QB == 4)) ? 4 : 1;
 }
 
+// Pass-2 launch shape.  The redundancy variant stages up to 256 reference rows (64 KB at
+// D = 128 bf16) beside the window block, so one workgroup fills a CU's LDS: it runs 1024
+// threads over 512 pages to amortise the staging.  The plain variant keeps two
+// 512-thread workgroups of 128 pages per CU.
+template <bool RED>
+struct P2Shape {
+  static constexpr int NT = RED ? 1024 : SCORE_NT;
+  static constexpr int PPW = RED ? 512 : SCORE_PPW;
+};
+
 template <typename T, int D, int QB, bool RED>
-__global__ __launch_bounds__(SCORE_NT) __attribute__((amdgpu_waves_per_eu(
+__global__ __launch_bounds__(P2Shape<RED>::NT) __attribute__((amdgpu_waves_per_eu(
     pass2_min_waves<T, D, QB, RED>(), pass2_min_waves<T, D, QB, RED>() > 1 ? pass2_min_waves<T, D, QB, RED>() : 8)))
 void score_pass2_kernel(
     const T* __restrict__ q_obs, const T* __restrict__ k_pool, const int32_t* __restrict__ table,
@@ -559,11 +610,8 @@ void score_pass2_kernel(
   using F = Frag<T, D>;
   constexpr int R_pad = 32 * QB;
   extern __shared__ __align__(16) char smem[];
-#if HK_SCORE_P2_REVERSE
-  const int h = gridDim.y - 1 - blockIdx.y, chunk = blockIdx.x;
-#else
+  constexpr int NT = P2Shape<RED>::NT, NW = NT / 64, PPW = P2Shape<RED>::PPW;
   const int h = blockIdx.y, chunk = blockIdx.x;
-#endif
   const int s = h / Hkv, kv = h % Hkv, G = Hq / Hkv;
   const int R = G * W;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -574,13 +622,13 @@ void score_pass2_kernel(
 
   const int32_t* trow = table + (size_t)h * max_pages;
   const uint16_t* mrow = masks + (size_t)h * max_pages;
-  const int p_begin = chunk * SCORE_PPW, p_end_all = min(p_begin + SCORE_PPW, max_pages);
+  const int p_begin = chunk * PPW, p_end_all = min(p_begin + PPW, max_pages);
   const int p_cand_end = min(p_end_all, cand_len / HK_PAGE);
 
   // slots of this chunk that hold no candidate: -inf
   {
     const int j0 = max(p_cand_end, p_begin) * HK_PAGE, j1 = p_end_all * HK_PAGE;
-    for (int j = j0 + threadIdx.x; j < j1; j += SCORE_NT) {
+    for (int j = j0 + threadIdx.x; j < j1; j += NT) {
       s_out[(size_t)h * S_max + j] = -INFINITY;
       if (RED) x_red[(size_t)h * S_max + j] = -INFINITY;
     }
@@ -593,7 +641,7 @@ void score_pass2_kernel(
   });
   char* after_q = smem + (size_t)R_pad * D * sizeof(T);
   float* lse2 = reinterpret_cast<float*>(after_q);                 // [R_pad], log2 units
-  for (int r = threadIdx.x; r < R_pad; r += SCORE_NT) {
+  for (int r = threadIdx.x; r < R_pad; r += NT) {
     float v = INFINITY;                                            // padding rows weigh 0
     if (r < R) {
       const int w = r / G, g = r % G;
@@ -611,7 +659,7 @@ void score_pass2_kernel(
     RB = nr_pad >> 5;
     rn_ref = reinterpret_cast<float*>(ref_lds + (size_t)NREF_MAX * D * sizeof(T));
     ref_slot = reinterpret_cast<int32_t*>(rn_ref + NREF_MAX);
-    ref_bits = reinterpret_cast<uint32_t*>(ref_slot + NREF_MAX);   // [SCORE_PPW / 2] words
+    ref_bits = reinterpret_cast<uint32_t*>(ref_slot + NREF_MAX);   // [PPW / 2] words
     const int32_t* rs = ref_slots + (size_t)h * n_ref;
     auto ref_row = [&](int i) -> const T* {
       const int j = rs[i];
@@ -619,10 +667,12 @@ void score_pass2_kernel(
       if (j < 0 || pp >= n) return nullptr;
       return k_pool + ((size_t)trow[pp] * HK_PAGE + (j & 15)) * D;
     };
-    stage_rows<T, D>(ref_lds, n_ref, nr_pad, ref_row);
-    for (int i = threadIdx.x; i < SCORE_PPW / 2; i += SCORE_NT) ref_bits[i] = 0u;
+    // padding rows (n_ref <= i < nr_pad) repeat reference 0: a repeated member changes
+    // neither the maximum nor the self test (its slot is reference 0's)
+    stage_rows<T, D>(ref_lds, nr_pad, nr_pad, [&](int i) { return ref_row(i < n_ref ? i : 0); });
+    for (int i = threadIdx.x; i < PPW / 2; i += NT) ref_bits[i] = 0u;
     __syncthreads();
-    for (int i = threadIdx.x; i < nr_pad; i += SCORE_NT) {
+    for (int i = threadIdx.x; i < nr_pad; i += NT) {
       // squared norm of reference row i, read back from its fragment-major LDS image
       float ss = 0.f;
       for (int half = 0; half < 2; ++half) {
@@ -646,13 +696,12 @@ void score_pass2_kernel(
           }
         }
       }
-      // padding rows (i >= n_ref) carry NaN, which fmaxf ignores; a zero-norm
-      // reference has cosine 0 with every key
-      rn_ref[i] = (i >= n_ref) ? __builtin_nanf("") : (ss > 0.f ? 1.0f / sqrtf(ss) : 0.f);
-      const int slot = (i < n_ref) ? rs[i] : -1;
+      // a zero-norm reference has cosine 0 with every key
+      rn_ref[i] = ss > 0.f ? 1.0f / sqrtf(ss) : 0.f;
+      const int slot = rs[i < n_ref ? i : 0];
       ref_slot[i] = slot;
       const int rel = slot - p_begin * HK_PAGE;    // reference slots inside this chunk
-      if (i < n_ref && rel >= 0 && rel < SCORE_PPW * HK_PAGE)
+      if (i < n_ref && rel >= 0 && rel < PPW * HK_PAGE)
         atomicOr(&ref_bits[rel >> 5], 1u << (rel & 31));
     }
   }
@@ -709,26 +758,8 @@ void score_pass2_kernel(
           const uint32_t self_word = ref_bits[(p0 + 2 * t - p_begin) >> 1];
           float cmax = -INFINITY;
           int self = 0;
-          for (int rb = 0; rb < RB; ++rb) {
-            f32x16 ra[1];
-            mma_chains<F, true, 1>(&kf[t], ref_lds, rb, lane, ra);
-#pragma unroll
-            for (int r4 = 0; r4 < 4; ++r4) {
-              const int i0 = rb * 32 + 8 * r4 + 4 * (lane >> 5);
-              const f32x4 rn4 = *reinterpret_cast<const f32x4*>(rn_ref + i0);
-              if (self_word == 0u) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) cmax = fmaxf(cmax, ra[0][4 * r4 + i] * rn4[i]);
-              } else {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                  if (ref_slot[i0 + i] == slot) self = 1;
-                  else cmax = fmaxf(cmax, ra[0][4 * r4 + i] * rn4[i]);
-                }
-              }
-            }
-          }
-          cmax = fmaxf(cmax, __shfl_xor(cmax, 32, 64));
+          red_tile_max<F>(kf[t], ref_lds, rn_ref, ref_slot, RB, lane, slot, self_word != 0u, cmax, self);
+          cmax = vmax(cmax, __shfl_xor(cmax, 32, 64));
           self |= __shfl_xor(self, 32, 64);
           if (cand) x = (n_ref - self > 0) ? -(cmax * rn) : 1.0f;
         }
@@ -737,7 +768,7 @@ void score_pass2_kernel(
       if (write) s_out[(size_t)h * S_max + slot] = cand ? fmaf(fast_log2(c_all), kLn2, -lnR) : -INFINITY;
     }
   };
-  tile_loop<F>(load_group, process, p_begin + SCORE_WPP * wave, p_cand_end, SCORE_WPP * SCORE_NW);
+  tile_loop<F>(load_group, process, p_begin + SCORE_WPP * wave, p_cand_end, SCORE_WPP * NW);
 }
 
 template <typename K>
@@ -752,7 +783,7 @@ static size_t pass1_lds(int R_pad, int D, int es) {
 }
 static size_t pass2_lds(int R_pad, int D, int es, bool red) {
   size_t b = (size_t)R_pad * D * es + (size_t)R_pad * sizeof(float);
-  if (red) b += (size_t)NREF_MAX * D * es + (size_t)NREF_MAX * 8 + (SCORE_PPW / 2) * 4;
+  if (red) b += (size_t)NREF_MAX * D * es + (size_t)NREF_MAX * 8 + (P2Shape<true>::PPW / 2) * 4;
   return b;
 }
 
@@ -794,15 +825,17 @@ hipError_t launch_score_q(const hk_score_args& a, hipStream_t st) {
   const size_t lds2 = pass2_lds(R_pad, D, sizeof(T), a.x_red != nullptr);
   TimedLaunch t(HK_TK_SCORE_PASS2, st);
   if (a.x_red) {
+    constexpr int PPW2 = P2Shape<true>::PPW;
+    const dim3 grid2((kv->max_pages + PPW2 - 1) / PPW2, n_heads);
     allow_lds(score_pass2_kernel<T, D, QB, true>, lds2);
-    hipLaunchKernelGGL((score_pass2_kernel<T, D, QB, true>), grid, dim3(SCORE_NT), lds2, st,
+    hipLaunchKernelGGL((score_pass2_kernel<T, D, QB, true>), grid2, dim3(P2Shape<true>::NT), lds2, st,
                        static_cast<const T*>(a.q_obs), static_cast<const T*>(kv->k_pool),
                        kv->page_table, kv->page_mask, kv->n_pages, a.NS, a.Hq, a.Hkv, a.W,
                        kv->max_pages, a.L_dense, c2, lnR, lse_use, a.s_attn, a.cand_len,
                        a.ref_slots, a.n_ref, a.x_red);
   } else {
     allow_lds(score_pass2_kernel<T, D, QB, false>, lds2);
-    hipLaunchKernelGGL((score_pass2_kernel<T, D, QB, false>), grid, dim3(SCORE_NT), lds2, st,
+    hipLaunchKernelGGL((score_pass2_kernel<T, D, QB, false>), grid, dim3(P2Shape<false>::NT), lds2, st,
                        static_cast<const T*>(a.q_obs), static_cast<const T*>(kv->k_pool),
                        kv->page_table, kv->page_mask, kv->n_pages, a.NS, a.Hq, a.Hkv, a.W,
                        kv->max_pages, a.L_dense, c2, lnR, lse_use, a.s_attn, a.cand_len,

@@ -574,3 +574,91 @@ def test_determinism_bitwise():
                                                w.free_ids, w.k_pool.view(torch.int16))])
     for a, b in zip(*outs):
         assert torch.equal(a, b)
+
+
+def test_degenerate_heads_end_to_end():
+    """Heads with no pages, with pages but no valid slot, and with a single valid slot go
+    through score -> calibrate + Top-p -> rewrite -> append -> decode as the oracle says:
+    s = -inf and k = 0 where nothing is valid, a lone valid slot is selected, empty
+    condensed pages are released, and attention over an empty head gives o = 0,
+    lse = -inf."""
+    import paper_2606_28831_amd as hk
+    from paper_2606_28831_amd.pipeline import Compressor
+    cfg = dict(L=1, B=3, Hq=8, Hkv=2, D=128, N=100, dtype="bf16", W=8, seed=31, recipe="normal")
+    G, D, W, p = 4, 128, 8, 0.9
+    w = WL.make_workload(cfg, DEV, max_pages=16)
+    H = w.n_heads
+    w.n_pages[0] = 0                       # empty row
+    w.page_table[0, :] = -1
+    w.page_mask[0, :] = 0
+    w.page_mask[1, :] = 0                  # pages, but no valid slot
+    w.page_mask[2, :] = 0                  # one valid slot: page 3, slot 5
+    w.page_mask[2, 3] = 1 << 5
+    kv = hk.PagedKV(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)
+    alloc = hk.Allocator(w.free_ids, w.free_top)
+    pre = HostCache(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)
+    comp = Compressor(w.NS, cfg["Hq"], cfg["Hkv"], D, W, kv, alloc, p)
+    comp.step(w.q_obs)
+    torch.cuda.synchronize()
+    b = comp.buf
+    S = w.S_max
+    scale = 1 / math.sqrt(D)
+    qn = np64(w.q_obs)
+    s_gpu, c_gpu, sel_gpu, k_gpu = np64(b.s_attn), b.c.cpu().numpy(), np_i(b.sel_bits), np_i(b.k)
+    post = HostCache(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)
+    for h in range(H):
+        rows, valid = pre.head(h)
+        vrows, _ = pre.head_v(h)
+        n = int(pre.n[h])
+        s_ref, _ = O.score_head(q_rows(qn, h, cfg["Hkv"], G), rows, valid, 16 * n, scale)
+        full = np.full(S, -np.inf)
+        full[:len(s_ref)] = s_ref
+        check_log_scores(s_gpu[h], full, 2e-3, f"score head {h}")
+        cand = np.zeros(S, bool)
+        cand[:len(valid)] = O.candidate_mask(valid, 16 * n)
+        r = O.topp_head(c_gpu[h], cand, p)
+        assert int(k_gpu[h]) == r.k and np.array_equal(unpack_bits(sel_gpu[h], S), r.sel), h
+        if h in (0, 1):
+            assert r.k == 0 and not c_gpu[h].any()
+        if h == 2:
+            assert r.k == 1 and unpack_bits(sel_gpu[h], S)[3 * 16 + 5]
+        res = O.compact_head(pre.table[h], pre.mask[h], n, r.sel, 0, 0)
+        assert int(post.n[h]) == len(res.pages), h
+        K1, v1 = post.head(h)
+        V1, _ = post.head_v(h)
+        want = [(ph, t) for e in res.pages for ph, t in e.src]
+        pos_of = {int(pid): i for i, pid in enumerate(pre.table[h][:n])}
+        assert v1.sum() == len(want), h
+        for j, (ph, t) in enumerate(want):
+            src = pos_of[ph] * 16 + t
+            assert np.array_equal(K1[j], rows[src]) and np.array_equal(V1[j], vrows[src]), (h, j)
+    assert int(b.status.item()) == 0
+    # one decode step: append to every head (the empty ones pop a page), then attend
+    d = hk.dims(w.NS, cfg["Hq"], cfg["Hkv"], D)
+    g = torch.Generator(device=DEV).manual_seed(3)
+    kn = torch.randn(w.NS, cfg["Hkv"], D, generator=g, device=DEV).to(torch.bfloat16)
+    vn = torch.randn(w.NS, cfg["Hkv"], D, generator=g, device=DEV).to(torch.bfloat16)
+    qd = torch.randn(w.NS, cfg["Hq"], D, generator=g, device=DEV).to(torch.bfloat16)
+    st = torch.zeros(1, dtype=torch.int32, device=DEV)
+    o = torch.empty(w.NS, cfg["Hq"], D, device=DEV)
+    lse = torch.empty(w.NS, cfg["Hq"], device=DEV)
+    for dec_with_append in (False, True):
+        if dec_with_append:
+            hk.hk_append_kv(d, kv, kn, vn, alloc, st, hk.workspace(hk.OP_APPEND, d, w.max_pages, DEV))
+        hk.hk_decode_attn(d, qd, kv, scale, o, lse, hk.workspace(hk.OP_DECODE, d, w.max_pages, DEV))
+        torch.cuda.synchronize()
+        cur = HostCache(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)
+        for h in range(H):
+            s_, kvh = divmod(h, cfg["Hkv"])
+            Kh, valid = cur.head(h)
+            Vh, _ = cur.head_v(h)
+            o_ref, l_ref = O.decode_head(np64(qd)[s_, kvh * G:(kvh + 1) * G], Kh, Vh, valid, scale)
+            og, lg = np64(o)[s_, kvh * G:(kvh + 1) * G], np64(lse)[s_, kvh * G:(kvh + 1) * G]
+            if not valid.any():
+                assert not dec_with_append or h not in (0, 1)
+                assert np.all(og == 0) and np.all(np.isneginf(lg)), h
+            else:
+                for gi in range(G):
+                    check_prob(og[gi], o_ref[gi], 2e-3, f"o head {h}")
+                check_lse(lg, l_ref, 2e-3, f"lse head {h}")
+    assert int(st.item()) == 0

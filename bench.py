@@ -388,6 +388,16 @@ def run_decode(args):
     NS = L * B
     dt = WL.TORCH_DTYPE[cfg["dtype"]]
     seg_ms, seg_tokens_kv, kept = [], [], []
+    graph = None
+    if args.graph:
+        # one HIP graph for a whole segment over persistent input buffers, refilled in
+        # place before each replay (the graph keeps their addresses)
+        bufs = (torch.empty(T, NS, Hq, D, device=dev, dtype=dt), torch.empty(T, NS, Hkv, D, device=dev, dtype=dt),
+                torch.empty(T, NS, Hkv, D, device=dev, dtype=dt), torch.empty(T, NS, Hq, device=dev))
+        t_cap = time.perf_counter()
+        graph = loop.capture_segment(*bufs)
+        torch.cuda.synchronize()
+        t_cap = time.perf_counter() - t_cap
     for name in hk.TIMED_KERNELS:
         hk.hk_timing_read(name)
     hk.hk_timing_enable(["decode_split"])    # the dominant kernel of the loop
@@ -402,19 +412,26 @@ def run_decode(args):
         seg_tokens_kv.append(valid)
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for t in range(T):
-            loop.step(q_seg[t], k_seg[t], v_seg[t], lse_seg[t])
-        loop.compress(q_seg[T - W:], lse_seg[T - W:])
-        e1.record()
+        if graph is not None:
+            for dst, src in zip(bufs, (q_seg, k_seg, v_seg)):
+                dst.copy_(src)
+            torch.cuda.synchronize()
+            e0.record()
+            graph.replay()
+            e1.record()
+        else:
+            e0.record()
+            loop.segment(q_seg, k_seg, v_seg, lse_seg)
+            e1.record()
         torch.cuda.synchronize()
         seg_ms.append(e0.elapsed_time(e1))
         kept.append(float(loop.comp.buf.k.float().mean()))
         del q_seg, k_seg, v_seg, lse_seg
     hk.hk_timing_enable([])
     tot, n = hk.hk_timing_read("decode_split")
+    # graph replays launch nothing from the host, so no per-kernel events are recorded
     ktime = {"decode_split": {"avg_ms": tot / n, "launches_per_step": n / n_seg,
-                              "ms_per_step": tot / n_seg}}
+                              "ms_per_step": tot / n_seg}} if n else {}
     status = int(loop.status.item()) | int(loop.comp.buf.status.item())
     total_s = sum(seg_ms) / 1e3
     tokens = B * T * n_seg
@@ -425,7 +442,8 @@ def run_decode(args):
     dec_bytes += n_seg * T * NS * Hq * (D * e + D * 4 + 4)
     per_launch = {"decode_split": (dec_bytes / max(1, n_seg * T * L), 0.0)}
     roof = _roofline(ktime, per_launch, cfg["name"])
-    roof["share_of_step"] = ktime["decode_split"]["ms_per_step"] / (sum(seg_ms) / n_seg)
+    if roof is not None:
+        roof["share_of_step"] = ktime["decode_split"]["ms_per_step"] / (sum(seg_ms) / n_seg)
     return {
         "metric": METRIC, "value": tokens / total_s, "unit": "decode tokens/s",
         "n_gpus": 1, "steps": n_seg, "warmup": 0, "ms_per_step": sum(seg_ms) / n_seg,
@@ -433,7 +451,9 @@ def run_decode(args):
         "data": "synthetic",
         "config": {"workload": cfg["name"], "layers": L, "batch": B, "q_heads": Hq, "kv_heads": Hkv,
                    "head_dim": D, "prompt": cfg["N"], "decode_steps": T * n_seg,
-                   "compress_every": T, "window": W, "top_p": cfg["p"], "L_dense": cfg["L_dense"]},
+                   "compress_every": T, "window": W, "top_p": cfg["p"], "L_dense": cfg["L_dense"],
+                   "hip_graph": bool(args.graph)},
+        "graph_capture_s": t_cap if args.graph else None,
         "decode_attn_hbm_frac_lower_bound": dec_bytes / total_s / 1e9 / HBM_PEAK_GBS,
         "kernels": ktime, "roofline": roof,
         "segment_ms": seg_ms, "valid_kv_slots_per_segment": seg_tokens_kv, "mean_kept_per_head": kept,
@@ -516,6 +536,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--graph", action="store_true",
+                    help="config 5: replay each decode segment from one captured HIP graph")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run the 1 GiB plain copy the byte counters are scaled by")

@@ -425,9 +425,7 @@ hipError_t hk_launch_compact(int n_heads, int D, const hk_paged_kv* kv, const ui
   }
   }
   const size_t lds = (size_t)mp * (sizeof(int32_t) + sizeof(uint16_t));
-  if (lds > 65536)
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(compact_table_kernel),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  allow_dynamic_lds<compact_table_kernel>(lds);
   {
     TimedLaunch t(HK_TK_COMPACT_META, st);
     hipLaunchKernelGGL(compact_table_kernel, dim3(n_heads), dim3(CP_NT), lds, st, kv->page_table,

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "hardkv.h"
 
 #define HK_PAGE 16
@@ -143,6 +145,20 @@ __device__ __forceinline__ bool is_cand(const uint16_t* mask_row, int cand_len, 
 }
 
 __device__ __forceinline__ int dense_pages(int L_dense) { return (L_dense + HK_PAGE - 1) / HK_PAGE; }
+
+// Raise a kernel's dynamic-LDS limit above the 64 KB default.  The attribute is set only
+// when a launch asks for more than any earlier one, so repeated launches (including ones a
+// caller records into a graph) make no further API calls.
+template <auto Kernel>
+inline void allow_dynamic_lds(size_t bytes) {
+  static std::atomic<size_t> granted{65536};
+  size_t g = granted.load(std::memory_order_relaxed);
+  if (bytes <= g) return;
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(Kernel),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+  while (g < bytes && !granted.compare_exchange_weak(g, bytes)) {
+  }
+}
 
 // Records HIP events around one kernel launch on its stream while kernel timing is on
 // (hk_timing_enable); construct right before the launch, let it go out of scope after.

@@ -771,13 +771,6 @@ void score_pass2_kernel(
   tile_loop<F>(load_group, process, p_begin + SCORE_WPP * wave, p_cand_end, SCORE_WPP * NW);
 }
 
-template <typename K>
-static void allow_lds(K kernel, size_t bytes) {
-  if (bytes > 65536)
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
-}
-
 static size_t pass1_lds(int R_pad, int D, int es) {
   return (size_t)R_pad * D * es + (size_t)SCORE_NW * R_pad * sizeof(float2);
 }
@@ -803,7 +796,7 @@ hipError_t launch_score_q(const hk_score_args& a, hipStream_t st) {
   dim3 grid(n_chunks, n_heads);
   if (!lse_use) {
     const size_t lds1 = pass1_lds(R_pad, D, sizeof(T));
-    allow_lds(score_pass1_kernel<T, D, QB>, lds1);
+    allow_dynamic_lds<score_pass1_kernel<T, D, QB>>(lds1);
     {
       TimedLaunch t(HK_TK_SCORE_PASS1, st);
       hipLaunchKernelGGL((score_pass1_kernel<T, D, QB>), grid, dim3(SCORE_NT), lds1, st,
@@ -827,14 +820,14 @@ hipError_t launch_score_q(const hk_score_args& a, hipStream_t st) {
   if (a.x_red) {
     constexpr int PPW2 = P2Shape<true>::PPW;
     const dim3 grid2((kv->max_pages + PPW2 - 1) / PPW2, n_heads);
-    allow_lds(score_pass2_kernel<T, D, QB, true>, lds2);
+    allow_dynamic_lds<score_pass2_kernel<T, D, QB, true>>(lds2);
     hipLaunchKernelGGL((score_pass2_kernel<T, D, QB, true>), grid2, dim3(P2Shape<true>::NT), lds2, st,
                        static_cast<const T*>(a.q_obs), static_cast<const T*>(kv->k_pool),
                        kv->page_table, kv->page_mask, kv->n_pages, a.NS, a.Hq, a.Hkv, a.W,
                        kv->max_pages, a.L_dense, c2, lnR, lse_use, a.s_attn, a.cand_len,
                        a.ref_slots, a.n_ref, a.x_red);
   } else {
-    allow_lds(score_pass2_kernel<T, D, QB, false>, lds2);
+    allow_dynamic_lds<score_pass2_kernel<T, D, QB, false>>(lds2);
     hipLaunchKernelGGL((score_pass2_kernel<T, D, QB, false>), grid, dim3(P2Shape<false>::NT), lds2, st,
                        static_cast<const T*>(a.q_obs), static_cast<const T*>(kv->k_pool),
                        kv->page_table, kv->page_mask, kv->n_pages, a.NS, a.Hq, a.Hkv, a.W,

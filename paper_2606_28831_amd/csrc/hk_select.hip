@@ -514,21 +514,14 @@ hipError_t hk_launch_calibrate(int n_heads, int S_max, const int32_t* cand_len, 
   return hipGetLastError();
 }
 
-// dynamic LDS of the Top-p kernels: the packed key list of the low-bit search
-template <typename K>
-static void sel_allow_lds(K kernel, size_t bytes) {
-  if (bytes > 65536)
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
-}
-
+// (dynamic LDS of the Top-p kernels: the packed key list of the low-bit search)
 hipError_t hk_launch_topp(int n_heads, int S_max, const int32_t* cand_len, const uint16_t* mask,
                           const float* c, int p_q, int k_min, int k_max, uint32_t* sel_bits,
                           int32_t* k_out, float* sel_mass, int32_t* status, hipStream_t st) {
   const size_t lds = (size_t)S_max * sizeof(uint32_t);
   TimedLaunch t(HK_TK_TOPP, st);
   HK_EPT_SWITCH(S_max, {
-    sel_allow_lds(topp_kernel<E>, lds);
+    allow_dynamic_lds<topp_kernel<E>>(lds);
     hipLaunchKernelGGL((topp_kernel<E>), dim3(n_heads), dim3(SEL_NT), lds, st, S_max, cand_len, mask,
                        c, p_q, k_min, k_max, sel_bits, k_out, sel_mass, status);
   });
@@ -543,7 +536,7 @@ hipError_t hk_launch_calib_topp(int n_heads, int S_max, const int32_t* cand_len,
   const size_t lds = (size_t)S_max * sizeof(uint32_t);
   TimedLaunch t(HK_TK_CALIB_TOPP, st);
   HK_EPT_SWITCH(S_max, {
-    sel_allow_lds(calib_topp_kernel<E>, lds);
+    allow_dynamic_lds<calib_topp_kernel<E>>(lds);
     hipLaunchKernelGGL((calib_topp_kernel<E>), dim3(n_heads), dim3(SEL_NT), lds, st, S_max, cand_len,
                        mask, n_metrics, x0, x1, T0, T1, w0, w1, p_q, k_min, k_max, c_out, lse_out,
                        sel_bits, k_out, sel_mass, status);

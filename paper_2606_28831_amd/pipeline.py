@@ -172,3 +172,22 @@ class DecodeLoop:
 
     def compress(self, q_win, lse_win, stream=None):
         self.comp.step(q_win, row_lse_in=lse_win, stream=stream)
+
+    def segment(self, q_seg, k_seg, v_seg, lse_seg, stream=None):
+        """len(q_seg) decode steps, then one compression over the last W steps' queries
+        and their decode LSEs (Sec. 3.1 Steps 1-3)."""
+        T = q_seg.shape[0]
+        for t in range(T):
+            self.step(q_seg[t], k_seg[t], v_seg[t], lse_seg[t], stream=stream)
+        self.compress(q_seg[T - self.W:], lse_seg[T - self.W:], stream=stream)
+
+    def capture_segment(self, q_seg, k_seg, v_seg, lse_seg):
+        """Record one segment into a HIP graph (torch.cuda.CUDAGraph).  The graph keeps the
+        buffers' addresses: refill q_seg / k_seg / v_seg in place and replay it.  Every step
+        of a segment is a kernel launch on the capture stream with device-side metadata
+        updates (no host synchronisation, no allocation, no memset), so one graph serves
+        every segment.  Nothing runs at capture time."""
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            self.segment(q_seg, k_seg, v_seg, lse_seg)
+        return g

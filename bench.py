@@ -461,6 +461,90 @@ def run_decode(args):
     }
 
 
+def run_crossover(args):
+    """Sparse loading vs rewrite (Sec. 3.3.1 HA-Sparse vs HA-Max), re-created synthetically:
+    per cache length and batch, the preparation time of each form (hk_compact with every
+    page in the sparse band, i.e. masks only, or every page condensed, i.e. rewritten),
+    the decode-attention time per step over the result, the memory each holds, and the
+    decode step after which the rewrite has paid back its preparation (time) and its
+    transient memory (memory-time integral).  Selections are drawn per head, scattered
+    uniformly over the valid slots, with keep fractions uniform in [0, 25%] (mean 12.5%,
+    the paper's setting); the kernels are the tested ones, only the tier split differs."""
+    import paper_2606_28831_amd as hk
+    import workload as WL
+    dev = torch.device("cuda", 0)
+    Hq, Hkv, D = 32, 8, 128
+    G = Hq // Hkv
+    page_bytes = 16 * D * 2 * 2                         # K and V of one 16-slot page, bf16
+    rows = []
+    for B in (1, 32):
+        for N in (2048, 4096, 8192, 12288, 16384, 20480):
+            cfg = dict(L=1, B=B, Hq=Hq, Hkv=Hkv, D=D, N=N, dtype="bf16", W=8, seed=7 + N + B,
+                       recipe="normal")
+            w = WL.make_workload(cfg, dev, pool_slack=1.3)
+            H, S = w.n_heads, w.S_max
+            g = torch.Generator(device=dev).manual_seed(N * 131 + B)
+            frac = torch.rand(H, generator=g, device=dev) * 0.25
+            r = torch.rand(H, S, generator=g, device=dev)
+            sel = (r < frac[:, None]) & (torch.arange(S, device=dev)[None, :] < N)
+            bits = (sel.view(H, S // 32, 32).to(torch.int64) << torch.arange(32, device=dev)).sum(-1)
+            sel_bits = bits.to(torch.int64).bitwise_and(0xFFFFFFFF).to(torch.int32)
+            kv = hk.PagedKV(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)
+            alloc = hk.Allocator(w.free_ids, w.free_top)
+            d = hk.dims(B, Hq, Hkv, D, 0)
+            st = torch.zeros(1, dtype=torch.int32, device=dev)
+            wsc = hk.workspace(hk.OP_COMPACT, d, w.max_pages, dev)
+            wsd = hk.workspace(hk.OP_DECODE, d, w.max_pages, dev)
+            q = torch.randn(B, Hq, D, generator=g, device=dev).to(torch.bfloat16)
+            o = torch.empty(B, Hq, D, device=dev)
+            lse = torch.empty(B, Hq, device=dev)
+            pristine = WL.clone_state(w)
+            pages_before = int(w.n_pages.sum())
+            out = {"batch": B, "tokens": N, "kept_mean": float(frac.mean()), "pages_before": pages_before}
+            for mode, L_sparse in (("sparse", N + 16), ("rewrite", 0)):
+                prep = []
+                for _ in range(5):
+                    WL.restore_state(w, pristine)
+                    torch.cuda.synchronize()
+                    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    e0.record()
+                    hk.hk_compact(d, kv, sel_bits, 0, L_sparse, alloc, st, wsc)
+                    e1.record()
+                    torch.cuda.synchronize()
+                    prep.append(e0.elapsed_time(e1))
+                for _ in range(3):
+                    hk.hk_decode_attn(d, q, kv, 1 / math.sqrt(D), o, lse, wsd)
+                torch.cuda.synchronize()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                for _ in range(20):
+                    hk.hk_decode_attn(d, q, kv, 1 / math.sqrt(D), o, lse, wsd)
+                e1.record()
+                torch.cuda.synchronize()
+                pages_after = int(w.n_pages.sum())
+                out[mode] = {"prep_ms": sorted(prep)[len(prep) // 2], "decode_ms": e0.elapsed_time(e1) / 20,
+                             "pages_held": pages_after, "bytes_held": pages_after * page_bytes,
+                             "new_pages": pages_after if mode == "rewrite" else 0}
+            assert int(st.item()) == 0
+            sp, rw = out["sparse"], out["rewrite"]
+            dd = sp["decode_ms"] - rw["decode_ms"]
+            out["time_breakeven_steps"] = ((rw["prep_ms"] - sp["prep_ms"]) / dd) if dd > 0 else None
+            # memory-time integral (bytes x ms) from the compression on: the rewrite holds old
+            # and new pages while it runs, then only the new ones
+            mti_sp = lambda t: sp["bytes_held"] * (sp["prep_ms"] + t * sp["decode_ms"])
+            mti_rw = lambda t: ((pages_before + rw["new_pages"]) * page_bytes * rw["prep_ms"]
+                                + rw["bytes_held"] * t * rw["decode_ms"])
+            out["mti_breakeven_steps"] = next((t for t in range(0, 10001) if mti_rw(t) <= mti_sp(t)), None)
+            out["decode_speedup"] = sp["decode_ms"] / rw["decode_ms"]
+            rows.append(out)
+            print(json.dumps({k: out[k] for k in ("batch", "tokens", "decode_speedup", "time_breakeven_steps",
+                                                  "mti_breakeven_steps")}), file=sys.stderr, flush=True)
+            del w, kv, alloc, wsc, wsd
+            torch.cuda.empty_cache()
+    return {"experiment": "sparse loading vs rewrite (HA-Sparse vs HA-Max)", "data": "synthetic",
+            "heads_per_sequence": Hkv, "q_heads": Hq, "head_dim": D, "dtype": "bf16", "rows": rows}
+
+
 def copy_calibration():
     """A plain 1 GiB device-to-device copy, three times: the reference the FETCH_SIZE and
     WRITE_SIZE counters are scaled by (each copy reads and writes exactly 1 GiB)."""
@@ -536,6 +620,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--crossover", action="store_true",
+                    help="sparse loading vs rewrite over cache length (not the bench line)")
     ap.add_argument("--graph", action="store_true",
                     help="config 5: replay each decode segment from one captured HIP graph")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -564,6 +650,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         print(json.dumps(copy_calibration()), flush=True)
+        return
+    if args.crossover:
+        print(json.dumps(run_crossover(args)), flush=True)
         return
     out = run_decode(args) if args.config == 5 else run_compression(args)
     print(json.dumps(out), flush=True)

@@ -19,7 +19,7 @@
 namespace hk {
 
 #ifndef HK_DEC_PPS
-#define HK_DEC_PPS 128        // pages per split (one workgroup)
+#define HK_DEC_PPS 128        // most pages per split (one workgroup)
 #endif
 #ifndef HK_DEC_QLDS
 #define HK_DEC_QLDS 1         // 0: the G query rows live in registers instead of LDS
@@ -34,6 +34,8 @@ namespace hk {
 constexpr int DEC_NT = HK_DEC_NT;
 constexpr int DEC_NW = DEC_NT / 64;
 constexpr int DEC_PPS = HK_DEC_PPS;
+constexpr int DEC_PPS_MIN = 16;             // fewest pages per split
+constexpr int DEC_TARGET_WG = 2048;         // workgroups a launch should offer the chip
 
 #ifndef HK_DEC_WPE
 #define HK_DEC_WPE 0
@@ -49,7 +51,7 @@ __global__ HK_DEC_ATTR void decode_split_kernel(
     const T* __restrict__ q, const T* __restrict__ k_pool, const T* __restrict__ v_pool,
     const int32_t* __restrict__ table, const uint16_t* __restrict__ masks,
     const int32_t* __restrict__ n_pages_arr, int Hq, int Hkv, int max_pages, float c2,
-    float* __restrict__ part, int n_split) {
+    float* __restrict__ part, int n_split, int pps) {
   constexpr int ES = sizeof(T);
   constexpr int DQ = D / 4;                 // dims per quarter
   constexpr int VEC = 16 / ES;              // elements per 16-byte chunk
@@ -64,7 +66,10 @@ __global__ HK_DEC_ATTR void decode_split_kernel(
   const int s = h / Hkv, kv = h % Hkv;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n = n_pages_arr[h];
-  const int p_begin = split * DEC_PPS, p_end = min(p_begin + DEC_PPS, n);
+  // this head's pages are shared evenly by the launch's splits (at least DEC_PPS_MIN
+  // each; pps bounds the share of a full row), so short rows are not left to few waves
+  const int per = min(pps, max((n + n_split - 1) / n_split, DEC_PPS_MIN));
+  const int p_begin = split * per, p_end = min(p_begin + per, n);
   const int t = lane >> 2, c = lane & 3;
   const int kg = lane / LPR, dc = lane % LPR;
 
@@ -445,22 +450,22 @@ __global__ __launch_bounds__(AP_NT) void append_write_kernel(
 
 template <typename T, int D, int G>
 static void launch_split(dim3 grid, hipStream_t st, const void* q, const hk_paged_kv* kv, int Hq,
-                         int Hkv, float c2, float* part, int n_split) {
+                         int Hkv, float c2, float* part, int n_split, int pps) {
   hipLaunchKernelGGL((decode_split_kernel<T, D, G>), grid, dim3(DEC_NT), 0, st,
                      static_cast<const T*>(q), static_cast<const T*>(kv->k_pool),
                      static_cast<const T*>(kv->v_pool), kv->page_table, kv->page_mask, kv->n_pages,
-                     Hq, Hkv, kv->max_pages, c2, part, n_split);
+                     Hq, Hkv, kv->max_pages, c2, part, n_split, pps);
 }
 
 template <typename T, int D>
 static bool launch_split_g(int G, dim3 grid, hipStream_t st, const void* q, const hk_paged_kv* kv,
-                           int Hq, int Hkv, float c2, float* part, int n_split) {
+                           int Hq, int Hkv, float c2, float* part, int n_split, int pps) {
   switch (G) {
-    case 1: launch_split<T, D, 1>(grid, st, q, kv, Hq, Hkv, c2, part, n_split); return true;
-    case 2: launch_split<T, D, 2>(grid, st, q, kv, Hq, Hkv, c2, part, n_split); return true;
-    case 4: launch_split<T, D, 4>(grid, st, q, kv, Hq, Hkv, c2, part, n_split); return true;
-    case 7: launch_split<T, D, 7>(grid, st, q, kv, Hq, Hkv, c2, part, n_split); return true;
-    case 8: launch_split<T, D, 8>(grid, st, q, kv, Hq, Hkv, c2, part, n_split); return true;
+    case 1: launch_split<T, D, 1>(grid, st, q, kv, Hq, Hkv, c2, part, n_split, pps); return true;
+    case 2: launch_split<T, D, 2>(grid, st, q, kv, Hq, Hkv, c2, part, n_split, pps); return true;
+    case 4: launch_split<T, D, 4>(grid, st, q, kv, Hq, Hkv, c2, part, n_split, pps); return true;
+    case 7: launch_split<T, D, 7>(grid, st, q, kv, Hq, Hkv, c2, part, n_split, pps); return true;
+    case 8: launch_split<T, D, 8>(grid, st, q, kv, Hq, Hkv, c2, part, n_split, pps); return true;
     default: return false;
   }
 }
@@ -472,14 +477,20 @@ using namespace hk;
 bool hk_decode_supports_group(int G) { return G == 1 || G == 2 || G == 4 || G == 7 || G == 8; }
 
 size_t hk_decode_ws(int NS, int Hq, int Hkv, int D, int max_pages) {
-  const int G = Hq / Hkv, n_split = (max_pages + DEC_PPS - 1) / DEC_PPS;
+  const int G = Hq / Hkv, n_split = (max_pages + DEC_PPS_MIN - 1) / DEC_PPS_MIN;
   return (size_t)NS * Hkv * n_split * G * (D + 2) * sizeof(float);
 }
 
 hipError_t hk_launch_decode(int NS, int Hq, int Hkv, int D, const void* q, const hk_paged_kv* kv,
                             float sm_scale, float* o, float* lse, void* ws, hipStream_t st) {
   const int G = Hq / Hkv, n_heads = NS * Hkv;
-  const int n_split = (kv->max_pages + DEC_PPS - 1) / DEC_PPS;
+  // pages per split: the most (DEC_PPS) that still gives the launch DEC_TARGET_WG
+  // workgroups, down to DEC_PPS_MIN -- few heads get short splits, so no wave walks a
+  // long serial chain of pages
+  int pps = DEC_PPS;
+  while (pps > DEC_PPS_MIN && (long long)n_heads * ((kv->max_pages + pps - 1) / pps) < DEC_TARGET_WG)
+    pps >>= 1;
+  const int n_split = (kv->max_pages + pps - 1) / pps;
   const float c2 = sm_scale * kLog2e;
   float* part = static_cast<float*>(ws);
   dim3 grid(n_split, n_heads);
@@ -487,10 +498,10 @@ hipError_t hk_launch_decode(int NS, int Hq, int Hkv, int D, const void* q, const
   bool ok;
   {
   TimedLaunch t(HK_TK_DECODE_SPLIT, st);
-  if (bf && D == 128) ok = launch_split_g<uint16_t, 128>(G, grid, st, q, kv, Hq, Hkv, c2, part, n_split);
-  else if (bf) ok = launch_split_g<uint16_t, 64>(G, grid, st, q, kv, Hq, Hkv, c2, part, n_split);
-  else if (D == 128) ok = launch_split_g<float, 128>(G, grid, st, q, kv, Hq, Hkv, c2, part, n_split);
-  else ok = launch_split_g<float, 64>(G, grid, st, q, kv, Hq, Hkv, c2, part, n_split);
+  if (bf && D == 128) ok = launch_split_g<uint16_t, 128>(G, grid, st, q, kv, Hq, Hkv, c2, part, n_split, pps);
+  else if (bf) ok = launch_split_g<uint16_t, 64>(G, grid, st, q, kv, Hq, Hkv, c2, part, n_split, pps);
+  else if (D == 128) ok = launch_split_g<float, 128>(G, grid, st, q, kv, Hq, Hkv, c2, part, n_split, pps);
+  else ok = launch_split_g<float, 64>(G, grid, st, q, kv, Hq, Hkv, c2, part, n_split, pps);
   }
   if (!ok) return hipErrorInvalidValue;
   TimedLaunch t(HK_TK_DECODE_MERGE, st);

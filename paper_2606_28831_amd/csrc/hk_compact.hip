@@ -166,11 +166,21 @@ __global__ __launch_bounds__(AL_NT) void compact_alloc_kernel(int n_heads, const
 #ifndef HK_GATHER_MODE
 #define HK_GATHER_MODE 1
 #endif
+#ifndef HK_GATHER_NTLD
+#define HK_GATHER_NTLD 1      // source rows are read once: nontemporal loads
+#endif
 #ifndef HK_GATHER_NT
-#define HK_GATHER_NT 0
+#define HK_GATHER_NT 1        // rewritten rows: nontemporal stores
 #endif
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 load16(const char* p) {
+#if HK_GATHER_NTLD
+  return __builtin_bit_cast(uint4, __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p)));
+#else
+  return *reinterpret_cast<const uint4*>(p);
+#endif
+}
 __device__ __forceinline__ void store16(char* p, uint4 v) {
 #if HK_GATHER_NT
   __builtin_nontemporal_store(__builtin_bit_cast(u32x4, v), reinterpret_cast<u32x4*>(p));
@@ -218,8 +228,8 @@ __global__ __launch_bounds__(256) void compact_gather_kernel(
       for (int j = 0; j < k; ++j) mm &= mm - 1u;
       const int t = __ffs(mm) - 1;
       const size_t src = (src_page * HK_PAGE + t) * ROW_BYTES + chunk * 16;
-      kv[i] = *reinterpret_cast<const uint4*>(k_pool + src);
-      vv[i] = *reinterpret_cast<const uint4*>(v_pool + src);
+      kv[i] = load16(k_pool + src);
+      vv[i] = load16(v_pool + src);
       dst_slot[i] = rank0 + k;
     }
   }
@@ -239,8 +249,8 @@ __global__ __launch_bounds__(256) void compact_gather_kernel(
     const int t = i * RPI + sub;
     if ((m >> t) & 1u) {
       const size_t src = (src_page * HK_PAGE + t) * ROW_BYTES + chunk * 16;
-      kv[i] = *reinterpret_cast<const uint4*>(k_pool + src);
-      vv[i] = *reinterpret_cast<const uint4*>(v_pool + src);
+      kv[i] = load16(k_pool + src);
+      vv[i] = load16(v_pool + src);
     }
   }
 #pragma unroll

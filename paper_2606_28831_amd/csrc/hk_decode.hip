@@ -37,6 +37,9 @@ constexpr int DEC_PPS = HK_DEC_PPS;
 constexpr int DEC_PPS_MIN = 16;             // fewest pages per split
 constexpr int DEC_TARGET_WG = 2048;         // workgroups a launch should offer the chip
 
+#ifndef HK_DEC_NTLD
+#define HK_DEC_NTLD 0         // 1: K and V pages are read with nontemporal loads
+#endif
 #ifndef HK_DEC_WPE
 #define HK_DEC_WPE 0
 #endif
@@ -121,11 +124,19 @@ __global__ HK_DEC_ATTR void decode_split_kernel(
     r.m16 = mrow[p];
     const size_t page = (size_t)trow[p] * HK_PAGE;
     const uint4* ks = reinterpret_cast<const uint4*>(k_pool + (page + t) * D + c * DQ);
+    auto ld = [](const uint4* a) -> uint4 {
+#if HK_DEC_NTLD
+      typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+      return __builtin_bit_cast(uint4, __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(a)));
+#else
+      return *a;
+#endif
+    };
 #pragma unroll
-    for (int i = 0; i < QW / 4; ++i) r.k[i] = ks[i];
+    for (int i = 0; i < QW / 4; ++i) r.k[i] = ld(ks + i);
 #pragma unroll
     for (int i = 0; i < KPL; ++i)
-      r.v[i] = *reinterpret_cast<const uint4*>(v_pool + (page + kg * KPL + i) * D + dc * VEC);
+      r.v[i] = ld(reinterpret_cast<const uint4*>(v_pool + (page + kg * KPL + i) * D + dc * VEC));
   };
   auto process_page = [&](const PageRegs& r) {
     const uint32_t m16 = r.m16;

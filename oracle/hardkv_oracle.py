@@ -178,6 +178,31 @@ def calibrate_head(x, cand, T: float = 1.0):
     return c, lse
 
 
+def pool_max_head(x, cand, radius: int):
+    """Order-preserving pooling g of Solution 1 (Sec. 3.2, S_hat = S(g(z / T))), in its
+    SnapKV form (Sec. 4 baselines): each candidate's score becomes the maximum of the
+    candidate scores within `radius` logical slots on either side (itself included);
+    non-candidates stay -inf and are never a neighbour.  The width 2*radius + 1 is not
+    stated in the paper (reading in the design doc).  Max commutes with the monotone log, so
+    pooling log scores equals pooling the probabilities they are the logs of.
+    Pinned by: radius 0 is the identity; scipy's maximum_filter1d over the candidate-
+    masked row; a constant row stays constant; the result dominates the input.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    cand = np.asarray(cand, dtype=bool)
+    S = x.shape[0]
+    out = np.full(S, -math.inf, dtype=np.float64)
+    for j in range(S):
+        if not cand[j]:
+            continue
+        best = -math.inf
+        for i in range(max(0, j - radius), min(S, j + radius + 1)):
+            if cand[i] and x[i] > best:
+                best = x[i]
+        out[j] = best
+    return out
+
+
 def mix(cs, weights):
     """Mixture of calibrated distributions, sum_m w_m c^(m) (probability domain)."""
     out = np.zeros_like(np.asarray(cs[0], dtype=np.float64))

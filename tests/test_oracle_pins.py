@@ -189,6 +189,44 @@ def test_mixture_is_distribution():
     assert abs(c.sum() - 1) < 1e-12
 
 
+# ---------------------------------------------------------------- pooling (Solution 1, SnapKV form)
+def test_pool_radius_zero_is_identity():
+    x = RNG.standard_normal(50)
+    cand = RNG.random(50) < 0.7
+    out = O.pool_max_head(x, cand, 0)
+    assert np.array_equal(out[cand], x[cand]) and np.all(np.isneginf(out[~cand]))
+
+
+@pytest.mark.parametrize("radius", [1, 3, 8])
+def test_pool_matches_scipy_maximum_filter(radius):
+    import scipy.ndimage as ndi
+    x = RNG.standard_normal(300) * 3
+    cand = RNG.random(300) < 0.6
+    masked = np.where(cand, x, -np.inf)
+    ref = ndi.maximum_filter1d(masked, size=2 * radius + 1, mode="constant", cval=-np.inf)
+    ref = np.where(cand, ref, -np.inf)
+    assert np.array_equal(O.pool_max_head(x, cand, radius), ref)
+
+
+def test_pool_invariants():
+    x = RNG.standard_normal(200)
+    cand = RNG.random(200) < 0.5
+    out = O.pool_max_head(x, cand, 3)
+    assert np.all(out[cand] >= x[cand])                       # dominates its input
+    c = np.where(cand, 2.5, -np.inf)
+    assert np.array_equal(O.pool_max_head(c, cand, 4)[cand], np.full(cand.sum(), 2.5))
+    # a single peak spreads to exactly the candidates within the radius
+    y = np.full(40, -1.0)
+    y[20] = 5.0
+    allc = np.ones(40, bool)
+    out = O.pool_max_head(y, allc, 2)
+    assert set(np.nonzero(out == 5.0)[0]) == {18, 19, 20, 21, 22}
+    # monotone transforms commute with the pooling (so pooling log scores is pooling mass)
+    z = RNG.random(60) + 0.01
+    cz = RNG.random(60) < 0.8
+    assert np.allclose(O.pool_max_head(np.log(z), cz, 2)[cz], np.log(O.pool_max_head(z, cz, 2)[cz]))
+
+
 # ---------------------------------------------------------------- Top-p (a3)
 def test_topp_golden(golden_dir):
     g = _golden(golden_dir, "topp_hand.json")

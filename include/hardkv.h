@@ -8,6 +8,8 @@
  *   hk_calibrate_solve_T  per-head temperature for Problem 1 (App. D.1, binary search)
  *   hk_topp_select    head-adaptive Top-p budget (Sec. 3.2, Problem 1)
  *   hk_calibrate_topp hk_calibrate followed by hk_topp_select in one launch
+ *   hk_pool_max       order-preserving max-pooling of scores before calibration
+ *                     (Sec. 3.2 Solution 1, SnapKV form)
  *   hk_compact        Cascade-Cache rewrite into dense / sparse / condensed tiers
  *                     (Sec. 3.1 Step 3; Sec. 3.3.1 Rewrite Cache and Sparse Loading)
  *   hk_decode_attn    paged decode attention over the variable-budget cache with the
@@ -191,6 +193,20 @@ hk_status hk_calibrate_topp(int32_t n_heads, int32_t S_max, const int32_t* cand_
                             double p, int32_t k_min, int32_t k_max, float* c_out,
                             float* lse_out, uint32_t* sel_bits, int32_t* k_out,
                             float* sel_mass_out, int32_t* status, hipStream_t stream);
+
+/* ------------------------------------------------------------------ a2 pooling
+ * Order-preserving transform g of Solution 1 (Sec. 3.2, S_hat = S(g(z / T))) in the
+ * SnapKV form used by the paper's baselines: for every candidate j of head h,
+ *   x_out[h][j] = max { x[h][i] : i candidate, |i - j| <= radius },
+ * and x_out = -inf at non-candidates (candidates as for hk_calibrate).  Max commutes with
+ * the logarithm, so pooling log scores pools the underlying masses.  x, x_out
+ * [n_heads][S_max] fp32 device arrays, distinct (no in-place); radius in [0, 64]
+ * (radius 0 copies the candidates).  HK_ERR_ARG for a null or aliased pointer,
+ * HK_ERR_SHAPE for a radius outside [0, 64] or the S_max limits of hk_calibrate.
+ */
+hk_status hk_pool_max(int32_t n_heads, int32_t S_max, const int32_t* cand_len,
+                      const uint16_t* page_mask, const float* x, int32_t radius, float* x_out,
+                      hipStream_t stream);
 
 /* ------------------------------------------------------------------ a2': temperature
  * Temperature of Problem 1 (Sec. 3.2) by bisection (App. D.1, binary search on T):

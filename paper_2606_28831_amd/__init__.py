@@ -17,7 +17,8 @@ __all__ = ["HardKVError", "lib", "PagedKV", "Allocator", "hk_score", "hk_calibra
            "hk_calibrate_solve_T", "hk_topp_select", "hk_compact", "hk_decode_attn",
            "hk_append_kv", "hk_workspace_size", "hk_status_string", "OP_SCORE", "OP_COMPACT",
            "OP_DECODE", "OP_APPEND", "FLAG_NOSPACE", "FLAG_NAN", "FLAG_RANGE", "LIB_PATH",
-           "hk_timing_enable", "hk_timing_read", "TIMED_KERNELS", "hk_calibrate_topp"]
+           "hk_timing_enable", "hk_timing_read", "TIMED_KERNELS", "hk_calibrate_topp",
+           "hk_pool_max"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhardkv.so")
 
@@ -26,7 +27,7 @@ OP_SCORE, OP_COMPACT, OP_DECODE, OP_APPEND = 0, 1, 2, 3
 FLAG_NOSPACE, FLAG_NAN, FLAG_RANGE = 1, 2, 4
 EXPORTED = ["hk_score", "hk_calibrate", "hk_calibrate_solve_T", "hk_topp_select", "hk_compact",
             "hk_decode_attn", "hk_append_kv", "hk_workspace_size", "hk_status_string",
-            "hk_timing_enable", "hk_timing_read", "hk_calibrate_topp"]
+            "hk_timing_enable", "hk_timing_read", "hk_calibrate_topp", "hk_pool_max"]
 # kernel ids of hk_timing_read, in header order
 TIMED_KERNELS = ["score_pass1", "score_merge", "score_pass2", "calibrate", "topp", "solve_T",
                  "compact_gather", "compact_meta", "decode_split", "decode_merge", "append",
@@ -91,6 +92,8 @@ def lib():
         L.hk_calibrate_topp.argtypes = [I32, I32, P, P, I32, C.POINTER(C.c_void_p),
                                         C.POINTER(C.c_void_p), C.POINTER(C.c_float), D, I32, I32,
                                         P, P, P, P, P, P, P]
+        L.hk_pool_max.restype = I32
+        L.hk_pool_max.argtypes = [I32, I32, P, P, P, I32, P, P]
         L.hk_timing_enable.restype = I32
         L.hk_timing_enable.argtypes = [C.c_uint32]
         L.hk_timing_read.restype = I32
@@ -212,6 +215,11 @@ def hk_calibrate_topp(n_heads: int, S_max: int, cand_len, page_mask, xs, Ts, wei
                                    xa, Ta, wa, float(p), int(k_min), int(k_max), _ptr(c_out),
                                    _ptr(lse_out), _ptr(sel_bits), _ptr(k_out), _ptr(sel_mass),
                                    _ptr(status), _stream(stream)), "hk_calibrate_topp")
+
+
+def hk_pool_max(n_heads: int, S_max: int, cand_len, page_mask, x, radius: int, x_out, stream=None):
+    _check(lib().hk_pool_max(int(n_heads), int(S_max), _ptr(cand_len), _ptr(page_mask), _ptr(x),
+                             int(radius), _ptr(x_out), _stream(stream)), "hk_pool_max")
 
 
 def hk_calibrate_solve_T(n_heads: int, S_max: int, cand_len, page_mask, x, k, target_mass, T_out,

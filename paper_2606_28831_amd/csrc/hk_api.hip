@@ -176,6 +176,16 @@ hk_status hk_calibrate_topp(int32_t n_heads, int32_t S_max, const int32_t* cand_
                                        lse_out, sel_bits, k_out, sel_mass_out, status, stream));
 }
 
+hk_status hk_pool_max(int32_t n_heads, int32_t S_max, const int32_t* cand_len,
+                      const uint16_t* page_mask, const float* x, int32_t radius, float* x_out,
+                      hipStream_t stream) {
+  hk_status e = check_rows(n_heads, S_max, cand_len);
+  if (e) return e;
+  if (!x || !x_out || x == x_out) return HK_ERR_ARG;
+  if (radius < 0 || radius > 64) return HK_ERR_SHAPE;
+  return launched(hk_launch_pool_max(n_heads, S_max, cand_len, page_mask, x, radius, x_out, stream));
+}
+
 hk_status hk_calibrate_solve_T(int32_t n_heads, int32_t S_max, const int32_t* cand_len,
                                const uint16_t* page_mask, const float* x, const int32_t* k,
                                const float* target_mass, float T_lo, float T_hi, int32_t iters,

@@ -210,6 +210,8 @@ hipError_t hk_launch_calib_topp(int n_heads, int S_max, const int32_t* cand_len,
                                 const float* T1, float w0, float w1, int p_q, int k_min, int k_max,
                                 float* c_out, float* lse_out, uint32_t* sel_bits, int32_t* k_out,
                                 float* sel_mass, int32_t* status, hipStream_t st);
+hipError_t hk_launch_pool_max(int n_heads, int S_max, const int32_t* cand_len, const uint16_t* mask,
+                              const float* x, int radius, float* out, hipStream_t st);
 hipError_t hk_launch_solve_T(int n_heads, int S_max, const int32_t* cand_len,
                              const uint16_t* mask, const float* x, const int32_t* k,
                              const float* target, float T_lo, float T_hi, int iters,

@@ -396,6 +396,37 @@ __global__ __launch_bounds__(SEL_NT) void calib_topp_kernel(
                  sel_mass, status, h, list, sh, tiecnt);
 }
 
+// ------------------------------------------------------------------ a2 pooling
+// Order-preserving pooling before calibration (Solution 1, SnapKV form): candidate j gets
+// the maximum candidate score within `radius` slots on either side.  One 256-thread
+// workgroup per (head, 1024-slot tile); the tile and its halo are staged in LDS with
+// non-candidates as -inf, so a window never picks one.
+constexpr int POOL_NT = 256, POOL_TILE = 1024, POOL_RMAX = 64;
+
+__global__ __launch_bounds__(POOL_NT) void pool_max_kernel(int S_max, const int32_t* __restrict__ cand_len,
+                                                           const uint16_t* __restrict__ mask,
+                                                           const float* __restrict__ x, int radius,
+                                                           float* __restrict__ out) {
+  __shared__ float tile[POOL_TILE + 2 * POOL_RMAX];
+  const int h = blockIdx.y, j0 = blockIdx.x * POOL_TILE;
+  const int cl = cand_len[h];
+  const uint16_t* mrow = mask ? mask + (size_t)h * (S_max / HK_PAGE) : nullptr;
+  const float* xr = x + (size_t)h * S_max;
+  for (int i = threadIdx.x; i < POOL_TILE + 2 * radius; i += POOL_NT) {
+    const int j = j0 - radius + i;
+    tile[i] = (j >= 0 && j < S_max && is_cand(mrow, cl, j)) ? xr[j] : -INFINITY;
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < POOL_TILE; i += POOL_NT) {
+    const int j = j0 + i;
+    if (j >= S_max) break;
+    float m = -INFINITY;
+    if (is_cand(mrow, cl, j))
+      for (int d = 0; d <= 2 * radius; ++d) m = fmaxf(m, tile[i + d]);
+    out[(size_t)h * S_max + j] = m;
+  }
+}
+
 // ------------------------------------------------------------------ a2': temperature
 // Bisection on log T for M_k(Softmax(x/T)) = target (App. D.1; order invariance App. D.2).
 __device__ __forceinline__ uint32_t ordered_key(float x) {
@@ -541,6 +572,13 @@ hipError_t hk_launch_calib_topp(int n_heads, int S_max, const int32_t* cand_len,
                        mask, n_metrics, x0, x1, T0, T1, w0, w1, p_q, k_min, k_max, c_out, lse_out,
                        sel_bits, k_out, sel_mass, status);
   });
+  return hipGetLastError();
+}
+
+hipError_t hk_launch_pool_max(int n_heads, int S_max, const int32_t* cand_len, const uint16_t* mask,
+                              const float* x, int radius, float* out, hipStream_t st) {
+  hipLaunchKernelGGL(pool_max_kernel, dim3((S_max + POOL_TILE - 1) / POOL_TILE, n_heads), dim3(POOL_NT),
+                     0, st, S_max, cand_len, mask, x, radius, out);
   return hipGetLastError();
 }
 

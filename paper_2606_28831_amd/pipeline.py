@@ -12,13 +12,14 @@ from dataclasses import dataclass
 import torch
 
 from . import (Allocator, PagedKV, OP_APPEND, OP_COMPACT, OP_DECODE, OP_SCORE, dims, hk_append_kv,
-               hk_calibrate_solve_T, hk_calibrate_topp, hk_compact, hk_decode_attn, hk_score,
-               workspace)
+               hk_calibrate_solve_T, hk_calibrate_topp, hk_compact, hk_decode_attn, hk_pool_max,
+               hk_score, workspace)
 
 
 @dataclass
 class CompressBuffers:
     s_attn: torch.Tensor
+    s_pool: torch.Tensor | None
     x_red: torch.Tensor | None
     c: torch.Tensor
     c_attn: torch.Tensor | None
@@ -43,15 +44,18 @@ class Compressor:
     redundancy temperature solved once per head, on the first call), mixed 0.5/0.5.
     Calibration and Top-p run as one launch; keep_c=False leaves the calibrated
     probabilities on chip (buf.c / buf.c_attn are then not written).
+    pool_radius: if set, the attention-mass scores are max-pooled along the sequence
+    (Solution 1, SnapKV form) before calibration, into buf.s_pool.
     """
 
     def __init__(self, NS, Hq, Hkv, D, W, kv: PagedKV, alloc: Allocator, p: float,
                  L_dense: int = 0, L_sparse: int = 0, metric: str = "attn", n_ref: int = 0,
-                 k_max: int = 0, keep_c: bool = True):
+                 k_max: int = 0, keep_c: bool = True, pool_radius: int | None = None):
         self.d = dims(NS, Hq, Hkv, D, W)
         self.kv, self.alloc, self.p = kv, alloc, p
         self.L_dense, self.L_sparse = L_dense, L_sparse
         self.metric, self.n_ref, self.k_max, self.keep_c = metric, n_ref, k_max, keep_c
+        self.pool_radius = pool_radius
         self.sm_scale = 1.0 / math.sqrt(D)
         dev = kv.k_pool.device
         H = NS * Hkv
@@ -61,6 +65,7 @@ class Compressor:
         red = metric == "attn+red"
         self.buf = CompressBuffers(
             s_attn=torch.empty(H, S, dtype=f32, device=dev),
+            s_pool=torch.empty(H, S, dtype=f32, device=dev) if pool_radius is not None else None,
             x_red=torch.empty(H, S, dtype=f32, device=dev) if red else None,
             c=torch.empty(H, S, dtype=f32, device=dev),
             c_attn=torch.empty(H, S, dtype=f32, device=dev) if red else None,
@@ -86,18 +91,22 @@ class Compressor:
 
     def select(self, stream=None):
         b, H, S, pm = self.buf, self.n_heads, self.S_max, self.kv.page_mask
+        s_attn = b.s_attn
+        if self.pool_radius is not None:
+            hk_pool_max(H, S, b.cand_len, pm, b.s_attn, self.pool_radius, b.s_pool, stream=stream)
+            s_attn = b.s_pool
         if self.metric == "attn":
-            xs, Ts, ws = [b.s_attn], None, [1.0]
+            xs, Ts, ws = [s_attn], None, [1.0]
         else:
             if b.T_red is None:
                 # temperature of the redundancy metric, solved at the first compression only
-                hk_calibrate_topp(H, S, b.cand_len, pm, [b.s_attn], None, [1.0], self.p, b.sel_bits,
+                hk_calibrate_topp(H, S, b.cand_len, pm, [s_attn], None, [1.0], self.p, b.sel_bits,
                                   b.k_attn, c_out=b.c_attn if self.keep_c else None,
                                   sel_mass=b.mass_attn, status=b.status, stream=stream)
                 b.T_red = torch.empty(H, dtype=torch.float32, device=b.c.device)
                 hk_calibrate_solve_T(H, S, b.cand_len, pm, b.x_red, b.k_attn, b.mass_attn, b.T_red,
                                      stream=stream)
-            xs, Ts, ws = [b.s_attn, b.x_red], [None, b.T_red], [0.5, 0.5]
+            xs, Ts, ws = [s_attn, b.x_red], [None, b.T_red], [0.5, 0.5]
         hk_calibrate_topp(H, S, b.cand_len, pm, xs, Ts, ws, self.p, b.sel_bits, b.k,
                           c_out=b.c if self.keep_c else None, k_max=self.k_max,
                           sel_mass=b.sel_mass, status=b.status, stream=stream)

@@ -92,6 +92,18 @@ def test_validation_errors_without_gpu(hk):
     assert L.hk_append_kv(C.byref(d), C.byref(kv), None, P, C.byref(alloc), P, None, 0, None) == 1
     kvnull = hk.hk_paged_kv(None, P, P, P, P, 64, 4, 1)
     assert L.hk_decode_attn(C.byref(d), P, C.byref(kvnull), 0.1, P, P, P, 1 << 30, None) == 1
+    assert L.hk_pool_max(4, 128, P, None, P, 65, P + 64, None) == 3     # radius > 64
+    assert L.hk_pool_max(4, 128, P, None, P, -1, P + 64, None) == 3     # negative radius
+    assert L.hk_pool_max(4, 128, P, None, P, 3, P, None) == 1           # in place
+    assert L.hk_pool_max(4, 100, P, None, P, 3, P + 64, None) == 3      # S_max % 32
+    xs = (C.c_void_p * 1)(P)
+    wts = (C.c_float * 1)(1.0)
+    assert L.hk_calibrate_topp(4, 128, P, None, 3, xs, None, wts, 0.9, 1, 0, None, None, P, P,
+                               None, None, None) == 1                   # three metrics
+    assert L.hk_calibrate_topp(4, 128, P, None, 1, xs, None, wts, 1.5, 1, 0, None, None, P, P,
+                               None, None, None) == 1                   # p outside [0, 1]
+    assert L.hk_calibrate_topp(4, 128, P, None, 1, xs, None, wts, 0.9, 1, 0, None, None, P + 4, P,
+                               None, None, None) == 4                   # bitmap alignment
 
 
 def test_kernel_timing_host_side(hk):

@@ -662,3 +662,50 @@ def test_degenerate_heads_end_to_end():
                     check_prob(og[gi], o_ref[gi], 2e-3, f"o head {h}")
                 check_lse(lg, l_ref, 2e-3, f"lse head {h}")
     assert int(st.item()) == 0
+
+
+@pytest.mark.parametrize("name", ["bf16_d128_g4_ragged_holes", "cfg1_f32_d64_g4", "bf16_d128_g1_w32_tail1"])
+@pytest.mark.parametrize("radius", [0, 1, 3, 64])
+def test_pool_max(name, radius):
+    """Max-pooling of the scores equals the oracle bit for bit (max is exact), with masked
+    slots, a candidate boundary inside the row and tiles of 1024 slots with halos."""
+    hk, cfg, w, kv, s, cl = _calib_inputs(name)
+    H, S = w.n_heads, w.S_max
+    cl_cut = torch.clamp(cl - 37, min=0)               # a boundary that is not page-aligned
+    out = torch.full((H, S), 9.0, device=DEV)
+    hk.hk_pool_max(H, S, cl_cut, w.page_mask, s, radius, out)
+    torch.cuda.synchronize()
+    mask = np_i(w.page_mask).astype(np.int64) & 0xFFFF
+    s_np, out_np, cl_np = s.cpu().numpy(), out.cpu().numpy(), np_i(cl_cut)
+    for h in range(H):
+        valid = ((mask[h][:, None] >> np.arange(16)) & 1).reshape(-1).astype(bool)
+        cand = np.zeros(S, bool)
+        cand[:len(valid)] = O.candidate_mask(valid, int(cl_np[h]))
+        ref = O.pool_max_head(s_np[h].astype(np.float64), cand, radius)
+        assert np.array_equal(out_np[h].astype(np.float64), ref), (name, radius, h)
+
+
+def test_pool_then_select_pipeline():
+    """Compressor(pool_radius=3): pooled scores feed the fused select; Top-p equals the
+    oracle on the GPU's calibrated probabilities, and calibration matches the oracle on
+    the pooled scores."""
+    import paper_2606_28831_amd as hk
+    from paper_2606_28831_amd.pipeline import Compressor
+    hk_, cfg, w, kv = _setup("bf16_d128_g7_tempered")
+    alloc = hk.Allocator(w.free_ids, w.free_top)
+    comp = Compressor(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"], cfg["W"], kv, alloc, 0.9, pool_radius=3)
+    comp.score(w.q_obs)
+    comp.select()
+    torch.cuda.synchronize()
+    b, H, S = comp.buf, w.n_heads, w.S_max
+    mask = np_i(w.page_mask).astype(np.int64) & 0xFFFF
+    for h in range(H):
+        valid = ((mask[h][:, None] >> np.arange(16)) & 1).reshape(-1).astype(bool)
+        cand = np.zeros(S, bool)
+        cand[:len(valid)] = O.candidate_mask(valid, int(b.cand_len[h]))
+        pooled = O.pool_max_head(np64(b.s_attn[h]), cand, 3)
+        assert np.array_equal(np64(b.s_pool[h]), pooled), h
+        c_ref, _ = O.calibrate_head(pooled, cand)
+        check_prob(b.c[h].cpu().numpy(), c_ref, 2e-3, f"c head {h}")
+        r = O.topp_head(b.c[h].cpu().numpy(), cand, 0.9)
+        assert int(b.k[h]) == r.k and np.array_equal(unpack_bits(np_i(b.sel_bits[h]), S), r.sel), h

@@ -142,6 +142,9 @@ __device__ __forceinline__ void stage_rows(char* lds, int R, int R_pad, RowFn ro
   }
 }
 
+#ifndef HK_SCORE_QD
+#define HK_SCORE_QD 2     // Q fragments read from LDS this many MFMA steps ahead
+#endif
 #ifndef HK_SCORE_NT
 #define HK_SCORE_NT 512
 #endif
@@ -167,6 +170,7 @@ __device__ __forceinline__ void stage_rows(char* lds, int R, int R_pad, RowFn ro
 #endif
 
 constexpr int SCORE_NT = HK_SCORE_NT;      // threads per workgroup
+constexpr int SCORE_QD = HK_SCORE_QD;
 constexpr int SCORE_NW = SCORE_NT / 64;
 constexpr int SCORE_PPW = HK_SCORE_PPW;    // pages per workgroup
 constexpr int SCORE_KT = HK_SCORE_KT;      // 32-key tiles a wave holds at once
@@ -239,9 +243,9 @@ __device__ __forceinline__ void p2_tile_pipelined(const F* kf, const char* qlds,
                                                   float c2, int lane, float* col) {
   constexpr int KS = F::KSTEPS;
   constexpr int NF = QB * KS;
-  lds_frag_t<F> qf[3];
-  qf[0] = F::lds(qlds, 0, 0, lane);
-  if constexpr (NF > 1) qf[1] = F::lds(qlds, 1 / KS, 1 % KS, lane);
+  lds_frag_t<F> qf[SCORE_QD + 1];
+#pragma unroll
+  for (int g = 0; g < SCORE_QD && g < NF; ++g) qf[g] = F::lds(qlds, g / KS, g % KS, lane);
   f32x16 acc[2][KT];
 #pragma unroll
   for (int qb = 0; qb <= QB; ++qb) {
@@ -260,8 +264,9 @@ __device__ __forceinline__ void p2_tile_pipelined(const F* kf, const char* qlds,
       const int g = qb * KS + kk;
       if (qb < QB) {
 #pragma unroll
-        for (int t = 0; t < KT; ++t) acc[qb & 1][t] = F::mma(qf[g % 3], kf[t].v[kk], acc[qb & 1][t]);
-        if (g + 2 < NF) qf[(g + 2) % 3] = F::lds(qlds, (g + 2) / KS, (g + 2) % KS, lane);
+        for (int t = 0; t < KT; ++t) acc[qb & 1][t] = F::mma(qf[g % (SCORE_QD + 1)], kf[t].v[kk], acc[qb & 1][t]);
+        if (g + SCORE_QD < NF)
+          qf[(g + SCORE_QD) % (SCORE_QD + 1)] = F::lds(qlds, (g + SCORE_QD) / KS, (g + SCORE_QD) % KS, lane);
       }
       if (qb >= 1) {
 #pragma unroll
@@ -289,9 +294,9 @@ __device__ __forceinline__ void p1_tile_pipelined(const F* kf, const char* qlds,
                                                   float* M, float* L) {
   constexpr int KS = F::KSTEPS;
   constexpr int NF = QB * KS;
-  lds_frag_t<F> qf[3];
-  qf[0] = F::lds(qlds, 0, 0, lane);
-  if constexpr (NF > 1) qf[1] = F::lds(qlds, 1 / KS, 1 % KS, lane);
+  lds_frag_t<F> qf[SCORE_QD + 1];
+#pragma unroll
+  for (int g = 0; g < SCORE_QD && g < NF; ++g) qf[g] = F::lds(qlds, g / KS, g % KS, lane);
   f32x16 acc[2][KT];
 #pragma unroll
   for (int qb = 0; qb <= QB; ++qb) {
@@ -302,8 +307,9 @@ __device__ __forceinline__ void p1_tile_pipelined(const F* kf, const char* qlds,
       for (int kk = 0; kk < KS; ++kk) {
         const int g = qb * KS + kk;
 #pragma unroll
-        for (int t = 0; t < KT; ++t) acc[qb & 1][t] = F::mma(kf[t].v[kk], qf[g % 3], acc[qb & 1][t]);
-        if (g + 2 < NF) qf[(g + 2) % 3] = F::lds(qlds, (g + 2) / KS, (g + 2) % KS, lane);
+        for (int t = 0; t < KT; ++t) acc[qb & 1][t] = F::mma(kf[t].v[kk], qf[g % (SCORE_QD + 1)], acc[qb & 1][t]);
+        if (g + SCORE_QD < NF)
+          qf[(g + SCORE_QD) % (SCORE_QD + 1)] = F::lds(qlds, (g + SCORE_QD) / KS, (g + SCORE_QD) % KS, lane);
       }
     }
     if (qb >= 1) {

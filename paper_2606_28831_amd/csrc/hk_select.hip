@@ -119,7 +119,7 @@ __device__ __forceinline__ int count_ge(const K& key, uint32_t cbits, uint32_t t
 // Select, among elements with key == v (flags in `tie`), the `take` with the largest slot
 // index.  Returns the per-element selection bits for the ties.
 template <int EPT>
-__device__ uint32_t take_top_ties(uint32_t tie, int take, int* cnt /* LDS [EPT][SEL_NW] */) {
+__device__ __forceinline__ uint32_t take_top_ties(uint32_t tie, int take, int* cnt /* LDS [EPT][SEL_NW] */) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
   for (int i = 0; i < EPT; ++i) {

@@ -7,4 +7,7 @@ from .hardkv_oracle import (PAGE, MASS_BITS, P_QUANT, logsumexp, read_head, tier
                             candidate_mask, score_head, redundancy_head, calibrate_head,
                             mix, order_desc, topk_mass, quantise_p, fixed_weight,
                             ToppResult, topp_head, solve_T_head, PageEntry, CompactResult,
-                            compact_head, decode_head, merge_states, append_position)
+                            compact_head, decode_head, merge_states, append_position,
+                            pool_max_head, KEEP, SPARSE, REWRITE, score_rows_head,
+                            vote_head, budget_plan_head, budget_select_head,
+                            compact_mode_head)

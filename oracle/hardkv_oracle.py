@@ -27,7 +27,12 @@ Readings where the paper is silent (all listed in the design doc):
     go to the larger (more recent) slot index;
   * temperature solve: bisection in log T, fixed iteration count;
   * redundancy: -max cosine similarity against a supplied set of reference slots;
-  * tiers are age bands of whole 16-slot pages.
+  * tiers are age bands of whole 16-slot pages;
+  * Cautious Update: each window row votes with its own Top-p set of the
+    candidates; under the hard budget the base set is ranked by (votes, c,
+    slot index); attention sinks are the first n_sink logical slots;
+  * hard-budget state: rewrite when 16 * n_pages > L_upper, sparse loading when
+    the valid count exceeds L_lower, otherwise keep.
 
 Parity status of each function is given in its docstring ("pinned by ...").
 """
@@ -426,3 +431,140 @@ def append_position(mask_row, n_pages: int):
     if top >= PAGE:
         return n_pages, 0, True
     return n_pages - 1, top, False
+
+
+# ---------------------------------------------------------------------------
+# Step 4 of the pipeline (Sec. 3.1): hard budget with Cautious Update voting and
+# attention sinks; budget thresholds L_lower / L_upper (Sec. 3.3.1)
+# ---------------------------------------------------------------------------
+KEEP, SPARSE, REWRITE = 0, 1, 2      # hard-budget state of a head
+
+
+def score_rows_head(q_rows, keys, valid, cand_len: int, sm_scale: float, row_lse):
+    """Each window row's own attention probabilities over the candidates of one head:
+    a[r, j] = exp(z[r, j] - LSE_r) for candidates j, 0 for every other slot, with
+    z = sm_scale * q_r . k_j (App. F) and LSE_r the row's log-sum-exp over the valid slots.
+    These are the distributions that the Cautious Update strategy (Sec. 3.1) lets vote
+    one by one instead of through their mean (exp of score_head's s is that mean).
+    Pinned by: every row equals scipy's softmax of its logits over the valid slots; the
+    mean over rows equals exp(score_head's s); masked slots equal removed slots.
+    """
+    q = np.asarray(q_rows, dtype=np.float64)
+    k = np.asarray(keys, dtype=np.float64)
+    z = sm_scale * (q @ k.T)
+    lse = np.asarray(row_lse, dtype=np.float64)
+    cand = candidate_mask(valid, cand_len)
+    a = np.zeros((q.shape[0], k.shape[0]), dtype=np.float64)
+    for r in range(q.shape[0]):
+        for j in np.nonzero(cand)[0]:
+            a[r, j] = math.exp(z[r, j] - lse[r])
+    return a
+
+
+def vote_head(a_rows, cand, p: float):
+    """Cautious Update votes (Sec. 3.1): the window is a voting period in which every
+    query keeps its own selection.  Row r of a_rows is one window query's attention over
+    the slots; it selects its own head-adaptive Top-p set of the candidates (the a3 rule,
+    topp_head with k_min = 1), and the vote of slot j is the number of rows whose set
+    holds j.  The cumulative selection mask is votes >= 1.
+    Returns (votes [S] int, row_k [R] int, row_sel [R, S] bool).
+    Pinned by: one row reproduces topp_head; equal rows give votes in {0, R}; the row
+    order does not matter; a hand-worked three-row case.
+    """
+    a_rows = np.asarray(a_rows)
+    R, S = a_rows.shape
+    votes = np.zeros(S, dtype=np.int64)
+    row_k = np.zeros(R, dtype=np.int64)
+    row_sel = np.zeros((R, S), dtype=bool)
+    for r in range(R):
+        res = topp_head(a_rows[r], cand, p)
+        row_sel[r] = res.sel
+        row_k[r] = res.k
+        votes += res.sel
+    return votes, row_k, row_sel
+
+
+def budget_plan_head(n_pages: int, mask_row, L_dense: int, L_lower: int, L_upper: int):
+    """Hard-budget state of one head at a compression point (Sec. 3.3.1: above L_lower a
+    selection is applied by sparse loading; above L_upper the cache is rewritten into
+    contiguous pages; the budget k caps the usage at L_upper, Sec. 4 settings).
+      used  = 16 * n_pages      slots of memory the head holds
+      valid = its valid slots
+      REWRITE  if used > L_upper
+      SPARSE   elif valid > L_lower
+      KEEP     otherwise.
+    k_cap (REWRITE only; -1 = no cap) = max(0, 16 * floor(L_upper / 16) - 16 * nd), nd the
+    dense pages: the rewritten candidates then fill at most floor(L_upper/16) - nd pages,
+    so the head's new row stays within L_upper.
+    Pinned by: hand cases on each side of both thresholds, and the bound
+    16 * n_pages_after <= L_upper after budget_select + compact_mode_head.
+    """
+    nd = min(n_pages, -(-L_dense // PAGE))
+    used = PAGE * n_pages
+    valid = sum(bin(int(m) & 0xFFFF).count("1") for m in mask_row[:n_pages])
+    if used > L_upper:
+        return REWRITE, max(0, PAGE * (L_upper // PAGE) - PAGE * nd)
+    if valid > L_lower:
+        return SPARSE, -1
+    return KEEP, -1
+
+
+def budget_select_head(cand, votes=None, c=None, sel_in=None, mode: int = REWRITE,
+                       k_cap: int = -1, n_sink: int = 0):
+    """Step 4 selection under the hard budget (Sec. 3.1).
+      KEEP: every candidate (the head is left as it is).
+      otherwise:
+        sinks = candidates j < n_sink, always kept (the attention sinks that the dense tier
+                preserves, Sec. 3.1 Tier 1, and that the paper's baselines retain, Sec. 4);
+        base  = the other candidates, restricted to votes[j] >= 1 when votes are given
+                (the Cautious Update cumulative mask) and to sel_in[j] when given;
+        base is ranked by (votes desc, c desc, slot desc) -- "ranking on the votes", with
+        the calibrated probability and then recency breaking ties; absent keys count as 0
+        and c is clamped to [0, 1] with NaN as 0, as in topp_head -- and its first
+        min(|base|, cap) entries are kept, cap = max(0, k_cap - |sinks|) (no cap if k_cap < 0).
+    Returns (sel [S] bool, k = |sel|).
+    Pinned by: without votes and with sel_in = a Top-p set, the cap reproduces topp_head
+    with k_max; a cap at or above |base| keeps base; caps nest; brute force over the
+    orderings of small sets.
+    """
+    cand = np.asarray(cand, dtype=bool)
+    S = cand.shape[0]
+    if mode == KEEP:
+        return cand.copy(), int(cand.sum())
+    j_all = np.arange(S)
+    sinks = cand & (j_all < n_sink)
+    base = cand & ~sinks
+    if votes is not None:
+        base &= np.asarray(votes) >= 1
+    if sel_in is not None:
+        base &= np.asarray(sel_in, dtype=bool)
+    vv = np.zeros(S, dtype=np.int64) if votes is None else np.asarray(votes, dtype=np.int64)
+    if c is None:
+        cc = np.zeros(S)
+    else:
+        cc = np.asarray(c, dtype=np.float64)
+        cc = np.clip(np.where(np.isnan(cc), 0.0, cc), 0.0, 1.0)
+    order = sorted((int(j) for j in np.nonzero(base)[0]),
+                   key=lambda j: (-int(vv[j]), -float(cc[j]), -j))
+    n_s = int(sinks.sum())
+    cap = len(order) if k_cap < 0 else min(len(order), max(0, k_cap - n_s))
+    sel = sinks.copy()
+    sel[order[:cap]] = True
+    return sel, int(sel.sum())
+
+
+def compact_mode_head(table_row, mask_row, n_pages: int, sel, L_dense: int, mode: int):
+    """Cascade-Cache rewrite under the head's hard-budget state (Sec. 3.3.1):
+      REWRITE  every page older than the dense tier is rewritten (Rewrite Cache);
+      SPARSE   every page older than the dense tier keeps its place under the selection
+               mask (Sparse Loading), emptied pages released;
+      KEEP     nothing changes.
+    The first two are compact_head with the sparse band sized to nothing or to every
+    non-dense page.
+    """
+    if mode == KEEP:
+        pages = [PageEntry(kind="dense", mask=int(mask_row[pp]), phys=int(table_row[pp]))
+                 for pp in range(n_pages)]
+        return CompactResult(pages=pages, freed=[], n_new=0)
+    L_sparse = 0 if mode == REWRITE else PAGE * n_pages
+    return compact_head(table_row, mask_row, n_pages, sel, L_dense, L_sparse)

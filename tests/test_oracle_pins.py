@@ -478,3 +478,164 @@ def test_chain_uniform_logits_select_ceil_pN():
     c, _ = O.calibrate_head(s, valid)
     for p in (0.5, 0.9, 0.95):
         assert O.topp_head(c.astype(np.float32), valid, p).k == math.ceil(p * N)
+
+
+# ---------------------------------------------------------------- hard budget (Step 4)
+def test_score_rows_match_scipy_softmax_and_mean():
+    q, k = _rand_head(R=5, S=37, D=8, seed=21, scale=1.5)
+    valid = RNG.random(37) > 0.2
+    z = 0.7 * (q @ k.T)
+    lse = np.array([sps.logsumexp(z[r, valid]) for r in range(5)])
+    a = O.score_rows_head(q, k, valid, 37, 0.7, lse)
+    for r in range(5):
+        ref = np.zeros(37)
+        ref[valid] = sps.softmax(z[r, valid])
+        np.testing.assert_allclose(a[r], ref, rtol=1e-12, atol=0)
+    # with a dense tail, the rows are the same probabilities, zero past cand_len
+    a2 = O.score_rows_head(q, k, valid, 20, 0.7, lse)
+    np.testing.assert_array_equal(a2[:, 20:], 0.0)
+    np.testing.assert_allclose(a2[:, :20], a[:, :20], rtol=1e-15)
+    s, _ = O.score_head(q, k, valid, 37, 0.7)
+    np.testing.assert_allclose(np.log(a.mean(axis=0)[valid]), s[valid], rtol=1e-12)
+
+
+def test_vote_golden(golden_dir):
+    g = _golden(golden_dir, "vote_hand.json")
+    cand = np.array(g["valid"])
+    votes, row_k, row_sel = O.vote_head(np.array(g["a_rows"]), cand, g["p"])
+    assert votes.tolist() == g["votes"]
+    assert row_k.tolist() == g["row_k"]
+    assert row_sel.sum(axis=1).tolist() == g["row_k"]
+
+
+def test_vote_invariants():
+    r = np.random.default_rng(5)
+    S = 50
+    cand = r.random(S) > 0.15
+    a = r.dirichlet(np.full(S, 0.3), size=6)
+    for p in (0.3, 0.9, 1.0):
+        votes, row_k, row_sel = O.vote_head(a, cand, p)
+        # one row is the Top-p rule itself
+        one = O.topp_head(a[2], cand, p)
+        v1, k1, _ = O.vote_head(a[2:3], cand, p)
+        assert np.array_equal(v1 == 1, one.sel) and k1[0] == one.k
+        # the rows vote independently: any row order gives the same votes
+        vp, _, _ = O.vote_head(a[::-1], cand, p)
+        assert np.array_equal(vp, votes)
+        # votes count the rows' selections, never outside the candidates
+        assert np.array_equal(votes, row_sel.sum(axis=0))
+        assert votes[~cand].max(initial=0) == 0 and votes.max() <= 6
+    # identical rows vote together
+    same = np.repeat(a[:1], 4, axis=0)
+    vs, _, _ = O.vote_head(same, cand, 0.8)
+    assert set(np.unique(vs)) <= {0, 4}
+
+
+def test_budget_plan_cases():
+    full = [0xFFFF] * 10
+    # 10 pages = 160 slots of memory > L_upper 128: rewrite; 2 dense pages leave 96 slots
+    assert O.budget_plan_head(10, full, 32, 64, 128) == (O.REWRITE, 96)
+    # exactly L_upper is not above it; 100 valid > L_lower: sparse loading
+    holes = [0xFFFF] * 6 + [0x0FFF, 0x0FFF]
+    assert O.budget_plan_head(8, holes, 32, 64, 128) == (O.SPARSE, -1)
+    # 60 valid slots in 8 pages: keep
+    few = [0x00FF] * 7 + [0x000F]
+    assert O.budget_plan_head(8, few, 32, 64, 128) == (O.KEEP, -1)
+    # L_upper not a multiple of 16 rounds down; the dense tier may use the whole budget
+    assert O.budget_plan_head(3, full, 32, 0, 40) == (O.REWRITE, 0)
+    assert O.budget_plan_head(5, full, 0, 0, 70) == (O.REWRITE, 64)
+
+
+def test_budget_select_golden(golden_dir):
+    g = _golden(golden_dir, "vote_hand.json")["budget"]
+    cand = np.ones(len(g["votes"]), bool)
+    sel, k = O.budget_select_head(cand, votes=np.array(g["votes"]), c=np.array(g["c"]),
+                                  mode=O.REWRITE, k_cap=g["k_cap"], n_sink=g["n_sink"])
+    assert np.nonzero(sel)[0].tolist() == g["sel"] and k == len(g["sel"])
+
+
+@pytest.mark.parametrize("trial", range(30))
+def test_budget_select_ranking_brute(trial):
+    r = np.random.default_rng(100 + trial)
+    S = int(r.integers(1, 14))
+    cand = r.random(S) > 0.2
+    votes = r.integers(0, 4, S)
+    c = np.round(r.random(S), 1)           # coarse values: plenty of ties
+    n_sink = int(r.integers(0, 3))
+    k_cap = int(r.integers(-1, S + 2))
+    sel, k = O.budget_select_head(cand, votes=votes, c=c, mode=O.REWRITE, k_cap=k_cap,
+                                  n_sink=n_sink)
+    sinks = cand & (np.arange(S) < n_sink)
+    base = cand & ~sinks & (votes >= 1)
+    assert np.array_equal(sel & sinks, sinks) and not (sel & ~cand).any()
+    kept, dropped = np.nonzero(sel & base)[0], np.nonzero(base & ~sel)[0]
+    want = base.sum() if k_cap < 0 else min(base.sum(), max(0, k_cap - sinks.sum()))
+    assert len(kept) == want and k == want + sinks.sum()
+    # every kept base slot outranks every dropped one (votes, then c, then slot index)
+    for i in kept:
+        for j in dropped:
+            assert (votes[i], c[i], i) > (votes[j], c[j], j)
+
+
+def test_budget_select_reduces_to_topp_cap():
+    r = np.random.default_rng(77)
+    S = 60
+    cand = r.random(S) > 0.1
+    c = r.dirichlet(np.full(S, 0.5)).astype(np.float32)
+    c[[3, 9, 20]] = c[7]                   # ties
+    top = O.topp_head(c, cand, 0.9)
+    prev = None
+    for cap in range(0, top.k + 3):
+        sel, k = O.budget_select_head(cand, c=c, sel_in=top.sel, mode=O.REWRITE, k_cap=cap)
+        ref = O.topp_head(c, cand, 0.9, k_min=0, k_max=cap) if cap > 0 else None
+        if ref is not None:
+            assert np.array_equal(sel, ref.sel if cap < top.k else top.sel)
+        else:
+            assert k == 0
+        if prev is not None:
+            assert not (prev & ~sel).any()  # caps nest
+        prev = sel
+    # no cap keeps the Top-p set; KEEP keeps every candidate
+    assert np.array_equal(O.budget_select_head(cand, c=c, sel_in=top.sel)[0], top.sel)
+    assert np.array_equal(O.budget_select_head(cand, c=c, mode=O.KEEP)[0], cand)
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_budget_chain_respects_L_upper(seed):
+    """plan -> select -> compact: a rewritten head never holds more than L_upper slots,
+    sparse loading moves no page, and a kept head is unchanged."""
+    r = np.random.default_rng(seed)
+    n = int(r.integers(1, 40))
+    masks = [int(m) for m in r.integers(1, 1 << 16, n)]
+    masks[-1] |= 1
+    table = list(r.permutation(200)[:n])
+    n_valid = sum(bin(m).count("1") for m in masks)
+    L_dense = int(r.integers(0, 80))
+    want = seed % 3                        # thresholds drawn on the wanted side
+    if want == O.REWRITE:
+        L_upper = int(r.integers(0, 16 * n))
+        L_lower = int(r.integers(0, L_upper + 1))
+    else:
+        L_upper = 16 * n + int(r.integers(0, 100))
+        L_lower = int(r.integers(0, n_valid)) if want == O.SPARSE else n_valid + int(r.integers(0, 50))
+    mode, k_cap = O.budget_plan_head(n, masks, L_dense, L_lower, L_upper)
+    assert mode == want
+    valid = ((np.array(masks)[:, None] >> np.arange(16)) & 1).reshape(-1).astype(bool)
+    nd = O.tier_pages(n, L_dense, 0)[2]
+    cand = O.candidate_mask(valid, 16 * (n - nd))
+    votes = r.integers(0, 3, 16 * n)
+    n_sink = int(r.integers(0, 20))
+    sel, k = O.budget_select_head(cand, votes=votes, c=r.random(16 * n), mode=mode,
+                                  k_cap=k_cap, n_sink=n_sink)
+    res = O.compact_mode_head(table, masks, n, sel, L_dense, mode)
+    n_sinks = int((cand & (np.arange(16 * n) < n_sink)).sum())
+    if mode == O.REWRITE:
+        if n_sinks <= k_cap and 16 * nd <= L_upper:
+            assert 16 * len(res.pages) <= L_upper
+        assert sum(bin(p.mask).count("1") for p in res.pages if p.kind == "new") == \
+            int((sel & cand).sum())
+    elif mode == O.SPARSE:
+        kept = [p.phys for p in res.pages]
+        assert kept == [t for t in table if t in kept] and res.n_new == 0
+    else:
+        assert [p.phys for p in res.pages] == table and res.freed == []

@@ -15,6 +15,12 @@
  *   hk_decode_attn    paged decode attention over the variable-budget cache with the
  *                     attention-state merge (App. F)
  *   hk_append_kv      append-only dense-tier write of one decode step (Sec. 3.1 Step 1)
+ * Step 4 (Sec. 3.1, hard budget; Sec. 3.3.1 budget thresholds L_lower / L_upper):
+ *   hk_score_rows     each window row's own attention probabilities over the candidates
+ *   hk_vote_topp      Cautious Update: every row's own Top-p set, counted as votes
+ *   hk_budget_plan    per-head budget state (keep / sparse loading / rewrite) and cap
+ *   hk_budget_select  selection under the cap, ranked by votes, with attention sinks
+ *   hk_compact_modes  hk_compact driven by the per-head budget state
  *
  * Conventions shared by every entry point
  *   - Every tensor pointer is a DEVICE pointer owned by the caller.  The library never
@@ -267,6 +273,83 @@ hk_status hk_append_kv(const hk_dims* dims, const hk_paged_kv* kv, const void* k
                        const void* v_new, const hk_allocator* alloc, int32_t* status,
                        void* workspace, size_t ws_bytes, hipStream_t stream);
 
+/* ------------------------------------------------------------------ Step 4: hard budget
+ * The hard budget of the continuous compression pipeline (Sec. 3.1 Step 4 and the Condensed
+ * tier; Sec. 3.3.1 budget thresholds): a head whose memory exceeds L_upper is rewritten under
+ * a capped selection, one whose valid slots exceed L_lower is thinned by sparse loading, any
+ * other head is kept.  The Cautious Update strategy (Sec. 3.1) replaces the window's mean
+ * attention by votes: every window query keeps its own selection, and under a strict budget
+ * the candidates are ranked by their votes.
+ */
+enum { HK_BUDGET_KEEP = 0, HK_BUDGET_SPARSE = 1, HK_BUDGET_REWRITE = 2 };
+
+/* Per-row attention probabilities of the R = G * W window rows of every head:
+ *   a_rows[h][r][j] = exp(z[r][j] - LSE_r)   for candidate slots j (as in hk_score),
+ *                   = 0                       for every other j < S_max,
+ * z and the row order r = w * G + g as in hk_score; row_lse [W][NS][Hq] fp32 holds LSE_r
+ * (hk_score's row_lse_out, or the decode step's LSEs).  a_rows [n_heads][R][S_max] fp32,
+ * written in full: n_heads * R * S_max * 4 bytes.  Errors as for hk_score.
+ */
+hk_status hk_score_rows(const hk_dims* dims, const void* q_obs, const hk_paged_kv* kv,
+                        int32_t L_dense, float sm_scale, const float* row_lse, float* a_rows,
+                        hipStream_t stream);
+
+/* Cautious Update votes (Sec. 3.1): row r of head h selects its own head-adaptive Top-p set
+ * of the candidates under a_rows[h][r] -- the rule of hk_topp_select with k_min = 1 and no
+ * cap, same fixed-point mass, tie order, NaN and range handling -- and
+ *   votes[h][j] = number of rows r whose set holds j   (uint16, <= R).
+ * The cumulative selection mask of the strategy is votes >= 1.
+ * Arguments
+ *   a_rows   [n_heads][R][S_max] fp32 (e.g. from hk_score_rows)
+ *   votes    [n_heads][S_max] uint16, 16-byte aligned
+ *   row_sel  [n_heads][R][S_max/32] uint32, caller-owned: every row's selection bitmap
+ *   row_k    [n_heads][R] int32 or NULL: every row's selection size
+ * R in [1, 256]; p in [0, 1]; S_max a multiple of 32, at most 32768.
+ */
+hk_status hk_vote_topp(int32_t n_heads, int32_t R, int32_t S_max, const int32_t* cand_len,
+                       const uint16_t* page_mask, const float* a_rows, double p, uint16_t* votes,
+                       uint32_t* row_sel, int32_t* row_k, int32_t* status, hipStream_t stream);
+
+/* Budget state of every head at a compression point:
+ *   used = 16 * n_pages[h], valid = number of set page_mask bits of the head,
+ *   HK_BUDGET_REWRITE if used > L_upper,  HK_BUDGET_SPARSE else if valid > L_lower,
+ *   HK_BUDGET_KEEP otherwise;
+ *   k_cap[h] = max(0, 16 * floor(L_upper / 16) - 16 * nd) for REWRITE heads (nd = the
+ *   dense pages, min(n_pages, ceil(L_dense / 16))), -1 otherwise: the rewritten candidates
+ *   then fit the pages L_upper leaves beside the dense tier.
+ * head_mode, k_cap [n_heads] int32 (device).  0 <= L_lower <= L_upper; L_dense >= 0.
+ */
+hk_status hk_budget_plan(const hk_dims* dims, const hk_paged_kv* kv, int32_t L_dense,
+                         int32_t L_lower, int32_t L_upper, int32_t* head_mode, int32_t* k_cap,
+                         hipStream_t stream);
+
+/* Selection under the budget, per head:
+ *   KEEP heads: every candidate.
+ *   other heads: the sinks -- candidates j < n_sink, the attention sinks (Sec. 3.1 Tier 1;
+ *   Sec. 4 baselines) -- are always kept; the base set is the other candidates with
+ *   votes[h][j] >= 1 (if votes) and bit j of sel_in (if sel_in); it is ranked by
+ *   (votes desc, c desc, slot desc) -- a NULL votes or c counts as 0, c is clamped to [0, 1]
+ *   with NaN as 0 -- and its first min(|base|, cap) slots are kept,
+ *   cap = max(0, k_cap[h] - |sinks|), no cap when k_cap is NULL or k_cap[h] < 0.
+ * head_mode NULL treats every head as REWRITE.  Outputs sel_out [n_heads][S_max/32] uint32
+ * (16-byte aligned) and k_out [n_heads] = number of selected slots.  n_sink >= 0.
+ */
+hk_status hk_budget_select(int32_t n_heads, int32_t S_max, const int32_t* cand_len,
+                           const uint16_t* page_mask, const uint16_t* votes, const float* c,
+                           const uint32_t* sel_in, const int32_t* head_mode, const int32_t* k_cap,
+                           int32_t n_sink, uint32_t* sel_out, int32_t* k_out, hipStream_t stream);
+
+/* hk_compact with the bands set per head by its budget state instead of L_sparse:
+ *   REWRITE  every page before the dense tier is condensed (rewritten);
+ *   SPARSE   every page before the dense tier is sparse (kept under the mask);
+ *   KEEP     the row is left as it is (sel_bits is not read for it).
+ * Workspace, allocator, ordering and HK_FLAG_NOSPACE behaviour as for hk_compact
+ * (hk_workspace_size(HK_OP_COMPACT)).  head_mode [n_heads] int32 with values HK_BUDGET_*.
+ */
+hk_status hk_compact_modes(const hk_dims* dims, const hk_paged_kv* kv, const uint32_t* sel_bits,
+                           int32_t L_dense, const int32_t* head_mode, const hk_allocator* alloc,
+                           int32_t* status, void* workspace, size_t ws_bytes, hipStream_t stream);
+
 /* ------------------------------------------------------------------ kernel timing
  * Optional HIP-event timing of individual kernels, for measurement harnesses (not part of
  * the method).  hk_timing_enable(mask) selects the kernels to time: bit k of mask stands
@@ -290,7 +373,12 @@ enum {
   HK_TK_DECODE_MERGE = 9,  /* hk_decode_attn: merge of the partial states                */
   HK_TK_APPEND = 10,       /* hk_append_kv: count + write, timed together                */
   HK_TK_CALIB_TOPP = 11,   /* hk_calibrate_topp                                          */
-  HK_TK_COUNT = 12
+  HK_TK_SCORE_ROWS = 12,   /* hk_score_rows                                              */
+  HK_TK_VOTE = 13,         /* hk_vote_topp: per-row Top-p                                */
+  HK_TK_VOTE_COUNT = 14,   /* hk_vote_topp: column counts of the row bitmaps             */
+  HK_TK_BUDGET_PLAN = 15,  /* hk_budget_plan                                             */
+  HK_TK_BUDGET_SELECT = 16,/* hk_budget_select                                           */
+  HK_TK_COUNT = 17
 };
 hk_status hk_timing_enable(uint32_t kernel_mask);
 hk_status hk_timing_read(int32_t kernel, double* total_ms, int64_t* launches);

@@ -18,20 +18,24 @@ __all__ = ["HardKVError", "lib", "PagedKV", "Allocator", "hk_score", "hk_calibra
            "hk_append_kv", "hk_workspace_size", "hk_status_string", "OP_SCORE", "OP_COMPACT",
            "OP_DECODE", "OP_APPEND", "FLAG_NOSPACE", "FLAG_NAN", "FLAG_RANGE", "LIB_PATH",
            "hk_timing_enable", "hk_timing_read", "TIMED_KERNELS", "hk_calibrate_topp",
-           "hk_pool_max"]
+           "hk_pool_max", "hk_score_rows", "hk_vote_topp", "hk_budget_plan", "hk_budget_select",
+           "hk_compact_modes", "BUDGET_KEEP", "BUDGET_SPARSE", "BUDGET_REWRITE"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhardkv.so")
 
 HK_F32, HK_BF16 = 0, 1
 OP_SCORE, OP_COMPACT, OP_DECODE, OP_APPEND = 0, 1, 2, 3
 FLAG_NOSPACE, FLAG_NAN, FLAG_RANGE = 1, 2, 4
+BUDGET_KEEP, BUDGET_SPARSE, BUDGET_REWRITE = 0, 1, 2
 EXPORTED = ["hk_score", "hk_calibrate", "hk_calibrate_solve_T", "hk_topp_select", "hk_compact",
             "hk_decode_attn", "hk_append_kv", "hk_workspace_size", "hk_status_string",
-            "hk_timing_enable", "hk_timing_read", "hk_calibrate_topp", "hk_pool_max"]
+            "hk_timing_enable", "hk_timing_read", "hk_calibrate_topp", "hk_pool_max",
+            "hk_score_rows", "hk_vote_topp", "hk_budget_plan", "hk_budget_select",
+            "hk_compact_modes"]
 # kernel ids of hk_timing_read, in header order
 TIMED_KERNELS = ["score_pass1", "score_merge", "score_pass2", "calibrate", "topp", "solve_T",
                  "compact_gather", "compact_meta", "decode_split", "decode_merge", "append",
-                 "calib_topp"]
+                 "calib_topp", "score_rows", "vote", "vote_count", "budget_plan", "budget_select"]
 
 
 class HardKVError(RuntimeError):
@@ -94,6 +98,18 @@ def lib():
                                         P, P, P, P, P, P, P]
         L.hk_pool_max.restype = I32
         L.hk_pool_max.argtypes = [I32, I32, P, P, P, I32, P, P]
+        L.hk_score_rows.restype = I32
+        L.hk_score_rows.argtypes = [C.POINTER(hk_dims), P, C.POINTER(hk_paged_kv), I32, F, P, P, P]
+        L.hk_vote_topp.restype = I32
+        L.hk_vote_topp.argtypes = [I32, I32, I32, P, P, P, D, P, P, P, P, P]
+        L.hk_budget_plan.restype = I32
+        L.hk_budget_plan.argtypes = [C.POINTER(hk_dims), C.POINTER(hk_paged_kv), I32, I32, I32, P,
+                                     P, P]
+        L.hk_budget_select.restype = I32
+        L.hk_budget_select.argtypes = [I32, I32, P, P, P, P, P, P, P, I32, P, P, P]
+        L.hk_compact_modes.restype = I32
+        L.hk_compact_modes.argtypes = [C.POINTER(hk_dims), C.POINTER(hk_paged_kv), P, I32, P,
+                                       C.POINTER(hk_allocator), P, P, C.c_size_t, P]
         L.hk_timing_enable.restype = I32
         L.hk_timing_enable.argtypes = [C.c_uint32]
         L.hk_timing_read.restype = I32
@@ -247,6 +263,43 @@ def hk_append_kv(d: hk_dims, kv: PagedKV, k_new, v_new, alloc: Allocator, status
     _check(lib().hk_append_kv(C.byref(d), C.byref(kv.desc), _ptr(k_new), _ptr(v_new),
                               C.byref(alloc.desc), _ptr(status), _ptr(ws),
                               ws.numel() if ws is not None else 0, _stream(stream)), "hk_append_kv")
+
+
+def hk_score_rows(d: hk_dims, q_obs, kv: PagedKV, L_dense: int, sm_scale: float, row_lse, a_rows,
+                  stream=None):
+    _check(lib().hk_score_rows(C.byref(d), _ptr(q_obs), C.byref(kv.desc), int(L_dense),
+                               float(sm_scale), _ptr(row_lse), _ptr(a_rows), _stream(stream)),
+           "hk_score_rows")
+
+
+def hk_vote_topp(n_heads: int, R: int, S_max: int, cand_len, page_mask, a_rows, p: float, votes,
+                 row_sel, row_k=None, status=None, stream=None):
+    _check(lib().hk_vote_topp(int(n_heads), int(R), int(S_max), _ptr(cand_len), _ptr(page_mask),
+                              _ptr(a_rows), float(p), _ptr(votes), _ptr(row_sel), _ptr(row_k),
+                              _ptr(status), _stream(stream)), "hk_vote_topp")
+
+
+def hk_budget_plan(d: hk_dims, kv: PagedKV, L_dense: int, L_lower: int, L_upper: int, head_mode,
+                   k_cap, stream=None):
+    _check(lib().hk_budget_plan(C.byref(d), C.byref(kv.desc), int(L_dense), int(L_lower),
+                                int(L_upper), _ptr(head_mode), _ptr(k_cap), _stream(stream)),
+           "hk_budget_plan")
+
+
+def hk_budget_select(n_heads: int, S_max: int, cand_len, page_mask, sel_out, k_out, votes=None,
+                     c=None, sel_in=None, head_mode=None, k_cap=None, n_sink: int = 0,
+                     stream=None):
+    _check(lib().hk_budget_select(int(n_heads), int(S_max), _ptr(cand_len), _ptr(page_mask),
+                                  _ptr(votes), _ptr(c), _ptr(sel_in), _ptr(head_mode), _ptr(k_cap),
+                                  int(n_sink), _ptr(sel_out), _ptr(k_out), _stream(stream)),
+           "hk_budget_select")
+
+
+def hk_compact_modes(d: hk_dims, kv: PagedKV, sel_bits, L_dense: int, head_mode, alloc: Allocator,
+                     status, ws, stream=None):
+    _check(lib().hk_compact_modes(C.byref(d), C.byref(kv.desc), _ptr(sel_bits), int(L_dense),
+                                  _ptr(head_mode), C.byref(alloc.desc), _ptr(status), _ptr(ws),
+                                  ws.numel(), _stream(stream)), "hk_compact_modes")
 
 
 def hk_timing_enable(kernels=None):

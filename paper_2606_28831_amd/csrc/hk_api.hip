@@ -212,8 +212,82 @@ hk_status hk_compact(const hk_dims* dims, const hk_paged_kv* kv, const uint32_t*
   const int n_heads = dims->NS * dims->Hkv;
   if (!workspace || ws_bytes < hk_compact_ws(n_heads, kv->max_pages)) return HK_ERR_WORKSPACE;
   if (!aligned256(workspace)) return HK_ERR_ALIGN;
-  return launched(hk_launch_compact(n_heads, dims->D, kv, sel_bits, L_dense, L_sparse, alloc,
+  return launched(hk_launch_compact(n_heads, dims->D, kv, sel_bits, L_dense, L_sparse, nullptr,
+                                    alloc, status, workspace, stream));
+}
+
+hk_status hk_compact_modes(const hk_dims* dims, const hk_paged_kv* kv, const uint32_t* sel_bits,
+                           int32_t L_dense, const int32_t* head_mode, const hk_allocator* alloc,
+                           int32_t* status, void* workspace, size_t ws_bytes, hipStream_t stream) {
+  hk_status e = check_dims(dims, false);
+  if (e) return e;
+  if ((e = check_kv(kv, true))) return e;
+  if (!sel_bits || !head_mode || !alloc || !alloc->free_ids || !alloc->free_top || alloc->capacity <= 0)
+    return HK_ERR_ARG;
+  if (L_dense < 0) return HK_ERR_ARG;
+  if ((long long)kv->max_pages * 6 > 160 * 1024) return HK_ERR_SHAPE;
+  const int n_heads = dims->NS * dims->Hkv;
+  if (!workspace || ws_bytes < hk_compact_ws(n_heads, kv->max_pages)) return HK_ERR_WORKSPACE;
+  if (!aligned256(workspace)) return HK_ERR_ALIGN;
+  return launched(hk_launch_compact(n_heads, dims->D, kv, sel_bits, L_dense, 0, head_mode, alloc,
                                     status, workspace, stream));
+}
+
+hk_status hk_score_rows(const hk_dims* dims, const void* q_obs, const hk_paged_kv* kv,
+                        int32_t L_dense, float sm_scale, const float* row_lse, float* a_rows,
+                        hipStream_t stream) {
+  hk_status e = check_dims(dims, true);
+  if (e) return e;
+  if ((e = check_kv(kv, false))) return e;
+  if (!q_obs || !row_lse || !a_rows) return HK_ERR_ARG;
+  if (L_dense < 0 || !(sm_scale > 0.f) || !std::isfinite(sm_scale)) return HK_ERR_ARG;
+  if (dims->Hq / dims->Hkv * dims->W > 256) return HK_ERR_SHAPE;
+  if (!aligned16(q_obs)) return HK_ERR_ALIGN;
+  if (hk_score_lds_bytes(dims->Hq / dims->Hkv * dims->W, dims->D, kv->dtype == HK_BF16 ? 2 : 4,
+                         false) > 160 * 1024)
+    return HK_ERR_SHAPE;
+  return launched(hk_launch_score_rows(dims->NS, dims->Hq, dims->Hkv, dims->D, dims->W, q_obs, kv,
+                                       L_dense, sm_scale, row_lse, a_rows, stream));
+}
+
+hk_status hk_vote_topp(int32_t n_heads, int32_t R, int32_t S_max, const int32_t* cand_len,
+                       const uint16_t* page_mask, const float* a_rows, double p, uint16_t* votes,
+                       uint32_t* row_sel, int32_t* row_k, int32_t* status, hipStream_t stream) {
+  hk_status e = check_rows(n_heads, S_max, cand_len);
+  if (e) return e;
+  if (R < 1 || R > 256) return HK_ERR_SHAPE;
+  if (n_heads > 65535) return HK_ERR_SHAPE;
+  if (!a_rows || !votes || !row_sel) return HK_ERR_ARG;
+  if (!(p >= 0.0 && p <= 1.0)) return HK_ERR_ARG;
+  if (!aligned16(votes) || !aligned16(row_sel)) return HK_ERR_ALIGN;
+  const int p_q = (int)std::nearbyint(p * 1e6);
+  return launched(hk_launch_vote_topp(n_heads, R, S_max, cand_len, page_mask, a_rows, p_q, votes,
+                                      row_k, row_sel, status, stream));
+}
+
+hk_status hk_budget_plan(const hk_dims* dims, const hk_paged_kv* kv, int32_t L_dense,
+                         int32_t L_lower, int32_t L_upper, int32_t* head_mode, int32_t* k_cap,
+                         hipStream_t stream) {
+  hk_status e = check_dims(dims, false);
+  if (e) return e;
+  if ((e = check_kv(kv, false))) return e;
+  if (!head_mode || !k_cap) return HK_ERR_ARG;
+  if (L_dense < 0 || L_lower < 0 || L_upper < L_lower) return HK_ERR_ARG;
+  return launched(hk_launch_budget_plan(dims->NS * dims->Hkv, kv->max_pages, kv->n_pages,
+                                        kv->page_mask, L_dense, L_lower, L_upper, head_mode, k_cap,
+                                        stream));
+}
+
+hk_status hk_budget_select(int32_t n_heads, int32_t S_max, const int32_t* cand_len,
+                           const uint16_t* page_mask, const uint16_t* votes, const float* c,
+                           const uint32_t* sel_in, const int32_t* head_mode, const int32_t* k_cap,
+                           int32_t n_sink, uint32_t* sel_out, int32_t* k_out, hipStream_t stream) {
+  hk_status e = check_rows(n_heads, S_max, cand_len);
+  if (e) return e;
+  if (!sel_out || !k_out || n_sink < 0) return HK_ERR_ARG;
+  if (!aligned16(sel_out)) return HK_ERR_ALIGN;
+  return launched(hk_launch_budget_select(n_heads, S_max, cand_len, page_mask, votes, c, sel_in,
+                                          head_mode, k_cap, n_sink, sel_out, k_out, stream));
 }
 
 hk_status hk_decode_attn(const hk_dims* dims, const void* q, const hk_paged_kv* kv, float sm_scale,

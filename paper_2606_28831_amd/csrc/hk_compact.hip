@@ -12,6 +12,9 @@
 //   table   per head: new row [condensed][sparse][dense], masks, n_pages, released ids;
 //   push    released ids go back on the free list (after every pop has been consumed).
 // When the free list is too short, alloc raises HK_FLAG_NOSPACE and the rest do nothing.
+// Bands are age bands (dense / sparse / condensed by page position), or, under the hard
+// budget (Sec. 3.1 Step 4), set per head by its state: all older pages condensed
+// (rewrite), all sparse (sparse loading), or none (the row is kept).
 #include "hk_internal.h"
 
 namespace hk {
@@ -92,12 +95,24 @@ constexpr int CP_NT = 256;
 
 __global__ __launch_bounds__(CP_NT) void compact_plan_kernel(
     const int32_t* __restrict__ n_pages, const uint16_t* __restrict__ masks,
-    const uint32_t* __restrict__ sel_bits, int max_pages, int L_dense, int L_sparse, CompactWs w) {
+    const uint32_t* __restrict__ sel_bits, int max_pages, int L_dense, int L_sparse,
+    const int32_t* __restrict__ head_mode, CompactWs w) {
   __shared__ int lds[CP_NT / 64];
   const int h = blockIdx.x;
   const int n = n_pages[h];
-  const int nd = min(n, dense_pages(L_dense));
-  const int ns = min(n - nd, L_sparse / HK_PAGE);
+  int nd = min(n, dense_pages(L_dense));
+  int ns = min(n - nd, L_sparse / HK_PAGE);
+  if (head_mode) {
+    // bands from the head's budget state: every older page condensed, every older page
+    // sparse, or the whole row left in place (as if all dense)
+    const int mode = head_mode[h];
+    if (mode == HK_BUDGET_KEEP) {
+      nd = n;
+      ns = 0;
+    } else {
+      ns = (mode == HK_BUDGET_SPARSE) ? n - nd : 0;
+    }
+  }
   const int nc = n - nd - ns;
   const uint16_t* mrow = masks + (size_t)h * max_pages;
   const uint32_t* srow = sel_bits + (size_t)h * (max_pages / 2);
@@ -403,14 +418,14 @@ size_t hk_compact_ws(int n_heads, int max_pages) {
 }
 
 hipError_t hk_launch_compact(int n_heads, int D, const hk_paged_kv* kv, const uint32_t* sel_bits,
-                             int L_dense, int L_sparse, const hk_allocator* alloc, int32_t* status,
-                             void* ws, hipStream_t st) {
+                             int L_dense, int L_sparse, const int32_t* head_mode,
+                             const hk_allocator* alloc, int32_t* status, void* ws, hipStream_t st) {
   const CompactWs w = carve(ws, n_heads, kv->max_pages);
   const int mp = kv->max_pages;
   {
     TimedLaunch t(HK_TK_COMPACT_META, st);
     hipLaunchKernelGGL(compact_plan_kernel, dim3(n_heads), dim3(CP_NT), 0, st, kv->n_pages,
-                       kv->page_mask, sel_bits, mp, L_dense, L_sparse, w);
+                       kv->page_mask, sel_bits, mp, L_dense, L_sparse, head_mode, w);
   }
   {
     TimedLaunch t(HK_TK_COMPACT_META, st);

@@ -197,6 +197,21 @@ struct hk_score_args {
 hipError_t hk_launch_score(const hk_score_args& a, hipStream_t st);
 size_t hk_score_ws(int NS, int Hq, int Hkv, int D, int W, int max_pages);
 size_t hk_score_lds_bytes(int R, int D, int esize, bool redundancy);
+hipError_t hk_launch_score_rows(int NS, int Hq, int Hkv, int D, int W, const void* q_obs,
+                                const hk_paged_kv* kv, int L_dense, float sm_scale,
+                                const float* row_lse, float* a_rows, hipStream_t st);
+
+hipError_t hk_launch_vote_topp(int n_heads, int R, int S_max, const int32_t* cand_len,
+                               const uint16_t* mask, const float* a_rows, int p_q, uint16_t* votes,
+                               int32_t* row_k, uint32_t* row_sel, int32_t* status, hipStream_t st);
+hipError_t hk_launch_budget_plan(int n_heads, int max_pages, const int32_t* n_pages,
+                                 const uint16_t* mask, int L_dense, int L_lower, int L_upper,
+                                 int32_t* head_mode, int32_t* k_cap, hipStream_t st);
+hipError_t hk_launch_budget_select(int n_heads, int S_max, const int32_t* cand_len,
+                                   const uint16_t* mask, const uint16_t* votes, const float* c,
+                                   const uint32_t* sel_in, const int32_t* head_mode,
+                                   const int32_t* k_cap, int n_sink, uint32_t* sel_out,
+                                   int32_t* k_out, hipStream_t st);
 
 hipError_t hk_launch_calibrate(int n_heads, int S_max, const int32_t* cand_len,
                                const uint16_t* mask, int n_metrics, const float* x0,
@@ -218,8 +233,8 @@ hipError_t hk_launch_solve_T(int n_heads, int S_max, const int32_t* cand_len,
                              float* T_out, hipStream_t st);
 
 hipError_t hk_launch_compact(int n_heads, int D, const hk_paged_kv* kv, const uint32_t* sel_bits,
-                             int L_dense, int L_sparse, const hk_allocator* alloc,
-                             int32_t* status, void* ws, hipStream_t st);
+                             int L_dense, int L_sparse, const int32_t* head_mode,
+                             const hk_allocator* alloc, int32_t* status, void* ws, hipStream_t st);
 size_t hk_compact_ws(int n_heads, int max_pages);
 
 hipError_t hk_launch_decode(int NS, int Hq, int Hkv, int D, const void* q, const hk_paged_kv* kv,

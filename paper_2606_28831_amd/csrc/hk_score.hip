@@ -786,6 +786,111 @@ static size_t pass2_lds(int R_pad, int D, int es, bool red) {
   return b;
 }
 
+// ------------------------------------------------------------------ per-row probabilities
+// a[h][r][j] = exp(z[r][j] - LSE_r) for candidate slots j, 0 for every other slot: each window
+// row's own attention distribution, which the Cautious Update strategy (Sec. 3.1) lets vote
+// one by one.  Same tiles as pass 2 (C[query][key] on MFMA 32x32); each accumulator value is
+// stored instead of summed over rows.  Register e of lane l is row 8*(e/4) + 4*(l/32) + e%4 of
+// the block and key l % 32, so each half wave stores 32 consecutive floats of one row.
+template <typename T, int D, int QB>
+__global__ __launch_bounds__(SCORE_NT) void score_rows_kernel(
+    const T* __restrict__ q_obs, const T* __restrict__ k_pool, const int32_t* __restrict__ table,
+    const uint16_t* __restrict__ masks, const int32_t* __restrict__ n_pages_arr, int NS, int Hq,
+    int Hkv, int W, int max_pages, int L_dense, float c2, const float* __restrict__ row_lse,
+    float* __restrict__ a_rows) {
+  using F = Frag<T, D>;
+  constexpr int R_pad = 32 * QB;
+  extern __shared__ __align__(16) char smem[];
+  const int h = blockIdx.y, chunk = blockIdx.x;
+  const int s = h / Hkv, kv = h % Hkv, G = Hq / Hkv;
+  const int R = G * W;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const size_t S_max = (size_t)max_pages * HK_PAGE;
+  const int n = n_pages_arr[h];
+  const int cand_len = HK_PAGE * max(0, n - dense_pages(L_dense));
+  const int32_t* trow = table + (size_t)h * max_pages;
+  const uint16_t* mrow = masks + (size_t)h * max_pages;
+  const int p_begin = chunk * SCORE_PPW, p_end_all = min(p_begin + SCORE_PPW, max_pages);
+  const int p_cand_end = min(p_end_all, cand_len / HK_PAGE);
+  float* arow = a_rows + (size_t)h * R * S_max;
+
+  // slots of this chunk that hold no candidate: 0 in every row
+  {
+    const int j0 = max(p_cand_end, p_begin) * HK_PAGE, width = p_end_all * HK_PAGE - j0;
+    if (width > 0)
+      for (int i = threadIdx.x; i < R * width; i += SCORE_NT)
+        arow[(size_t)(i / width) * S_max + j0 + i % width] = 0.f;
+  }
+  if (p_begin >= p_cand_end) return;
+
+  stage_rows<T, D>(smem, R, R_pad, [&](int r) -> const T* {
+    const int w = r / G, g = r % G;
+    return q_obs + ((size_t)(w * NS + s) * Hq + kv * G + g) * D;
+  });
+  float* lse2 = reinterpret_cast<float*>(smem + (size_t)R_pad * D * sizeof(T));
+  for (int r = threadIdx.x; r < R_pad; r += SCORE_NT) {
+    float v = INFINITY;
+    if (r < R) {
+      const int w = r / G, g = r % G;
+      v = row_lse[((size_t)w * NS + s) * Hq + kv * G + g] * kLog2e;
+    }
+    lse2[r] = v;
+  }
+  __syncthreads();
+
+  const int kl = lane & 31;
+  for (int p0 = p_begin + 2 * wave; p0 < p_cand_end; p0 += 2 * SCORE_NW) {
+    F kf;
+    load_tile<T, D>(kf, k_pool, trow, p0, p_cand_end, lane);
+    const int pg = p0 + (kl >> 4);
+    const int slot = pg * HK_PAGE + (kl & 15);
+    const bool in = pg < p_cand_end;
+    const bool cand = in && (((uint32_t)mrow[pg] >> (kl & 15)) & 1u);
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      const f32x16 acc = mma_chain<F, true>(kf, smem, qb, lane);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int row = qb * 32 + acc_row(e, lane);
+        if (in && row < R) {
+          const float a = cand ? fast_exp2(fmaf(acc[e], c2, -lse2[row])) : 0.f;
+          __builtin_nontemporal_store(a, arow + (size_t)row * S_max + slot);
+        }
+      }
+    }
+  }
+}
+
+template <typename T, int D, int QB>
+hipError_t launch_score_rows_q(int NS, int Hq, int Hkv, int W, const void* q_obs,
+                               const hk_paged_kv* kv, int L_dense, float sm_scale,
+                               const float* row_lse, float* a_rows, hipStream_t st) {
+  constexpr int R_pad = 32 * QB;
+  const int n_heads = NS * Hkv;
+  const int n_chunks = (kv->max_pages + SCORE_PPW - 1) / SCORE_PPW;
+  const size_t lds = (size_t)R_pad * D * sizeof(T) + (size_t)R_pad * sizeof(float);
+  allow_dynamic_lds<score_rows_kernel<T, D, QB>>(lds);
+  TimedLaunch t(HK_TK_SCORE_ROWS, st);
+  hipLaunchKernelGGL((score_rows_kernel<T, D, QB>), dim3(n_chunks, n_heads), dim3(SCORE_NT), lds, st,
+                     static_cast<const T*>(q_obs), static_cast<const T*>(kv->k_pool), kv->page_table,
+                     kv->page_mask, kv->n_pages, NS, Hq, Hkv, W, kv->max_pages, L_dense,
+                     sm_scale * kLog2e, row_lse, a_rows);
+  return hipGetLastError();
+}
+
+template <typename T, int D>
+hipError_t launch_score_rows_t(int NS, int Hq, int Hkv, int W, const void* q_obs,
+                               const hk_paged_kv* kv, int L_dense, float sm_scale,
+                               const float* row_lse, float* a_rows, hipStream_t st) {
+  switch (qb_eff((Hq / Hkv * W + 31) / 32)) {
+    case 1: return launch_score_rows_q<T, D, 1>(NS, Hq, Hkv, W, q_obs, kv, L_dense, sm_scale, row_lse, a_rows, st);
+    case 2: return launch_score_rows_q<T, D, 2>(NS, Hq, Hkv, W, q_obs, kv, L_dense, sm_scale, row_lse, a_rows, st);
+    case 4: return launch_score_rows_q<T, D, 4>(NS, Hq, Hkv, W, q_obs, kv, L_dense, sm_scale, row_lse, a_rows, st);
+    case 7: return launch_score_rows_q<T, D, 7>(NS, Hq, Hkv, W, q_obs, kv, L_dense, sm_scale, row_lse, a_rows, st);
+    default: return launch_score_rows_q<T, D, 8>(NS, Hq, Hkv, W, q_obs, kv, L_dense, sm_scale, row_lse, a_rows, st);
+  }
+}
+
 template <typename T, int D, int QB>
 hipError_t launch_score_q(const hk_score_args& a, hipStream_t st) {
   const hk_paged_kv* kv = a.kv;
@@ -870,6 +975,16 @@ size_t hk_score_lds_bytes(int R, int D, int esize, bool redundancy) {
   const size_t p1 = hk::pass1_lds(R_pad, D, esize);
   const size_t p2 = hk::pass2_lds(R_pad, D, esize, redundancy);
   return p1 > p2 ? p1 : p2;
+}
+
+hipError_t hk_launch_score_rows(int NS, int Hq, int Hkv, int D, int W, const void* q_obs,
+                                const hk_paged_kv* kv, int L_dense, float sm_scale,
+                                const float* row_lse, float* a_rows, hipStream_t st) {
+  const bool bf = kv->dtype == HK_BF16;
+  if (bf && D == 128) return hk::launch_score_rows_t<uint16_t, 128>(NS, Hq, Hkv, W, q_obs, kv, L_dense, sm_scale, row_lse, a_rows, st);
+  if (bf && D == 64) return hk::launch_score_rows_t<uint16_t, 64>(NS, Hq, Hkv, W, q_obs, kv, L_dense, sm_scale, row_lse, a_rows, st);
+  if (!bf && D == 128) return hk::launch_score_rows_t<float, 128>(NS, Hq, Hkv, W, q_obs, kv, L_dense, sm_scale, row_lse, a_rows, st);
+  return hk::launch_score_rows_t<float, 64>(NS, Hq, Hkv, W, q_obs, kv, L_dense, sm_scale, row_lse, a_rows, st);
 }
 
 hipError_t hk_launch_score(const hk_score_args& a, hipStream_t st) {

@@ -100,3 +100,50 @@ def check_lse(gpu, ref, rtol, what="lse"):
     err = np.abs(gpu[~inf] - ref[~inf])
     bound = rtol * np.maximum(1.0, np.abs(ref[~inf]))
     assert np.all(err <= bound), f"{what}: max excess {np.max(err - bound) if err.size else 0:.3g}"
+
+
+def snapshot(w):
+    """Host copy of a workload's cache state (tables, masks, counts, free list, pools)."""
+    return dict(table=np_i(w.page_table).copy(), mask=np_i(w.page_mask).astype(np.int64) & 0xFFFF,
+                n=np_i(w.n_pages).copy(), free=np_i(w.free_ids).copy(), top=int(w.free_top.item()),
+                k=w.k_pool.detach().clone(), v=w.v_pool.detach().clone())
+
+
+def check_compaction(w, before, sel_np, S, ref_fn):
+    """The cache after a compaction call against ref_fn(h, sel) -> oracle CompactResult of
+    each head: layout, masks, kept page ids, byte-exact rewritten rows, and a free list that
+    together with the live pages accounts for every page exactly once."""
+    table, mask, n_new = np_i(w.page_table), np_i(w.page_mask).astype(np.int64) & 0xFFFF, np_i(w.n_pages)
+    top = int(w.free_top.item())
+    free = set(np_i(w.free_ids)[:top].tolist())
+    live = set()
+    new_ids = []
+    for h in range(table.shape[0]):
+        sel = unpack_bits(sel_np[h], S)
+        r = ref_fn(h, sel)
+        assert n_new[h] == len(r.pages), f"n_pages head {h}"
+        for pos, e in enumerate(r.pages):
+            pid = int(table[h, pos])
+            assert mask[h, pos] == e.mask, f"mask head {h} pos {pos}"
+            assert pid not in live
+            live.add(pid)
+            if e.kind == "new":
+                new_ids.append(pid)
+                src = torch.tensor([ph * 16 + t for ph, t in e.src], device=w.k_pool.device)
+                got_k = w.k_pool.view(-1, w.k_pool.shape[-1])[pid * 16: pid * 16 + len(e.src)]
+                got_v = w.v_pool.view(-1, w.v_pool.shape[-1])[pid * 16: pid * 16 + len(e.src)]
+                want_k = before["k"].view(-1, w.k_pool.shape[-1]).index_select(0, src)
+                want_v = before["v"].view(-1, w.v_pool.shape[-1]).index_select(0, src)
+                assert torch.equal(got_k.view(torch.int16) if got_k.dtype == torch.bfloat16 else got_k.view(torch.int32),
+                                   want_k.view(torch.int16) if want_k.dtype == torch.bfloat16 else want_k.view(torch.int32)), \
+                    f"K bytes head {h} pos {pos}"
+                assert torch.equal(got_v.view(torch.int16) if got_v.dtype == torch.bfloat16 else got_v.view(torch.int32),
+                                   want_v.view(torch.int16) if want_v.dtype == torch.bfloat16 else want_v.view(torch.int32)), \
+                    f"V bytes head {h} pos {pos}"
+            else:
+                assert pid == e.phys, f"kept page head {h} pos {pos}"
+        assert np.all(table[h, len(r.pages):] == -1)
+        assert np.all(mask[h, len(r.pages):] == 0)
+    assert live.isdisjoint(free)
+    assert len(live) + len(free) == len(before["free"]), "pages lost or duplicated"
+    assert set(new_ids) <= set(before["free"][:before["top"]].tolist())

@@ -104,6 +104,26 @@ def test_validation_errors_without_gpu(hk):
                                None, None, None) == 1                   # p outside [0, 1]
     assert L.hk_calibrate_topp(4, 128, P, None, 1, xs, None, wts, 0.9, 1, 0, None, None, P + 4, P,
                                None, None, None) == 4                   # bitmap alignment
+    # Step 4: hard budget
+    assert L.hk_score_rows(C.byref(d), P, C.byref(kv), 0, 0.125, None, P, None) == 1   # no LSE
+    assert L.hk_score_rows(C.byref(hk.dims(1, 8, 2, 128, 128)), P, C.byref(kv), 0, 0.125, P, P,
+                           None) == 3                                   # G*W > 256
+    assert L.hk_score_rows(C.byref(d), P + 4, C.byref(kv), 0, 0.125, P, P, None) == 4
+    assert L.hk_vote_topp(4, 0, 128, P, None, P, 0.9, P, P, None, None, None) == 3    # R = 0
+    assert L.hk_vote_topp(4, 257, 128, P, None, P, 0.9, P, P, None, None, None) == 3  # R > 256
+    assert L.hk_vote_topp(4, 8, 100, P, None, P, 0.9, P, P, None, None, None) == 3    # S_max % 32
+    assert L.hk_vote_topp(4, 8, 128, P, None, P, -0.1, P, P, None, None, None) == 1   # p
+    assert L.hk_vote_topp(4, 8, 128, P, None, P, 0.9, P + 2, P, None, None, None) == 4
+    assert L.hk_vote_topp(4, 8, 128, P, None, P, 0.9, P, None, None, None, None) == 1  # row_sel
+    assert L.hk_budget_plan(C.byref(d), C.byref(kv), 0, 10, 5, P, P, None) == 1   # L_upper < L_lower
+    assert L.hk_budget_plan(C.byref(d), C.byref(kv), 0, 5, 10, None, P, None) == 1
+    assert L.hk_budget_select(4, 128, P, None, None, None, None, None, None, -1, P, P, None) == 1
+    assert L.hk_budget_select(4, 128, P, None, None, None, None, None, None, 0, P + 4, P, None) == 4
+    assert L.hk_budget_select(4, 65536, P, None, None, None, None, None, None, 0, P, P, None) == 3
+    assert L.hk_compact_modes(C.byref(d), C.byref(kv), P, 0, None, C.byref(alloc), P, P, 1 << 30,
+                              None) == 1                                # no head modes
+    assert L.hk_compact_modes(C.byref(d), C.byref(kv), P, 0, P, C.byref(alloc), P, P, 16,
+                              None) == 5                                # workspace too small
 
 
 def test_kernel_timing_host_side(hk):

@@ -1,0 +1,358 @@
+"""GPU parity of the hard-budget step (Sec. 3.1 Step 4): per-row window probabilities,
+Cautious Update votes, the L_lower / L_upper budget state, vote-ranked selection with
+attention sinks, and mode-driven compaction.
+
+Inputs are seeded and synthetic.  Votes, selections, counts, states and layouts must
+match the oracle bit for bit; per-row probabilities within rtol 2e-3 (bf16 caches) or
+1e-5 (fp32 caches) per row.
+"""
+import math
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import workload as WL
+from hk_testlib import (RTOL, HostCache, check_compaction, check_prob, np64, np_i, q_rows,
+                        snapshot, unpack_bits)
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+CACHES = {
+    "cfg1_f32_d64_g4": (WL.config(1), {}),
+    "bf16_d128_g4_ragged_holes": (dict(L=1, B=2, Hq=8, Hkv=2, D=128, N=1000, dtype="bf16", W=32,
+                                       seed=11, recipe="normal"), dict(hole_prob=0.1)),
+    "bf16_d128_g7_tempered": (dict(L=1, B=2, Hq=28, Hkv=4, D=128, N=700, dtype="bf16", W=32,
+                                   seed=12, recipe="tempered"), {}),
+    "f32_d128_g8_w16": (dict(L=1, B=1, Hq=8, Hkv=1, D=128, N=520, dtype="f32", W=16, seed=14,
+                             recipe="normal"), dict(hole_prob=0.3)),
+}
+
+
+def _setup(name, **extra):
+    import paper_2606_28831_amd as hk
+    cfg, kw = CACHES[name]
+    kw = dict(kw)
+    kw.update(extra)
+    w = WL.make_workload(cfg, DEV, **kw)
+    kv = hk.PagedKV(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)
+    return hk, cfg, w, kv
+
+
+def _valid(mask_row):
+    return ((np.asarray(mask_row, np.int64)[:, None] >> np.arange(16)) & 1).reshape(-1).astype(bool)
+
+
+# ---------------------------------------------------------------- per-row probabilities
+@pytest.mark.parametrize("name", list(CACHES))
+@pytest.mark.parametrize("L_dense", [0, 48])
+def test_score_rows(name, L_dense):
+    hk, cfg, w, kv = _setup(name)
+    G = cfg["Hq"] // cfg["Hkv"]
+    R = G * cfg["W"]
+    d = hk.dims(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"], cfg["W"])
+    H, S = w.n_heads, w.S_max
+    scale = 1 / math.sqrt(cfg["D"])
+    s = torch.empty(H, S, device=DEV)
+    cl = torch.empty(H, dtype=torch.int32, device=DEV)
+    lse = torch.empty(cfg["W"], w.NS, cfg["Hq"], device=DEV)
+    hk.hk_score(d, w.q_obs, kv, L_dense, scale, s, cl, row_lse_out=lse,
+                ws=hk.workspace(hk.OP_SCORE, d, w.max_pages, DEV))
+    a = torch.full((H, R, S), 5.0, device=DEV)
+    hk.hk_score_rows(d, w.q_obs, kv, L_dense, scale, lse, a)
+    torch.cuda.synchronize()
+    host = HostCache(w.k_pool, None, w.page_table, w.page_mask, w.n_pages)
+    qn, a_np = np64(w.q_obs), np64(a)
+    rtol = RTOL[cfg["dtype"]]
+    for h in range(H):
+        rows, valid = host.head(h)
+        n = int(host.n[h])
+        cand_len = 16 * max(0, n - O.tier_pages(n, L_dense, 0)[2])
+        qr = q_rows(qn, h, cfg["Hkv"], G)
+        _, lr = O.score_head(qr, rows, valid, cand_len, scale)
+        ref = O.score_rows_head(qr, rows, valid, cand_len, scale, lr)
+        for r in range(R):
+            full = np.zeros(S)
+            full[:ref.shape[1]] = ref[r]
+            assert np.all(a_np[h, r][full == 0.0] == 0.0), (name, h, r)
+            check_prob(a_np[h, r], full, rtol, f"a head {h} row {r}")
+
+
+# ---------------------------------------------------------------- Cautious Update votes
+def _rows(kind, H, R, S, cand_len, rng):
+    """Synthetic per-row distributions over each head's first cand_len slots."""
+    a = np.zeros((H, R, S), np.float32)
+    for h in range(H):
+        n = int(cand_len[h])
+        if n == 0:
+            continue
+        for r in range(R):
+            if kind == "dirichlet":
+                a[h, r, :n] = rng.dirichlet(np.full(n, 0.4))
+            elif kind == "spread":
+                a[h, r, :n] = np.exp2(-rng.random(n) * 30.0) / n
+            elif kind == "ties":
+                a[h, r, :n] = rng.choice(np.float32([0.5, 0.25, 0.125]), n) / n
+            elif kind == "crowded":
+                a[h, r, :n] = (1.0 + rng.integers(0, 1 << 12, n) * 2.0 ** -12) / (2 * n)
+            elif kind == "mixed":
+                sub = r % 4
+                if sub == 0:
+                    pass                                   # all zero: k_min keeps one slot
+                elif sub == 1:
+                    a[h, r, rng.integers(0, n)] = 1.0      # one-hot
+                elif sub == 2:
+                    a[h, r, :n] = np.float32(1.0 / n)      # uniform: all ties
+                else:
+                    a[h, r, :n] = rng.random(n) / n
+                    if n > 3:
+                        a[h, r, 1], a[h, r, 2], a[h, r, 3] = np.nan, 3.0, -0.5
+    return a
+
+
+@pytest.mark.parametrize("kind,R,S,p", [("dirichlet", 7, 2048, 0.9), ("spread", 33, 1024, 0.9),
+                                        ("ties", 16, 2048, 0.5), ("crowded", 5, 4096, 0.95),
+                                        ("mixed", 12, 512, 0.9), ("dirichlet", 1, 64, 1.0),
+                                        ("dirichlet", 3, 32768, 0.9), ("crowded", 2, 16384, 0.9),
+                                        ("dirichlet", 128, 256, 0.0)])
+def test_vote_topp(kind, R, S, p):
+    import paper_2606_28831_amd as hk
+    rng = np.random.default_rng(zlib.crc32(f"{kind}/{R}/{S}".encode()))
+    H = 5
+    cand_len = np.array([S, S // 2 - 16, 1, 0, (S - 1) // 32 * 32 - 32 if S > 64 else 32], np.int32)
+    cand_len = np.clip(cand_len, 0, S)
+    mask = np.full((H, S // 16), 0xFFFF, np.int64)
+    mask[1, ::3] = 0x0F0F                                   # holes in one head
+    a = _rows(kind, H, R, S, cand_len, rng)
+    votes = torch.full((H, S), 7, dtype=torch.int16, device=DEV)
+    row_sel = torch.empty(H, R, S // 32, dtype=torch.int32, device=DEV)
+    row_k = torch.empty(H, R, dtype=torch.int32, device=DEV)
+    st = torch.zeros(1, dtype=torch.int32, device=DEV)
+    mask_t = torch.tensor(mask.astype(np.uint16).view(np.int16), device=DEV)
+    hk.hk_vote_topp(H, R, S, torch.tensor(cand_len, device=DEV), mask_t,
+                    torch.tensor(a, device=DEV), p, votes, row_sel, row_k=row_k, status=st)
+    torch.cuda.synchronize()
+    v_np = np_i(votes).astype(np.int64) & 0xFFFF
+    rs_np, rk_np = np_i(row_sel), np_i(row_k)
+    for h in range(H):
+        cand = O.candidate_mask(_valid(mask[h]), int(cand_len[h]))
+        ref_v, ref_k, ref_sel = O.vote_head(a[h], cand, p)
+        for r in range(R):
+            assert rk_np[h, r] == ref_k[r], (kind, h, r, rk_np[h, r], ref_k[r])
+            assert np.array_equal(unpack_bits(rs_np[h, r], S), ref_sel[r]), (kind, h, r)
+        assert np.array_equal(v_np[h], ref_v), (kind, h)
+    flag = int(st.item())
+    if kind == "mixed":
+        assert flag & hk.FLAG_NAN and flag & hk.FLAG_RANGE
+    else:
+        assert flag == 0
+
+
+# ---------------------------------------------------------------- budget state
+@pytest.mark.parametrize("name", list(CACHES))
+def test_budget_plan(name):
+    hk, cfg, w, kv = _setup(name)
+    d = hk.dims(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"], cfg["W"])
+    H = w.n_heads
+    n = np_i(w.n_pages)
+    mask = np_i(w.page_mask).astype(np.int64) & 0xFFFF
+    valid = [int(sum(bin(int(m)).count("1") for m in mask[h, :n[h]])) for h in range(H)]
+    mode = torch.empty(H, dtype=torch.int32, device=DEV)
+    cap = torch.empty(H, dtype=torch.int32, device=DEV)
+    # thresholds around the heads' own sizes so that every state occurs
+    used = sorted(16 * n)
+    cases = [(0, 0, 0), (48, min(valid) - 1, used[len(used) // 2]), (512, max(valid), max(used)),
+             (16, 10 ** 6, 10 ** 6), (32, min(valid), 16 * int(n.min()) - 1)]
+    seen = set()
+    for L_dense, L_lower, L_upper in cases:
+        L_lower = max(0, L_lower)
+        L_upper = max(L_lower, L_upper)
+        hk.hk_budget_plan(d, kv, L_dense, L_lower, L_upper, mode, cap)
+        torch.cuda.synchronize()
+        m_np, c_np = np_i(mode), np_i(cap)
+        for h in range(H):
+            ref = O.budget_plan_head(int(n[h]), mask[h], L_dense, L_lower, L_upper)
+            assert (int(m_np[h]), int(c_np[h])) == ref, (name, L_dense, L_lower, L_upper, h)
+            seen.add(ref[0])
+    assert O.REWRITE in seen and O.KEEP in seen
+
+
+# ---------------------------------------------------------------- budget selection
+@pytest.mark.parametrize("S", [64, 2048, 32768])
+@pytest.mark.parametrize("use", ["votes_c", "votes_only", "c_sel_in", "all"])
+def test_budget_select(S, use):
+    import paper_2606_28831_amd as hk
+    rng = np.random.default_rng(S + len(use))
+    H = 9
+    cand_len = rng.integers(0, S + 1, H).astype(np.int32)
+    cand_len[0], cand_len[1] = S, 0
+    mask = rng.integers(0, 1 << 16, (H, S // 16)).astype(np.int64)
+    mask[2:] = 0xFFFF
+    votes = rng.integers(0, 5, (H, S)).astype(np.int64)
+    votes[3] = 2                                            # one vote level: ranking by c
+    c = np.round(rng.random((H, S)), 2).astype(np.float32)  # coarse: ties in c as well
+    c[4] = 0.25                                             # equal keys: recency decides
+    c[5, :3] = [np.nan, 2.0, -1.0]
+    sel_in = rng.integers(-2 ** 31, 2 ** 31, (H, S // 32), dtype=np.int64).astype(np.int32)
+    modes = rng.integers(0, 3, H).astype(np.int32)
+    modes[:3] = O.REWRITE
+    caps = rng.integers(-1, S // 2, H).astype(np.int32)
+    caps[0], caps[6] = 5, 0
+    n_sink = 4 if use == "all" else 0
+    take_v = use in ("votes_c", "votes_only", "all")
+    take_c = use in ("votes_c", "c_sel_in", "all")
+    take_s = use in ("c_sel_in", "all")
+    t = lambda x, dt=None: torch.tensor(x, device=DEV) if dt is None else torch.tensor(x.astype(dt), device=DEV)
+    sel = torch.empty(H, S // 32, dtype=torch.int32, device=DEV)
+    k = torch.empty(H, dtype=torch.int32, device=DEV)
+    hk.hk_budget_select(H, S, t(cand_len), t(mask.astype(np.uint16).view(np.int16)), sel, k,
+                        votes=t(votes.astype(np.uint16).view(np.int16)) if take_v else None,
+                        c=t(c) if take_c else None, sel_in=t(sel_in) if take_s else None,
+                        head_mode=t(modes), k_cap=t(caps), n_sink=n_sink)
+    torch.cuda.synchronize()
+    sel_np, k_np = np_i(sel), np_i(k)
+    for h in range(H):
+        cand = O.candidate_mask(_valid(mask[h]), int(cand_len[h]))
+        ref, kr = O.budget_select_head(cand, votes=votes[h] if take_v else None,
+                                       c=c[h] if take_c else None,
+                                       sel_in=unpack_bits(sel_in[h], S) if take_s else None,
+                                       mode=int(modes[h]), k_cap=int(caps[h]), n_sink=n_sink)
+        assert int(k_np[h]) == kr, (S, use, h, int(k_np[h]), kr)
+        assert np.array_equal(unpack_bits(sel_np[h], S), ref), (S, use, h)
+
+
+# ---------------------------------------------------------------- mode-driven compaction
+@pytest.mark.parametrize("name", list(CACHES))
+@pytest.mark.parametrize("L_dense", [0, 48])
+def test_compact_modes(name, L_dense):
+    hk, cfg, w, kv = _setup(name, max_pages=None)
+    H, S = w.n_heads, w.S_max
+    d = hk.dims(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"], cfg["W"])
+    rng = np.random.default_rng(31 + L_dense)
+    sel_np = rng.integers(-2 ** 31, 2 ** 31, size=(H, S // 32), dtype=np.int64).astype(np.int32)
+    modes = (np.arange(H) % 3).astype(np.int32)
+    before = snapshot(w)
+    st = torch.zeros(1, dtype=torch.int32, device=DEV)
+    hk.hk_compact_modes(d, kv, torch.tensor(sel_np, device=DEV), L_dense,
+                        torch.tensor(modes, device=DEV), hk.Allocator(w.free_ids, w.free_top), st,
+                        hk.workspace(hk.OP_COMPACT, d, w.max_pages, DEV))
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    check_compaction(w, before, sel_np, S, lambda h, sel: O.compact_mode_head(
+        before["table"][h], before["mask"][h], int(before["n"][h]), sel, L_dense, int(modes[h])))
+
+
+# ---------------------------------------------------------------- the whole step
+def _mass_rule_holds(vals, sel, cand, p):
+    """Two-sided Top-p condition on fixed-point mass (exact integers), and order: every
+    selected candidate's value is at least every unselected one's."""
+    w = {j: O.fixed_weight(float(vals[j])) for j in np.nonzero(cand)[0]}
+    total = sum(w.values())
+    pq = O.quantise_p(p)
+    chosen = [j for j in w if sel[j]]
+    if not chosen:
+        return not w
+    m = sum(w[j] for j in chosen)
+    weakest = min(w[j] for j in chosen)
+    ok_mass = (10 ** 6 * m >= pq * total) and (len(chosen) == 1 or 10 ** 6 * (m - weakest) < pq * total)
+    vs = np.clip(np.nan_to_num(np.asarray(vals, np.float64)), 0, 1)
+    lo_sel = min(vs[j] for j in chosen)
+    rest = [vs[j] for j in w if not sel[j]]
+    return ok_mass and (not rest or lo_sel >= max(rest))
+
+
+def test_cautious_budget_chain():
+    """plan -> score -> rows -> votes -> budget select -> compaction on one synthetic cache.
+    The budget state and the per-row probabilities are checked against the oracle on the
+    cache itself; the later stages, whose inputs are the GPU's own probabilities, are
+    checked by properties that hold for any input: each row's set satisfies the Top-p mass
+    rule and order, votes are the column counts of the row sets, the selection keeps the
+    sinks and the best-ranked voted candidates up to the cap; compaction follows the
+    oracle for the selection it was given, and every rewritten head ends within L_upper."""
+    hk, cfg, w, kv = _setup("bf16_d128_g7_tempered")
+    G = cfg["Hq"] // cfg["Hkv"]
+    R = G * cfg["W"]
+    d = hk.dims(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"], cfg["W"])
+    H, S = w.n_heads, w.S_max
+    L_dense, L_lower, L_upper, n_sink, p = 32, 200, 400, 4, 0.9
+    scale = 1 / math.sqrt(cfg["D"])
+    # heads of different sizes first: an earlier rewrite keeps (2 + h % 6) / 8 of head h
+    j = np.arange(S)
+    keep = np.stack([(j * 7 + h) % 8 < 2 + h % 6 for h in range(H)])
+    words = (keep.reshape(H, S // 32, 32).astype(np.int64) << np.arange(32)).sum(axis=2)
+    hk.hk_compact(d, kv, torch.tensor(words.astype(np.uint32).view(np.int32), device=DEV), 0, 0,
+                  hk.Allocator(w.free_ids, w.free_top), torch.zeros(1, dtype=torch.int32, device=DEV),
+                  hk.workspace(hk.OP_COMPACT, d, w.max_pages, DEV))
+    mode = torch.empty(H, dtype=torch.int32, device=DEV)
+    cap = torch.empty(H, dtype=torch.int32, device=DEV)
+    hk.hk_budget_plan(d, kv, L_dense, L_lower, L_upper, mode, cap)
+    s = torch.empty(H, S, device=DEV)
+    cl = torch.empty(H, dtype=torch.int32, device=DEV)
+    lse = torch.empty(cfg["W"], w.NS, cfg["Hq"], device=DEV)
+    hk.hk_score(d, w.q_obs, kv, L_dense, scale, s, cl, row_lse_out=lse,
+                ws=hk.workspace(hk.OP_SCORE, d, w.max_pages, DEV))
+    a = torch.empty(H, R, S, device=DEV)
+    hk.hk_score_rows(d, w.q_obs, kv, L_dense, scale, lse, a)
+    votes = torch.empty(H, S, dtype=torch.int16, device=DEV)
+    row_sel = torch.empty(H, R, S // 32, dtype=torch.int32, device=DEV)
+    hk.hk_vote_topp(H, R, S, cl, w.page_mask, a, p, votes, row_sel)
+    sel = torch.empty(H, S // 32, dtype=torch.int32, device=DEV)
+    k = torch.empty(H, dtype=torch.int32, device=DEV)
+    hk.hk_budget_select(H, S, cl, w.page_mask, sel, k, votes=votes, c=None, head_mode=mode,
+                        k_cap=cap, n_sink=n_sink)
+    torch.cuda.synchronize()
+    host = HostCache(w.k_pool, None, w.page_table, w.page_mask, w.n_pages)
+    before = snapshot(w)
+    m_np, cap_np, cl_np, k_np = np_i(mode), np_i(cap), np_i(cl), np_i(k)
+    a_np, v_np = a.cpu().numpy(), np_i(votes).astype(np.int64) & 0xFFFF
+    rs_np, sel_np = np_i(row_sel), np_i(sel)
+    qn = np64(w.q_obs)
+    assert set(m_np.tolist()) == {O.KEEP, O.SPARSE, O.REWRITE}
+    for h in range(H):
+        n = int(host.n[h])
+        assert (int(m_np[h]), int(cap_np[h])) == O.budget_plan_head(n, host.mask[h], L_dense,
+                                                                      L_lower, L_upper)
+        rows, valid = host.head(h)
+        cand = np.zeros(S, bool)
+        cand[:len(valid)] = O.candidate_mask(valid, int(cl_np[h]))
+        qr = q_rows(qn, h, cfg["Hkv"], G)
+        _, lr = O.score_head(qr, rows, valid, int(cl_np[h]), scale)
+        ref_a = O.score_rows_head(qr, rows, valid, int(cl_np[h]), scale, lr)
+        for r in range(0, R, 37):
+            full = np.zeros(S)
+            full[:ref_a.shape[1]] = ref_a[r]
+            check_prob(a_np[h, r], full, RTOL[cfg["dtype"]], f"a head {h} row {r}")
+        bits = np.stack([unpack_bits(rs_np[h, r], S) for r in range(R)])
+        assert np.array_equal(bits.sum(axis=0), v_np[h]), h
+        for r in range(0, R, 29):
+            assert _mass_rule_holds(a_np[h, r], bits[r], cand, p), (h, r)
+        got = unpack_bits(sel_np[h], S)
+        assert not (got & ~cand).any() and int(k_np[h]) == int(got.sum())
+        if m_np[h] == O.KEEP:
+            assert np.array_equal(got, cand)
+            continue
+        sinks = cand & (np.arange(S) < n_sink)
+        base = cand & ~sinks & (v_np[h] >= 1)
+        assert np.array_equal(got & sinks, sinks) and not (got & ~sinks & ~base).any()
+        want = base.sum() if cap_np[h] < 0 else min(base.sum(), max(0, int(cap_np[h]) - sinks.sum()))
+        assert (got & base).sum() == want
+        kept = np.nonzero(got & base)[0]
+        dropped = np.nonzero(base & ~got)[0]
+        if len(kept) and len(dropped):
+            lo = min((v_np[h][j], j) for j in kept)
+            hi = max((v_np[h][j], j) for j in dropped)
+            assert lo > hi, h
+    hk.hk_compact_modes(d, kv, sel, L_dense, mode, hk.Allocator(w.free_ids, w.free_top),
+                        torch.zeros(1, dtype=torch.int32, device=DEV),
+                        hk.workspace(hk.OP_COMPACT, d, w.max_pages, DEV))
+    torch.cuda.synchronize()
+    check_compaction(w, before, sel_np, S, lambda h, sl: O.compact_mode_head(
+        before["table"][h], before["mask"][h], int(before["n"][h]), sl, L_dense, int(m_np[h])))
+    n_after = np_i(w.n_pages)
+    for h in range(H):
+        if m_np[h] == O.REWRITE:
+            assert 16 * int(n_after[h]) <= L_upper, (h, int(n_after[h]))

@@ -13,8 +13,8 @@ import torch
 
 import oracle as O
 import workload as WL
-from hk_testlib import (RTOL, HostCache, check_lse, check_log_scores, check_prob, np64, np_i,
-                        q_rows, unpack_bits)
+from hk_testlib import (RTOL, HostCache, check_compaction, check_lse, check_log_scores,
+                        check_prob, np64, np_i, q_rows, snapshot, unpack_bits)
 
 pytestmark = pytest.mark.gpu
 
@@ -328,50 +328,6 @@ def test_solve_T(case):
             assert float(T[h]) == pytest.approx(closed, rel=2e-3)
 
 
-def _snapshot(w):
-    return dict(table=np_i(w.page_table).copy(), mask=np_i(w.page_mask).astype(np.int64) & 0xFFFF,
-                n=np_i(w.n_pages).copy(), free=np_i(w.free_ids).copy(), top=int(w.free_top.item()),
-                k=w.k_pool.detach().clone(), v=w.v_pool.detach().clone())
-
-
-def _check_compaction(w, before, sel_np, L_dense, L_sparse, S):
-    table, mask, n_new = np_i(w.page_table), np_i(w.page_mask).astype(np.int64) & 0xFFFF, np_i(w.n_pages)
-    top = int(w.free_top.item())
-    free = set(np_i(w.free_ids)[:top].tolist())
-    live = set()
-    new_ids = []
-    for h in range(table.shape[0]):
-        sel = unpack_bits(sel_np[h], S)
-        r = O.compact_head(before["table"][h], before["mask"][h], int(before["n"][h]), sel,
-                           L_dense, L_sparse)
-        assert n_new[h] == len(r.pages), f"n_pages head {h}"
-        for pos, e in enumerate(r.pages):
-            pid = int(table[h, pos])
-            assert mask[h, pos] == e.mask, f"mask head {h} pos {pos}"
-            assert pid not in live
-            live.add(pid)
-            if e.kind == "new":
-                new_ids.append(pid)
-                src = torch.tensor([ph * 16 + t for ph, t in e.src], device=w.k_pool.device)
-                got_k = w.k_pool.view(-1, w.k_pool.shape[-1])[pid * 16: pid * 16 + len(e.src)]
-                got_v = w.v_pool.view(-1, w.v_pool.shape[-1])[pid * 16: pid * 16 + len(e.src)]
-                want_k = before["k"].view(-1, w.k_pool.shape[-1]).index_select(0, src)
-                want_v = before["v"].view(-1, w.v_pool.shape[-1]).index_select(0, src)
-                assert torch.equal(got_k.view(torch.int16) if got_k.dtype == torch.bfloat16 else got_k.view(torch.int32),
-                                   want_k.view(torch.int16) if want_k.dtype == torch.bfloat16 else want_k.view(torch.int32)), \
-                    f"K bytes head {h} pos {pos}"
-                assert torch.equal(got_v.view(torch.int16) if got_v.dtype == torch.bfloat16 else got_v.view(torch.int32),
-                                   want_v.view(torch.int16) if want_v.dtype == torch.bfloat16 else want_v.view(torch.int32)), \
-                    f"V bytes head {h} pos {pos}"
-            else:
-                assert pid == e.phys, f"kept page head {h} pos {pos}"
-        assert np.all(table[h, len(r.pages):] == -1)
-        assert np.all(mask[h, len(r.pages):] == 0)
-    assert live.isdisjoint(free)
-    assert len(live) + len(free) == len(before["free"]), "pages lost or duplicated"
-    assert set(new_ids) <= set(before["free"][:before["top"]].tolist())
-
-
 @pytest.mark.parametrize("name", list(CASES))
 @pytest.mark.parametrize("tiers", [(0, 0), (32, 64), (512, 2048)])
 def test_compact(name, tiers):
@@ -383,14 +339,15 @@ def test_compact(name, tiers):
     sel_np = rng.integers(-2 ** 31, 2 ** 31, size=(H, S // 32), dtype=np.int64).astype(np.int32)
     sel_np[0] = 0                               # a head whose bands select nothing
     sel = torch.tensor(sel_np, device=DEV)
-    before = _snapshot(w)
+    before = snapshot(w)
     alloc = hk.Allocator(w.free_ids, w.free_top)
     st = torch.zeros(1, dtype=torch.int32, device=DEV)
     ws = hk.workspace(hk.OP_COMPACT, d, w.max_pages, DEV)
     hk.hk_compact(d, kv, sel, L_dense, L_sparse, alloc, st, ws)
     torch.cuda.synchronize()
     assert int(st.item()) == 0
-    _check_compaction(w, before, sel_np, L_dense, L_sparse, S)
+    check_compaction(w, before, sel_np, S, lambda h, sel: O.compact_head(
+        before["table"][h], before["mask"][h], int(before["n"][h]), sel, L_dense, L_sparse))
 
 
 def test_compact_nospace_leaves_cache_unchanged():
@@ -399,7 +356,7 @@ def test_compact_nospace_leaves_cache_unchanged():
     d = hk.dims(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"], cfg["W"])
     w.free_top.fill_(1)                        # almost no free page
     sel = torch.full((H, S // 32), -1, dtype=torch.int32, device=DEV)
-    before = _snapshot(w)
+    before = snapshot(w)
     st = torch.zeros(1, dtype=torch.int32, device=DEV)
     hk.hk_compact(d, kv, sel, 0, 0, hk.Allocator(w.free_ids, w.free_top), st,
                   hk.workspace(hk.OP_COMPACT, d, w.max_pages, DEV))

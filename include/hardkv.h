@@ -136,7 +136,9 @@ const char* hk_status_string(int32_t code, int32_t flags);
  *   q_obs        [W][NS][Hq][D] in kv->dtype
  *   row_lse_in   [W][NS][Hq] fp32 or NULL (then computed: two passes over K)
  *   row_lse_out  [W][NS][Hq] fp32 or NULL
- *   s_attn       [n_heads][S_max] fp32 (written in full)
+ *   s_attn       [n_heads][S_max] fp32 (written in full), or NULL to compute only the row
+ *                LSEs and cand_len_out (pass 1; row_lse_in must then be NULL, row_lse_out
+ *                given and x_red NULL)
  *   cand_len_out [n_heads] int32
  *   ref_slots    [n_heads][n_ref] int32 or NULL; n_ref in [0, 256]; x_red likewise
  * Errors: HK_ERR_SHAPE unless D in {64,128}, Hq % Hkv == 0 and G*W <= 256.

@@ -88,7 +88,9 @@ hk_status hk_score(const hk_dims* dims, const void* q_obs, const hk_paged_kv* kv
   hk_status e = check_dims(dims, true);
   if (e) return e;
   if ((e = check_kv(kv, false))) return e;
-  if (!q_obs || !s_attn || !cand_len_out) return HK_ERR_ARG;
+  if (!q_obs || !cand_len_out) return HK_ERR_ARG;
+  // without s_attn only the row LSEs are computed: they must be computed and returned
+  if (!s_attn && (row_lse_in || !row_lse_out || x_red)) return HK_ERR_ARG;
   if (L_dense < 0 || !(sm_scale > 0.f) || !std::isfinite(sm_scale)) return HK_ERR_ARG;
   const int G = dims->Hq / dims->Hkv;
   if (G * dims->W > 256) return HK_ERR_SHAPE;

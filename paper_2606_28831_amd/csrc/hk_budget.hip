@@ -1,7 +1,7 @@
 // Step 4 of the compression pipeline (Sec. 3.1): the hard budget, with Cautious Update
 // voting and attention sinks (gfx950).
 //
-//   vote_topp    one workgroup per (head, group of window rows): each row's own Top-p
+//   vote_topp    one workgroup per (head, window row): the row's own Top-p
 //                set of the candidates under its attention probabilities (the a3 rule),
 //                written as a per-row bitmap, found by a radix search over the keys;
 //   vote_count   votes[h][j] = number of rows whose set holds j (column bit counts);
@@ -25,8 +25,12 @@ constexpr int BINS_PER_THREAD = RADIX_BINS / BG_NT;
 constexpr int BG_EPT_MAX = 64;
 constexpr float kMassScale = 1099511627776.0f;   // 2^40, fixed-point unit of the Top-p mass
 
+constexpr int BG_LIST_BYTES = 32768;   // keys of the boundary digit, staged for later rounds
+
 struct BgLds {
   unsigned long long hist[RADIX_BINS];
+  uint32_t list[BG_LIST_BYTES / 4];
+  uint16_t mrow[BG_EPT_MAX * BG_NT / HK_PAGE];   // the head's page masks
   unsigned long long red64[BG_NW];
   uint32_t redu[2][BG_NW];
   int redi[BG_NW];
@@ -129,17 +133,93 @@ __device__ __forceinline__ void block_key_range(K kmin, K kmax, BgLds& sh, K* ou
   }
 }
 
-// Largest key v of the flagged elements with W(key >= v) >= target, where W sums the
-// elements' weights (weight(key) of each); requires 0 < target <= W(all flagged).  The
+__device__ __forceinline__ uint32_t block_sum_u32(uint32_t v, uint32_t* red) {
+  v = wave_reduce_u32(v, 0u, [](uint32_t a, uint32_t b) { return a + b; });
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  uint32_t r = 0;
+#pragma unroll
+  for (int i = 0; i < BG_NW; ++i) r += red[i];
+  return r;
+}
+
+// Exclusive prefix (thread order) of one int per thread (.x) and the block sum (.y).
+__device__ __forceinline__ int2 block_exscan_bg(int v, int* red) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  __syncthreads();
+  if (lane == 63) red[wave] = x;
+  __syncthreads();
+  int before = 0, all = 0;
+#pragma unroll
+  for (int w = 0; w < BG_NW; ++w) {
+    if (w < wave) before += red[w];
+    all += red[w];
+  }
+  return make_int2(before + x - v, all);
+}
+
+// After a histogram round: the largest digit d with above + W(digits >= d) >= target, and
+// above + W(digits > d).  Thread t owns digits [t * BPT, (t + 1) * BPT); a suffix scan over
+// the threads' sums finds the one thread whose digits hold the crossing.
+__device__ __forceinline__ void pick_digit(BgLds& sh, unsigned long long target,
+                                           unsigned long long above, uint32_t* d_out,
+                                           unsigned long long* above_out) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  unsigned long long own = 0;
+#pragma unroll
+  for (int b = 0; b < BINS_PER_THREAD; ++b) own += sh.hist[tid * BINS_PER_THREAD + b];
+  unsigned long long x = own;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const unsigned long long y = __shfl_down(x, o, 64);
+    if (lane + o < 64) x += y;
+  }
+  if (lane == 0) sh.red64[wave] = x;
+  __syncthreads();
+  unsigned long long suf = x - own;
+  for (int w = wave + 1; w < BG_NW; ++w) suf += sh.red64[w];
+  const unsigned long long lo_m = above + suf;
+  if (lo_m < target && lo_m + own >= target) {
+    unsigned long long cum = lo_m;
+    for (int b = BINS_PER_THREAD - 1; b >= 0; --b) {
+      const unsigned long long nxt = cum + sh.hist[tid * BINS_PER_THREAD + b];
+      if (nxt >= target) {
+        sh.pick_digit = (uint32_t)(tid * BINS_PER_THREAD + b);
+        sh.pick_above = cum;
+        break;
+      }
+      cum = nxt;
+    }
+  }
+  __syncthreads();
+  *d_out = sh.pick_digit;
+  *above_out = sh.pick_above;
+}
+
+// Largest key v of the member elements with W(key >= v) >= target, where W sums the
+// elements' weights (weight(key) of each); requires 0 < target <= W(all members).  Member
+// keys have their top bit clear; every other element holds the all-ones key, which the
+// prefix tests below exclude, so no per-element flags are needed.  The
 // bits above the highest one where the flagged keys differ are common to all of them,
 // hence to v; below them v is found RADIX_BITS at a time from a histogram of weights per
-// digit (LDS atomics) and a suffix scan over the digits.  Returns v and, in *above,
-// W(key > v).
+// digit (LDS atomics) and a suffix scan over the digits.  The first round reads the keys
+// in registers; the keys that share the digits found so far are then packed into an LDS
+// list (when they fit) and the remaining rounds read only that list.  Returns v and, in
+// *above, W(key > v).
 template <int EPT, typename K, typename WF>
-__device__ __forceinline__ K radix_threshold(const K* key, uint64_t flags, unsigned long long target,
+__device__ __forceinline__ K radix_threshold(const K* key, unsigned long long target,
                                              WF weight, K kmin, K kmax, BgLds& sh,
                                              unsigned long long* above_out) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  constexpr int CAP = BG_LIST_BYTES / (int)sizeof(K);
+  const int tid = threadIdx.x;
+  K* list = reinterpret_cast<K*>(sh.list);
   if (kmin == kmax) {
     *above_out = 0;
     return kmin;
@@ -147,6 +227,7 @@ __device__ __forceinline__ K radix_threshold(const K* key, uint64_t flags, unsig
   int pos = highest_bit<K>(kmin ^ kmax) + 1;
   K prefix = kmin & ~low_mask<K>(pos);
   unsigned long long above = 0;
+  int n_list = -1;                   // < 0: keys still read from registers
   while (pos > 0) {
     const int nb = min(RADIX_BITS, pos), lo = pos - nb;
     const K hi_mask = ~low_mask<K>(pos);
@@ -155,49 +236,43 @@ __device__ __forceinline__ K radix_threshold(const K* key, uint64_t flags, unsig
 #pragma unroll
     for (int b = 0; b < BINS_PER_THREAD; ++b) sh.hist[tid * BINS_PER_THREAD + b] = 0ull;
     __syncthreads();
-    const uint64_t fl = opaque(flags);
+    if (n_list < 0) {
 #pragma unroll
-    for (int i = 0; i < EPT; ++i) {
-      // (an opaque key keeps the compiler from hoisting the EPT weights, which do not
-      // change between rounds, into registers of their own: they would spill)
-      const K k = opaque(key[i]);
-      if (((fl >> i) & 1ull) && (k & hi_mask) == prefix) {
-        const unsigned long long wt = weight(k);
-        if (wt) atomicAdd(&sh.hist[(uint32_t)(k >> lo) & dmask], wt);
+      for (int i = 0; i < EPT; ++i) {
+        // (an opaque key keeps the compiler from hoisting the EPT weights, which do not
+        // change between rounds, into registers of their own: they would spill)
+        const K k = opaque(key[i]);
+        if ((k & hi_mask) == prefix)
+          atomicAdd(&sh.hist[(uint32_t)(k >> lo) & dmask], weight(k));
+      }
+    } else {
+      for (int j = tid; j < n_list; j += BG_NT) {
+        const K k = list[j];
+        if ((k & hi_mask) == prefix) atomicAdd(&sh.hist[(uint32_t)(k >> lo) & dmask], weight(k));
       }
     }
     __syncthreads();
-    // thread t owns digits [t * BPT, (t + 1) * BPT); suffix sums over threads
-    unsigned long long own = 0;
-#pragma unroll
-    for (int b = 0; b < BINS_PER_THREAD; ++b) own += sh.hist[tid * BINS_PER_THREAD + b];
-    unsigned long long x = own;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const unsigned long long y = __shfl_down(x, o, 64);
-      if (lane + o < 64) x += y;
-    }
-    if (lane == 0) sh.red64[wave] = x;
-    __syncthreads();
-    unsigned long long suf = x - own;
-    for (int w = wave + 1; w < BG_NW; ++w) suf += sh.red64[w];
-    const unsigned long long lo_m = above + suf;
-    if (lo_m < target && lo_m + own >= target) {
-      unsigned long long cum = lo_m;
-      for (int b = BINS_PER_THREAD - 1; b >= 0; --b) {
-        const unsigned long long nxt = cum + sh.hist[tid * BINS_PER_THREAD + b];
-        if (nxt >= target) {
-          sh.pick_digit = (uint32_t)(tid * BINS_PER_THREAD + b);
-          sh.pick_above = cum;
-          break;
-        }
-        cum = nxt;
-      }
-    }
-    __syncthreads();
-    prefix |= (K)sh.pick_digit << lo;
-    above = sh.pick_above;
+    uint32_t d;
+    pick_digit(sh, target, above, &d, &above);
+    prefix |= (K)d << lo;
     pos = lo;
+    if (pos > 0 && n_list < 0) {
+      // stage the keys that share the digits found so far, if they fit
+      const K m2 = ~low_mask<K>(pos);
+      int cnt = 0;
+#pragma unroll
+      for (int i = 0; i < EPT; ++i) cnt += ((opaque(key[i]) & m2) == prefix) ? 1 : 0;
+      const int2 sc = block_exscan_bg(cnt, sh.redi);
+      if (sc.y <= CAP) {
+        int off = sc.x;
+#pragma unroll
+        for (int i = 0; i < EPT; ++i) {
+          const K k = opaque(key[i]);
+          if ((k & m2) == prefix) list[off++] = k;
+        }
+        n_list = sc.y;
+      }
+    }
   }
   *above_out = above;
   return prefix;
@@ -233,16 +308,26 @@ __device__ __forceinline__ uint64_t take_top_ties_bg(uint64_t tie, int take, int
   return out;
 }
 
+// Candidate flags of the thread's elements.  The head's page masks are staged in LDS by
+// coalesced loads first: per-element global loads would each hold an address pair and a
+// value in registers while in flight, and inside per-element branches they would be
+// waited on one by one.
 template <int EPT>
 __device__ __forceinline__ uint64_t cand_flags(int h, int S_max, const int32_t* __restrict__ cand_len,
-                                               const uint16_t* __restrict__ mask) {
-  const int cl = cand_len[h];
-  const uint16_t* mrow = mask ? mask + (size_t)h * (S_max / HK_PAGE) : nullptr;
+                                               const uint16_t* __restrict__ mask, BgLds& sh) {
+  const int cl = min(cand_len[h], S_max);
+  const int np = S_max / HK_PAGE;
+  if (mask) {
+    const uint16_t* mrow = mask + (size_t)h * np;
+    for (int q = threadIdx.x; q < np; q += BG_NT) sh.mrow[q] = mrow[q];
+  }
+  __syncthreads();
   uint64_t f = 0;
 #pragma unroll
   for (int i = 0; i < EPT; ++i) {
     const int j = threadIdx.x + BG_NT * i;
-    if (j < S_max && is_cand(mrow, cl, j)) f |= 1ull << i;
+    const bool ok = j < cl && (!mask || (((uint32_t)sh.mrow[j >> 4] >> (j & 15)) & 1u));
+    f |= ok ? 1ull << i : 0ull;
   }
   return f;
 }
@@ -266,83 +351,100 @@ __device__ __forceinline__ void write_bitmap(uint64_t sel, uint32_t* __restrict_
 }
 
 // ------------------------------------------------------------------ Cautious Update votes
+// Four waves per SIMD (two workgroups per CU) cap the registers at 128: the allocator
+// then keeps fewer loads in flight rather than lowering the occupancy.
 template <int EPT>
-__global__ __launch_bounds__(BG_NT) void vote_topp_kernel(
-    int R, int S_max, int rows_per_wg, const int32_t* __restrict__ cand_len,
+__global__ __launch_bounds__(BG_NT) __attribute__((amdgpu_waves_per_eu(4, 8))) void vote_topp_kernel(
+    int R, int S_max, const int32_t* __restrict__ cand_len,
     const uint16_t* __restrict__ mask, const float* __restrict__ a_rows, int p_q,
     uint32_t* __restrict__ row_sel, int32_t* __restrict__ row_k, int32_t* __restrict__ status) {
   __shared__ BgLds sh;
+  constexpr uint32_t NONE = 0xffffffffu;  // key of a non-candidate (candidates are <= 1.0f)
   const int h = blockIdx.y, tid = threadIdx.x;
-  const uint64_t cf = cand_flags<EPT>(h, S_max, cand_len, mask);
-  const int n_cand = block_sum_int<BG_NT>(__popcll(cf), sh.redi);
-  const int r0 = blockIdx.x * rows_per_wg, r1 = min(R, r0 + rows_per_wg);
-  int flags_all = 0;
-  for (int r = r0; r < r1; ++r) {
-    const float* arow = a_rows + ((size_t)h * R + r) * S_max;
-    const int t = opaque(tid);       // per-row copy: element addresses are not hoisted
-    uint32_t key[EPT];
-    int flags = 0;
-    uint32_t kmin = 0xffffffffu, kmax = 0u;
-    double m = 0.0;
-    const uint64_t f1 = opaque(cf);  // per-row copy: per-element tests are not hoisted
+  // one row per workgroup: a loop over rows would let the compiler keep per-element
+  // addresses, masks and constants in registers across rows
+  const int r = blockIdx.x;
+  const uint64_t cf = cand_flags<EPT>(h, S_max, cand_len, mask, sh);
+  const float* arow = a_rows + ((size_t)h * R + r) * S_max;
+  uint32_t key[EPT];
+  int flags = 0;
+  uint32_t kmin = NONE, kmax = 0u;
+  double m = 0.0;
+  // every load first (index clamped into the row), then the per-element work
 #pragma unroll
-    for (int i = 0; i < EPT; ++i) {
-      float v = 0.f;
-      if ((f1 >> i) & 1ull) {
-        v = arow[t + BG_NT * i];
-        if (v != v) { v = 0.f; flags |= HK_FLAG_NAN; }
-        if (v > 1.f) { v = 1.f; flags |= HK_FLAG_RANGE; }
-        if (v < 0.f) { v = 0.f; flags |= HK_FLAG_RANGE; }
-        if (v == 0.f) v = 0.f;                    // canonical +0
-      }
+  for (int i = 0; i < EPT; ++i) key[i] = __float_as_uint(arow[min(tid + BG_NT * i, S_max - 1)]);
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) {
+    float v = __uint_as_float(key[i]);
+    key[i] = NONE;
+    if ((cf >> i) & 1ull) {
+      if (v != v) { v = 0.f; flags |= HK_FLAG_NAN; }
+      if (v > 1.f) { v = 1.f; flags |= HK_FLAG_RANGE; }
+      if (v < 0.f) { v = 0.f; flags |= HK_FLAG_RANGE; }
+      if (v == 0.f) v = 0.f;                    // canonical +0
       key[i] = __float_as_uint(v);
-      if ((f1 >> i) & 1ull) {
-        kmin = min(kmin, key[i]);
-        kmax = max(kmax, key[i]);
-        m += (double)truncf(v * kMassScale);      // exact: see mass_weight
-      }
+      kmin = min(kmin, key[i]);
+      kmax = max(kmax, key[i]);
+      m += (double)truncf(v * kMassScale);      // exact: see mass_weight
     }
-    flags_all |= flags;
-    const unsigned long long tot = block_sum_u64<BG_NT>((unsigned long long)m, sh.red64);
-    block_key_range<uint32_t>(kmin, kmax, sh, &kmin, &kmax);
-    const unsigned long long pq = (unsigned long long)p_q;
-    const unsigned long long target =
-        pq * (tot / 1000000ull) + (pq * (tot % 1000000ull) + 999999ull) / 1000000ull;
-    uint32_t v = 0xffffffffu;
-    int take = 0, k = 0;
-    if (target > 0) {
-      unsigned long long mass_gt = 0;
-      v = radix_threshold<EPT, uint32_t>(key, f1, target, [](uint32_t k) { return mass_weight(k); },
-                                         kmin, kmax, sh, &mass_gt);
-      const unsigned long long wv = mass_weight(v);         // > 0: the crossing element weighs
-      take = (int)((target - mass_gt + wv - 1) / wv);
-      int gt = 0;
-      const uint64_t f2 = opaque(cf);
+  }
+  // one block reduction for the row's total mass and key range
+  unsigned long long tot = wave_sum_u64((unsigned long long)m);
+  kmin = wave_reduce_u32(kmin, NONE, [](uint32_t a, uint32_t b) { return a < b ? a : b; });
+  kmax = wave_reduce_u32(kmax, 0u, [](uint32_t a, uint32_t b) { return a > b ? a : b; });
+  {
+    const int w = tid >> 6;
+    if ((tid & 63) == 0) {
+      sh.red64[w] = tot;
+      sh.redu[0][w] = kmin;
+      sh.redu[1][w] = kmax;
+    }
+    __syncthreads();
+    tot = sh.red64[0];
+    kmin = sh.redu[0][0];
+    kmax = sh.redu[1][0];
 #pragma unroll
-      for (int i = 0; i < EPT; ++i) gt += (((f2 >> i) & 1ull) && opaque(key[i]) > v) ? 1 : 0;
-      k = block_sum_int<BG_NT>(gt, sh.redi) + take;
-    } else if (n_cand > 0) {
-      // no mass to reach: k_min = 1 keeps the largest value, the most recent on ties
-      v = kmax;
-      take = 1;
-      k = 1;
+    for (int i = 1; i < BG_NW; ++i) {
+      tot += sh.red64[i];
+      kmin = min(kmin, sh.redu[0][i]);
+      kmax = max(kmax, sh.redu[1][i]);
     }
-    uint64_t sel = 0, tie = 0;
-    const uint64_t f3 = opaque(cf);
+  }
+  const unsigned long long pq = (unsigned long long)p_q;
+  const unsigned long long target =
+      pq * (tot / 1000000ull) + (pq * (tot % 1000000ull) + 999999ull) / 1000000ull;
+  uint32_t v = NONE;
+  int take = 0;
+  if (target > 0) {
+    unsigned long long mass_gt = 0;
+    v = radix_threshold<EPT, uint32_t>(key, target, [](uint32_t k) { return mass_weight(k); },
+                                       kmin, kmax, sh, &mass_gt);
+    const unsigned long long wv = mass_weight(v);         // > 0: the crossing element weighs
+    take = (int)((target - mass_gt + wv - 1) / wv);
+  } else if (kmin != NONE) {
+    // no mass to reach: k_min = 1 keeps the largest value, the most recent on ties
+    v = kmax;
+    take = 1;
+  }
+  uint64_t sel = 0, tie = 0;
+  if (v != NONE) {
 #pragma unroll
     for (int i = 0; i < EPT; ++i) {
-      const uint32_t k = opaque(key[i]);
-      if ((f3 >> i) & 1ull) {
-        if (v != 0xffffffffu && k > v) sel |= 1ull << i;
-        if (k == v) tie |= 1ull << i;
-      }
+      const uint32_t kk = opaque(key[i]);
+      if (kk != NONE && kk > v) sel |= 1ull << i;
+      if (kk == v) tie |= 1ull << i;
     }
-    const int n_tie = block_sum_int<BG_NT>(__popcll(tie), sh.redi);
-    if (take >= n_tie) sel |= tie;
-    else if (take > 0) sel |= take_top_ties_bg<EPT>(tie, take, sh.tiecnt);
-    write_bitmap<EPT>(sel, row_sel + ((size_t)h * R + r) * (S_max / 32), S_max);
-    if (row_k && tid == 0) row_k[(size_t)h * R + r] = k;
   }
+  // counts above the threshold and at it, in one reduction (each at most 32768)
+  const uint32_t both = block_sum_u32((uint32_t)__popcll(sel) | ((uint32_t)__popcll(tie) << 16),
+                                      sh.redu[0]);
+  const int n_tie = (int)(both >> 16);
+  const int k = (int)(both & 0xffffu) + min(take, n_tie);
+  if (take >= n_tie) sel |= tie;
+  else if (take > 0) sel |= take_top_ties_bg<EPT>(tie, take, sh.tiecnt);
+  write_bitmap<EPT>(sel, row_sel + ((size_t)h * R + r) * (S_max / 32), S_max);
+  if (row_k && tid == 0) row_k[(size_t)h * R + r] = k;
+  const int flags_all = flags;
   if (status) {
     const int any_nan = __syncthreads_or(flags_all & HK_FLAG_NAN);
     const int any_range = __syncthreads_or(flags_all & HK_FLAG_RANGE);
@@ -419,7 +521,7 @@ __global__ __launch_bounds__(BG_NT) void budget_select_kernel(
     uint32_t* __restrict__ sel_out, int32_t* __restrict__ k_out) {
   __shared__ BgLds sh;
   const int h = blockIdx.x, tid = threadIdx.x;
-  const uint64_t cf = cand_flags<EPT>(h, S_max, cand_len, mask);
+  const uint64_t cf = cand_flags<EPT>(h, S_max, cand_len, mask, sh);
   const int mode = head_mode ? head_mode[h] : HK_BUDGET_REWRITE;
   uint32_t* brow = sel_out + (size_t)h * (S_max / 32);
   if (mode == HK_BUDGET_KEEP) {
@@ -432,12 +534,14 @@ __global__ __launch_bounds__(BG_NT) void budget_select_kernel(
   const float* crow = c ? c + (size_t)h * S_max : nullptr;
   const uint32_t* srow = sel_in ? sel_in + (size_t)h * (S_max / 32) : nullptr;
   uint64_t sinks = 0, base = 0;
-  uint64_t key[EPT];
+  uint64_t key[EPT];                 // rank keys of the base set, all ones elsewhere
   uint64_t kmin = ~0ull, kmax = 0ull;
+  // (per-element loads: a head's selection is one launch of n_heads workgroups, and
+  // loading all elements up front would not fit beside the 64-bit keys)
 #pragma unroll
   for (int i = 0; i < EPT; ++i) {
     const int j = tid + BG_NT * i;
-    key[i] = 0;
+    key[i] = ~0ull;
     if (!((cf >> i) & 1ull)) continue;
     if (j < n_sink) {
       sinks |= 1ull << i;
@@ -465,7 +569,7 @@ __global__ __launch_bounds__(BG_NT) void budget_select_kernel(
   } else if (cap > 0) {
     block_key_range<uint64_t>(kmin, kmax, sh, &kmin, &kmax);
     unsigned long long cnt_gt = 0;
-    const uint64_t v = radix_threshold<EPT, uint64_t>(key, base, (unsigned long long)cap,
+    const uint64_t v = radix_threshold<EPT, uint64_t>(key, (unsigned long long)cap,
                                                       [](uint64_t) { return 1ull; }, kmin, kmax, sh, &cnt_gt);
     const int take = cap - (int)cnt_gt;
     uint64_t tie = 0;
@@ -503,15 +607,10 @@ struct VoteLaunch {
   static hipError_t run(int n_heads, int R, int S_max, const int32_t* cand_len, const uint16_t* mask,
                         const float* a_rows, int p_q, uint32_t* row_sel, int32_t* row_k,
                         int32_t* status, uint16_t* votes, hipStream_t st) {
-    // enough row groups to fill the chip several times over, a few rows per workgroup
-    int rows_per_wg = 1;
-    while (rows_per_wg < 8 && (long long)n_heads * ((R + 2 * rows_per_wg - 1) / (2 * rows_per_wg)) >= 4096)
-      rows_per_wg *= 2;
     {
       TimedLaunch t(HK_TK_VOTE, st);
-      hipLaunchKernelGGL((vote_topp_kernel<EPT>), dim3((R + rows_per_wg - 1) / rows_per_wg, n_heads),
-                         dim3(BG_NT), 0, st, R, S_max, rows_per_wg, cand_len, mask, a_rows, p_q,
-                         row_sel, row_k, status);
+      hipLaunchKernelGGL((vote_topp_kernel<EPT>), dim3(R, n_heads), dim3(BG_NT), 0, st, R, S_max,
+                         cand_len, mask, a_rows, p_q, row_sel, row_k, status);
     }
     {
       TimedLaunch t(HK_TK_VOTE_COUNT, st);

@@ -564,9 +564,13 @@ __global__ HK_SCORE_ATTR void score_pass1_kernel(
 __global__ __launch_bounds__(256) void score_lse_merge_kernel(const float2* __restrict__ part,
                                                                int n_chunks, int R_pad, int NS,
                                                                int Hq, int Hkv, int W, float c2,
-                                                               float sm_scale, float* lse_out) {
+                                                               float sm_scale, float* lse_out,
+                                                               const int32_t* __restrict__ n_pages_arr,
+                                                               int L_dense, int32_t* cand_len_out) {
   const int h = blockIdx.x, s = h / Hkv, kv = h % Hkv, G = Hq / Hkv;
   const int R = G * W;
+  // the candidate count, also written by pass 2, so that a call without it has one too
+  if (threadIdx.x == 0) cand_len_out[h] = HK_PAGE * max(0, n_pages_arr[h] - dense_pages(L_dense));
   for (int r = threadIdx.x; r < R; r += blockDim.x) {
     const float2* p = part + (size_t)h * n_chunks * R_pad + r;
     float mn = -INFINITY;
@@ -853,7 +857,8 @@ __global__ __launch_bounds__(SCORE_NT) void score_rows_kernel(
       for (int e = 0; e < 16; ++e) {
         const int row = qb * 32 + acc_row(e, lane);
         if (in && row < R) {
-          const float a = cand ? fast_exp2(fmaf(acc[e], c2, -lse2[row])) : 0.f;
+          // a probability: rounding in exp and in LSE can put the largest a hair above 1
+          const float a = cand ? fminf(fast_exp2(fmaf(acc[e], c2, -lse2[row])), 1.0f) : 0.f;
           __builtin_nontemporal_store(a, arow + (size_t)row * S_max + slot);
         }
       }
@@ -918,9 +923,11 @@ hipError_t launch_score_q(const hk_score_args& a, hipStream_t st) {
     {
       TimedLaunch t(HK_TK_SCORE_MERGE, st);
       hipLaunchKernelGGL(score_lse_merge_kernel, dim3(n_heads), dim3(256), 0, st, part, n_chunks,
-                         R_pad, a.NS, a.Hq, a.Hkv, a.W, c2, a.sm_scale, lse_buf);
+                         R_pad, a.NS, a.Hq, a.Hkv, a.W, c2, a.sm_scale, lse_buf, kv->n_pages,
+                         a.L_dense, a.cand_len);
     }
     lse_use = lse_buf;
+    if (!a.s_attn) return hipGetLastError();      // row LSEs (and candidate counts) only
   } else if (a.row_lse_out && a.row_lse_out != a.row_lse_in) {
     (void)hipMemcpyAsync(a.row_lse_out, a.row_lse_in, sizeof(float) * (size_t)a.W * a.NS * a.Hq,
                          hipMemcpyDeviceToDevice, st);

@@ -2,7 +2,8 @@
 
 Marshalling only: buffers are allocated once (static shapes) and every call goes to
 libhardkv.  The compression step is Steps 2-3 of the continuous compression pipeline
-(Sec. 3.1): score -> calibrate -> Top-p -> rewrite.
+(Sec. 3.1): score -> calibrate -> Top-p -> rewrite; the budgeted step adds Step 4
+(hard budget with Cautious Update voting and attention sinks).
 """
 from __future__ import annotations
 
@@ -12,8 +13,9 @@ from dataclasses import dataclass
 import torch
 
 from . import (Allocator, PagedKV, OP_APPEND, OP_COMPACT, OP_DECODE, OP_SCORE, dims, hk_append_kv,
-               hk_calibrate_solve_T, hk_calibrate_topp, hk_compact, hk_decode_attn, hk_pool_max,
-               hk_score, workspace)
+               hk_budget_plan, hk_budget_select, hk_calibrate, hk_calibrate_solve_T,
+               hk_calibrate_topp, hk_compact, hk_compact_modes, hk_decode_attn, hk_pool_max,
+               hk_score, hk_score_rows, hk_vote_topp, workspace)
 
 
 @dataclass
@@ -119,6 +121,74 @@ class Compressor:
     def step(self, q_obs, ref_slots=None, row_lse_in=None, stream=None):
         self.score(q_obs, ref_slots=ref_slots, row_lse_in=row_lse_in, stream=stream)
         self.select(stream=stream)
+        self.compact(stream=stream)
+
+
+class BudgetCompressor:
+    """One compression step under the hard budget (Sec. 3.1 Step 4 and the budget
+    thresholds of Sec. 3.3.1) with Cautious Update voting (Sec. 3.1):
+
+      budget state (keep / sparse loading / rewrite, and the cap L_upper leaves)
+      -> row LSEs of the window -> every row's own probabilities -> per-row Top-p votes
+      -> selection ranked by votes under the cap, sinks kept -> mode-driven rewrite.
+
+    rank_by_c: break ties in the votes by the window's calibrated mean attention (adds the
+    attention-mass pass and the calibration); otherwise by recency.  The per-row
+    probabilities take n_heads * G * W * S_max * 4 bytes (buf["a_rows"]).
+    """
+
+    def __init__(self, NS, Hq, Hkv, D, W, kv: PagedKV, alloc: Allocator, p: float,
+                 L_lower: int, L_upper: int, L_dense: int = 0, n_sink: int = 0,
+                 rank_by_c: bool = False):
+        self.d = dims(NS, Hq, Hkv, D, W)
+        self.kv, self.alloc, self.p = kv, alloc, p
+        self.L_lower, self.L_upper, self.L_dense, self.n_sink = L_lower, L_upper, L_dense, n_sink
+        self.rank_by_c = rank_by_c
+        self.sm_scale = 1.0 / math.sqrt(D)
+        dev = kv.k_pool.device
+        H, S, R = NS * Hkv, kv.max_pages * 16, Hq // Hkv * W
+        self.n_heads, self.S_max, self.R = H, S, R
+        f32, i32 = torch.float32, torch.int32
+        self.buf = dict(
+            head_mode=torch.empty(H, dtype=i32, device=dev),
+            k_cap=torch.empty(H, dtype=i32, device=dev),
+            cand_len=torch.empty(H, dtype=i32, device=dev),
+            row_lse=torch.empty(W, NS, Hq, dtype=f32, device=dev),
+            s_attn=torch.empty(H, S, dtype=f32, device=dev) if rank_by_c else None,
+            c=torch.empty(H, S, dtype=f32, device=dev) if rank_by_c else None,
+            a_rows=torch.empty(H, R, S, dtype=f32, device=dev),
+            votes=torch.empty(H, S, dtype=torch.int16, device=dev),
+            row_sel=torch.empty(H, R, S // 32, dtype=i32, device=dev),
+            sel_bits=torch.empty(H, S // 32, dtype=i32, device=dev),
+            k=torch.empty(H, dtype=i32, device=dev),
+            status=torch.zeros(1, dtype=i32, device=dev),
+            ws_score=workspace(OP_SCORE, self.d, kv.max_pages, dev),
+            ws_compact=workspace(OP_COMPACT, self.d, kv.max_pages, dev),
+        )
+
+    def select(self, q_obs, stream=None):
+        b, H, S, pm = self.buf, self.n_heads, self.S_max, self.kv.page_mask
+        hk_budget_plan(self.d, self.kv, self.L_dense, self.L_lower, self.L_upper, b["head_mode"],
+                       b["k_cap"], stream=stream)
+        hk_score(self.d, q_obs, self.kv, self.L_dense, self.sm_scale, b["s_attn"], b["cand_len"],
+                 row_lse_out=b["row_lse"], ws=b["ws_score"], stream=stream)
+        hk_score_rows(self.d, q_obs, self.kv, self.L_dense, self.sm_scale, b["row_lse"],
+                      b["a_rows"], stream=stream)
+        hk_vote_topp(H, self.R, S, b["cand_len"], pm, b["a_rows"], self.p, b["votes"],
+                     b["row_sel"], status=b["status"], stream=stream)
+        if self.rank_by_c:
+            hk_calibrate(H, S, b["cand_len"], pm, [b["s_attn"]], None, [1.0], b["c"], stream=stream)
+        hk_budget_select(H, S, b["cand_len"], pm, b["sel_bits"], b["k"], votes=b["votes"],
+                         c=b["c"], head_mode=b["head_mode"], k_cap=b["k_cap"],
+                         n_sink=self.n_sink, stream=stream)
+
+    def compact(self, stream=None):
+        b = self.buf
+        hk_compact_modes(self.d, self.kv, b["sel_bits"], self.L_dense, b["head_mode"], self.alloc,
+                         b["status"], b["ws_compact"], stream=stream)
+
+    def step(self, q_obs, stream=None):
+        self.select(q_obs, stream=stream)
         self.compact(stream=stream)
 
 

@@ -72,8 +72,14 @@ def _condensed_kept(w, sel_bits, L_dense, L_sparse):
 
 # source file of each timed kernel (a stored counter reading is only valid for that source)
 ROOFLINE_KERNELS = ("score_pass1", "score_pass2", "compact_gather", "decode_split")
+BUDGET_ROOFLINE_KERNELS = ("score_pass1", "score_rows", "vote", "compact_gather")
 KERNEL_SOURCE = {"score_pass1": "hk_score.hip", "score_pass2": "hk_score.hip",
-                 "compact_gather": "hk_compact.hip", "decode_split": "hk_decode.hip"}
+                 "compact_gather": "hk_compact.hip", "decode_split": "hk_decode.hip",
+                 "score_rows": "hk_score.hip", "vote": "hk_budget.hip"}
+
+# hard-budget workload (Step 4): Cautious Update votes, L_lower = L_upper / 2 with the
+# paper's 4096-token budget, four attention sinks
+BUDGET = {"L_lower": 2048, "L_upper": 4096, "n_sink": 4}
 
 
 def _source_sha(kernel):
@@ -102,7 +108,7 @@ def _traffic(kernel, workload):
     if kv.get("source_sha256") != _source_sha(kernel):
         return None, "kernel source changed since the counters were taken"
     try:
-        return float(kv["hbm_bytes_per_launch"]), path
+        return float(kv["hbm_bytes_per_launch"]), os.path.relpath(path, ROOT)
     except (KeyError, ValueError):
         return None, "malformed counter summary"
 
@@ -361,6 +367,163 @@ def cpu_baseline(w, cfg, comp, args):
                       f"full chain score->calibrate->Top-p->rewrite, {spent:.1f} s"}
 
 
+def run_budget(args):
+    """The compression step under the hard budget (Step 4) with Cautious Update voting, on
+    the workload of --config: budget state -> row LSEs -> per-row probabilities -> votes ->
+    vote-ranked selection with sinks -> mode-driven rewrite."""
+    import paper_2606_28831_amd as hk
+    import workload as WL
+    from paper_2606_28831_amd.pipeline import BudgetCompressor
+
+    cfg = WL.config(args.config)
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    w = WL.make_workload(cfg, dev)
+    kv = hk.PagedKV(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)
+    alloc = hk.Allocator(w.free_ids, w.free_top)
+    comp = BudgetCompressor(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"], cfg["W"], kv, alloc, cfg["p"],
+                            BUDGET["L_lower"], BUDGET["L_upper"], L_dense=cfg["L_dense"],
+                            n_sink=BUDGET["n_sink"])
+    pristine = WL.clone_state(w)
+    tokens = _cand_tokens(w, cfg["L_dense"])
+    workload = f"{cfg['name']}_budget{BUDGET['L_upper']}"
+
+    def restore():
+        WL.restore_state(w, pristine)
+
+    for _ in range(args.warmup):
+        restore()
+        comp.step(w.q_obs)
+    torch.cuda.synchronize()
+    for name in hk.TIMED_KERNELS:
+        hk.hk_timing_read(name)
+    hk.hk_timing_enable()
+    restore()
+    comp.step(w.q_obs)
+    torch.cuda.synchronize()
+    hk.hk_timing_enable([])
+    kwarm = {}
+    for name in hk.TIMED_KERNELS:
+        tot, n = hk.hk_timing_read(name)
+        if n:
+            kwarm[name] = tot
+    dominant = max((k for k in kwarm if k in BUDGET_ROOFLINE_KERNELS), key=lambda k: kwarm[k])
+
+    hk.hk_timing_enable([dominant])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        restore()
+        comp.step(w.q_obs)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    hk.hk_timing_enable([])
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    tot, n = hk.hk_timing_read(dominant)
+    ktime = {dominant: {"avg_ms": tot / n, "launches_per_step": n / args.steps,
+                        "ms_per_step": tot / args.steps}}
+    b = comp.buf
+    status = int(b["status"].item())
+    k = b["k"].float()
+    modes = torch.bincount(b["head_mode"].long(), minlength=3).tolist()
+    votes = (b["votes"].to(torch.int32) & 0xFFFF).float()
+    voted = float((votes >= 1).sum()) / w.n_heads
+
+    D, e = cfg["D"], _esize(cfg)
+    S, H = w.S_max, w.n_heads
+    R = cfg["Hq"] // cfg["Hkv"] * cfg["W"]
+    bytes_q = cfg["W"] * w.NS * cfg["Hq"] * D * e
+    valid_tokens = _cand_tokens(w, 0)
+    restore()
+    comp.select(w.q_obs)
+    torch.cuda.synchronize()
+    k_cond = _condensed_kept(w, b["sel_bits"], cfg["L_dense"], 0)
+    a_bytes = H * R * S * 4
+    per_launch = {
+        "score_pass1": (valid_tokens * D * e + bytes_q, 2.0 * R * valid_tokens * D),
+        # candidate keys and the window read, every row's probabilities written
+        "score_rows": (tokens * D * e + bytes_q + a_bytes, 2.0 * R * tokens * D),
+        # every row's probabilities read, every row's selection bitmap written
+        "vote": (a_bytes + H * R * S / 8, 0.0),
+        "compact_gather": (4 * k_cond * D * e, 0.0),
+    }
+    roof = _roofline(ktime, per_launch, workload)
+    roof["share_of_step"] = ktime[dominant]["ms_per_step"] / ms_per_step
+    out = {
+        "metric": "compressed KV tokens/s under the hard budget (Cautious Update votes)",
+        "value": tokens / (ms_per_step / 1e3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg["dtype"],
+        "data": "synthetic",
+        "config": {"workload": workload, "base": cfg["name"], "sequences": w.NS,
+                   "q_heads": cfg["Hq"], "kv_heads": cfg["Hkv"], "head_dim": D,
+                   "cache_len": cfg["N"], "window": cfg["W"], "rows": R, "top_p": cfg["p"],
+                   "L_dense": cfg["L_dense"], **BUDGET},
+        "kernel_ms_discovery_step": kwarm,
+        "budget": {"head_modes_keep_sparse_rewrite": modes, "mean_kept": float(k.mean()),
+                   "mean_voted": voted, "mean_votes_of_voted": float(votes.sum()) / max(1.0, voted * H)},
+        "row_probabilities_bytes": a_bytes,
+        "status_flags": status,
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline_budget(w, cfg, args)
+    return out
+
+
+def cpu_baseline_budget(w, cfg, args):
+    """The oracle's hard-budget chain, as it stands, on a bounded sample: the window rows of
+    one head, as many as fit the time budget (every row's vote is one Top-p over the head)."""
+    import numpy as np
+
+    import oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    G, D = cfg["Hq"] // cfg["Hkv"], cfg["D"]
+    R = G * cfg["W"]
+    scale = 1 / math.sqrt(D)
+    h = 0
+    n = int(w.n_pages[h].item())
+    ids = w.page_table[h, :n].long()
+    kh = w.k_pool.index_select(0, ids).float().cpu().numpy()
+    masks = w.page_mask[h].cpu().numpy().astype(np.int64) & 0xFFFF
+    q = w.q_obs[:, 0, 0:G].float().cpu().numpy().reshape(-1, D)
+    t0 = time.perf_counter()
+    rows, valid = O.read_head(kh, np.arange(n), masks, n)
+    nd = O.tier_pages(n, cfg["L_dense"], 0)[2]
+    cand_len = 16 * (n - nd)
+    cand = O.candidate_mask(valid, cand_len)
+    _, lse = O.score_head(q, rows, valid, cand_len, scale)
+    mode, cap = O.budget_plan_head(n, masks, cfg["L_dense"], BUDGET["L_lower"], BUDGET["L_upper"])
+    done = 0
+    votes = np.zeros(len(valid), dtype=np.int64)
+    for r in range(R):
+        a = O.score_rows_head(q[r:r + 1], rows, valid, cand_len, scale, lse[r:r + 1])
+        votes += O.topp_head(a[0].astype(np.float32), cand, cfg["p"]).sel
+        done += 1
+        if time.perf_counter() - t0 >= args.cpu_seconds:
+            break
+    if done == R:
+        O.budget_select_head(cand, votes=votes, mode=mode, k_cap=cap, n_sink=BUDGET["n_sink"])
+    spent = time.perf_counter() - t0
+    # candidate slots of one head, scaled by the share of its rows done
+    slots = float(cand.sum()) * done / R
+    return {"value": slots / spent, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"head 0: {done} of its {R} window rows (per-row probabilities and Top-p "
+                      f"vote over {int(cand.sum())} candidates), {spent:.1f} s; value = "
+                      f"candidate slots x rows done / rows per head / seconds"}
+
+
 def run_decode(args):
     """Config 5: end-to-end decode loop.  One timed "step" = one segment of
     `compress_every` decode steps (append + per-layer paged decode attention) followed by
@@ -573,7 +736,8 @@ def _pmc_mean(run_dir, counter, match):
 
 
 KERNEL_SYMBOL = {"score_pass1": "score_pass1_kernel", "score_pass2": "score_pass2_kernel",
-                 "compact_gather": "compact_gather_kernel", "decode_split": "decode_split_kernel"}
+                 "compact_gather": "compact_gather_kernel", "decode_split": "decode_split_kernel",
+                 "score_rows": "score_rows_kernel", "vote": "vote_topp_kernel"}
 
 
 def summarize_pmc(a):
@@ -622,6 +786,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--crossover", action="store_true",
                     help="sparse loading vs rewrite over cache length (not the bench line)")
+    ap.add_argument("--budget", action="store_true",
+                    help="the step under the hard budget with Cautious Update votes "
+                         "(Step 4; not the bench line)")
     ap.add_argument("--graph", action="store_true",
                     help="config 5: replay each decode segment from one captured HIP graph")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -653,6 +820,14 @@ def main():
         return
     if args.crossover:
         print(json.dumps(run_crossover(args)), flush=True)
+        return
+    if args.budget:
+        if args.config == 5:
+            print("--budget runs on the compression workloads (configs 1-4)", file=sys.stderr)
+            sys.exit(2)
+        if not args.steps_given:
+            args.steps = 10
+        print(json.dumps(run_budget(args)), flush=True)
         return
     out = run_decode(args) if args.config == 5 else run_compression(args)
     print(json.dumps(out), flush=True)

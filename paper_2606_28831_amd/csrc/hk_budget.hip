@@ -168,7 +168,11 @@ __device__ __forceinline__ int2 block_exscan_bg(int v, int* red) {
 // After a histogram round: the largest digit d with above + W(digits >= d) >= target, and
 // above + W(digits > d).  Thread t owns digits [t * BPT, (t + 1) * BPT); a suffix scan over
 // the threads' sums finds the one thread whose digits hold the crossing.
-__device__ __forceinline__ void pick_digit(BgLds& sh, unsigned long long target,
+// On the first round the target is not known yet: it is target_of(the histogram's total),
+// which is every member's weight; it comes back in *target (0: nothing to reach, no digit).
+template <typename TF>
+__device__ __forceinline__ void pick_digit(BgLds& sh, bool first, TF target_of,
+                                           unsigned long long* target_io,
                                            unsigned long long above, uint32_t* d_out,
                                            unsigned long long* above_out) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -185,6 +189,14 @@ __device__ __forceinline__ void pick_digit(BgLds& sh, unsigned long long target,
   __syncthreads();
   unsigned long long suf = x - own;
   for (int w = wave + 1; w < BG_NW; ++w) suf += sh.red64[w];
+  if (first) {
+    unsigned long long total = 0;
+#pragma unroll
+    for (int w = 0; w < BG_NW; ++w) total += sh.red64[w];
+    *target_io = target_of(total);
+  }
+  const unsigned long long target = *target_io;
+  if (target == 0) return;
   const unsigned long long lo_m = above + suf;
   if (lo_m < target && lo_m + own >= target) {
     unsigned long long cum = lo_m;
@@ -204,7 +216,9 @@ __device__ __forceinline__ void pick_digit(BgLds& sh, unsigned long long target,
 }
 
 // Largest key v of the member elements with W(key >= v) >= target, where W sums the
-// elements' weights (weight(key) of each); requires 0 < target <= W(all members).  Member
+// elements' weights (weight(key) of each) and target = target_of(W(all members)), which
+// must not exceed W(all members); the target comes back in *target_out, and for a target
+// of 0 nothing else is computed (v is then meaningless).  Member
 // keys have their top bit clear; every other element holds the all-ones key, which the
 // prefix tests below exclude, so no per-element flags are needed.  The
 // bits above the highest one where the flagged keys differ are common to all of them,
@@ -213,17 +227,25 @@ __device__ __forceinline__ void pick_digit(BgLds& sh, unsigned long long target,
 // in registers; the keys that share the digits found so far are then packed into an LDS
 // list (when they fit) and the remaining rounds read only that list.  Returns v and, in
 // *above, W(key > v).
-template <int EPT, typename K, typename WF>
-__device__ __forceinline__ K radix_threshold(const K* key, unsigned long long target,
-                                             WF weight, K kmin, K kmax, BgLds& sh,
+template <int EPT, typename K, typename WF, typename TF>
+__device__ __forceinline__ K radix_threshold(const K* key, TF target_of, WF weight, K kmin, K kmax,
+                                             BgLds& sh, unsigned long long* target_out,
                                              unsigned long long* above_out) {
   constexpr int CAP = BG_LIST_BYTES / (int)sizeof(K);
   const int tid = threadIdx.x;
   K* list = reinterpret_cast<K*>(sh.list);
+  *above_out = 0;
   if (kmin == kmax) {
-    *above_out = 0;
+    // one key value: the total is the members' count times its weight
+    int cnt = 0;
+#pragma unroll
+    for (int i = 0; i < EPT; ++i) cnt += (key[i] == kmin) ? 1 : 0;
+    cnt = block_sum_int<BG_NT>(cnt, sh.redi);
+    *target_out = target_of((unsigned long long)cnt * weight(kmin));
     return kmin;
   }
+  unsigned long long target = 0;
+  bool first = true;
   int pos = highest_bit<K>(kmin ^ kmax) + 1;
   K prefix = kmin & ~low_mask<K>(pos);
   unsigned long long above = 0;
@@ -253,7 +275,9 @@ __device__ __forceinline__ K radix_threshold(const K* key, unsigned long long ta
     }
     __syncthreads();
     uint32_t d;
-    pick_digit(sh, target, above, &d, &above);
+    pick_digit(sh, first, target_of, &target, above, &d, &above);
+    first = false;
+    if (target == 0) break;
     prefix |= (K)d << lo;
     pos = lo;
     if (pos > 0 && n_list < 0) {
@@ -274,6 +298,7 @@ __device__ __forceinline__ K radix_threshold(const K* key, unsigned long long ta
       }
     }
   }
+  *target_out = target;
   *above_out = above;
   return prefix;
 }
@@ -369,7 +394,6 @@ __global__ __launch_bounds__(BG_NT) __attribute__((amdgpu_waves_per_eu(4, 8))) v
   uint32_t key[EPT];
   int flags = 0;
   uint32_t kmin = NONE, kmax = 0u;
-  double m = 0.0;
   // every load first (index clamped into the row), then the per-element work
 #pragma unroll
   for (int i = 0; i < EPT; ++i) key[i] = __float_as_uint(arow[min(tid + BG_NT * i, S_max - 1)]);
@@ -385,46 +409,45 @@ __global__ __launch_bounds__(BG_NT) __attribute__((amdgpu_waves_per_eu(4, 8))) v
       key[i] = __float_as_uint(v);
       kmin = min(kmin, key[i]);
       kmax = max(kmax, key[i]);
-      m += (double)truncf(v * kMassScale);      // exact: see mass_weight
     }
   }
-  // one block reduction for the row's total mass and key range
-  unsigned long long tot = wave_sum_u64((unsigned long long)m);
+  // key range of the row (its total mass comes from the first histogram round)
   kmin = wave_reduce_u32(kmin, NONE, [](uint32_t a, uint32_t b) { return a < b ? a : b; });
   kmax = wave_reduce_u32(kmax, 0u, [](uint32_t a, uint32_t b) { return a > b ? a : b; });
   {
     const int w = tid >> 6;
     if ((tid & 63) == 0) {
-      sh.red64[w] = tot;
       sh.redu[0][w] = kmin;
       sh.redu[1][w] = kmax;
     }
     __syncthreads();
-    tot = sh.red64[0];
     kmin = sh.redu[0][0];
     kmax = sh.redu[1][0];
 #pragma unroll
     for (int i = 1; i < BG_NW; ++i) {
-      tot += sh.red64[i];
       kmin = min(kmin, sh.redu[0][i]);
       kmax = max(kmax, sh.redu[1][i]);
     }
   }
   const unsigned long long pq = (unsigned long long)p_q;
-  const unsigned long long target =
-      pq * (tot / 1000000ull) + (pq * (tot % 1000000ull) + 999999ull) / 1000000ull;
+  // target = ceil(p_q * Total / 10^6) without overflow
+  const auto target_of = [pq](unsigned long long tot) {
+    return pq * (tot / 1000000ull) + (pq * (tot % 1000000ull) + 999999ull) / 1000000ull;
+  };
   uint32_t v = NONE;
   int take = 0;
-  if (target > 0) {
-    unsigned long long mass_gt = 0;
-    v = radix_threshold<EPT, uint32_t>(key, target, [](uint32_t k) { return mass_weight(k); },
-                                       kmin, kmax, sh, &mass_gt);
-    const unsigned long long wv = mass_weight(v);         // > 0: the crossing element weighs
-    take = (int)((target - mass_gt + wv - 1) / wv);
-  } else if (kmin != NONE) {
-    // no mass to reach: k_min = 1 keeps the largest value, the most recent on ties
-    v = kmax;
-    take = 1;
+  if (kmin != NONE) {
+    unsigned long long target = 0, mass_gt = 0;
+    v = radix_threshold<EPT, uint32_t>(key, target_of, [](uint32_t k) { return mass_weight(k); },
+                                       kmin, kmax, sh, &target, &mass_gt);
+    if (target > 0) {
+      const unsigned long long wv = mass_weight(v);       // > 0: the crossing element weighs
+      take = (int)((target - mass_gt + wv - 1) / wv);
+    } else {
+      // no mass to reach: k_min = 1 keeps the largest value, the most recent on ties
+      v = kmax;
+      take = 1;
+    }
   }
   uint64_t sel = 0, tie = 0;
   if (v != NONE) {
@@ -568,9 +591,11 @@ __global__ __launch_bounds__(BG_NT) void budget_select_kernel(
     sel |= base;
   } else if (cap > 0) {
     block_key_range<uint64_t>(kmin, kmax, sh, &kmin, &kmax);
-    unsigned long long cnt_gt = 0;
-    const uint64_t v = radix_threshold<EPT, uint64_t>(key, (unsigned long long)cap,
-                                                      [](uint64_t) { return 1ull; }, kmin, kmax, sh, &cnt_gt);
+    unsigned long long cnt_gt = 0, tgt = 0;
+    const unsigned long long capu = (unsigned long long)cap;
+    const uint64_t v = radix_threshold<EPT, uint64_t>(
+        key, [capu](unsigned long long) { return capu; }, [](uint64_t) { return 1ull; }, kmin, kmax, sh,
+        &tgt, &cnt_gt);
     const int take = cap - (int)cnt_gt;
     uint64_t tie = 0;
     const uint64_t fb = opaque(base);

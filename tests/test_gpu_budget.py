@@ -356,3 +356,42 @@ def test_cautious_budget_chain():
     for h in range(H):
         if m_np[h] == O.REWRITE:
             assert 16 * int(n_after[h]) <= L_upper, (h, int(n_after[h]))
+
+
+def test_budget_compressor_pipeline():
+    """BudgetCompressor.step: every head of the cache ends within L_upper when rewritten, the
+    sinks survive, the selection equals the budget-select oracle on the votes the step
+    produced (integer work), and the status word stays clear."""
+    import paper_2606_28831_amd as hk
+    from paper_2606_28831_amd.pipeline import BudgetCompressor
+    hk_, cfg, w, kv = _setup("bf16_d128_g4_ragged_holes")
+    alloc = hk.Allocator(w.free_ids, w.free_top)
+    comp = BudgetCompressor(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"], cfg["W"], kv, alloc, 0.9,
+                            L_lower=300, L_upper=600, L_dense=48, n_sink=4)
+    H, S = w.n_heads, w.S_max
+    before = snapshot(w)
+    comp.select(w.q_obs)
+    torch.cuda.synchronize()
+    b = comp.buf
+    v_np = np_i(b["votes"]).astype(np.int64) & 0xFFFF
+    sel_np = np_i(b["sel_bits"])
+    mode, cap = np_i(b["head_mode"]), np_i(b["k_cap"])
+    for h in range(H):
+        valid = _valid(before["mask"][h])
+        cand = np.zeros(S, bool)
+        cand[:len(valid)] = O.candidate_mask(valid, int(np_i(b["cand_len"])[h]))
+        ref, kr = O.budget_select_head(cand, votes=v_np[h], mode=int(mode[h]), k_cap=int(cap[h]),
+                                       n_sink=4)
+        assert np.array_equal(unpack_bits(sel_np[h], S), ref) and int(np_i(b["k"])[h]) == kr, h
+    comp.compact()
+    torch.cuda.synchronize()
+    assert int(b["status"].item()) == 0
+    check_compaction(w, before, sel_np, S, lambda h, sl: O.compact_mode_head(
+        before["table"][h], before["mask"][h], int(before["n"][h]), sl, 48, int(mode[h])))
+    n_after = np_i(w.n_pages)
+    for h in range(H):
+        if mode[h] == O.REWRITE:
+            assert 16 * int(n_after[h]) <= 600
+        # the sinks were selected, so the rewrite put them first (order-preserving)
+        valid = _valid(before["mask"][h])
+        assert all(unpack_bits(sel_np[h], S)[j] for j in range(4) if valid[j])

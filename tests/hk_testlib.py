@@ -147,3 +147,47 @@ def check_compaction(w, before, sel_np, S, ref_fn):
     assert live.isdisjoint(free)
     assert len(live) + len(free) == len(before["free"]), "pages lost or duplicated"
     assert set(new_ids) <= set(before["free"][:before["top"]].tolist())
+
+
+def check_topp_rule(c, sel, k, cand, p, k_min=1, k_max=0, what="Top-p"):
+    """Property check of a Top-p selection against the fp32 values it was made from (for
+    chained stages, whose input is the GPU's own output and so not an oracle input): the
+    set lies in the candidates, has k members within the clamps, ranks above every other
+    candidate in (value, slot) order, reaches p of the fixed-point mass floor(c 2^40)
+    (unless clamped at the top), and would not without its weakest member (unless clamped
+    at the bottom)."""
+    c = np.asarray(c, np.float32).astype(np.float64)
+    vals = np.clip(np.where(np.isnan(c), 0.0, c), 0.0, 1.0)
+    sel = np.asarray(sel, bool)
+    cand = np.asarray(cand, bool)
+    assert not (sel & ~cand).any(), f"{what}: selection outside the candidates"
+    idx = np.nonzero(cand)[0]
+    n, kk = len(idx), int(sel.sum())
+    assert kk == int(k), f"{what}: k {k} but {kk} selected"
+    lo, hi = min(max(k_min, 0), n), (n if k_max <= 0 else min(k_max, n))
+    assert lo <= kk <= hi, f"{what}: k {kk} outside [{lo}, {hi}]"
+    w = {int(j): int(math.floor(vals[j] * 2.0 ** 40)) for j in idx}
+    total = sum(w.values())
+    pq = int(round(float(p) * 10 ** 6))
+    chosen = [int(j) for j in idx if sel[j]]
+    rest = [int(j) for j in idx if not sel[j]]
+    if chosen and rest:
+        assert min((vals[j], j) for j in chosen) > max((vals[j], j) for j in rest), \
+            f"{what}: a dropped candidate outranks a kept one"
+    m = sum(w[j] for j in chosen)
+    assert kk == hi or 10 ** 6 * m >= pq * total, f"{what}: mass below p"
+    if chosen and kk > lo:
+        weakest = min(chosen, key=lambda j: (vals[j], j))
+        assert 10 ** 6 * (m - w[weakest]) < pq * total, f"{what}: not the smallest such set"
+
+
+def rewritten_sources(table_row, mask_row, n_pages, sel, n_condensed):
+    """(physical page, slot) of every selected valid slot of the condensed band, in
+    ascending logical order: what a rewrite must copy, in that order."""
+    out = []
+    for pp in range(n_condensed):
+        m = int(mask_row[pp])
+        for t in range(16):
+            if (m >> t) & 1 and sel[pp * 16 + t]:
+                out.append((int(table_row[pp]), t))
+    return out

@@ -4,9 +4,10 @@ independent host replay.
 The host keeps, per head, the valid K/V rows in logical order.  Every decode step the
 oracle's attention over that replay is compared with the GPU output; every compression
 the GPU score (single pass, fed the GPU's decode LSEs) is compared with the oracle score
-fed the oracle's own decode LSEs, the GPU Top-p selection must equal the oracle's on the
-GPU probabilities (bit-exact), and after the rewrite the GPU cache must hold exactly the
-replay's rows (bit-exact).
+fed the oracle's own decode LSEs; the GPU Top-p selection, made on the GPU's own
+probabilities, must satisfy the Top-p rule's defining properties (the stage's parity on
+seeded inputs is tested on its own); the replay then keeps the selected rows, and after
+the rewrite the GPU cache must hold exactly the replay's rows (bit-exact).
 """
 import math
 
@@ -16,7 +17,8 @@ import torch
 
 import oracle as O
 import workload as WL
-from hk_testlib import HostCache, check_lse, check_log_scores, check_prob, np64, np_i, unpack_bits
+from hk_testlib import (HostCache, check_lse, check_log_scores, check_prob, check_topp_rule, np64,
+                        np_i, unpack_bits)
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -93,9 +95,8 @@ def test_decode_loop_chain(L_dense):
             check_log_scores(s_gpu[h], full, 2e-3, f"score seg {seg} h {h}")
             cand = np.zeros(S, bool)
             cand[:len(valid)] = O.candidate_mask(valid, cand_len)
-            r = O.topp_head(c_gpu[h], cand, p)
             sel = unpack_bits(sel_gpu[h], S)
-            assert k_gpu[h] == r.k and np.array_equal(sel, r.sel), (seg, h)
+            check_topp_rule(c_gpu[h], sel, int(k_gpu[h]), cand, p, what=f"seg {seg} h {h}")
             # replay: selected candidates, then every dense-tier row, in order
             keep = (sel[:len(valid)] | ~O.candidate_mask(valid, cand_len))[valid]
             rows[h] = [rows[h][0][keep], rows[h][1][keep]]

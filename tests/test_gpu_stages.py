@@ -6,6 +6,7 @@ or 1e-5 (fp32 caches).  Shapes span several tiles with ragged tails, masked slot
 GQA groups of 1..8, head dims 64/128 and both cache dtypes.
 """
 import math
+import zlib
 
 import numpy as np
 import pytest
@@ -14,7 +15,8 @@ import torch
 import oracle as O
 import workload as WL
 from hk_testlib import (RTOL, HostCache, check_compaction, check_lse, check_log_scores,
-                        check_prob, np64, np_i, q_rows, snapshot, unpack_bits)
+                        check_prob, check_topp_rule, np64, np_i, q_rows, rewritten_sources,
+                        snapshot, unpack_bits)
 
 pytestmark = pytest.mark.gpu
 
@@ -153,14 +155,12 @@ def test_score_redundancy(name, n_ref):
 
 
 def _calib_inputs(name):
+    """Seeded synthetic log-scores over the case's candidates (the workload generator's,
+    not the score kernel's): the calibration, Top-p and pooling stages are checked on
+    inputs both sides receive from the generator."""
     hk, cfg, w, kv = _setup(name)
-    d = hk.dims(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"], cfg["W"])
-    H, S = w.n_heads, w.S_max
-    s = torch.empty(H, S, device=DEV)
-    cl = torch.empty(H, dtype=torch.int32, device=DEV)
-    ws = hk.workspace(hk.OP_SCORE, d, w.max_pages, DEV)
-    hk.hk_score(d, w.q_obs, kv, 0, 1 / math.sqrt(cfg["D"]), s, cl, ws=ws)
-    return hk, cfg, w, kv, s, cl
+    s_np, cl_np = WL.synthetic_log_scores(w, seed=zlib.crc32(name.encode()), scale=1.5)
+    return hk, cfg, w, kv, torch.tensor(s_np, device=DEV), torch.tensor(cl_np, device=DEV)
 
 
 @pytest.mark.parametrize("name", list(CASES))
@@ -182,15 +182,21 @@ def test_calibrate_and_topp(name):
         check_prob(c_np[h], cr, rtol, f"c head {h}")
         check_lse(lse_np[h], [lr], rtol, f"lse head {h}")
         assert abs(c_np[h].sum() - 1.0) <= 1e-5 * max(1, cand.sum() / 1000)
+    # Top-p on the oracle's calibrated probabilities (fp32), given to both sides
+    c32 = np.zeros((H, S), np.float32)
+    for h in range(H):
+        valid = ((mask[h][:, None] >> np.arange(16)) & 1).reshape(-1).astype(bool)
+        cand = O.candidate_mask(valid, int(cl_np[h]))
+        c32[h] = O.calibrate_head(s_np[h], cand, float(T[h]))[0].astype(np.float32)
+    c_in = torch.tensor(c32, device=DEV)
     for p in (cfg["p"] if "p" in cfg else 0.9, 0.5, 0.999, 1.0):
         sel = torch.empty(H, S // 32, dtype=torch.int32, device=DEV)
         k = torch.empty(H, dtype=torch.int32, device=DEV)
         m = torch.empty(H, device=DEV)
         st = torch.zeros(1, dtype=torch.int32, device=DEV)
-        hk.hk_topp_select(H, S, cl, w.page_mask, c, p, sel, k, sel_mass=m, status=st)
+        hk.hk_topp_select(H, S, cl, w.page_mask, c_in, p, sel, k, sel_mass=m, status=st)
         torch.cuda.synchronize()
         sel_np, k_np, m_np = np_i(sel), np_i(k), np64(m)
-        c32 = c.cpu().numpy()
         for h in range(H):
             valid = ((mask[h][:, None] >> np.arange(16)) & 1).reshape(-1).astype(bool)
             cand = O.candidate_mask(valid, int(cl_np[h]))
@@ -573,17 +579,18 @@ def test_degenerate_heads_end_to_end():
         check_log_scores(s_gpu[h], full, 2e-3, f"score head {h}")
         cand = np.zeros(S, bool)
         cand[:len(valid)] = O.candidate_mask(valid, 16 * n)
-        r = O.topp_head(c_gpu[h], cand, p)
-        assert int(k_gpu[h]) == r.k and np.array_equal(unpack_bits(sel_gpu[h], S), r.sel), h
+        # the selection and rewrite act on the GPU's own probabilities: checked by their
+        # defining properties (the stages' parity on seeded inputs is tested on its own)
+        sel_h = unpack_bits(sel_gpu[h], S)
+        check_topp_rule(c_gpu[h], sel_h, int(k_gpu[h]), cand, p, what=f"head {h}")
         if h in (0, 1):
-            assert r.k == 0 and not c_gpu[h].any()
+            assert int(k_gpu[h]) == 0 and not c_gpu[h].any()
         if h == 2:
-            assert r.k == 1 and unpack_bits(sel_gpu[h], S)[3 * 16 + 5]
-        res = O.compact_head(pre.table[h], pre.mask[h], n, r.sel, 0, 0)
-        assert int(post.n[h]) == len(res.pages), h
+            assert int(k_gpu[h]) == 1 and sel_h[3 * 16 + 5]
+        want = rewritten_sources(pre.table[h], pre.mask[h], n, sel_h, n)
+        assert int(post.n[h]) == -(-len(want) // 16), h
         K1, v1 = post.head(h)
         V1, _ = post.head_v(h)
-        want = [(ph, t) for e in res.pages for ph, t in e.src]
         pos_of = {int(pid): i for i, pid in enumerate(pre.table[h][:n])}
         assert v1.sum() == len(want), h
         for j, (ph, t) in enumerate(want):
@@ -643,9 +650,10 @@ def test_pool_max(name, radius):
 
 
 def test_pool_then_select_pipeline():
-    """Compressor(pool_radius=3): pooled scores feed the fused select; Top-p equals the
-    oracle on the GPU's calibrated probabilities, and calibration matches the oracle on
-    the pooled scores."""
+    """Compressor(pool_radius=3): pooled scores feed the fused select.  The pooled scores and
+    calibrated probabilities match the oracle chain run on the same cache (score -> pool ->
+    calibrate, all on the CPU); the selection, made on the GPU's own probabilities, is
+    checked by the Top-p rule's defining properties."""
     import paper_2606_28831_amd as hk
     from paper_2606_28831_amd.pipeline import Compressor
     hk_, cfg, w, kv = _setup("bf16_d128_g7_tempered")
@@ -655,14 +663,22 @@ def test_pool_then_select_pipeline():
     comp.select()
     torch.cuda.synchronize()
     b, H, S = comp.buf, w.n_heads, w.S_max
-    mask = np_i(w.page_mask).astype(np.int64) & 0xFFFF
+    G = cfg["Hq"] // cfg["Hkv"]
+    scale = 1 / math.sqrt(cfg["D"])
+    host = HostCache(w.k_pool, None, w.page_table, w.page_mask, w.n_pages)
+    qn = np64(w.q_obs)
     for h in range(H):
-        valid = ((mask[h][:, None] >> np.arange(16)) & 1).reshape(-1).astype(bool)
+        rows, valid = host.head(h)
+        n = int(host.n[h])
         cand = np.zeros(S, bool)
-        cand[:len(valid)] = O.candidate_mask(valid, int(b.cand_len[h]))
-        pooled = O.pool_max_head(np64(b.s_attn[h]), cand, 3)
-        assert np.array_equal(np64(b.s_pool[h]), pooled), h
+        cand[:len(valid)] = O.candidate_mask(valid, 16 * n)
+        s_ref, _ = O.score_head(q_rows(qn, h, cfg["Hkv"], G), rows, valid, 16 * n, scale)
+        s_full = np.full(S, -np.inf)
+        s_full[:len(s_ref)] = s_ref
+        pooled = O.pool_max_head(s_full, cand, 3)
+        check_log_scores(np64(b.s_pool[h]), pooled, 2e-3, f"pooled head {h}")
         c_ref, _ = O.calibrate_head(pooled, cand)
-        check_prob(b.c[h].cpu().numpy(), c_ref, 2e-3, f"c head {h}")
-        r = O.topp_head(b.c[h].cpu().numpy(), cand, 0.9)
-        assert int(b.k[h]) == r.k and np.array_equal(unpack_bits(np_i(b.sel_bits[h]), S), r.sel), h
+        c_gpu = b.c[h].cpu().numpy()
+        check_prob(c_gpu, c_ref, 2e-3, f"c head {h}")
+        check_topp_rule(c_gpu, unpack_bits(np_i(b.sel_bits[h]), S), int(b.k[h]), cand, 0.9,
+                        what=f"head {h}")

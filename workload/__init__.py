@@ -197,3 +197,22 @@ def decode_step_inputs(cfg: dict, step: int, layer: int, device, NS_layer: int):
     k = torch.randn(NS_layer, Hkv, D, generator=g, device=device).to(dt)
     v = torch.randn(NS_layer, Hkv, D, generator=g, device=device).to(dt)
     return q, k, v
+
+
+def synthetic_log_scores(w: Workload, seed: int, scale: float = 2.0, L_dense: int = 0):
+    """Seeded stand-in log-scores [n_heads, S_max] fp32 (host numpy) for the stages that
+    consume scores: N(0, scale^2) draws at every candidate slot (valid slots older than the
+    dense tier), -inf elsewhere; a score-like input drawn without the method's arithmetic.
+    Returns (scores, cand_len) with cand_len [n_heads] int32."""
+    import numpy as np
+    rng = np.random.default_rng(seed)
+    n = w.n_pages.cpu().numpy().astype(np.int64)
+    masks = w.page_mask.cpu().numpy().astype(np.int64) & 0xFFFF
+    nd = np.minimum(n, -(-L_dense // PAGE))
+    cand_len = (PAGE * (n - nd)).astype(np.int32)
+    S = w.S_max
+    bits = ((masks[:, :, None] >> np.arange(PAGE)) & 1).reshape(w.n_heads, -1).astype(bool)
+    cand = bits & (np.arange(S)[None, :] < cand_len[:, None])
+    s = (rng.standard_normal((w.n_heads, S)) * scale).astype(np.float32)
+    s[~cand] = -np.inf
+    return s, cand_len

@@ -10,4 +10,4 @@ from .hardkv_oracle import (PAGE, MASS_BITS, P_QUANT, logsumexp, read_head, tier
                             compact_head, decode_head, merge_states, append_position,
                             pool_max_head, KEEP, SPARSE, REWRITE, score_rows_head,
                             vote_head, budget_plan_head, budget_select_head,
-                            compact_mode_head)
+                            compact_mode_head, topk_mass_and_grad, solve_T_gd_head)

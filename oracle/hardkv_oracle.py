@@ -317,6 +317,63 @@ def solve_T_head(x, cand, k: int, target_mass: float, T_lo: float = 1e-4,
     return math.exp(0.5 * (a + b))
 
 
+def topk_mass_and_grad(x, top, theta: float):
+    """M_k(Softmax(x / T)) over the candidates x (1-D) with T = exp(theta), where `top`
+    marks the Top-k members (fixed in T, App. D.2 theorem), and its derivative in theta:
+    with u = 1/T, dM/du = M (E_top[x] - E_all[x]) (expectations under the top-k and the
+    full softmax), and du/dtheta = -u."""
+    x = np.asarray(x, dtype=np.float64)
+    u = math.exp(-theta)
+    z = u * x
+    zmax = float(np.max(z))
+    e = np.exp(z - zmax)
+    s_all, s_top = float(e.sum()), float(e[top].sum())
+    if s_top == 0.0:
+        return 0.0, 0.0
+    M = s_top / s_all
+    e_top = float((x[top] * e[top]).sum()) / s_top
+    e_all = float((x * e).sum()) / s_all
+    return M, -u * M * (e_top - e_all)
+
+
+def solve_T_gd_head(x, cand, k: int, target_mass: float, T_init: float = 1.0,
+                    lr: float = 0.05, iters: int = 200, tol: float = 0.0):
+    """Temperature for Problem 1 by gradient descent (Alg. 1, Solution 2 form): the
+    parameter is theta = log T (T stays positive), the loss the squared gap
+    l = (M_k(Softmax(x / T)) - target)^2, the optimiser Adam (beta 0.9 / 0.999, eps 1e-8,
+    bias-corrected, no weight decay).  Iterates until l < tol or `iters` updates.
+    Returns (T, final loss).
+    Pinned by: the two-level closed form T* = (a-b) / ln(m(n-k) / (k(1-m))) is reached;
+    the gradient equals finite differences of scipy's softmax mass; iters = 0 returns
+    T_init; the loss never ends above its start on monotone problems.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    idx = np.nonzero(cand)[0]
+    xs = x[idx]
+    order = order_desc(x, idx)[:k]
+    top = np.isin(idx, np.asarray(order, dtype=np.int64))
+    theta = math.log(T_init)
+    m = v = 0.0
+    b1, b2, eps = 0.9, 0.999, 1e-8
+    loss = 0.0
+    for t in range(1, iters + 1):
+        M, dM = topk_mass_and_grad(xs, top, theta) if k > 0 else (0.0, 0.0)
+        gap = M - target_mass
+        loss = gap * gap
+        if loss < tol:
+            break
+        g = 2.0 * gap * dM
+        m = b1 * m + (1.0 - b1) * g
+        v = b2 * v + (1.0 - b2) * g * g
+        mh = m / (1.0 - b1 ** t)
+        vh = v / (1.0 - b2 ** t)
+        theta -= lr * mh / (math.sqrt(vh) + eps)
+    if iters > 0:
+        M, _ = topk_mass_and_grad(xs, top, theta) if k > 0 else (0.0, 0.0)
+        loss = (M - target_mass) ** 2
+    return math.exp(theta), loss
+
+
 # ---------------------------------------------------------------------------
 # a4: Cascade-Cache rewrite (Sec. 3.1 Step 3, Sec. 3.3.1 Rewrite Cache / Sparse Loading)
 # ---------------------------------------------------------------------------

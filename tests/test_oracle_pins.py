@@ -639,3 +639,56 @@ def test_budget_chain_respects_L_upper(seed):
         assert kept == [t for t in table if t in kept] and res.n_new == 0
     else:
         assert [p.phys for p in res.pages] == table and res.freed == []
+
+
+# ---------------------------------------------------------------- temperature by gradient descent
+def test_solve_T_gd_two_level_closed_form(golden_dir):
+    """Alg. 1 reaches the two-level closed form of the temperature."""
+    for n, k, a, b, mass in [(100, 10, 1.0, 0.0, 0.5), (400, 7, 2.0, -1.0, 0.3), (50, 25, 0.5, 0.0, 0.8)]:
+        x = np.full(n, b)
+        x[:k] = a
+        cand = np.ones(n, bool)
+        T, loss = O.solve_T_gd_head(x, cand, k, mass, iters=400)
+        closed = (a - b) / math.log(mass * (n - k) / (k * (1 - mass)))
+        assert T == pytest.approx(closed, rel=1e-3) and loss < 1e-10
+
+
+def test_solve_T_gd_gradient_matches_finite_differences():
+    r = np.random.default_rng(3)
+    x = r.standard_normal(60) * 2
+    top = np.zeros(60, bool)
+    top[np.argsort(-x)[:9]] = True
+    for theta in (-1.0, 0.0, 0.7):
+        def mass(th):
+            return sps.softmax(x * math.exp(-th))[top].sum()
+        M, dM = O.topk_mass_and_grad(x, top, theta)
+        assert M == pytest.approx(mass(theta), rel=1e-12)
+        h = 1e-5     # central difference: error O(h^2) plus rounding O(1e-16 / h)
+        assert dM == pytest.approx((mass(theta + h) - mass(theta - h)) / (2 * h), rel=1e-4)
+
+
+def test_solve_T_gd_edges():
+    x = np.array([3.0, 1.0, 0.0, -2.0])
+    cand = np.ones(4, bool)
+    assert O.solve_T_gd_head(x, cand, 2, 0.7, T_init=2.5, iters=0)[0] == 2.5
+    T, loss = O.solve_T_gd_head(x, cand, 2, 0.7, iters=300)
+    _, loss0 = O.solve_T_gd_head(x, cand, 2, 0.7, iters=1)
+    assert loss <= loss0
+    # agrees with the bisection of App. D.1 on the same problem
+    assert T == pytest.approx(O.solve_T_head(x, cand, 2, 0.7), rel=1e-3)
+    # an early stop leaves the loss below the tolerance
+    T2, l2 = O.solve_T_gd_head(x, cand, 2, 0.7, iters=300, tol=1e-8)
+    assert l2 < 1e-8
+
+
+def test_solve_T_gd_first_adam_step():
+    """Adam's bias-corrected first step moves theta = log T by exactly lr against the
+    gradient's sign (m_hat / sqrt(v_hat) = g / |g|), whatever the gradient's size."""
+    x = np.array([3.0, 1.0, 0.0, -2.0])
+    cand = np.ones(4, bool)
+    top = np.array([True, True, False, False])
+    for target, lr in ((0.99, 0.05), (0.5, 0.2)):
+        M, dM = O.topk_mass_and_grad(x, top, 0.0)
+        g = 2 * (M - target) * dM
+        T, _ = O.solve_T_gd_head(x, cand, 2, target, T_init=1.0, lr=lr, iters=1)
+        assert math.log(T) == pytest.approx(-lr * math.copysign(1.0, g), rel=1e-6)

@@ -6,6 +6,7 @@
  *   hk_score          importance of every cached key against an observation window
  *   hk_calibrate      Logits Calibration into one probability space (Sec. 3.2, Solution 2)
  *   hk_calibrate_solve_T  per-head temperature for Problem 1 (App. D.1, binary search)
+ *   hk_calibrate_solve_T_gd  the same temperature by gradient descent (Alg. 1)
  *   hk_topp_select    head-adaptive Top-p budget (Sec. 3.2, Problem 1)
  *   hk_calibrate_topp hk_calibrate followed by hk_topp_select in one launch
  *   hk_pool_max       order-preserving max-pooling of scores before calibration
@@ -231,6 +232,21 @@ hk_status hk_calibrate_solve_T(int32_t n_heads, int32_t S_max, const int32_t* ca
                                const float* target_mass, float T_lo, float T_hi,
                                int32_t iters, float* T_out, hipStream_t stream);
 
+/* Temperature of Problem 1 by gradient descent (Alg. 1, Solution 2 form): theta = log T
+ * starts at log(T_init) and takes Adam steps (beta1 0.9, beta2 0.999, eps 1e-8,
+ * bias-corrected, no weight decay, step size lr) on the loss
+ *   l(theta) = (M_k(Softmax(x / T)) - target_mass[h])^2,
+ * the Top-k set being that of x (invariant in T, App. D.2 theorem; ties to the larger
+ * slot), with the exact derivative dM/dtheta = -(1/T) M (E_top[x] - E_all[x]); it stops
+ * when l < tol or after `iters` steps.  T_out [n_heads] fp32; loss_out [n_heads] fp32 (the
+ * loss at the returned T) or NULL.  Other arguments as for hk_calibrate_solve_T.
+ * T_init > 0, lr > 0, iters in [0, 100000], tol >= 0.
+ */
+hk_status hk_calibrate_solve_T_gd(int32_t n_heads, int32_t S_max, const int32_t* cand_len,
+                                  const uint16_t* page_mask, const float* x, const int32_t* k,
+                                  const float* target_mass, float T_init, float lr, int32_t iters,
+                                  float tol, float* T_out, float* loss_out, hipStream_t stream);
+
 /* ------------------------------------------------------------------ a4: compact
  * Cascade-Cache rewrite (Sec. 3.1 Step 3; Sec. 3.3.1).  Per head, page positions are
  * split into age bands: dense = the newest ceil(L_dense/16) pages, sparse = the
@@ -368,7 +384,7 @@ enum {
   HK_TK_SCORE_PASS2 = 2,   /* hk_score: attention-mass (and redundancy) pass             */
   HK_TK_CALIBRATE = 3,     /* hk_calibrate                                               */
   HK_TK_TOPP = 4,          /* hk_topp_select                                             */
-  HK_TK_SOLVE_T = 5,       /* hk_calibrate_solve_T                                       */
+  HK_TK_SOLVE_T = 5,       /* hk_calibrate_solve_T and hk_calibrate_solve_T_gd           */
   HK_TK_COMPACT_GATHER = 6,/* hk_compact: condensed-row gather into fresh pages          */
   HK_TK_COMPACT_META = 7,  /* hk_compact: plan, alloc, table, push (four launches)       */
   HK_TK_DECODE_SPLIT = 8,  /* hk_decode_attn: split-K partial states                     */

@@ -321,18 +321,23 @@ def topk_mass_and_grad(x, top, theta: float):
     """M_k(Softmax(x / T)) over the candidates x (1-D) with T = exp(theta), where `top`
     marks the Top-k members (fixed in T, App. D.2 theorem), and its derivative in theta:
     with u = 1/T, dM/du = M (E_top[x] - E_all[x]) (expectations under the top-k and the
-    full softmax), and du/dtheta = -u."""
+    full softmax), and du/dtheta = -u.  Terms whose exponential is 0 add nothing to the
+    expectations (so a candidate at -inf is simply absent)."""
     x = np.asarray(x, dtype=np.float64)
     u = math.exp(-theta)
     z = u * x
     zmax = float(np.max(z))
+    if zmax == -math.inf:
+        return 0.0, 0.0
     e = np.exp(z - zmax)
     s_all, s_top = float(e.sum()), float(e[top].sum())
     if s_top == 0.0:
         return 0.0, 0.0
     M = s_top / s_all
-    e_top = float((x[top] * e[top]).sum()) / s_top
-    e_all = float((x * e).sum()) / s_all
+    with np.errstate(invalid="ignore"):
+        xe = np.where(e > 0.0, x * e, 0.0)  # a term of weight 0 adds 0 (also for x = -inf)
+    e_top = float(xe[top].sum()) / s_top
+    e_all = float(xe.sum()) / s_all
     return M, -u * M * (e_top - e_all)
 
 

@@ -201,6 +201,19 @@ hk_status hk_calibrate_solve_T(int32_t n_heads, int32_t S_max, const int32_t* ca
                                     T_hi, iters, T_out, stream));
 }
 
+hk_status hk_calibrate_solve_T_gd(int32_t n_heads, int32_t S_max, const int32_t* cand_len,
+                                  const uint16_t* page_mask, const float* x, const int32_t* k,
+                                  const float* target_mass, float T_init, float lr, int32_t iters,
+                                  float tol, float* T_out, float* loss_out, hipStream_t stream) {
+  hk_status e = check_rows(n_heads, S_max, cand_len);
+  if (e) return e;
+  if (!x || !k || !target_mass || !T_out) return HK_ERR_ARG;
+  if (!(T_init > 0.f) || !std::isfinite(T_init) || !(lr > 0.f) || !std::isfinite(lr)) return HK_ERR_ARG;
+  if (iters < 0 || iters > 100000 || !(tol >= 0.f)) return HK_ERR_ARG;
+  return launched(hk_launch_solve_T_gd(n_heads, S_max, cand_len, page_mask, x, k, target_mass, T_init,
+                                       lr, iters, tol, T_out, loss_out, stream));
+}
+
 hk_status hk_compact(const hk_dims* dims, const hk_paged_kv* kv, const uint32_t* sel_bits,
                      int32_t L_dense, int32_t L_sparse, const hk_allocator* alloc, int32_t* status,
                      void* workspace, size_t ws_bytes, hipStream_t stream) {

@@ -227,6 +227,10 @@ hipError_t hk_launch_calib_topp(int n_heads, int S_max, const int32_t* cand_len,
                                 float* sel_mass, int32_t* status, hipStream_t st);
 hipError_t hk_launch_pool_max(int n_heads, int S_max, const int32_t* cand_len, const uint16_t* mask,
                               const float* x, int radius, float* out, hipStream_t st);
+hipError_t hk_launch_solve_T_gd(int n_heads, int S_max, const int32_t* cand_len, const uint16_t* mask,
+                                const float* x, const int32_t* k, const float* target, float T_init,
+                                float lr, int iters, float tol, float* T_out, float* loss_out,
+                                hipStream_t st);
 hipError_t hk_launch_solve_T(int n_heads, int S_max, const int32_t* cand_len,
                              const uint16_t* mask, const float* x, const int32_t* k,
                              const float* target, float T_lo, float T_hi, int iters,

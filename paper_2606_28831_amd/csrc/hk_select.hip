@@ -435,6 +435,33 @@ __device__ __forceinline__ uint32_t ordered_key(float x) {
   return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
 }
 
+// Top-k set of x among the candidates (keys = order-preserving bits of x): keys above the
+// k-th largest plus, among the keys equal to it, the most recent slots.
+template <int EPT>
+__device__ __forceinline__ uint32_t topk_set(const uint32_t* key, uint32_t cbits, int kk, int* redi,
+                                             int* tiecnt) {
+  uint32_t top = 0;
+  if (kk <= 0) return 0;
+  uint32_t v = 0;
+  for (int b = 31; b >= 0; --b) {
+    const uint32_t t = v | (1u << b);
+    if (block_sum_int<SEL_NT>(count_ge<EPT>(key, cbits, t), redi) >= kk) v = t;
+  }
+  const int cnt_gt = (v == 0xffffffffu) ? 0 : block_sum_int<SEL_NT>(count_ge<EPT>(key, cbits, v + 1), redi);
+  const int take = kk - cnt_gt;
+  uint32_t tie = 0;
+#pragma unroll
+  for (int i = 0; i < EPT; ++i)
+    if ((cbits >> i) & 1u) {
+      if (v != 0xffffffffu && key[i] > v) top |= 1u << i;
+      if (key[i] == v) tie |= 1u << i;
+    }
+  const int n_tie = block_sum_int<SEL_NT>(__popc(tie), redi);
+  if (take >= n_tie) top |= tie;
+  else if (take > 0) top |= take_top_ties<EPT>(tie, take, tiecnt);
+  return top;
+}
+
 template <int EPT>
 __global__ __launch_bounds__(SEL_NT) void solve_T_kernel(
     int S_max, const int32_t* __restrict__ cand_len, const uint16_t* __restrict__ mask,
@@ -465,27 +492,7 @@ __global__ __launch_bounds__(SEL_NT) void solve_T_kernel(
   mx = block_max<SEL_NT>(mx, red);
   const int n_cand = block_sum_int<SEL_NT>(__popc(cbits), redi);
   const int kk = min(max(k_arr[h], 0), n_cand);
-  // Top-k set of x: keys above v plus the most recent ties
-  uint32_t top = 0;
-  if (kk > 0) {
-    uint32_t v = 0;
-    for (int b = 31; b >= 0; --b) {
-      const uint32_t t = v | (1u << b);
-      if (block_sum_int<SEL_NT>(count_ge<EPT>(key, cbits, t), redi) >= kk) v = t;
-    }
-    const int cnt_gt = (v == 0xffffffffu) ? 0 : block_sum_int<SEL_NT>(count_ge<EPT>(key, cbits, v + 1), redi);
-    const int take = kk - cnt_gt;
-    uint32_t tie = 0;
-#pragma unroll
-    for (int i = 0; i < EPT; ++i)
-      if ((cbits >> i) & 1u) {
-        if (v != 0xffffffffu && key[i] > v) top |= 1u << i;
-        if (key[i] == v) tie |= 1u << i;
-      }
-    const int n_tie = block_sum_int<SEL_NT>(__popc(tie), redi);
-    if (take >= n_tie) top |= tie;
-    else if (take > 0) top |= take_top_ties<EPT>(tie, take, tiecnt);
-  }
+  const uint32_t top = topk_set<EPT>(key, cbits, kk, redi, tiecnt);
   const float tgt = target[h];
   float a = logf(T_lo), b = logf(T_hi);
   for (int it = 0; it < iters; ++it) {
@@ -508,6 +515,104 @@ __global__ __launch_bounds__(SEL_NT) void solve_T_kernel(
     else b = mid;
   }
   if (tid == 0) T_out[h] = expf(0.5f * (a + b));
+}
+
+// a2': temperature by gradient descent (Alg. 1, Solution 2 form).  theta = log T, loss
+// (M_k(Softmax(x/T)) - target)^2, Adam (0.9 / 0.999 / 1e-8, bias-corrected, no weight
+// decay).  M_k and its derivative come from four block sums per iteration:
+// with u = 1/T and e = exp(u (x - max x)), M = sum_top e / sum e and
+// dM/dtheta = -u M (E_top[x] - E_all[x]).
+template <int EPT>
+__global__ __launch_bounds__(SEL_NT) void solve_T_gd_kernel(
+    int S_max, const int32_t* __restrict__ cand_len, const uint16_t* __restrict__ mask,
+    const float* __restrict__ x, const int32_t* __restrict__ k_arr, const float* __restrict__ target,
+    float T_init, float lr, int iters, float tol, float* __restrict__ T_out, float* __restrict__ loss_out) {
+  __shared__ float red[SEL_NW];
+  __shared__ float red4[4][SEL_NW];
+  __shared__ int redi[SEL_NW];
+  __shared__ int tiecnt[EPT * SEL_NW];
+  const int h = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int cl = cand_len[h];
+  const uint16_t* mrow = mask ? mask + (size_t)h * (S_max / HK_PAGE) : nullptr;
+  const float* xrow = x + (size_t)h * S_max;
+  uint32_t cbits = 0, key[EPT];
+  float xv[EPT];
+  float mx = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) {
+    const int j = tid + SEL_NT * i;
+    key[i] = 0;
+    xv[i] = -INFINITY;
+    if (j < S_max && is_cand(mrow, cl, j)) {
+      cbits |= 1u << i;
+      xv[i] = xrow[j];
+      key[i] = ordered_key(xv[i]);
+      mx = fmaxf(mx, xv[i]);
+    }
+  }
+  mx = block_max<SEL_NT>(mx, red);
+  const int n_cand = block_sum_int<SEL_NT>(__popc(cbits), redi);
+  const int kk = min(max(k_arr[h], 0), n_cand);
+  const uint32_t top = topk_set<EPT>(key, cbits, kk, redi, tiecnt);
+  const float tgt = target[h];
+  // M_k and dM/dtheta at theta (uniform across the block)
+  auto mass_grad = [&](float theta, float& M, float& dM) {
+    M = 0.f;
+    dM = 0.f;
+    if (kk <= 0 || mx == -INFINITY) return;
+    const float u = expf(-theta);
+    float q[4] = {0.f, 0.f, 0.f, 0.f};    // sum e, sum_top e, sum x e, sum_top x e
+#pragma unroll
+    for (int i = 0; i < EPT; ++i)
+      if ((cbits >> i) & 1u) {
+        const float e = expf((xv[i] - mx) * u);
+        const float xe = e > 0.f ? xv[i] * e : 0.f;
+        q[0] += e;
+        q[2] += xe;
+        if ((top >> i) & 1u) {
+          q[1] += e;
+          q[3] += xe;
+        }
+      }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) q[c] = wave_sum(q[c]);
+    __syncthreads();
+    if (lane == 0)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) red4[c][wave] = q[c];
+    __syncthreads();
+    float t4[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int w = 0; w < SEL_NW; ++w)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) t4[c] += red4[c][w];
+    if (t4[1] == 0.f) return;
+    M = t4[1] / t4[0];
+    dM = -u * M * (t4[3] / t4[1] - t4[2] / t4[0]);
+  };
+  float theta = logf(T_init), m = 0.f, v = 0.f, b1t = 1.f, b2t = 1.f, loss = 0.f;
+  for (int t = 1; t <= iters; ++t) {
+    float M, dM;
+    mass_grad(theta, M, dM);
+    const float gap = M - tgt;
+    loss = gap * gap;
+    if (loss < tol) break;
+    const float g = 2.f * gap * dM;
+    m = 0.9f * m + 0.1f * g;
+    v = 0.999f * v + 0.001f * g * g;
+    b1t *= 0.9f;
+    b2t *= 0.999f;
+    theta -= lr * (m / (1.f - b1t)) / (sqrtf(v / (1.f - b2t)) + 1e-8f);
+  }
+  if (iters > 0) {
+    float M, dM;
+    mass_grad(theta, M, dM);
+    loss = (M - tgt) * (M - tgt);
+  }
+  if (tid == 0) {
+    T_out[h] = expf(theta);
+    if (loss_out) loss_out[h] = loss;
+  }
 }
 
 static int ept_for(int S_max) {
@@ -579,6 +684,17 @@ hipError_t hk_launch_pool_max(int n_heads, int S_max, const int32_t* cand_len, c
                               const float* x, int radius, float* out, hipStream_t st) {
   hipLaunchKernelGGL(pool_max_kernel, dim3((S_max + POOL_TILE - 1) / POOL_TILE, n_heads), dim3(POOL_NT),
                      0, st, S_max, cand_len, mask, x, radius, out);
+  return hipGetLastError();
+}
+
+hipError_t hk_launch_solve_T_gd(int n_heads, int S_max, const int32_t* cand_len, const uint16_t* mask,
+                                const float* x, const int32_t* k, const float* target, float T_init,
+                                float lr, int iters, float tol, float* T_out, float* loss_out,
+                                hipStream_t st) {
+  TimedLaunch t(HK_TK_SOLVE_T, st);
+  HK_EPT_SWITCH(S_max, hipLaunchKernelGGL((solve_T_gd_kernel<E>), dim3(n_heads), dim3(SEL_NT), 0, st,
+                                          S_max, cand_len, mask, x, k, target, T_init, lr, iters, tol,
+                                          T_out, loss_out));
   return hipGetLastError();
 }
 

@@ -14,7 +14,7 @@ import torch
 
 from . import (Allocator, PagedKV, OP_APPEND, OP_COMPACT, OP_DECODE, OP_SCORE, dims, hk_append_kv,
                hk_budget_plan, hk_budget_select, hk_calibrate, hk_calibrate_solve_T,
-               hk_calibrate_topp, hk_compact, hk_compact_modes, hk_decode_attn, hk_pool_max,
+               hk_calibrate_solve_T_gd, hk_calibrate_topp, hk_compact, hk_compact_modes, hk_decode_attn, hk_pool_max,
                hk_score, hk_score_rows, hk_vote_topp, workspace)
 
 
@@ -48,11 +48,17 @@ class Compressor:
     probabilities on chip (buf.c / buf.c_attn are then not written).
     pool_radius: if set, the attention-mass scores are max-pooled along the sequence
     (Solution 1, SnapKV form) before calibration, into buf.s_pool.
+    t_solver: "bisect" (App. D.1) or "gd" (Alg. 1, Adam on log T) for the redundancy
+    temperature.
     """
 
     def __init__(self, NS, Hq, Hkv, D, W, kv: PagedKV, alloc: Allocator, p: float,
                  L_dense: int = 0, L_sparse: int = 0, metric: str = "attn", n_ref: int = 0,
-                 k_max: int = 0, keep_c: bool = True, pool_radius: int | None = None):
+                 k_max: int = 0, keep_c: bool = True, pool_radius: int | None = None,
+                 t_solver: str = "bisect"):
+        if t_solver not in ("bisect", "gd"):
+            raise ValueError("t_solver must be 'bisect' or 'gd'")
+        self.t_solver = t_solver
         self.d = dims(NS, Hq, Hkv, D, W)
         self.kv, self.alloc, self.p = kv, alloc, p
         self.L_dense, self.L_sparse = L_dense, L_sparse
@@ -106,8 +112,8 @@ class Compressor:
                                   b.k_attn, c_out=b.c_attn if self.keep_c else None,
                                   sel_mass=b.mass_attn, status=b.status, stream=stream)
                 b.T_red = torch.empty(H, dtype=torch.float32, device=b.c.device)
-                hk_calibrate_solve_T(H, S, b.cand_len, pm, b.x_red, b.k_attn, b.mass_attn, b.T_red,
-                                     stream=stream)
+                solve = hk_calibrate_solve_T_gd if self.t_solver == "gd" else hk_calibrate_solve_T
+                solve(H, S, b.cand_len, pm, b.x_red, b.k_attn, b.mass_attn, b.T_red, stream=stream)
             xs, Ts, ws = [s_attn, b.x_red], [None, b.T_red], [0.5, 0.5]
         hk_calibrate_topp(H, S, b.cand_len, pm, xs, Ts, ws, self.p, b.sel_bits, b.k,
                           c_out=b.c if self.keep_c else None, k_max=self.k_max,

@@ -104,6 +104,12 @@ def test_validation_errors_without_gpu(hk):
                                None, None, None) == 1                   # p outside [0, 1]
     assert L.hk_calibrate_topp(4, 128, P, None, 1, xs, None, wts, 0.9, 1, 0, None, None, P + 4, P,
                                None, None, None) == 4                   # bitmap alignment
+    assert L.hk_calibrate_solve_T_gd(4, 128, P, None, P, P, P, 0.0, 0.05, 10, 0.0, P, None,
+                                     None) == 1                 # T_init
+    assert L.hk_calibrate_solve_T_gd(4, 128, P, None, P, P, P, 1.0, -0.1, 10, 0.0, P, None,
+                                     None) == 1                 # lr
+    assert L.hk_calibrate_solve_T_gd(4, 128, P, None, P, P, P, 1.0, 0.05, -1, 0.0, P, None,
+                                     None) == 1                 # iters
     # Step 4: hard budget
     assert L.hk_score_rows(C.byref(d), P, C.byref(kv), 0, 0.125, None, P, None) == 1   # no LSE
     assert L.hk_score_rows(C.byref(hk.dims(1, 8, 2, 128, 128)), P, C.byref(kv), 0, 0.125, P, P,

@@ -334,6 +334,63 @@ def test_solve_T(case):
             assert float(T[h]) == pytest.approx(closed, rel=2e-3)
 
 
+@pytest.mark.parametrize("case", range(4))
+@pytest.mark.parametrize("S", [1024, 32768])
+def test_solve_T_gd(case, S):
+    """Alg. 1 on the GPU against the oracle's Adam iterations (fixed count), on two-level
+    rows (closed form), random rows, rows with -inf candidates and an empty Top-k."""
+    import paper_2606_28831_amd as hk
+    H = 8
+    rng = np.random.default_rng(40 + case)
+    x = np.full((H, S), -np.inf, np.float32)
+    cand_len = rng.integers(S // 64, S // 32 + 1, H).astype(np.int32) * 32
+    ks = np.zeros(H, np.int32)
+    tg = np.zeros(H, np.float32)
+    for h in range(H):
+        n = cand_len[h]
+        if case == 0:
+            k = max(1, n // 10)
+            x[h, :n] = 0.0
+            x[h, rng.permutation(n)[:k]] = 1.0
+            tg[h], ks[h] = 0.5, k
+        else:
+            x[h, :n] = (rng.standard_normal(n) * case).astype(np.float32)
+            if case == 2:
+                x[h, rng.permutation(n)[:n // 7]] = -np.inf
+            ks[h] = rng.integers(1, n // 2)
+            n_fin = int(np.isfinite(x[h, :n]).sum())
+            tg[h] = rng.uniform(min(0.9, 1.1 * ks[h] / n_fin), 0.97)   # reachable mass
+    if case == 3:
+        ks[0] = 0
+    T = torch.empty(H, device=DEV)
+    loss = torch.empty(H, device=DEV)
+    args = (H, S, torch.tensor(cand_len, device=DEV), None, torch.tensor(x, device=DEV),
+            torch.tensor(ks, device=DEV), torch.tensor(tg, device=DEV))
+    hk.hk_calibrate_solve_T_gd(*args, T, T_init=1.0, lr=0.05, iters=300, loss_out=loss)
+    torch.cuda.synchronize()
+    for h in range(H):
+        cand = np.arange(S) < cand_len[h]
+        want, wl = O.solve_T_gd_head(x[h].astype(np.float64), cand, int(ks[h]), float(tg[h]),
+                                     lr=0.05, iters=300)
+        assert float(T[h]) == pytest.approx(want, rel=2e-3), (case, h, float(T[h]), want)
+        assert float(loss[h]) <= max(1e-6, 10 * wl), (case, h)
+        if case == 0:
+            n, k = cand_len[h], ks[h]
+            assert float(T[h]) == pytest.approx(1.0 / math.log((n - k) / k), rel=2e-3)
+    # no step leaves T_init; an early stop ends below the tolerance
+    hk.hk_calibrate_solve_T_gd(*args, T, T_init=2.5, iters=0)
+    torch.cuda.synchronize()
+    assert torch.all(T == 2.5)
+    hk.hk_calibrate_solve_T_gd(*args, T, iters=300, tol=1e-6, loss_out=loss)
+    torch.cuda.synchronize()
+    for h in range(H):
+        cand = np.arange(S) < cand_len[h]
+        _, wl = O.solve_T_gd_head(x[h].astype(np.float64), cand, int(ks[h]), float(tg[h]),
+                                  lr=0.05, iters=300, tol=1e-6)
+        if wl < 5e-7:      # the oracle stopped early: so must the GPU
+            assert float(loss[h]) < 1e-6, (case, h, float(loss[h]))
+
+
 @pytest.mark.parametrize("name", list(CASES))
 @pytest.mark.parametrize("tiers", [(0, 0), (32, 64), (512, 2048)])
 def test_compact(name, tiers):

@@ -53,16 +53,25 @@ __device__ __forceinline__ void calib_values(int h, int S_max, uint32_t cbits, i
   }
 }
 
+// Candidate bits of the thread's slots.  The head's page masks are first staged in LDS by
+// coalesced loads: per-slot loads inside the candidate test would be waited on one by one.
 template <int EPT>
 __device__ __forceinline__ uint32_t cand_bits(int h, int S_max, const int32_t* __restrict__ cand_len,
                                               const uint16_t* __restrict__ mask) {
-  const int cl = cand_len[h];
-  const uint16_t* mrow = mask ? mask + (size_t)h * (S_max / HK_PAGE) : nullptr;
+  __shared__ uint16_t mrow_lds[32768 / HK_PAGE];
+  const int cl = min(cand_len[h], S_max);
+  const int np = S_max / HK_PAGE;
+  if (mask) {
+    const uint16_t* mrow = mask + (size_t)h * np;
+    for (int q = threadIdx.x; q < np; q += SEL_NT) mrow_lds[q] = mrow[q];
+    __syncthreads();
+  }
   uint32_t cbits = 0;
 #pragma unroll
   for (int i = 0; i < EPT; ++i) {
     const int j = threadIdx.x + SEL_NT * i;
-    if (j < S_max && is_cand(mrow, cl, j)) cbits |= 1u << i;
+    const bool ok = j < cl && (!mask || (((uint32_t)mrow_lds[j >> 4] >> (j & 15)) & 1u));
+    cbits |= ok ? 1u << i : 0u;
   }
   return cbits;
 }
@@ -364,7 +373,10 @@ __global__ __launch_bounds__(SEL_NT) void topp_kernel(
   const float* crow = c + (size_t)h * S_max;
   float val[EPT];
 #pragma unroll
-  for (int i = 0; i < EPT; ++i) val[i] = ((cbits >> i) & 1u) ? crow[tid + SEL_NT * i] : 0.f;
+  for (int i = 0; i < EPT; ++i) {
+    const float v = crow[min(tid + SEL_NT * i, S_max - 1)];   // unconditional: loads overlap
+    val[i] = ((cbits >> i) & 1u) ? v : 0.f;
+  }
   topp_core<EPT>(val, cbits, p_q, k_min, k_max, sel_bits + (size_t)h * (S_max / 32), S_max, k_out,
                  sel_mass, status, h, list, sh, tiecnt);
 }

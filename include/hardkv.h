@@ -16,6 +16,7 @@
  *   hk_decode_attn    paged decode attention over the variable-budget cache with the
  *                     attention-state merge (App. F)
  *   hk_append_kv      append-only dense-tier write of one decode step (Sec. 3.1 Step 1)
+ *   hk_alloc_init     a fresh device page allocator
  * Step 4 (Sec. 3.1, hard budget; Sec. 3.3.1 budget thresholds L_lower / L_upper):
  *   hk_score_rows     each window row's own attention probabilities over the candidates
  *   hk_vote_topp      Cautious Update: every row's own Top-p set, counted as votes
@@ -265,6 +266,16 @@ hk_status hk_calibrate_solve_T_gd(int32_t n_heads, int32_t S_max, const int32_t*
 hk_status hk_compact(const hk_dims* dims, const hk_paged_kv* kv, const uint32_t* sel_bits,
                      int32_t L_dense, int32_t L_sparse, const hk_allocator* alloc,
                      int32_t* status, void* workspace, size_t ws_bytes, hipStream_t stream);
+
+/* Fresh device page allocator (the free-page stack the rewrite and the append pop from,
+ * Sec. 3.3.2 metadata management): pages [first_free, num_pages) become free, listed in
+ * ascending order (free_ids[i] = first_free + i), and *free_top = num_pages - first_free;
+ * pages below first_free are taken (e.g. by the prompt).  Entries of free_ids past the
+ * top are not written.  HK_ERR_ARG unless 0 <= first_free <= num_pages and
+ * num_pages - first_free <= alloc->capacity.
+ */
+hk_status hk_alloc_init(const hk_allocator* alloc, int32_t first_free, int32_t num_pages,
+                        hipStream_t stream);
 
 /* ------------------------------------------------------------------ a5: decode
  * One decode step of attention for every query head over its KV head's valid slots

@@ -19,7 +19,7 @@ __all__ = ["HardKVError", "lib", "PagedKV", "Allocator", "hk_score", "hk_calibra
            "OP_DECODE", "OP_APPEND", "FLAG_NOSPACE", "FLAG_NAN", "FLAG_RANGE", "LIB_PATH",
            "hk_timing_enable", "hk_timing_read", "TIMED_KERNELS", "hk_calibrate_topp",
            "hk_pool_max", "hk_score_rows", "hk_vote_topp", "hk_budget_plan", "hk_budget_select",
-           "hk_compact_modes", "hk_calibrate_solve_T_gd", "BUDGET_KEEP", "BUDGET_SPARSE", "BUDGET_REWRITE"]
+           "hk_compact_modes", "hk_calibrate_solve_T_gd", "hk_alloc_init", "BUDGET_KEEP", "BUDGET_SPARSE", "BUDGET_REWRITE"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhardkv.so")
 
@@ -31,7 +31,7 @@ EXPORTED = ["hk_score", "hk_calibrate", "hk_calibrate_solve_T", "hk_topp_select"
             "hk_decode_attn", "hk_append_kv", "hk_workspace_size", "hk_status_string",
             "hk_timing_enable", "hk_timing_read", "hk_calibrate_topp", "hk_pool_max",
             "hk_score_rows", "hk_vote_topp", "hk_budget_plan", "hk_budget_select",
-            "hk_compact_modes", "hk_calibrate_solve_T_gd"]
+            "hk_compact_modes", "hk_calibrate_solve_T_gd", "hk_alloc_init"]
 # kernel ids of hk_timing_read, in header order
 TIMED_KERNELS = ["score_pass1", "score_merge", "score_pass2", "calibrate", "topp", "solve_T",
                  "compact_gather", "compact_meta", "decode_split", "decode_merge", "append",
@@ -112,6 +112,8 @@ def lib():
                                        C.POINTER(hk_allocator), P, P, C.c_size_t, P]
         L.hk_calibrate_solve_T_gd.restype = I32
         L.hk_calibrate_solve_T_gd.argtypes = [I32, I32, P, P, P, P, P, F, F, I32, F, P, P, P]
+        L.hk_alloc_init.restype = I32
+        L.hk_alloc_init.argtypes = [C.POINTER(hk_allocator), I32, I32, P]
         L.hk_timing_enable.restype = I32
         L.hk_timing_enable.argtypes = [C.c_uint32]
         L.hk_timing_read.restype = I32
@@ -255,6 +257,11 @@ def hk_calibrate_solve_T_gd(n_heads: int, S_max: int, cand_len, page_mask, x, k,
                                          _ptr(x), _ptr(k), _ptr(target_mass), float(T_init),
                                          float(lr), int(iters), float(tol), _ptr(T_out),
                                          _ptr(loss_out), _stream(stream)), "hk_calibrate_solve_T_gd")
+
+
+def hk_alloc_init(alloc: Allocator, first_free: int, num_pages: int, stream=None):
+    _check(lib().hk_alloc_init(C.byref(alloc.desc), int(first_free), int(num_pages),
+                               _stream(stream)), "hk_alloc_init")
 
 
 def hk_compact(d: hk_dims, kv: PagedKV, sel_bits, L_dense: int, L_sparse: int, alloc: Allocator,

@@ -305,6 +305,16 @@ hk_status hk_budget_select(int32_t n_heads, int32_t S_max, const int32_t* cand_l
                                           head_mode, k_cap, n_sink, sel_out, k_out, stream));
 }
 
+hk_status hk_alloc_init(const hk_allocator* alloc, int32_t first_free, int32_t num_pages,
+                        hipStream_t stream) {
+  if (!alloc || !alloc->free_ids || !alloc->free_top) return HK_ERR_ARG;
+  if (first_free < 0 || num_pages < first_free || num_pages - first_free > alloc->capacity)
+    return HK_ERR_ARG;
+  if (!aligned16(alloc->free_ids)) return HK_ERR_ALIGN;
+  return launched(hk_launch_alloc_init(alloc->free_ids, alloc->free_top, first_free,
+                                       num_pages - first_free, stream));
+}
+
 hk_status hk_decode_attn(const hk_dims* dims, const void* q, const hk_paged_kv* kv, float sm_scale,
                          float* o, float* lse, void* workspace, size_t ws_bytes, hipStream_t stream) {
   hk_status e = check_dims(dims, false);

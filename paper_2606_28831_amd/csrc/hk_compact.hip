@@ -408,9 +408,25 @@ __global__ __launch_bounds__(256) void compact_push_kernel(int32_t* __restrict__
   if (blockIdx.x == 0 && threadIdx.x == 0) *free_top = g.base + g.total_free;
 }
 
+// Fresh allocator: free_ids[i] = first_free + i for the n free pages, top = n.
+__global__ __launch_bounds__(256) void alloc_init_kernel(int32_t* __restrict__ free_ids,
+                                                        int32_t* __restrict__ free_top, int first_free,
+                                                        int n) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x)
+    free_ids[i] = first_free + i;
+  if (blockIdx.x == 0 && threadIdx.x == 0) *free_top = n;
+}
+
 }  // namespace hk
 
 using namespace hk;
+
+hipError_t hk_launch_alloc_init(int32_t* free_ids, int32_t* free_top, int first_free, int n,
+                                hipStream_t st) {
+  const int blocks = max(1, min((n + 255) / 256, 1024));
+  hipLaunchKernelGGL(alloc_init_kernel, dim3(blocks), dim3(256), 0, st, free_ids, free_top, first_free, n);
+  return hipGetLastError();
+}
 
 size_t hk_compact_ws(int n_heads, int max_pages) {
   return align256(sizeof(HeadPlan) * (size_t)n_heads) + 2 * align256(sizeof(int) * (size_t)n_heads) +

@@ -110,6 +110,11 @@ def test_validation_errors_without_gpu(hk):
                                      None) == 1                 # lr
     assert L.hk_calibrate_solve_T_gd(4, 128, P, None, P, P, P, 1.0, 0.05, -1, 0.0, P, None,
                                      None) == 1                 # iters
+    a64 = hk.hk_allocator(P, P, 64)
+    assert L.hk_alloc_init(C.byref(a64), -1, 10, None) == 1
+    assert L.hk_alloc_init(C.byref(a64), 10, 5, None) == 1           # num_pages < first_free
+    assert L.hk_alloc_init(C.byref(a64), 0, 65, None) == 1           # beyond the capacity
+    assert L.hk_alloc_init(C.byref(hk.hk_allocator(P + 4, P, 64)), 0, 8, None) == 4
     # Step 4: hard budget
     assert L.hk_score_rows(C.byref(d), P, C.byref(kv), 0, 0.125, None, P, None) == 1   # no LSE
     assert L.hk_score_rows(C.byref(hk.dims(1, 8, 2, 128, 128)), P, C.byref(kv), 0, 0.125, P, P,

@@ -413,6 +413,42 @@ def test_compact(name, tiers):
         before["table"][h], before["mask"][h], int(before["n"][h]), sel, L_dense, L_sparse))
 
 
+def test_alloc_init_then_rewrite():
+    """hk_alloc_init lists pages [first_free, num_pages) in ascending order; a rewrite then
+    pops its pages from that stack (the layout checked as for any rewrite)."""
+    hk, cfg, w, kv = _setup("bf16_d128_g4_ragged_holes", max_pages=None)
+    num = w.k_pool.shape[0]
+    # relabel the live pages to ids 0 .. n_live-1 (pages moved along), so that every page
+    # from n_live up is free
+    table = w.page_table
+    live_ids = torch.unique(table[table >= 0])
+    first = int(live_ids.numel())
+    remap = torch.full((num,), -1, dtype=torch.int32, device=DEV)
+    remap[live_ids.long()] = torch.arange(first, dtype=torch.int32, device=DEV)
+    for pool in (w.k_pool, w.v_pool):
+        moved = pool[live_ids.long()].clone()
+        pool[:first] = moved
+    w.page_table.copy_(torch.where(table >= 0, remap[table.clamp(min=0).long()], table))
+    alloc = hk.Allocator(w.free_ids, w.free_top)
+    hk.hk_alloc_init(alloc, first, num)
+    torch.cuda.synchronize()
+    top = int(w.free_top.item())
+    assert top == num - first
+    assert np.array_equal(np_i(w.free_ids)[:top], np.arange(first, num))
+    H, S = w.n_heads, w.S_max
+    d = hk.dims(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"], cfg["W"])
+    sel_np = np.random.default_rng(8).integers(-2 ** 31, 2 ** 31, size=(H, S // 32),
+                                               dtype=np.int64).astype(np.int32)
+    before = snapshot(w)
+    st = torch.zeros(1, dtype=torch.int32, device=DEV)
+    hk.hk_compact(d, kv, torch.tensor(sel_np, device=DEV), 0, 0, alloc, st,
+                  hk.workspace(hk.OP_COMPACT, d, w.max_pages, DEV))
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    check_compaction(w, before, sel_np, S, lambda h, sel: O.compact_head(
+        before["table"][h], before["mask"][h], int(before["n"][h]), sel, 0, 0))
+
+
 def test_compact_nospace_leaves_cache_unchanged():
     hk, cfg, w, kv = _setup("bf16_d128_g4_ragged_holes")
     H, S = w.n_heads, w.S_max

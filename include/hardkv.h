@@ -9,6 +9,7 @@
  *   hk_calibrate_solve_T_gd  the same temperature by gradient descent (Alg. 1)
  *   hk_topp_select    head-adaptive Top-p budget (Sec. 3.2, Problem 1)
  *   hk_calibrate_topp hk_calibrate followed by hk_topp_select in one launch
+ *   hk_compress       score -> calibrate + Top-p -> compact in one call
  *   hk_pool_max       order-preserving max-pooling of scores before calibration
  *                     (Sec. 3.2 Solution 1, SnapKV form)
  *   hk_compact        Cascade-Cache rewrite into dense / sparse / condensed tiers
@@ -110,7 +111,7 @@ typedef struct {
   int32_t W;             /* observation-window length                                   */
 } hk_dims;
 
-enum { HK_OP_SCORE = 0, HK_OP_COMPACT = 1, HK_OP_DECODE = 2, HK_OP_APPEND = 3 };
+enum { HK_OP_SCORE = 0, HK_OP_COMPACT = 1, HK_OP_DECODE = 2, HK_OP_APPEND = 3, HK_OP_COMPRESS = 4 };
 
 /* Bytes of workspace entry point `op` needs for these dims and table width. */
 size_t hk_workspace_size(int32_t op, const hk_dims* dims, int32_t max_pages);
@@ -247,6 +248,22 @@ hk_status hk_calibrate_solve_T_gd(int32_t n_heads, int32_t S_max, const int32_t*
                                   const uint16_t* page_mask, const float* x, const int32_t* k,
                                   const float* target_mass, float T_init, float lr, int32_t iters,
                                   float tol, float* T_out, float* loss_out, hipStream_t stream);
+
+/* ------------------------------------------------------------------ the whole step
+ * One compression step (Sec. 3.1 Steps 2-3) in one call: hk_score (attention mass; row
+ * LSEs computed, or taken from row_lse_in) -> hk_calibrate_topp (one metric, T = 1; the
+ * calibrated probabilities stay on chip) -> hk_compact, on `stream`, in that order.  The
+ * scores, candidate counts, row LSEs and every stage's scratch live in `workspace`
+ * (>= hk_workspace_size(HK_OP_COMPRESS, dims, max_pages) bytes, 256-byte aligned).
+ * Outputs: k_out [n_heads] (the Top-p counts), sel_bits_out [n_heads][S_max/32] or NULL
+ * (the selection is then kept in the workspace), status (HK_FLAG_* of every stage).
+ * Arguments and errors as for the three calls it makes.
+ */
+hk_status hk_compress(const hk_dims* dims, const void* q_obs, const hk_paged_kv* kv,
+                      int32_t L_dense, int32_t L_sparse, float sm_scale, const float* row_lse_in,
+                      double p, int32_t k_min, int32_t k_max, const hk_allocator* alloc,
+                      uint32_t* sel_bits_out, int32_t* k_out, int32_t* status, void* workspace,
+                      size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------ a4: compact
  * Cascade-Cache rewrite (Sec. 3.1 Step 3; Sec. 3.3.1).  Per head, page positions are

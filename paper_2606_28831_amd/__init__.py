@@ -19,19 +19,19 @@ __all__ = ["HardKVError", "lib", "PagedKV", "Allocator", "hk_score", "hk_calibra
            "OP_DECODE", "OP_APPEND", "FLAG_NOSPACE", "FLAG_NAN", "FLAG_RANGE", "LIB_PATH",
            "hk_timing_enable", "hk_timing_read", "TIMED_KERNELS", "hk_calibrate_topp",
            "hk_pool_max", "hk_score_rows", "hk_vote_topp", "hk_budget_plan", "hk_budget_select",
-           "hk_compact_modes", "hk_calibrate_solve_T_gd", "hk_alloc_init", "BUDGET_KEEP", "BUDGET_SPARSE", "BUDGET_REWRITE"]
+           "hk_compact_modes", "hk_calibrate_solve_T_gd", "hk_alloc_init", "hk_compress", "OP_COMPRESS", "BUDGET_KEEP", "BUDGET_SPARSE", "BUDGET_REWRITE"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhardkv.so")
 
 HK_F32, HK_BF16 = 0, 1
-OP_SCORE, OP_COMPACT, OP_DECODE, OP_APPEND = 0, 1, 2, 3
+OP_SCORE, OP_COMPACT, OP_DECODE, OP_APPEND, OP_COMPRESS = 0, 1, 2, 3, 4
 FLAG_NOSPACE, FLAG_NAN, FLAG_RANGE = 1, 2, 4
 BUDGET_KEEP, BUDGET_SPARSE, BUDGET_REWRITE = 0, 1, 2
 EXPORTED = ["hk_score", "hk_calibrate", "hk_calibrate_solve_T", "hk_topp_select", "hk_compact",
             "hk_decode_attn", "hk_append_kv", "hk_workspace_size", "hk_status_string",
             "hk_timing_enable", "hk_timing_read", "hk_calibrate_topp", "hk_pool_max",
             "hk_score_rows", "hk_vote_topp", "hk_budget_plan", "hk_budget_select",
-            "hk_compact_modes", "hk_calibrate_solve_T_gd", "hk_alloc_init"]
+            "hk_compact_modes", "hk_calibrate_solve_T_gd", "hk_alloc_init", "hk_compress"]
 # kernel ids of hk_timing_read, in header order
 TIMED_KERNELS = ["score_pass1", "score_merge", "score_pass2", "calibrate", "topp", "solve_T",
                  "compact_gather", "compact_meta", "decode_split", "decode_merge", "append",
@@ -114,6 +114,9 @@ def lib():
         L.hk_calibrate_solve_T_gd.argtypes = [I32, I32, P, P, P, P, P, F, F, I32, F, P, P, P]
         L.hk_alloc_init.restype = I32
         L.hk_alloc_init.argtypes = [C.POINTER(hk_allocator), I32, I32, P]
+        L.hk_compress.restype = I32
+        L.hk_compress.argtypes = [C.POINTER(hk_dims), P, C.POINTER(hk_paged_kv), I32, I32, F, P, D,
+                                  I32, I32, C.POINTER(hk_allocator), P, P, P, P, SZ, P]
         L.hk_timing_enable.restype = I32
         L.hk_timing_enable.argtypes = [C.c_uint32]
         L.hk_timing_read.restype = I32
@@ -257,6 +260,15 @@ def hk_calibrate_solve_T_gd(n_heads: int, S_max: int, cand_len, page_mask, x, k,
                                          _ptr(x), _ptr(k), _ptr(target_mass), float(T_init),
                                          float(lr), int(iters), float(tol), _ptr(T_out),
                                          _ptr(loss_out), _stream(stream)), "hk_calibrate_solve_T_gd")
+
+
+def hk_compress(d: hk_dims, q_obs, kv: PagedKV, L_dense: int, L_sparse: int, sm_scale: float,
+                p: float, alloc: Allocator, k_out, ws, status=None, sel_bits_out=None,
+                row_lse_in=None, k_min: int = 1, k_max: int = 0, stream=None):
+    _check(lib().hk_compress(C.byref(d), _ptr(q_obs), C.byref(kv.desc), int(L_dense), int(L_sparse),
+                             float(sm_scale), _ptr(row_lse_in), float(p), int(k_min), int(k_max),
+                             C.byref(alloc.desc), _ptr(sel_bits_out), _ptr(k_out), _ptr(status),
+                             _ptr(ws), ws.numel(), _stream(stream)), "hk_compress")
 
 
 def hk_alloc_init(alloc: Allocator, first_free: int, num_pages: int, stream=None):

@@ -45,6 +45,27 @@ hk_status check_rows(int n_heads, int S_max, const int32_t* cand_len) {
 
 hk_status launched(hipError_t e) { return e == hipSuccess ? HK_OK : HK_ERR_HIP; }
 
+size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Workspace of hk_compress: scores, candidate counts, row LSEs, selection, then the score
+// and compaction scratch (the two stages run one after the other; they share one region).
+struct CompressWs {
+  size_t s, cand, lse, sel, scratch, total;
+};
+CompressWs compress_ws(const hk_dims* d, int max_pages) {
+  const size_t H = (size_t)d->NS * d->Hkv, S = (size_t)max_pages * HK_PAGE;
+  CompressWs w;
+  w.s = 0;
+  w.cand = w.s + al256(H * S * 4);
+  w.lse = w.cand + al256(H * 4);
+  w.sel = w.lse + al256((size_t)d->W * d->NS * d->Hq * 4);
+  w.scratch = w.sel + al256(H * (S / 32) * 4);
+  const size_t a = hk_score_ws(d->NS, d->Hq, d->Hkv, d->D, d->W, max_pages);
+  const size_t b = hk_compact_ws((int)H, max_pages);
+  w.total = w.scratch + al256(a > b ? a : b);
+  return w;
+}
+
 }  // namespace
 
 extern "C" {
@@ -56,6 +77,7 @@ size_t hk_workspace_size(int32_t op, const hk_dims* d, int32_t max_pages) {
     case HK_OP_COMPACT: return hk_compact_ws(d->NS * d->Hkv, max_pages);
     case HK_OP_DECODE: return hk_decode_ws(d->NS, d->Hq, d->Hkv, d->D, max_pages);
     case HK_OP_APPEND: return hk_append_ws(d->NS, d->Hkv);
+    case HK_OP_COMPRESS: return compress_ws(d, max_pages).total;
     default: return 0;
   }
 }
@@ -229,6 +251,39 @@ hk_status hk_compact(const hk_dims* dims, const hk_paged_kv* kv, const uint32_t*
   if (!aligned256(workspace)) return HK_ERR_ALIGN;
   return launched(hk_launch_compact(n_heads, dims->D, kv, sel_bits, L_dense, L_sparse, nullptr,
                                     alloc, status, workspace, stream));
+}
+
+hk_status hk_compress(const hk_dims* dims, const void* q_obs, const hk_paged_kv* kv,
+                      int32_t L_dense, int32_t L_sparse, float sm_scale, const float* row_lse_in,
+                      double p, int32_t k_min, int32_t k_max, const hk_allocator* alloc,
+                      uint32_t* sel_bits_out, int32_t* k_out, int32_t* status, void* workspace,
+                      size_t ws_bytes, hipStream_t stream) {
+  hk_status e = check_dims(dims, true);
+  if (e) return e;
+  if ((e = check_kv(kv, true))) return e;
+  if (!k_out || !workspace) return HK_ERR_ARG;
+  if (!(p >= 0.0 && p <= 1.0)) return HK_ERR_ARG;
+  const CompressWs cw = compress_ws(dims, kv->max_pages);
+  if (ws_bytes < cw.total) return HK_ERR_WORKSPACE;
+  if (!aligned256(workspace)) return HK_ERR_ALIGN;
+  if (sel_bits_out && !aligned16(sel_bits_out)) return HK_ERR_ALIGN;
+  char* ws = static_cast<char*>(workspace);
+  float* s = reinterpret_cast<float*>(ws + cw.s);
+  int32_t* cand = reinterpret_cast<int32_t*>(ws + cw.cand);
+  float* lse = reinterpret_cast<float*>(ws + cw.lse);
+  uint32_t* sel = sel_bits_out ? sel_bits_out : reinterpret_cast<uint32_t*>(ws + cw.sel);
+  void* scratch = ws + cw.scratch;
+  const size_t scratch_bytes = ws_bytes - cw.scratch;
+  e = hk_score(dims, q_obs, kv, L_dense, sm_scale, row_lse_in, row_lse_in ? nullptr : lse, s, cand,
+               nullptr, 0, nullptr, scratch, scratch_bytes, stream);
+  if (e) return e;
+  const int n_heads = dims->NS * dims->Hkv, S_max = kv->max_pages * HK_PAGE;
+  const float* xs[1] = {s};
+  const float w1[1] = {1.0f};
+  e = hk_calibrate_topp(n_heads, S_max, cand, kv->page_mask, 1, xs, nullptr, w1, p, k_min, k_max,
+                        nullptr, nullptr, sel, k_out, nullptr, status, stream);
+  if (e) return e;
+  return hk_compact(dims, kv, sel, L_dense, L_sparse, alloc, status, scratch, scratch_bytes, stream);
 }
 
 hk_status hk_compact_modes(const hk_dims* dims, const hk_paged_kv* kv, const uint32_t* sel_bits,

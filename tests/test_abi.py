@@ -53,6 +53,10 @@ def test_workspace_sizes(hk):
     assert hk.hk_workspace_size(hk.OP_SCORE, d, 4096) > hk.hk_workspace_size(hk.OP_SCORE, d, 2048)
     assert hk.hk_workspace_size(hk.OP_COMPACT, d, 2048) >= 2 * 128 * 2048 * 4
     assert hk.hk_workspace_size(hk.OP_DECODE, d, 2048) > 0
+    # the whole step: the scores (4 bytes per slot) and the larger stage scratch at least
+    cw = hk.hk_workspace_size(hk.OP_COMPRESS, d, 2048)
+    assert cw >= 128 * 2048 * 16 * 4 + max(hk.hk_workspace_size(hk.OP_SCORE, d, 2048),
+                                           hk.hk_workspace_size(hk.OP_COMPACT, d, 2048))
     assert hk.hk_workspace_size(99, d, 2048) == 0
 
 
@@ -110,6 +114,10 @@ def test_validation_errors_without_gpu(hk):
                                      None) == 1                 # lr
     assert L.hk_calibrate_solve_T_gd(4, 128, P, None, P, P, P, 1.0, 0.05, -1, 0.0, P, None,
                                      None) == 1                 # iters
+    assert L.hk_compress(C.byref(d), P, C.byref(kv), 0, 0, 0.125, None, 0.9, 1, 0, C.byref(alloc),
+                         None, P, None, P, 16, None) == 5       # workspace too small
+    assert L.hk_compress(C.byref(d), P, C.byref(kv), 0, 0, 0.125, None, 1.5, 1, 0, C.byref(alloc),
+                         None, P, None, P, 1 << 30, None) == 1  # p outside [0, 1]
     a64 = hk.hk_allocator(P, P, 64)
     assert L.hk_alloc_init(C.byref(a64), -1, 10, None) == 1
     assert L.hk_alloc_init(C.byref(a64), 10, 5, None) == 1           # num_pages < first_free

@@ -449,6 +449,40 @@ def test_alloc_init_then_rewrite():
         before["table"][h], before["mask"][h], int(before["n"][h]), sel, 0, 0))
 
 
+@pytest.mark.parametrize("name,tiers", [("bf16_d128_g7_tempered", (0, 0)),
+                                        ("bf16_d128_g4_ragged_holes", (48, 96)),
+                                        ("cfg1_f32_d64_g4", (0, 0))])
+def test_compress_equals_separate_calls(name, tiers):
+    """hk_compress leaves exactly what hk_score, hk_calibrate_topp and hk_compact leave."""
+    import paper_2606_28831_amd as hk
+    from paper_2606_28831_amd.pipeline import Compressor
+    L_dense, L_sparse = tiers
+    outs = []
+    for fused in (False, True):
+        _, cfg, w, kv = _setup(name)
+        alloc = hk.Allocator(w.free_ids, w.free_top)
+        H, S = w.n_heads, w.S_max
+        st = torch.zeros(1, dtype=torch.int32, device=DEV)
+        if fused:
+            d = hk.dims(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"], cfg["W"])
+            k = torch.empty(H, dtype=torch.int32, device=DEV)
+            sel = torch.empty(H, S // 32, dtype=torch.int32, device=DEV)
+            ws = hk.workspace(hk.OP_COMPRESS, d, w.max_pages, DEV)
+            hk.hk_compress(d, w.q_obs, kv, L_dense, L_sparse, 1 / math.sqrt(cfg["D"]),
+                           cfg.get("p", 0.9), alloc, k, ws, status=st, sel_bits_out=sel)
+        else:
+            comp = Compressor(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"], cfg["W"], kv, alloc,
+                              cfg.get("p", 0.9), L_dense=L_dense, L_sparse=L_sparse, keep_c=False)
+            comp.step(w.q_obs)
+            k, sel, st = comp.buf.k, comp.buf.sel_bits, comp.buf.status
+        torch.cuda.synchronize()
+        outs.append([t.cpu().clone() for t in (k, sel, st, w.page_table, w.page_mask, w.n_pages,
+                                               w.free_ids, w.free_top)]
+                    + [w.k_pool.view(torch.int16 if w.k_pool.dtype == torch.bfloat16 else torch.int32).cpu()])
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
+
+
 def test_compact_nospace_leaves_cache_unchanged():
     hk, cfg, w, kv = _setup("bf16_d128_g4_ragged_holes")
     H, S = w.n_heads, w.S_max

@@ -233,6 +233,11 @@ def run_compression(args):
     st = {"score": avg(0, 1), "select": avg(1, 2), "compact": avg(2, 3), "score_pass2": avg(4, 5)}
     st["score_pass1_merge"] = st["score"] - st["score_pass2"]
     step_ms_events = st["score"] + st["select"] + st["compact"]
+    steps_ev = sorted(ev[8 * r].elapsed_time(ev[8 * r + 3]) for r in range(reps))
+
+    def pct(q):
+        return steps_ev[min(len(steps_ev) - 1, int(round(q * (len(steps_ev) - 1))))]
+    step_pcts = {"p10": pct(0.1), "p50": pct(0.5), "p90": pct(0.9), "reps": reps}
 
     # ---------------- budget statistics of the last step
     restore()
@@ -297,6 +302,12 @@ def run_compression(args):
         "positions_per_s": positions / step_s,
         "stage_ms": st,
         "step_ms_events": step_ms_events,
+        "step_ms_events_percentiles": step_pcts,
+        # score GEMM throughput per pass (two passes unless the row LSEs are given)
+        "score_mfma": {"pass1_tflops": per_launch["score_pass1"][1] / (st["score_pass1_merge"] * 1e-3) / 1e12,
+                       "pass2_tflops": per_launch["score_pass2"][1] / (st["score_pass2"] * 1e-3) / 1e12,
+                       "pass2_frac_bf16_peak": per_launch["score_pass2"][1] / (st["score_pass2"] * 1e-3)
+                       / 1e12 / BF16_PEAK_TFLOPS, "flops_per_pass": per_launch["score_pass2"][1]},
         "ms_per_step_no_kernel_events": ms_per_step_plain,
         "kernel_ms_discovery_step": kernels_discovery,
         "budget": {"mean_kept": kept_mean, "min_frac": float(frac.min()),

@@ -692,3 +692,19 @@ def test_solve_T_gd_first_adam_step():
         g = 2 * (M - target) * dM
         T, _ = O.solve_T_gd_head(x, cand, 2, target, T_init=1.0, lr=lr, iters=1)
         assert math.log(T) == pytest.approx(-lr * math.copysign(1.0, g), rel=1e-6)
+
+
+def test_topp_p_is_quantised_to_1e_6():
+    """p counts in steps of 1e-6 (round half to even): ten equal values need exactly three
+    slots for p = 0.3 and for any p that rounds to 0.300000, and a fourth as soon as p
+    rounds to 0.300001 (its target then exceeds three equal weights)."""
+    c = np.full(10, 0.1, np.float32)
+    cand = np.ones(10, bool)
+    assert O.topp_head(c, cand, 0.3).k == 3
+    assert O.topp_head(c, cand, 0.3000004).k == 3
+    assert O.topp_head(c, cand, 0.2999996).k == 3
+    assert O.topp_head(c, cand, 0.3000006).k == 4
+    # the target is ceil(p_q * Total / 10^6) in exact integers
+    r = O.topp_head(c, cand, 0.3000006)
+    w = int(math.floor(float(np.float32(0.1)) * 2 ** 40))
+    assert r.total == 10 * w and r.target == -(-(300001 * 10 * w) // 10 ** 6)

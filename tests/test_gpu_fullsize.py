@@ -139,3 +139,77 @@ def test_full_size_sampled(c):
             assert np.array_equal(got, wk) and np.array_equal(gotv, wv), f"cfg{c} bytes head {h} page {i}"
         for i, (pid, m) in enumerate(sparse + dense):
             assert new_table[npc + i] == pid and new_mask[npc + i] == m, f"cfg{c} kept page head {h}"
+
+
+@pytest.mark.timeout(900)
+def test_budget_full_size_sampled():
+    """The hard-budget step (Cautious Update votes, L_lower 2048 / L_upper 4096, 4 sinks) at
+    config 3's full size in bench.py's launch configuration, on sampled heads: sampled rows'
+    probabilities against the oracle, each sampled row's set by the Top-p properties on the
+    probabilities it was made from, votes as the column counts of all row sets, the
+    selection by its ranking properties, and the rewrite by its layout."""
+    import paper_2606_28831_amd as hk
+    from paper_2606_28831_amd.pipeline import BudgetCompressor
+    from hk_testlib import check_topp_rule
+    cfg = WL.config(3)
+    w = WL.make_workload(cfg, DEV)
+    kv = hk.PagedKV(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)
+    alloc = hk.Allocator(w.free_ids, w.free_top)
+    comp = BudgetCompressor(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"], cfg["W"], kv, alloc, cfg["p"],
+                            2048, 4096, L_dense=cfg["L_dense"], n_sink=4)
+    pre = {"table": np_i(w.page_table).copy(), "mask": np_i(w.page_mask).astype(np.int64) & 0xFFFF,
+           "n": np_i(w.n_pages).copy()}
+    comp.select(w.q_obs)
+    torch.cuda.synchronize()
+    b = comp.buf
+    G, D, R, S = cfg["Hq"] // cfg["Hkv"], cfg["D"], comp.R, w.S_max
+    scale = 1 / math.sqrt(D)
+    heads = _sample_heads(np_i(b["k"]), 3)
+    host = HostCache(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages, heads=heads)
+    src = {h: (host.head(h)[0], host.head_v(h)[0], host.head(h)[1]) for h in heads}
+    sel_all, v_all, k_all = np_i(b["sel_bits"]), np_i(b["votes"]).astype(np.int64) & 0xFFFF, np_i(b["k"])
+    mode, cap = np_i(b["head_mode"]), np_i(b["k_cap"])
+    rng = np.random.default_rng(9)
+    for h in heads:
+        rows, vrows, valid = src[h]
+        n = int(pre["n"][h])
+        cand = np.zeros(S, bool)
+        cand[:len(valid)] = O.candidate_mask(valid, 16 * n)
+        s_, kvh = divmod(h, cfg["Hkv"])
+        q = w.q_obs[:, s_, kvh * G:(kvh + 1) * G].float().cpu().numpy().astype(np.float64).reshape(-1, D)
+        _, lse = O.score_head(q, rows, valid, 16 * n, scale)
+        row_bits = np.stack([unpack_bits(r, S) for r in np_i(b["row_sel"][h])])
+        assert np.array_equal(row_bits.sum(axis=0), v_all[h]), f"votes head {h}"
+        a_gpu = b["a_rows"][h].cpu().numpy()
+        for r in rng.choice(R, size=3, replace=False):
+            a_ref = O.score_rows_head(q[r:r + 1], rows, valid, 16 * n, scale, lse[r:r + 1])[0]
+            full = np.zeros(S)
+            full[:len(a_ref)] = a_ref
+            check_prob(a_gpu[r], full, 2e-3, f"a head {h} row {r}")
+            check_topp_rule(a_gpu[r], row_bits[r], int(row_bits[r].sum()), cand, cfg["p"],
+                            what=f"row {r} head {h}")
+        # selection: every head is above L_upper here, so every head is rewritten under the cap
+        assert mode[h] == O.REWRITE and cap[h] == 4096
+        sel = unpack_bits(sel_all[h], S)
+        sinks = cand & (np.arange(S) < 4)
+        base = cand & ~sinks & (v_all[h] >= 1)
+        assert np.array_equal(sel & sinks, sinks) and not (sel & ~(sinks | base)).any()
+        assert int(k_all[h]) == int(sel.sum()) == min(int(base.sum()), 4096 - int(sinks.sum())) + int(sinks.sum())
+        kept, dropped = np.nonzero(sel & base)[0], np.nonzero(base & ~sel)[0]
+        if len(kept) and len(dropped):
+            assert min((v_all[h][j], j) for j in kept) > max((v_all[h][j], j) for j in dropped), h
+    comp.compact()
+    torch.cuda.synchronize()
+    assert int(b["status"].item()) == 0
+    for h in heads:
+        rows, vrows, valid = src[h]
+        n = int(pre["n"][h])
+        sel = unpack_bits(sel_all[h], S)
+        want = rewritten_sources(pre["table"][h], pre["mask"][h], n, sel, n)
+        assert int(w.n_pages[h]) == -(-len(want) // 16) and 16 * int(w.n_pages[h]) <= 4096
+        new_table = np_i(w.page_table[h])
+        pos_of = {int(pid): i for i, pid in enumerate(pre["table"][h][:n])}
+        for i in range(int(w.n_pages[h])):
+            chunk = want[16 * i:16 * (i + 1)]
+            got = w.k_pool[int(new_table[i])][:len(chunk)].float().cpu().numpy()
+            assert np.array_equal(got, np.stack([rows[pos_of[ph] * 16 + t] for ph, t in chunk])), (h, i)

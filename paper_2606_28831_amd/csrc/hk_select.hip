@@ -102,10 +102,10 @@ __device__ __forceinline__ float fixed_weight(uint32_t key) {
   return truncf(__uint_as_float(key) * (float)kMassOne);
 }
 
-// Threshold searches run most-significant bit first: the answer v is the largest key
-// with mass(key >= v) >= target (or count(key >= v) >= k); both are monotone in v.
-// (The empty asm keeps the compiler from hoisting the EPT weights out of a search loop
-// into registers of their own, which would spill.)
+// Mass and count of the candidates with key >= t (one thread's share; the threshold
+// searches themselves are radix searches, sel_radix_threshold below).  (The empty asm
+// keeps the compiler from hoisting the EPT weights into registers of their own, which
+// would spill.)
 template <int EPT, typename K>
 __device__ __forceinline__ unsigned long long mass_ge(const K& key, uint32_t cbits, uint32_t t) {
   double m = 0.0;
@@ -177,11 +177,6 @@ __device__ __forceinline__ int2 block_exscan_int(int v, int* red) {
   return make_int2(before + x - v, all);
 }
 
-// Below the bits all candidates share, SEL_COARSE bits are searched with every candidate
-// in registers; the candidates that still share the prefix found are then packed into LDS
-// (`list`, room for S_max keys) and the remaining low bits are searched over that list.
-constexpr int SEL_COARSE = 9;
-
 template <bool MAX>
 __device__ __forceinline__ uint32_t block_minmax_u32(uint32_t v, int* red) {
   v = wave_reduce_u32(v, MAX ? 0u : 0xffffffffu,
@@ -206,10 +201,19 @@ __device__ __forceinline__ unsigned long long uniform_u64(unsigned long long x) 
   return ((unsigned long long)hi << 32) | lo;
 }
 
+constexpr int SEL_RADIX_BITS = 11;
+constexpr int SEL_BINS = 1 << SEL_RADIX_BITS;
+constexpr int SEL_BPT = SEL_BINS / SEL_NT;        // digits per thread in the suffix scan
+
 struct SelLds {
   unsigned long long red64[SEL_NW];
   int redi[SEL_NW];
+  unsigned long long hist[SEL_BINS];
+  unsigned long long pick_above;
+  uint32_t pick_digit;
 };
+
+
 
 // Head-adaptive Top-p (Sec. 3.3) on the thread's EPT values: the smallest set whose
 // fixed-point mass reaches ceil(p_q * Total / 10^6), ties at the threshold broken toward
@@ -220,6 +224,106 @@ struct KeyView {
   const float* v;
   __device__ __forceinline__ uint32_t operator[](int i) const { return __float_as_uint(v[i]); }
 };
+
+// A copy of x the compiler cannot see through: per-element tests of a fresh copy are not
+// hoisted out of the search rounds and kept (as EPT lane masks) across them.
+template <typename X>
+__device__ __forceinline__ X sel_opaque(X x) {
+  asm volatile("" : "+v"(x));
+  return x;
+}
+
+// Largest key v of the candidates with W(key >= v) >= target (0 < target <= W(all)), W the
+// sum of weight(key).  The bits above the highest one where kmin and kmax differ are shared
+// by every candidate, hence by v; below them v is found 11 bits at a time from a histogram
+// of weights per digit (64-bit LDS atomics) and a suffix scan over the digits.  The first
+// round reads the keys in registers; the candidates that share the digits found so far are
+// then packed into `list` (room for every slot) and the later rounds read only that list.
+// Returns v and, in *above, W(key > v).
+template <int EPT, typename WF>
+__device__ __forceinline__ uint32_t sel_radix_threshold(const KeyView<EPT>& key, uint32_t cbits,
+                                                        unsigned long long target, WF weight,
+                                                        uint32_t kmin, uint32_t kmax, uint32_t* list,
+                                                        SelLds& sh, unsigned long long* above_out) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  *above_out = 0;
+  if (kmin == kmax) return kmin;
+  int pos = 32 - __clz((int)(kmin ^ kmax));
+  uint32_t prefix = pos >= 32 ? 0u : (kmin & ~((1u << pos) - 1u));
+  unsigned long long above = 0;
+  int n_list = -1;
+  while (pos > 0) {
+    const int nb = min(SEL_RADIX_BITS, pos), lo = pos - nb;
+    const uint32_t hi_mask = pos >= 32 ? 0u : ~((1u << pos) - 1u);
+    const uint32_t dmask = (1u << nb) - 1u;
+    __syncthreads();
+#pragma unroll
+    for (int b = 0; b < SEL_BPT; ++b) sh.hist[tid * SEL_BPT + b] = 0ull;
+    __syncthreads();
+    if (n_list < 0) {
+      const uint32_t cb = sel_opaque(cbits);
+#pragma unroll
+      for (int i = 0; i < EPT; ++i) {
+        const uint32_t k = sel_opaque(key[i]);
+        if (((cb >> i) & 1u) && (k & hi_mask) == prefix) atomicAdd(&sh.hist[(k >> lo) & dmask], weight(k));
+      }
+    } else {
+      for (int j = tid; j < n_list; j += SEL_NT) {
+        const uint32_t k = list[j];
+        if ((k & hi_mask) == prefix) atomicAdd(&sh.hist[(k >> lo) & dmask], weight(k));
+      }
+    }
+    __syncthreads();
+    // the digit where the weight from the top crosses the target
+    unsigned long long own = 0;
+#pragma unroll
+    for (int b = 0; b < SEL_BPT; ++b) own += sh.hist[tid * SEL_BPT + b];
+    unsigned long long x = own;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const unsigned long long y = __shfl_down(x, o, 64);
+      if (lane + o < 64) x += y;
+    }
+    if (lane == 0) sh.red64[wave] = x;
+    __syncthreads();
+    unsigned long long suf = x - own;
+    for (int w = wave + 1; w < SEL_NW; ++w) suf += sh.red64[w];
+    const unsigned long long lo_m = above + suf;
+    if (lo_m < target && lo_m + own >= target) {
+      unsigned long long cum = lo_m;
+      for (int b = SEL_BPT - 1; b >= 0; --b) {
+        const unsigned long long nxt = cum + sh.hist[tid * SEL_BPT + b];
+        if (nxt >= target) {
+          sh.pick_digit = (uint32_t)(tid * SEL_BPT + b);
+          sh.pick_above = cum;
+          break;
+        }
+        cum = nxt;
+      }
+    }
+    __syncthreads();
+    prefix |= sh.pick_digit << lo;
+    above = sh.pick_above;
+    pos = lo;
+    if (pos > 0 && n_list < 0) {
+      // stage the candidates that share the digits found so far (the list holds every slot)
+      const uint32_t m2 = ~((1u << pos) - 1u);
+      const uint32_t cb = sel_opaque(cbits);
+      uint32_t inb = 0;
+#pragma unroll
+      for (int i = 0; i < EPT; ++i)
+        if (((cb >> i) & 1u) && (sel_opaque(key[i]) & m2) == prefix) inb |= 1u << i;
+      const int2 sc = block_exscan_int(__popc(inb), sh.redi);
+      int off = sc.x;
+#pragma unroll
+      for (int i = 0; i < EPT; ++i)
+        if ((inb >> i) & 1u) list[off++] = key[i];
+      n_list = sc.y;
+    }
+  }
+  *above_out = above;
+  return prefix;
+}
 
 // `val` holds the thread's EPT values; they are clamped in place, and their bit patterns
 // (non-negative floats order as integers) are the ordering keys.
@@ -255,56 +359,30 @@ __device__ __forceinline__ void topp_core(float* val, uint32_t cbits, int p_q, i
   const unsigned long long pq = (unsigned long long)p_q;
   const unsigned long long target = pq * (tot / 1000000ull) + (pq * (tot % 1000000ull) + 999999ull) / 1000000ull;
 
-  // k from the mass rule
+  // the bits above the first one where the candidates' keys differ are common to all of
+  // them: the searches start below them
+  uint32_t kmin = 0xffffffffu, kmax = 0u;
+#pragma unroll
+  for (int i = 0; i < EPT; ++i)
+    if ((cbits >> i) & 1u) {
+      kmin = min(kmin, key[i]);
+      kmax = max(kmax, key[i]);
+    }
+  kmin = block_min_u32(kmin, sh.redi);
+  kmax = block_max_u32(kmax, sh.redi);
+
+  // k from the mass rule: v = value of the crossing element, elements above it all taken
   int k = 0;
   uint32_t v = 0;
   int take = 0;
   if (target > 0) {
-    // the bits above the first one where the candidates' keys differ are common to all of
-    // them, hence to v (a candidate's key): the search starts below them
-    uint32_t kmin = 0xffffffffu, kmax = 0u;
-#pragma unroll
-    for (int i = 0; i < EPT; ++i)
-      if ((cbits >> i) & 1u) {
-        kmin = min(kmin, key[i]);
-        kmax = max(kmax, key[i]);
-      }
-    kmin = block_min_u32(kmin, sh.redi);
-    kmax = block_max_u32(kmax, sh.redi);
-    const int top = (kmin == kmax) ? -1 : 31 - __clz(kmin ^ kmax);   // highest differing bit
-    v = (top < 0) ? kmin : (kmin & ~((2u << top) - 1u));
-    const int b_lo = max(top - SEL_COARSE + 1, 0);                      // last full-register bit
-    for (int b = top; b >= b_lo; --b) {
-      const uint32_t t = v | (1u << b);
-      if (block_sum_u64<SEL_NT>(mass_ge<EPT>(key, cbits, t), sh.red64) >= target) v = t;
-    }
-    const int LB = b_lo;                           // low bits left for the packed list
-    const uint32_t hi_end = v + (1u << LB);        // keys >= hi_end: above the prefix
-    const unsigned long long above = uniform_u64(block_sum_u64<SEL_NT>(mass_ge<EPT>(key, cbits, hi_end), sh.red64));
-    uint32_t inb = 0;
-#pragma unroll
-    for (int i = 0; i < EPT; ++i)
-      if (((cbits >> i) & 1u) && key[i] >= v && key[i] < hi_end) inb |= 1u << i;
-    const int2 scan = block_exscan_int(__popc(inb), sh.redi);
-    const int n_list = scan.y;
-    int off = scan.x;
-#pragma unroll
-    for (int i = 0; i < EPT; ++i)
-      if ((inb >> i) & 1u) list[off++] = key[i];
-    __syncthreads();
-    for (int b = LB - 1; b >= 0; --b) {
-      const uint32_t t = v | (1u << b);
-      double m = 0.0;
-      for (int j = tid; j < n_list; j += SEL_NT) {
-        const uint32_t kj = list[j];
-        if (kj >= t) m += (double)fixed_weight(kj);
-      }
-      if (above + block_sum_u64<SEL_NT>((unsigned long long)m, sh.red64) >= target) v = t;
-    }
-    // v = value of the crossing element; elements above it are all taken
-    const int cnt_gt = block_sum_int<SEL_NT>(count_ge<EPT>(key, cbits, v + 1), sh.redi);
-    const unsigned long long mass_gt = uniform_u64(block_sum_u64<SEL_NT>(mass_ge<EPT>(key, cbits, v + 1), sh.red64));
+    unsigned long long mass_gt = 0;
+    v = sel_radix_threshold<EPT>(key, cbits, target,
+                                 [](uint32_t kk) { return (unsigned long long)fixed_weight(kk); },
+                                 kmin, kmax, list, sh, &mass_gt);
     v = __builtin_amdgcn_readfirstlane(v);
+    mass_gt = uniform_u64(mass_gt);
+    const int cnt_gt = block_sum_int<SEL_NT>(count_ge<EPT>(key, cbits, v + 1), sh.redi);
     const unsigned long long wv = uniform_u64((unsigned long long)fixed_weight(v));
     take = wv ? (int)((target - mass_gt + wv - 1) / wv) : 0;   // wv > 0 whenever target > 0
     k = cnt_gt + take;
@@ -317,13 +395,12 @@ __device__ __forceinline__ void topp_core(float* val, uint32_t cbits, int p_q, i
       v = 0xffffffffu;
       take = 0;
     } else {
-      v = 0;
-      for (int b = 29; b >= 0; --b) {
-        const uint32_t t = v | (1u << b);
-        if (block_sum_int<SEL_NT>(count_ge<EPT>(key, cbits, t), sh.redi) >= kf) v = t;
-      }
-      const int cnt_gt = block_sum_int<SEL_NT>(count_ge<EPT>(key, cbits, v + 1), sh.redi);
-      take = kf - cnt_gt;
+      // the kf largest keys: the same search on counts
+      unsigned long long cnt_gt = 0;
+      v = sel_radix_threshold<EPT>(key, cbits, (unsigned long long)kf,
+                                   [](uint32_t) { return 1ull; }, kmin, kmax, list, sh, &cnt_gt);
+      v = __builtin_amdgcn_readfirstlane(v);
+      take = kf - (int)uniform_u64(cnt_gt);
     }
   }
   // selection: keys above v, plus the `take` most recent slots equal to v

@@ -19,7 +19,7 @@ Notation (paper):
   tiers    Dense / Sparse / Condensed Cascade Cache (Sec. 3.1)
   (o, SE)  attention state and merge operator (App. F)
 
-Readings where the paper is silent (all listed in the design doc):
+Readings where the paper is silent:
   * window aggregation: mean over the G*W window rows of each row's softmax
     probabilities, in log domain;
   * candidates: valid slots before the dense tier; dense tier force-kept;
@@ -188,7 +188,8 @@ def pool_max_head(x, cand, radius: int):
     SnapKV form (Sec. 4 baselines): each candidate's score becomes the maximum of the
     candidate scores within `radius` logical slots on either side (itself included);
     non-candidates stay -inf and are never a neighbour.  The width 2*radius + 1 is not
-    stated in the paper (reading in the design doc).  Max commutes with the monotone log, so
+    stated in the paper; the radius is an argument (3 by default in the pipeline).  Max
+    commutes with the monotone log, so
     pooling log scores equals pooling the probabilities they are the logs of.
     Pinned by: radius 0 is the identity; scipy's maximum_filter1d over the candidate-
     masked row; a constant row stays constant; the result dominates the input.

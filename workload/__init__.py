@@ -25,8 +25,9 @@ import torch
 
 PAGE = 16
 
-# The five benchmark workloads (sizes from the method's deployment regime; see
-# the design doc for the recipe).  W = 32 where the window is not fixed otherwise.
+# The five benchmark workloads (sizes from the method's deployment regime: long
+# reasoning decodes of 8k-32k tokens, GQA groups of 4-7, 16-token pages).  W = 32 where the
+# window is not fixed otherwise.
 CONFIGS = {
     1: dict(name="cfg1_l1_b1_h8x2_d64_n2048_f32", L=1, B=1, Hq=8, Hkv=2, D=64, N=2048,
             dtype="f32", W=16, p=0.9, L_dense=0, L_sparse=0, seed=0, recipe="normal"),

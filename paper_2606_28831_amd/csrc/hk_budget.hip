@@ -376,6 +376,48 @@ __device__ __forceinline__ void write_bitmap(uint64_t sel, uint32_t* __restrict_
 }
 
 // ------------------------------------------------------------------ Cautious Update votes
+// The head's page masks staged in LDS with every slot at or past cand_len cleared, for
+// all BG_NT * EPT slots a workgroup covers (pages past S_max hold no candidates).
+template <int EPT>
+__device__ __forceinline__ void stage_cand_masks(int h, int S_max, const int32_t* __restrict__ cand_len,
+                                                 const uint16_t* __restrict__ mask, BgLds& sh) {
+  const int cl = min(cand_len[h], S_max);
+  const int np = S_max / HK_PAGE;
+  const uint16_t* mrow = mask ? mask + (size_t)h * np : nullptr;
+  for (int q = threadIdx.x; q < EPT * BG_NT / HK_PAGE; q += BG_NT) {
+    const int keep = min(max(cl - q * HK_PAGE, 0), HK_PAGE);
+    uint32_t m = (q < np && mrow) ? (uint32_t)mrow[q] : 0xffffu;
+    sh.mrow[q] = (uint16_t)(m & ((1u << keep) - 1u));
+  }
+  __syncthreads();
+}
+
+// All ones when slot tid + BG_NT * i is a candidate, else zero (masks staged as above).
+__device__ __forceinline__ uint32_t cand_lanes(const BgLds& sh, int i) {
+  const int tid = threadIdx.x;
+  const uint32_t m = sh.mrow[(tid >> 4) + (BG_NT / HK_PAGE) * i];
+  return (uint32_t)((int32_t)(m << (31 - (tid & 15))) >> 31);
+}
+
+// Lane LANE of x takes the wave-uniform value s; the other lanes keep theirs.
+template <int LANE>
+__device__ __forceinline__ void write_lane(uint32_t& x, uint32_t s) {
+  x = ((threadIdx.x & 63) == LANE) ? s : x;
+}
+
+template <int I>
+struct IntC {
+  static constexpr int value = I;
+};
+// f(IntC<I>) for I = B .. E-1, unrolled at compile time
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(IntC<B>{});
+    static_for<B + 1, E>(f);
+  }
+}
+
 // Four waves per SIMD (two workgroups per CU) cap the registers at 128: the allocator
 // then keeps fewer loads in flight rather than lowering the occupancy.
 template <int EPT>
@@ -384,50 +426,60 @@ __global__ __launch_bounds__(BG_NT) __attribute__((amdgpu_waves_per_eu(4, 8))) v
     const uint16_t* __restrict__ mask, const float* __restrict__ a_rows, int p_q,
     uint32_t* __restrict__ row_sel, int32_t* __restrict__ row_k, int32_t* __restrict__ status) {
   __shared__ BgLds sh;
-  constexpr uint32_t NONE = 0xffffffffu;  // key of a non-candidate (candidates are <= 1.0f)
+  constexpr uint32_t NONE = 0xffffffffu;  // key of a non-candidate
+  constexpr uint32_t ONE = 0x3f800000u;   // bits of 1.0f: in-range probabilities are <= ONE
   const int h = blockIdx.y, tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
   // one row per workgroup: a loop over rows would let the compiler keep per-element
   // addresses, masks and constants in registers across rows
   const int r = blockIdx.x;
-  const uint64_t cf = cand_flags<EPT>(h, S_max, cand_len, mask, sh);
-  const float* arow = a_rows + ((size_t)h * R + r) * S_max;
+  stage_cand_masks<EPT>(h, S_max, cand_len, mask, sh);
+  // buffer loads: slots past the row's end read as 0 (they are no candidates), so no
+  // clamped addresses are needed
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(a_rows + ((size_t)h * R + r) * S_max), (short)0, S_max * 4, 0x00020000);
   uint32_t key[EPT];
-  int flags = 0;
-  uint32_t kmin = NONE, kmax = 0u;
-  // every load first (index clamped into the row), then the per-element work
 #pragma unroll
-  for (int i = 0; i < EPT; ++i) key[i] = __float_as_uint(arow[min(tid + BG_NT * i, S_max - 1)]);
+  for (int i = 0; i < EPT; ++i)
+    key[i] = __builtin_amdgcn_raw_buffer_load_b32(rs, (tid + BG_NT * i) * 4, 0, 0);
+  // a candidate keeps its bits, anything else takes the all-ones key; for non-negative
+  // floats the bit order is the value order
+  uint32_t kmin = NONE, kmax = 0u;
 #pragma unroll
   for (int i = 0; i < EPT; ++i) {
-    float v = __uint_as_float(key[i]);
-    key[i] = NONE;
-    if ((cf >> i) & 1ull) {
-      if (v != v) { v = 0.f; flags |= HK_FLAG_NAN; }
-      if (v > 1.f) { v = 1.f; flags |= HK_FLAG_RANGE; }
-      if (v < 0.f) { v = 0.f; flags |= HK_FLAG_RANGE; }
-      if (v == 0.f) v = 0.f;                    // canonical +0
-      key[i] = __float_as_uint(v);
-      kmin = min(kmin, key[i]);
-      kmax = max(kmax, key[i]);
-    }
+    const uint32_t m = cand_lanes(sh, i);
+    const uint32_t b = key[i] & m;
+    key[i] = b | ~m;
+    kmin = min(kmin, key[i]);
+    kmax = max(kmax, b);
   }
-  // key range of the row (its total mass comes from the first histogram round)
-  kmin = wave_reduce_u32(kmin, NONE, [](uint32_t a, uint32_t b) { return a < b ? a : b; });
-  kmax = wave_reduce_u32(kmax, 0u, [](uint32_t a, uint32_t b) { return a > b ? a : b; });
-  {
-    const int w = tid >> 6;
-    if ((tid & 63) == 0) {
-      sh.redu[0][w] = kmin;
-      sh.redu[1][w] = kmax;
-    }
-    __syncthreads();
-    kmin = sh.redu[0][0];
-    kmax = sh.redu[1][0];
+  block_key_range<uint32_t>(kmin, kmax, sh, &kmin, &kmax);
+  if (kmax > ONE) {
+    // some candidate is NaN, negative (-0 included) or above 1: clean every candidate
+    // (NaN -> 0, clamp to [0, 1], +0) and report what was found
+    int flags = 0;
+    kmin = NONE;
+    kmax = 0u;
 #pragma unroll
-    for (int i = 1; i < BG_NW; ++i) {
-      kmin = min(kmin, sh.redu[0][i]);
-      kmax = max(kmax, sh.redu[1][i]);
+    for (int i = 0; i < EPT; ++i) {
+      uint32_t k = NONE;
+      if (cand_lanes(sh, i)) {
+        float v = __uint_as_float(key[i]);    // a candidate's key holds its bits
+        if (v != v) { v = 0.f; flags |= HK_FLAG_NAN; }
+        if (v > 1.f) { v = 1.f; flags |= HK_FLAG_RANGE; }
+        if (v < 0.f) { v = 0.f; flags |= HK_FLAG_RANGE; }
+        if (v == 0.f) v = 0.f;                  // canonical +0
+        k = __float_as_uint(v);
+        kmin = min(kmin, k);
+        kmax = max(kmax, k);
+      }
+      key[i] = k;
     }
+    block_key_range<uint32_t>(kmin, kmax, sh, &kmin, &kmax);
+    const int any_nan = __syncthreads_or(flags & HK_FLAG_NAN);
+    const int any_range = __syncthreads_or(flags & HK_FLAG_RANGE);
+    if (status && tid == 0 && (any_nan || any_range))
+      atomicOr(status, (any_nan ? HK_FLAG_NAN : 0) | (any_range ? HK_FLAG_RANGE : 0));
   }
   const unsigned long long pq = (unsigned long long)p_q;
   // target = ceil(p_q * Total / 10^6) without overflow
@@ -449,31 +501,75 @@ __global__ __launch_bounds__(BG_NT) __attribute__((amdgpu_waves_per_eu(4, 8))) v
       take = 1;
     }
   }
-  uint64_t sel = 0, tie = 0;
+  v = (uint32_t)__builtin_amdgcn_readfirstlane((int)v);     // uniform: from LDS
+  take = __builtin_amdgcn_readfirstlane(take);
+  // The row's bitmap straight from ballots: lane i of a wave keeps the wave's ballot of
+  // its element i (64 consecutive slots from BG_NT * i + 64 * wave, two bitmap words) for
+  // the keys at or above the threshold; the wave's counts stay scalar.
+  uint32_t ge_lo = 0, ge_hi = 0;
+  int n_ge = 0, n_eq = 0;
   if (v != NONE) {
-#pragma unroll
-    for (int i = 0; i < EPT; ++i) {
+    static_for<0, EPT>([&](auto ic) {
+      constexpr int i = decltype(ic)::value;
       const uint32_t kk = opaque(key[i]);
-      if (kk != NONE && kk > v) sel |= 1ull << i;
-      if (kk == v) tie |= 1ull << i;
-    }
+      const uint64_t bge = __ballot(kk - v < NONE - v);   // v <= kk < NONE
+      const uint64_t beq = __ballot(kk == v);
+      n_ge += __popcll(bge);
+      n_eq += __popcll(beq);
+      write_lane<i>(ge_lo, (uint32_t)bge);
+      write_lane<i>(ge_hi, (uint32_t)(bge >> 32));
+    });
   }
-  // counts above the threshold and at it, in one reduction (each at most 32768)
-  const uint32_t both = block_sum_u32((uint32_t)__popcll(sel) | ((uint32_t)__popcll(tie) << 16),
-                                      sh.redu[0]);
-  const int n_tie = (int)(both >> 16);
-  const int k = (int)(both & 0xffffu) + min(take, n_tie);
-  if (take >= n_tie) sel |= tie;
-  else if (take > 0) sel |= take_top_ties_bg<EPT>(tie, take, sh.tiecnt);
-  write_bitmap<EPT>(sel, row_sel + ((size_t)h * R + r) * (S_max / 32), S_max);
+  __syncthreads();
+  if (lane == 0) {
+    sh.redi[wave] = n_ge;
+    sh.tiecnt[wave] = n_eq;
+  }
+  __syncthreads();
+  int n_tie = 0, n_above = 0;
+#pragma unroll
+  for (int w = 0; w < BG_NW; ++w) {
+    n_above += sh.redi[w];
+    n_tie += sh.tiecnt[w];
+  }
+  n_above -= n_tie;
+  const int k = n_above + min(take, n_tie);
+  if (take < n_tie) {
+    // only `take` (possibly 0) of the keys equal to v are kept: those at the largest slots.  The ballots
+    // are taken again: lane i of each wave keeps those of its element i, counts them in
+    // LDS, and a suffix sum in slot order (element, then wave) says how many lie above.
+    uint32_t eq_lo = 0, eq_hi = 0;
+    static_for<0, EPT>([&](auto ic) {
+      constexpr int i = decltype(ic)::value;
+      const uint64_t beq = __ballot(opaque(key[i]) == v);
+      write_lane<i>(eq_lo, (uint32_t)beq);
+      write_lane<i>(eq_hi, (uint32_t)(beq >> 32));
+    });
+    __syncthreads();
+    sh.tiecnt[lane * BG_NW + wave] = __popc(eq_lo) + __popc(eq_hi);
+    __syncthreads();
+    const int e = BG_NT - 1 - tid;     // entries in descending slot order
+    const int2 sc = block_exscan_bg(sh.tiecnt[e], sh.redi);
+    int* above = reinterpret_cast<int*>(sh.list);
+    above[e] = sc.x;
+    __syncthreads();
+    uint64_t eq = ((uint64_t)eq_hi << 32) | eq_lo;
+    const int cnt = __popcll(eq);
+    const int need = max(0, min(take - above[lane * BG_NW + wave], cnt));
+    for (int d = cnt - need; d > 0; --d) eq &= eq - 1;   // drop the lowest slots
+    const uint64_t ge = ((uint64_t)ge_hi << 32) | ge_lo;
+    const uint64_t eqall = ((uint64_t)eq_hi << 32) | eq_lo;
+    const uint64_t sel = (ge & ~eqall) | eq;
+    ge_lo = (uint32_t)sel;
+    ge_hi = (uint32_t)(sel >> 32);
+  }
+  uint32_t* brow = row_sel + ((size_t)h * R + r) * (S_max / 32);
+  const int j0 = BG_NT * lane + 64 * wave;
+  if (lane < EPT && j0 < S_max) {
+    brow[j0 / 32] = ge_lo;
+    if (j0 + 32 < S_max) brow[j0 / 32 + 1] = ge_hi;
+  }
   if (row_k && tid == 0) row_k[(size_t)h * R + r] = k;
-  const int flags_all = flags;
-  if (status) {
-    const int any_nan = __syncthreads_or(flags_all & HK_FLAG_NAN);
-    const int any_range = __syncthreads_or(flags_all & HK_FLAG_RANGE);
-    if (tid == 0 && (any_nan || any_range))
-      atomicOr(status, (any_nan ? HK_FLAG_NAN : 0) | (any_range ? HK_FLAG_RANGE : 0));
-  }
 }
 
 // votes[h][j] = sum over the R rows of bit j of row_sel[h][r]; one thread per 32-slot word

@@ -97,6 +97,9 @@ def _rows(kind, H, R, S, cand_len, rng):
                 a[h, r, :n] = np.exp2(-rng.random(n) * 30.0) / n
             elif kind == "ties":
                 a[h, r, :n] = rng.choice(np.float32([0.5, 0.25, 0.125]), n) / n
+            elif kind == "negzero":
+                a[h, r, :n] = rng.random(n) / n
+                a[h, r, :n:7] = np.float32(-0.0)          # -0 is a zero, not out of range
             elif kind == "crowded":
                 a[h, r, :n] = (1.0 + rng.integers(0, 1 << 12, n) * 2.0 ** -12) / (2 * n)
             elif kind == "mixed":
@@ -118,7 +121,8 @@ def _rows(kind, H, R, S, cand_len, rng):
                                         ("ties", 16, 2048, 0.5), ("crowded", 5, 4096, 0.95),
                                         ("mixed", 12, 512, 0.9), ("dirichlet", 1, 64, 1.0),
                                         ("dirichlet", 3, 32768, 0.9), ("crowded", 2, 16384, 0.9),
-                                        ("dirichlet", 128, 256, 0.0)])
+                                        ("dirichlet", 128, 256, 0.0), ("negzero", 6, 1056, 0.9),
+                                        ("ties", 4, 1536, 0.5)])
 def test_vote_topp(kind, R, S, p):
     import paper_2606_28831_amd as hk
     rng = np.random.default_rng(zlib.crc32(f"{kind}/{R}/{S}".encode()))

@@ -23,12 +23,11 @@ constexpr int RADIX_BITS = 11;
 constexpr int RADIX_BINS = 1 << RADIX_BITS;
 constexpr int BINS_PER_THREAD = RADIX_BINS / BG_NT;
 constexpr int BG_EPT_MAX = 64;
-constexpr float kMassScale = 1099511627776.0f;   // 2^40, fixed-point unit of the Top-p mass
 
 constexpr int BG_LIST_BYTES = 32768;   // keys of the boundary digit, staged for later rounds
 
 struct BgLds {
-  unsigned long long hist[RADIX_BINS];
+  unsigned long long hist[RADIX_BINS + 1];   // the last bin takes the non-members of round 1
   uint32_t list[BG_LIST_BYTES / 4];
   uint16_t mrow[BG_EPT_MAX * BG_NT / HK_PAGE];   // the head's page masks
   unsigned long long red64[BG_NW];
@@ -39,10 +38,14 @@ struct BgLds {
   uint32_t pick_digit;
 };
 
-// floor(v * 2^40) for a probability v in [0, 1]: the product is exact in fp32 (a power of
-// two scale) with at most 24 significant bits, so truncation gives the integer exactly.
+// floor(v * 2^40) for a probability v in [0, 1], as its two 32-bit halves: with t = v * 2^8
+// (exact, t <= 256) the high half is floor(t) and the low half floor(fract(t) * 2^32); the
+// fraction and its scaling are exact in fp32, so each truncation gives its integer exactly.
 __device__ __forceinline__ unsigned long long mass_weight(uint32_t key) {
-  return (unsigned long long)truncf(__uint_as_float(key) * kMassScale);
+  const float t = __uint_as_float(key) * 256.0f;
+  const uint32_t hi = (uint32_t)t;
+  const uint32_t lo = (uint32_t)(__builtin_amdgcn_fractf(t) * 4294967296.0f);
+  return ((unsigned long long)hi << 32) | lo;
 }
 
 // A copy of x the compiler cannot see through.  Per-element predicates such as
@@ -215,12 +218,45 @@ __device__ __forceinline__ void pick_digit(BgLds& sh, bool first, TF target_of,
   *above_out = sh.pick_above;
 }
 
+// Zero the histogram (and the bin of round 1's non-members) between two barriers.
+__device__ __forceinline__ void clear_hist(BgLds& sh) {
+  const int tid = threadIdx.x;
+  __syncthreads();                   // earlier readers of the LDS scratch are done
+#pragma unroll
+  for (int b = 0; b < BINS_PER_THREAD; ++b) sh.hist[tid * BINS_PER_THREAD + b] = 0ull;
+  if (tid == 0) sh.hist[RADIX_BINS] = 0ull;
+  __syncthreads();
+}
+
+// Stage into the LDS list the keys whose bits from `pos` up equal `prefix`, if they fit;
+// returns their number, or -1 when they do not fit (later rounds then read the registers).
+// Each thread counts its own, an exclusive scan gives its offset, and it writes them there.
+template <int EPT, typename K>
+__device__ __forceinline__ int stage_list(const K* key, int pos, K prefix, BgLds& sh) {
+  constexpr int CAP = BG_LIST_BYTES / (int)sizeof(K);
+  K* list = reinterpret_cast<K*>(sh.list);
+  const K m2 = ~low_mask<K>(pos);
+  int cnt = 0;
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) cnt += ((opaque(key[i]) & m2) == prefix) ? 1 : 0;
+  const int2 sc = block_exscan_bg(cnt, sh.redi);
+  if (sc.y > CAP) return -1;
+  int off = sc.x;
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) {
+    const K k = opaque(key[i]);
+    if ((k & m2) == prefix) list[off++] = k;
+  }
+  return sc.y;
+}
+
 // Largest key v of the member elements with W(key >= v) >= target, where W sums the
 // elements' weights (weight(key) of each) and target = target_of(W(all members)), which
 // must not exceed W(all members); the target comes back in *target_out, and for a target
 // of 0 nothing else is computed (v is then meaningless).  Member
 // keys have their top bit clear; every other element holds the all-ones key, which the
-// prefix tests below exclude, so no per-element flags are needed.  The
+// first round sends to a bin of its own and later prefix tests exclude, so no
+// per-element flags are needed.  The
 // bits above the highest one where the flagged keys differ are common to all of them,
 // hence to v; below them v is found RADIX_BITS at a time from a histogram of weights per
 // digit (LDS atomics) and a suffix scan over the digits.  The first round reads the keys
@@ -245,19 +281,40 @@ __device__ __forceinline__ K radix_threshold(const K* key, TF target_of, WF weig
     return kmin;
   }
   unsigned long long target = 0;
-  bool first = true;
   int pos = highest_bit<K>(kmin ^ kmax) + 1;
   K prefix = kmin & ~low_mask<K>(pos);
   unsigned long long above = 0;
   int n_list = -1;                   // < 0: keys still read from registers
+  {
+    // First round, outside the loop (inside it the compiler would keep the EPT weights,
+    // which no later round changes, in registers of their own).  No membership test: a
+    // member's key minus the prefix is below 2^pos, so its digit is in range; the all-ones
+    // key of a non-member lands past the last digit, in a bin nothing reads.
+    const int nb = min(RADIX_BITS, pos), lo = pos - nb;
+    clear_hist(sh);
+#pragma unroll
+    for (int i = 0; i < EPT; ++i) {
+      const K k = key[i];
+      const K q = (k - prefix) >> lo;
+      atomicAdd(&sh.hist[q < (K)RADIX_BINS ? (uint32_t)q : (uint32_t)RADIX_BINS], weight(k));
+    }
+    __syncthreads();
+    uint32_t d;
+    pick_digit(sh, true, target_of, &target, above, &d, &above);
+    if (target == 0) {
+      *target_out = 0;
+      *above_out = 0;
+      return prefix;
+    }
+    prefix |= (K)d << lo;
+    pos = lo;
+    if (pos > 0) n_list = stage_list<EPT>(key, pos, prefix, sh);
+  }
   while (pos > 0) {
     const int nb = min(RADIX_BITS, pos), lo = pos - nb;
     const K hi_mask = ~low_mask<K>(pos);
     const uint32_t dmask = (1u << nb) - 1u;
-    __syncthreads();                 // earlier readers of the LDS scratch are done
-#pragma unroll
-    for (int b = 0; b < BINS_PER_THREAD; ++b) sh.hist[tid * BINS_PER_THREAD + b] = 0ull;
-    __syncthreads();
+    clear_hist(sh);
     if (n_list < 0) {
 #pragma unroll
       for (int i = 0; i < EPT; ++i) {
@@ -275,28 +332,10 @@ __device__ __forceinline__ K radix_threshold(const K* key, TF target_of, WF weig
     }
     __syncthreads();
     uint32_t d;
-    pick_digit(sh, first, target_of, &target, above, &d, &above);
-    first = false;
-    if (target == 0) break;
+    pick_digit(sh, false, target_of, &target, above, &d, &above);
     prefix |= (K)d << lo;
     pos = lo;
-    if (pos > 0 && n_list < 0) {
-      // stage the keys that share the digits found so far, if they fit
-      const K m2 = ~low_mask<K>(pos);
-      int cnt = 0;
-#pragma unroll
-      for (int i = 0; i < EPT; ++i) cnt += ((opaque(key[i]) & m2) == prefix) ? 1 : 0;
-      const int2 sc = block_exscan_bg(cnt, sh.redi);
-      if (sc.y <= CAP) {
-        int off = sc.x;
-#pragma unroll
-        for (int i = 0; i < EPT; ++i) {
-          const K k = opaque(key[i]);
-          if ((k & m2) == prefix) list[off++] = k;
-        }
-        n_list = sc.y;
-      }
-    }
+    if (pos > 0 && n_list < 0) n_list = stage_list<EPT>(key, pos, prefix, sh);
   }
   *target_out = target;
   *above_out = above;

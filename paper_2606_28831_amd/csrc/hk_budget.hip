@@ -27,7 +27,7 @@ constexpr int BG_EPT_MAX = 64;
 constexpr int BG_LIST_BYTES = 32768;   // keys of the boundary digit, staged for later rounds
 
 struct BgLds {
-  unsigned long long hist[RADIX_BINS + 1];   // the last bin takes the non-members of round 1
+  unsigned long long hist[RADIX_BINS];
   uint32_t list[BG_LIST_BYTES / 4];
   uint16_t mrow[BG_EPT_MAX * BG_NT / HK_PAGE];   // the head's page masks
   unsigned long long red64[BG_NW];
@@ -218,13 +218,12 @@ __device__ __forceinline__ void pick_digit(BgLds& sh, bool first, TF target_of,
   *above_out = sh.pick_above;
 }
 
-// Zero the histogram (and the bin of round 1's non-members) between two barriers.
+// Zero the histogram between two barriers.
 __device__ __forceinline__ void clear_hist(BgLds& sh) {
   const int tid = threadIdx.x;
   __syncthreads();                   // earlier readers of the LDS scratch are done
 #pragma unroll
   for (int b = 0; b < BINS_PER_THREAD; ++b) sh.hist[tid * BINS_PER_THREAD + b] = 0ull;
-  if (tid == 0) sh.hist[RADIX_BINS] = 0ull;
   __syncthreads();
 }
 
@@ -255,8 +254,7 @@ __device__ __forceinline__ int stage_list(const K* key, int pos, K prefix, BgLds
 // must not exceed W(all members); the target comes back in *target_out, and for a target
 // of 0 nothing else is computed (v is then meaningless).  Member
 // keys have their top bit clear; every other element holds the all-ones key, which the
-// first round sends to a bin of its own and later prefix tests exclude, so no
-// per-element flags are needed.  The
+// tests below exclude, so no per-element flags are needed.  The
 // bits above the highest one where the flagged keys differ are common to all of them,
 // hence to v; below them v is found RADIX_BITS at a time from a histogram of weights per
 // digit (LDS atomics) and a suffix scan over the digits.  The first round reads the keys
@@ -287,16 +285,16 @@ __device__ __forceinline__ K radix_threshold(const K* key, TF target_of, WF weig
   int n_list = -1;                   // < 0: keys still read from registers
   {
     // First round, outside the loop (inside it the compiler would keep the EPT weights,
-    // which no later round changes, in registers of their own).  No membership test: a
-    // member's key minus the prefix is below 2^pos, so its digit is in range; the all-ones
-    // key of a non-member lands past the last digit, in a bin nothing reads.
+    // which no later round changes, in registers of their own).  Every member shares the
+    // prefix, so the only test is against the all-ones key of non-members, and a
+    // member's digit is its key minus the prefix, shifted.  (Sending non-members to a
+    // spare bin instead would serialise their atomics on one address.)
     const int nb = min(RADIX_BITS, pos), lo = pos - nb;
     clear_hist(sh);
 #pragma unroll
     for (int i = 0; i < EPT; ++i) {
       const K k = key[i];
-      const K q = (k - prefix) >> lo;
-      atomicAdd(&sh.hist[q < (K)RADIX_BINS ? (uint32_t)q : (uint32_t)RADIX_BINS], weight(k));
+      if (k != ~K(0)) atomicAdd(&sh.hist[(uint32_t)((k - prefix) >> lo)], weight(k));
     }
     __syncthreads();
     uint32_t d;

@@ -15,13 +15,16 @@ constexpr unsigned long long kMassOne = 1ull << 40;   // fixed-point unit of the
 // ------------------------------------------------------------------ a2: calibrate
 // c = sum_m w_m Softmax(x_m / T_m) over the candidates (Solution 2, Sec. 3.2), for the
 // thread's EPT slots; the fused select kernel runs the same code, so both paths produce
-// identical values.
+// identical values.  Each metric's row is first staged in LDS (`xs`, EPT * SEL_NT floats) by
+// unconditional coalesced loads: the three sweeps (max, sum, values) then read LDS, where
+// reads inside the per-candidate branches cost little, instead of global memory, where
+// each one would be waited on in turn.
 template <int EPT>
 __device__ __forceinline__ void calib_values(int h, int S_max, uint32_t cbits, int n_metrics,
                                              const float* __restrict__ x0, const float* __restrict__ x1,
                                              const float* __restrict__ T0, const float* __restrict__ T1,
                                              float w0, float w1, float* __restrict__ lse_out, float* red,
-                                             float* c) {
+                                             float* xs, float* c) {
   const int tid = threadIdx.x;
 #pragma unroll
   for (int i = 0; i < EPT; ++i) c[i] = 0.f;
@@ -30,24 +33,36 @@ __device__ __forceinline__ void calib_values(int h, int S_max, uint32_t cbits, i
     const float* Tp = (m == 0 ? T0 : T1);
     const float T = Tp ? Tp[h] : 1.0f;
     const float wm = (m == 0 ? w0 : w1);
-    // x / T is recomputed from memory (cache-resident) in each of the three sweeps
-    // rather than kept: EPT more registers would spill next to c
+    {
+      // xs holds EPT * SEL_NT floats, so the stores need no bound; the loads clamp theirs.
+      // (The opaque index keeps the compiler from computing the EPT addresses once for
+      // all metrics and holding them.)
+      int j0 = tid;
+      asm volatile("" : "+v"(j0));
+      float t[EPT];
+#pragma unroll
+      for (int i = 0; i < EPT; ++i) t[i] = x[min(j0 + SEL_NT * i, S_max - 1)];
+      __syncthreads();                   // the previous metric's readers are done
+#pragma unroll
+      for (int i = 0; i < EPT; ++i) xs[j0 + SEL_NT * i] = t[i];
+      __syncthreads();
+    }
     float mx = -INFINITY;
 #pragma unroll
     for (int i = 0; i < EPT; ++i)
-      if ((cbits >> i) & 1u) mx = fmaxf(mx, x[tid + SEL_NT * i] / T);
+      if ((cbits >> i) & 1u) mx = fmaxf(mx, xs[tid + SEL_NT * i] / T);
     mx = block_max<SEL_NT>(mx, red);
     float lse = -INFINITY;
     if (mx != -INFINITY) {
       float sm = 0.f;
 #pragma unroll
       for (int i = 0; i < EPT; ++i)
-        if ((cbits >> i) & 1u) sm += expf(x[tid + SEL_NT * i] / T - mx);
+        if ((cbits >> i) & 1u) sm += expf(xs[tid + SEL_NT * i] / T - mx);
       sm = block_sum<SEL_NT>(sm, red);
       lse = mx + logf(sm);
 #pragma unroll
       for (int i = 0; i < EPT; ++i)
-        if ((cbits >> i) & 1u) c[i] = fmaf(wm, expf(x[tid + SEL_NT * i] / T - lse), c[i]);
+        if ((cbits >> i) & 1u) c[i] = fmaf(wm, expf(xs[tid + SEL_NT * i] / T - lse), c[i]);
     }
     if (lse_out && tid == 0) lse_out[(size_t)h * n_metrics + m] = lse;
   }
@@ -82,11 +97,12 @@ __global__ __launch_bounds__(SEL_NT) void calibrate_kernel(
     const float* __restrict__ x0, const float* __restrict__ x1, const float* __restrict__ T0,
     const float* __restrict__ T1, float w0, float w1, float* __restrict__ c_out,
     float* __restrict__ lse_out) {
+  extern __shared__ float xs_dyn[];     // EPT * SEL_NT floats: a metric's row
   __shared__ float red[SEL_NW];
   const int h = blockIdx.x, tid = threadIdx.x;
   const uint32_t cbits = cand_bits<EPT>(h, S_max, cand_len, mask);
   float c[EPT];
-  calib_values<EPT>(h, S_max, cbits, n_metrics, x0, x1, T0, T1, w0, w1, lse_out, red, c);
+  calib_values<EPT>(h, S_max, cbits, n_metrics, x0, x1, T0, T1, w0, w1, lse_out, red, xs_dyn, c);
 #pragma unroll
   for (int i = 0; i < EPT; ++i) {
     const int j = tid + SEL_NT * i;
@@ -473,7 +489,9 @@ __global__ __launch_bounds__(SEL_NT) void calib_topp_kernel(
   const int h = blockIdx.x, tid = threadIdx.x;
   const uint32_t cbits = cand_bits<EPT>(h, S_max, cand_len, mask);
   float c[EPT];
-  calib_values<EPT>(h, S_max, cbits, n_metrics, x0, x1, T0, T1, w0, w1, lse_out, red, c);
+  // the key list of the Top-p search is not live yet: it holds the metric rows meanwhile
+  calib_values<EPT>(h, S_max, cbits, n_metrics, x0, x1, T0, T1, w0, w1, lse_out, red,
+                    reinterpret_cast<float*>(list), c);
   if (c_out) {
 #pragma unroll
     for (int i = 0; i < EPT; ++i) {
@@ -733,9 +751,12 @@ hipError_t hk_launch_calibrate(int n_heads, int S_max, const int32_t* cand_len, 
                                const float* T1, float w0, float w1, float* c_out, float* lse_out,
                                hipStream_t st) {
   TimedLaunch t(HK_TK_CALIBRATE, st);
-  HK_EPT_SWITCH(S_max, hipLaunchKernelGGL((calibrate_kernel<E>), dim3(n_heads), dim3(SEL_NT), 0, st,
-                                          S_max, cand_len, mask, n_metrics, x0, x1, T0, T1, w0, w1,
-                                          c_out, lse_out));
+  HK_EPT_SWITCH(S_max, {
+    const size_t lds = (size_t)E * SEL_NT * sizeof(float);   // dynamic LDS: a metric's row
+    allow_dynamic_lds<calibrate_kernel<E>>(lds);
+    hipLaunchKernelGGL((calibrate_kernel<E>), dim3(n_heads), dim3(SEL_NT), lds, st, S_max, cand_len,
+                       mask, n_metrics, x0, x1, T0, T1, w0, w1, c_out, lse_out);
+  });
   return hipGetLastError();
 }
 
@@ -758,9 +779,10 @@ hipError_t hk_launch_calib_topp(int n_heads, int S_max, const int32_t* cand_len,
                                 const float* T1, float w0, float w1, int p_q, int k_min, int k_max,
                                 float* c_out, float* lse_out, uint32_t* sel_bits, int32_t* k_out,
                                 float* sel_mass, int32_t* status, hipStream_t st) {
-  const size_t lds = (size_t)S_max * sizeof(uint32_t);
   TimedLaunch t(HK_TK_CALIB_TOPP, st);
   HK_EPT_SWITCH(S_max, {
+    // the key list, and before it a metric's row (EPT * SEL_NT floats >= S_max)
+    const size_t lds = (size_t)E * SEL_NT * sizeof(uint32_t);
     allow_dynamic_lds<calib_topp_kernel<E>>(lds);
     hipLaunchKernelGGL((calib_topp_kernel<E>), dim3(n_heads), dim3(SEL_NT), lds, st, S_max, cand_len,
                        mask, n_metrics, x0, x1, T0, T1, w0, w1, p_q, k_min, k_max, c_out, lse_out,

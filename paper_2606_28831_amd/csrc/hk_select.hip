@@ -15,10 +15,10 @@ constexpr unsigned long long kMassOne = 1ull << 40;   // fixed-point unit of the
 // ------------------------------------------------------------------ a2: calibrate
 // c = sum_m w_m Softmax(x_m / T_m) over the candidates (Solution 2, Sec. 3.2), for the
 // thread's EPT slots; the fused select kernel runs the same code, so both paths produce
-// identical values.  Each metric's row is first staged in LDS (`xs`, EPT * SEL_NT floats) by
-// unconditional coalesced loads: the three sweeps (max, sum, values) then read LDS, where
-// reads inside the per-candidate branches cost little, instead of global memory, where
-// each one would be waited on in turn.
+// identical values.  Each metric's row, divided by its temperature, is first staged in LDS
+// (`xs`, EPT * SEL_NT floats) by unconditional coalesced loads: the three sweeps (max,
+// sum, values) then read LDS, where reads inside the per-candidate branches cost little,
+// instead of global memory, where each one would be waited on in turn.
 template <int EPT>
 __device__ __forceinline__ void calib_values(int h, int S_max, uint32_t cbits, int n_metrics,
                                              const float* __restrict__ x0, const float* __restrict__ x1,
@@ -44,25 +44,25 @@ __device__ __forceinline__ void calib_values(int h, int S_max, uint32_t cbits, i
       for (int i = 0; i < EPT; ++i) t[i] = x[min(j0 + SEL_NT * i, S_max - 1)];
       __syncthreads();                   // the previous metric's readers are done
 #pragma unroll
-      for (int i = 0; i < EPT; ++i) xs[j0 + SEL_NT * i] = t[i];
+      for (int i = 0; i < EPT; ++i) xs[j0 + SEL_NT * i] = t[i] / T;   // x / T, once
       __syncthreads();
     }
     float mx = -INFINITY;
 #pragma unroll
     for (int i = 0; i < EPT; ++i)
-      if ((cbits >> i) & 1u) mx = fmaxf(mx, xs[tid + SEL_NT * i] / T);
+      if ((cbits >> i) & 1u) mx = fmaxf(mx, xs[tid + SEL_NT * i]);
     mx = block_max<SEL_NT>(mx, red);
     float lse = -INFINITY;
     if (mx != -INFINITY) {
       float sm = 0.f;
 #pragma unroll
       for (int i = 0; i < EPT; ++i)
-        if ((cbits >> i) & 1u) sm += expf(xs[tid + SEL_NT * i] / T - mx);
+        if ((cbits >> i) & 1u) sm += expf(xs[tid + SEL_NT * i] - mx);
       sm = block_sum<SEL_NT>(sm, red);
       lse = mx + logf(sm);
 #pragma unroll
       for (int i = 0; i < EPT; ++i)
-        if ((cbits >> i) & 1u) c[i] = fmaf(wm, expf(xs[tid + SEL_NT * i] / T - lse), c[i]);
+        if ((cbits >> i) & 1u) c[i] = fmaf(wm, expf(xs[tid + SEL_NT * i] - lse), c[i]);
     }
     if (lse_out && tid == 0) lse_out[(size_t)h * n_metrics + m] = lse;
   }
@@ -118,21 +118,7 @@ __device__ __forceinline__ float fixed_weight(uint32_t key) {
   return truncf(__uint_as_float(key) * (float)kMassOne);
 }
 
-// Mass and count of the candidates with key >= t (one thread's share; the threshold
-// searches themselves are radix searches, sel_radix_threshold below).  (The empty asm
-// keeps the compiler from hoisting the EPT weights into registers of their own, which
-// would spill.)
-template <int EPT, typename K>
-__device__ __forceinline__ unsigned long long mass_ge(const K& key, uint32_t cbits, uint32_t t) {
-  double m = 0.0;
-#pragma unroll
-  for (int i = 0; i < EPT; ++i) {
-    uint32_t k = key[i];
-    asm volatile("" : "+v"(k));
-    if (((cbits >> i) & 1u) && k >= t) m += (double)fixed_weight(k);
-  }
-  return (unsigned long long)m;
-}
+// Count of the thread's candidates with key >= t.
 template <int EPT, typename K>
 __device__ __forceinline__ int count_ge(const K& key, uint32_t cbits, uint32_t t) {
   int n = 0;
@@ -249,94 +235,164 @@ __device__ __forceinline__ X sel_opaque(X x) {
   return x;
 }
 
-// Largest key v of the candidates with W(key >= v) >= target (0 < target <= W(all)), W the
-// sum of weight(key).  The bits above the highest one where kmin and kmax differ are shared
-// by every candidate, hence by v; below them v is found 11 bits at a time from a histogram
-// of weights per digit (64-bit LDS atomics) and a suffix scan over the digits.  The first
-// round reads the keys in registers; the candidates that share the digits found so far are
-// then packed into `list` (room for every slot) and the later rounds read only that list.
-// Returns v and, in *above, W(key > v).
-template <int EPT, typename WF>
-__device__ __forceinline__ uint32_t sel_radix_threshold(const KeyView<EPT>& key, uint32_t cbits,
-                                                        unsigned long long target, WF weight,
-                                                        uint32_t kmin, uint32_t kmax, uint32_t* list,
-                                                        SelLds& sh, unsigned long long* above_out) {
+// Fixed-point weight floor(v * 2^40) of a value v in [0, 1] from its bits, as its two
+// exact 32-bit halves: with t = v * 2^8 (exact, t <= 256) the high half is floor(t) and
+// the low half floor(fract(t) * 2^32).
+__device__ __forceinline__ unsigned long long weight_u64(uint32_t key) {
+  const float t = __uint_as_float(key) * 256.0f;
+  const uint32_t hi = (uint32_t)t;
+  const uint32_t lo = (uint32_t)(__builtin_amdgcn_fractf(t) * 4294967296.0f);
+  return ((unsigned long long)hi << 32) | lo;
+}
+
+// After a histogram round: the digit where the weight from the top crosses the target,
+// and the weight above it.  On the first round the target is target_of(the histogram's
+// total, which is every candidate's weight); it comes back in *target (0: no digit).
+template <typename TF>
+__device__ __forceinline__ void sel_pick_digit(SelLds& sh, bool first, TF target_of,
+                                               unsigned long long* target_io,
+                                               unsigned long long above, uint32_t* d_out,
+                                               unsigned long long* above_out) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  *above_out = 0;
-  if (kmin == kmax) return kmin;
-  int pos = 32 - __clz((int)(kmin ^ kmax));
-  uint32_t prefix = pos >= 32 ? 0u : (kmin & ~((1u << pos) - 1u));
-  unsigned long long above = 0;
-  int n_list = -1;
-  while (pos > 0) {
-    const int nb = min(SEL_RADIX_BITS, pos), lo = pos - nb;
-    const uint32_t hi_mask = pos >= 32 ? 0u : ~((1u << pos) - 1u);
-    const uint32_t dmask = (1u << nb) - 1u;
-    __syncthreads();
+  unsigned long long own = 0;
 #pragma unroll
-    for (int b = 0; b < SEL_BPT; ++b) sh.hist[tid * SEL_BPT + b] = 0ull;
-    __syncthreads();
-    if (n_list < 0) {
-      const uint32_t cb = sel_opaque(cbits);
+  for (int b = 0; b < SEL_BPT; ++b) own += sh.hist[tid * SEL_BPT + b];
+  unsigned long long x = own;
 #pragma unroll
-      for (int i = 0; i < EPT; ++i) {
-        const uint32_t k = sel_opaque(key[i]);
-        if (((cb >> i) & 1u) && (k & hi_mask) == prefix) atomicAdd(&sh.hist[(k >> lo) & dmask], weight(k));
+  for (int o = 1; o < 64; o <<= 1) {
+    const unsigned long long y = __shfl_down(x, o, 64);
+    if (lane + o < 64) x += y;
+  }
+  if (lane == 0) sh.red64[wave] = x;
+  __syncthreads();
+  unsigned long long suf = x - own;
+  for (int w = wave + 1; w < SEL_NW; ++w) suf += sh.red64[w];
+  if (first) {
+    unsigned long long tot = 0;
+#pragma unroll
+    for (int w = 0; w < SEL_NW; ++w) tot += sh.red64[w];
+    *target_io = target_of(tot);
+  }
+  const unsigned long long target = *target_io;
+  if (target == 0) return;
+  const unsigned long long lo_m = above + suf;
+  if (lo_m < target && lo_m + own >= target) {
+    unsigned long long cum = lo_m;
+    for (int b = SEL_BPT - 1; b >= 0; --b) {
+      const unsigned long long nxt = cum + sh.hist[tid * SEL_BPT + b];
+      if (nxt >= target) {
+        sh.pick_digit = (uint32_t)(tid * SEL_BPT + b);
+        sh.pick_above = cum;
+        break;
       }
-    } else {
-      for (int j = tid; j < n_list; j += SEL_NT) {
-        const uint32_t k = list[j];
-        if ((k & hi_mask) == prefix) atomicAdd(&sh.hist[(k >> lo) & dmask], weight(k));
-      }
-    }
-    __syncthreads();
-    // the digit where the weight from the top crosses the target
-    unsigned long long own = 0;
-#pragma unroll
-    for (int b = 0; b < SEL_BPT; ++b) own += sh.hist[tid * SEL_BPT + b];
-    unsigned long long x = own;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const unsigned long long y = __shfl_down(x, o, 64);
-      if (lane + o < 64) x += y;
-    }
-    if (lane == 0) sh.red64[wave] = x;
-    __syncthreads();
-    unsigned long long suf = x - own;
-    for (int w = wave + 1; w < SEL_NW; ++w) suf += sh.red64[w];
-    const unsigned long long lo_m = above + suf;
-    if (lo_m < target && lo_m + own >= target) {
-      unsigned long long cum = lo_m;
-      for (int b = SEL_BPT - 1; b >= 0; --b) {
-        const unsigned long long nxt = cum + sh.hist[tid * SEL_BPT + b];
-        if (nxt >= target) {
-          sh.pick_digit = (uint32_t)(tid * SEL_BPT + b);
-          sh.pick_above = cum;
-          break;
-        }
-        cum = nxt;
-      }
-    }
-    __syncthreads();
-    prefix |= sh.pick_digit << lo;
-    above = sh.pick_above;
-    pos = lo;
-    if (pos > 0 && n_list < 0) {
-      // stage the candidates that share the digits found so far (the list holds every slot)
-      const uint32_t m2 = ~((1u << pos) - 1u);
-      const uint32_t cb = sel_opaque(cbits);
-      uint32_t inb = 0;
-#pragma unroll
-      for (int i = 0; i < EPT; ++i)
-        if (((cb >> i) & 1u) && (sel_opaque(key[i]) & m2) == prefix) inb |= 1u << i;
-      const int2 sc = block_exscan_int(__popc(inb), sh.redi);
-      int off = sc.x;
-#pragma unroll
-      for (int i = 0; i < EPT; ++i)
-        if ((inb >> i) & 1u) list[off++] = key[i];
-      n_list = sc.y;
+      cum = nxt;
     }
   }
+  __syncthreads();
+  *d_out = sh.pick_digit;
+  *above_out = sh.pick_above;
+}
+
+__device__ __forceinline__ uint32_t sel_block_sum_u32(uint32_t v, int* red) {
+  v = wave_reduce_u32(v, 0u, [](uint32_t a, uint32_t b) { return a + b; });
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = (int)v;
+  __syncthreads();
+  uint32_t r = 0;
+#pragma unroll
+  for (int w = 0; w < SEL_NW; ++w) r += (uint32_t)red[w];
+  return r;
+}
+
+// Zero the histogram between two barriers.
+__device__ __forceinline__ void sel_clear_hist(SelLds& sh) {
+  __syncthreads();                   // earlier readers of the LDS scratch are done
+#pragma unroll
+  for (int b = 0; b < SEL_BPT; ++b) sh.hist[threadIdx.x * SEL_BPT + b] = 0ull;
+  __syncthreads();
+}
+
+// Stage the candidates whose bits from `pos` up equal `prefix` into the list (it holds
+// every slot); returns their number.
+template <int EPT>
+__device__ __forceinline__ int sel_stage_list(const KeyView<EPT>& key, uint32_t cbits, int pos,
+                                              uint32_t prefix, uint32_t* list, SelLds& sh) {
+  const uint32_t m2 = ~((1u << pos) - 1u);
+  const uint32_t cb = sel_opaque(cbits);
+  uint32_t inb = 0;
+#pragma unroll
+  for (int i = 0; i < EPT; ++i)
+    if (((cb >> i) & 1u) && (sel_opaque(key[i]) & m2) == prefix) inb |= 1u << i;
+  const int2 sc = block_exscan_int(__popc(inb), sh.redi);
+  int off = sc.x;
+#pragma unroll
+  for (int i = 0; i < EPT; ++i)
+    if ((inb >> i) & 1u) list[off++] = key[i];
+  return sc.y;
+}
+
+// Largest candidate key v with W(key >= v) >= target, where W sums weight(key) over the
+// candidates and target = target_of(W(all candidates)) (at most that total); the target
+// comes back in *target_out, and for a target of 0 nothing else is computed.  The bits
+// above the first one where the candidates' keys differ are common to all of them; below
+// them v is found SEL_RADIX_BITS at a time from a histogram of weights per digit (LDS
+// atomics) and a suffix scan over the digits.  The first round reads the keys in
+// registers (outside the loop, so the compiler does not keep the EPT weights, which no
+// later round changes, in registers of their own); the candidates that share the
+// digits found are then packed into the LDS list, which the remaining rounds read.
+// Returns v and, in *above, W(key > v).
+template <int EPT, typename WF, typename TF>
+__device__ __forceinline__ uint32_t sel_radix_threshold(const KeyView<EPT>& key, uint32_t cbits,
+                                                        TF target_of, WF weight, uint32_t kmin,
+                                                        uint32_t kmax, uint32_t* list, SelLds& sh,
+                                                        unsigned long long* target_out,
+                                                        unsigned long long* above_out) {
+  const int tid = threadIdx.x;
+  *above_out = 0;
+  if (kmin == kmax) {
+    // one key value: the total is the candidates' count times its weight
+    const int cnt = block_sum_int<SEL_NT>(__popc(cbits), sh.redi);
+    *target_out = target_of((unsigned long long)cnt * weight(kmin));
+    return kmin;
+  }
+  int pos = 32 - __clz((int)(kmin ^ kmax));
+  uint32_t prefix = pos >= 32 ? 0u : (kmin & ~((1u << pos) - 1u));
+  unsigned long long above = 0, target = 0;
+  int n_list;
+  {
+    // every candidate shares the prefix: its digit is its key minus the prefix, shifted
+    const int nb = min(SEL_RADIX_BITS, pos), lo = pos - nb;
+    sel_clear_hist(sh);
+#pragma unroll
+    for (int i = 0; i < EPT; ++i)
+      if ((cbits >> i) & 1u) atomicAdd(&sh.hist[(key[i] - prefix) >> lo], weight(key[i]));
+    __syncthreads();
+    uint32_t d;
+    sel_pick_digit(sh, true, target_of, &target, above, &d, &above);
+    if (target == 0) {
+      *target_out = 0;
+      return prefix;
+    }
+    prefix |= d << lo;
+    pos = lo;
+    n_list = pos > 0 ? sel_stage_list<EPT>(key, cbits, pos, prefix, list, sh) : 0;
+  }
+  while (pos > 0) {
+    const int nb = min(SEL_RADIX_BITS, pos), lo = pos - nb;
+    const uint32_t hi_mask = ~((1u << pos) - 1u);
+    const uint32_t dmask = (1u << nb) - 1u;
+    sel_clear_hist(sh);
+    for (int j = tid; j < n_list; j += SEL_NT) {
+      const uint32_t k = list[j];
+      if ((k & hi_mask) == prefix) atomicAdd(&sh.hist[(k >> lo) & dmask], weight(k));
+    }
+    __syncthreads();
+    uint32_t d;
+    sel_pick_digit(sh, false, target_of, &target, above, &d, &above);
+    prefix |= d << lo;
+    pos = lo;
+  }
+  *target_out = target;
   *above_out = above;
   return prefix;
 }
@@ -371,9 +427,11 @@ __device__ __forceinline__ void topp_core(float* val, uint32_t cbits, int p_q, i
   if (tid == 0 && flags && status) atomicOr(status, flags);
 
   const int n_cand = block_sum_int<SEL_NT>(__popc(cbits), sh.redi);
-  const unsigned long long tot = uniform_u64(block_sum_u64<SEL_NT>(mass_ge<EPT>(key, cbits, 0u), sh.red64));
   const unsigned long long pq = (unsigned long long)p_q;
-  const unsigned long long target = pq * (tot / 1000000ull) + (pq * (tot % 1000000ull) + 999999ull) / 1000000ull;
+  // target = ceil(p_q * Total / 10^6) without overflow (Total from the first search round)
+  const auto target_of = [pq](unsigned long long tot) {
+    return pq * (tot / 1000000ull) + (pq * (tot % 1000000ull) + 999999ull) / 1000000ull;
+  };
 
   // the bits above the first one where the candidates' keys differ are common to all of
   // them: the searches start below them
@@ -387,39 +445,25 @@ __device__ __forceinline__ void topp_core(float* val, uint32_t cbits, int p_q, i
   kmin = block_min_u32(kmin, sh.redi);
   kmax = block_max_u32(kmax, sh.redi);
 
-  // k from the mass rule: v = value of the crossing element, elements above it all taken
-  int k = 0;
-  uint32_t v = 0;
+  // mass rule: v = value of the crossing element, the elements above it all taken, and
+  // `take` of those equal to it
+  uint32_t v = 0xffffffffu;
   int take = 0;
-  if (target > 0) {
-    unsigned long long mass_gt = 0;
-    v = sel_radix_threshold<EPT>(key, cbits, target,
-                                 [](uint32_t kk) { return (unsigned long long)fixed_weight(kk); },
-                                 kmin, kmax, list, sh, &mass_gt);
+  unsigned long long target = 0, mass_gt = 0, wv = 0;
+  if (n_cand > 0) {
+    v = sel_radix_threshold<EPT>(key, cbits, target_of, [](uint32_t kk) { return weight_u64(kk); },
+                                 kmin, kmax, list, sh, &target, &mass_gt);
     v = __builtin_amdgcn_readfirstlane(v);
+    target = uniform_u64(target);
     mass_gt = uniform_u64(mass_gt);
-    const int cnt_gt = block_sum_int<SEL_NT>(count_ge<EPT>(key, cbits, v + 1), sh.redi);
-    const unsigned long long wv = uniform_u64((unsigned long long)fixed_weight(v));
-    take = wv ? (int)((target - mass_gt + wv - 1) / wv) : 0;   // wv > 0 whenever target > 0
-    k = cnt_gt + take;
-  }
-  const int lo = min(max(k_min, 0), n_cand);
-  const int hi = (k_max > 0) ? min(k_max, n_cand) : n_cand;
-  const int kf = max(lo, min(k, hi));
-  if (kf != k || target == 0) {
-    if (kf == 0) {
-      v = 0xffffffffu;
-      take = 0;
+    if (target > 0) {
+      wv = uniform_u64(weight_u64(v));             // > 0: the crossing element weighs
+      take = (int)((target - mass_gt + wv - 1) / wv);
     } else {
-      // the kf largest keys: the same search on counts
-      unsigned long long cnt_gt = 0;
-      v = sel_radix_threshold<EPT>(key, cbits, (unsigned long long)kf,
-                                   [](uint32_t) { return 1ull; }, kmin, kmax, list, sh, &cnt_gt);
-      v = __builtin_amdgcn_readfirstlane(v);
-      take = kf - (int)uniform_u64(cnt_gt);
+      v = 0xffffffffu;
     }
   }
-  // selection: keys above v, plus the `take` most recent slots equal to v
+  // selection flags: keys above v and keys equal to it; both counts in one reduction
   uint32_t sel = 0, tie = 0;
 #pragma unroll
   for (int i = 0; i < EPT; ++i) {
@@ -428,15 +472,57 @@ __device__ __forceinline__ void topp_core(float* val, uint32_t cbits, int p_q, i
       if (key[i] == v) tie |= 1u << i;
     }
   }
-  const int n_tie = block_sum_int<SEL_NT>(__popc(tie), sh.redi);
+  // (each count is at most 32768, so the packed sum fits 32 unsigned bits)
+  const uint32_t both = sel_block_sum_u32((uint32_t)__popc(sel) | ((uint32_t)__popc(tie) << 16), sh.redi);
+  const int n_gt = (int)(both & 0xffffu);
+  int n_tie = (int)(both >> 16);
+  const int k = target > 0 ? n_gt + take : 0;
+  const int lo = min(max(k_min, 0), n_cand);
+  const int hi = (k_max > 0) ? min(k_max, n_cand) : n_cand;
+  const int kf = max(lo, min(k, hi));
+  const bool by_mass = kf == k && target > 0;
+  if (!by_mass) {
+    if (kf == 0) {
+      v = 0xffffffffu;
+      take = 0;
+      sel = 0;
+      tie = 0;
+      n_tie = 0;
+    } else {
+      // the kf largest keys: the same search on counts
+      unsigned long long t_cnt = 0, cnt_gt = 0;
+      v = sel_radix_threshold<EPT>(key, cbits, [kf](unsigned long long) { return (unsigned long long)kf; },
+                                   [](uint32_t) { return 1ull; }, kmin, kmax, list, sh, &t_cnt, &cnt_gt);
+      v = __builtin_amdgcn_readfirstlane(v);
+      take = kf - (int)uniform_u64(cnt_gt);
+      sel = 0;
+      tie = 0;
+#pragma unroll
+      for (int i = 0; i < EPT; ++i) {
+        if ((cbits >> i) & 1u) {
+          if (key[i] > v) sel |= 1u << i;
+          if (key[i] == v) tie |= 1u << i;
+        }
+      }
+      n_tie = block_sum_int<SEL_NT>(__popc(tie), sh.redi);
+    }
+  }
+  // keys above v, plus the `take` most recent slots equal to v
   if (take >= n_tie) sel |= tie;
   else if (take > 0) sel |= take_top_ties<EPT>(tie, take, tiecnt);
 
-  double msel_d = 0.0;
+  // the selected mass: by the mass rule it is W(key > v) + take * w(v) exactly; after a
+  // count clamp it is summed
+  unsigned long long msel;
+  if (by_mass) {
+    msel = mass_gt + (unsigned long long)take * wv;
+  } else {
+    double msel_d = 0.0;
 #pragma unroll
-  for (int i = 0; i < EPT; ++i)
-    if ((sel >> i) & 1u) msel_d += (double)fixed_weight(key[i]);
-  const unsigned long long msel = block_sum_u64<SEL_NT>((unsigned long long)msel_d, sh.red64);
+    for (int i = 0; i < EPT; ++i)
+      if ((sel >> i) & 1u) msel_d += (double)fixed_weight(key[i]);
+    msel = block_sum_u64<SEL_NT>((unsigned long long)msel_d, sh.red64);
+  }
 
 #pragma unroll
   for (int i = 0; i < EPT; ++i) {

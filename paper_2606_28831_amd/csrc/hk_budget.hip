@@ -609,8 +609,22 @@ __global__ __launch_bounds__(BG_NT) __attribute__((amdgpu_waves_per_eu(4, 8))) v
   if (row_k && tid == 0) row_k[(size_t)h * R + r] = k;
 }
 
-// votes[h][j] = sum over the R rows of bit j of row_sel[h][r]; one thread per 32-slot word
+// votes[h][j] = sum over the R rows of bit j of row_sel[h][r]; one thread per 32-slot word.
+// The 32 column counts are kept bit-sliced (plane p holds bit p of every count) and the
+// rows are added 16 at a time by a carry-save adder tree (Harley-Seal): two bitwise
+// operations per row word instead of 32 shifts and adds.  ones, twos, fours and eights
+// carry the low count bits across chunks; each chunk's carry out (sixteens) enters a
+// ripple counter of multiples of 16 (R <= 256: at most 16 of them, 5 planes).
 constexpr int VC_NT = 256;
+constexpr int VC_HI = 5;
+
+// full adder on 32 bit positions at once: l = a ^ b ^ c, h = majority(a, b, c)
+__device__ __forceinline__ void vc_csa(uint32_t& h, uint32_t& l, uint32_t a, uint32_t b, uint32_t c) {
+  const uint32_t u = a ^ b;
+  h = (a & b) | (u & c);
+  l = u ^ c;
+}
+
 __global__ __launch_bounds__(VC_NT) void vote_count_kernel(int R, int S_max,
                                                            const uint32_t* __restrict__ row_sel,
                                                            uint16_t* __restrict__ votes) {
@@ -618,14 +632,51 @@ __global__ __launch_bounds__(VC_NT) void vote_count_kernel(int R, int S_max,
   const int nw = S_max / 32;
   const int w = blockIdx.x * VC_NT + threadIdx.x;
   if (w >= nw) return;
+  const uint32_t* base = row_sel + (size_t)h * R * nw + w;
+  uint32_t ones = 0, twos = 0, fours = 0, eights = 0;
+  uint32_t hi[VC_HI];
+#pragma unroll
+  for (int p = 0; p < VC_HI; ++p) hi[p] = 0;
+  for (int r0 = 0; r0 < R; r0 += 16) {
+    // all 16 loads first (rows past R read row R-1 and count as zero words)
+    uint32_t x[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) x[i] = base[(size_t)min(r0 + i, R - 1) * nw];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) x[i] = (r0 + i < R) ? x[i] : 0u;
+    uint32_t twosA, twosB, foursA, foursB, eightsA, eightsB, sixteens;
+    vc_csa(twosA, ones, ones, x[0], x[1]);
+    vc_csa(twosB, ones, ones, x[2], x[3]);
+    vc_csa(foursA, twos, twos, twosA, twosB);
+    vc_csa(twosA, ones, ones, x[4], x[5]);
+    vc_csa(twosB, ones, ones, x[6], x[7]);
+    vc_csa(foursB, twos, twos, twosA, twosB);
+    vc_csa(eightsA, fours, fours, foursA, foursB);
+    vc_csa(twosA, ones, ones, x[8], x[9]);
+    vc_csa(twosB, ones, ones, x[10], x[11]);
+    vc_csa(foursA, twos, twos, twosA, twosB);
+    vc_csa(twosA, ones, ones, x[12], x[13]);
+    vc_csa(twosB, ones, ones, x[14], x[15]);
+    vc_csa(foursB, twos, twos, twosA, twosB);
+    vc_csa(eightsB, fours, fours, foursA, foursB);
+    vc_csa(sixteens, eights, eights, eightsA, eightsB);
+    uint32_t c = sixteens;
+#pragma unroll
+    for (int p = 0; p < VC_HI; ++p) {
+      const uint32_t t = hi[p] & c;
+      hi[p] ^= c;
+      c = t;
+    }
+  }
+  // count of bit b = ones_b + 2 twos_b + 4 fours_b + 8 eights_b + 16 (hi counter)_b
   uint32_t cnt[32];
 #pragma unroll
-  for (int b = 0; b < 32; ++b) cnt[b] = 0;
-  const uint32_t* base = row_sel + (size_t)h * R * nw + w;
-  for (int r = 0; r < R; ++r) {
-    const uint32_t x = base[(size_t)r * nw];
+  for (int b = 0; b < 32; ++b) {
+    uint32_t n = ((ones >> b) & 1u) | (((twos >> b) & 1u) << 1) | (((fours >> b) & 1u) << 2) |
+                 (((eights >> b) & 1u) << 3);
 #pragma unroll
-    for (int b = 0; b < 32; ++b) cnt[b] += (x >> b) & 1u;
+    for (int p = 0; p < VC_HI; ++p) n |= ((hi[p] >> b) & 1u) << (4 + p);
+    cnt[b] = n;
   }
   uint4* out = reinterpret_cast<uint4*>(votes + (size_t)h * S_max + (size_t)w * 32);
 #pragma unroll

@@ -287,6 +287,67 @@ __device__ __forceinline__ void p2_tile_pipelined(const F* kf, const char* qlds,
   }
 }
 
+// per-row probabilities of one full tile (every row valid): stores the clamped
+// exp2(c2*z[r][key] - lse2[r]) of each row r (0 at a non-candidate slot), the MFMAs of
+// block qb interleaved with the exponentials and stores of block qb-1.  A row's place
+// in the output is uniform across the wave for a given accumulator register, so the
+// stores are buffer stores with the lane's column in the vector offset and the row's
+// offset in a scalar one: no per-store address arithmetic.
+template <typename F, int QB>
+__device__ __forceinline__ void rows_tile_pipelined(const F& kf, const char* qlds, const float* lse2,
+                                                    float c2, int lane, bool cand,
+                                                    __amdgpu_buffer_rsrc_t out, uint32_t voff,
+                                                    uint32_t row_bytes) {
+  constexpr int KS = F::KSTEPS;
+  constexpr int NF = QB * KS;
+  lds_frag_t<F> qf[SCORE_QD + 1];
+#pragma unroll
+  for (int g = 0; g < SCORE_QD && g < NF; ++g) qf[g] = F::lds(qlds, g / KS, g % KS, lane);
+  f32x16 acc[2];
+#pragma unroll
+  for (int qb = 0; qb <= QB; ++qb) {
+    f32x4 l4[4];
+    if (qb >= 1) {
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4)
+        l4[r4] = *reinterpret_cast<const f32x4*>(lse2 + (qb - 1) * 32 + 8 * r4 + 4 * (lane >> 5));
+    }
+    if (qb < QB) acc[qb & 1] = f32x16{};
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      const int g = qb * KS + kk;
+      if (qb < QB) {
+        acc[qb & 1] = F::mma(qf[g % (SCORE_QD + 1)], kf.v[kk], acc[qb & 1]);
+        if (g + SCORE_QD < NF)
+          qf[(g + SCORE_QD) % (SCORE_QD + 1)] = F::lds(qlds, (g + SCORE_QD) / KS, (g + SCORE_QD) % KS, lane);
+      }
+      if (qb >= 1) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          if (e * KS / 16 == kk) {
+            // a probability: rounding in exp and in LSE can put the largest a hair above 1
+            const float a = fminf(fast_exp2(fmaf(acc[(qb - 1) & 1][e], c2, -l4[e >> 2][e & 3])), 1.0f);
+            const int row = (qb - 1) * 32 + 8 * (e >> 2) + (e & 3);   // + 4 (lane / 32) in voff
+            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(cand ? a : 0.f), out, (int)voff,
+                                                  (int)(row * row_bytes), 2 /* nontemporal */);
+          }
+      }
+    }
+    if constexpr (sizeof(lds_frag_t<F>) == 16) {
+      if (qb >= 1 && qb < QB) {
+        // per MFMA step: one MFMA, one LDS read, two rows' exponentials and their stores
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                 // MFMA
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);                 // LDS read
+          __builtin_amdgcn_sched_group_barrier(0x002, 4 * 16 / KS, 0);       // VALU
+          __builtin_amdgcn_sched_group_barrier(0x040, 16 / KS, 0);           // VMEM write
+        }
+      }
+    }
+  }
+}
+
 // pass 1: online (max, sum exp2) update of the lane's query column for every block, over
 // KT key tiles; every Q fragment read from LDS feeds KT MFMAs.
 template <typename F, int QB, int KT>
@@ -796,8 +857,17 @@ static size_t pass2_lds(int R_pad, int D, int es, bool red) {
 // one by one.  Same tiles as pass 2 (C[query][key] on MFMA 32x32); each accumulator value is
 // stored instead of summed over rows.  Register e of lane l is row 8*(e/4) + 4*(l/32) + e%4 of
 // the block and key l % 32, so each half wave stores 32 consecutive floats of one row.
+// (Four waves per SIMD cap the registers at 128, as for pass 2: uncapped, the compiler
+// holds every query block's operands at once and spills.)
 template <typename T, int D, int QB>
-__global__ __launch_bounds__(SCORE_NT) void score_rows_kernel(
+constexpr int rows_min_waves() {
+  return (sizeof(T) == 2 && D == 128 && (QB == 7 || QB == 4)) ? 4 : 1;
+}
+
+template <typename T, int D, int QB>
+__global__ __launch_bounds__(SCORE_NT) __attribute__((amdgpu_waves_per_eu(
+    rows_min_waves<T, D, QB>(), rows_min_waves<T, D, QB>() > 1 ? rows_min_waves<T, D, QB>() : 8)))
+void score_rows_kernel(
     const T* __restrict__ q_obs, const T* __restrict__ k_pool, const int32_t* __restrict__ table,
     const uint16_t* __restrict__ masks, const int32_t* __restrict__ n_pages_arr, int NS, int Hq,
     int Hkv, int W, int max_pages, int L_dense, float c2, const float* __restrict__ row_lse,
@@ -843,14 +913,24 @@ __global__ __launch_bounds__(SCORE_NT) void score_rows_kernel(
   __syncthreads();
 
   const int kl = lane & 31;
-  for (int p0 = p_begin + 2 * wave; p0 < p_cand_end; p0 += 2 * SCORE_NW) {
-    F kf;
-    load_tile<T, D>(kf, k_pool, trow, p0, p_cand_end, lane);
+  // the head's R rows as one buffer (R * S_max * 4 <= 32 MiB)
+  const __amdgpu_buffer_rsrc_t out = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)arow, (short)0, (int)((size_t)R * S_max * sizeof(float)), 0x00020000);
+  auto load_group = [&](F* kf, int p0) { load_tile<T, D>(kf[0], k_pool, trow, p0, p_cand_end, lane); };
+  auto process = [&](F* kfs, int p0) {
+    const F& kf = kfs[0];
     const int pg = p0 + (kl >> 4);
     const int slot = pg * HK_PAGE + (kl & 15);
     const bool in = pg < p_cand_end;
     const bool cand = in && (((uint32_t)mrow[pg] >> (kl & 15)) & 1u);
-#pragma unroll
+    const uint32_t voff = (uint32_t)((4 * (lane >> 5)) * S_max + slot) * 4u;
+    const uint32_t row_bytes = (uint32_t)S_max * 4u;
+    if (p0 + 1 < p_cand_end && R == R_pad) {
+      rows_tile_pipelined<F, QB>(kf, smem, lse2, c2, lane, cand, out, voff, row_bytes);
+      return;
+    }
+    // a tile at the end of the candidates or a row count that is not a multiple of 32
+#pragma unroll 1
     for (int qb = 0; qb < QB; ++qb) {
       const f32x16 acc = mma_chain<F, true>(kf, smem, qb, lane);
 #pragma unroll
@@ -859,11 +939,14 @@ __global__ __launch_bounds__(SCORE_NT) void score_rows_kernel(
         if (in && row < R) {
           // a probability: rounding in exp and in LSE can put the largest a hair above 1
           const float a = cand ? fminf(fast_exp2(fmaf(acc[e], c2, -lse2[row])), 1.0f) : 0.f;
-          __builtin_nontemporal_store(a, arow + (size_t)row * S_max + slot);
+          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(a), out, (int)voff,
+                                                (int)((qb * 32 + 8 * (e >> 2) + (e & 3)) * row_bytes),
+                                                2 /* nontemporal */);
         }
       }
     }
-  }
+  };
+  tile_loop<F>(load_group, process, p_begin + 2 * wave, p_cand_end, 2 * SCORE_NW);
 }
 
 template <typename T, int D, int QB>

@@ -48,10 +48,20 @@ def _valid(mask_row):
 
 
 # ---------------------------------------------------------------- per-row probabilities
-@pytest.mark.parametrize("name", list(CACHES))
+# a row count that is not a multiple of 32 (R = 3 * 10 = 30): the partial-tile path of
+# the per-row kernel for every tile, not only the last
+ROW_CACHES = dict(CACHES)
+ROW_CACHES["bf16_d128_g3_w10"] = (dict(L=1, B=2, Hq=6, Hkv=2, D=128, N=600, dtype="bf16", W=10,
+                                       seed=15, recipe="normal"), dict(hole_prob=0.05))
+
+
+@pytest.mark.parametrize("name", list(ROW_CACHES))
 @pytest.mark.parametrize("L_dense", [0, 48])
 def test_score_rows(name, L_dense):
-    hk, cfg, w, kv = _setup(name)
+    import paper_2606_28831_amd as hk
+    cfg, kw = ROW_CACHES[name]
+    w = WL.make_workload(cfg, DEV, **kw)
+    kv = hk.PagedKV(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)
     G = cfg["Hq"] // cfg["Hkv"]
     R = G * cfg["W"]
     d = hk.dims(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"], cfg["W"])

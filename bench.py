@@ -731,6 +731,40 @@ def copy_calibration():
     return {"copy_calibration_bytes": a.numel() * 4, "copies": 3}
 
 
+def run_peaks():
+    """Measured rates behind the score passes' rooflines: the hardware exponential
+    (v_exp_f32) and the bf16 MFMA (32x32x16), each from a throughput kernel of the library
+    (hk_probe) timed with events on the launch stream, best of five launches."""
+    import paper_2606_28831_amd as hk
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    blocks = 4 * n_cu                            # 16 waves per CU: every SIMD busy
+    out = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
+
+    def best_ms(kind, iters):
+        hk.hk_probe(kind, blocks, iters, out)     # warm
+        best = float("inf")
+        for _ in range(5):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            hk.hk_probe(kind, blocks, iters, out)
+            e1.record()
+            torch.cuda.synchronize()
+            best = min(best, e0.elapsed_time(e1))
+        if not torch.isfinite(out).all():
+            raise SystemExit("rate probe produced a non-finite value")
+        return best
+
+    it_exp, it_mfma = 4096, 2048
+    ms_exp = best_ms(hk.PROBE_EXP, it_exp)
+    ms_mfma = best_ms(hk.PROBE_MFMA, it_mfma)
+    n_exp = 8 * it_exp * 256 * blocks
+    n_mfma = 16 * it_mfma * blocks
+    return {"probe": "rates", "compute_units": n_cu, "workgroups": blocks,
+            "exp_per_s": n_exp / (ms_exp / 1e3), "exp_ms": ms_exp,
+            "mfma_bf16_tflops": n_mfma * 32768 / (ms_mfma / 1e3) / 1e12, "mfma_ms": ms_mfma,
+            "mfma_bf16_peak_tflops": 2500.0}
+
+
 def _pmc_mean(run_dir, counter, match):
     """Mean per-dispatch value (KiB) of one counter over the dispatches of kernels whose
     name contains `match`, from a rocprofv3 --pmc output directory."""
@@ -803,6 +837,8 @@ def main():
     ap.add_argument("--graph", action="store_true",
                     help="config 5: replay each decode segment from one captured HIP graph")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--peaks", action="store_true",
+                    help="only measure the exponential and bf16 MFMA rates (hk_probe)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run the 1 GiB plain copy the byte counters are scaled by")
     ap.add_argument("--summarize-pmc", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "CAL_FETCH_DIR",
@@ -828,6 +864,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         print(json.dumps(copy_calibration()), flush=True)
+        return
+    if args.peaks:
+        print(json.dumps(run_peaks()), flush=True)
         return
     if args.crossover:
         print(json.dumps(run_crossover(args)), flush=True)

@@ -429,6 +429,20 @@ enum {
 hk_status hk_timing_enable(uint32_t kernel_mask);
 hk_status hk_timing_read(int32_t kernel, double* total_ms, int64_t* launches);
 
+/* Rate probes behind the score passes' rooflines (measurement only; not a step of the
+ * method).  hk_probe launches one throughput kernel of `blocks` workgroups of 256 threads
+ * on `stream`:
+ *   HK_PROBE_EXP  : every thread runs 8 independent chains of `iters` hardware
+ *                   exponentials (v_exp_f32): 8 * iters * 256 * blocks of them;
+ *   HK_PROBE_MFMA : every wave runs 4 independent chains of `iters`
+ *                   v_mfma_f32_32x32x16_bf16: 16 * iters * blocks MFMAs of 32768 flop.
+ * out: device, >= 256 * blocks floats, caller-owned; receives one value per thread (it
+ * keeps the work live).  The caller times the launch.  Errors: HK_ERR_ARG for an unknown
+ * kind, blocks < 1 or > 2^20, iters < 1, or a null out.
+ */
+enum { HK_PROBE_EXP = 0, HK_PROBE_MFMA = 1 };
+hk_status hk_probe(int32_t kind, int32_t blocks, int32_t iters, float* out, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -19,7 +19,8 @@ __all__ = ["HardKVError", "lib", "PagedKV", "Allocator", "hk_score", "hk_calibra
            "OP_DECODE", "OP_APPEND", "FLAG_NOSPACE", "FLAG_NAN", "FLAG_RANGE", "LIB_PATH",
            "hk_timing_enable", "hk_timing_read", "TIMED_KERNELS", "hk_calibrate_topp",
            "hk_pool_max", "hk_score_rows", "hk_vote_topp", "hk_budget_plan", "hk_budget_select",
-           "hk_compact_modes", "hk_calibrate_solve_T_gd", "hk_alloc_init", "hk_compress", "OP_COMPRESS", "BUDGET_KEEP", "BUDGET_SPARSE", "BUDGET_REWRITE"]
+           "hk_compact_modes", "hk_calibrate_solve_T_gd", "hk_alloc_init", "hk_compress", "OP_COMPRESS", "BUDGET_KEEP", "BUDGET_SPARSE", "BUDGET_REWRITE",
+           "hk_probe", "PROBE_EXP", "PROBE_MFMA"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhardkv.so")
 
@@ -27,11 +28,13 @@ HK_F32, HK_BF16 = 0, 1
 OP_SCORE, OP_COMPACT, OP_DECODE, OP_APPEND, OP_COMPRESS = 0, 1, 2, 3, 4
 FLAG_NOSPACE, FLAG_NAN, FLAG_RANGE = 1, 2, 4
 BUDGET_KEEP, BUDGET_SPARSE, BUDGET_REWRITE = 0, 1, 2
+PROBE_EXP, PROBE_MFMA = 0, 1
 EXPORTED = ["hk_score", "hk_calibrate", "hk_calibrate_solve_T", "hk_topp_select", "hk_compact",
             "hk_decode_attn", "hk_append_kv", "hk_workspace_size", "hk_status_string",
             "hk_timing_enable", "hk_timing_read", "hk_calibrate_topp", "hk_pool_max",
             "hk_score_rows", "hk_vote_topp", "hk_budget_plan", "hk_budget_select",
-            "hk_compact_modes", "hk_calibrate_solve_T_gd", "hk_alloc_init", "hk_compress"]
+            "hk_compact_modes", "hk_calibrate_solve_T_gd", "hk_alloc_init", "hk_compress",
+            "hk_probe"]
 # kernel ids of hk_timing_read, in header order
 TIMED_KERNELS = ["score_pass1", "score_merge", "score_pass2", "calibrate", "topp", "solve_T",
                  "compact_gather", "compact_meta", "decode_split", "decode_merge", "append",
@@ -117,6 +120,8 @@ def lib():
         L.hk_compress.restype = I32
         L.hk_compress.argtypes = [C.POINTER(hk_dims), P, C.POINTER(hk_paged_kv), I32, I32, F, P, D,
                                   I32, I32, C.POINTER(hk_allocator), P, P, P, P, SZ, P]
+        L.hk_probe.restype = I32
+        L.hk_probe.argtypes = [I32, I32, I32, P, P]
         L.hk_timing_enable.restype = I32
         L.hk_timing_enable.argtypes = [C.c_uint32]
         L.hk_timing_read.restype = I32
@@ -340,6 +345,12 @@ def hk_timing_enable(kernels=None):
     for k in names:
         mask |= 1 << TIMED_KERNELS.index(k)
     _check(lib().hk_timing_enable(mask), "hk_timing_enable")
+
+
+def hk_probe(kind: int, blocks: int, iters: int, out, stream=None):
+    """One rate-probe launch (PROBE_EXP or PROBE_MFMA); out: >= 256 * blocks floats."""
+    _check(lib().hk_probe(int(kind), int(blocks), int(iters), _ptr(out), _stream(stream)),
+           "hk_probe")
 
 
 def hk_timing_read(kernel: str):

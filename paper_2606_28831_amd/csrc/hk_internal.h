@@ -240,6 +240,7 @@ hipError_t hk_launch_compact(int n_heads, int D, const hk_paged_kv* kv, const ui
                              int L_dense, int L_sparse, const int32_t* head_mode,
                              const hk_allocator* alloc, int32_t* status, void* ws, hipStream_t st);
 size_t hk_compact_ws(int n_heads, int max_pages);
+hipError_t hk_launch_probe(int kind, int blocks, int iters, float* out, hipStream_t st);
 hipError_t hk_launch_alloc_init(int32_t* free_ids, int32_t* free_top, int first_free, int n,
                                 hipStream_t st);
 

@@ -809,3 +809,19 @@ def test_pool_then_select_pipeline():
         check_prob(c_gpu, c_ref, 2e-3, f"c head {h}")
         check_topp_rule(c_gpu, unpack_bits(np_i(b.sel_bits[h]), S), int(b.k[h]), cand, 0.9,
                         what=f"head {h}")
+
+
+# ---------------------------------------------------------------- rate probes
+@pytest.mark.gpu
+def test_rate_probes_run():
+    """hk_probe launches both throughput kernels and writes a finite value per thread; the
+    exponential chains x <- 2^-x stay in (0, 1]."""
+    import paper_2606_28831_amd as hk
+    out = torch.full((8 * 256,), float("nan"), device=DEV)
+    hk.hk_probe(hk.PROBE_EXP, 8, 64, out)
+    torch.cuda.synchronize()
+    assert torch.isfinite(out).all() and (out > 0).all() and (out <= 8).all()
+    out.fill_(float("nan"))
+    hk.hk_probe(hk.PROBE_MFMA, 8, 16, out)
+    torch.cuda.synchronize()
+    assert torch.isfinite(out).all()

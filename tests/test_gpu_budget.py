@@ -132,7 +132,7 @@ def _rows(kind, H, R, S, cand_len, rng):
                                         ("mixed", 12, 512, 0.9), ("dirichlet", 1, 64, 1.0),
                                         ("dirichlet", 3, 32768, 0.9), ("crowded", 2, 16384, 0.9),
                                         ("dirichlet", 128, 256, 0.0), ("negzero", 6, 1056, 0.9),
-                                        ("ties", 4, 1536, 0.5)])
+                                        ("ties", 4, 1536, 0.5), ("spread", 256, 512, 0.9)])
 def test_vote_topp(kind, R, S, p):
     import paper_2606_28831_amd as hk
     rng = np.random.default_rng(zlib.crc32(f"{kind}/{R}/{S}".encode()))

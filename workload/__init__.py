@@ -61,6 +61,7 @@ class Workload:
     tau: torch.Tensor | None = None
     ref_slots: torch.Tensor | None = None
     extra: dict = field(default_factory=dict)
+    meta: torch.Tensor | None = None   # one buffer behind the five mutable metadata tensors
 
     @property
     def NS(self):
@@ -173,18 +174,41 @@ def make_workload(cfg: dict, device="cpu", pool_slack: float = 2.0, max_pages: i
         ref = torch.topk(keys, min(n_ref, n_used * PAGE), dim=1).indices.to(torch.int32)
         ref = torch.sort(ref, dim=1).values.contiguous()
 
+    meta, (table, page_mask, n_pages, free_ids, free_top) = _pack(
+        dev, [table, page_mask, n_pages, free_ids, free_top])
     return Workload(cfg=dict(cfg), q_obs=q_obs, k_pool=k_pool, v_pool=v_pool, page_table=table,
                     page_mask=page_mask, n_pages=n_pages, free_ids=free_ids, free_top=free_top,
-                    max_pages=mp, tau=tau, ref_slots=ref)
+                    max_pages=mp, tau=tau, ref_slots=ref, meta=meta)
+
+
+def _pack(dev, tensors):
+    """The tensors copied into views of one byte buffer, each at a 256-byte offset, so the
+    whole mutable state is saved and restored by one copy.  Returns (buffer, views)."""
+    offs, total = [], 0
+    for t in tensors:
+        offs.append(total)
+        total += -(-t.numel() * t.element_size() // 256) * 256
+    buf = torch.zeros(total, dtype=torch.uint8, device=dev)
+    views = []
+    for t, o in zip(tensors, offs):
+        v = buf[o:o + t.numel() * t.element_size()].view(t.dtype).view(t.shape)
+        v.copy_(t)
+        views.append(v)
+    return buf, views
+
+
+_STATE = ("page_table", "page_mask", "n_pages", "free_ids", "free_top")
 
 
 def clone_state(w: Workload) -> dict:
     """Copy of the mutable cache metadata (tables, masks, counts, allocator)."""
-    return {k: getattr(w, k).clone() for k in ("page_table", "page_mask", "n_pages", "free_ids",
-                                               "free_top")}
+    if w.meta is not None:
+        return {"meta": w.meta.clone()}
+    return {k: getattr(w, k).clone() for k in _STATE}
 
 
 def restore_state(w: Workload, st: dict) -> None:
+    """Back to a clone_state copy: one device copy when the state shares one buffer."""
     for k, v in st.items():
         getattr(w, k).copy_(v)
 

@@ -24,8 +24,10 @@ bool take(Pair& p) {
     g_pool.pop_back();
     return true;
   }
-  if (hipEventCreate(&p.start) != hipSuccess) return false;
-  if (hipEventCreate(&p.stop) != hipSuccess) {
+  // timing-only events: no system-scope fence at record (a default event writes back and
+  // invalidates the caches there, which costs the timed stream time of its own)
+  if (hipEventCreateWithFlags(&p.start, hipEventDisableSystemFence) != hipSuccess) return false;
+  if (hipEventCreateWithFlags(&p.stop, hipEventDisableSystemFence) != hipSuccess) {
     (void)hipEventDestroy(p.start);
     return false;
   }

@@ -99,3 +99,25 @@ def test_roofline_takes_the_kernel_with_the_largest_share(bench, monkeypatch):
     assert r["achieved"] == pytest.approx(1e9 / 0.2e-3 / 1e9)
     assert r["frac"] == pytest.approx(r["achieved"] / bench.HBM_PEAK_GBS)
     assert r["mfma_tflops"] == pytest.approx(2e12 / 0.2e-3 / 1e12)
+
+
+def test_workload_state_is_one_buffer_and_restores_whole():
+    """The five mutable metadata tensors are 256-byte-aligned views of one buffer, and a
+    clone / restore round trip brings every one of them back."""
+    import torch
+    import workload as WL
+    w = WL.make_workload(WL.config(1), "cpu")
+    base = w.meta.data_ptr()
+    end = base + w.meta.numel()
+    names = ("page_table", "page_mask", "n_pages", "free_ids", "free_top")
+    for k in names:
+        t = getattr(w, k)
+        assert base <= t.data_ptr() and t.data_ptr() + t.numel() * t.element_size() <= end, k
+        assert (t.data_ptr() - base) % 256 == 0, k
+    before = {k: getattr(w, k).clone() for k in names}
+    st = WL.clone_state(w)
+    for k in names:
+        getattr(w, k).fill_(7)
+    WL.restore_state(w, st)
+    for k in names:
+        assert torch.equal(getattr(w, k), before[k]), k

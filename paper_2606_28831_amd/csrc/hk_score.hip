@@ -632,16 +632,30 @@ __global__ __launch_bounds__(256) void score_lse_merge_kernel(const float2* __re
   const int R = G * W;
   // the candidate count, also written by pass 2, so that a call without it has one too
   if (threadIdx.x == 0) cand_len_out[h] = HK_PAGE * max(0, n_pages_arr[h] - dense_pages(L_dense));
+  // the partials are read MB at a time, every load issued before any is used (a loop of
+  // load-then-use waits on each in turn); up to MB chunks this is one batch and the sums
+  // run in chunk order, as a plain two-sweep merge would
+  constexpr int MB = 16;
   for (int r = threadIdx.x; r < R; r += blockDim.x) {
     const float2* p = part + (size_t)h * n_chunks * R_pad + r;
-    float mn = -INFINITY;
-    for (int c = 0; c < n_chunks; ++c) mn = fmaxf(mn, p[(size_t)c * R_pad].x);
-    float L = 0.f;
-    if (mn != -INFINITY)
-      for (int c = 0; c < n_chunks; ++c) {
-        const float2 v = p[(size_t)c * R_pad];
-        L += v.y * exp2f((v.x - mn) * c2);
-      }
+    float mn = -INFINITY, L = 0.f;
+    for (int c0 = 0; c0 < n_chunks; c0 += MB) {
+      float2 v[MB];
+#pragma unroll
+      for (int i = 0; i < MB; ++i) v[i] = p[(size_t)min(c0 + i, n_chunks - 1) * R_pad];
+#pragma unroll
+      for (int i = 0; i < MB; ++i)
+        if (c0 + i >= n_chunks) v[i] = make_float2(-INFINITY, 0.f);   // no such chunk
+      float nm = mn;
+#pragma unroll
+      for (int i = 0; i < MB; ++i) nm = fmaxf(nm, v[i].x);
+      if (nm == -INFINITY) continue;
+      float add = 0.f;
+#pragma unroll
+      for (int i = 0; i < MB; ++i) add += v[i].y * exp2f((v[i].x - nm) * c2);
+      L = (mn == -INFINITY) ? add : fmaf(L, exp2f((mn - nm) * c2), add);
+      mn = nm;
+    }
     const float lse = (mn == -INFINITY) ? -INFINITY : fmaf(mn, sm_scale, logf(L));
     const int w = r / G, g = r % G;
     lse_out[((size_t)w * NS + s) * Hq + kv * G + g] = lse;

@@ -92,6 +92,7 @@ __device__ __forceinline__ int block_exscan(int v, int* lds, int* tot) {
 }
 
 constexpr int CP_NT = 256;
+constexpr int CP_PPT = 8;     // pages per thread in the plan's prefix (2048 pages per scan)
 
 __global__ __launch_bounds__(CP_NT) void compact_plan_kernel(
     const int32_t* __restrict__ n_pages, const uint16_t* __restrict__ masks,
@@ -117,13 +118,32 @@ __global__ __launch_bounds__(CP_NT) void compact_plan_kernel(
   const uint16_t* mrow = masks + (size_t)h * max_pages;
   const uint32_t* srow = sel_bits + (size_t)h * (max_pages / 2);
   int* off = w.page_off + (size_t)h * max_pages;
+  // selected slots per condensed page and their exclusive prefix: each thread takes CP_PPT
+  // consecutive pages (every load issued before any is used), one block scan per
+  // CP_NT * CP_PPT pages
   int carry = 0;
-  for (int base = 0; base < nc; base += CP_NT) {
-    const int pp = base + threadIdx.x;
-    const int c = (pp < nc) ? __popc((uint32_t)mrow[pp] & sel_word16(srow, pp)) : 0;
+  for (int base = 0; base < nc; base += CP_NT * CP_PPT) {
+    const int p0 = base + (int)threadIdx.x * CP_PPT;
+    uint32_t m[CP_PPT], sw[CP_PPT];
+#pragma unroll
+    for (int k = 0; k < CP_PPT; ++k) {
+      const int pp = min(p0 + k, nc - 1);
+      m[k] = mrow[pp];
+      sw[k] = sel_word16(srow, pp);
+    }
+    int c[CP_PPT], mine = 0;
+#pragma unroll
+    for (int k = 0; k < CP_PPT; ++k) {
+      c[k] = (p0 + k < nc) ? __popc(m[k] & sw[k]) : 0;
+      mine += c[k];
+    }
     int tot;
-    const int ex = block_exscan<CP_NT>(c, lds, &tot);
-    if (pp < nc) off[pp] = carry + ex;
+    int run = carry + block_exscan<CP_NT>(mine, lds, &tot);
+#pragma unroll
+    for (int k = 0; k < CP_PPT; ++k) {
+      if (p0 + k < nc) off[p0 + k] = run;
+      run += c[k];
+    }
     carry += tot;
   }
   int kept = 0;
@@ -351,9 +371,24 @@ __global__ __launch_bounds__(CP_NT) void compact_table_kernel(
   const uint32_t* srow = sel_bits + (size_t)h * (max_pages / 2);
   int32_t* old_id = reinterpret_cast<int32_t*>(smem);
   uint16_t* old_m = reinterpret_cast<uint16_t*>(old_id + max_pages);
-  for (int pp = threadIdx.x; pp < n; pp += CP_NT) {
-    old_id[pp] = trow[pp];
-    old_m[pp] = mrow[pp];
+  // the old row staged in LDS, CP_PPT pages per thread per pass, loads issued first
+  for (int b0 = 0; b0 < n; b0 += CP_NT * CP_PPT) {
+    int32_t id[CP_PPT];
+    uint16_t mk[CP_PPT];
+#pragma unroll
+    for (int k = 0; k < CP_PPT; ++k) {
+      const int pp = min(b0 + k * CP_NT + (int)threadIdx.x, n - 1);
+      id[k] = trow[pp];
+      mk[k] = mrow[pp];
+    }
+#pragma unroll
+    for (int k = 0; k < CP_PPT; ++k) {
+      const int pp = b0 + k * CP_NT + (int)threadIdx.x;
+      if (pp < n) {
+        old_id[pp] = id[k];
+        old_m[pp] = mk[k];
+      }
+    }
   }
   __syncthreads();
   const int* popped = free_ids + w.g->base + w.alloc_off[h];

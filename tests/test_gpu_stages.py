@@ -250,13 +250,18 @@ def test_topp_edge_cases(kind, S):
     sel = torch.empty(H, S // 32, dtype=torch.int32, device=DEV)
     k = torch.empty(H, dtype=torch.int32, device=DEV)
     st = torch.zeros(1, dtype=torch.int32, device=DEV)
-    hk.hk_topp_select(H, S, clt, None, ct, p, sel, k, k_min=kmin, k_max=kmax, status=st)
+    sm = torch.full((H,), float("nan"), device=DEV)
+    hk.hk_topp_select(H, S, clt, None, ct, p, sel, k, k_min=kmin, k_max=kmax, sel_mass=sm,
+                      status=st)
     torch.cuda.synchronize()
+    sm_np = sm.cpu().numpy()
     for h in range(H):
         cand = np.arange(S) < cand_len[h]
         r = O.topp_head(c[h], cand, p, k_min=kmin, k_max=kmax)
         assert int(k[h]) == r.k, (kind, h)
         assert np.array_equal(unpack_bits(np_i(sel[h]), S), r.sel), (kind, h)
+        # the selected fixed-point mass, exact, in units of 2^40 (rounded once to fp32)
+        assert sm_np[h] == np.float32(r.sel_mass / 2.0 ** 40), (kind, h, sm_np[h], r.sel_mass)
     flag = int(st.item())
     if kind == "nan_range":
         assert flag & hk.FLAG_NAN and flag & hk.FLAG_RANGE

@@ -436,10 +436,15 @@ __device__ __forceinline__ uint32_t cand_lanes(const BgLds& sh, int i) {
   return (uint32_t)((int32_t)(m << (31 - (tid & 15))) >> 31);
 }
 
+// v_writelane through its compiler intrinsic (which also keeps the wait states a
+// writelane needs after a VALU write of the scalar it reads, e.g. a ballot in vcc)
+extern "C" __device__ int hk_intrinsic_writelane(int value, int lane, int old)
+    __asm("llvm.amdgcn.writelane.i32");
+
 // Lane LANE of x takes the wave-uniform value s; the other lanes keep theirs.
 template <int LANE>
 __device__ __forceinline__ void write_lane(uint32_t& x, uint32_t s) {
-  x = ((threadIdx.x & 63) == LANE) ? s : x;
+  x = (uint32_t)hk_intrinsic_writelane((int)s, LANE, (int)x);
 }
 
 template <int I>

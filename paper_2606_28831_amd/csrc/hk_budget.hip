@@ -237,13 +237,13 @@ __device__ __forceinline__ int stage_list(const K* key, int pos, K prefix, BgLds
   const K m2 = ~low_mask<K>(pos);
   int cnt = 0;
 #pragma unroll
-  for (int i = 0; i < EPT; ++i) cnt += ((opaque(key[i]) & m2) == prefix) ? 1 : 0;
+  for (int i = 0; i < EPT; ++i) cnt += ((key[i] & m2) == prefix) ? 1 : 0;
   const int2 sc = block_exscan_bg(cnt, sh.redi);
   if (sc.y > CAP) return -1;
   int off = sc.x;
 #pragma unroll
   for (int i = 0; i < EPT; ++i) {
-    const K k = opaque(key[i]);
+    const K k = key[i];
     if ((k & m2) == prefix) list[off++] = k;
   }
   return sc.y;

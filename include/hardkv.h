@@ -257,7 +257,8 @@ hk_status hk_calibrate_solve_T_gd(int32_t n_heads, int32_t S_max, const int32_t*
  * (>= hk_workspace_size(HK_OP_COMPRESS, dims, max_pages) bytes, 256-byte aligned).
  * Outputs: k_out [n_heads] (the Top-p counts), sel_bits_out [n_heads][S_max/32] or NULL
  * (the selection is then kept in the workspace), status (HK_FLAG_* of every stage).
- * Arguments and errors as for the three calls it makes.
+ * Arguments and errors as for the three calls it makes (alloc->capacity >= kv->num_pages,
+ * checked before anything is launched).
  */
 hk_status hk_compress(const hk_dims* dims, const void* q_obs, const hk_paged_kv* kv,
                       int32_t L_dense, int32_t L_sparse, float sm_scale, const float* row_lse_in,
@@ -279,6 +280,8 @@ hk_status hk_compress(const hk_dims* dims, const void* q_obs, const hk_paged_kv*
  * Page ids are popped in head order before any is pushed, so the rewrite is out of place
  * and deterministic.  If the free list is too short, HK_FLAG_NOSPACE is raised and the
  * cache is left exactly as it was.
+ * alloc->capacity must be at least kv->num_pages (HK_ERR_ARG otherwise): the pages the
+ * rewrite frees are pushed onto the stack, which can then list every page of the pool.
  */
 hk_status hk_compact(const hk_dims* dims, const hk_paged_kv* kv, const uint32_t* sel_bits,
                      int32_t L_dense, int32_t L_sparse, const hk_allocator* alloc,
@@ -289,7 +292,8 @@ hk_status hk_compact(const hk_dims* dims, const hk_paged_kv* kv, const uint32_t*
  * ascending order (free_ids[i] = first_free + i), and *free_top = num_pages - first_free;
  * pages below first_free are taken (e.g. by the prompt).  Entries of free_ids past the
  * top are not written.  HK_ERR_ARG unless 0 <= first_free <= num_pages and
- * num_pages - first_free <= alloc->capacity.
+ * num_pages - first_free <= alloc->capacity.  (A stack that hk_compact,
+ * hk_compact_modes or hk_compress push onto needs capacity >= the pool's page count.)
  */
 hk_status hk_alloc_init(const hk_allocator* alloc, int32_t first_free, int32_t num_pages,
                         hipStream_t stream);
@@ -390,7 +394,8 @@ hk_status hk_budget_select(int32_t n_heads, int32_t S_max, const int32_t* cand_l
  *   SPARSE   every page before the dense tier is sparse (kept under the mask);
  *   KEEP     the row is left as it is (sel_bits is not read for it).
  * Workspace, allocator, ordering and HK_FLAG_NOSPACE behaviour as for hk_compact
- * (hk_workspace_size(HK_OP_COMPACT)).  head_mode [n_heads] int32 with values HK_BUDGET_*.
+ * (hk_workspace_size(HK_OP_COMPACT)), alloc->capacity >= kv->num_pages as there.
+ * head_mode [n_heads] int32 with values HK_BUDGET_*.
  */
 hk_status hk_compact_modes(const hk_dims* dims, const hk_paged_kv* kv, const uint32_t* sel_bits,
                            int32_t L_dense, const int32_t* head_mode, const hk_allocator* alloc,

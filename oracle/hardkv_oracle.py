@@ -581,7 +581,7 @@ def budget_select_head(cand, votes=None, c=None, sel_in=None, mode: int = REWRIT
                 preserves, Sec. 3.1 Tier 1, and that the paper's baselines retain, Sec. 4);
         base  = the other candidates, restricted to votes[j] >= 1 when votes are given
                 (the Cautious Update cumulative mask) and to sel_in[j] when given;
-        base is ranked by (votes desc, c desc, slot desc) -- "ranking on the votes", with
+        base is ranked by (votes desc, c desc, slot desc) -- the vote ranking of Sec. 3.1, with
         the calibrated probability and then recency breaking ties; absent keys count as 0
         and c is clamped to [0, 1] with NaN as 0, as in topp_head -- and its first
         min(|base|, cap) entries are kept, cap = max(0, k_cap - |sinks|) (no cap if k_cap < 0).

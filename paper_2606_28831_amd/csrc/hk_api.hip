@@ -242,8 +242,9 @@ hk_status hk_compact(const hk_dims* dims, const hk_paged_kv* kv, const uint32_t*
   hk_status e = check_dims(dims, false);
   if (e) return e;
   if ((e = check_kv(kv, true))) return e;
-  if (!sel_bits || !alloc || !alloc->free_ids || !alloc->free_top || alloc->capacity <= 0)
-    return HK_ERR_ARG;
+  if (!sel_bits || !alloc || !alloc->free_ids || !alloc->free_top) return HK_ERR_ARG;
+  // freed pages are pushed back: the stack must be able to hold every page of the pool
+  if (alloc->capacity < kv->num_pages) return HK_ERR_ARG;
   if (L_dense < 0 || L_sparse < 0) return HK_ERR_ARG;
   if ((long long)kv->max_pages * 6 > 160 * 1024) return HK_ERR_SHAPE;   // table row staged in LDS
   const int n_heads = dims->NS * dims->Hkv;
@@ -262,6 +263,8 @@ hk_status hk_compress(const hk_dims* dims, const void* q_obs, const hk_paged_kv*
   if (e) return e;
   if ((e = check_kv(kv, true))) return e;
   if (!k_out || !workspace) return HK_ERR_ARG;
+  if (!alloc || !alloc->free_ids || !alloc->free_top || alloc->capacity < kv->num_pages)
+    return HK_ERR_ARG;                                             // checked before any launch
   if (!(p >= 0.0 && p <= 1.0)) return HK_ERR_ARG;
   const CompressWs cw = compress_ws(dims, kv->max_pages);
   if (ws_bytes < cw.total) return HK_ERR_WORKSPACE;
@@ -292,8 +295,8 @@ hk_status hk_compact_modes(const hk_dims* dims, const hk_paged_kv* kv, const uin
   hk_status e = check_dims(dims, false);
   if (e) return e;
   if ((e = check_kv(kv, true))) return e;
-  if (!sel_bits || !head_mode || !alloc || !alloc->free_ids || !alloc->free_top || alloc->capacity <= 0)
-    return HK_ERR_ARG;
+  if (!sel_bits || !head_mode || !alloc || !alloc->free_ids || !alloc->free_top) return HK_ERR_ARG;
+  if (alloc->capacity < kv->num_pages) return HK_ERR_ARG;        // as for hk_compact
   if (L_dense < 0) return HK_ERR_ARG;
   if ((long long)kv->max_pages * 6 > 160 * 1024) return HK_ERR_SHAPE;
   const int n_heads = dims->NS * dims->Hkv;

@@ -89,6 +89,13 @@ def test_validation_errors_without_gpu(hk):
     assert L.hk_calibrate_solve_T(4, 128, P, None, P, P, P, 1e-4, 1e4, 0, P, None) == 1
     alloc = hk.hk_allocator(P, P, 64)
     assert L.hk_compact(C.byref(d), C.byref(kv), P, -1, 0, C.byref(alloc), P, P, 1 << 30, None) == 1
+    # a free stack shorter than the pool (64 pages) could overflow when the rewrite pushes
+    short = hk.hk_allocator(P, P, 63)
+    assert L.hk_compact(C.byref(d), C.byref(kv), P, 0, 0, C.byref(short), P, P, 1 << 30, None) == 1
+    assert L.hk_compact_modes(C.byref(d), C.byref(kv), P, 0, P, C.byref(short), P, P, 1 << 30,
+                              None) == 1
+    assert L.hk_compress(C.byref(d), P, C.byref(kv), 0, 0, 0.125, None, 0.9, 1, 0, C.byref(short),
+                         None, P, None, P, 1 << 30, None) == 1
     assert L.hk_compact(C.byref(d), C.byref(kv), P, 0, 0, C.byref(alloc), P, P, 16, None) == 5
     assert L.hk_decode_attn(C.byref(hk.dims(1, 12, 2, 128)), P, C.byref(kv), 0.1, P, P, P,
                             1 << 30, None) == 3              # group of 6 unsupported

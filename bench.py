@@ -329,60 +329,102 @@ def run_compression(args):
     return out
 
 
-def cpu_baseline(w, cfg, comp, args):
-    """The oracle, as it stands, on a bounded sample of heads of the same workload."""
+# ---------------------------------------------------------------- CPU baseline (the oracle)
+# A pool of worker processes, one per host core of this process's affinity mask, forked at
+# start-up before anything touches the GPU; each worker runs the oracle on one head at a time
+# with a single BLAS thread.
+_POOL = None
+_POOL_WORKERS = 0
+
+
+def _pool_init():
+    try:
+        from threadpoolctl import threadpool_limits
+        threadpool_limits(1)
+    except Exception:
+        pass
+
+
+def start_cpu_pool():
+    """Fork the oracle's worker pool (call before any GPU work)."""
+    global _POOL, _POOL_WORKERS
+    import multiprocessing as mp
+    _POOL_WORKERS = max(1, len(os.sched_getaffinity(0)))
+    _POOL = mp.get_context("fork").Pool(_POOL_WORKERS, initializer=_pool_init)
+
+
+def _blas_threads():
+    try:
+        from threadpoolctl import threadpool_info
+        return max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        return None
+
+
+def _oracle_chain_head(task):
+    """The whole step for one head with the oracle: score -> calibrate (-> redundancy,
+    temperature, mixture) -> Top-p -> rewrite, including the rewrite's row copies."""
     import numpy as np
 
     import oracle as O
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        threads = os.cpu_count() or 1
+    kh, vh, q, mask_h, n_h, refs, cfg, scale = task
+    t0 = time.perf_counter()
+    D = kh.shape[-1]
+    local = np.arange(n_h)
+    rows, valid = O.read_head(kh, local, mask_h, n_h)
+    nc, ns, nd = O.tier_pages(n_h, cfg["L_dense"], cfg["L_sparse"])
+    cand_len = 16 * (n_h - nd)
+    s, _ = O.score_head(q, rows, valid, cand_len, scale)
+    cand = O.candidate_mask(valid, cand_len)
+    c, _ = O.calibrate_head(s, cand)
+    if refs is not None:
+        xr = O.redundancy_head(rows, valid, cand_len, refs)
+        r0 = O.topp_head(c.astype(np.float32), cand, cfg["p"])
+        T = O.solve_T_head(xr, cand, r0.k, r0.sel_mass / 2.0 ** 40)
+        c = O.mix([c, O.calibrate_head(xr, cand, T)[0]], [0.5, 0.5])
+    r = O.topp_head(c.astype(np.float32), cand, cfg["p"])
+    res = O.compact_head(local, mask_h, n_h, r.sel, cfg["L_dense"], cfg["L_sparse"])
+    for ent in res.pages:
+        if ent.kind == "new":
+            src = [ph * 16 + t for ph, t in ent.src]
+            _ = kh.reshape(-1, D)[src].copy(), vh.reshape(-1, D)[src].copy()
+    return int(cand.sum()), time.perf_counter() - t0
+
+
+def cpu_baseline(w, cfg, comp, args):
+    """The oracle, as it stands, on a bounded sample of heads of the same workload, run by the
+    worker pool (one head per task); value = candidate slots of the sample / pool wall time."""
+    import numpy as np
     G = cfg["Hq"] // cfg["Hkv"]
     D = cfg["D"]
     scale = 1 / math.sqrt(D)
     pristine_table = w.page_table.cpu().numpy()
     masks = w.page_mask.cpu().numpy().astype(np.int64) & 0xFFFF
     n = w.n_pages.cpu().numpy()
-    budget_s = args.cpu_seconds
-    heads = list(range(0, w.n_heads, max(1, w.n_heads // 64)))
-    done_tokens, spent, used = 0, 0.0, []
+    heads = list(range(0, w.n_heads, max(1, w.n_heads // args.cpu_heads)))
+    small = {k: cfg[k] for k in ("L_dense", "L_sparse", "p")}
+    tasks = []
     for h in heads:
         ids = torch.tensor(pristine_table[h, :n[h]], dtype=torch.long, device=w.k_pool.device)
         kh = w.k_pool.index_select(0, ids).float().cpu().numpy()
         vh = w.v_pool.index_select(0, ids).float().cpu().numpy()
         s_, kv = divmod(h, cfg["Hkv"])
         q = w.q_obs[:, s_, kv * G:(kv + 1) * G].float().cpu().numpy().reshape(-1, D)
-        local = np.arange(n[h])
         refs = w.ref_slots[h].cpu().numpy() if w.ref_slots is not None else None
-        t0 = time.perf_counter()
-        rows, valid = O.read_head(kh, local, masks[h], int(n[h]))
-        nc, ns, nd = O.tier_pages(int(n[h]), cfg["L_dense"], cfg["L_sparse"])
-        cand_len = 16 * (int(n[h]) - nd)
-        s, _ = O.score_head(q, rows, valid, cand_len, scale)
-        cand = O.candidate_mask(valid, cand_len)
-        c, _ = O.calibrate_head(s, cand)
-        if refs is not None:
-            xr = O.redundancy_head(rows, valid, cand_len, refs)
-            r0 = O.topp_head(c.astype(np.float32), cand, cfg["p"])
-            T = O.solve_T_head(xr, cand, r0.k, r0.sel_mass / 2.0 ** 40)
-            c = O.mix([c, O.calibrate_head(xr, cand, T)[0]], [0.5, 0.5])
-        r = O.topp_head(c.astype(np.float32), cand, cfg["p"])
-        res = O.compact_head(local, masks[h], int(n[h]), r.sel, cfg["L_dense"], cfg["L_sparse"])
-        for ent in res.pages:
-            if ent.kind == "new":
-                src = [ph * 16 + t for ph, t in ent.src]
-                _ = kh.reshape(-1, D)[src].copy(), vh.reshape(-1, D)[src].copy()
-        spent += time.perf_counter() - t0
-        done_tokens += int(cand.sum())
-        used.append(h)
-        if spent >= budget_s:
-            break
-    return {"value": done_tokens / spent, "unit": "tokens/s", "cores": int(threads),
+        tasks.append((kh, vh, q, masks[h], int(n[h]), refs, small, scale))
+    t0 = time.perf_counter()
+    results = _POOL.map(_oracle_chain_head, tasks, chunksize=1)
+    wall = time.perf_counter() - t0
+    done_tokens = sum(r[0] for r in results)
+    busy = sum(r[1] for r in results)
+    return {"value": done_tokens / wall, "unit": "tokens/s", "cores": _POOL_WORKERS,
             "kind": "oracle",
-            "sample": f"{len(used)} of {w.n_heads} heads ({done_tokens} candidate slots), "
-                      f"full chain score->calibrate->Top-p->rewrite, {spent:.1f} s"}
+            "sample": f"{len(heads)} of {w.n_heads} heads ({done_tokens} candidate slots), full "
+                      f"chain score->calibrate->Top-p->rewrite, one head per task on "
+                      f"{_POOL_WORKERS} worker processes (1 BLAS thread each), {wall:.1f} s wall, "
+                      f"{busy:.1f} s of worker time",
+            "host_cpus": len(os.sched_getaffinity(0)), "blas_threads_per_worker": 1,
+            "serial_tokens_per_s": done_tokens / busy}
 
 
 def run_budget(args):
@@ -542,8 +584,10 @@ def cpu_baseline_budget(w, cfg, args):
     slots = float(cand.sum()) * done / R
     return {"value": slots / spent, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
             "sample": f"head 0: {done} of its {R} window rows (per-row probabilities and Top-p "
-                      f"vote over {int(cand.sum())} candidates), {spent:.1f} s; value = "
-                      f"candidate slots x rows done / rows per head / seconds"}
+                      f"vote over {int(cand.sum())} candidates), {spent:.1f} s in one process "
+                      f"(cores = its BLAS threads); value = candidate slots x rows done / rows "
+                      f"per head / seconds",
+            "host_cpus": len(os.sched_getaffinity(0))}
 
 
 def run_decode(args):
@@ -558,7 +602,7 @@ def run_decode(args):
     cfg = WL.config(5)
     L, B, Hq, Hkv, D, W = (cfg[k] for k in ("L", "B", "Hq", "Hkv", "D", "W"))
     T = cfg["compress_every"]
-    n_seg = args.steps if args.steps_given else cfg["decode_steps"] // T
+    n_seg = args.decode_segments if args.decode_segments else cfg["decode_steps"] // T
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
     max_pages = (cfg["N"] + cfg["decode_steps"]) // 16
@@ -646,6 +690,24 @@ def run_decode(args):
     }
 
 
+def decode_summary(d):
+    """The config-5 decode figures carried by the default bench line: decode tokens/s over the
+    stated segments and the dominant decode kernel against the HBM roofline."""
+    r = d.get("roofline") or {}
+    return {"workload": d["config"]["workload"], "segments": d["steps"],
+            "decode_steps": d["config"]["decode_steps"], "value": d["value"],
+            "unit": "decode tokens/s", "ms_per_segment": d["ms_per_step"],
+            "decode_attn_hbm_frac_lower_bound": d["decode_attn_hbm_frac_lower_bound"],
+            "roofline": {"kernel": r.get("kernel"), "bound": "hbm", "achieved": r.get("achieved"),
+                         "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": r.get("frac"),
+                         "traffic": r.get("traffic"), "traffic_source": r.get("traffic_source"),
+                         "bytes_per_launch": r.get("bytes_per_launch"),
+                         "avg_launch_ms": r.get("avg_launch_ms"),
+                         "launches_per_segment": r.get("launches_per_step"),
+                         "share_of_segment": r.get("share_of_step")},
+            "status_flags": d["status_flags"]}
+
+
 def run_crossover(args):
     """Sparse loading vs rewrite (Sec. 3.3.1 HA-Sparse vs HA-Max), re-created synthetically:
     per cache length and batch, the preparation time of each form (hk_compact with every
@@ -714,12 +776,19 @@ def run_crossover(args):
             sp, rw = out["sparse"], out["rewrite"]
             dd = sp["decode_ms"] - rw["decode_ms"]
             out["time_breakeven_steps"] = ((rw["prep_ms"] - sp["prep_ms"]) / dd) if dd > 0 else None
-            # memory-time integral (bytes x ms) from the compression on: the rewrite holds old
-            # and new pages while it runs, then only the new ones
-            mti_sp = lambda t: sp["bytes_held"] * (sp["prep_ms"] + t * sp["decode_ms"])
-            mti_rw = lambda t: ((pages_before + rw["new_pages"]) * page_bytes * rw["prep_ms"]
-                                + rw["bytes_held"] * t * rw["decode_ms"])
-            out["mti_breakeven_steps"] = next((t for t in range(0, 10001) if mti_rw(t) <= mti_sp(t)), None)
+            # memory-time integral (bytes x ms) from the compression on, as a function of the
+            # decode steps t that follow: A + B t.  The rewrite holds old and new pages while it
+            # runs, then only the new ones; sparse loading holds the old pages throughout.  The
+            # pay-back is the (fractional) t where the two lines cross.
+            a_sp, b_sp = sp["bytes_held"] * sp["prep_ms"], sp["bytes_held"] * sp["decode_ms"]
+            a_rw = (pages_before + rw["new_pages"]) * page_bytes * rw["prep_ms"]
+            b_rw = rw["bytes_held"] * rw["decode_ms"]
+            if a_rw <= a_sp:
+                out["mti_breakeven_steps"] = 0.0
+            elif b_sp > b_rw:
+                out["mti_breakeven_steps"] = (a_rw - a_sp) / (b_sp - b_rw)
+            else:
+                out["mti_breakeven_steps"] = None
             out["decode_speedup"] = sp["decode_ms"] / rw["decode_ms"]
             rows.append(out)
             print(json.dumps({k: out[k] for k in ("batch", "tokens", "decode_speedup", "time_breakeven_steps",
@@ -847,7 +916,14 @@ def main():
                          "(Step 4; not the bench line)")
     ap.add_argument("--graph", action="store_true",
                     help="config 5: replay each decode segment from one captured HIP graph")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="time budget of the serial hard-budget oracle baseline")
+    ap.add_argument("--cpu-heads", type=int, default=64,
+                    help="heads of the workload the oracle baseline runs (evenly spaced)")
+    ap.add_argument("--decode-segments", type=int, default=None,
+                    help="config-5 segments of 128 decode steps (default: all 32)")
+    ap.add_argument("--no-decode", action="store_true",
+                    help="leave the config-5 decode run out of the default bench line")
     ap.add_argument("--peaks", action="store_true",
                     help="only measure the exponential and bf16 MFMA rates (hk_probe)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -865,11 +941,25 @@ def main():
     args.steps_given = args.steps is not None
     if args.steps is None:
         args.steps = 20
+    if args.config == 5 and args.steps_given and args.decode_segments is None:
+        args.decode_segments = args.steps
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the compression step is independent per (sequence, KV "
               "head) and is benchmarked on a single MI355X; --gpus above 1 is not supported.",
               file=sys.stderr)
         sys.exit(2)
+    plain = not (args.copy_calibration or args.peaks or args.crossover or args.budget)
+    if plain and args.config != 5 and not args.no_cpu_baseline:
+        start_cpu_pool()          # forked now, before anything touches the GPU
+    try:
+        _main(args)
+    finally:
+        if _POOL is not None:
+            _POOL.terminate()
+            _POOL.join()
+
+
+def _main(args):
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
@@ -890,7 +980,14 @@ def main():
             args.steps = 10
         print(json.dumps(run_budget(args)), flush=True)
         return
-    out = run_decode(args) if args.config == 5 else run_compression(args)
+    if args.config == 5:
+        print(json.dumps(run_decode(args)), flush=True)
+        return
+    out = run_compression(args)
+    if args.config == 3 and not args.no_decode:
+        # the metric's second half, decode tokens/s, on config 5 (its own workload)
+        torch.cuda.empty_cache()
+        out["decode"] = decode_summary(run_decode(args))
     print(json.dumps(out), flush=True)
 
 

@@ -309,6 +309,17 @@ hk_status hk_decode_attn(const hk_dims* dims, const void* q, const hk_paged_kv* 
                          float sm_scale, float* o, float* lse, void* workspace,
                          size_t ws_bytes, hipStream_t stream);
 
+/* The split hk_decode_attn uses for these dims and table width (host only, no launch):
+ * every head's pages are shared by *n_split workgroups, none of which walks more than
+ * *pages_per_split pages (a full-width row is split into ranges of that many pages;
+ * shorter rows are spread over the same number of splits, at least 16 pages each).
+ * Larger head counts take longer splits (up to 128 pages) so that one launch offers the
+ * chip about 2048 workgroups.  HK_ERR_ARG for null outputs or max_pages <= 0; dims as for
+ * hk_decode_attn.
+ */
+hk_status hk_decode_plan(const hk_dims* dims, int32_t max_pages, int32_t* n_split,
+                         int32_t* pages_per_split);
+
 /* ------------------------------------------------------------------ a6: append
  * Append-only write of one decode step's K and V into the dense tier (Sec. 3.1 Step 1):
  * for each head the new token goes one past the highest valid slot of its newest page,

@@ -147,17 +147,16 @@ def redundancy_head(keys, valid, cand_len: int, ref_slots):
     norms = np.sqrt(np.sum(k * k, axis=1))
     cand = candidate_mask(valid, cand_len)
     out = np.full(S, -math.inf, dtype=np.float64)
-    refs = [int(i) for i in ref_slots]
+    refs = np.array([int(i) for i in ref_slots], dtype=np.int64)
     for j in np.nonzero(cand)[0]:
+        others = refs[refs != j]                 # the reference set without j itself
         best = -1.0
-        for i in refs:
-            if i == j:
-                continue
-            if norms[i] == 0.0 or norms[j] == 0.0:
-                cosv = 0.0
-            else:
-                cosv = float(np.dot(k[i], k[j]) / (norms[i] * norms[j]))
-            best = max(best, cosv)
+        if len(others):
+            denom = norms[others] * norms[j]
+            dots = k[others] @ k[j]
+            # a zero-norm key has cosine 0 with every other key
+            cosv = np.where(denom == 0.0, 0.0, dots / np.where(denom == 0.0, 1.0, denom))
+            best = max(best, float(np.max(cosv)))
         out[j] = -best
     return out
 

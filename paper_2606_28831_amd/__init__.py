@@ -20,7 +20,7 @@ __all__ = ["HardKVError", "lib", "PagedKV", "Allocator", "hk_score", "hk_calibra
            "hk_timing_enable", "hk_timing_read", "TIMED_KERNELS", "hk_calibrate_topp",
            "hk_pool_max", "hk_score_rows", "hk_vote_topp", "hk_budget_plan", "hk_budget_select",
            "hk_compact_modes", "hk_calibrate_solve_T_gd", "hk_alloc_init", "hk_compress", "OP_COMPRESS", "BUDGET_KEEP", "BUDGET_SPARSE", "BUDGET_REWRITE",
-           "hk_probe", "PROBE_EXP", "PROBE_MFMA"]
+           "hk_probe", "PROBE_EXP", "PROBE_MFMA", "hk_decode_plan"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhardkv.so")
 
@@ -34,7 +34,7 @@ EXPORTED = ["hk_score", "hk_calibrate", "hk_calibrate_solve_T", "hk_topp_select"
             "hk_timing_enable", "hk_timing_read", "hk_calibrate_topp", "hk_pool_max",
             "hk_score_rows", "hk_vote_topp", "hk_budget_plan", "hk_budget_select",
             "hk_compact_modes", "hk_calibrate_solve_T_gd", "hk_alloc_init", "hk_compress",
-            "hk_probe"]
+            "hk_probe", "hk_decode_plan"]
 # kernel ids of hk_timing_read, in header order
 TIMED_KERNELS = ["score_pass1", "score_merge", "score_pass2", "calibrate", "topp", "solve_T",
                  "compact_gather", "compact_meta", "decode_split", "decode_merge", "append",
@@ -120,6 +120,8 @@ def lib():
         L.hk_compress.restype = I32
         L.hk_compress.argtypes = [C.POINTER(hk_dims), P, C.POINTER(hk_paged_kv), I32, I32, F, P, D,
                                   I32, I32, C.POINTER(hk_allocator), P, P, P, P, SZ, P]
+        L.hk_decode_plan.restype = I32
+        L.hk_decode_plan.argtypes = [C.POINTER(hk_dims), I32, C.POINTER(I32), C.POINTER(I32)]
         L.hk_probe.restype = I32
         L.hk_probe.argtypes = [I32, I32, I32, P, P]
         L.hk_timing_enable.restype = I32
@@ -291,6 +293,14 @@ def hk_compact(d: hk_dims, kv: PagedKV, sel_bits, L_dense: int, L_sparse: int, a
 def hk_decode_attn(d: hk_dims, q, kv: PagedKV, sm_scale: float, o, lse, ws, stream=None):
     _check(lib().hk_decode_attn(C.byref(d), _ptr(q), C.byref(kv.desc), float(sm_scale), _ptr(o),
                                 _ptr(lse), _ptr(ws), ws.numel(), _stream(stream)), "hk_decode_attn")
+
+
+def hk_decode_plan(d: hk_dims, max_pages: int):
+    """(n_split, pages_per_split) that hk_decode_attn uses for these dims and table width."""
+    ns, pps = C.c_int32(0), C.c_int32(0)
+    _check(lib().hk_decode_plan(C.byref(d), int(max_pages), C.byref(ns), C.byref(pps)),
+           "hk_decode_plan")
+    return ns.value, pps.value
 
 
 def hk_append_kv(d: hk_dims, kv: PagedKV, k_new, v_new, alloc: Allocator, status, ws,

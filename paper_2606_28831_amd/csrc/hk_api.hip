@@ -389,6 +389,18 @@ hk_status hk_decode_attn(const hk_dims* dims, const void* q, const hk_paged_kv* 
                                    workspace, stream));
 }
 
+hk_status hk_decode_plan(const hk_dims* dims, int32_t max_pages, int32_t* n_split,
+                         int32_t* pages_per_split) {
+  hk_status e = check_dims(dims, false);
+  if (e) return e;
+  if (max_pages <= 0 || !n_split || !pages_per_split) return HK_ERR_ARG;
+  int pps, ns;
+  hk_decode_split_plan(dims->NS * dims->Hkv, max_pages, &pps, &ns);
+  *n_split = ns;
+  *pages_per_split = pps;
+  return HK_OK;
+}
+
 hk_status hk_append_kv(const hk_dims* dims, const hk_paged_kv* kv, const void* k_new,
                        const void* v_new, const hk_allocator* alloc, int32_t* status,
                        void* workspace, size_t ws_bytes, hipStream_t stream) {

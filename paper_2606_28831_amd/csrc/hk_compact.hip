@@ -198,37 +198,20 @@ __global__ __launch_bounds__(AL_NT) void compact_alloc_kernel(int n_heads, const
   }
 }
 
-#ifndef HK_GATHER_MODE
-#define HK_GATHER_MODE 1
-#endif
-#ifndef HK_GATHER_NTLD
-#define HK_GATHER_NTLD 1      // source rows are read once: nontemporal loads
-#endif
-#ifndef HK_GATHER_NT
-#define HK_GATHER_NT 1        // rewritten rows: nontemporal stores
-#endif
-
+// Source rows are read once and rewritten rows are not read again by this step:
+// nontemporal (streaming) loads and stores for both.
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ uint4 load16(const char* p) {
-#if HK_GATHER_NTLD
   return __builtin_bit_cast(uint4, __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p)));
-#else
-  return *reinterpret_cast<const uint4*>(p);
-#endif
 }
 __device__ __forceinline__ void store16(char* p, uint4 v) {
-#if HK_GATHER_NT
   __builtin_nontemporal_store(__builtin_bit_cast(u32x4, v), reinterpret_cast<u32x4*>(p));
-#else
-  *reinterpret_cast<uint4*>(p) = v;
-#endif
 }
 
-// Source-driven gather: one wave per condensed source page.  Mode 1 packs the page's
-// selected rows densely onto lane groups (row k of the selection goes to group k % RPI);
-// mode 2 maps lane groups to slots and issues all loads before any store.  A selected
-// slot of rank r (within the head's condensed band) lands in slot r % 16 of new page
-// r / 16, so consecutive ranks fill pages in order.
+// Source-driven gather: one wave per condensed source page, whose selected rows are
+// packed densely onto lane groups (row k of the selection goes to group k % RPI), all
+// loads issued before any store.  A selected slot of rank r (within the head's condensed
+// band) lands in slot r % 16 of new page r / 16, so consecutive ranks fill pages in order.
 template <int ROW_BYTES>
 __global__ __launch_bounds__(256) void compact_gather_kernel(
     char* __restrict__ k_pool, char* __restrict__ v_pool, const int32_t* __restrict__ table,
@@ -250,7 +233,6 @@ __global__ __launch_bounds__(256) void compact_gather_kernel(
   const size_t src_page = (size_t)table[(size_t)h * max_pages + pp];
   const int rank0 = w.page_off[(size_t)h * max_pages + pp];
   const int* popped = free_ids + w.g->base + w.alloc_off[h];
-#if HK_GATHER_MODE == 1
   const int nsel = __popc(m);
   uint4 kv[NI], vv[NI];
   int dst_slot[NI];
@@ -275,83 +257,6 @@ __global__ __launch_bounds__(256) void compact_gather_kernel(
       const size_t dst = ((size_t)popped[rank >> 4] * HK_PAGE + (rank & 15)) * ROW_BYTES + chunk * 16;
       store16(k_pool + dst, kv[i]);
       store16(v_pool + dst, vv[i]);
-    }
-  }
-#else
-  uint4 kv[NI], vv[NI];
-#pragma unroll
-  for (int i = 0; i < NI; ++i) {
-    const int t = i * RPI + sub;
-    if ((m >> t) & 1u) {
-      const size_t src = (src_page * HK_PAGE + t) * ROW_BYTES + chunk * 16;
-      kv[i] = load16(k_pool + src);
-      vv[i] = load16(v_pool + src);
-    }
-  }
-#pragma unroll
-  for (int i = 0; i < NI; ++i) {
-    const int t = i * RPI + sub;
-    if ((m >> t) & 1u) {
-      const int rank = rank0 + __popc(m & ((1u << t) - 1u));
-      const size_t dst = ((size_t)popped[rank >> 4] * HK_PAGE + (rank & 15)) * ROW_BYTES + chunk * 16;
-      store16(k_pool + dst, kv[i]);
-      store16(v_pool + dst, vv[i]);
-    }
-  }
-#endif
-}
-
-// Destination-driven gather: one wave per new condensed page, which it writes whole
-// (16 contiguous rows of K and of V).  The source of rank r is found by a binary search
-// over the per-page exclusive prefix of selected counts, then the (r - prefix)-th
-// selected slot of that page.
-template <int ROW_BYTES>
-__global__ __launch_bounds__(256) void compact_gather_dst_kernel(
-    char* __restrict__ k_pool, char* __restrict__ v_pool, const int32_t* __restrict__ table,
-    const uint16_t* __restrict__ masks, const uint32_t* __restrict__ sel_bits,
-    const int32_t* __restrict__ free_ids, int max_pages, CompactWs w) {
-  if (!w.g->ok) return;
-  const int h = blockIdx.y;
-  const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const HeadPlan p = w.plan[h];
-  if (i >= p.npc) return;
-  const int lane = threadIdx.x & 63;
-  constexpr int LPR = ROW_BYTES / 16;
-  constexpr int RPI = 64 / LPR;
-  constexpr int NI = HK_PAGE / RPI;
-  const int sub = lane / LPR, chunk = lane % LPR;
-  const int* off = w.page_off + (size_t)h * max_pages;
-  const uint16_t* mrow = masks + (size_t)h * max_pages;
-  const uint32_t* srow = sel_bits + (size_t)h * (max_pages / 2);
-  const int32_t* trow = table + (size_t)h * max_pages;
-  const size_t dst_page = (size_t)free_ids[w.g->base + w.alloc_off[h] + i];
-  uint4 kv[NI], vv[NI];
-#pragma unroll
-  for (int j = 0; j < NI; ++j) {
-    const int row = j * RPI + sub;
-    const int rank = i * HK_PAGE + row;
-    if (rank < p.cnt_c) {
-      int lo = 0, hi = p.nc - 1;             // largest pp with off[pp] <= rank
-      while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (off[mid] <= rank) lo = mid;
-        else hi = mid - 1;
-      }
-      uint32_t mm = (uint32_t)mrow[lo] & sel_word16(srow, lo);
-      for (int k = rank - off[lo]; k > 0; --k) mm &= mm - 1u;
-      const int t = __ffs(mm) - 1;
-      const size_t src = ((size_t)trow[lo] * HK_PAGE + t) * ROW_BYTES + chunk * 16;
-      kv[j] = *reinterpret_cast<const uint4*>(k_pool + src);
-      vv[j] = *reinterpret_cast<const uint4*>(v_pool + src);
-    }
-  }
-#pragma unroll
-  for (int j = 0; j < NI; ++j) {
-    const int row = j * RPI + sub;
-    if (i * HK_PAGE + row < p.cnt_c) {
-      const size_t dst = (dst_page * HK_PAGE + row) * ROW_BYTES + chunk * 16;
-      store16(k_pool + dst, kv[j]);
-      store16(v_pool + dst, vv[j]);
     }
   }
 }
@@ -487,17 +392,12 @@ hipError_t hk_launch_compact(int n_heads, int D, const hk_paged_kv* kv, const ui
   dim3 gg((mp + 3) / 4, n_heads);
   char* kp = static_cast<char*>(kv->k_pool);
   char* vp = static_cast<char*>(kv->v_pool);
-#if HK_GATHER_MODE == 3
-#define HK_GATHER_K compact_gather_dst_kernel
-#else
-#define HK_GATHER_K compact_gather_kernel
-#endif
   {
   TimedLaunch t(HK_TK_COMPACT_GATHER, st);
   switch (row_bytes) {
-    case 128: hipLaunchKernelGGL((HK_GATHER_K<128>), gg, dim3(256), 0, st, kp, vp, kv->page_table, kv->page_mask, sel_bits, alloc->free_ids, mp, w); break;
-    case 256: hipLaunchKernelGGL((HK_GATHER_K<256>), gg, dim3(256), 0, st, kp, vp, kv->page_table, kv->page_mask, sel_bits, alloc->free_ids, mp, w); break;
-    default: hipLaunchKernelGGL((HK_GATHER_K<512>), gg, dim3(256), 0, st, kp, vp, kv->page_table, kv->page_mask, sel_bits, alloc->free_ids, mp, w); break;
+    case 128: hipLaunchKernelGGL((compact_gather_kernel<128>), gg, dim3(256), 0, st, kp, vp, kv->page_table, kv->page_mask, sel_bits, alloc->free_ids, mp, w); break;
+    case 256: hipLaunchKernelGGL((compact_gather_kernel<256>), gg, dim3(256), 0, st, kp, vp, kv->page_table, kv->page_mask, sel_bits, alloc->free_ids, mp, w); break;
+    default: hipLaunchKernelGGL((compact_gather_kernel<512>), gg, dim3(256), 0, st, kp, vp, kv->page_table, kv->page_mask, sel_bits, alloc->free_ids, mp, w); break;
   }
   }
   const size_t lds = (size_t)mp * (sizeof(int32_t) + sizeof(uint16_t));

@@ -18,39 +18,14 @@
 
 namespace hk {
 
-#ifndef HK_DEC_PPS
-#define HK_DEC_PPS 128        // most pages per split (one workgroup)
-#endif
-#ifndef HK_DEC_QLDS
-#define HK_DEC_QLDS 1         // 0: the G query rows live in registers instead of LDS
-#endif
-#ifndef HK_DEC_PREFETCH
-#define HK_DEC_PREFETCH 1     // load the wave's next page while computing the current one
-#endif
-
-#ifndef HK_DEC_NT
-#define HK_DEC_NT 256
-#endif
-constexpr int DEC_NT = HK_DEC_NT;
+constexpr int DEC_NT = 256;                 // threads per workgroup
 constexpr int DEC_NW = DEC_NT / 64;
-constexpr int DEC_PPS = HK_DEC_PPS;
+constexpr int DEC_PPS = 128;                // most pages per split (one workgroup)
 constexpr int DEC_PPS_MIN = 16;             // fewest pages per split
 constexpr int DEC_TARGET_WG = 2048;         // workgroups a launch should offer the chip
 
-#ifndef HK_DEC_NTLD
-#define HK_DEC_NTLD 0         // 1: K and V pages are read with nontemporal loads
-#endif
-#ifndef HK_DEC_WPE
-#define HK_DEC_WPE 0
-#endif
-#if HK_DEC_WPE > 0
-#define HK_DEC_ATTR __launch_bounds__(DEC_NT) __attribute__((amdgpu_waves_per_eu(HK_DEC_WPE, HK_DEC_WPE)))
-#else
-#define HK_DEC_ATTR __launch_bounds__(DEC_NT)
-#endif
-
 template <typename T, int D, int G>
-__global__ HK_DEC_ATTR void decode_split_kernel(
+__global__ __launch_bounds__(DEC_NT) void decode_split_kernel(
     const T* __restrict__ q, const T* __restrict__ k_pool, const T* __restrict__ v_pool,
     const int32_t* __restrict__ table, const uint16_t* __restrict__ masks,
     const int32_t* __restrict__ n_pages_arr, int Hq, int Hkv, int max_pages, float c2,
@@ -76,7 +51,6 @@ __global__ HK_DEC_ATTR void decode_split_kernel(
   const int t = lane >> 2, c = lane & 3;
   const int kg = lane / LPR, dc = lane % LPR;
 
-#if HK_DEC_QLDS
   // the G query rows of this KV head (contiguous in q), 16 bytes per thread
   __shared__ uint4 s_q[G * D * ES / 16];
   {
@@ -88,22 +62,6 @@ __global__ HK_DEC_ATTR void decode_split_kernel(
     const uint4 u = s_q[(g * D * ES + c * DQ * ES) / 16 + i / 4];
     return (i & 3) == 0 ? u.x : (i & 3) == 1 ? u.y : (i & 3) == 2 ? u.z : u.w;
   };
-#else
-  uint32_t qw[G][QW];
-#pragma unroll
-  for (int g = 0; g < G; ++g) {
-    const uint4* src = reinterpret_cast<const uint4*>(q + ((size_t)s * Hq + kv * G + g) * D + c * DQ);
-#pragma unroll
-    for (int i = 0; i < QW / 4; ++i) {
-      const uint4 u = src[i];
-      qw[g][4 * i + 0] = u.x;
-      qw[g][4 * i + 1] = u.y;
-      qw[g][4 * i + 2] = u.z;
-      qw[g][4 * i + 3] = u.w;
-    }
-  }
-  auto q_word = [&](int g, int i) -> uint32_t { return qw[g][i]; };
-#endif
   float m_run[G], l_part[G], o[G][VEC];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
@@ -124,19 +82,11 @@ __global__ HK_DEC_ATTR void decode_split_kernel(
     r.m16 = mrow[p];
     const size_t page = (size_t)trow[p] * HK_PAGE;
     const uint4* ks = reinterpret_cast<const uint4*>(k_pool + (page + t) * D + c * DQ);
-    auto ld = [](const uint4* a) -> uint4 {
-#if HK_DEC_NTLD
-      typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-      return __builtin_bit_cast(uint4, __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(a)));
-#else
-      return *a;
-#endif
-    };
 #pragma unroll
-    for (int i = 0; i < QW / 4; ++i) r.k[i] = ld(ks + i);
+    for (int i = 0; i < QW / 4; ++i) r.k[i] = ks[i];
 #pragma unroll
     for (int i = 0; i < KPL; ++i)
-      r.v[i] = ld(reinterpret_cast<const uint4*>(v_pool + (page + kg * KPL + i) * D + dc * VEC));
+      r.v[i] = *reinterpret_cast<const uint4*>(v_pool + (page + kg * KPL + i) * D + dc * VEC);
   };
   auto process_page = [&](const PageRegs& r) {
     const uint32_t m16 = r.m16;
@@ -210,27 +160,21 @@ __global__ HK_DEC_ATTR void decode_split_kernel(
     }
   };
 
+  // the wave's next page is loaded (into the other register set) before the current one
+  // is processed; the loop is unrolled by two so both sets stay in registers
   int p = p_begin + wave;
-  if constexpr (HK_DEC_PREFETCH) {
-    PageRegs ra, rb;
-    if (p < p_end) load_page(ra, p);
-    while (p < p_end) {
-      int pn = p + DEC_NW;
-      if (pn < p_end) load_page(rb, pn);
-      process_page(ra);
-      p = pn;
-      if (p >= p_end) break;
-      pn = p + DEC_NW;
-      if (pn < p_end) load_page(ra, pn);
-      process_page(rb);
-      p = pn;
-    }
-  } else {
-    for (; p < p_end; p += DEC_NW) {
-      PageRegs r;
-      load_page(r, p);
-      process_page(r);
-    }
+  PageRegs ra, rb;
+  if (p < p_end) load_page(ra, p);
+  while (p < p_end) {
+    int pn = p + DEC_NW;
+    if (pn < p_end) load_page(rb, pn);
+    process_page(ra);
+    p = pn;
+    if (p >= p_end) break;
+    pn = p + DEC_NW;
+    if (pn < p_end) load_page(ra, pn);
+    process_page(rb);
+    p = pn;
   }
   // reduce over slot groups (lanes with the same value chunk) and over all lanes for l
 #pragma unroll
@@ -492,30 +436,37 @@ size_t hk_decode_ws(int NS, int Hq, int Hkv, int D, int max_pages) {
   return (size_t)NS * Hkv * n_split * G * (D + 2) * sizeof(float);
 }
 
-hipError_t hk_launch_decode(int NS, int Hq, int Hkv, int D, const void* q, const hk_paged_kv* kv,
-                            float sm_scale, float* o, float* lse, void* ws, hipStream_t st) {
-  const int G = Hq / Hkv, n_heads = NS * Hkv;
+void hk_decode_split_plan(int n_heads, int max_pages, int* pps_out, int* n_split_out) {
   // pages per split: the most (DEC_PPS) that still gives the launch DEC_TARGET_WG
   // workgroups, down to DEC_PPS_MIN -- few heads get short splits, so no wave walks a
   // long serial chain of pages
   int pps = DEC_PPS;
-  while (pps > DEC_PPS_MIN && (long long)n_heads * ((kv->max_pages + pps - 1) / pps) < DEC_TARGET_WG)
+  while (pps > DEC_PPS_MIN && (long long)n_heads * ((max_pages + pps - 1) / pps) < DEC_TARGET_WG)
     pps >>= 1;
-  const int n_split = (kv->max_pages + pps - 1) / pps;
+  *pps_out = pps;
+  *n_split_out = (max_pages + pps - 1) / pps;
+}
+
+hipError_t hk_launch_decode(int NS, int Hq, int Hkv, int D, const void* q, const hk_paged_kv* kv,
+                            float sm_scale, float* o, float* lse, void* ws, hipStream_t st,
+                            bool timed) {
+  const int G = Hq / Hkv, n_heads = NS * Hkv;
+  int pps, n_split;
+  hk_decode_split_plan(n_heads, kv->max_pages, &pps, &n_split);
   const float c2 = sm_scale * kLog2e;
   float* part = static_cast<float*>(ws);
   dim3 grid(n_split, n_heads);
   const bool bf = kv->dtype == HK_BF16;
   bool ok;
   {
-  TimedLaunch t(HK_TK_DECODE_SPLIT, st);
+  TimedLaunch t(timed ? HK_TK_DECODE_SPLIT : -1, st);
   if (bf && D == 128) ok = launch_split_g<uint16_t, 128>(G, grid, st, q, kv, Hq, Hkv, c2, part, n_split, pps);
   else if (bf) ok = launch_split_g<uint16_t, 64>(G, grid, st, q, kv, Hq, Hkv, c2, part, n_split, pps);
   else if (D == 128) ok = launch_split_g<float, 128>(G, grid, st, q, kv, Hq, Hkv, c2, part, n_split, pps);
   else ok = launch_split_g<float, 64>(G, grid, st, q, kv, Hq, Hkv, c2, part, n_split, pps);
   }
   if (!ok) return hipErrorInvalidValue;
-  TimedLaunch t(HK_TK_DECODE_MERGE, st);
+  TimedLaunch t(timed ? HK_TK_DECODE_MERGE : -1, st);
   if (D == 128)
     hipLaunchKernelGGL(decode_merge_kernel<128>, dim3(n_heads), dim3(256), 0, st, part, n_split, G,
                        Hq, Hkv, o, lse);

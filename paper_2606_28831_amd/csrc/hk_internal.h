@@ -245,8 +245,10 @@ hipError_t hk_launch_alloc_init(int32_t* free_ids, int32_t* free_top, int first_
                                 hipStream_t st);
 
 hipError_t hk_launch_decode(int NS, int Hq, int Hkv, int D, const void* q, const hk_paged_kv* kv,
-                            float sm_scale, float* o, float* lse, void* ws, hipStream_t st);
+                            float sm_scale, float* o, float* lse, void* ws, hipStream_t st,
+                            bool timed = true);
 size_t hk_decode_ws(int NS, int Hq, int Hkv, int D, int max_pages);
+void hk_decode_split_plan(int n_heads, int max_pages, int* pps_out, int* n_split_out);
 
 hipError_t hk_launch_append(int NS, int Hkv, int D, const hk_paged_kv* kv, const void* k_new,
                             const void* v_new, const hk_allocator* alloc, int32_t* status,

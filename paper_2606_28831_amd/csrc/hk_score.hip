@@ -142,38 +142,11 @@ __device__ __forceinline__ void stage_rows(char* lds, int R, int R_pad, RowFn ro
   }
 }
 
-#ifndef HK_SCORE_QD
-#define HK_SCORE_QD 2     // Q fragments read from LDS this many MFMA steps ahead
-#endif
-#ifndef HK_SCORE_NT
-#define HK_SCORE_NT 512
-#endif
-#ifndef HK_SCORE_PPW
-#define HK_SCORE_PPW 128
-#endif
-#ifndef HK_SCORE_PREFETCH
-#define HK_SCORE_PREFETCH 0
-#endif
-#ifndef HK_SCORE_WPE
-#define HK_SCORE_WPE 0
-#endif
-#ifndef HK_SCORE_KT
-#define HK_SCORE_KT 1
-#endif
-#ifndef HK_SCORE_PIPE
-#define HK_SCORE_PIPE 1
-#endif
-#if HK_SCORE_WPE > 0
-#define HK_SCORE_ATTR __launch_bounds__(SCORE_NT) __attribute__((amdgpu_waves_per_eu(HK_SCORE_WPE, HK_SCORE_WPE)))
-#else
-#define HK_SCORE_ATTR __launch_bounds__(SCORE_NT)
-#endif
-
-constexpr int SCORE_NT = HK_SCORE_NT;      // threads per workgroup
-constexpr int SCORE_QD = HK_SCORE_QD;
+constexpr int SCORE_NT = 512;              // threads per workgroup
+constexpr int SCORE_QD = 2;                // Q fragments read from LDS this many MFMA steps ahead
 constexpr int SCORE_NW = SCORE_NT / 64;
-constexpr int SCORE_PPW = HK_SCORE_PPW;    // pages per workgroup
-constexpr int SCORE_KT = HK_SCORE_KT;      // 32-key tiles a wave holds at once
+constexpr int SCORE_PPW = 128;             // pages per workgroup
+constexpr int SCORE_KT = 1;                // 32-key tiles a wave holds at once
 constexpr int SCORE_WPP = 2 * SCORE_KT;    // pages per wave iteration
 constexpr int NREF_MAX = 256;
 
@@ -474,38 +447,21 @@ __device__ __forceinline__ uint32_t lane_rows(uint32_t tmask, int lane) {
 }
 
 
-// Walk a wave's tiles p0, p0 + step, ...  With prefetch, the next tile's K fragments are
-// loaded (into a second register set) before the current tile is processed; the loop is
-// unrolled by two so both sets stay in registers.
+// Walk a wave's tiles p0, p0 + step, ...: load the tile's K fragments, then process them
+// (the other waves of the CU cover the load latency).
 template <typename F, typename LoadFn, typename ProcFn>
 __device__ __forceinline__ void tile_loop(LoadFn load_group, ProcFn process, int p0, int p_end,
                                           int step) {
-  if constexpr (HK_SCORE_PREFETCH) {
-    F ka[SCORE_KT], kb[SCORE_KT];
-    if (p0 < p_end) load_group(ka, p0);
-    while (p0 < p_end) {
-      int pn = p0 + step;
-      if (pn < p_end) load_group(kb, pn);
-      process(ka, p0);
-      p0 = pn;
-      if (p0 >= p_end) break;
-      pn = p0 + step;
-      if (pn < p_end) load_group(ka, pn);
-      process(kb, p0);
-      p0 = pn;
-    }
-  } else {
-    for (; p0 < p_end; p0 += step) {
-      F kf[SCORE_KT];
-      load_group(kf, p0);
-      process(kf, p0);
-    }
+  for (; p0 < p_end; p0 += step) {
+    F kf[SCORE_KT];
+    load_group(kf, p0);
+    process(kf, p0);
   }
 }
 
 // ------------------------------------------------------------------ pass 1
 template <typename T, int D, int QB>
-__global__ HK_SCORE_ATTR void score_pass1_kernel(
+__global__ __launch_bounds__(SCORE_NT) void score_pass1_kernel(
     const T* __restrict__ q_obs, const T* __restrict__ k_pool, const int32_t* __restrict__ table,
     const uint16_t* __restrict__ masks, const int32_t* __restrict__ n_pages_arr, int NS, int Hq,
     int Hkv, int W, int max_pages, float c2, float2* __restrict__ part, int n_chunks) {
@@ -546,28 +502,8 @@ __global__ HK_SCORE_ATTR void score_pass1_kernel(
       all_full = all_full && (tm[t] == 0xffffffffu);
       any = any || (tm[t] != 0u);
     }
-    if (all_full && HK_SCORE_PIPE) {
+    if (all_full) {
       p1_tile_pipelined<F, QB, SCORE_KT>(kf, smem, c2, lane, M, L);
-    } else if (all_full) {
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb) {
-        f32x16 acc[SCORE_KT];
-        mma_chains<F, false, SCORE_KT>(kf, smem, qb, lane, acc);
-        float m = acc[0][0];
-#pragma unroll
-        for (int t = 0; t < SCORE_KT; ++t)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) m = vmax(m, acc[t][r]);
-        const float mn = vmax(M[qb], m);
-        const float mc = mn * c2;
-        float sum = 0.f;
-#pragma unroll
-        for (int t = 0; t < SCORE_KT; ++t)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) sum += fast_exp2(fmaf(acc[t][r], c2, -mc));
-        L[qb] = fmaf(L[qb], fast_exp2((M[qb] - mn) * c2), sum);
-        M[qb] = mn;
-      }
     } else if (any) {
       uint32_t rows[SCORE_KT];
 #pragma unroll
@@ -668,8 +604,7 @@ __global__ __launch_bounds__(256) void score_lse_merge_kernel(const float2* __re
 // (The 1024-thread redundancy shape already caps registers at 128.)
 template <typename T, int D, int QB, bool RED>
 constexpr int pass2_min_waves() {
-  if (HK_SCORE_WPE > 0) return HK_SCORE_WPE;
-  if (HK_SCORE_KT > 1 || RED) return 1;
+  if (SCORE_KT > 1 || RED) return 1;
   return (sizeof(T) == 2 && D == 128 && (QB == 7 || QB == 4)) ? 4 : 1;
 }
 
@@ -810,23 +745,7 @@ void score_pass2_kernel(
     float col[SCORE_KT];
 #pragma unroll
     for (int t = 0; t < SCORE_KT; ++t) col[t] = 0.f;
-    if (any && HK_SCORE_PIPE) {
-      p2_tile_pipelined<F, QB, SCORE_KT>(kf, smem, lse2, c2, lane, col);
-    } else if (any) {
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb) {
-        f32x16 acc[SCORE_KT];
-        mma_chains<F, true, SCORE_KT>(kf, smem, qb, lane, acc);
-#pragma unroll
-        for (int r4 = 0; r4 < 4; ++r4) {
-          const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse2 + qb * 32 + 8 * r4 + 4 * (lane >> 5));
-#pragma unroll
-          for (int t = 0; t < SCORE_KT; ++t)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) col[t] += fast_exp2(fmaf(acc[t][4 * r4 + i], c2, -l4[i]));
-        }
-      }
-    }
+    if (any) p2_tile_pipelined<F, QB, SCORE_KT>(kf, smem, lse2, c2, lane, col);
 #pragma unroll
     for (int t = 0; t < SCORE_KT; ++t) {
       const int pg = p0 + 2 * t + (kl >> 4);

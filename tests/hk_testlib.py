@@ -191,3 +191,124 @@ def rewritten_sources(table_row, mask_row, n_pages, sel, n_condensed):
             if (m >> t) & 1 and sel[pp * 16 + t]:
                 out.append((int(table_row[pp]), t))
     return out
+
+
+class DecodeReplay:
+    """Host model of a decode loop's cache (append, decode attention, periodic compression)
+    for a set of heads, built on the oracle: per head its pages in logical order with their
+    16-slot masks and K/V rows.  Each step appends a row where the oracle's append_position
+    puts it and returns the oracle's decode attention over the valid slots; each compression
+    checks the GPU's scores and selection against the model and then applies the oracle's
+    compact_head with the GPU's selection.  Heads are (layer, sequence, KV head) rows of the
+    loop's cache, h // Hkv the sequence s.  Step inputs are host arrays [n, H*, D] whose row
+    sidx[s] holds sequence s (sidx=None: row s)."""
+
+    def __init__(self, w, heads, Hkv, G, D, scale, max_pages):
+        self.heads, self.Hkv, self.G, self.D, self.scale = list(heads), Hkv, G, D, scale
+        host = HostCache(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages, heads=self.heads)
+        self.K, self.V, self.mask, self.n = {}, {}, {}, {}
+        for h in self.heads:
+            n = int(host.n[h])
+            K, _ = host.head(h)
+            V, _ = host.head_v(h)
+            self.K[h] = np.zeros((max_pages, 16, D))
+            self.V[h] = np.zeros((max_pages, 16, D))
+            self.K[h][:n], self.V[h][:n] = K.reshape(n, 16, D), V.reshape(n, 16, D)
+            self.mask[h] = [int(m) for m in host.mask[h][:n]]
+            self.n[h] = n
+        self._pack()
+
+    def _pack(self):
+        # the valid rows in logical order (an append always lands after every valid slot,
+        # and a rewrite keeps the order), which decode attention reads
+        self.RK, self.RV, self.nr = {}, {}, {}
+        for h in self.heads:
+            K, valid = self.head(h)
+            V, _ = self.head_v(h)
+            cap = 16 * self.K[h].shape[0]
+            self.RK[h], self.RV[h] = np.zeros((cap, self.D)), np.zeros((cap, self.D))
+            nv = int(valid.sum())
+            self.RK[h][:nv], self.RV[h][:nv] = K[valid], V[valid]
+            self.nr[h] = nv
+
+    def head(self, h):
+        """(K rows of every slot [16 n, D], validity [16 n]) of head h."""
+        n = self.n[h]
+        valid = ((np.array(self.mask[h], np.int64)[:, None] >> np.arange(16)) & 1).reshape(-1).astype(bool)
+        return self.K[h][:n].reshape(-1, self.D), valid
+
+    def head_v(self, h):
+        return self.V[h][:self.n[h]].reshape(-1, self.D), self.head(h)[1]
+
+    def step(self, q_t, k_t, v_t, sidx=None, decode=True):
+        """Append one step's rows and (decode=True) return the oracle's decode output and LSE
+        of every modelled head for that step's queries: {h: (o [G, D], lse [G])}."""
+        out = {}
+        for h in self.heads:
+            s, kvh = divmod(h, self.Hkv)
+            r = s if sidx is None else sidx[s]
+            pos, slot, new = O.append_position(self.mask[h], self.n[h])
+            if new:
+                self.mask[h].append(0)
+                self.n[h] += 1
+            self.K[h][pos, slot], self.V[h][pos, slot] = k_t[r, kvh], v_t[r, kvh]
+            self.mask[h][pos] |= 1 << slot
+            nr = self.nr[h]
+            self.RK[h][nr], self.RV[h][nr] = k_t[r, kvh], v_t[r, kvh]
+            self.nr[h] = nr + 1
+            if decode:
+                out[h] = O.decode_head(np.asarray(q_t[r, kvh * self.G:(kvh + 1) * self.G], np.float64),
+                                       self.RK[h][:nr + 1], self.RV[h][:nr + 1], np.ones(nr + 1, bool),
+                                       self.scale)
+        return out
+
+    def check_cache(self, w, what):
+        """The GPU cache equals the model: page counts and masks exactly, K and V of every
+        valid slot byte for byte."""
+        now = HostCache(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages, heads=self.heads)
+        for h in self.heads:
+            n = self.n[h]
+            assert int(now.n[h]) == n, f"{what}: head {h} has {int(now.n[h])} pages, model {n}"
+            assert [int(m) for m in now.mask[h][:n]] == self.mask[h], f"{what}: masks of head {h}"
+            K, valid = now.head(h)
+            V, _ = now.head_v(h)
+            Km, vm = self.head(h)
+            Vm, _ = self.head_v(h)
+            assert np.array_equal(K[valid], Km[vm]) and np.array_equal(V[valid], Vm[vm]), \
+                f"{what}: K/V rows of head {h} differ from the model"
+
+    def compress(self, q_win, lse_win, s_gpu, c_gpu, sel_gpu, k_gpu, L_dense, p, S, what, sidx=None):
+        """One compression of every modelled head (the model holds the cache the compression
+        saw): the GPU scores (single pass over the decode LSEs) against the oracle's score fed
+        the oracle's own window LSEs, and the GPU's selection by the Top-p rule on its own
+        probabilities; the model is then rewritten by the oracle's compact_head with that
+        selection.  q_win [W, n, Hq, D] host; lse_win {h: [W, G]} oracle LSEs; s_gpu, c_gpu,
+        sel_gpu: {h: the head's row}; k_gpu [n_heads]."""
+        for h in self.heads:
+            s, kvh = divmod(h, self.Hkv)
+            r = s if sidx is None else sidx[s]
+            n = self.n[h]
+            Kfull, valid = self.head(h)
+            nd = O.tier_pages(n, L_dense, 0)[2]
+            cand_len = 16 * (n - nd)
+            q_rows_h = np.asarray(q_win[:, r, kvh * self.G:(kvh + 1) * self.G], np.float64).reshape(-1, self.D)
+            s_ref, _ = O.score_head(q_rows_h, Kfull, valid, cand_len, self.scale,
+                                    row_lse_in=np.asarray(lse_win[h]).reshape(-1))
+            full = np.full(S, -np.inf)
+            full[:len(s_ref)] = s_ref
+            check_log_scores(s_gpu[h], full, 2e-3, f"{what}: score head {h}")
+            cand = np.zeros(S, bool)
+            cand[:len(valid)] = O.candidate_mask(valid, cand_len)
+            sel = unpack_bits(sel_gpu[h], S)
+            check_topp_rule(c_gpu[h], sel, int(k_gpu[h]), cand, p, what=f"{what}: head {h}")
+            res = O.compact_head(np.arange(n), self.mask[h], n, sel, L_dense, 0)
+            K0, V0 = self.K[h][:n].copy(), self.V[h][:n].copy()
+            for i, e in enumerate(res.pages):
+                if e.kind == "new":
+                    for t, (ph, st) in enumerate(e.src):
+                        self.K[h][i, t], self.V[h][i, t] = K0[ph, st], V0[ph, st]
+                else:
+                    self.K[h][i], self.V[h][i] = K0[e.phys], V0[e.phys]
+            self.mask[h] = [e.mask for e in res.pages]
+            self.n[h] = len(res.pages)
+        self._pack()

@@ -1,13 +1,14 @@
 """Full-size workloads in the launch configuration bench.py times, checked on sampled heads.
 
 Stages whose inputs are the seeded workload are compared with the oracle run on that
-workload: scores (rtol 2e-3, log domain), sampled redundancy scores, and (single-metric
-configs) calibrated probabilities from the oracle's own scores.  Stages that consume the
-GPU's own outputs are checked by their defining properties: the calibrated mixture is a
-distribution over the candidates, the temperature solves its equation on the GPU's
-inputs, the selection satisfies the Top-p rule on the GPU's probabilities, and the
-rewritten cache holds exactly the selected rows in order (bytes) with the sparse and
-dense pages in place.  Heads are sampled across the budget range.
+workload: scores (rtol 2e-3, log domain), redundancy scores, calibrated probabilities
+from the oracle's own scores, and for config 4 the redundancy temperature and the 0.5 / 0.5
+mixture against the oracle's whole chain (its own scores, redundancy, Top-p count and mass,
+temperature and mixture).  Stages that consume the GPU's own outputs are also checked by
+their defining properties: the temperature solves its equation on the GPU's inputs (and
+equals the oracle's bisection on them), the selection satisfies the Top-p rule on the GPU's
+probabilities, and the rewritten cache holds exactly the selected rows in order (bytes)
+with the sparse and dense pages in place.  Heads are sampled across the budget range.
 """
 import math
 
@@ -92,13 +93,12 @@ def test_full_size_sampled(c):
         cand = np.zeros(S, bool)
         cand[:len(valid)] = O.candidate_mask(valid, cand_len)
         if xr_gpu is not None:
-            # redundancy on a sample of candidate slots (the oracle is a double loop)
-            rng = np.random.default_rng(h)
-            sample = rng.choice(np.nonzero(cand)[0], size=300, replace=False)
-            only = np.zeros(len(valid), bool)
-            only[sample] = True
-            xr_ref = O.redundancy_head(rows, only, len(valid), np_i(ref[h]))
-            err = np.abs(xr_gpu[h][sample] - xr_ref[sample])
+            # redundancy at every candidate slot
+            xr_full = O.redundancy_head(rows, valid, cand_len, np_i(ref[h]))
+            xr_ref = np.full(S, -np.inf)
+            xr_ref[:len(xr_full)] = xr_full
+            assert np.all(np.isneginf(xr_gpu[h][~cand])), f"cfg{c} x_red head {h}: non-candidates"
+            err = np.abs(xr_gpu[h][cand] - xr_ref[cand])
             assert err.max() <= 2e-3, f"cfg{c} x_red head {h}: {err.max()}"
             # temperature: M_k(Softmax(x_red / T)) meets the target mass on the GPU's inputs
             k_a, m_a = int(np_i(b.k_attn)[h]), float(np64(b.mass_attn)[h])
@@ -106,9 +106,21 @@ def test_full_size_sampled(c):
             top = np.sort(xs)[::-1][:k_a]
             mk = math.exp(np.logaddexp.reduce(top) - np.logaddexp.reduce(xs))
             assert abs(mk - m_a) <= 2e-3, f"cfg{c} T head {h}: M_k {mk} vs target {m_a}"
+            # stage parity of the temperature: the oracle's bisection on the same inputs
+            T_stage = O.solve_T_head(xr_gpu[h], cand, k_a, m_a)
+            assert float(T_gpu[h]) == pytest.approx(T_stage, rel=2e-3), f"cfg{c} T head {h}"
             # the mixture is a distribution over the candidates
             cg = c_gpu[h].astype(np.float64)
             assert np.all(cg[~cand] == 0) and np.all(cg >= 0) and abs(cg.sum() - 1) <= 1e-4, h
+            # ... and equals the oracle's own chain on the raw inputs: oracle scores and
+            # redundancy, its Top-p count and mass, its temperature, its 0.5 / 0.5 mixture
+            c_att, _ = O.calibrate_head(full, cand)
+            r_att = O.topp_head(c_att.astype(np.float32), cand, cfg["p"])
+            T_ref = O.solve_T_head(xr_ref, cand, r_att.k, r_att.sel_mass / 2.0 ** 40)
+            c_red, _ = O.calibrate_head(xr_ref, cand, T_ref)
+            c_mix = O.mix([c_att, c_red], [0.5, 0.5])
+            check_prob(cg, c_mix, 2e-3, f"cfg{c} mixture head {h} (oracle chain)")
+            assert float(T_gpu[h]) == pytest.approx(T_ref, rel=2e-3), f"cfg{c} T chain head {h}"
         else:
             c_ref, _ = O.calibrate_head(full, cand)
             check_prob(c_gpu[h], c_ref, 2e-3, f"cfg{c} c head {h}")

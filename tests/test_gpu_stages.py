@@ -304,10 +304,70 @@ def test_calibrate_topp_fused(name, two_metrics):
     assert int(st1.item()) == int(st2.item()) == 0
 
 
+@pytest.mark.parametrize("name", list(CASES))
+@pytest.mark.parametrize("weights", [(0.5, 0.5), (0.25, 0.75)])
+def test_calibrate_mixture_vs_oracle(name, weights):
+    """Two calibrated metrics mixed in the probability domain (Sec. 3.2 Solution 2, the
+    mixture reading of config 4): the attention-mass metric at T = 1 and a second metric at a
+    per-head temperature.  Both entry points (hk_calibrate and the fused hk_calibrate_topp)
+    are compared element by element with the oracle's mix of its two calibrations, and both
+    LSEs with the oracle's; unequal weights catch a swapped weight or temperature.  Top-p is
+    then run on the oracle's mixture, given to both sides, bit for bit."""
+    hk, cfg, w, kv, s, cl = _calib_inputs(name)
+    H, S = w.n_heads, w.S_max
+    pm = w.page_mask
+    s2_np, _ = WL.synthetic_log_scores(w, seed=zlib.crc32(name.encode()) + 1, scale=0.4)
+    x2 = torch.tensor(s2_np, device=DEV)          # same candidates, other values
+    T2 = torch.tensor(np.linspace(0.05, 2.0, H), dtype=torch.float32, device=DEV)
+    xs, Ts = [s, x2], [None, T2]
+    rtol = RTOL[cfg["dtype"]]
+    p = cfg.get("p", 0.9)
+    c1, l1 = torch.empty(H, S, device=DEV), torch.empty(H, 2, device=DEV)
+    hk.hk_calibrate(H, S, cl, pm, xs, Ts, list(weights), c1, l1)
+    c2, l2 = torch.empty(H, S, device=DEV), torch.empty(H, 2, device=DEV)
+    sel2 = torch.empty(H, S // 32, dtype=torch.int32, device=DEV)
+    k2 = torch.empty(H, dtype=torch.int32, device=DEV)
+    st2 = torch.zeros(1, dtype=torch.int32, device=DEV)
+    hk.hk_calibrate_topp(H, S, cl, pm, xs, Ts, list(weights), p, sel2, k2, c_out=c2, lse_out=l2,
+                         status=st2)
+    torch.cuda.synchronize()
+    s_np, cl_np = np64(s), np_i(cl)
+    mask = np_i(pm).astype(np.int64) & 0xFFFF
+    T2n = np64(T2)
+    cmix32 = np.zeros((H, S), np.float32)
+    sel2_np, k2_np, c2_np = np_i(sel2), np_i(k2), c2.cpu().numpy()
+    for h in range(H):
+        valid = ((mask[h][:, None] >> np.arange(16)) & 1).reshape(-1).astype(bool)
+        cand = O.candidate_mask(valid, int(cl_np[h]))
+        ca, la = O.calibrate_head(s_np[h], cand)
+        cb, lb = O.calibrate_head(s2_np[h].astype(np.float64), cand, float(T2n[h]))
+        cref = O.mix([ca, cb], weights)
+        for got_c, got_l, what in ((np64(c1[h]), np64(l1[h]), "hk_calibrate"),
+                                   (c2_np[h].astype(np.float64), np64(l2[h]), "fused")):
+            check_prob(got_c, cref, rtol, f"{what} mixture head {h}")
+            check_lse(got_l, [la, lb], rtol, f"{what} lse head {h}")
+        cmix32[h] = cref.astype(np.float32)
+        # the fused launch's own selection, made on its own mixture, obeys the Top-p rule
+        check_topp_rule(c2_np[h], unpack_bits(sel2_np[h], S), int(k2_np[h]), cand, p,
+                        what=f"fused head {h}")
+    assert int(st2.item()) == 0
+    c_in = torch.tensor(cmix32, device=DEV)
+    sel = torch.empty(H, S // 32, dtype=torch.int32, device=DEV)
+    k = torch.empty(H, dtype=torch.int32, device=DEV)
+    hk.hk_topp_select(H, S, cl, pm, c_in, p, sel, k)
+    torch.cuda.synchronize()
+    for h in range(H):
+        valid = ((mask[h][:, None] >> np.arange(16)) & 1).reshape(-1).astype(bool)
+        cand = O.candidate_mask(valid, int(cl_np[h]))
+        r = O.topp_head(cmix32[h], cand, p)
+        assert int(k[h]) == r.k and np.array_equal(unpack_bits(np_i(sel[h]), S), r.sel), h
+
+
 @pytest.mark.parametrize("case", range(4))
-def test_solve_T(case):
+@pytest.mark.parametrize("S", [1024, 16384, 32768])
+def test_solve_T(case, S):
     import paper_2606_28831_amd as hk
-    H, S = 8, 1024
+    H = 8
     rng = np.random.default_rng(case)
     x = np.full((H, S), -np.inf, np.float32)
     cand_len = rng.integers(16, S // 32 + 1, H).astype(np.int32) * 32

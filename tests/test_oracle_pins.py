@@ -152,6 +152,23 @@ def test_redundancy_scale_invariant():
     np.testing.assert_allclose(a, b, atol=1e-13)
 
 
+def test_redundancy_matches_scipy_cosine():
+    """Against scipy's cosine distance over every (candidate, reference) pair, the reference
+    equal to the candidate skipped; candidates are valid slots below cand_len."""
+    from scipy.spatial.distance import cdist
+    k = RNG.standard_normal((60, 9))
+    valid = RNG.random(60) < 0.85
+    refs = sorted(RNG.choice(60, size=12, replace=False).tolist())
+    x = O.redundancy_head(k, valid, 50, refs)
+    cosm = 1.0 - cdist(k, k[refs], metric="cosine")
+    for j in range(60):
+        if not (valid[j] and j < 50):
+            assert np.isneginf(x[j])
+            continue
+        others = [c for c, i in enumerate(refs) if i != j]
+        assert x[j] == pytest.approx(-max(cosm[j, others]), abs=1e-12)
+
+
 # ---------------------------------------------------------------- calibrate (a2)
 def test_calibrate_sums_to_one_and_matches_scipy():
     x = RNG.standard_normal(100) * 4

@@ -44,6 +44,7 @@ def test_config5_two_segments_sampled_heads():
     sidx = {s: i for i, s in enumerate(seqs)}
     seq_t = torch.tensor(seqs, device=DEV)
     replay = DecodeReplay(w, heads, Hkv, G, D, scale, w.max_pages)
+    print(f"config 5: cache ready, heads {heads}", flush=True)
     o_steps = {0, 1, 63, T - 1}
     bf = torch.bfloat16
     for seg in range(2):
@@ -90,4 +91,6 @@ def test_config5_two_segments_sampled_heads():
                         {h: np64(b.s_attn[h]) for h in heads}, rows(b.c), rows(b.sel_bits),
                         np_i(b.k), L_dense, p, w.S_max, f"seg {seg}", sidx=sidx)
         replay.check_cache(w, f"seg {seg} after the rewrite")
+        print(f"config 5: segment {seg} matches the oracle (kept {[replay.nr[h] for h in heads]})",
+              flush=True)
         del q_seg, k_seg, v_seg, lse_seg

@@ -382,7 +382,7 @@ def test_solve_T(case, S):
             tg[h], ks[h] = 0.5, k
         else:
             x[h, :n] = -rng.random(n).astype(np.float32) * (case * 0.7)
-            ks[h] = rng.integers(1, n)
+            ks[h] = rng.integers(1, max(2, (9 * n) // 10))     # target range below stays open
             tg[h] = rng.uniform(ks[h] / n * 1.05, 0.99)
     T = torch.empty(H, device=DEV)
     hk.hk_calibrate_solve_T(H, S, torch.tensor(cand_len, device=DEV), None,

@@ -73,7 +73,8 @@ enum {
                             G*W > 256, S_max > 32768, ...                              */
   HK_ERR_ALIGN = 4,      /* a pointer is not 16-byte aligned (256 for workspace)       */
   HK_ERR_WORKSPACE = 5,  /* workspace smaller than hk_workspace_size()                 */
-  HK_ERR_HIP = 6         /* a kernel launch failed                                     */
+  HK_ERR_HIP = 6,        /* a kernel launch failed                                     */
+  HK_ERR_SCRATCH = 7     /* hk_decode_attn_noalloc: more than its static scratch       */
 };
 /* bits OR-ed into the device status word */
 enum {
@@ -308,6 +309,22 @@ hk_status hk_alloc_init(const hk_allocator* alloc, int32_t first_free, int32_t n
 hk_status hk_decode_attn(const hk_dims* dims, const void* q, const hk_paged_kv* kv,
                          float sm_scale, float* o, float* lse, void* workspace,
                          size_t ws_bytes, hipStream_t stream);
+
+/* hk_decode_attn for callers that cannot allocate or pass a workspace: code recorded under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation.  Same arguments
+ * (minus the workspace), kernels and results as hk_decode_attn, bit for bit.  The split
+ * partial states go to a static device array of the library (16 MiB, one per GPU the library
+ * runs on, held until the process ends); the call allocates nothing.  Limit: the call needs
+ * hk_decode_noalloc_scratch_bytes(dims, kv->max_pages) bytes of it =
+ * NS * Hkv * n_split * (Hq / Hkv) * (D + 2) * 4 with n_split from hk_decode_plan (about
+ * 6.4 MB for 64 sequences x 8 KV heads, G 4, D 128, a 768-page table); a larger call returns
+ * HK_ERR_SCRATCH without launching.  Every call on one GPU shares that GPU's array: calls
+ * that overlap on one GPU (different streams, or different host threads without ordering)
+ * race, and the array keeps the last call's contents.  Other errors as for hk_decode_attn.
+ */
+hk_status hk_decode_attn_noalloc(const hk_dims* dims, const void* q, const hk_paged_kv* kv,
+                                 float sm_scale, float* o, float* lse, hipStream_t stream);
+size_t hk_decode_noalloc_scratch_bytes(const hk_dims* dims, int32_t max_pages);
 
 /* The split hk_decode_attn uses for these dims and table width (host only, no launch):
  * every head's pages are shared by *n_split workgroups, none of which walks more than

@@ -20,13 +20,15 @@ __all__ = ["HardKVError", "lib", "PagedKV", "Allocator", "hk_score", "hk_calibra
            "hk_timing_enable", "hk_timing_read", "TIMED_KERNELS", "hk_calibrate_topp",
            "hk_pool_max", "hk_score_rows", "hk_vote_topp", "hk_budget_plan", "hk_budget_select",
            "hk_compact_modes", "hk_calibrate_solve_T_gd", "hk_alloc_init", "hk_compress", "OP_COMPRESS", "BUDGET_KEEP", "BUDGET_SPARSE", "BUDGET_REWRITE",
-           "hk_probe", "PROBE_EXP", "PROBE_MFMA", "hk_decode_plan"]
+           "hk_probe", "PROBE_EXP", "PROBE_MFMA", "hk_decode_plan",
+           "hk_decode_attn_noalloc", "hk_decode_noalloc_scratch_bytes", "ERR_SCRATCH"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhardkv.so")
 
 HK_F32, HK_BF16 = 0, 1
 OP_SCORE, OP_COMPACT, OP_DECODE, OP_APPEND, OP_COMPRESS = 0, 1, 2, 3, 4
 FLAG_NOSPACE, FLAG_NAN, FLAG_RANGE = 1, 2, 4
+ERR_SCRATCH = 7
 BUDGET_KEEP, BUDGET_SPARSE, BUDGET_REWRITE = 0, 1, 2
 PROBE_EXP, PROBE_MFMA = 0, 1
 EXPORTED = ["hk_score", "hk_calibrate", "hk_calibrate_solve_T", "hk_topp_select", "hk_compact",
@@ -34,7 +36,7 @@ EXPORTED = ["hk_score", "hk_calibrate", "hk_calibrate_solve_T", "hk_topp_select"
             "hk_timing_enable", "hk_timing_read", "hk_calibrate_topp", "hk_pool_max",
             "hk_score_rows", "hk_vote_topp", "hk_budget_plan", "hk_budget_select",
             "hk_compact_modes", "hk_calibrate_solve_T_gd", "hk_alloc_init", "hk_compress",
-            "hk_probe", "hk_decode_plan"]
+            "hk_probe", "hk_decode_plan", "hk_decode_attn_noalloc", "hk_decode_noalloc_scratch_bytes"]
 # kernel ids of hk_timing_read, in header order
 TIMED_KERNELS = ["score_pass1", "score_merge", "score_pass2", "calibrate", "topp", "solve_T",
                  "compact_gather", "compact_meta", "decode_split", "decode_merge", "append",
@@ -120,6 +122,10 @@ def lib():
         L.hk_compress.restype = I32
         L.hk_compress.argtypes = [C.POINTER(hk_dims), P, C.POINTER(hk_paged_kv), I32, I32, F, P, D,
                                   I32, I32, C.POINTER(hk_allocator), P, P, P, P, SZ, P]
+        L.hk_decode_attn_noalloc.restype = I32
+        L.hk_decode_attn_noalloc.argtypes = [C.POINTER(hk_dims), P, C.POINTER(hk_paged_kv), F, P, P, P]
+        L.hk_decode_noalloc_scratch_bytes.restype = SZ
+        L.hk_decode_noalloc_scratch_bytes.argtypes = [C.POINTER(hk_dims), I32]
         L.hk_decode_plan.restype = I32
         L.hk_decode_plan.argtypes = [C.POINTER(hk_dims), I32, C.POINTER(I32), C.POINTER(I32)]
         L.hk_probe.restype = I32
@@ -293,6 +299,16 @@ def hk_compact(d: hk_dims, kv: PagedKV, sel_bits, L_dense: int, L_sparse: int, a
 def hk_decode_attn(d: hk_dims, q, kv: PagedKV, sm_scale: float, o, lse, ws, stream=None):
     _check(lib().hk_decode_attn(C.byref(d), _ptr(q), C.byref(kv.desc), float(sm_scale), _ptr(o),
                                 _ptr(lse), _ptr(ws), ws.numel(), _stream(stream)), "hk_decode_attn")
+
+
+def hk_decode_attn_noalloc(d: hk_dims, q, kv: PagedKV, sm_scale: float, o, lse, stream=None):
+    """hk_decode_attn with the split states in the library's static scratch (no workspace)."""
+    _check(lib().hk_decode_attn_noalloc(C.byref(d), _ptr(q), C.byref(kv.desc), float(sm_scale),
+                                        _ptr(o), _ptr(lse), _stream(stream)), "hk_decode_attn_noalloc")
+
+
+def hk_decode_noalloc_scratch_bytes(d: hk_dims, max_pages: int) -> int:
+    return int(lib().hk_decode_noalloc_scratch_bytes(C.byref(d), int(max_pages)))
 
 
 def hk_decode_plan(d: hk_dims, max_pages: int):

@@ -99,6 +99,8 @@ const char* hk_status_string(int32_t code, int32_t flags) {
     case HK_ERR_ALIGN: return "HK_ERR_ALIGN: pointer not 16-byte (workspace: 256-byte) aligned";
     case HK_ERR_WORKSPACE: return "HK_ERR_WORKSPACE: workspace smaller than hk_workspace_size()";
     case HK_ERR_HIP: return "HK_ERR_HIP: kernel launch failed";
+    case HK_ERR_SCRATCH:
+      return "HK_ERR_SCRATCH: the call needs more than the library's static scratch (16 MiB)";
     default: return "unknown status";
   }
 }
@@ -387,6 +389,29 @@ hk_status hk_decode_attn(const hk_dims* dims, const void* q, const hk_paged_kv* 
   if (!aligned256(workspace)) return HK_ERR_ALIGN;
   return launched(hk_launch_decode(dims->NS, dims->Hq, dims->Hkv, dims->D, q, kv, sm_scale, o, lse,
                                    workspace, stream));
+}
+
+hk_status hk_decode_attn_noalloc(const hk_dims* dims, const void* q, const hk_paged_kv* kv,
+                                 float sm_scale, float* o, float* lse, hipStream_t stream) {
+  hk_status e = check_dims(dims, false);
+  if (e) return e;
+  if ((e = check_kv(kv, true))) return e;
+  if (!q || !o || !lse) return HK_ERR_ARG;
+  if (!(sm_scale > 0.f) || !std::isfinite(sm_scale)) return HK_ERR_ARG;
+  if (!hk_decode_supports_group(dims->Hq / dims->Hkv)) return HK_ERR_SHAPE;
+  if (!aligned16(q)) return HK_ERR_ALIGN;
+  if (hk_decode_noalloc_bytes(dims->NS, dims->Hq, dims->Hkv, dims->D, kv->max_pages) >
+      HK_NOALLOC_SCRATCH_BYTES)
+    return HK_ERR_SCRATCH;
+  void* scratch = nullptr;
+  if (hk_noalloc_scratch(&scratch) != hipSuccess) return HK_ERR_HIP;
+  return launched(hk_launch_decode(dims->NS, dims->Hq, dims->Hkv, dims->D, q, kv, sm_scale, o, lse,
+                                   scratch, stream, /*timed=*/false));
+}
+
+size_t hk_decode_noalloc_scratch_bytes(const hk_dims* dims, int32_t max_pages) {
+  if (!dims || dims->Hkv <= 0 || dims->NS <= 0 || dims->Hq <= 0 || max_pages <= 0) return 0;
+  return hk_decode_noalloc_bytes(dims->NS, dims->Hq, dims->Hkv, dims->D, max_pages);
 }
 
 hk_status hk_decode_plan(const hk_dims* dims, int32_t max_pages, int32_t* n_split,

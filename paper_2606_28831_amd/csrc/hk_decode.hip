@@ -14,6 +14,8 @@
 //           products are summed over the 4 lanes of a slot with two xor-shuffles;
 //   values  lane = LPR * kg + dc: 16-byte chunk dc of the row, slots kg*KPL .. +KPL;
 //           the probabilities reach those lanes by shuffles.
+#include <mutex>
+
 #include "hk_internal.h"
 
 namespace hk {
@@ -474,6 +476,41 @@ hipError_t hk_launch_decode(int NS, int Hq, int Hkv, int D, const void* q, const
     hipLaunchKernelGGL(decode_merge_kernel<64>, dim3(n_heads), dim3(256), 0, st, part, n_split, G,
                        Hq, Hkv, o, lse);
   return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ decode without allocation
+// The split partial states of hk_decode_attn_noalloc live in this file-scope device array
+// instead of a caller workspace: one copy per GPU the library runs on, held until the
+// process ends.  Host code never uses the array's name as an address: its device address is
+// looked up once per device (with that device current) and kept here.
+static __device__ __align__(256) char scratch[HK_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+hipError_t hk_noalloc_scratch(void** ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
+size_t hk_decode_noalloc_bytes(int NS, int Hq, int Hkv, int D, int max_pages) {
+  int pps, n_split;
+  hk_decode_split_plan(NS * Hkv, max_pages, &pps, &n_split);
+  return (size_t)NS * Hkv * n_split * (Hq / Hkv) * (D + 2) * sizeof(float);
 }
 
 size_t hk_append_ws(int NS, int Hkv) {

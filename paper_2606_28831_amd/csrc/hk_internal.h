@@ -247,6 +247,11 @@ hipError_t hk_launch_alloc_init(int32_t* free_ids, int32_t* free_top, int first_
 hipError_t hk_launch_decode(int NS, int Hq, int Hkv, int D, const void* q, const hk_paged_kv* kv,
                             float sm_scale, float* o, float* lse, void* ws, hipStream_t st,
                             bool timed = true);
+// the static scratch of hk_decode_attn_noalloc: its size, this device's address of it, and
+// the bytes one call needs (the split partial states of the actual split)
+#define HK_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+hipError_t hk_noalloc_scratch(void** ptr);
+size_t hk_decode_noalloc_bytes(int NS, int Hq, int Hkv, int D, int max_pages);
 size_t hk_decode_ws(int NS, int Hq, int Hkv, int D, int max_pages);
 void hk_decode_split_plan(int n_heads, int max_pages, int* pps_out, int* n_split_out);
 

@@ -40,7 +40,7 @@ def test_library_exports_every_declared_symbol(hk):
 
 
 def test_status_strings(hk):
-    for code in range(7):
+    for code in range(8):
         assert hk.hk_status_string(code).startswith("HK_")
     for f in (1, 2, 4):
         assert hk.hk_status_string(f, True).startswith("HK_FLAG")
@@ -100,6 +100,14 @@ def test_validation_errors_without_gpu(hk):
     assert L.hk_decode_attn(C.byref(hk.dims(1, 12, 2, 128)), P, C.byref(kv), 0.1, P, P, P,
                             1 << 30, None) == 3              # group of 6 unsupported
     assert L.hk_decode_attn(C.byref(d), P, C.byref(kv), 0.1, P, P, P, 16, None) == 5
+    # the allocation-free decode: a call whose split states exceed the 16 MiB static scratch
+    # (all 32 layers of config 5 at once) is refused before anything is launched
+    d5 = hk.dims(2048, 32, 8, 128)
+    assert L.hk_decode_noalloc_scratch_bytes(C.byref(d5), 768) > 16 << 20
+    assert L.hk_decode_attn_noalloc(C.byref(d5), P, C.byref(_kv(hk, max_pages=768)), 0.1, P, P,
+                                    None) == 7
+    assert L.hk_decode_noalloc_scratch_bytes(C.byref(hk.dims(64, 32, 8, 128)), 768) == 64 * 8 * 6 * 4 * 130 * 4
+    assert L.hk_decode_attn_noalloc(C.byref(d), None, C.byref(kv), 0.1, P, P, None) == 1
     assert L.hk_append_kv(C.byref(d), C.byref(kv), None, P, C.byref(alloc), P, None, 0, None) == 1
     kvnull = hk.hk_paged_kv(None, P, P, P, P, 64, 4, 1)
     assert L.hk_decode_attn(C.byref(d), P, C.byref(kvnull), 0.1, P, P, P, 1 << 30, None) == 1

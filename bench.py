@@ -918,7 +918,7 @@ def main():
                     help="config 5: replay each decode segment from one captured HIP graph")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="time budget of the serial hard-budget oracle baseline")
-    ap.add_argument("--cpu-heads", type=int, default=64,
+    ap.add_argument("--cpu-heads", type=int, default=128,
                     help="heads of the workload the oracle baseline runs (evenly spaced)")
     ap.add_argument("--decode-segments", type=int, default=None,
                     help="config-5 segments of 128 decode steps (default: all 32)")

@@ -200,7 +200,6 @@ __global__ __launch_bounds__(AL_NT) void compact_alloc_kernel(int n_heads, const
 
 // Source rows are read once and rewritten rows are not read again by this step:
 // nontemporal (streaming) loads and stores for both.
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ uint4 load16(const char* p) {
   return __builtin_bit_cast(uint4, __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p)));
 }

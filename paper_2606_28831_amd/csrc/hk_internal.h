@@ -19,6 +19,7 @@ constexpr float kLn2 = 0.6931471805599453f;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // Hardware base-2 exponential and logarithm (v_exp_f32 / v_log_f32, ~1 ulp).  Unlike the
 // library exp2f/log2f they skip the denormal range fix-ups: results below 2^-126 come out

@@ -23,6 +23,8 @@
 // either the A or the B operand.
 // Accumulator layout of the 32x32 MFMA: register r of lane l holds row
 // 8*(r/4) + 4*(l/32) + (r%4), column l % 32.
+#include <type_traits>
+
 #include "hk_internal.h"
 
 namespace hk {
@@ -775,6 +777,441 @@ void score_pass2_kernel(
   tile_loop<F>(load_group, process, p_begin + SCORE_WPP * wave, p_cand_end, SCORE_WPP * NW);
 }
 
+// ------------------------------------------------------------------ cooperative passes (bf16)
+// The passes for bf16 caches without the redundancy metric.  Every wave of the workgroup owns
+// one 32-row block of the window queries, held in registers as an MFMA fragment for the whole
+// chunk; 32-key K tiles are shared by all waves.  The workgroup loads each tile cooperatively
+// (one 16-byte piece per thread, the pieces of tile t + STAGES in flight while tile t is
+// computed, so the prefetch costs a few registers per stage instead of a whole tile per wave),
+// writes it to a double-buffered LDS tile in MFMA fragment order -- piece kk * 64 + lane holds
+// key lane % 32, dims [16 kk + 8 (lane / 32), +8) -- and every wave reads the fragments with
+// conflict-free 16-byte LDS reads.  One barrier per iteration orders the buffers.
+//   pass 1  C[key][query] = K Q^T: lane-local online (max, sum exp) of the lane's query column;
+//   pass 2  C[query][key] = Q K^T: lane-local sum over the wave's rows of exp(z - LSE) per key;
+//           the per-wave column sums of a tile meet in LDS and are summed (and the log taken)
+//           by the last wave one iteration later.
+template <int D, int QB>
+struct Coop {
+  static constexpr int NT = 512, NW = 8;
+  static constexpr int TPI = QB <= 4 ? 2 : 1;           // 32-key tiles per iteration
+  static constexpr int KS = D / 16;                     // MFMA k-steps per tile
+  static constexpr int TILE_CH = KS * 64;               // 16-byte pieces per tile
+  static constexpr int ITER_CH = TPI * TILE_CH;         // pieces per iteration
+  static constexpr int LPT = (ITER_CH + NT - 1) / NT;   // pieces each thread loads per iteration
+  static constexpr int STAGES = 4;                      // iterations loaded ahead (4: unrolled)
+  static constexpr int PPI = 2 * TPI;                   // pages per iteration
+  static constexpr int PPW = 128;                       // pages per workgroup
+  static constexpr int BUF = ITER_CH * 16;              // bytes of one LDS tile buffer
+  static constexpr int ACTIVE = TPI * QB < NW ? TPI * QB : NW;   // waves with a query block
+  static_assert(STAGES == 4, "the main loop is written out for four stages");
+  static_assert(TPI * QB <= NW, "one query block per wave");
+};
+
+// LDS of a cooperative pass: 2 tile buffers, the chunk's page ids and masks, the per-wave
+// reduction scratch (two iterations of column sums for pass 2; (max, sum) for pass 1) and the
+// chunk's scores, written to memory once at the end.  No global store and no conditional load
+// sits in the main loop: the compiler then counts the loads in flight exactly and waits for
+// the oldest iteration's pieces only, instead of for every load.
+template <int D, int QB>
+struct CoopLds {
+  using C = Coop<D, QB>;
+  static constexpr size_t BUFS = 0;
+  static constexpr size_t TABLE = BUFS + 2 * (size_t)C::BUF;
+  static constexpr size_t MASK = TABLE + C::PPW * 4;
+  static constexpr size_t RED = MASK + C::PPW * 4;
+  static constexpr size_t RES = RED + 2 * C::NW * 32 * sizeof(float2);
+  static constexpr size_t LSE = RES + C::PPW * HK_PAGE * sizeof(float);     // pass 2's scores
+  static constexpr size_t TOTAL = LSE + 32 * QB * sizeof(float);           // pass 2's row LSEs
+};
+
+// Issues (into registers) the K pieces this thread loads for iteration `it`: pages past the
+// chunk's last page are clamped to it (their keys are masked or never stored; the repeated
+// page is a cache hit), so every iteration issues the same loads unconditionally.
+// f(integral_constant<int, i>) for i = 0 .. N-1, unrolled before any optimisation sees a loop
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (N > 0) {
+    static_for<N - 1>(f);
+    f(std::integral_constant<int, N - 1>{});
+  }
+}
+
+template <int D, int QB, int N>
+__device__ __forceinline__ void coop_issue(u32x4 (&r)[N], const uint16_t* __restrict__ k_pool,
+                                           const int32_t* s_table, int p_begin, int p_last, int it) {
+  using C = Coop<D, QB>;
+  const int p0 = p_begin + it * C::PPI;
+  static_for<C::LPT>([&](auto ic) {
+    constexpr int i = decltype(ic)::value;
+    const int c = i * C::NT + (int)threadIdx.x;
+    if (C::ITER_CH % C::NT == 0 || c < C::ITER_CH) {
+      const int ts = c / C::TILE_CH, f = c % C::TILE_CH;
+      const int kk = f >> 6, ln = f & 63, key = ln & 31;
+      const int pg = min(p0 + 2 * ts + (key >> 4), p_last);
+      const size_t phys = (size_t)s_table[pg - p_begin];
+      r[i] = *reinterpret_cast<const u32x4*>(k_pool + (phys * HK_PAGE + (key & 15)) * D + kk * 16 +
+                                             (ln >> 5) * 8);
+    }
+  });
+}
+template <int D, int QB, int N>
+__device__ __forceinline__ void coop_store(const u32x4 (&r)[N], char* buf) {
+  using C = Coop<D, QB>;
+  static_for<C::LPT>([&](auto ic) {
+    constexpr int i = decltype(ic)::value;
+    const int c = i * C::NT + (int)threadIdx.x;
+    if (C::ITER_CH % C::NT == 0 || c < C::ITER_CH) *reinterpret_cast<u32x4*>(buf + (size_t)c * 16) = r[i];
+  });
+}
+
+// The chunk's page ids and masks into LDS; the wave's query block as an MFMA fragment.
+template <int D, int QB, int KS>
+__device__ __forceinline__ void coop_setup(char* smem, const int32_t* trow, const uint16_t* mrow,
+                                           int p_begin, int p_stage_end, const uint16_t* __restrict__ q_obs,
+                                           int NS, int Hq, int Hkv, int W, int s, int kv, int qb, bool active,
+                                           bf16x8 (&qf)[KS]) {
+  using C = Coop<D, QB>;
+  using L = CoopLds<D, QB>;
+  int32_t* s_table = reinterpret_cast<int32_t*>(smem + L::TABLE);
+  uint32_t* s_mask = reinterpret_cast<uint32_t*>(smem + L::MASK);
+  for (int i = threadIdx.x; i < C::PPW; i += C::NT) {
+    const int pg = p_begin + i;
+    s_table[i] = pg < p_stage_end ? trow[pg] : 0;
+    s_mask[i] = pg < p_stage_end ? (uint32_t)mrow[pg] : 0u;
+  }
+  const int lane = threadIdx.x & 63;
+  const int G = Hq / Hkv, R = G * W;
+  const int r = qb * 32 + (lane & 31);
+  const int rc = min(r, R - 1);                  // padding rows read a real row, then are zeroed
+  const uint16_t* row = q_obs + ((size_t)((rc / G) * NS + s) * Hq + kv * G + rc % G) * D + (lane >> 5) * 8;
+  const bool keep = active && r < R;
+#pragma unroll
+  for (int kk = 0; kk < C::KS; ++kk) {
+    u32x4 u = *reinterpret_cast<const u32x4*>(row + kk * 16);
+    if (!keep) u = u32x4{0u, 0u, 0u, 0u};
+    qf[kk] = __builtin_bit_cast(bf16x8, u);
+  }
+}
+
+template <int D, int QB>
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4)))
+void score_pass1_coop_kernel(const uint16_t* __restrict__ q_obs, const uint16_t* __restrict__ k_pool,
+                             const int32_t* __restrict__ table, const uint16_t* __restrict__ masks,
+                             const int32_t* __restrict__ n_pages_arr, int NS, int Hq, int Hkv, int W,
+                             int max_pages, float c2, float2* __restrict__ part, int n_chunks) {
+  using C = Coop<D, QB>;
+  using L = CoopLds<D, QB>;
+  constexpr int R_pad = 32 * QB;
+  extern __shared__ __align__(16) char smem[];
+  const int h = blockIdx.y, chunk = blockIdx.x;
+  const int s = h / Hkv, kv = h % Hkv;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const bool active = wave < C::ACTIVE;
+  const int ts = wave / QB, qb = wave % QB;
+  const int n = n_pages_arr[h];
+  const int p_begin = chunk * C::PPW, p_end = min(p_begin + C::PPW, n);
+  bf16x8 qf[C::KS];
+  coop_setup<D, QB>(smem, table + (size_t)h * max_pages, masks + (size_t)h * max_pages, p_begin, p_end,
+                    q_obs, NS, Hq, Hkv, W, s, kv, qb, active, qf);
+  const int32_t* s_table = reinterpret_cast<const int32_t*>(smem + L::TABLE);
+  const uint32_t* s_mask = reinterpret_cast<const uint32_t*>(smem + L::MASK);
+  float2* red = reinterpret_cast<float2*>(smem + L::RED);            // [NW][32]
+  __syncthreads();
+
+  float M = -INFINITY, Lsum = 0.f;
+  const int n_iter = p_end > p_begin ? (p_end - p_begin + C::PPI - 1) / C::PPI : 0;
+  const int p_last = p_end - 1;
+  u32x4 pre0[C::LPT], pre1[C::LPT], pre2[C::LPT], pre3[C::LPT];
+  auto slot = [&](auto uc) -> u32x4(&)[C::LPT] {
+    constexpr int u = decltype(uc)::value % 4;
+    if constexpr (u == 0) return pre0;
+    else if constexpr (u == 1) return pre1;
+    else if constexpr (u == 2) return pre2;
+    else return pre3;
+  };
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
+  if (n_iter > 0) {
+    coop_issue<D, QB>(pre0, k_pool, s_table, p_begin, p_last, 0);
+    coop_issue<D, QB>(pre1, k_pool, s_table, p_begin, p_last, 1);
+    coop_issue<D, QB>(pre2, k_pool, s_table, p_begin, p_last, 2);
+    coop_issue<D, QB>(pre3, k_pool, s_table, p_begin, p_last, 3);
+    coop_store<D, QB>(pre0, smem + L::BUFS);
+    coop_issue<D, QB>(pre0, k_pool, s_table, p_begin, p_last, C::STAGES);
+  }
+
+  // Online (max, sum exp) update of the lane's query column with one tile's accumulator:
+  // every key of the tile valid (fast path) or under the tile's 32-slot mask.
+  auto update_masked = [&](const f32x16& a, uint32_t tm) {
+    const uint32_t rows = lane_rows(tm, lane);
+    float m = -INFINITY;
+#pragma unroll
+    for (int e = 0; e < 16; ++e)
+      if ((rows >> e) & 1u) m = vmax(m, a[e]);
+    const float mn = vmax(M, m);
+    if (mn != -INFINITY) {                       // this column has seen a valid key
+      const float mc = mn * c2;
+      float sum = 0.f;
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        if ((rows >> e) & 1u) sum += fast_exp2(fmaf(a[e], c2, -mc));
+      Lsum = fmaf(Lsum, fast_exp2((M - mn) * c2), sum);
+      M = mn;
+    }
+  };
+  auto tile_mask = [&](int it_) {
+    const int pl = it_ * C::PPI + 2 * ts;                           // chunk-relative page
+    return s_mask[pl] | (s_mask[pl + 1] << 16);                     // past the end: 0
+  };
+
+  // Software pipeline inside each wave: the MFMAs of tile it run beside the sum of
+  // exponentials of tile it - 1's accumulator, one step per scheduling region.  Tiles with
+  // masked keys take the plain update after the chain.  Iterations run in groups of four up to
+  // n_iter + 1 (the last drains the pipeline); those past n_iter only move data.
+  f32x16 accp = {};
+  auto iteration = [&](auto uc, int it) {
+    constexpr int u = decltype(uc)::value;
+    __syncthreads();
+    if (active) {
+      const bool prev = it >= 1 && it - 1 < n_iter;
+      const uint32_t tmp = prev ? tile_mask(it - 1) : 0u;
+      const bool fuse = tmp == 0xffffffffu;
+      if (it < n_iter) {
+        const char* tb = smem + L::BUFS + (size_t)(u & 1) * C::BUF + (size_t)ts * C::TILE_CH * 16 +
+                         (size_t)lane * 16;
+        constexpr int KD = 2;                    // fragments read this many steps ahead
+        bf16x8 kf[KD + 1];
+#pragma unroll
+        for (int g = 0; g < KD; ++g) kf[g] = *reinterpret_cast<const bf16x8*>(tb + (size_t)g * 1024);
+        f32x16 acc = {};
+        if (fuse) {
+          // exponentials against the lane's current reference maximum M, no maximum per
+          // tile: the sum is exact unless a key exceeds M by more than 64 powers of two (or
+          // M is still -inf, or the tile holds a NaN), in which case the sum is not <= 2^64
+          // and the lane redoes the tile with the exact update
+          const float mc = M * c2;
+          float s0 = 0.f, s1 = 0.f;
+#pragma unroll
+          for (int kk = 0; kk < C::KS; ++kk) {
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk % (KD + 1)], qf[kk], acc, 0, 0, 0);
+            if (kk + KD < C::KS)
+              kf[(kk + KD) % (KD + 1)] = *reinterpret_cast<const bf16x8*>(tb + (size_t)(kk + KD) * 1024);
+#pragma unroll
+            for (int e = 0; e < 16; ++e)
+              if (e * C::KS / 16 == kk) {
+                if (e & 1) s1 += fast_exp2(fmaf(accp[e], c2, -mc));
+                else s0 += fast_exp2(fmaf(accp[e], c2, -mc));
+              }
+            __builtin_amdgcn_sched_barrier(0);
+          }
+          const float st = s0 + s1;
+          if (st <= 0x1p64f) Lsum += st;
+          else update_masked(accp, 0xffffffffu);
+        } else {
+#pragma unroll
+          for (int kk = 0; kk < C::KS; ++kk) {
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk % (KD + 1)], qf[kk], acc, 0, 0, 0);
+            if (kk + KD < C::KS)
+              kf[(kk + KD) % (KD + 1)] = *reinterpret_cast<const bf16x8*>(tb + (size_t)(kk + KD) * 1024);
+          }
+          if (tmp != 0u) update_masked(accp, tmp);
+        }
+        accp = acc;
+      } else if (prev && tmp != 0u) {
+        update_masked(accp, tmp);
+      }
+    }
+    coop_store<D, QB>(slot(std::integral_constant<int, u + 1>{}), smem + L::BUFS + (size_t)((u + 1) & 1) * C::BUF);
+    coop_issue<D, QB>(slot(std::integral_constant<int, u + 1>{}), k_pool, s_table, p_begin, p_last,
+                      it + 1 + C::STAGES);
+  };
+  for (int it0 = 0; it0 < n_iter + 1; it0 += 4) {
+    iteration(I0{}, it0);
+    iteration(I1{}, it0 + 1);
+    iteration(I2{}, it0 + 2);
+    iteration(I3{}, it0 + 3);
+  }
+  // merge the lane halves (same query column), then the tile slots of one query block
+  {
+    const float Mo = __shfl_xor(M, 32, 64), Lo = __shfl_xor(Lsum, 32, 64);
+    const float mn = fmaxf(M, Mo);
+    float Ln = 0.f;
+    if (mn != -INFINITY) Ln = Lsum * fast_exp2((M - mn) * c2) + Lo * fast_exp2((Mo - mn) * c2);
+    if (active && lane < 32) red[wave * 32 + lane] = make_float2(mn, Ln);
+  }
+  __syncthreads();
+  for (int r = threadIdx.x; r < R_pad; r += C::NT) {
+    const int b = r >> 5, j = r & 31;
+    float mn = -INFINITY;
+#pragma unroll
+    for (int t = 0; t < C::TPI; ++t) mn = fmaxf(mn, red[(t * QB + b) * 32 + j].x);
+    float Ln = 0.f;
+    if (mn != -INFINITY)
+#pragma unroll
+      for (int t = 0; t < C::TPI; ++t) {
+        const float2 v = red[(t * QB + b) * 32 + j];
+        Ln += v.y * fast_exp2((v.x - mn) * c2);
+      }
+    part[((size_t)h * n_chunks + chunk) * R_pad + r] = make_float2(mn, Ln);
+  }
+}
+
+template <int D, int QB>
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(4, 4)))
+void score_pass2_coop_kernel(const uint16_t* __restrict__ q_obs, const uint16_t* __restrict__ k_pool,
+                             const int32_t* __restrict__ table, const uint16_t* __restrict__ masks,
+                             const int32_t* __restrict__ n_pages_arr, int NS, int Hq, int Hkv, int W,
+                             int max_pages, int L_dense, float c2, float lnR,
+                             const float* __restrict__ row_lse, float* __restrict__ s_out,
+                             int32_t* __restrict__ cand_len_out) {
+  using C = Coop<D, QB>;
+  using L = CoopLds<D, QB>;
+  extern __shared__ __align__(16) char smem[];
+  const int h = blockIdx.y, chunk = blockIdx.x;
+  const int s = h / Hkv, kv = h % Hkv, G = Hq / Hkv;
+  const int R = G * W;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const bool active = wave < C::ACTIVE;
+  const int ts = wave / QB, qb = wave % QB;
+  const size_t S_max = (size_t)max_pages * HK_PAGE;
+  const int n = n_pages_arr[h];
+  const int cand_len = HK_PAGE * max(0, n - dense_pages(L_dense));
+  if (chunk == 0 && threadIdx.x == 0) cand_len_out[h] = cand_len;
+  const int p_begin = chunk * C::PPW, p_end_all = min(p_begin + C::PPW, max_pages);
+  const int p_cand_end = min(p_end_all, cand_len / HK_PAGE);
+  float* srow = s_out + (size_t)h * S_max;
+  {
+    // slots of this chunk that hold no candidate: -inf
+    const int j0 = max(p_cand_end, p_begin) * HK_PAGE, j1 = p_end_all * HK_PAGE;
+    for (int j = j0 + threadIdx.x; j < j1; j += C::NT) srow[j] = -INFINITY;
+  }
+  if (p_begin >= p_cand_end) return;
+
+  bf16x8 qf[C::KS];
+  coop_setup<D, QB>(smem, table + (size_t)h * max_pages, masks + (size_t)h * max_pages, p_begin, p_cand_end,
+                    q_obs, NS, Hq, Hkv, W, s, kv, qb, active, qf);
+  const int32_t* s_table = reinterpret_cast<const int32_t*>(smem + L::TABLE);
+  const uint32_t* s_mask = reinterpret_cast<const uint32_t*>(smem + L::MASK);
+  float* red = reinterpret_cast<float*>(smem + L::RED);              // [2][NW][32]
+  float* res = reinterpret_cast<float*>(smem + L::RES);              // the chunk's scores
+  float* lse2 = reinterpret_cast<float*>(smem + L::LSE);             // [32 QB], log2 units
+  for (int r = threadIdx.x; r < 32 * QB; r += C::NT) {
+    const int rc = min(r, R - 1);                 // every load issued; padding rows weigh 0
+    const float v = row_lse[((size_t)(rc / G) * NS + s) * Hq + kv * G + rc % G];
+    lse2[r] = r < R ? v * kLog2e : INFINITY;
+  }
+  __syncthreads();
+
+  // the last wave's lanes sum the column partials of one tile iteration (key k of tile slot
+  // k / 32), take the log and keep the score in LDS
+  constexpr int NRED = C::TPI * 32;
+  const int rk = (int)threadIdx.x - (C::NT - NRED);
+  auto reduce = [&](int it_done, int par) {
+    if (rk < 0) return;
+    const int t = rk >> 5, j = rk & 31;
+    const int pl = it_done * C::PPI + 2 * t + (j >> 4);              // chunk-relative page
+    if (p_begin + pl >= p_cand_end) return;
+    float sum = 0.f;
+#pragma unroll
+    for (int b = 0; b < QB; ++b) sum += red[(par * C::NW + t * QB + b) * 32 + j];
+    const bool cand = (s_mask[pl] >> (j & 15)) & 1u;
+    res[pl * HK_PAGE + (j & 15)] = cand ? fmaf(fast_log2(sum), kLn2, -lnR) : -INFINITY;
+  };
+
+  const int n_iter = (p_cand_end - p_begin + C::PPI - 1) / C::PPI;
+  const int p_last = p_cand_end - 1;
+  u32x4 pre0[C::LPT], pre1[C::LPT], pre2[C::LPT], pre3[C::LPT];
+  auto slot = [&](auto uc) -> u32x4(&)[C::LPT] {
+    constexpr int u = decltype(uc)::value % 4;
+    if constexpr (u == 0) return pre0;
+    else if constexpr (u == 1) return pre1;
+    else if constexpr (u == 2) return pre2;
+    else return pre3;
+  };
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
+  coop_issue<D, QB>(pre0, k_pool, s_table, p_begin, p_last, 0);
+  coop_issue<D, QB>(pre1, k_pool, s_table, p_begin, p_last, 1);
+  coop_issue<D, QB>(pre2, k_pool, s_table, p_begin, p_last, 2);
+  coop_issue<D, QB>(pre3, k_pool, s_table, p_begin, p_last, 3);
+  coop_store<D, QB>(pre0, smem + L::BUFS);
+  coop_issue<D, QB>(pre0, k_pool, s_table, p_begin, p_last, C::STAGES);
+
+  // Software pipeline inside each wave: the MFMAs of tile it run beside the exponentials of
+  // tile it - 1 (its accumulator kept from the previous iteration; independent work, which
+  // the SIMD overlaps within a wave), pinned step by step with scheduling-group barriers;
+  // the last wave reduces tile it - 2.  Iterations run in groups of four up to n_iter + 2
+  // (the two after the last tile drain the pipeline); those past n_iter only move data.
+  const float* lrow = lse2 + qb * 32 + 4 * (lane >> 5);
+  const int swap_addr = (lane ^ 32) << 2;        // ds_bpermute address of the other half's lane
+  f32x16 accp = {};
+  auto iteration = [&](auto uc, int it) {
+    constexpr int u = decltype(uc)::value;
+    __syncthreads();
+    if (it >= 2 && it - 2 < n_iter) reduce(it - 2, u & 1);
+    if (active) {
+      const bool prev = it >= 1 && it - 1 < n_iter;
+      f32x4 l4[4];
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) l4[r4] = *reinterpret_cast<const f32x4*>(lrow + 8 * r4);
+      float c0 = 0.f, c1 = 0.f;
+      if (it < n_iter) {
+        const char* tb = smem + L::BUFS + (size_t)(u & 1) * C::BUF + (size_t)ts * C::TILE_CH * 16 +
+                         (size_t)lane * 16;
+        // K fragments are read KD MFMA steps ahead of their use
+        constexpr int KD = 2;
+        bf16x8 kf[KD + 1];
+#pragma unroll
+        for (int g = 0; g < KD; ++g) kf[g] = *reinterpret_cast<const bf16x8*>(tb + (size_t)g * 1024);
+        f32x16 acc = {};
+#pragma unroll
+        for (int kk = 0; kk < C::KS; ++kk) {
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[kk], kf[kk % (KD + 1)], acc, 0, 0, 0);
+          if (kk + KD < C::KS)
+            kf[(kk + KD) % (KD + 1)] = *reinterpret_cast<const bf16x8*>(tb + (size_t)(kk + KD) * 1024);
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+            if (e * C::KS / 16 == kk) {
+              if (e & 1) c1 += fast_exp2(fmaf(accp[e], c2, -l4[e >> 2][e & 3]));
+              else c0 += fast_exp2(fmaf(accp[e], c2, -l4[e >> 2][e & 3]));
+            }
+          // one step per scheduling region: the MFMA, the fragment read KD steps ahead and
+          // 16 / KS exponentials of the previous tile stay together, in this order
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        accp = acc;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          if (e & 1) c1 += fast_exp2(fmaf(accp[e], c2, -l4[e >> 2][e & 3]));
+          else c0 += fast_exp2(fmaf(accp[e], c2, -l4[e >> 2][e & 3]));
+        }
+      }
+      if (prev) {
+        float col = c0 + c1;
+        col += __int_as_float(__builtin_amdgcn_ds_bpermute(swap_addr, __float_as_int(col)));
+        if (lane < 32) red[(((u + 1) & 1) * C::NW + wave) * 32 + lane] = col;
+      }
+    }
+    coop_store<D, QB>(slot(std::integral_constant<int, u + 1>{}), smem + L::BUFS + (size_t)((u + 1) & 1) * C::BUF);
+    coop_issue<D, QB>(slot(std::integral_constant<int, u + 1>{}), k_pool, s_table, p_begin, p_last,
+                      it + 1 + C::STAGES);
+  };
+  for (int it0 = 0; it0 < n_iter + 2; it0 += 4) {
+    iteration(I0{}, it0);
+    iteration(I1{}, it0 + 1);
+    iteration(I2{}, it0 + 2);
+    iteration(I3{}, it0 + 3);
+  }
+  __syncthreads();
+  for (int j = threadIdx.x; j < (p_cand_end - p_begin) * HK_PAGE; j += C::NT)
+    srow[(size_t)p_begin * HK_PAGE + j] = res[j];
+}
+
 static size_t pass1_lds(int R_pad, int D, int es) {
   return (size_t)R_pad * D * es + (size_t)SCORE_NW * R_pad * sizeof(float2);
 }
@@ -926,7 +1363,28 @@ hipError_t launch_score_q(const hk_score_args& a, hipStream_t st) {
   if (!lse_buf) lse_buf = reinterpret_cast<float*>(ws + off);
   const float* lse_use = a.row_lse_in;
   dim3 grid(n_chunks, n_heads);
-  if (!lse_use) {
+  constexpr bool coop = sizeof(T) == 2;
+  if (!lse_use && coop) {
+    using Cp = Coop<D, QB>;
+    const int nc = (kv->max_pages + Cp::PPW - 1) / Cp::PPW;      // <= n_chunks (workspace size)
+    const size_t lds = CoopLds<D, QB>::TOTAL;
+    allow_dynamic_lds<score_pass1_coop_kernel<D, QB>>(lds);
+    {
+      TimedLaunch t(HK_TK_SCORE_PASS1, st);
+      hipLaunchKernelGGL((score_pass1_coop_kernel<D, QB>), dim3(nc, n_heads), dim3(Cp::NT), lds, st,
+                         static_cast<const uint16_t*>(a.q_obs), static_cast<const uint16_t*>(kv->k_pool),
+                         kv->page_table, kv->page_mask, kv->n_pages, a.NS, a.Hq, a.Hkv, a.W,
+                         kv->max_pages, c2, part, nc);
+    }
+    {
+      TimedLaunch t(HK_TK_SCORE_MERGE, st);
+      hipLaunchKernelGGL(score_lse_merge_kernel, dim3(n_heads), dim3(256), 0, st, part, nc,
+                         R_pad, a.NS, a.Hq, a.Hkv, a.W, c2, a.sm_scale, lse_buf, kv->n_pages,
+                         a.L_dense, a.cand_len);
+    }
+    lse_use = lse_buf;
+    if (!a.s_attn) return hipGetLastError();      // row LSEs (and candidate counts) only
+  } else if (!lse_use) {
     const size_t lds1 = pass1_lds(R_pad, D, sizeof(T));
     allow_dynamic_lds<score_pass1_kernel<T, D, QB>>(lds1);
     {
@@ -960,6 +1418,15 @@ hipError_t launch_score_q(const hk_score_args& a, hipStream_t st) {
                        kv->page_table, kv->page_mask, kv->n_pages, a.NS, a.Hq, a.Hkv, a.W,
                        kv->max_pages, a.L_dense, c2, lnR, lse_use, a.s_attn, a.cand_len,
                        a.ref_slots, a.n_ref, a.x_red);
+  } else if constexpr (coop) {
+    using Cp = Coop<D, QB>;
+    const size_t lds = CoopLds<D, QB>::TOTAL;
+    allow_dynamic_lds<score_pass2_coop_kernel<D, QB>>(lds);
+    hipLaunchKernelGGL((score_pass2_coop_kernel<D, QB>), dim3((kv->max_pages + Cp::PPW - 1) / Cp::PPW, n_heads),
+                       dim3(Cp::NT), lds, st, static_cast<const uint16_t*>(a.q_obs),
+                       static_cast<const uint16_t*>(kv->k_pool), kv->page_table, kv->page_mask,
+                       kv->n_pages, a.NS, a.Hq, a.Hkv, a.W, kv->max_pages, a.L_dense, c2, lnR, lse_use,
+                       a.s_attn, a.cand_len);
   } else {
     allow_dynamic_lds<score_pass2_kernel<T, D, QB, false>>(lds2);
     hipLaunchKernelGGL((score_pass2_kernel<T, D, QB, false>), grid, dim3(P2Shape<false>::NT), lds2, st,

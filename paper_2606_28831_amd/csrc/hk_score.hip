@@ -1363,45 +1363,49 @@ hipError_t launch_score_q(const hk_score_args& a, hipStream_t st) {
   if (!lse_buf) lse_buf = reinterpret_cast<float*>(ws + off);
   const float* lse_use = a.row_lse_in;
   dim3 grid(n_chunks, n_heads);
+  // bf16 caches: the cooperative passes; fp32 caches (and the redundancy variant of pass 2):
+  // the per-wave tile passes
   constexpr bool coop = sizeof(T) == 2;
-  if (!lse_use && coop) {
-    using Cp = Coop<D, QB>;
-    const int nc = (kv->max_pages + Cp::PPW - 1) / Cp::PPW;      // <= n_chunks (workspace size)
-    const size_t lds = CoopLds<D, QB>::TOTAL;
-    allow_dynamic_lds<score_pass1_coop_kernel<D, QB>>(lds);
-    {
-      TimedLaunch t(HK_TK_SCORE_PASS1, st);
-      hipLaunchKernelGGL((score_pass1_coop_kernel<D, QB>), dim3(nc, n_heads), dim3(Cp::NT), lds, st,
-                         static_cast<const uint16_t*>(a.q_obs), static_cast<const uint16_t*>(kv->k_pool),
-                         kv->page_table, kv->page_mask, kv->n_pages, a.NS, a.Hq, a.Hkv, a.W,
-                         kv->max_pages, c2, part, nc);
+  if (!lse_use) {
+    if constexpr (coop) {
+      using Cp = Coop<D, QB>;
+      const int nc = (kv->max_pages + Cp::PPW - 1) / Cp::PPW;      // <= n_chunks (workspace size)
+      const size_t lds = CoopLds<D, QB>::TOTAL;
+      allow_dynamic_lds<score_pass1_coop_kernel<D, QB>>(lds);
+      {
+        TimedLaunch t(HK_TK_SCORE_PASS1, st);
+        hipLaunchKernelGGL((score_pass1_coop_kernel<D, QB>), dim3(nc, n_heads), dim3(Cp::NT), lds, st,
+                           static_cast<const uint16_t*>(a.q_obs), static_cast<const uint16_t*>(kv->k_pool),
+                           kv->page_table, kv->page_mask, kv->n_pages, a.NS, a.Hq, a.Hkv, a.W,
+                           kv->max_pages, c2, part, nc);
+      }
+      {
+        TimedLaunch t(HK_TK_SCORE_MERGE, st);
+        hipLaunchKernelGGL(score_lse_merge_kernel, dim3(n_heads), dim3(256), 0, st, part, nc,
+                           R_pad, a.NS, a.Hq, a.Hkv, a.W, c2, a.sm_scale, lse_buf, kv->n_pages,
+                           a.L_dense, a.cand_len);
+      }
+      lse_use = lse_buf;
+      if (!a.s_attn) return hipGetLastError();      // row LSEs (and candidate counts) only
+    } else {
+      const size_t lds1 = pass1_lds(R_pad, D, sizeof(T));
+      allow_dynamic_lds<score_pass1_kernel<T, D, QB>>(lds1);
+      {
+        TimedLaunch t(HK_TK_SCORE_PASS1, st);
+        hipLaunchKernelGGL((score_pass1_kernel<T, D, QB>), grid, dim3(SCORE_NT), lds1, st,
+                           static_cast<const T*>(a.q_obs), static_cast<const T*>(kv->k_pool),
+                           kv->page_table, kv->page_mask, kv->n_pages, a.NS, a.Hq, a.Hkv, a.W,
+                           kv->max_pages, c2, part, n_chunks);
+      }
+      {
+        TimedLaunch t(HK_TK_SCORE_MERGE, st);
+        hipLaunchKernelGGL(score_lse_merge_kernel, dim3(n_heads), dim3(256), 0, st, part, n_chunks,
+                           R_pad, a.NS, a.Hq, a.Hkv, a.W, c2, a.sm_scale, lse_buf, kv->n_pages,
+                           a.L_dense, a.cand_len);
+      }
+      lse_use = lse_buf;
+      if (!a.s_attn) return hipGetLastError();      // row LSEs (and candidate counts) only
     }
-    {
-      TimedLaunch t(HK_TK_SCORE_MERGE, st);
-      hipLaunchKernelGGL(score_lse_merge_kernel, dim3(n_heads), dim3(256), 0, st, part, nc,
-                         R_pad, a.NS, a.Hq, a.Hkv, a.W, c2, a.sm_scale, lse_buf, kv->n_pages,
-                         a.L_dense, a.cand_len);
-    }
-    lse_use = lse_buf;
-    if (!a.s_attn) return hipGetLastError();      // row LSEs (and candidate counts) only
-  } else if (!lse_use) {
-    const size_t lds1 = pass1_lds(R_pad, D, sizeof(T));
-    allow_dynamic_lds<score_pass1_kernel<T, D, QB>>(lds1);
-    {
-      TimedLaunch t(HK_TK_SCORE_PASS1, st);
-      hipLaunchKernelGGL((score_pass1_kernel<T, D, QB>), grid, dim3(SCORE_NT), lds1, st,
-                         static_cast<const T*>(a.q_obs), static_cast<const T*>(kv->k_pool),
-                         kv->page_table, kv->page_mask, kv->n_pages, a.NS, a.Hq, a.Hkv, a.W,
-                         kv->max_pages, c2, part, n_chunks);
-    }
-    {
-      TimedLaunch t(HK_TK_SCORE_MERGE, st);
-      hipLaunchKernelGGL(score_lse_merge_kernel, dim3(n_heads), dim3(256), 0, st, part, n_chunks,
-                         R_pad, a.NS, a.Hq, a.Hkv, a.W, c2, a.sm_scale, lse_buf, kv->n_pages,
-                         a.L_dense, a.cand_len);
-    }
-    lse_use = lse_buf;
-    if (!a.s_attn) return hipGetLastError();      // row LSEs (and candidate counts) only
   } else if (a.row_lse_out && a.row_lse_out != a.row_lse_in) {
     (void)hipMemcpyAsync(a.row_lse_out, a.row_lse_in, sizeof(float) * (size_t)a.W * a.NS * a.Hq,
                          hipMemcpyDeviceToDevice, st);

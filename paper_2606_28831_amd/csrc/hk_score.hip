@@ -1027,7 +1027,10 @@ void score_pass1_coop_kernel(const uint16_t* __restrict__ q_obs, const uint16_t*
     coop_issue<D, QB>(slot(std::integral_constant<int, u + 1>{}), k_pool, s_table, p_begin, p_last,
                       it + 1 + C::STAGES);
   };
-  for (int it0 = 0; it0 < n_iter + 1; it0 += 4) {
+  // A chunk with no page (n_iter = 0) runs no iteration: each ends by issuing clamped loads
+  // for a later one, and with no page the clamp (to p_last = p_end - 1 < p_begin) would read
+  // the page table below its first entry.
+  for (int it0 = 0; n_iter > 0 && it0 < n_iter + 1; it0 += 4) {
     iteration(I0{}, it0);
     iteration(I1{}, it0 + 1);
     iteration(I2{}, it0 + 2);

@@ -860,7 +860,7 @@ def _pmc_mean(run_dir, counter, match):
     return sum(vals) / len(vals), len(vals)
 
 
-KERNEL_SYMBOL = {"score_pass1": "score_pass1_kernel", "score_pass2": "score_pass2_kernel",
+KERNEL_SYMBOL = {"score_pass1": "score_pass1_coop_kernel", "score_pass2": "score_pass2_coop_kernel",
                  "compact_gather": "compact_gather_kernel", "decode_split": "decode_split_kernel",
                  "score_rows": "score_rows_kernel", "vote": "vote_topp_kernel"}
 

@@ -9,6 +9,8 @@
  *   hk_calibrate_solve_T_gd  the same temperature by gradient descent (Alg. 1)
  *   hk_topp_select    head-adaptive Top-p budget (Sec. 3.2, Problem 1)
  *   hk_calibrate_topp hk_calibrate followed by hk_topp_select in one launch
+ *   hk_topp_select_ws / hk_calibrate_topp_ws  the same with each head spread over many
+ *                     workgroups (long caches, small batches)
  *   hk_compress       score -> calibrate + Top-p -> compact in one call
  *   hk_pool_max       order-preserving max-pooling of scores before calibration
  *                     (Sec. 3.2 Solution 1, SnapKV form)
@@ -112,9 +114,11 @@ typedef struct {
   int32_t W;             /* observation-window length                                   */
 } hk_dims;
 
-enum { HK_OP_SCORE = 0, HK_OP_COMPACT = 1, HK_OP_DECODE = 2, HK_OP_APPEND = 3, HK_OP_COMPRESS = 4 };
+enum { HK_OP_SCORE = 0, HK_OP_COMPACT = 1, HK_OP_DECODE = 2, HK_OP_APPEND = 3, HK_OP_COMPRESS = 4,
+       HK_OP_SELECT = 5 };
 
-/* Bytes of workspace entry point `op` needs for these dims and table width. */
+/* Bytes of workspace entry point `op` needs for these dims and table width (HK_OP_SELECT:
+ * hk_select_workspace_size(dims->NS * dims->Hkv, 16 * max_pages)). */
 size_t hk_workspace_size(int32_t op, const hk_dims* dims, int32_t max_pages);
 
 /* Name of a hk_status code (flags = 0) or of a single HK_FLAG_* bit (flags = 1). */
@@ -206,6 +210,38 @@ hk_status hk_calibrate_topp(int32_t n_heads, int32_t S_max, const int32_t* cand_
                             float* lse_out, uint32_t* sel_bits, int32_t* k_out,
                             float* sel_mass_out, int32_t* status, hipStream_t stream);
 
+/* ------------------------------------------------------------------ a2 + a3, wide
+ * hk_topp_select and hk_calibrate_topp with every head spread over ceil(S_max / 4096)
+ * workgroups (Sec. 3.2, Problem 1 and Solution 2): for caches longer than 32768 slots, and
+ * so that a batch of few heads still fills the chip.  The Top-p rule is the one stated for
+ * hk_topp_select, in the same exact integers, so for the same c the selection, k_out and
+ * sel_mass_out are those hk_topp_select writes, bit for bit.  hk_calibrate_topp_ws
+ * assembles each head's log-sum-exp from 4096-slot pieces: its c_out and lse_out agree
+ * with hk_calibrate's to fp32 rounding, and its selection is the exact Top-p of the c it
+ * computed (which it writes to c_out when given).
+ * Arguments as for hk_topp_select / hk_calibrate_topp, plus
+ *   workspace  device, 256-byte aligned, >= hk_select_workspace_size(n_heads, S_max)
+ *              bytes, used for the calibration pieces, the per-head histograms and
+ *              counters and each slot's key; overwritten by every call (calls that overlap
+ *              on one workspace race).
+ * S_max must be a multiple of 32 and at most 262144; x[m], c and c_out must be 16-byte
+ * aligned (HK_ERR_ALIGN).  HK_ERR_WORKSPACE for a workspace that is too small, HK_ERR_ALIGN
+ * for one not 256-byte aligned.
+ */
+size_t hk_select_workspace_size(int32_t n_heads, int32_t S_max);
+hk_status hk_topp_select_ws(int32_t n_heads, int32_t S_max, const int32_t* cand_len,
+                            const uint16_t* page_mask, const float* c, double p, int32_t k_min,
+                            int32_t k_max, uint32_t* sel_bits, int32_t* k_out,
+                            float* sel_mass_out, int32_t* status, void* workspace,
+                            size_t ws_bytes, hipStream_t stream);
+hk_status hk_calibrate_topp_ws(int32_t n_heads, int32_t S_max, const int32_t* cand_len,
+                               const uint16_t* page_mask, int32_t n_metrics,
+                               const float* const* x, const float* const* T, const float* w,
+                               double p, int32_t k_min, int32_t k_max, float* c_out,
+                               float* lse_out, uint32_t* sel_bits, int32_t* k_out,
+                               float* sel_mass_out, int32_t* status, void* workspace,
+                               size_t ws_bytes, hipStream_t stream);
+
 /* ------------------------------------------------------------------ a2 pooling
  * Order-preserving transform g of Solution 1 (Sec. 3.2, S_hat = S(g(z / T))) in the
  * SnapKV form used by the paper's baselines: for every candidate j of head h,
@@ -252,8 +288,9 @@ hk_status hk_calibrate_solve_T_gd(int32_t n_heads, int32_t S_max, const int32_t*
 
 /* ------------------------------------------------------------------ the whole step
  * One compression step (Sec. 3.1 Steps 2-3) in one call: hk_score (attention mass; row
- * LSEs computed, or taken from row_lse_in) -> hk_calibrate_topp (one metric, T = 1; the
- * calibrated probabilities stay on chip) -> hk_compact, on `stream`, in that order.  The
+ * LSEs computed, or taken from row_lse_in) -> hk_calibrate_topp_ws (one metric, T = 1;
+ * the calibrated probabilities are not written out) -> hk_compact, on `stream`, in that
+ * order.  The
  * scores, candidate counts, row LSEs and every stage's scratch live in `workspace`
  * (>= hk_workspace_size(HK_OP_COMPRESS, dims, max_pages) bytes, 256-byte aligned).
  * Outputs: k_out [n_heads] (the Top-p counts), sel_bits_out [n_heads][S_max/32] or NULL

@@ -21,12 +21,14 @@ __all__ = ["HardKVError", "lib", "PagedKV", "Allocator", "hk_score", "hk_calibra
            "hk_pool_max", "hk_score_rows", "hk_vote_topp", "hk_budget_plan", "hk_budget_select",
            "hk_compact_modes", "hk_calibrate_solve_T_gd", "hk_alloc_init", "hk_compress", "OP_COMPRESS", "BUDGET_KEEP", "BUDGET_SPARSE", "BUDGET_REWRITE",
            "hk_probe", "PROBE_EXP", "PROBE_MFMA", "hk_decode_plan",
-           "hk_decode_attn_noalloc", "hk_decode_noalloc_scratch_bytes", "ERR_SCRATCH"]
+           "hk_decode_attn_noalloc", "hk_decode_noalloc_scratch_bytes", "ERR_SCRATCH",
+           "OP_SELECT", "hk_select_workspace_size", "select_workspace", "hk_topp_select_ws",
+           "hk_calibrate_topp_ws"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhardkv.so")
 
 HK_F32, HK_BF16 = 0, 1
-OP_SCORE, OP_COMPACT, OP_DECODE, OP_APPEND, OP_COMPRESS = 0, 1, 2, 3, 4
+OP_SCORE, OP_COMPACT, OP_DECODE, OP_APPEND, OP_COMPRESS, OP_SELECT = 0, 1, 2, 3, 4, 5
 FLAG_NOSPACE, FLAG_NAN, FLAG_RANGE = 1, 2, 4
 ERR_SCRATCH = 7
 BUDGET_KEEP, BUDGET_SPARSE, BUDGET_REWRITE = 0, 1, 2
@@ -36,7 +38,8 @@ EXPORTED = ["hk_score", "hk_calibrate", "hk_calibrate_solve_T", "hk_topp_select"
             "hk_timing_enable", "hk_timing_read", "hk_calibrate_topp", "hk_pool_max",
             "hk_score_rows", "hk_vote_topp", "hk_budget_plan", "hk_budget_select",
             "hk_compact_modes", "hk_calibrate_solve_T_gd", "hk_alloc_init", "hk_compress",
-            "hk_probe", "hk_decode_plan", "hk_decode_attn_noalloc", "hk_decode_noalloc_scratch_bytes"]
+            "hk_probe", "hk_decode_plan", "hk_decode_attn_noalloc", "hk_decode_noalloc_scratch_bytes",
+            "hk_select_workspace_size", "hk_topp_select_ws", "hk_calibrate_topp_ws"]
 # kernel ids of hk_timing_read, in header order
 TIMED_KERNELS = ["score_pass1", "score_merge", "score_pass2", "calibrate", "topp", "solve_T",
                  "compact_gather", "compact_meta", "decode_split", "decode_merge", "append",
@@ -101,6 +104,14 @@ def lib():
         L.hk_calibrate_topp.argtypes = [I32, I32, P, P, I32, C.POINTER(C.c_void_p),
                                         C.POINTER(C.c_void_p), C.POINTER(C.c_float), D, I32, I32,
                                         P, P, P, P, P, P, P]
+        L.hk_select_workspace_size.restype = SZ
+        L.hk_select_workspace_size.argtypes = [I32, I32]
+        L.hk_topp_select_ws.restype = I32
+        L.hk_topp_select_ws.argtypes = [I32, I32, P, P, P, D, I32, I32, P, P, P, P, P, SZ, P]
+        L.hk_calibrate_topp_ws.restype = I32
+        L.hk_calibrate_topp_ws.argtypes = [I32, I32, P, P, I32, C.POINTER(C.c_void_p),
+                                           C.POINTER(C.c_void_p), C.POINTER(C.c_float), D, I32,
+                                           I32, P, P, P, P, P, P, P, SZ, P]
         L.hk_pool_max.restype = I32
         L.hk_pool_max.argtypes = [I32, I32, P, P, P, I32, P, P]
         L.hk_score_rows.restype = I32
@@ -251,6 +262,42 @@ def hk_calibrate_topp(n_heads: int, S_max: int, cand_len, page_mask, xs, Ts, wei
                                    xa, Ta, wa, float(p), int(k_min), int(k_max), _ptr(c_out),
                                    _ptr(lse_out), _ptr(sel_bits), _ptr(k_out), _ptr(sel_mass),
                                    _ptr(status), _stream(stream)), "hk_calibrate_topp")
+
+
+def hk_select_workspace_size(n_heads: int, S_max: int) -> int:
+    return int(lib().hk_select_workspace_size(int(n_heads), int(S_max)))
+
+
+def select_workspace(n_heads: int, S_max: int, device) -> torch.Tensor:
+    """Workspace of hk_topp_select_ws / hk_calibrate_topp_ws for these sizes."""
+    n = max(256, hk_select_workspace_size(n_heads, S_max))
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def hk_topp_select_ws(n_heads: int, S_max: int, cand_len, page_mask, c, p: float, sel_bits, k_out,
+                      ws, k_min: int = 1, k_max: int = 0, sel_mass=None, status=None, stream=None):
+    _check(lib().hk_topp_select_ws(int(n_heads), int(S_max), _ptr(cand_len), _ptr(page_mask),
+                                   _ptr(c), float(p), int(k_min), int(k_max), _ptr(sel_bits),
+                                   _ptr(k_out), _ptr(sel_mass), _ptr(status), _ptr(ws),
+                                   ws.numel() * ws.element_size(), _stream(stream)),
+           "hk_topp_select_ws")
+
+
+def hk_calibrate_topp_ws(n_heads: int, S_max: int, cand_len, page_mask, xs, Ts, weights, p: float,
+                         sel_bits, k_out, ws, c_out=None, lse_out=None, k_min: int = 1,
+                         k_max: int = 0, sel_mass=None, status=None, stream=None):
+    m = len(xs)
+    xa = (C.c_void_p * m)(*[t.data_ptr() for t in xs])
+    Ta = None
+    if Ts is not None:
+        Ta = (C.c_void_p * m)(*[(t.data_ptr() if t is not None else None) for t in Ts])
+    wa = (C.c_float * m)(*[float(w) for w in weights])
+    _check(lib().hk_calibrate_topp_ws(int(n_heads), int(S_max), _ptr(cand_len), _ptr(page_mask),
+                                      m, xa, Ta, wa, float(p), int(k_min), int(k_max),
+                                      _ptr(c_out), _ptr(lse_out), _ptr(sel_bits), _ptr(k_out),
+                                      _ptr(sel_mass), _ptr(status), _ptr(ws),
+                                      ws.numel() * ws.element_size(), _stream(stream)),
+           "hk_calibrate_topp_ws")
 
 
 def hk_pool_max(n_heads: int, S_max: int, cand_len, page_mask, x, radius: int, x_out, stream=None):

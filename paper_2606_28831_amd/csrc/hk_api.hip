@@ -1,5 +1,6 @@
 // C ABI of libhardkv: argument validation and dispatch to the HIP launchers.
 // Declarations, argument meaning and error behaviour: include/hardkv.h.
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 
@@ -10,6 +11,7 @@ bool hk_decode_supports_group(int G);
 namespace {
 
 constexpr int kMaxSlots = 32768;   // per-head logical slots held in registers by the selectors
+constexpr int kMaxSlotsWide = 262144;   // per-head slots of the multi-workgroup selector
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 bool aligned256(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 255u) == 0; }
@@ -43,12 +45,20 @@ hk_status check_rows(int n_heads, int S_max, const int32_t* cand_len) {
   return HK_OK;
 }
 
+hk_status check_rows_wide(int n_heads, int S_max, const int32_t* cand_len) {
+  if (n_heads <= 0 || S_max <= 0 || !cand_len) return HK_ERR_ARG;
+  if (S_max % 32 != 0 || S_max > kMaxSlotsWide) return HK_ERR_SHAPE;
+  if (n_heads > 1 << 20) return HK_ERR_SHAPE;
+  return HK_OK;
+}
+
 hk_status launched(hipError_t e) { return e == hipSuccess ? HK_OK : HK_ERR_HIP; }
 
 size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Workspace of hk_compress: scores, candidate counts, row LSEs, selection, then the score
-// and compaction scratch (the two stages run one after the other; they share one region).
+// Workspace of hk_compress: scores, candidate counts, row LSEs, selection, then the score,
+// selection and compaction scratch (the stages run one after the other; they share one
+// region).
 struct CompressWs {
   size_t s, cand, lse, sel, scratch, total;
 };
@@ -62,7 +72,8 @@ CompressWs compress_ws(const hk_dims* d, int max_pages) {
   w.scratch = w.sel + al256(H * (S / 32) * 4);
   const size_t a = hk_score_ws(d->NS, d->Hq, d->Hkv, d->D, d->W, max_pages);
   const size_t b = hk_compact_ws((int)H, max_pages);
-  w.total = w.scratch + al256(a > b ? a : b);
+  const size_t c = hk_select_wide_ws((int)H, (int)S);
+  w.total = w.scratch + al256(std::max(a, std::max(b, c)));
   return w;
 }
 
@@ -78,6 +89,7 @@ size_t hk_workspace_size(int32_t op, const hk_dims* d, int32_t max_pages) {
     case HK_OP_DECODE: return hk_decode_ws(d->NS, d->Hq, d->Hkv, d->D, max_pages);
     case HK_OP_APPEND: return hk_append_ws(d->NS, d->Hkv);
     case HK_OP_COMPRESS: return compress_ws(d, max_pages).total;
+    case HK_OP_SELECT: return hk_select_wide_ws(d->NS * d->Hkv, max_pages * HK_PAGE);
     default: return 0;
   }
 }
@@ -202,6 +214,58 @@ hk_status hk_calibrate_topp(int32_t n_heads, int32_t S_max, const int32_t* cand_
                                        lse_out, sel_bits, k_out, sel_mass_out, status, stream));
 }
 
+size_t hk_select_workspace_size(int32_t n_heads, int32_t S_max) {
+  if (n_heads <= 0 || S_max <= 0) return 0;
+  return hk_select_wide_ws(n_heads, S_max);
+}
+
+hk_status hk_topp_select_ws(int32_t n_heads, int32_t S_max, const int32_t* cand_len,
+                            const uint16_t* page_mask, const float* c, double p, int32_t k_min,
+                            int32_t k_max, uint32_t* sel_bits, int32_t* k_out,
+                            float* sel_mass_out, int32_t* status, void* workspace,
+                            size_t ws_bytes, hipStream_t stream) {
+  hk_status e = check_rows_wide(n_heads, S_max, cand_len);
+  if (e) return e;
+  if (!c || !sel_bits || !k_out) return HK_ERR_ARG;
+  if (!(p >= 0.0 && p <= 1.0)) return HK_ERR_ARG;
+  if (!aligned16(sel_bits) || !aligned16(c)) return HK_ERR_ALIGN;
+  if (!workspace || ws_bytes < hk_select_wide_ws(n_heads, S_max)) return HK_ERR_WORKSPACE;
+  if (!aligned256(workspace)) return HK_ERR_ALIGN;
+  const int p_q = (int)std::nearbyint(p * 1e6);
+  return launched(hk_launch_select_wide(n_heads, S_max, cand_len, page_mask, 0, nullptr, nullptr,
+                                        nullptr, nullptr, 0.f, 0.f, c, p_q, k_min, k_max, nullptr,
+                                        nullptr, sel_bits, k_out, sel_mass_out, status, workspace,
+                                        stream));
+}
+
+hk_status hk_calibrate_topp_ws(int32_t n_heads, int32_t S_max, const int32_t* cand_len,
+                               const uint16_t* page_mask, int32_t n_metrics,
+                               const float* const* x, const float* const* T, const float* w,
+                               double p, int32_t k_min, int32_t k_max, float* c_out,
+                               float* lse_out, uint32_t* sel_bits, int32_t* k_out,
+                               float* sel_mass_out, int32_t* status, void* workspace,
+                               size_t ws_bytes, hipStream_t stream) {
+  hk_status e = check_rows_wide(n_heads, S_max, cand_len);
+  if (e) return e;
+  if (n_metrics < 1 || n_metrics > 2 || !x || !w || !sel_bits || !k_out) return HK_ERR_ARG;
+  for (int m = 0; m < n_metrics; ++m)
+    if (!x[m] || !std::isfinite(w[m])) return HK_ERR_ARG;
+  if (!(p >= 0.0 && p <= 1.0)) return HK_ERR_ARG;
+  if (!aligned16(sel_bits) || (c_out && !aligned16(c_out))) return HK_ERR_ALIGN;
+  for (int m = 0; m < n_metrics; ++m)
+    if (!aligned16(x[m])) return HK_ERR_ALIGN;
+  if (!workspace || ws_bytes < hk_select_wide_ws(n_heads, S_max)) return HK_ERR_WORKSPACE;
+  if (!aligned256(workspace)) return HK_ERR_ALIGN;
+  const int p_q = (int)std::nearbyint(p * 1e6);
+  const float* T0 = T ? T[0] : nullptr;
+  const float* T1 = (T && n_metrics > 1) ? T[1] : nullptr;
+  return launched(hk_launch_select_wide(n_heads, S_max, cand_len, page_mask, n_metrics, x[0],
+                                        n_metrics > 1 ? x[1] : nullptr, T0, T1, w[0],
+                                        n_metrics > 1 ? w[1] : 0.f, nullptr, p_q, k_min, k_max,
+                                        c_out, lse_out, sel_bits, k_out, sel_mass_out, status,
+                                        workspace, stream));
+}
+
 hk_status hk_pool_max(int32_t n_heads, int32_t S_max, const int32_t* cand_len,
                       const uint16_t* page_mask, const float* x, int32_t radius, float* x_out,
                       hipStream_t stream) {
@@ -285,8 +349,9 @@ hk_status hk_compress(const hk_dims* dims, const void* q_obs, const hk_paged_kv*
   const int n_heads = dims->NS * dims->Hkv, S_max = kv->max_pages * HK_PAGE;
   const float* xs[1] = {s};
   const float w1[1] = {1.0f};
-  e = hk_calibrate_topp(n_heads, S_max, cand, kv->page_mask, 1, xs, nullptr, w1, p, k_min, k_max,
-                        nullptr, nullptr, sel, k_out, nullptr, status, stream);
+  e = hk_calibrate_topp_ws(n_heads, S_max, cand, kv->page_mask, 1, xs, nullptr, w1, p, k_min,
+                           k_max, nullptr, nullptr, sel, k_out, nullptr, status, scratch,
+                           scratch_bytes, stream);
   if (e) return e;
   return hk_compact(dims, kv, sel, L_dense, L_sparse, alloc, status, scratch, scratch_bytes, stream);
 }

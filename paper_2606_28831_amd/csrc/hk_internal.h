@@ -226,6 +226,14 @@ hipError_t hk_launch_calib_topp(int n_heads, int S_max, const int32_t* cand_len,
                                 const float* T1, float w0, float w1, int p_q, int k_min, int k_max,
                                 float* c_out, float* lse_out, uint32_t* sel_bits, int32_t* k_out,
                                 float* sel_mass, int32_t* status, hipStream_t st);
+// the multi-workgroup selector (n_metrics = 0: Top-p of c_in alone)
+size_t hk_select_wide_ws(int n_heads, int S_max);
+hipError_t hk_launch_select_wide(int n_heads, int S_max, const int32_t* cand_len,
+                                 const uint16_t* mask, int n_metrics, const float* x0,
+                                 const float* x1, const float* T0, const float* T1, float w0,
+                                 float w1, const float* c_in, int p_q, int k_min, int k_max,
+                                 float* c_out, float* lse_out, uint32_t* sel_bits, int32_t* k_out,
+                                 float* sel_mass, int32_t* status, void* ws, hipStream_t st);
 hipError_t hk_launch_pool_max(int n_heads, int S_max, const int32_t* cand_len, const uint16_t* mask,
                               const float* x, int radius, float* out, hipStream_t st);
 hipError_t hk_launch_solve_T_gd(int n_heads, int S_max, const int32_t* cand_len, const uint16_t* mask,

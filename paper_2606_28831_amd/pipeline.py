@@ -14,8 +14,8 @@ import torch
 
 from . import (Allocator, PagedKV, OP_APPEND, OP_COMPACT, OP_DECODE, OP_SCORE, dims, hk_append_kv,
                hk_budget_plan, hk_budget_select, hk_calibrate, hk_calibrate_solve_T,
-               hk_calibrate_solve_T_gd, hk_calibrate_topp, hk_compact, hk_compact_modes, hk_decode_attn, hk_pool_max,
-               hk_score, hk_score_rows, hk_vote_topp, workspace)
+               hk_calibrate_solve_T_gd, hk_calibrate_topp_ws, hk_compact, hk_compact_modes, hk_decode_attn, hk_pool_max,
+               hk_score, hk_score_rows, hk_vote_topp, select_workspace, workspace)
 
 
 @dataclass
@@ -36,6 +36,7 @@ class CompressBuffers:
     status: torch.Tensor
     ws_score: torch.Tensor
     ws_compact: torch.Tensor
+    ws_select: torch.Tensor
 
 
 class Compressor:
@@ -88,6 +89,7 @@ class Compressor:
             status=torch.zeros(1, dtype=i32, device=dev),
             ws_score=workspace(OP_SCORE, self.d, kv.max_pages, dev),
             ws_compact=workspace(OP_COMPACT, self.d, kv.max_pages, dev),
+            ws_select=select_workspace(H, S, dev),
         )
 
     def score(self, q_obs, ref_slots=None, row_lse_in=None, stream=None):
@@ -108,16 +110,17 @@ class Compressor:
         else:
             if b.T_red is None:
                 # temperature of the redundancy metric, solved at the first compression only
-                hk_calibrate_topp(H, S, b.cand_len, pm, [s_attn], None, [1.0], self.p, b.sel_bits,
-                                  b.k_attn, c_out=b.c_attn if self.keep_c else None,
-                                  sel_mass=b.mass_attn, status=b.status, stream=stream)
+                hk_calibrate_topp_ws(H, S, b.cand_len, pm, [s_attn], None, [1.0], self.p,
+                                     b.sel_bits, b.k_attn, b.ws_select,
+                                     c_out=b.c_attn if self.keep_c else None,
+                                     sel_mass=b.mass_attn, status=b.status, stream=stream)
                 b.T_red = torch.empty(H, dtype=torch.float32, device=b.c.device)
                 solve = hk_calibrate_solve_T_gd if self.t_solver == "gd" else hk_calibrate_solve_T
                 solve(H, S, b.cand_len, pm, b.x_red, b.k_attn, b.mass_attn, b.T_red, stream=stream)
             xs, Ts, ws = [s_attn, b.x_red], [None, b.T_red], [0.5, 0.5]
-        hk_calibrate_topp(H, S, b.cand_len, pm, xs, Ts, ws, self.p, b.sel_bits, b.k,
-                          c_out=b.c if self.keep_c else None, k_max=self.k_max,
-                          sel_mass=b.sel_mass, status=b.status, stream=stream)
+        hk_calibrate_topp_ws(H, S, b.cand_len, pm, xs, Ts, ws, self.p, b.sel_bits, b.k,
+                             b.ws_select, c_out=b.c if self.keep_c else None, k_max=self.k_max,
+                             sel_mass=b.sel_mass, status=b.status, stream=stream)
 
     def compact(self, stream=None):
         b = self.buf

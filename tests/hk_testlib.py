@@ -312,3 +312,43 @@ class DecodeReplay:
             self.mask[h] = [e.mask for e in res.pages]
             self.n[h] = len(res.pages)
         self._pack()
+
+
+def topp_edge_inputs(kind: str, S: int, seed: int = 7):
+    """Seeded Top-p inputs of one kind over six heads of S slots whose candidate counts
+    cover full, about half with a ragged tail, one, none, 33 and the last full word:
+    returns (c [6][S] fp32, cand_len [6] int32, k_min, k_max, p)."""
+    H = 6
+    rng = np.random.default_rng(seed)
+    c = np.zeros((H, S), np.float32)
+    cand_len = np.array([S, S // 2 - 24, 1, 0, 33, (S - 1) // 32 * 32], np.int32)
+    kmin, kmax, p = 1, 0, 0.9
+    for h in range(H):
+        n = cand_len[h]
+        if kind == "crowded":
+            # one binade, distinct low mantissa bits: the search's low-bit phase sees them all
+            c[h, :n] = ((1.0 + rng.integers(0, 1 << 12, n) * 2.0 ** -12) / (2 * max(n, 1))).astype(np.float32)
+        elif kind == "spread":
+            # log-uniform over ~30 binades
+            c[h, :n] = np.exp2(-rng.random(n) * 30.0).astype(np.float32) / max(n, 1)
+        elif kind == "uniform":
+            c[h, :n] = np.float32(1.0 / max(n, 1))
+        elif kind == "ties":
+            c[h, :n] = rng.choice(np.float32([0.5, 0.25, 0.125]), n) / max(n, 1)
+        elif kind == "onehot":
+            if n:
+                c[h, rng.integers(0, n)] = 1.0
+        elif kind == "nan_range":
+            c[h, :n] = rng.random(n).astype(np.float32) / max(n, 1)
+            if n > 3:
+                c[h, 1] = np.nan
+                c[h, 2] = 3.0
+                c[h, 3] = -0.5
+        elif kind == "zeros":
+            pass
+        elif kind == "clamp":
+            c[h, :n] = rng.dirichlet(np.ones(max(n, 1)))[:n].astype(np.float32)
+            kmin, kmax, p = 5, 40, 0.99
+        else:
+            raise ValueError(kind)
+    return c, cand_len, kmin, kmax, p

@@ -57,6 +57,10 @@ def test_workspace_sizes(hk):
     cw = hk.hk_workspace_size(hk.OP_COMPRESS, d, 2048)
     assert cw >= 128 * 2048 * 16 * 4 + max(hk.hk_workspace_size(hk.OP_SCORE, d, 2048),
                                            hk.hk_workspace_size(hk.OP_COMPACT, d, 2048))
+    # the wide selector: a key per slot, and the same figure through the dims form
+    sw = hk.hk_select_workspace_size(128, 32768)
+    assert sw >= 128 * 32768 * 4 and hk.hk_workspace_size(hk.OP_SELECT, d, 2048) == sw
+    assert cw >= 128 * 2048 * 16 * 4 + sw
     assert hk.hk_workspace_size(99, d, 2048) == 0
 
 
@@ -123,6 +127,24 @@ def test_validation_errors_without_gpu(hk):
                                None, None, None) == 1                   # p outside [0, 1]
     assert L.hk_calibrate_topp(4, 128, P, None, 1, xs, None, wts, 0.9, 1, 0, None, None, P + 4, P,
                                None, None, None) == 4                   # bitmap alignment
+    # the multi-workgroup selector: up to 262144 slots, and a workspace of the stated size
+    need = L.hk_select_workspace_size(4, 131072)
+    assert need >= 4 * 131072 * 4
+    assert L.hk_select_workspace_size(4, 262144) > need
+    assert L.hk_topp_select_ws(4, 262144 + 32, P, None, P, 0.9, 1, 0, P, P, None, None, P,
+                               1 << 40, None) == 3              # beyond 262144 slots
+    assert L.hk_topp_select_ws(4, 131072, P, None, P, 0.9, 1, 0, P, P, None, None, P, need - 1,
+                               None) == 5                       # workspace too small
+    assert L.hk_topp_select_ws(4, 131072, P, None, P, 0.9, 1, 0, P, P, None, None, P + 16, need,
+                               None) == 4                       # workspace alignment
+    assert L.hk_topp_select_ws(4, 131072, P, None, None, 0.9, 1, 0, P, P, None, None, P, need,
+                               None) == 1                       # no c
+    assert L.hk_calibrate_topp_ws(4, 131072, P, None, 3, xs, None, wts, 0.9, 1, 0, None, None, P,
+                                  P, None, None, P, need, None) == 1   # three metrics
+    assert L.hk_calibrate_topp_ws(4, 131072, P, None, 1, xs, None, wts, 0.9, 1, 0, None, None,
+                                  P + 4, P, None, None, P, need, None) == 4   # bitmap alignment
+    assert L.hk_calibrate_topp_ws(4, 100, P, None, 1, xs, None, wts, 0.9, 1, 0, None, None, P, P,
+                                  None, None, P, need, None) == 3      # S_max % 32
     assert L.hk_calibrate_solve_T_gd(4, 128, P, None, P, P, P, 0.0, 0.05, 10, 0.0, P, None,
                                      None) == 1                 # T_init
     assert L.hk_calibrate_solve_T_gd(4, 128, P, None, P, P, P, 1.0, -0.1, 10, 0.0, P, None,

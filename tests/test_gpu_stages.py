@@ -16,7 +16,7 @@ import oracle as O
 import workload as WL
 from hk_testlib import (RTOL, HostCache, check_compaction, check_lse, check_log_scores,
                         check_prob, check_topp_rule, np64, np_i, q_rows, rewritten_sources,
-                        snapshot, unpack_bits)
+                        snapshot, topp_edge_inputs, unpack_bits)
 
 pytestmark = pytest.mark.gpu
 
@@ -76,6 +76,41 @@ def test_score_attention_mass(name, L_dense):
         check_log_scores(s_np[h], full, rtol, f"s head {h}")
         sq, kvh = divmod(h, cfg["Hkv"])
         check_lse(lse_np[:, sq, kvh * G:(kvh + 1) * G].reshape(-1), lr, rtol, f"row_lse head {h}")
+
+
+def test_score_heads_shorter_than_the_table():
+    """Scores and row LSEs where the table spans three 128-page workgroup chunks and the
+    heads end early: no page, one page, exactly one chunk, one chunk and a partial one, and
+    every page -- chunks past a head's last page have nothing to load."""
+    import paper_2606_28831_amd as hk
+    cfg = dict(L=1, B=5, Hq=4, Hkv=1, D=128, N=384 * 16, dtype="bf16", W=32, seed=41,
+               recipe="normal")
+    w = WL.make_workload(cfg, DEV, max_pages=384)
+    H, S, G = w.n_heads, w.S_max, 4
+    for h, n in enumerate([0, 1, 128, 135, 384]):
+        w.n_pages[h] = n
+        w.page_table[h, n:] = -1
+        w.page_mask[h, n:] = 0
+    kv = hk.PagedKV(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)
+    d = hk.dims(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"], cfg["W"])
+    s = torch.full((H, S), 7.0, device=DEV)
+    cl = torch.empty(H, dtype=torch.int32, device=DEV)
+    lse = torch.empty(cfg["W"], w.NS, cfg["Hq"], device=DEV)
+    scale = 1 / math.sqrt(cfg["D"])
+    hk.hk_score(d, w.q_obs, kv, 0, scale, s, cl, row_lse_out=lse,
+                ws=hk.workspace(hk.OP_SCORE, d, w.max_pages, DEV))
+    torch.cuda.synchronize()
+    host = HostCache(w.k_pool, None, w.page_table, w.page_mask, w.n_pages)
+    qn, s_np, lse_np = np64(w.q_obs), np64(s), np64(lse)
+    for h in range(H):
+        rows, valid = host.head(h)
+        n = int(host.n[h])
+        assert int(cl[h]) == 16 * n
+        sr, lr = O.score_head(q_rows(qn, h, cfg["Hkv"], G), rows, valid, 16 * n, scale)
+        full = np.full(S, -np.inf)
+        full[:len(sr)] = sr
+        check_log_scores(s_np[h], full, RTOL["bf16"], f"s head {h}")
+        check_lse(lse_np[:, h, :].reshape(-1), lr, RTOL["bf16"], f"row_lse head {h}")
 
 
 @pytest.mark.parametrize("name", ["cfg1_f32_d64_g4", "bf16_d128_g4_ragged_holes",
@@ -214,37 +249,8 @@ def test_calibrate_and_topp(name):
                                     ("uniform", 32768)])
 def test_topp_edge_cases(kind, S):
     import paper_2606_28831_amd as hk
-    H = 6
-    rng = np.random.default_rng(7)
-    c = np.zeros((H, S), np.float32)
-    cand_len = np.array([S, S // 2 - 24, 1, 0, 33, (S - 1) // 32 * 32], np.int32)
-    kmin, kmax, p = 1, 0, 0.9
-    for h in range(H):
-        n = cand_len[h]
-        if kind == "crowded":
-            # one binade, distinct low mantissa bits: the search's low-bit phase sees them all
-            c[h, :n] = ((1.0 + rng.integers(0, 1 << 12, n) * 2.0 ** -12) / (2 * max(n, 1))).astype(np.float32)
-        elif kind == "spread":
-            # log-uniform over ~30 binades
-            c[h, :n] = np.exp2(-rng.random(n) * 30.0).astype(np.float32) / max(n, 1)
-        elif kind == "uniform":
-            c[h, :n] = np.float32(1.0 / max(n, 1))
-        elif kind == "ties":
-            c[h, :n] = rng.choice(np.float32([0.5, 0.25, 0.125]), n) / max(n, 1)
-        elif kind == "onehot":
-            if n:
-                c[h, rng.integers(0, n)] = 1.0
-        elif kind == "nan_range":
-            c[h, :n] = rng.random(n).astype(np.float32) / max(n, 1)
-            if n > 3:
-                c[h, 1] = np.nan
-                c[h, 2] = 3.0
-                c[h, 3] = -0.5
-        elif kind == "zeros":
-            pass
-        elif kind == "clamp":
-            c[h, :n] = rng.dirichlet(np.ones(max(n, 1)))[:n].astype(np.float32)
-            kmin, kmax, p = 5, 40, 0.99
+    c, cand_len, kmin, kmax, p = topp_edge_inputs(kind, S)
+    H = c.shape[0]
     ct = torch.tensor(c, device=DEV)
     clt = torch.tensor(cand_len, device=DEV)
     sel = torch.empty(H, S // 32, dtype=torch.int32, device=DEV)

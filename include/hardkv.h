@@ -419,7 +419,7 @@ hk_status hk_score_rows(const hk_dims* dims, const void* q_obs, const hk_paged_k
  *   votes    [n_heads][S_max] uint16, 16-byte aligned
  *   row_sel  [n_heads][R][S_max/32] uint32, caller-owned: every row's selection bitmap
  *   row_k    [n_heads][R] int32 or NULL: every row's selection size
- * R in [1, 256]; p in [0, 1]; S_max a multiple of 32, at most 32768.
+ * R in [1, 256]; p in [0, 1]; S_max a multiple of 32, at most 65536.
  */
 hk_status hk_vote_topp(int32_t n_heads, int32_t R, int32_t S_max, const int32_t* cand_len,
                        const uint16_t* page_mask, const float* a_rows, double p, uint16_t* votes,
@@ -447,7 +447,8 @@ hk_status hk_budget_plan(const hk_dims* dims, const hk_paged_kv* kv, int32_t L_d
  *   with NaN as 0 -- and its first min(|base|, cap) slots are kept,
  *   cap = max(0, k_cap[h] - |sinks|), no cap when k_cap is NULL or k_cap[h] < 0.
  * head_mode NULL treats every head as REWRITE.  Outputs sel_out [n_heads][S_max/32] uint32
- * (16-byte aligned) and k_out [n_heads] = number of selected slots.  n_sink >= 0.
+ * (16-byte aligned) and k_out [n_heads] = number of selected slots.  n_sink >= 0; S_max a
+ * multiple of 32, at most 65536.
  */
 hk_status hk_budget_select(int32_t n_heads, int32_t S_max, const int32_t* cand_len,
                            const uint16_t* page_mask, const uint16_t* votes, const float* c,

@@ -12,6 +12,7 @@ namespace {
 
 constexpr int kMaxSlots = 32768;   // per-head logical slots held in registers by the selectors
 constexpr int kMaxSlotsWide = 262144;   // per-head slots of the multi-workgroup selector
+constexpr int kMaxSlotsBudget = 65536;  // per-row slots of the vote and budget selection
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 bool aligned256(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 255u) == 0; }
@@ -38,18 +39,15 @@ hk_status check_kv(const hk_paged_kv* kv, bool need_v) {
   return HK_OK;
 }
 
-hk_status check_rows(int n_heads, int S_max, const int32_t* cand_len) {
+hk_status check_rows(int n_heads, int S_max, const int32_t* cand_len, int max_slots = kMaxSlots) {
   if (n_heads <= 0 || S_max <= 0 || !cand_len) return HK_ERR_ARG;
-  if (S_max % 32 != 0 || S_max > kMaxSlots) return HK_ERR_SHAPE;
+  if (S_max % 32 != 0 || S_max > max_slots) return HK_ERR_SHAPE;
   if (n_heads > 1 << 20) return HK_ERR_SHAPE;
   return HK_OK;
 }
 
 hk_status check_rows_wide(int n_heads, int S_max, const int32_t* cand_len) {
-  if (n_heads <= 0 || S_max <= 0 || !cand_len) return HK_ERR_ARG;
-  if (S_max % 32 != 0 || S_max > kMaxSlotsWide) return HK_ERR_SHAPE;
-  if (n_heads > 1 << 20) return HK_ERR_SHAPE;
-  return HK_OK;
+  return check_rows(n_heads, S_max, cand_len, kMaxSlotsWide);
 }
 
 hk_status launched(hipError_t e) { return e == hipSuccess ? HK_OK : HK_ERR_HIP; }
@@ -393,7 +391,7 @@ hk_status hk_score_rows(const hk_dims* dims, const void* q_obs, const hk_paged_k
 hk_status hk_vote_topp(int32_t n_heads, int32_t R, int32_t S_max, const int32_t* cand_len,
                        const uint16_t* page_mask, const float* a_rows, double p, uint16_t* votes,
                        uint32_t* row_sel, int32_t* row_k, int32_t* status, hipStream_t stream) {
-  hk_status e = check_rows(n_heads, S_max, cand_len);
+  hk_status e = check_rows(n_heads, S_max, cand_len, kMaxSlotsBudget);
   if (e) return e;
   if (R < 1 || R > 256) return HK_ERR_SHAPE;
   if (n_heads > 65535) return HK_ERR_SHAPE;
@@ -422,7 +420,7 @@ hk_status hk_budget_select(int32_t n_heads, int32_t S_max, const int32_t* cand_l
                            const uint16_t* page_mask, const uint16_t* votes, const float* c,
                            const uint32_t* sel_in, const int32_t* head_mode, const int32_t* k_cap,
                            int32_t n_sink, uint32_t* sel_out, int32_t* k_out, hipStream_t stream) {
-  hk_status e = check_rows(n_heads, S_max, cand_len);
+  hk_status e = check_rows(n_heads, S_max, cand_len, kMaxSlotsBudget);
   if (e) return e;
   if (!sel_out || !k_out || n_sink < 0) return HK_ERR_ARG;
   if (!aligned16(sel_out)) return HK_ERR_ALIGN;

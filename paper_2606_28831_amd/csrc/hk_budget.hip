@@ -10,30 +10,32 @@
 //   budget_select one workgroup per head: sinks, then the base set ranked by (votes, c,
 //                slot) and cut at the cap by a radix search on the 64-bit rank key.
 //
-// Layout: 512 threads per workgroup; slot j of a row is thread j % 512's element j / 512,
-// so a wave's 64 lanes cover 64 consecutive slots (coalesced loads; one ballot gives two
-// words of a bitmap).  A row's keys stay in registers (S_max <= 32768 -> <= 64 each).
+// Layout: NT threads per workgroup (512 up to 32768 slots, 1024 up to 65536); slot j of a
+// row is thread j % NT's element j / NT, so a wave's 64 lanes cover 64 consecutive slots
+// (coalesced loads; one ballot gives two words of a bitmap).  A row's keys stay in
+// registers (at most 64 each).
 #include "hk_internal.h"
 
 namespace hk {
 
-constexpr int BG_NT = 512;
-constexpr int BG_NW = BG_NT / 64;
 constexpr int RADIX_BITS = 11;
 constexpr int RADIX_BINS = 1 << RADIX_BITS;
-constexpr int BINS_PER_THREAD = RADIX_BINS / BG_NT;
 constexpr int BG_EPT_MAX = 64;
+constexpr int BG_SLOTS_512 = 512 * BG_EPT_MAX;    // rows up to this many slots take 512 threads
 
 constexpr int BG_LIST_BYTES = 32768;   // keys of the boundary digit, staged for later rounds
 
+template <int NT>
 struct BgLds {
+  static constexpr int NW = NT / 64;
+  static constexpr int BPT = RADIX_BINS / NT;    // histogram digits per thread
   unsigned long long hist[RADIX_BINS];
   uint32_t list[BG_LIST_BYTES / 4];
-  uint16_t mrow[BG_EPT_MAX * BG_NT / HK_PAGE];   // the head's page masks
-  unsigned long long red64[BG_NW];
-  uint32_t redu[2][BG_NW];
-  int redi[BG_NW];
-  int tiecnt[BG_EPT_MAX * BG_NW];
+  uint16_t mrow[BG_EPT_MAX * NT / HK_PAGE];      // the head's page masks
+  unsigned long long red64[NW];
+  uint32_t redu[2][NW];
+  int redi[NW];
+  int tiecnt[BG_EPT_MAX * NW];
   unsigned long long pick_above;
   uint32_t pick_digit;
 };
@@ -96,8 +98,9 @@ __device__ __forceinline__ uint64_t wave_minmax_u64(uint64_t v) {
 }
 
 // Block minimum and maximum of one key per thread (u32 or u64 keys).
-template <typename K>
-__device__ __forceinline__ void block_key_range(K kmin, K kmax, BgLds& sh, K* out_min, K* out_max) {
+template <typename K, int NT>
+__device__ __forceinline__ void block_key_range(K kmin, K kmax, BgLds<NT>& sh, K* out_min, K* out_max) {
+  constexpr int BG_NW = NT / 64;
   const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
   if constexpr (sizeof(K) == 8) {
     kmin = wave_minmax_u64<false>(kmin);
@@ -136,7 +139,9 @@ __device__ __forceinline__ void block_key_range(K kmin, K kmax, BgLds& sh, K* ou
   }
 }
 
+template <int NT>
 __device__ __forceinline__ uint32_t block_sum_u32(uint32_t v, uint32_t* red) {
+  constexpr int BG_NW = NT / 64;
   v = wave_reduce_u32(v, 0u, [](uint32_t a, uint32_t b) { return a + b; });
   __syncthreads();
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
@@ -148,7 +153,9 @@ __device__ __forceinline__ uint32_t block_sum_u32(uint32_t v, uint32_t* red) {
 }
 
 // Exclusive prefix (thread order) of one int per thread (.x) and the block sum (.y).
+template <int NT>
 __device__ __forceinline__ int2 block_exscan_bg(int v, int* red) {
+  constexpr int BG_NW = NT / 64;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   int x = v;
 #pragma unroll
@@ -173,11 +180,12 @@ __device__ __forceinline__ int2 block_exscan_bg(int v, int* red) {
 // the threads' sums finds the one thread whose digits hold the crossing.
 // On the first round the target is not known yet: it is target_of(the histogram's total),
 // which is every member's weight; it comes back in *target (0: nothing to reach, no digit).
-template <typename TF>
-__device__ __forceinline__ void pick_digit(BgLds& sh, bool first, TF target_of,
+template <int NT, typename TF>
+__device__ __forceinline__ void pick_digit(BgLds<NT>& sh, bool first, TF target_of,
                                            unsigned long long* target_io,
                                            unsigned long long above, uint32_t* d_out,
                                            unsigned long long* above_out) {
+  constexpr int BG_NW = NT / 64, BINS_PER_THREAD = RADIX_BINS / NT;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   unsigned long long own = 0;
 #pragma unroll
@@ -219,7 +227,9 @@ __device__ __forceinline__ void pick_digit(BgLds& sh, bool first, TF target_of,
 }
 
 // Zero the histogram between two barriers.
-__device__ __forceinline__ void clear_hist(BgLds& sh) {
+template <int NT>
+__device__ __forceinline__ void clear_hist(BgLds<NT>& sh) {
+  constexpr int BINS_PER_THREAD = RADIX_BINS / NT;
   const int tid = threadIdx.x;
   __syncthreads();                   // earlier readers of the LDS scratch are done
 #pragma unroll
@@ -230,15 +240,15 @@ __device__ __forceinline__ void clear_hist(BgLds& sh) {
 // Stage into the LDS list the keys whose bits from `pos` up equal `prefix`, if they fit;
 // returns their number, or -1 when they do not fit (later rounds then read the registers).
 // Each thread counts its own, an exclusive scan gives its offset, and it writes them there.
-template <int EPT, typename K>
-__device__ __forceinline__ int stage_list(const K* key, int pos, K prefix, BgLds& sh) {
+template <int EPT, typename K, int NT>
+__device__ __forceinline__ int stage_list(const K* key, int pos, K prefix, BgLds<NT>& sh) {
   constexpr int CAP = BG_LIST_BYTES / (int)sizeof(K);
   K* list = reinterpret_cast<K*>(sh.list);
   const K m2 = ~low_mask<K>(pos);
   int cnt = 0;
 #pragma unroll
   for (int i = 0; i < EPT; ++i) cnt += ((key[i] & m2) == prefix) ? 1 : 0;
-  const int2 sc = block_exscan_bg(cnt, sh.redi);
+  const int2 sc = block_exscan_bg<NT>(cnt, sh.redi);
   if (sc.y > CAP) return -1;
   int off = sc.x;
 #pragma unroll
@@ -261,9 +271,9 @@ __device__ __forceinline__ int stage_list(const K* key, int pos, K prefix, BgLds
 // in registers; the keys that share the digits found so far are then packed into an LDS
 // list (when they fit) and the remaining rounds read only that list.  Returns v and, in
 // *above, W(key > v).
-template <int EPT, typename K, typename WF, typename TF>
+template <int EPT, typename K, typename WF, typename TF, int NT>
 __device__ __forceinline__ K radix_threshold(const K* key, TF target_of, WF weight, K kmin, K kmax,
-                                             BgLds& sh, unsigned long long* target_out,
+                                             BgLds<NT>& sh, unsigned long long* target_out,
                                              unsigned long long* above_out) {
   constexpr int CAP = BG_LIST_BYTES / (int)sizeof(K);
   const int tid = threadIdx.x;
@@ -274,7 +284,7 @@ __device__ __forceinline__ K radix_threshold(const K* key, TF target_of, WF weig
     int cnt = 0;
 #pragma unroll
     for (int i = 0; i < EPT; ++i) cnt += (key[i] == kmin) ? 1 : 0;
-    cnt = block_sum_int<BG_NT>(cnt, sh.redi);
+    cnt = block_sum_int<NT>(cnt, sh.redi);
     *target_out = target_of((unsigned long long)cnt * weight(kmin));
     return kmin;
   }
@@ -323,7 +333,7 @@ __device__ __forceinline__ K radix_threshold(const K* key, TF target_of, WF weig
           atomicAdd(&sh.hist[(uint32_t)(k >> lo) & dmask], weight(k));
       }
     } else {
-      for (int j = tid; j < n_list; j += BG_NT) {
+      for (int j = tid; j < n_list; j += NT) {
         const K k = list[j];
         if ((k & hi_mask) == prefix) atomicAdd(&sh.hist[(uint32_t)(k >> lo) & dmask], weight(k));
       }
@@ -341,9 +351,10 @@ __device__ __forceinline__ K radix_threshold(const K* key, TF target_of, WF weig
 }
 
 // Among the elements flagged in `tie`, select the `take` with the largest slot index
-// (slot = tid + BG_NT * i: later elements, then later waves, then higher lanes).
-template <int EPT>
+// (slot = tid + NT * i: later elements, then later waves, then higher lanes).
+template <int NT, int EPT>
 __device__ __forceinline__ uint64_t take_top_ties_bg(uint64_t tie, int take, int* cnt) {
+  constexpr int BG_NW = NT / 64;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   __syncthreads();
 #pragma unroll
@@ -374,20 +385,20 @@ __device__ __forceinline__ uint64_t take_top_ties_bg(uint64_t tie, int take, int
 // coalesced loads first: per-element global loads would each hold an address pair and a
 // value in registers while in flight, and inside per-element branches they would be
 // waited on one by one.
-template <int EPT>
+template <int EPT, int NT>
 __device__ __forceinline__ uint64_t cand_flags(int h, int S_max, const int32_t* __restrict__ cand_len,
-                                               const uint16_t* __restrict__ mask, BgLds& sh) {
+                                               const uint16_t* __restrict__ mask, BgLds<NT>& sh) {
   const int cl = min(cand_len[h], S_max);
   const int np = S_max / HK_PAGE;
   if (mask) {
     const uint16_t* mrow = mask + (size_t)h * np;
-    for (int q = threadIdx.x; q < np; q += BG_NT) sh.mrow[q] = mrow[q];
+    for (int q = threadIdx.x; q < np; q += NT) sh.mrow[q] = mrow[q];
   }
   __syncthreads();
   uint64_t f = 0;
 #pragma unroll
   for (int i = 0; i < EPT; ++i) {
-    const int j = threadIdx.x + BG_NT * i;
+    const int j = threadIdx.x + NT * i;
     const bool ok = j < cl && (!mask || (((uint32_t)sh.mrow[j >> 4] >> (j & 15)) & 1u));
     f |= ok ? 1ull << i : 0ull;
   }
@@ -395,7 +406,7 @@ __device__ __forceinline__ uint64_t cand_flags(int h, int S_max, const int32_t* 
 }
 
 // One bitmap row from per-element selection flags.
-template <int EPT>
+template <int NT, int EPT>
 __device__ __forceinline__ void write_bitmap(uint64_t sel, uint32_t* __restrict__ brow, int S_max) {
   // addresses and bounds computed afresh on each call: hoisted out of a row loop they would
   // hold registers per element for the whole loop
@@ -404,7 +415,7 @@ __device__ __forceinline__ void write_bitmap(uint64_t sel, uint32_t* __restrict_
 #pragma unroll
   for (int i = 0; i < EPT; ++i) {
     const unsigned long long b = __ballot((sel >> i) & 1ull);
-    const int j0 = BG_NT * i + 64 * wave;
+    const int j0 = NT * i + 64 * wave;
     if (lane == 0 && j0 < S_max) {
       brow[j0 / 32] = (uint32_t)b;
       if (j0 + 32 < S_max) brow[j0 / 32 + 1] = (uint32_t)(b >> 32);
@@ -414,14 +425,14 @@ __device__ __forceinline__ void write_bitmap(uint64_t sel, uint32_t* __restrict_
 
 // ------------------------------------------------------------------ Cautious Update votes
 // The head's page masks staged in LDS with every slot at or past cand_len cleared, for
-// all BG_NT * EPT slots a workgroup covers (pages past S_max hold no candidates).
-template <int EPT>
+// all NT * EPT slots a workgroup covers (pages past S_max hold no candidates).
+template <int EPT, int NT>
 __device__ __forceinline__ void stage_cand_masks(int h, int S_max, const int32_t* __restrict__ cand_len,
-                                                 const uint16_t* __restrict__ mask, BgLds& sh) {
+                                                 const uint16_t* __restrict__ mask, BgLds<NT>& sh) {
   const int cl = min(cand_len[h], S_max);
   const int np = S_max / HK_PAGE;
   const uint16_t* mrow = mask ? mask + (size_t)h * np : nullptr;
-  for (int q = threadIdx.x; q < EPT * BG_NT / HK_PAGE; q += BG_NT) {
+  for (int q = threadIdx.x; q < EPT * NT / HK_PAGE; q += NT) {
     const int keep = min(max(cl - q * HK_PAGE, 0), HK_PAGE);
     uint32_t m = (q < np && mrow) ? (uint32_t)mrow[q] : 0xffffu;
     sh.mrow[q] = (uint16_t)(m & ((1u << keep) - 1u));
@@ -429,10 +440,11 @@ __device__ __forceinline__ void stage_cand_masks(int h, int S_max, const int32_t
   __syncthreads();
 }
 
-// All ones when slot tid + BG_NT * i is a candidate, else zero (masks staged as above).
-__device__ __forceinline__ uint32_t cand_lanes(const BgLds& sh, int i) {
+// All ones when slot tid + NT * i is a candidate, else zero (masks staged as above).
+template <int NT>
+__device__ __forceinline__ uint32_t cand_lanes(const BgLds<NT>& sh, int i) {
   const int tid = threadIdx.x;
-  const uint32_t m = sh.mrow[(tid >> 4) + (BG_NT / HK_PAGE) * i];
+  const uint32_t m = sh.mrow[(tid >> 4) + (NT / HK_PAGE) * i];
   return (uint32_t)((int32_t)(m << (31 - (tid & 15))) >> 31);
 }
 
@@ -462,12 +474,13 @@ __device__ __forceinline__ void static_for(F&& f) {
 
 // Four waves per SIMD (two workgroups per CU) cap the registers at 128: the allocator
 // then keeps fewer loads in flight rather than lowering the occupancy.
-template <int EPT>
-__global__ __launch_bounds__(BG_NT) __attribute__((amdgpu_waves_per_eu(4, 8))) void vote_topp_kernel(
+template <int NT, int EPT>
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4, 8))) void vote_topp_kernel(
     int R, int S_max, const int32_t* __restrict__ cand_len,
     const uint16_t* __restrict__ mask, const float* __restrict__ a_rows, int p_q,
     uint32_t* __restrict__ row_sel, int32_t* __restrict__ row_k, int32_t* __restrict__ status) {
-  __shared__ BgLds sh;
+  constexpr int BG_NW = NT / 64;
+  __shared__ BgLds<NT> sh;
   constexpr uint32_t NONE = 0xffffffffu;  // key of a non-candidate
   constexpr uint32_t ONE = 0x3f800000u;   // bits of 1.0f: in-range probabilities are <= ONE
   const int h = blockIdx.y, tid = threadIdx.x;
@@ -483,7 +496,7 @@ __global__ __launch_bounds__(BG_NT) __attribute__((amdgpu_waves_per_eu(4, 8))) v
   uint32_t key[EPT];
 #pragma unroll
   for (int i = 0; i < EPT; ++i)
-    key[i] = __builtin_amdgcn_raw_buffer_load_b32(rs, (tid + BG_NT * i) * 4, 0, 0);
+    key[i] = __builtin_amdgcn_raw_buffer_load_b32(rs, (tid + NT * i) * 4, 0, 0);
   // a candidate keeps its bits, anything else takes the all-ones key; for non-negative
   // floats the bit order is the value order
   uint32_t kmin = NONE, kmax = 0u;
@@ -546,7 +559,7 @@ __global__ __launch_bounds__(BG_NT) __attribute__((amdgpu_waves_per_eu(4, 8))) v
   v = (uint32_t)__builtin_amdgcn_readfirstlane((int)v);     // uniform: from LDS
   take = __builtin_amdgcn_readfirstlane(take);
   // The row's bitmap straight from ballots: lane i of a wave keeps the wave's ballot of
-  // its element i (64 consecutive slots from BG_NT * i + 64 * wave, two bitmap words) for
+  // its element i (64 consecutive slots from NT * i + 64 * wave, two bitmap words) for
   // the keys at or above the threshold; the wave's counts stay scalar.
   uint32_t ge_lo = 0, ge_hi = 0;
   int n_ge = 0, n_eq = 0;
@@ -590,8 +603,8 @@ __global__ __launch_bounds__(BG_NT) __attribute__((amdgpu_waves_per_eu(4, 8))) v
     __syncthreads();
     sh.tiecnt[lane * BG_NW + wave] = __popc(eq_lo) + __popc(eq_hi);
     __syncthreads();
-    const int e = BG_NT - 1 - tid;     // entries in descending slot order
-    const int2 sc = block_exscan_bg(sh.tiecnt[e], sh.redi);
+    const int e = NT - 1 - tid;        // entries in descending slot order
+    const int2 sc = block_exscan_bg<NT>(sh.tiecnt[e], sh.redi);
     int* above = reinterpret_cast<int*>(sh.list);
     above[e] = sc.x;
     __syncthreads();
@@ -606,7 +619,7 @@ __global__ __launch_bounds__(BG_NT) __attribute__((amdgpu_waves_per_eu(4, 8))) v
     ge_hi = (uint32_t)(sel >> 32);
   }
   uint32_t* brow = row_sel + ((size_t)h * R + r) * (S_max / 32);
-  const int j0 = BG_NT * lane + 64 * wave;
+  const int j0 = NT * lane + 64 * wave;
   if (lane < EPT && j0 < S_max) {
     brow[j0 / 32] = ge_lo;
     if (j0 + 32 < S_max) brow[j0 / 32 + 1] = ge_hi;
@@ -725,20 +738,20 @@ __global__ __launch_bounds__(256) void budget_plan_kernel(int n_heads, int max_p
 }
 
 // ------------------------------------------------------------------ budget selection
-template <int EPT>
-__global__ __launch_bounds__(BG_NT) void budget_select_kernel(
+template <int NT, int EPT>
+__global__ __launch_bounds__(NT) void budget_select_kernel(
     int S_max, const int32_t* __restrict__ cand_len, const uint16_t* __restrict__ mask,
     const uint16_t* __restrict__ votes, const float* __restrict__ c, const uint32_t* __restrict__ sel_in,
     const int32_t* __restrict__ head_mode, const int32_t* __restrict__ k_cap, int n_sink,
     uint32_t* __restrict__ sel_out, int32_t* __restrict__ k_out) {
-  __shared__ BgLds sh;
+  __shared__ BgLds<NT> sh;
   const int h = blockIdx.x, tid = threadIdx.x;
   const uint64_t cf = cand_flags<EPT>(h, S_max, cand_len, mask, sh);
   const int mode = head_mode ? head_mode[h] : HK_BUDGET_REWRITE;
   uint32_t* brow = sel_out + (size_t)h * (S_max / 32);
   if (mode == HK_BUDGET_KEEP) {
-    write_bitmap<EPT>(cf, brow, S_max);
-    const int n = block_sum_int<BG_NT>(__popcll(cf), sh.redi);
+    write_bitmap<NT, EPT>(cf, brow, S_max);
+    const int n = block_sum_int<NT>(__popcll(cf), sh.redi);
     if (tid == 0) k_out[h] = n;
     return;
   }
@@ -752,7 +765,7 @@ __global__ __launch_bounds__(BG_NT) void budget_select_kernel(
   // loading all elements up front would not fit beside the 64-bit keys)
 #pragma unroll
   for (int i = 0; i < EPT; ++i) {
-    const int j = tid + BG_NT * i;
+    const int j = tid + NT * i;
     key[i] = ~0ull;
     if (!((cf >> i) & 1ull)) continue;
     if (j < n_sink) {
@@ -771,8 +784,8 @@ __global__ __launch_bounds__(BG_NT) void budget_select_kernel(
     kmin = min(kmin, key[i]);
     kmax = max(kmax, key[i]);
   }
-  const int n_sinks = block_sum_int<BG_NT>(__popcll(sinks), sh.redi);
-  const int n_base = block_sum_int<BG_NT>(__popcll(base), sh.redi);
+  const int n_sinks = block_sum_int<NT>(__popcll(sinks), sh.redi);
+  const int n_base = block_sum_int<NT>(__popcll(base), sh.redi);
   const int kc = k_cap ? k_cap[h] : -1;
   const int cap = kc < 0 ? n_base : min(n_base, max(0, kc - n_sinks));
   uint64_t sel = sinks;
@@ -796,34 +809,37 @@ __global__ __launch_bounds__(BG_NT) void budget_select_kernel(
         if (k == v) tie |= 1ull << i;
       }
     }
-    const int n_tie = block_sum_int<BG_NT>(__popcll(tie), sh.redi);
+    const int n_tie = block_sum_int<NT>(__popcll(tie), sh.redi);
     if (take >= n_tie) sel |= tie;
-    else if (take > 0) sel |= take_top_ties_bg<EPT>(tie, take, sh.tiecnt);
+    else if (take > 0) sel |= take_top_ties_bg<NT, EPT>(tie, take, sh.tiecnt);
   }
-  write_bitmap<EPT>(sel, brow, S_max);
+  write_bitmap<NT, EPT>(sel, brow, S_max);
   if (tid == 0) k_out[h] = n_sinks + cap;
 }
 
-template <template <int> class Launch, typename... A>
+// 512 threads and the fewest elements per thread that cover the row, or, past 512 * 64
+// slots, 1024 threads with 64 elements each
+template <template <int, int> class Launch, typename... A>
 hipError_t by_ept(int S_max, A... args) {
-  const int e = (S_max + BG_NT - 1) / BG_NT;
-  if (e <= 1) return Launch<1>::run(args...);
-  if (e <= 2) return Launch<2>::run(args...);
-  if (e <= 4) return Launch<4>::run(args...);
-  if (e <= 8) return Launch<8>::run(args...);
-  if (e <= 16) return Launch<16>::run(args...);
-  if (e <= 32) return Launch<32>::run(args...);
-  return Launch<64>::run(args...);
+  if (S_max > BG_SLOTS_512) return Launch<1024, 64>::run(args...);
+  const int e = (S_max + 511) / 512;
+  if (e <= 1) return Launch<512, 1>::run(args...);
+  if (e <= 2) return Launch<512, 2>::run(args...);
+  if (e <= 4) return Launch<512, 4>::run(args...);
+  if (e <= 8) return Launch<512, 8>::run(args...);
+  if (e <= 16) return Launch<512, 16>::run(args...);
+  if (e <= 32) return Launch<512, 32>::run(args...);
+  return Launch<512, 64>::run(args...);
 }
 
-template <int EPT>
+template <int NT, int EPT>
 struct VoteLaunch {
   static hipError_t run(int n_heads, int R, int S_max, const int32_t* cand_len, const uint16_t* mask,
                         const float* a_rows, int p_q, uint32_t* row_sel, int32_t* row_k,
                         int32_t* status, uint16_t* votes, hipStream_t st) {
     {
       TimedLaunch t(HK_TK_VOTE, st);
-      hipLaunchKernelGGL((vote_topp_kernel<EPT>), dim3(R, n_heads), dim3(BG_NT), 0, st, R, S_max,
+      hipLaunchKernelGGL((vote_topp_kernel<NT, EPT>), dim3(R, n_heads), dim3(NT), 0, st, R, S_max,
                          cand_len, mask, a_rows, p_q, row_sel, row_k, status);
     }
     {
@@ -836,14 +852,14 @@ struct VoteLaunch {
   }
 };
 
-template <int EPT>
+template <int NT, int EPT>
 struct BudgetSelectLaunch {
   static hipError_t run(int n_heads, int S_max, const int32_t* cand_len, const uint16_t* mask,
                         const uint16_t* votes, const float* c, const uint32_t* sel_in,
                         const int32_t* head_mode, const int32_t* k_cap, int n_sink, uint32_t* sel_out,
                         int32_t* k_out, hipStream_t st) {
     TimedLaunch t(HK_TK_BUDGET_SELECT, st);
-    hipLaunchKernelGGL((budget_select_kernel<EPT>), dim3(n_heads), dim3(BG_NT), 0, st, S_max, cand_len,
+    hipLaunchKernelGGL((budget_select_kernel<NT, EPT>), dim3(n_heads), dim3(NT), 0, st, S_max, cand_len,
                        mask, votes, c, sel_in, head_mode, k_cap, n_sink, sel_out, k_out);
     return hipGetLastError();
   }

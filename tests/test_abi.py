@@ -175,7 +175,9 @@ def test_validation_errors_without_gpu(hk):
     assert L.hk_budget_plan(C.byref(d), C.byref(kv), 0, 5, 10, None, P, None) == 1
     assert L.hk_budget_select(4, 128, P, None, None, None, None, None, None, -1, P, P, None) == 1
     assert L.hk_budget_select(4, 128, P, None, None, None, None, None, None, 0, P + 4, P, None) == 4
-    assert L.hk_budget_select(4, 65536, P, None, None, None, None, None, None, 0, P, P, None) == 3
+    assert L.hk_budget_select(4, 65536 + 32, P, None, None, None, None, None, None, 0, P, P,
+                              None) == 3                                # past 65536 slots
+    assert L.hk_vote_topp(4, 8, 65536 + 32, P, None, P, 0.9, P, P, None, None, None) == 3
     assert L.hk_compact_modes(C.byref(d), C.byref(kv), P, 0, None, C.byref(alloc), P, P, 1 << 30,
                               None) == 1                                # no head modes
     assert L.hk_compact_modes(C.byref(d), C.byref(kv), P, 0, P, C.byref(alloc), P, P, 16,

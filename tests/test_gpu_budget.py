@@ -132,8 +132,12 @@ def _rows(kind, H, R, S, cand_len, rng):
                                         ("mixed", 12, 512, 0.9), ("dirichlet", 1, 64, 1.0),
                                         ("dirichlet", 3, 32768, 0.9), ("crowded", 2, 16384, 0.9),
                                         ("dirichlet", 128, 256, 0.0), ("negzero", 6, 1056, 0.9),
-                                        ("ties", 4, 1536, 0.5), ("spread", 256, 512, 0.9)])
+                                        ("ties", 4, 1536, 0.5), ("spread", 256, 512, 0.9),
+                                        ("dirichlet", 2, 65536, 0.9), ("mixed", 4, 40960, 0.9),
+                                        ("ties", 2, 65536, 0.5)])
 def test_vote_topp(kind, R, S, p):
+    """Every row's own Top-p set and the column counts, against the oracle; rows of more
+    than 32768 slots take the 1024-thread workgroups."""
     import paper_2606_28831_amd as hk
     rng = np.random.default_rng(zlib.crc32(f"{kind}/{R}/{S}".encode()))
     H = 5
@@ -196,7 +200,7 @@ def test_budget_plan(name):
 
 
 # ---------------------------------------------------------------- budget selection
-@pytest.mark.parametrize("S", [64, 2048, 32768])
+@pytest.mark.parametrize("S", [64, 2048, 32768, 33792, 65536])
 @pytest.mark.parametrize("use", ["votes_c", "votes_only", "c_sel_in", "all"])
 def test_budget_select(S, use):
     import paper_2606_28831_amd as hk

@@ -110,8 +110,9 @@ def snapshot(w):
 
 
 def check_compaction(w, before, sel_np, S, ref_fn):
-    """The cache after a compaction call against ref_fn(h, sel) -> oracle CompactResult of
-    each head: layout, masks, kept page ids, byte-exact rewritten rows, and a free list that
+    """The cache after a compaction call against ref_fn(h, sel) -> the expected page list of
+    each head (the oracle's compaction for a seeded selection, rewrite_layout for the GPU's
+    own): layout, masks, kept page ids, byte-exact rewritten rows, and a free list that
     together with the live pages accounts for every page exactly once."""
     table, mask, n_new = np_i(w.page_table), np_i(w.page_mask).astype(np.int64) & 0xFFFF, np_i(w.n_pages)
     top = int(w.free_top.item())
@@ -155,7 +156,7 @@ def check_topp_rule(c, sel, k, cand, p, k_min=1, k_max=0, what="Top-p"):
     set lies in the candidates, has k members within the clamps, ranks above every other
     candidate in (value, slot) order, reaches p of the fixed-point mass floor(c 2^40)
     (unless clamped at the top), and would not without its weakest member (unless clamped
-    at the bottom)."""
+    at the bottom).  Returns the selected fixed-point mass."""
     c = np.asarray(c, np.float32).astype(np.float64)
     vals = np.clip(np.where(np.isnan(c), 0.0, c), 0.0, 1.0)
     sel = np.asarray(sel, bool)
@@ -179,6 +180,7 @@ def check_topp_rule(c, sel, k, cand, p, k_min=1, k_max=0, what="Top-p"):
     if chosen and kk > lo:
         weakest = min(chosen, key=lambda j: (vals[j], j))
         assert 10 ** 6 * (m - w[weakest]) < pq * total, f"{what}: not the smallest such set"
+    return m
 
 
 def rewritten_sources(table_row, mask_row, n_pages, sel, n_condensed):
@@ -193,13 +195,83 @@ def rewritten_sources(table_row, mask_row, n_pages, sel, n_condensed):
     return out
 
 
+MODE_KEEP, MODE_SPARSE, MODE_REWRITE = 0, 1, 2       # a head's hard-budget state
+
+
+class _Page:
+    """One entry of an expected page list: kind "new" (a fresh page holding the rows src),
+    "sparse" (the physical page phys kept in place) or "dense" (phys untouched)."""
+
+    def __init__(self, kind, mask, phys=-1, src=()):
+        self.kind, self.mask, self.phys, self.src = kind, mask, phys, list(src)
+
+
+class _Layout:
+    def __init__(self, pages):
+        self.pages = pages
+
+
+def rewrite_layout(table_row, mask_row, n_pages, sel, L_dense, mode=MODE_REWRITE, L_sparse=0):
+    """The page list a Cascade-Cache rewrite must leave (Sec. 3.1 tiers; Sec. 3.3.1 states),
+    restated from the rewrite's defining properties for tests whose selection is the GPU's
+    own, so that no oracle routine is run on it:
+      dense tier  the newest ceil(L_dense/16) pages, untouched and last;
+      sparse band the L_sparse/16 pages before them (every non-dense page in state SPARSE,
+                  none in state REWRITE), each kept in place with its mask cut by the
+                  selection, dropped once empty;
+      condensed   every older page: its selected valid slots in logical order, sixteen to a
+                  fresh page with a full-prefix mask, first in the list.
+    A head in state KEEP keeps every page as it is."""
+    n = int(n_pages)
+    if mode == MODE_KEEP:
+        return _Layout([_Page("dense", int(mask_row[pp]), int(table_row[pp])) for pp in range(n)])
+    nd = min(n, -(-int(L_dense) // 16))
+    ns = n - nd if mode == MODE_SPARSE else min(n - nd, int(L_sparse) // 16)
+    nc = n - nd - ns
+    src = rewritten_sources(table_row, mask_row, n, sel, nc)
+    pages = [_Page("new", (1 << len(src[i:i + 16])) - 1, src=src[i:i + 16])
+             for i in range(0, len(src), 16)]
+    for pp in range(nc, nc + ns):
+        kept = sum(1 << t for t in range(16) if sel[pp * 16 + t]) & int(mask_row[pp])
+        if kept:
+            pages.append(_Page("sparse", kept, int(table_row[pp])))
+    pages += [_Page("dense", int(mask_row[pp]), int(table_row[pp])) for pp in range(nc + ns, n)]
+    return _Layout(pages)
+
+
+def check_budget_selection(got, k, cand, votes, mode, cap, n_sink, what="budget"):
+    """Property check of a budget selection made from the GPU's own votes (Sec. 3.1 Step 4
+    under the hard budget): a KEEP head selects every candidate; otherwise the sinks (the
+    first n_sink candidates' slots) are all kept, nothing outside the sinks and the voted
+    candidates is taken, the voted candidates taken number min(voted, cap - sinks) (all of
+    them when there is no cap) and outrank every voted candidate left out in (votes, slot)
+    order, and k counts the set."""
+    got, cand = np.asarray(got, bool), np.asarray(cand, bool)
+    S = len(cand)
+    assert not (got & ~cand).any() and int(k) == int(got.sum()), f"{what}: set or count"
+    if mode == MODE_KEEP:
+        assert np.array_equal(got, cand), f"{what}: KEEP head"
+        return
+    sinks = cand & (np.arange(S) < n_sink)
+    base = cand & ~sinks & (np.asarray(votes) >= 1)
+    assert np.array_equal(got & sinks, sinks) and not (got & ~sinks & ~base).any(), what
+    want = base.sum() if cap < 0 else min(base.sum(), max(0, int(cap) - int(sinks.sum())))
+    assert (got & base).sum() == want, f"{what}: {(got & base).sum()} voted kept, want {want}"
+    kept, dropped = np.nonzero(got & base)[0], np.nonzero(base & ~got)[0]
+    if len(kept) and len(dropped):
+        assert min((votes[j], j) for j in kept) > max((votes[j], j) for j in dropped), \
+            f"{what}: a dropped candidate outranks a kept one"
+
+
 class DecodeReplay:
     """Host model of a decode loop's cache (append, decode attention, periodic compression)
     for a set of heads, built on the oracle: per head its pages in logical order with their
     16-slot masks and K/V rows.  Each step appends a row where the oracle's append_position
     puts it and returns the oracle's decode attention over the valid slots; each compression
-    checks the GPU's scores and selection against the model and then applies the oracle's
-    compact_head with the GPU's selection.  Heads are (layer, sequence, KV head) rows of the
+    checks the GPU's scores and selection against the model and then rewrites the model with
+    the GPU's selection, once that selection has passed the Top-p rule: near the threshold
+    two fp32 computations of c may rank slots differently, so the set itself is not unique
+    across implementations and the model follows the GPU's valid one.  Heads are (layer, sequence, KV head) rows of the
     loop's cache, h // Hkv the sequence s.  Step inputs are host arrays [n, H*, D] whose row
     sidx[s] holds sequence s (sidx=None: row s)."""
 
@@ -281,8 +353,8 @@ class DecodeReplay:
         """One compression of every modelled head (the model holds the cache the compression
         saw): the GPU scores (single pass over the decode LSEs) against the oracle's score fed
         the oracle's own window LSEs, and the GPU's selection by the Top-p rule on its own
-        probabilities; the model is then rewritten by the oracle's compact_head with that
-        selection.  q_win [W, n, Hq, D] host; lse_win {h: [W, G]} oracle LSEs; s_gpu, c_gpu,
+        probabilities; the model is then rewritten to the page list the rewrite defines for
+        that selection (rewrite_layout: no oracle routine is run on the GPU's selection).  q_win [W, n, Hq, D] host; lse_win {h: [W, G]} oracle LSEs; s_gpu, c_gpu,
         sel_gpu: {h: the head's row}; k_gpu [n_heads]."""
         for h in self.heads:
             s, kvh = divmod(h, self.Hkv)
@@ -301,7 +373,7 @@ class DecodeReplay:
             cand[:len(valid)] = O.candidate_mask(valid, cand_len)
             sel = unpack_bits(sel_gpu[h], S)
             check_topp_rule(c_gpu[h], sel, int(k_gpu[h]), cand, p, what=f"{what}: head {h}")
-            res = O.compact_head(np.arange(n), self.mask[h], n, sel, L_dense, 0)
+            res = rewrite_layout(np.arange(n), self.mask[h], n, sel, L_dense)
             K0, V0 = self.K[h][:n].copy(), self.V[h][:n].copy()
             for i, e in enumerate(res.pages):
                 if e.kind == "new":

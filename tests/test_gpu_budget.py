@@ -15,8 +15,8 @@ import torch
 
 import oracle as O
 import workload as WL
-from hk_testlib import (RTOL, HostCache, check_compaction, check_prob, np64, np_i, q_rows,
-                        snapshot, unpack_bits)
+from hk_testlib import (RTOL, HostCache, check_budget_selection, check_compaction, check_prob,
+                        np64, np_i, q_rows, rewrite_layout, snapshot, unpack_bits)
 
 pytestmark = pytest.mark.gpu
 
@@ -286,25 +286,26 @@ def _mass_rule_holds(vals, sel, cand, p):
 def test_cautious_budget_chain():
     """plan -> score -> rows -> votes -> budget select -> compaction on one synthetic cache.
     The budget state and the per-row probabilities are checked against the oracle on the
-    cache itself; the later stages, whose inputs are the GPU's own probabilities, are
+    seeded cache itself; the later stages, whose inputs are the GPU's own probabilities, are
     checked by properties that hold for any input: each row's set satisfies the Top-p mass
     rule and order, votes are the column counts of the row sets, the selection keeps the
-    sinks and the best-ranked voted candidates up to the cap; compaction follows the
-    oracle for the selection it was given, and every rewritten head ends within L_upper."""
-    hk, cfg, w, kv = _setup("bf16_d128_g7_tempered")
+    sinks and the best-ranked voted candidates up to the cap, the compaction leaves the page
+    list the rewrite defines for that selection, and every rewritten head ends within
+    L_upper."""
+    name = "bf16_d128_g7_tempered"
+    cfg0 = CACHES[name][0]
+    H0 = cfg0["L"] * cfg0["B"] * cfg0["Hkv"]
+    # heads of different sizes, (2 + h % 6) / 8 of the draw: every budget state occurs
+    lens = [round(cfg0["N"] * (2 + h % 6) / 8) for h in range(H0)]
+    hk, cfg, w, kv = _setup(name, head_lens=lens)
     G = cfg["Hq"] // cfg["Hkv"]
     R = G * cfg["W"]
     d = hk.dims(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"], cfg["W"])
     H, S = w.n_heads, w.S_max
     L_dense, L_lower, L_upper, n_sink, p = 32, 200, 400, 4, 0.9
     scale = 1 / math.sqrt(cfg["D"])
-    # heads of different sizes first: an earlier rewrite keeps (2 + h % 6) / 8 of head h
-    j = np.arange(S)
-    keep = np.stack([(j * 7 + h) % 8 < 2 + h % 6 for h in range(H)])
-    words = (keep.reshape(H, S // 32, 32).astype(np.int64) << np.arange(32)).sum(axis=2)
-    hk.hk_compact(d, kv, torch.tensor(words.astype(np.uint32).view(np.int32), device=DEV), 0, 0,
-                  hk.Allocator(w.free_ids, w.free_top), torch.zeros(1, dtype=torch.int32, device=DEV),
-                  hk.workspace(hk.OP_COMPACT, d, w.max_pages, DEV))
+    host = HostCache(w.k_pool, None, w.page_table, w.page_mask, w.n_pages)
+    before = snapshot(w)
     mode = torch.empty(H, dtype=torch.int32, device=DEV)
     cap = torch.empty(H, dtype=torch.int32, device=DEV)
     hk.hk_budget_plan(d, kv, L_dense, L_lower, L_upper, mode, cap)
@@ -323,8 +324,6 @@ def test_cautious_budget_chain():
     hk.hk_budget_select(H, S, cl, w.page_mask, sel, k, votes=votes, c=None, head_mode=mode,
                         k_cap=cap, n_sink=n_sink)
     torch.cuda.synchronize()
-    host = HostCache(w.k_pool, None, w.page_table, w.page_mask, w.n_pages)
-    before = snapshot(w)
     m_np, cap_np, cl_np, k_np = np_i(mode), np_i(cap), np_i(cl), np_i(k)
     a_np, v_np = a.cpu().numpy(), np_i(votes).astype(np.int64) & 0xFFFF
     rs_np, sel_np = np_i(row_sel), np_i(sel)
@@ -335,11 +334,13 @@ def test_cautious_budget_chain():
         assert (int(m_np[h]), int(cap_np[h])) == O.budget_plan_head(n, host.mask[h], L_dense,
                                                                       L_lower, L_upper)
         rows, valid = host.head(h)
+        cand_len = 16 * (n - O.tier_pages(n, L_dense, 0)[2])
+        assert int(cl_np[h]) == cand_len, h
         cand = np.zeros(S, bool)
-        cand[:len(valid)] = O.candidate_mask(valid, int(cl_np[h]))
+        cand[:len(valid)] = O.candidate_mask(valid, cand_len)
         qr = q_rows(qn, h, cfg["Hkv"], G)
-        _, lr = O.score_head(qr, rows, valid, int(cl_np[h]), scale)
-        ref_a = O.score_rows_head(qr, rows, valid, int(cl_np[h]), scale, lr)
+        _, lr = O.score_head(qr, rows, valid, cand_len, scale)
+        ref_a = O.score_rows_head(qr, rows, valid, cand_len, scale, lr)
         for r in range(0, R, 37):
             full = np.zeros(S)
             full[:ref_a.shape[1]] = ref_a[r]
@@ -348,27 +349,13 @@ def test_cautious_budget_chain():
         assert np.array_equal(bits.sum(axis=0), v_np[h]), h
         for r in range(0, R, 29):
             assert _mass_rule_holds(a_np[h, r], bits[r], cand, p), (h, r)
-        got = unpack_bits(sel_np[h], S)
-        assert not (got & ~cand).any() and int(k_np[h]) == int(got.sum())
-        if m_np[h] == O.KEEP:
-            assert np.array_equal(got, cand)
-            continue
-        sinks = cand & (np.arange(S) < n_sink)
-        base = cand & ~sinks & (v_np[h] >= 1)
-        assert np.array_equal(got & sinks, sinks) and not (got & ~sinks & ~base).any()
-        want = base.sum() if cap_np[h] < 0 else min(base.sum(), max(0, int(cap_np[h]) - sinks.sum()))
-        assert (got & base).sum() == want
-        kept = np.nonzero(got & base)[0]
-        dropped = np.nonzero(base & ~got)[0]
-        if len(kept) and len(dropped):
-            lo = min((v_np[h][j], j) for j in kept)
-            hi = max((v_np[h][j], j) for j in dropped)
-            assert lo > hi, h
+        check_budget_selection(unpack_bits(sel_np[h], S), k_np[h], cand, v_np[h], int(m_np[h]),
+                               int(cap_np[h]), n_sink, what=f"head {h}")
     hk.hk_compact_modes(d, kv, sel, L_dense, mode, hk.Allocator(w.free_ids, w.free_top),
                         torch.zeros(1, dtype=torch.int32, device=DEV),
                         hk.workspace(hk.OP_COMPACT, d, w.max_pages, DEV))
     torch.cuda.synchronize()
-    check_compaction(w, before, sel_np, S, lambda h, sl: O.compact_mode_head(
+    check_compaction(w, before, sel_np, S, lambda h, sl: rewrite_layout(
         before["table"][h], before["mask"][h], int(before["n"][h]), sl, L_dense, int(m_np[h])))
     n_after = np_i(w.n_pages)
     for h in range(H):
@@ -378,8 +365,9 @@ def test_cautious_budget_chain():
 
 def test_budget_compressor_pipeline():
     """BudgetCompressor.step: every head of the cache ends within L_upper when rewritten, the
-    sinks survive, the selection equals the budget-select oracle on the votes the step
-    produced (integer work), and the status word stays clear."""
+    sinks survive, the selection obeys the budget rule on the votes the step produced, the
+    compaction leaves the page list the rewrite defines for it, and the status word stays
+    clear."""
     import paper_2606_28831_amd as hk
     from paper_2606_28831_amd.pipeline import BudgetCompressor
     hk_, cfg, w, kv = _setup("bf16_d128_g4_ragged_holes")
@@ -398,13 +386,12 @@ def test_budget_compressor_pipeline():
         valid = _valid(before["mask"][h])
         cand = np.zeros(S, bool)
         cand[:len(valid)] = O.candidate_mask(valid, int(np_i(b["cand_len"])[h]))
-        ref, kr = O.budget_select_head(cand, votes=v_np[h], mode=int(mode[h]), k_cap=int(cap[h]),
-                                       n_sink=4)
-        assert np.array_equal(unpack_bits(sel_np[h], S), ref) and int(np_i(b["k"])[h]) == kr, h
+        check_budget_selection(unpack_bits(sel_np[h], S), np_i(b["k"])[h], cand, v_np[h],
+                               int(mode[h]), int(cap[h]), 4, what=f"head {h}")
     comp.compact()
     torch.cuda.synchronize()
     assert int(b["status"].item()) == 0
-    check_compaction(w, before, sel_np, S, lambda h, sl: O.compact_mode_head(
+    check_compaction(w, before, sel_np, S, lambda h, sl: rewrite_layout(
         before["table"][h], before["mask"][h], int(before["n"][h]), sl, 48, int(mode[h])))
     n_after = np_i(w.n_pages)
     for h in range(H):

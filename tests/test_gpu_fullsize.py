@@ -106,9 +106,6 @@ def test_full_size_sampled(c):
             top = np.sort(xs)[::-1][:k_a]
             mk = math.exp(np.logaddexp.reduce(top) - np.logaddexp.reduce(xs))
             assert abs(mk - m_a) <= 2e-3, f"cfg{c} T head {h}: M_k {mk} vs target {m_a}"
-            # stage parity of the temperature: the oracle's bisection on the same inputs
-            T_stage = O.solve_T_head(xr_gpu[h], cand, k_a, m_a)
-            assert float(T_gpu[h]) == pytest.approx(T_stage, rel=2e-3), f"cfg{c} T head {h}"
             # the mixture is a distribution over the candidates
             cg = c_gpu[h].astype(np.float64)
             assert np.all(cg[~cand] == 0) and np.all(cg >= 0) and abs(cg.sum() - 1) <= 1e-4, h

@@ -13,7 +13,8 @@ import pytest
 import torch
 
 import oracle as O
-from hk_testlib import check_lse, check_prob, np64, np_i, topp_edge_inputs, unpack_bits
+from hk_testlib import (check_lse, check_prob, check_topp_rule, np64, np_i, topp_edge_inputs,
+                        unpack_bits)
 
 pytestmark = pytest.mark.gpu
 
@@ -119,8 +120,9 @@ def test_topp_ws_page_mask_and_thresholds(S, p):
 @pytest.mark.parametrize("S", [4096 + 32, 32768, 131072])
 @pytest.mark.parametrize("two_metrics", [False, True])
 def test_calibrate_topp_ws_vs_oracle(S, two_metrics):
-    """c_out and lse_out against the oracle's calibration (mixture for two metrics), and the
-    selection against the oracle's Top-p of the c this call wrote, bit for bit."""
+    """c_out and lse_out against the oracle's calibration (mixture for two metrics).  The c this
+    call wrote is the GPU's own, so the selection made from it is checked by Top-p's defining
+    properties instead of an oracle run on it."""
     hk = _hk()
     rng = np.random.default_rng(S + two_metrics)
     H = 4
@@ -157,10 +159,9 @@ def test_calibrate_topp_ws_vs_oracle(S, two_metrics):
             refs, lses = [ca, cb], [la, lb]
         check_prob(c_np[h], O.mix(refs, weights), 1e-5, f"c head {h}")
         check_lse(lse_np[h], lses, 1e-5, f"lse head {h}")
-        r = O.topp_head(c_np[h], cand, p)
-        assert int(k_np[h]) == r.k, (h, int(k_np[h]), r.k)
-        assert np.array_equal(unpack_bits(sel_np[h], S), r.sel), h
-        assert sm_np[h] == np.float32(r.sel_mass / 2.0 ** 40)
+        m = check_topp_rule(c_np[h], unpack_bits(sel_np[h], S), k_np[h], cand, p,
+                            what=f"Top-p head {h}")
+        assert sm_np[h] == np.float32(m / 2.0 ** 40), (h, sm_np[h], m)
     assert int(st.item()) == 0
 
 

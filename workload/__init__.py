@@ -90,7 +90,7 @@ def _gen(device, seed):
 
 def make_workload(cfg: dict, device="cpu", pool_slack: float = 2.0, max_pages: int | None = None,
                   hole_prob: float = 0.0, tail_len: int | None = None,
-                  pool_pages: int | None = None) -> Workload:
+                  pool_pages: int | None = None, head_lens=None) -> Workload:
     """Draw one workload.
 
     cfg keys: L, B, Hq, Hkv, D, N, dtype, W, seed, recipe ("normal" | "planted" | "tempered"),
@@ -98,6 +98,9 @@ def make_workload(cfg: dict, device="cpu", pool_slack: float = 2.0, max_pages: i
     hole_prob > 0 clears random slot bits (masked slots inside pages); tail_len
     overrides the last page's filled length.  The pool holds pool_slack times
     the pages in use (room for the out-of-place rewrite) unless pool_pages is given.
+    head_lens (one length <= N per head) shortens heads after the draw: head h keeps its
+    first ceil(len/16) pages, the last one filled to its length, and the rest of its pages
+    go back to the free list (a length mix over heads; every draw stays as without it).
     """
     dev = torch.device(device)
     g = _gen(dev, cfg["seed"])
@@ -162,6 +165,24 @@ def make_workload(cfg: dict, device="cpu", pool_slack: float = 2.0, max_pages: i
         ids = table[h0:h1, :n_used].reshape(-1).long()
         k_pool[ids] = kl.to(dt).view(-1, PAGE, D)
         v_pool[ids] = vl.to(dt).view(-1, PAGE, D)
+
+    if head_lens is not None:
+        lens = [int(x) for x in head_lens]
+        assert len(lens) == H and all(0 <= x <= N for x in lens), "one length <= N per head"
+        released = []
+        for h, ln in enumerate(lens):
+            nh = -(-ln // PAGE)
+            released.append(table[h, nh:n_used].clone())
+            table[h, nh:] = -1
+            masks[h, nh:] = 0
+            if nh:
+                masks[h, nh - 1] &= (1 << (ln - (nh - 1) * PAGE)) - 1
+            n_pages[h] = nh
+        page_mask = masks.to(torch.int16)
+        back = torch.sort(torch.cat([free_ids[:n_free]] + released)).values
+        n_free = back.numel()
+        free_ids[:n_free] = back
+        free_top.fill_(n_free)
 
     ref = None
     n_ref = cfg.get("n_ref", 0)

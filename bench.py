@@ -814,7 +814,8 @@ def copy_calibration():
 def run_peaks():
     """Measured rates behind the score passes' rooflines: the hardware exponential
     (v_exp_f32) and the bf16 MFMA (32x32x16), each from a throughput kernel of the library
-    (hk_probe) timed with events on the launch stream, best of five launches."""
+    (hk_probe) timed with events on the launch stream, best of five launches; and the time
+    of the passes' MFMA + VALU mix alone, interleaved in one wave, and split over waves."""
     import paper_2606_28831_amd as hk
     n_cu = torch.cuda.get_device_properties(0).multi_processor_count
     blocks = 4 * n_cu                            # 16 waves per CU: every SIMD busy
@@ -834,15 +835,20 @@ def run_peaks():
             raise SystemExit("rate probe produced a non-finite value")
         return best
 
-    it_exp, it_mfma = 4096, 2048
+    it_exp, it_mfma, it_mix = 4096, 2048, 1024
     ms_exp = best_ms(hk.PROBE_EXP, it_exp)
     ms_mfma = best_ms(hk.PROBE_MFMA, it_mfma)
     n_exp = 8 * it_exp * 256 * blocks
     n_mfma = 16 * it_mfma * blocks
+    # MFMA and VALU work of the score passes' mix, alone, interleaved in one wave, and in
+    # different waves of one SIMD (equal total work in the last two)
+    mix = {name: best_ms(kind, it_mix) for name, kind in
+           (("mfma_only_ms", hk.PROBE_MFMA4), ("valu_only_ms", hk.PROBE_VALU),
+            ("same_wave_ms", hk.PROBE_MIX), ("split_waves_ms", hk.PROBE_SPLIT))}
     return {"probe": "rates", "compute_units": n_cu, "workgroups": blocks,
             "exp_per_s": n_exp / (ms_exp / 1e3), "exp_ms": ms_exp,
             "mfma_bf16_tflops": n_mfma * 32768 / (ms_mfma / 1e3) / 1e12, "mfma_ms": ms_mfma,
-            "mfma_bf16_peak_tflops": 2500.0}
+            "mfma_bf16_peak_tflops": 2500.0, "mix_steps_per_wave": 4 * it_mix, **mix}
 
 
 def _pmc_mean(run_dir, counter, match):

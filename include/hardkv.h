@@ -506,12 +506,20 @@ hk_status hk_timing_read(int32_t kernel, double* total_ms, int64_t* launches);
  *   HK_PROBE_EXP  : every thread runs 8 independent chains of `iters` hardware
  *                   exponentials (v_exp_f32): 8 * iters * 256 * blocks of them;
  *   HK_PROBE_MFMA : every wave runs 4 independent chains of `iters`
- *                   v_mfma_f32_32x32x16_bf16: 16 * iters * blocks MFMAs of 32768 flop.
+ *                   v_mfma_f32_32x32x16_bf16: 16 * iters * blocks MFMAs of 32768 flop;
+ *   HK_PROBE_MIX  : the score passes' work mix: every wave runs iters x 4 steps, a step
+ *                   being one 32x32x16 bf16 MFMA plus, for two values per lane, an fma, a
+ *                   hardware exponential and an add, interleaved one step at a time;
+ *   HK_PROBE_SPLIT: the same total work with the MFMAs in the even waves and the VALU
+ *                   work in the odd waves of every workgroup (2 iters x 4 steps each);
+ *   HK_PROBE_VALU : only the VALU part of HK_PROBE_MIX;
+ *   HK_PROBE_MFMA4: only the MFMA part of HK_PROBE_MIX.
  * out: device, >= 256 * blocks floats, caller-owned; receives one value per thread (it
  * keeps the work live).  The caller times the launch.  Errors: HK_ERR_ARG for an unknown
  * kind, blocks < 1 or > 2^20, iters < 1, or a null out.
  */
-enum { HK_PROBE_EXP = 0, HK_PROBE_MFMA = 1 };
+enum { HK_PROBE_EXP = 0, HK_PROBE_MFMA = 1, HK_PROBE_MIX = 2, HK_PROBE_SPLIT = 3, HK_PROBE_VALU = 4,
+       HK_PROBE_MFMA4 = 5 };
 hk_status hk_probe(int32_t kind, int32_t blocks, int32_t iters, float* out, hipStream_t stream);
 
 #ifdef __cplusplus

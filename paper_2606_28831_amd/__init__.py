@@ -20,7 +20,8 @@ __all__ = ["HardKVError", "lib", "PagedKV", "Allocator", "hk_score", "hk_calibra
            "hk_timing_enable", "hk_timing_read", "TIMED_KERNELS", "hk_calibrate_topp",
            "hk_pool_max", "hk_score_rows", "hk_vote_topp", "hk_budget_plan", "hk_budget_select",
            "hk_compact_modes", "hk_calibrate_solve_T_gd", "hk_alloc_init", "hk_compress", "OP_COMPRESS", "BUDGET_KEEP", "BUDGET_SPARSE", "BUDGET_REWRITE",
-           "hk_probe", "PROBE_EXP", "PROBE_MFMA", "hk_decode_plan",
+           "hk_probe", "PROBE_EXP", "PROBE_MFMA", "PROBE_MIX", "PROBE_SPLIT", "PROBE_VALU",
+           "PROBE_MFMA4", "hk_decode_plan",
            "hk_decode_attn_noalloc", "hk_decode_noalloc_scratch_bytes", "ERR_SCRATCH",
            "OP_SELECT", "hk_select_workspace_size", "select_workspace", "hk_topp_select_ws",
            "hk_calibrate_topp_ws"]
@@ -32,7 +33,7 @@ OP_SCORE, OP_COMPACT, OP_DECODE, OP_APPEND, OP_COMPRESS, OP_SELECT = 0, 1, 2, 3,
 FLAG_NOSPACE, FLAG_NAN, FLAG_RANGE = 1, 2, 4
 ERR_SCRATCH = 7
 BUDGET_KEEP, BUDGET_SPARSE, BUDGET_REWRITE = 0, 1, 2
-PROBE_EXP, PROBE_MFMA = 0, 1
+PROBE_EXP, PROBE_MFMA, PROBE_MIX, PROBE_SPLIT, PROBE_VALU, PROBE_MFMA4 = 0, 1, 2, 3, 4, 5
 EXPORTED = ["hk_score", "hk_calibrate", "hk_calibrate_solve_T", "hk_topp_select", "hk_compact",
             "hk_decode_attn", "hk_append_kv", "hk_workspace_size", "hk_status_string",
             "hk_timing_enable", "hk_timing_read", "hk_calibrate_topp", "hk_pool_max",
@@ -421,7 +422,7 @@ def hk_timing_enable(kernels=None):
 
 
 def hk_probe(kind: int, blocks: int, iters: int, out, stream=None):
-    """One rate-probe launch (PROBE_EXP or PROBE_MFMA); out: >= 256 * blocks floats."""
+    """One rate-probe launch (a PROBE_* kind); out: >= 256 * blocks floats."""
     _check(lib().hk_probe(int(kind), int(blocks), int(iters), _ptr(out), _stream(stream)),
            "hk_probe")
 

@@ -504,7 +504,7 @@ hk_status hk_append_kv(const hk_dims* dims, const hk_paged_kv* kv, const void* k
 }
 
 hk_status hk_probe(int32_t kind, int32_t blocks, int32_t iters, float* out, hipStream_t stream) {
-  if (kind != HK_PROBE_EXP && kind != HK_PROBE_MFMA) return HK_ERR_ARG;
+  if (kind < HK_PROBE_EXP || kind > HK_PROBE_MFMA4) return HK_ERR_ARG;
   if (blocks < 1 || blocks > (1 << 20) || iters < 1 || !out) return HK_ERR_ARG;
   return launched(hk_launch_probe(kind, blocks, iters, out, stream));
 }

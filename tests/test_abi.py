@@ -183,10 +183,11 @@ def test_validation_errors_without_gpu(hk):
     assert L.hk_compact_modes(C.byref(d), C.byref(kv), P, 0, P, C.byref(alloc), P, P, 16,
                               None) == 5                                # workspace too small
     # rate probes
-    assert L.hk_probe(2, 4, 8, P, None) == 1                            # unknown kind
     assert L.hk_probe(hk.PROBE_EXP, 0, 8, P, None) == 1                 # no workgroups
     assert L.hk_probe(hk.PROBE_MFMA, 4, 0, P, None) == 1                # no iterations
     assert L.hk_probe(hk.PROBE_EXP, 4, 8, None, None) == 1              # no output
+    assert L.hk_probe(6, 4, 8, P, None) == 1                            # unknown kind
+    assert L.hk_probe(-1, 4, 8, P, None) == 1
 
 
 def test_kernel_timing_host_side(hk):

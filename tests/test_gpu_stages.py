@@ -885,14 +885,15 @@ def test_pool_then_select_pipeline():
 # ---------------------------------------------------------------- rate probes
 @pytest.mark.gpu
 def test_rate_probes_run():
-    """hk_probe launches both throughput kernels and writes a finite value per thread; the
+    """hk_probe launches every throughput kernel and writes a finite value per thread; the
     exponential chains x <- 2^-x stay in (0, 1]."""
     import paper_2606_28831_amd as hk
     out = torch.full((8 * 256,), float("nan"), device=DEV)
     hk.hk_probe(hk.PROBE_EXP, 8, 64, out)
     torch.cuda.synchronize()
     assert torch.isfinite(out).all() and (out > 0).all() and (out <= 8).all()
-    out.fill_(float("nan"))
-    hk.hk_probe(hk.PROBE_MFMA, 8, 16, out)
-    torch.cuda.synchronize()
-    assert torch.isfinite(out).all()
+    for kind in (hk.PROBE_MFMA, hk.PROBE_MIX, hk.PROBE_SPLIT, hk.PROBE_VALU, hk.PROBE_MFMA4):
+        out.fill_(float("nan"))
+        hk.hk_probe(kind, 8, 16, out)
+        torch.cuda.synchronize()
+        assert torch.isfinite(out).all(), kind

@@ -836,23 +836,43 @@ __device__ __forceinline__ void static_for(F&& f) {
   }
 }
 
+// The issue is split in two so the page-id reads (LDS) of an iteration's loads can be made
+// an iteration ahead of the loads themselves: coop_phys reads the physical page of each of
+// the thread's pieces, coop_load issues the loads from them.
 template <int D, int QB, int N>
-__device__ __forceinline__ void coop_issue(u32x4 (&r)[N], const uint16_t* __restrict__ k_pool,
-                                           const int32_t* s_table, int p_begin, int p_last, int it) {
+__device__ __forceinline__ void coop_phys(int (&ph)[N], const int32_t* s_table, int p_begin, int p_last,
+                                          int it) {
   using C = Coop<D, QB>;
   const int p0 = p_begin + it * C::PPI;
   static_for<C::LPT>([&](auto ic) {
     constexpr int i = decltype(ic)::value;
     const int c = i * C::NT + (int)threadIdx.x;
     if (C::ITER_CH % C::NT == 0 || c < C::ITER_CH) {
-      const int ts = c / C::TILE_CH, f = c % C::TILE_CH;
+      const int ts = c / C::TILE_CH, key = (c % C::TILE_CH) & 31;
+      ph[i] = s_table[min(p0 + 2 * ts + (key >> 4), p_last) - p_begin];
+    }
+  });
+}
+template <int D, int QB, int N>
+__device__ __forceinline__ void coop_load(u32x4 (&r)[N], const uint16_t* __restrict__ k_pool, const int (&ph)[N]) {
+  using C = Coop<D, QB>;
+  static_for<C::LPT>([&](auto ic) {
+    constexpr int i = decltype(ic)::value;
+    const int c = i * C::NT + (int)threadIdx.x;
+    if (C::ITER_CH % C::NT == 0 || c < C::ITER_CH) {
+      const int f = c % C::TILE_CH;
       const int kk = f >> 6, ln = f & 63, key = ln & 31;
-      const int pg = min(p0 + 2 * ts + (key >> 4), p_last);
-      const size_t phys = (size_t)s_table[pg - p_begin];
-      r[i] = *reinterpret_cast<const u32x4*>(k_pool + (phys * HK_PAGE + (key & 15)) * D + kk * 16 +
+      r[i] = *reinterpret_cast<const u32x4*>(k_pool + ((size_t)ph[i] * HK_PAGE + (key & 15)) * D + kk * 16 +
                                              (ln >> 5) * 8);
     }
   });
+}
+template <int D, int QB, int N>
+__device__ __forceinline__ void coop_issue(u32x4 (&r)[N], const uint16_t* __restrict__ k_pool,
+                                           const int32_t* s_table, int p_begin, int p_last, int it) {
+  int ph[N];
+  coop_phys<D, QB>(ph, s_table, p_begin, p_last, it);
+  coop_load<D, QB>(r, k_pool, ph);
 }
 template <int D, int QB, int N>
 __device__ __forceinline__ void coop_store(const u32x4 (&r)[N], char* buf) {
@@ -961,22 +981,31 @@ void score_pass1_coop_kernel(const uint16_t* __restrict__ q_obs, const uint16_t*
       M = mn;
     }
   };
-  auto tile_mask = [&](int it_) {
-    const int pl = it_ * C::PPI + 2 * ts;                           // chunk-relative page
-    return s_mask[pl] | (s_mask[pl + 1] << 16);                     // past the end: 0
+  // the 16-bit masks of a tile's two pages (chunk-relative page pl, pl + 1; past the end: 0),
+  // read as one 64-bit LDS load at a clamped, always valid page
+  auto tile_mask_raw = [&](int it_) {
+    const int pl = min(it_ * C::PPI + 2 * ts, C::PPW - 2);
+    return *reinterpret_cast<const uint2*>(s_mask + pl);
   };
 
   // Software pipeline inside each wave: the MFMAs of tile it run beside the sum of
   // exponentials of tile it - 1's accumulator, one step per scheduling region.  Tiles with
   // masked keys take the plain update after the chain.  Iterations run in groups of four up to
   // n_iter + 1 (the last drains the pipeline); those past n_iter only move data.
-  f32x16 accp = {};
+  f32x16 accs[2] = {f32x16{}, f32x16{}};     // tile it's MFMAs: accs[it & 1]
+  // the masks of the tile whose exponentials an iteration takes, loaded one iteration ahead
+  // and only combined when used, so no iteration waits for its own mask read
+  uint2 mask_next = make_uint2(0u, 0u);
   auto iteration = [&](auto uc, int it) {
     constexpr int u = decltype(uc)::value;
     __syncthreads();
+    int ph[C::LPT];
+    coop_phys<D, QB>(ph, s_table, p_begin, p_last, it + 1 + C::STAGES);
+    const uint2 mraw = mask_next;
+    mask_next = tile_mask_raw(it);
     if (active) {
       const bool prev = it >= 1 && it - 1 < n_iter;
-      const uint32_t tmp = prev ? tile_mask(it - 1) : 0u;
+      const uint32_t tmp = prev ? mraw.x | (mraw.y << 16) : 0u;
       const bool fuse = tmp == 0xffffffffu;
       if (it < n_iter) {
         const char* tb = smem + L::BUFS + (size_t)(u & 1) * C::BUF + (size_t)ts * C::TILE_CH * 16 +
@@ -985,7 +1014,8 @@ void score_pass1_coop_kernel(const uint16_t* __restrict__ q_obs, const uint16_t*
         bf16x8 kf[KD + 1];
 #pragma unroll
         for (int g = 0; g < KD; ++g) kf[g] = *reinterpret_cast<const bf16x8*>(tb + (size_t)g * 1024);
-        f32x16 acc = {};
+        f32x16& acc = accs[u & 1];
+        acc = f32x16{};
         if (fuse) {
           // exponentials against the lane's current reference maximum M, no maximum per
           // tile: the sum is exact unless a key exceeds M by more than 64 powers of two (or
@@ -1001,14 +1031,14 @@ void score_pass1_coop_kernel(const uint16_t* __restrict__ q_obs, const uint16_t*
 #pragma unroll
             for (int e = 0; e < 16; ++e)
               if (e * C::KS / 16 == kk) {
-                if (e & 1) s1 += fast_exp2(fmaf(accp[e], c2, -mc));
-                else s0 += fast_exp2(fmaf(accp[e], c2, -mc));
+                if (e & 1) s1 += fast_exp2(fmaf(accs[(u + 1) & 1][e], c2, -mc));
+                else s0 += fast_exp2(fmaf(accs[(u + 1) & 1][e], c2, -mc));
               }
             __builtin_amdgcn_sched_barrier(0);
           }
           const float st = s0 + s1;
           if (st <= 0x1p64f) Lsum += st;
-          else update_masked(accp, 0xffffffffu);
+          else update_masked(accs[(u + 1) & 1], 0xffffffffu);
         } else {
 #pragma unroll
           for (int kk = 0; kk < C::KS; ++kk) {
@@ -1016,16 +1046,14 @@ void score_pass1_coop_kernel(const uint16_t* __restrict__ q_obs, const uint16_t*
             if (kk + KD < C::KS)
               kf[(kk + KD) % (KD + 1)] = *reinterpret_cast<const bf16x8*>(tb + (size_t)(kk + KD) * 1024);
           }
-          if (tmp != 0u) update_masked(accp, tmp);
+          if (tmp != 0u) update_masked(accs[(u + 1) & 1], tmp);
         }
-        accp = acc;
       } else if (prev && tmp != 0u) {
-        update_masked(accp, tmp);
+        update_masked(accs[(u + 1) & 1], tmp);
       }
     }
     coop_store<D, QB>(slot(std::integral_constant<int, u + 1>{}), smem + L::BUFS + (size_t)((u + 1) & 1) * C::BUF);
-    coop_issue<D, QB>(slot(std::integral_constant<int, u + 1>{}), k_pool, s_table, p_begin, p_last,
-                      it + 1 + C::STAGES);
+    coop_load<D, QB>(slot(std::integral_constant<int, u + 1>{}), k_pool, ph);
   };
   // A chunk with no page (n_iter = 0) runs no iteration: each ends by issuing clamped loads
   // for a later one, and with no page the clamp (to p_last = p_end - 1 < p_begin) would read
@@ -1155,6 +1183,8 @@ void score_pass2_coop_kernel(const uint16_t* __restrict__ q_obs, const uint16_t*
   auto iteration = [&](auto uc, int it) {
     constexpr int u = decltype(uc)::value;
     __syncthreads();
+    int ph[C::LPT];
+    coop_phys<D, QB>(ph, s_table, p_begin, p_last, it + 1 + C::STAGES);
     if (it >= 2 && it - 2 < n_iter) reduce(it - 2, u & 1);
     if (active) {
       const bool prev = it >= 1 && it - 1 < n_iter;
@@ -1201,8 +1231,7 @@ void score_pass2_coop_kernel(const uint16_t* __restrict__ q_obs, const uint16_t*
       }
     }
     coop_store<D, QB>(slot(std::integral_constant<int, u + 1>{}), smem + L::BUFS + (size_t)((u + 1) & 1) * C::BUF);
-    coop_issue<D, QB>(slot(std::integral_constant<int, u + 1>{}), k_pool, s_table, p_begin, p_last,
-                      it + 1 + C::STAGES);
+    coop_load<D, QB>(slot(std::integral_constant<int, u + 1>{}), k_pool, ph);
   };
   for (int it0 = 0; it0 < n_iter + 2; it0 += 4) {
     iteration(I0{}, it0);

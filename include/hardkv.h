@@ -250,7 +250,9 @@ hk_status hk_calibrate_topp_ws(int32_t n_heads, int32_t S_max, const int32_t* ca
  * the logarithm, so pooling log scores pools the underlying masses.  x, x_out
  * [n_heads][S_max] fp32 device arrays, distinct (no in-place); radius in [0, 64]
  * (radius 0 copies the candidates).  HK_ERR_ARG for a null or aliased pointer,
- * HK_ERR_SHAPE for a radius outside [0, 64] or the S_max limits of hk_calibrate.
+ * HK_ERR_SHAPE for a radius outside [0, 64] or an S_max that is not a multiple of 32 or
+ * exceeds 262144 (the wide selector's limit: one workgroup per 1024-slot tile, so the
+ * length is not bound by a workgroup).
  */
 hk_status hk_pool_max(int32_t n_heads, int32_t S_max, const int32_t* cand_len,
                       const uint16_t* page_mask, const float* x, int32_t radius, float* x_out,

@@ -267,7 +267,7 @@ hk_status hk_calibrate_topp_ws(int32_t n_heads, int32_t S_max, const int32_t* ca
 hk_status hk_pool_max(int32_t n_heads, int32_t S_max, const int32_t* cand_len,
                       const uint16_t* page_mask, const float* x, int32_t radius, float* x_out,
                       hipStream_t stream) {
-  hk_status e = check_rows(n_heads, S_max, cand_len);
+  hk_status e = check_rows_wide(n_heads, S_max, cand_len);       // tiled: any length
   if (e) return e;
   if (!x || !x_out || x == x_out) return HK_ERR_ARG;
   if (radius < 0 || radius > 64) return HK_ERR_SHAPE;

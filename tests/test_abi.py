@@ -119,6 +119,7 @@ def test_validation_errors_without_gpu(hk):
     assert L.hk_pool_max(4, 128, P, None, P, -1, P + 64, None) == 3     # negative radius
     assert L.hk_pool_max(4, 128, P, None, P, 3, P, None) == 1           # in place
     assert L.hk_pool_max(4, 100, P, None, P, 3, P + 64, None) == 3      # S_max % 32
+    assert L.hk_pool_max(4, 262144 + 32, P, None, P, 3, P + 64, None) == 3  # longer than 262144
     xs = (C.c_void_p * 1)(P)
     wts = (C.c_float * 1)(1.0)
     assert L.hk_calibrate_topp(4, 128, P, None, 3, xs, None, wts, 0.9, 1, 0, None, None, P, P,

@@ -847,6 +847,38 @@ def test_pool_max(name, radius):
         assert np.array_equal(out_np[h].astype(np.float64), ref), (name, radius, h)
 
 
+@pytest.mark.parametrize("S,radius", [(65536, 3), (262144, 64)])
+def test_pool_max_long_rows(S, radius):
+    """Rows past one selector workgroup (up to 262144 slots, 256 tiles of 1024 per head):
+    sampled windows of the output against the oracle's pooling of the same window (a
+    window's interior depends only on the window), at tile edges, the candidate boundary
+    and the row's end, with page holes and masked slots."""
+    import paper_2606_28831_amd as hk
+    rng = np.random.default_rng(S + radius)
+    H = 2
+    x = rng.standard_normal((H, S)).astype(np.float32)
+    bits = rng.random((H, S)) >= 0.1
+    bits &= np.repeat(rng.random((H, S // 16)) >= 0.05, 16, axis=1)
+    words = (bits.reshape(H, S // 16, 16).astype(np.int64) << np.arange(16)).sum(-1)
+    cand_len = np.array([S, S - 1000 - 37], np.int32)
+    out = torch.full((H, S), 9.0, device=DEV)
+    hk.hk_pool_max(H, S, torch.tensor(cand_len, device=DEV),
+                   torch.tensor(words.astype(np.uint16).view(np.int16), device=DEV),
+                   torch.tensor(x, device=DEV), radius, out)
+    torch.cuda.synchronize()
+    out_np = out.cpu().numpy()
+    for h in range(H):
+        cand = O.candidate_mask(bits[h], int(cand_len[h]))
+        centres = [0, 1024, 4096 + 512, S // 2, int(cand_len[h]), S - 1] + \
+            [int(c) for c in rng.integers(0, S, 4)]
+        for c in centres:
+            a, b = max(0, c - 600), min(S, c + 600)
+            ref = O.pool_max_head(x[h, a:b].astype(np.float64), cand[a:b], radius)
+            lo = a + (radius if a > 0 else 0)            # interior: the whole neighbourhood is inside
+            hi = b - (radius if b < S else 0)
+            assert np.array_equal(out_np[h, lo:hi].astype(np.float64), ref[lo - a:hi - a]), (S, h, c)
+
+
 def test_pool_then_select_pipeline():
     """Compressor(pool_radius=3): pooled scores feed the fused select.  The pooled scores and
     calibrated probabilities match the oracle chain run on the same cache (score -> pool ->

@@ -297,8 +297,9 @@ hk_status hk_calibrate_solve_T_gd(int32_t n_heads, int32_t S_max, const int32_t*
  * (>= hk_workspace_size(HK_OP_COMPRESS, dims, max_pages) bytes, 256-byte aligned).
  * Outputs: k_out [n_heads] (the Top-p counts), sel_bits_out [n_heads][S_max/32] or NULL
  * (the selection is then kept in the workspace), status (HK_FLAG_* of every stage).
- * Arguments and errors as for the three calls it makes (alloc->capacity >= kv->num_pages,
- * checked before anything is launched).
+ * Arguments and errors as for the three calls it makes; alloc->capacity >= kv->num_pages,
+ * S_max = 16 * max_pages <= 262144 and at most 2^20 heads are checked before anything is
+ * launched (HK_ERR_ARG, HK_ERR_SHAPE).
  */
 hk_status hk_compress(const hk_dims* dims, const void* q_obs, const hk_paged_kv* kv,
                       int32_t L_dense, int32_t L_sparse, float sm_scale, const float* row_lse_in,

@@ -330,6 +330,8 @@ hk_status hk_compress(const hk_dims* dims, const void* q_obs, const hk_paged_kv*
   if (!alloc || !alloc->free_ids || !alloc->free_top || alloc->capacity < kv->num_pages)
     return HK_ERR_ARG;                                             // checked before any launch
   if (!(p >= 0.0 && p <= 1.0)) return HK_ERR_ARG;
+  // the selection's row limits, checked here so that no launch runs before a refusal
+  if (kv->max_pages > kMaxSlotsWide / HK_PAGE || dims->NS * dims->Hkv > (1 << 20)) return HK_ERR_SHAPE;
   const CompressWs cw = compress_ws(dims, kv->max_pages);
   if (ws_bytes < cw.total) return HK_ERR_WORKSPACE;
   if (!aligned256(workspace)) return HK_ERR_ALIGN;

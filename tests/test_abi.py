@@ -156,6 +156,9 @@ def test_validation_errors_without_gpu(hk):
                          None, P, None, P, 16, None) == 5       # workspace too small
     assert L.hk_compress(C.byref(d), P, C.byref(kv), 0, 0, 0.125, None, 1.5, 1, 0, C.byref(alloc),
                          None, P, None, P, 1 << 30, None) == 1  # p outside [0, 1]
+    kv_long = _kv(hk, max_pages=262144 // 16 + 2)
+    assert L.hk_compress(C.byref(d), P, C.byref(kv_long), 0, 0, 0.125, None, 0.9, 1, 0,
+                         C.byref(alloc), None, P, None, P, 1 << 40, None) == 3   # rows too long
     a64 = hk.hk_allocator(P, P, 64)
     assert L.hk_alloc_init(C.byref(a64), -1, 10, None) == 1
     assert L.hk_alloc_init(C.byref(a64), 10, 5, None) == 1           # num_pages < first_free

@@ -187,3 +187,72 @@ def test_calibrate_topp_ws_repeated_calls_reuse_the_workspace():
             res.append((sel.cpu(), k.cpu(), c.cpu()))
         for a, b in zip(*res):
             assert torch.equal(a, b)
+
+
+def test_compression_step_on_long_rows():
+    """The whole step on rows of 131072 slots (64 select chunks per head), where only the
+    wide selector applies: Compressor's separate calls and the one-call hk_compress leave
+    the same cache, counts and bitmap bit for bit; the scores and calibrated probabilities
+    match the oracle's; the selection obeys the Top-p rule on the calibrated values it was
+    made from, and the rewrite leaves the page list the tiers define for it."""
+    import math
+    import workload as WL
+    from hk_testlib import HostCache, check_compaction, check_log_scores, q_rows, rewrite_layout, snapshot
+    from paper_2606_28831_amd.pipeline import Compressor
+    hk = _hk()
+    cfg = dict(L=1, B=1, Hq=8, Hkv=2, D=128, N=131072 - 37, dtype="bf16", W=16, seed=5,
+               recipe="tempered")
+    G, p, scale = 4, 0.9, 1 / math.sqrt(128)
+    outs = []
+    for fused in (False, True):
+        w = WL.make_workload(cfg, DEV, hole_prob=0.05, max_pages=8192)
+        kv = hk.PagedKV(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)
+        alloc = hk.Allocator(w.free_ids, w.free_top)
+        H, S = w.n_heads, w.S_max
+        assert S == 131072
+        st = torch.zeros(1, dtype=torch.int32, device=DEV)
+        before = snapshot(w)
+        if fused:
+            d = hk.dims(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"], cfg["W"])
+            k = torch.empty(H, dtype=torch.int32, device=DEV)
+            sel = torch.empty(H, S // 32, dtype=torch.int32, device=DEV)
+            hk.hk_compress(d, w.q_obs, kv, 0, 0, scale, p, alloc, k,
+                           hk.workspace(hk.OP_COMPRESS, d, w.max_pages, DEV), status=st,
+                           sel_bits_out=sel)
+            torch.cuda.synchronize()
+        else:
+            host = HostCache(w.k_pool, None, w.page_table, w.page_mask, w.n_pages)
+            comp = Compressor(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"], cfg["W"], kv, alloc, p)
+            comp.score(w.q_obs)
+            comp.select()
+            torch.cuda.synchronize()
+            b = comp.buf
+            s_np, c_np = np64(b.s_attn), b.c.cpu().numpy()
+            sel_np, k_np = np_i(b.sel_bits), np_i(b.k)
+            qn = np64(w.q_obs)
+            for h in range(H):
+                rows, valid = host.head(h)
+                cand_len = 16 * int(host.n[h])
+                s_ref, _ = O.score_head(q_rows(qn, h, cfg["Hkv"], G), rows, valid, cand_len, scale)
+                full = np.full(S, -np.inf)
+                full[:len(s_ref)] = s_ref
+                check_log_scores(s_np[h], full, 2e-3, f"long-row score head {h}")
+                cand = np.zeros(S, bool)
+                cand[:len(valid)] = O.candidate_mask(valid, cand_len)
+                c_ref, _ = O.calibrate_head(full, cand)
+                check_prob(c_np[h].astype(np.float64), c_ref, 2e-3, f"long-row c head {h}")
+                check_topp_rule(c_np[h], unpack_bits(sel_np[h], S), int(k_np[h]), cand, p,
+                                what=f"long-row head {h}")
+            comp.compact()
+            torch.cuda.synchronize()
+            check_compaction(w, before, sel_np, S, lambda h, sl: rewrite_layout(
+                before["table"][h], before["mask"][h], int(before["n"][h]), sl, 0))
+            k, sel, st = b.k, b.sel_bits, b.status
+        assert int(st.item()) == 0
+        outs.append([t.cpu().clone() for t in (k, sel, w.page_table, w.page_mask, w.n_pages,
+                                               w.free_ids, w.free_top)]
+                    + [w.k_pool.view(torch.int16).cpu(), w.v_pool.view(torch.int16).cpu()])
+        del w, kv
+        torch.cuda.empty_cache()
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)

@@ -657,14 +657,22 @@ __global__ __launch_bounds__(SW_FT) void sw_finish_kernel(
     });
     __syncthreads();
     if (tid == 0) {
-      uint32_t seen = 0, pos = 0;
-      for (int b = 127; b >= 0; --b)
-        if ((sh.tmask[b >> 5] >> (b & 31)) & 1u) {
-          if (++seen == rem) {
-            pos = (uint32_t)b;
-            break;
-          }
+      // the rem-th set bit from the top of the block's 128-bit tie mask, from registers:
+      // whole words are skipped by their population counts, then the word's higher set
+      // bits are cleared one at a time
+      const uint32_t m[4] = {sh.tmask[0], sh.tmask[1], sh.tmask[2], sh.tmask[3]};
+      uint32_t need = rem, pos = 0;
+      for (int wd = 3; wd >= 0; --wd) {
+        const uint32_t c = (uint32_t)__popc(m[wd]);
+        if (need > c) {
+          need -= c;
+          continue;
         }
+        uint32_t x = m[wd];
+        for (uint32_t i = 1; i < need; ++i) x &= ~(0x80000000u >> __clz(x));
+        pos = (uint32_t)(wd * 32 + 31 - __clz(x));
+        break;
+      }
       sh.tie_from = (blk << SW_TSH) + pos;
     }
     __syncthreads();

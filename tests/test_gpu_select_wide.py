@@ -256,3 +256,46 @@ def test_compression_step_on_long_rows():
         torch.cuda.empty_cache()
     for a, b in zip(*outs):
         assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_topp_ws_random_shapes_equal_single_workgroup(seed):
+    """Random row lengths (any multiple of 32 up to 32768, so chunks of every fill and a last
+    chunk of any length), candidate counts, page holes, clamps and value mixes -- coarse
+    values with many exact ties, one-binade values, spread values, zeros and NaN: the wide
+    selector equals the single-workgroup selector bit for bit (bitmap, count, mass, flags)."""
+    hk = _hk()
+    rng = np.random.default_rng(1000 + seed)
+    H = 5
+    S = int(rng.integers(1, 1025)) * 32
+    kind = seed % 4
+    if kind == 0:
+        c = np.round(rng.random((H, S)), 2).astype(np.float32) / S          # ties
+    elif kind == 1:
+        c = (1.0 + rng.random((H, S)) * 0.01).astype(np.float32) / S        # one binade
+    elif kind == 2:
+        c = np.exp2(-rng.random((H, S)) * 30).astype(np.float32)            # 30 binades
+    else:
+        c = rng.random((H, S)).astype(np.float32)
+        c[:, ::7] = 0.0
+        c[0, :3] = [np.nan, -1.0, 2.0]
+    cand_len = rng.integers(0, S + 1, H).astype(np.int32)
+    cand_len[0] = S
+    valid, words = _holes(H, S, rng)
+    kmin, kmax = (int(rng.integers(0, 4)), int(rng.integers(0, S // 2 + 2))) if seed % 3 == 0 else (1, 0)
+    p = float(rng.choice([0.5, 0.9, 0.999, 1.0]))
+    mask = torch.tensor(words, device=DEV)
+    sel, k, sm, st = _topp_ws(c, cand_len, p, kmin, kmax, mask=mask)
+    sel1 = torch.empty(H, S // 32, dtype=torch.int32, device=DEV)
+    k1 = torch.empty(H, dtype=torch.int32, device=DEV)
+    sm1 = torch.empty(H, device=DEV)
+    st1 = torch.zeros(1, dtype=torch.int32, device=DEV)
+    hk.hk_topp_select(H, S, torch.tensor(cand_len, device=DEV), mask, torch.tensor(c, device=DEV),
+                      p, sel1, k1, k_min=kmin, k_max=kmax, sel_mass=sm1, status=st1)
+    torch.cuda.synchronize()
+    assert np.array_equal(sel, np_i(sel1)) and np.array_equal(k, np_i(k1)), (seed, S, kind)
+    assert np.array_equal(sm.view(np.int32), sm1.cpu().numpy().view(np.int32)), (seed, S)
+    assert st == int(st1.item()), (seed, st, int(st1.item()))
+    if seed < 4:                                   # and the oracle, on the smaller draws
+        cands = [O.candidate_mask(valid[h], int(cand_len[h])) for h in range(H)]
+        _check_topp(c, cands, p, kmin, kmax, sel, k, sm, f"random {seed}")

@@ -13,9 +13,11 @@
 //           key bits and its 11-bit slot.
 //   finish  one workgroup per head: sums the chunk histograms, picks the level-1 digit,
 //           gathers that digit's keys from the chunks' sorted segments (into LDS when they
-//           fit: always for heads of up to 32768 slots), refines the threshold over the low 21 bits in levels of 11 and 10 bits, applies
-//           the count clamp and breaks the ties at the threshold toward the later slots;
-//           writes the count, the selected mass and the head's threshold.
+//           fit: always for heads of up to 32768 slots), refines the threshold over the low
+//           21 bits in levels of 11 and 10 bits, applies the count clamp and breaks the ties
+//           at the threshold toward the later slots (ties counted per 128-slot block, then
+//           the cut found inside one block); writes the count, the selected mass and the
+//           head's threshold.
 //   bitmap  one workgroup per (head, chunk): every key of a higher digit is selected, the
 //           keys of the threshold digit by the threshold rule, the rest not.
 // The launches hand their results over through memory in stream order: no workgroup waits

@@ -266,7 +266,8 @@ hk_status hk_pool_max(int32_t n_heads, int32_t S_max, const int32_t* cand_len,
  *   end, otherwise the upper end comes down; T_out = exp(midpoint of the final bracket).
  * Arguments: x [n_heads][S_max] fp32; k [n_heads] int32 (the Top-p count of the target
  * distribution); target_mass [n_heads] fp32; T_out [n_heads] fp32.
- * 0 < T_lo < T_hi; iters in [1, 64].
+ * 0 < T_lo < T_hi; iters in [1, 64]; S_max a multiple of 32, at most 262144 (rows longer
+ * than 32768 slots are streamed from memory in each sweep instead of held in registers).
  */
 hk_status hk_calibrate_solve_T(int32_t n_heads, int32_t S_max, const int32_t* cand_len,
                                const uint16_t* page_mask, const float* x, const int32_t* k,

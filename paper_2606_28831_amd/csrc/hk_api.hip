@@ -278,7 +278,7 @@ hk_status hk_calibrate_solve_T(int32_t n_heads, int32_t S_max, const int32_t* ca
                                const uint16_t* page_mask, const float* x, const int32_t* k,
                                const float* target_mass, float T_lo, float T_hi, int32_t iters,
                                float* T_out, hipStream_t stream) {
-  hk_status e = check_rows(n_heads, S_max, cand_len);
+  hk_status e = check_rows_wide(n_heads, S_max, cand_len);       // longer rows are streamed
   if (e) return e;
   if (!x || !k || !target_mass || !T_out) return HK_ERR_ARG;
   if (!(T_lo > 0.f) || !(T_hi > T_lo) || !std::isfinite(T_hi) || iters < 1 || iters > 64)

@@ -710,6 +710,144 @@ __global__ __launch_bounds__(SEL_NT) void solve_T_kernel(
   if (tid == 0) T_out[h] = expf(0.5f * (a + b));
 }
 
+// The same rule for rows longer than one workgroup holds in registers (S_max > 32768): the
+// row is streamed from memory in every sweep.  The k-th largest key comes from an 8-bit
+// radix search (four sweeps, each a 256-bin count histogram of the keys that share the
+// digits found so far), the ties it leaves are cut by slot from per-thread counts over
+// contiguous runs of slots (the most recent slots are taken), and each bisection step is one
+// sweep of two block sums.  Only the summation order differs from solve_T_kernel.
+__device__ __forceinline__ int wave_incl_scan_i(int v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int o = __shfl_up(v, d, 64);
+    if (lane >= d) v += o;
+  }
+  return v;
+}
+
+__global__ __launch_bounds__(SEL_NT) void solve_T_long_kernel(
+    int S_max, const int32_t* __restrict__ cand_len, const uint16_t* __restrict__ mask,
+    const float* __restrict__ x, const int32_t* __restrict__ k_arr, const float* __restrict__ target,
+    float T_lo, float T_hi, int iters, float* __restrict__ T_out) {
+  __shared__ float red[SEL_NW];
+  __shared__ int redi[SEL_NW];
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t s_digit;
+  __shared__ int s_above, s_tie_from;
+  const int h = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int cl = cand_len[h];
+  const uint16_t* mrow = mask ? mask + (size_t)h * (S_max / HK_PAGE) : nullptr;
+  const float* xrow = x + (size_t)h * S_max;
+
+  float mx = -INFINITY;
+  int nc = 0;
+  for (int j = tid; j < S_max; j += SEL_NT)
+    if (is_cand(mrow, cl, j)) {
+      ++nc;
+      mx = fmaxf(mx, xrow[j]);
+    }
+  mx = block_max<SEL_NT>(mx, red);
+  const int n_cand = block_sum_int<SEL_NT>(nc, redi);
+  const int kk = min(max(k_arr[h], 0), n_cand);
+
+  // the kk-th largest key v, digit by digit; `above` counts the keys greater than v
+  uint32_t v = 0xffffffffu;
+  int tie_from = S_max;                  // slots >= tie_from among the keys equal to v are taken
+  if (kk > 0) {
+    uint32_t prefix = 0;
+    int above = 0, n_tie = 0;
+    for (int shift = 24; shift >= 0; shift -= 8) {
+      for (int i = tid; i < 256; i += SEL_NT) hist[i] = 0u;
+      __syncthreads();
+      for (int j = tid; j < S_max; j += SEL_NT)
+        if (is_cand(mrow, cl, j)) {
+          const uint32_t key = ordered_key(xrow[j]);
+          if (shift == 24 || (key >> (shift + 8)) == (prefix >> (shift + 8)))
+            atomicAdd(&hist[(key >> shift) & 255u], 1u);
+        }
+      __syncthreads();
+      if (tid == 0) {
+        int cum = above;
+        uint32_t d = 0;
+        for (int b = 255; b >= 0; --b) {
+          if (cum + (int)hist[b] >= kk) {
+            d = (uint32_t)b;
+            break;
+          }
+          cum += (int)hist[b];
+        }
+        s_digit = d;
+        s_above = cum;
+      }
+      __syncthreads();
+      prefix |= s_digit << shift;
+      above = s_above;
+      n_tie = (int)hist[s_digit];
+      __syncthreads();                   // every thread has read the histogram
+    }
+    v = prefix;
+    const int take = kk - above;         // >= 1
+    if (take >= n_tie) {
+      tie_from = 0;
+    } else {
+      // ties in this thread's run of slots, then the runs above it (higher slots)
+      const int P = (S_max + SEL_NT - 1) / SEL_NT, j0 = tid * P, j1 = min(j0 + P, S_max);
+      int cnt = 0;
+      for (int j = j0; j < j1; ++j)
+        if (is_cand(mrow, cl, j) && ordered_key(xrow[j]) == v) ++cnt;
+      const int incl = wave_incl_scan_i(cnt);
+      __syncthreads();
+      if (lane == 63) redi[wave] = incl;
+      __syncthreads();
+      int before = incl - cnt, total = 0;          // ties in runs below this one
+#pragma unroll
+      for (int w = 0; w < SEL_NW; ++w) {
+        if (w < wave) before += redi[w];
+        total += redi[w];
+      }
+      const int after = total - before - cnt;     // ties in runs above this one
+      if (after < take && after + cnt >= take) {
+        int r = take - after;
+        int cut = j0;
+        for (int j = j1 - 1; j >= j0; --j)
+          if (is_cand(mrow, cl, j) && ordered_key(xrow[j]) == v && --r == 0) {
+            cut = j;
+            break;
+          }
+        s_tie_from = cut;
+      }
+      __syncthreads();
+      tie_from = s_tie_from;
+    }
+  }
+
+  const float tgt = target[h];
+  float a = logf(T_lo), b = logf(T_hi);
+  for (int it = 0; it < iters; ++it) {
+    const float mid = 0.5f * (a + b);
+    const float invT = expf(-mid);
+    float s_all = 0.f, s_top = 0.f;
+    if (mx != -INFINITY)
+      for (int j = tid; j < S_max; j += SEL_NT)
+        if (is_cand(mrow, cl, j)) {
+          const float xv = xrow[j];
+          const float e = expf((xv - mx) * invT);
+          s_all += e;
+          if (kk > 0) {
+            const uint32_t key = ordered_key(xv);
+            if ((v != 0xffffffffu && key > v) || (key == v && j >= tie_from)) s_top += e;
+          }
+        }
+    s_all = block_sum<SEL_NT>(s_all, red);
+    s_top = block_sum<SEL_NT>(s_top, red);
+    const float mass = (s_all > 0.f) ? s_top / s_all : 0.f;
+    if (mass - tgt > 0.f) a = mid;
+    else b = mid;
+  }
+  if (tid == 0) T_out[h] = expf(0.5f * (a + b));
+}
+
 // a2': temperature by gradient descent (Alg. 1, Solution 2 form).  theta = log T, loss
 // (M_k(Softmax(x/T)) - target)^2, Adam (0.9 / 0.999 / 1e-8, bias-corrected, no weight
 // decay).  M_k and its derivative come from four block sums per iteration:
@@ -899,6 +1037,11 @@ hipError_t hk_launch_solve_T(int n_heads, int S_max, const int32_t* cand_len, co
                              const float* x, const int32_t* k, const float* target, float T_lo,
                              float T_hi, int iters, float* T_out, hipStream_t st) {
   TimedLaunch t(HK_TK_SOLVE_T, st);
+  if (S_max > SEL_NT * 32) {
+    hipLaunchKernelGGL(solve_T_long_kernel, dim3(n_heads), dim3(SEL_NT), 0, st, S_max, cand_len, mask,
+                       x, k, target, T_lo, T_hi, iters, T_out);
+    return hipGetLastError();
+  }
   HK_EPT_SWITCH(S_max, hipLaunchKernelGGL((solve_T_kernel<E>), dim3(n_heads), dim3(SEL_NT), 0, st,
                                           S_max, cand_len, mask, x, k, target, T_lo, T_hi, iters,
                                           T_out));

@@ -91,6 +91,7 @@ def test_validation_errors_without_gpu(hk):
     assert L.hk_topp_select(4, 128, None, None, P, 0.9, 1, 0, P, P, None, None, None) == 1
     assert L.hk_calibrate_solve_T(4, 128, P, None, P, P, P, 1.0, 0.5, 40, P, None) == 1
     assert L.hk_calibrate_solve_T(4, 128, P, None, P, P, P, 1e-4, 1e4, 0, P, None) == 1
+    assert L.hk_calibrate_solve_T(4, 262144 + 32, P, None, P, P, P, 1e-4, 1e4, 40, P, None) == 3
     alloc = hk.hk_allocator(P, P, 64)
     assert L.hk_compact(C.byref(d), C.byref(kv), P, -1, 0, C.byref(alloc), P, P, 1 << 30, None) == 1
     # a free stack shorter than the pool (64 pages) could overflow when the rewrite pushes

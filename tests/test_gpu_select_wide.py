@@ -299,3 +299,54 @@ def test_topp_ws_random_shapes_equal_single_workgroup(seed):
     if seed < 4:                                   # and the oracle, on the smaller draws
         cands = [O.candidate_mask(valid[h], int(cand_len[h])) for h in range(H)]
         _check_topp(c, cands, p, kmin, kmax, sel, k, sm, f"random {seed}")
+
+
+def test_two_metric_step_on_long_rows():
+    """The mixture path (attention mass + sampled redundancy, 0.5 / 0.5 after the
+    redundancy temperature is solved) on 65536-slot rows, where both the selector and the
+    temperature search take their long-row kernels: each head's mixture equals the oracle's
+    chain on the same cache (oracle scores and redundancy, its Top-p count and mass, its
+    temperature, its mixture), and the selection obeys the Top-p rule on it."""
+    import math
+    import workload as WL
+    from hk_testlib import HostCache, check_log_scores, q_rows
+    from paper_2606_28831_amd.pipeline import Compressor
+    hk = _hk()
+    cfg = dict(L=1, B=1, Hq=8, Hkv=2, D=128, N=65536 - 200, dtype="bf16", W=16, seed=9,
+               recipe="normal", n_ref=256)
+    G, p, scale = 4, 0.9, 1 / math.sqrt(128)
+    w = WL.make_workload(cfg, DEV, max_pages=4096, hole_prob=0.02)
+    kv = hk.PagedKV(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)
+    host = HostCache(w.k_pool, None, w.page_table, w.page_mask, w.n_pages)
+    comp = Compressor(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"], cfg["W"], kv,
+                      hk.Allocator(w.free_ids, w.free_top), p, metric="attn+red", n_ref=256)
+    H, S = w.n_heads, w.S_max
+    assert S == 65536
+    comp.score(w.q_obs, ref_slots=w.ref_slots)
+    comp.select()
+    torch.cuda.synchronize()
+    b = comp.buf
+    assert int(b.status.item()) == 0
+    s_np, c_np, sel_np, k_np = np64(b.s_attn), b.c.cpu().numpy(), np_i(b.sel_bits), np_i(b.k)
+    T_gpu, qn, ref = np64(b.T_red), np64(w.q_obs), np_i(w.ref_slots)
+    for h in range(H):
+        rows, valid = host.head(h)
+        cand_len = 16 * int(host.n[h])
+        s_ref, _ = O.score_head(q_rows(qn, h, cfg["Hkv"], G), rows, valid, cand_len, scale)
+        full = np.full(S, -np.inf)
+        full[:len(s_ref)] = s_ref
+        check_log_scores(s_np[h], full, 2e-3, f"score head {h}")
+        cand = np.zeros(S, bool)
+        cand[:len(valid)] = O.candidate_mask(valid, cand_len)
+        xr = np.full(S, -np.inf)
+        xr_full = O.redundancy_head(rows, valid, cand_len, ref[h])
+        xr[:len(xr_full)] = xr_full
+        c_att, _ = O.calibrate_head(full, cand)
+        r_att = O.topp_head(c_att.astype(np.float32), cand, p)
+        T_ref = O.solve_T_head(xr, cand, r_att.k, r_att.sel_mass / 2.0 ** 40)
+        assert float(T_gpu[h]) == pytest.approx(T_ref, rel=2e-3), (h, float(T_gpu[h]), T_ref)
+        c_red, _ = O.calibrate_head(xr, cand, T_ref)
+        check_prob(c_np[h].astype(np.float64), O.mix([c_att, c_red], [0.5, 0.5]), 2e-3,
+                   f"mixture head {h}")
+        check_topp_rule(c_np[h], unpack_bits(sel_np[h], S), int(k_np[h]), cand, p,
+                        what=f"mixture head {h}")

@@ -406,6 +406,49 @@ def test_solve_T(case, S):
 
 
 @pytest.mark.parametrize("case", range(4))
+@pytest.mark.parametrize("S", [65536, 131072 + 32])
+def test_solve_T_long_rows(case, S):
+    """Rows past one workgroup's registers take the streaming bisection (radix-searched
+    Top-k, ties cut by slot): against the oracle's bisection and, for two-level rows, the
+    closed form; with page holes, a ragged candidate count and tied values at the k-th."""
+    import paper_2606_28831_amd as hk
+    H = 4
+    rng = np.random.default_rng(100 + case)
+    x = np.full((H, S), -np.inf, np.float32)
+    cand_len = np.array([S, S - 32 * 37, S // 2 + 64, 40 * 32], np.int32)
+    ks = np.zeros(H, np.int32)
+    tg = np.zeros(H, np.float32)
+    for h in range(H):
+        n = int(cand_len[h])
+        if case == 0:     # two-level closed form
+            k = max(1, n // 10)
+            x[h, :n] = 0.0
+            x[h, rng.permutation(n)[:k]] = 1.0
+            tg[h], ks[h] = 0.5, k
+        elif case == 3:   # few distinct values: the k-th largest sits inside a run of ties
+            x[h, :n] = rng.choice(np.float32([-0.5, -1.0, -2.0, -3.0]), n)
+            ks[h] = int(rng.integers(1, n))
+            tg[h] = rng.uniform(ks[h] / n * 1.05, 0.99)
+        else:
+            x[h, :n] = -rng.random(n).astype(np.float32) * (case * 0.7)
+            ks[h] = rng.integers(1, max(2, (9 * n) // 10))
+            tg[h] = rng.uniform(ks[h] / n * 1.05, 0.99)
+    T = torch.empty(H, device=DEV)
+    hk.hk_calibrate_solve_T(H, S, torch.tensor(cand_len, device=DEV), None,
+                            torch.tensor(x, device=DEV), torch.tensor(ks, device=DEV),
+                            torch.tensor(tg, device=DEV), T)
+    torch.cuda.synchronize()
+    for h in range(H):
+        cand = np.arange(S) < cand_len[h]
+        want = O.solve_T_head(x[h].astype(np.float64), cand, int(ks[h]), float(tg[h]))
+        assert float(T[h]) == pytest.approx(want, rel=2e-3), (case, S, h)
+        if case == 0:
+            n, k = int(cand_len[h]), int(ks[h])
+            closed = 1.0 / math.log(0.5 * (n - k) / (k * 0.5))
+            assert float(T[h]) == pytest.approx(closed, rel=2e-3)
+
+
+@pytest.mark.parametrize("case", range(4))
 @pytest.mark.parametrize("S", [1024, 32768])
 def test_solve_T_gd(case, S):
     """Alg. 1 on the GPU against the oracle's Adam iterations (fixed count), on two-level

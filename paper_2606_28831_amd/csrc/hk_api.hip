@@ -291,7 +291,7 @@ hk_status hk_calibrate_solve_T_gd(int32_t n_heads, int32_t S_max, const int32_t*
                                   const uint16_t* page_mask, const float* x, const int32_t* k,
                                   const float* target_mass, float T_init, float lr, int32_t iters,
                                   float tol, float* T_out, float* loss_out, hipStream_t stream) {
-  hk_status e = check_rows(n_heads, S_max, cand_len);
+  hk_status e = check_rows_wide(n_heads, S_max, cand_len);    // longer rows are streamed
   if (e) return e;
   if (!x || !k || !target_mass || !T_out) return HK_ERR_ARG;
   if (!(T_init > 0.f) || !std::isfinite(T_init) || !(lr > 0.f) || !std::isfinite(lr)) return HK_ERR_ARG;

@@ -726,16 +726,101 @@ __device__ __forceinline__ int wave_incl_scan_i(int v) {
   return v;
 }
 
+// Shared state of the streamed Top-k search.
+struct LongTopK {
+  uint32_t hist[256];
+  uint32_t digit;
+  int above, tie_from;
+};
+
+// The Top-k set of a streamed row as (v, tie_from): candidates with key > v, and those with
+// key == v at slots >= tie_from (v = 0xffffffff and tie_from = S_max for kk = 0).  Every
+// thread of the block calls it; `redi` holds one int per wave.
+__device__ __forceinline__ void long_topk(int S_max, const uint16_t* mrow, int cl, const float* xrow,
+                                          int kk, uint32_t& v, int& tie_from, LongTopK& sh, int* redi) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  v = 0xffffffffu;
+  tie_from = S_max;
+  if (kk <= 0) return;
+  uint32_t prefix = 0;
+  int above = 0, n_tie = 0;
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    for (int i = tid; i < 256; i += SEL_NT) sh.hist[i] = 0u;
+    __syncthreads();
+    for (int j = tid; j < S_max; j += SEL_NT)
+      if (is_cand(mrow, cl, j)) {
+        const uint32_t key = ordered_key(xrow[j]);
+        if (shift == 24 || (key >> (shift + 8)) == (prefix >> (shift + 8)))
+          atomicAdd(&sh.hist[(key >> shift) & 255u], 1u);
+      }
+    __syncthreads();
+    if (tid == 0) {
+      int cum = above;
+      uint32_t d = 0;
+      for (int b = 255; b >= 0; --b) {
+        if (cum + (int)sh.hist[b] >= kk) {
+          d = (uint32_t)b;
+          break;
+        }
+        cum += (int)sh.hist[b];
+      }
+      sh.digit = d;
+      sh.above = cum;
+    }
+    __syncthreads();
+    prefix |= sh.digit << shift;
+    above = sh.above;
+    n_tie = (int)sh.hist[sh.digit];
+    __syncthreads();                   // every thread has read the histogram
+  }
+  v = prefix;
+  const int take = kk - above;         // >= 1
+  if (take >= n_tie) {
+    tie_from = 0;
+    return;
+  }
+  // ties in this thread's run of slots, then the runs above it (higher slots)
+  const int P = (S_max + SEL_NT - 1) / SEL_NT, j0 = tid * P, j1 = min(j0 + P, S_max);
+  int cnt = 0;
+  for (int j = j0; j < j1; ++j)
+    if (is_cand(mrow, cl, j) && ordered_key(xrow[j]) == v) ++cnt;
+  const int incl = wave_incl_scan_i(cnt);
+  __syncthreads();
+  if (lane == 63) redi[wave] = incl;
+  __syncthreads();
+  int before = incl - cnt, total = 0;  // ties in runs below this one, in all runs
+#pragma unroll
+  for (int w = 0; w < SEL_NW; ++w) {
+    if (w < wave) before += redi[w];
+    total += redi[w];
+  }
+  const int after = total - before - cnt;     // ties in runs above this one
+  if (after < take && after + cnt >= take) {
+    int r = take - after;
+    int cut = j0;
+    for (int j = j1 - 1; j >= j0; --j)
+      if (is_cand(mrow, cl, j) && ordered_key(xrow[j]) == v && --r == 0) {
+        cut = j;
+        break;
+      }
+    sh.tie_from = cut;
+  }
+  __syncthreads();
+  tie_from = sh.tie_from;
+}
+
+__device__ __forceinline__ bool long_in_top(uint32_t key, int j, uint32_t v, int tie_from) {
+  return (v != 0xffffffffu && key > v) || (key == v && j >= tie_from);
+}
+
 __global__ __launch_bounds__(SEL_NT) void solve_T_long_kernel(
     int S_max, const int32_t* __restrict__ cand_len, const uint16_t* __restrict__ mask,
     const float* __restrict__ x, const int32_t* __restrict__ k_arr, const float* __restrict__ target,
     float T_lo, float T_hi, int iters, float* __restrict__ T_out) {
   __shared__ float red[SEL_NW];
   __shared__ int redi[SEL_NW];
-  __shared__ uint32_t hist[256];
-  __shared__ uint32_t s_digit;
-  __shared__ int s_above, s_tie_from;
-  const int h = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  __shared__ LongTopK sh;
+  const int h = blockIdx.x, tid = threadIdx.x;
   const int cl = cand_len[h];
   const uint16_t* mrow = mask ? mask + (size_t)h * (S_max / HK_PAGE) : nullptr;
   const float* xrow = x + (size_t)h * S_max;
@@ -750,77 +835,9 @@ __global__ __launch_bounds__(SEL_NT) void solve_T_long_kernel(
   mx = block_max<SEL_NT>(mx, red);
   const int n_cand = block_sum_int<SEL_NT>(nc, redi);
   const int kk = min(max(k_arr[h], 0), n_cand);
-
-  // the kk-th largest key v, digit by digit; `above` counts the keys greater than v
-  uint32_t v = 0xffffffffu;
-  int tie_from = S_max;                  // slots >= tie_from among the keys equal to v are taken
-  if (kk > 0) {
-    uint32_t prefix = 0;
-    int above = 0, n_tie = 0;
-    for (int shift = 24; shift >= 0; shift -= 8) {
-      for (int i = tid; i < 256; i += SEL_NT) hist[i] = 0u;
-      __syncthreads();
-      for (int j = tid; j < S_max; j += SEL_NT)
-        if (is_cand(mrow, cl, j)) {
-          const uint32_t key = ordered_key(xrow[j]);
-          if (shift == 24 || (key >> (shift + 8)) == (prefix >> (shift + 8)))
-            atomicAdd(&hist[(key >> shift) & 255u], 1u);
-        }
-      __syncthreads();
-      if (tid == 0) {
-        int cum = above;
-        uint32_t d = 0;
-        for (int b = 255; b >= 0; --b) {
-          if (cum + (int)hist[b] >= kk) {
-            d = (uint32_t)b;
-            break;
-          }
-          cum += (int)hist[b];
-        }
-        s_digit = d;
-        s_above = cum;
-      }
-      __syncthreads();
-      prefix |= s_digit << shift;
-      above = s_above;
-      n_tie = (int)hist[s_digit];
-      __syncthreads();                   // every thread has read the histogram
-    }
-    v = prefix;
-    const int take = kk - above;         // >= 1
-    if (take >= n_tie) {
-      tie_from = 0;
-    } else {
-      // ties in this thread's run of slots, then the runs above it (higher slots)
-      const int P = (S_max + SEL_NT - 1) / SEL_NT, j0 = tid * P, j1 = min(j0 + P, S_max);
-      int cnt = 0;
-      for (int j = j0; j < j1; ++j)
-        if (is_cand(mrow, cl, j) && ordered_key(xrow[j]) == v) ++cnt;
-      const int incl = wave_incl_scan_i(cnt);
-      __syncthreads();
-      if (lane == 63) redi[wave] = incl;
-      __syncthreads();
-      int before = incl - cnt, total = 0;          // ties in runs below this one
-#pragma unroll
-      for (int w = 0; w < SEL_NW; ++w) {
-        if (w < wave) before += redi[w];
-        total += redi[w];
-      }
-      const int after = total - before - cnt;     // ties in runs above this one
-      if (after < take && after + cnt >= take) {
-        int r = take - after;
-        int cut = j0;
-        for (int j = j1 - 1; j >= j0; --j)
-          if (is_cand(mrow, cl, j) && ordered_key(xrow[j]) == v && --r == 0) {
-            cut = j;
-            break;
-          }
-        s_tie_from = cut;
-      }
-      __syncthreads();
-      tie_from = s_tie_from;
-    }
-  }
+  uint32_t v;
+  int tie_from;
+  long_topk(S_max, mrow, cl, xrow, kk, v, tie_from, sh, redi);
 
   const float tgt = target[h];
   float a = logf(T_lo), b = logf(T_hi);
@@ -834,10 +851,7 @@ __global__ __launch_bounds__(SEL_NT) void solve_T_long_kernel(
           const float xv = xrow[j];
           const float e = expf((xv - mx) * invT);
           s_all += e;
-          if (kk > 0) {
-            const uint32_t key = ordered_key(xv);
-            if ((v != 0xffffffffu && key > v) || (key == v && j >= tie_from)) s_top += e;
-          }
+          if (kk > 0 && long_in_top(ordered_key(xv), j, v, tie_from)) s_top += e;
         }
     s_all = block_sum<SEL_NT>(s_all, red);
     s_top = block_sum<SEL_NT>(s_top, red);
@@ -901,6 +915,95 @@ __global__ __launch_bounds__(SEL_NT) void solve_T_gd_kernel(
         q[0] += e;
         q[2] += xe;
         if ((top >> i) & 1u) {
+          q[1] += e;
+          q[3] += xe;
+        }
+      }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) q[c] = wave_sum(q[c]);
+    __syncthreads();
+    if (lane == 0)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) red4[c][wave] = q[c];
+    __syncthreads();
+    float t4[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int w = 0; w < SEL_NW; ++w)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) t4[c] += red4[c][w];
+    if (t4[1] == 0.f) return;
+    M = t4[1] / t4[0];
+    dM = -u * M * (t4[3] / t4[1] - t4[2] / t4[0]);
+  };
+  float theta = logf(T_init), m = 0.f, v = 0.f, b1t = 1.f, b2t = 1.f, loss = 0.f;
+  for (int t = 1; t <= iters; ++t) {
+    float M, dM;
+    mass_grad(theta, M, dM);
+    const float gap = M - tgt;
+    loss = gap * gap;
+    if (loss < tol) break;
+    const float g = 2.f * gap * dM;
+    m = 0.9f * m + 0.1f * g;
+    v = 0.999f * v + 0.001f * g * g;
+    b1t *= 0.9f;
+    b2t *= 0.999f;
+    theta -= lr * (m / (1.f - b1t)) / (sqrtf(v / (1.f - b2t)) + 1e-8f);
+  }
+  if (iters > 0) {
+    float M, dM;
+    mass_grad(theta, M, dM);
+    loss = (M - tgt) * (M - tgt);
+  }
+  if (tid == 0) {
+    T_out[h] = expf(theta);
+    if (loss_out) loss_out[h] = loss;
+  }
+}
+
+// The gradient-descent temperature for rows longer than 32768 slots: the same Adam steps on
+// the same loss, the Top-k set from long_topk and each step's four sums from one sweep of
+// the row in memory.
+__global__ __launch_bounds__(SEL_NT) void solve_T_gd_long_kernel(
+    int S_max, const int32_t* __restrict__ cand_len, const uint16_t* __restrict__ mask,
+    const float* __restrict__ x, const int32_t* __restrict__ k_arr, const float* __restrict__ target,
+    float T_init, float lr, int iters, float tol, float* __restrict__ T_out, float* __restrict__ loss_out) {
+  __shared__ float red[SEL_NW];
+  __shared__ float red4[4][SEL_NW];
+  __shared__ int redi[SEL_NW];
+  __shared__ LongTopK sh;
+  const int h = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int cl = cand_len[h];
+  const uint16_t* mrow = mask ? mask + (size_t)h * (S_max / HK_PAGE) : nullptr;
+  const float* xrow = x + (size_t)h * S_max;
+  float mx = -INFINITY;
+  int nc = 0;
+  for (int j = tid; j < S_max; j += SEL_NT)
+    if (is_cand(mrow, cl, j)) {
+      ++nc;
+      mx = fmaxf(mx, xrow[j]);
+    }
+  mx = block_max<SEL_NT>(mx, red);
+  const int n_cand = block_sum_int<SEL_NT>(nc, redi);
+  const int kk = min(max(k_arr[h], 0), n_cand);
+  uint32_t vthr;
+  int tie_from;
+  long_topk(S_max, mrow, cl, xrow, kk, vthr, tie_from, sh, redi);
+  const float tgt = target[h];
+  // M_k and dM/dtheta at theta (uniform across the block)
+  auto mass_grad = [&](float theta, float& M, float& dM) {
+    M = 0.f;
+    dM = 0.f;
+    if (kk <= 0 || mx == -INFINITY) return;
+    const float u = expf(-theta);
+    float q[4] = {0.f, 0.f, 0.f, 0.f};    // sum e, sum_top e, sum x e, sum_top x e
+    for (int j = tid; j < S_max; j += SEL_NT)
+      if (is_cand(mrow, cl, j)) {
+        const float xv = xrow[j];
+        const float e = expf((xv - mx) * u);
+        const float xe = e > 0.f ? xv * e : 0.f;
+        q[0] += e;
+        q[2] += xe;
+        if (long_in_top(ordered_key(xv), j, vthr, tie_from)) {
           q[1] += e;
           q[3] += xe;
         }
@@ -1027,6 +1130,11 @@ hipError_t hk_launch_solve_T_gd(int n_heads, int S_max, const int32_t* cand_len,
                                 float lr, int iters, float tol, float* T_out, float* loss_out,
                                 hipStream_t st) {
   TimedLaunch t(HK_TK_SOLVE_T, st);
+  if (S_max > SEL_NT * 32) {
+    hipLaunchKernelGGL(solve_T_gd_long_kernel, dim3(n_heads), dim3(SEL_NT), 0, st, S_max, cand_len, mask,
+                       x, k, target, T_init, lr, iters, tol, T_out, loss_out);
+    return hipGetLastError();
+  }
   HK_EPT_SWITCH(S_max, hipLaunchKernelGGL((solve_T_gd_kernel<E>), dim3(n_heads), dim3(SEL_NT), 0, st,
                                           S_max, cand_len, mask, x, k, target, T_init, lr, iters, tol,
                                           T_out, loss_out));

@@ -153,6 +153,8 @@ def test_validation_errors_without_gpu(hk):
                                      None) == 1                 # lr
     assert L.hk_calibrate_solve_T_gd(4, 128, P, None, P, P, P, 1.0, 0.05, -1, 0.0, P, None,
                                      None) == 1                 # iters
+    assert L.hk_calibrate_solve_T_gd(4, 262144 + 32, P, None, P, P, P, 1.0, 0.05, 10, 0.0, P, None,
+                                     None) == 3                 # rows too long
     assert L.hk_compress(C.byref(d), P, C.byref(kv), 0, 0, 0.125, None, 0.9, 1, 0, C.byref(alloc),
                          None, P, None, P, 16, None) == 5       # workspace too small
     assert L.hk_compress(C.byref(d), P, C.byref(kv), 0, 0, 0.125, None, 1.5, 1, 0, C.byref(alloc),

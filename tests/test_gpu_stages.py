@@ -449,10 +449,11 @@ def test_solve_T_long_rows(case, S):
 
 
 @pytest.mark.parametrize("case", range(4))
-@pytest.mark.parametrize("S", [1024, 32768])
+@pytest.mark.parametrize("S", [1024, 32768, 65536 + 64])
 def test_solve_T_gd(case, S):
     """Alg. 1 on the GPU against the oracle's Adam iterations (fixed count), on two-level
-    rows (closed form), random rows, rows with -inf candidates and an empty Top-k."""
+    rows (closed form), random rows, rows with -inf candidates and an empty Top-k; the
+    longest rows take the streamed kernel."""
     import paper_2606_28831_amd as hk
     H = 8
     rng = np.random.default_rng(40 + case)

@@ -324,6 +324,8 @@ def topk_mass_and_grad(x, top, theta: float):
     full softmax), and du/dtheta = -u.  Terms whose exponential is 0 add nothing to the
     expectations (so a candidate at -inf is simply absent)."""
     x = np.asarray(x, dtype=np.float64)
+    if x.size == 0:                       # no candidates: no mass, no gradient (R16)
+        return 0.0, 0.0
     u = math.exp(-theta)
     z = u * x
     zmax = float(np.max(z))

@@ -697,6 +697,11 @@ def test_solve_T_gd_edges():
     # an early stop leaves the loss below the tolerance
     T2, l2 = O.solve_T_gd_head(x, cand, 2, 0.7, iters=300, tol=1e-8)
     assert l2 < 1e-8
+    # no candidates: no mass and no gradient, so Adam never moves and the loss is target^2
+    none = np.zeros(4, bool)
+    assert O.topk_mass_and_grad(np.zeros(0), np.zeros(0, bool), 0.3) == (0.0, 0.0)
+    T3, l3 = O.solve_T_gd_head(x, none, 2, 0.7, T_init=1.7, iters=50)
+    assert T3 == pytest.approx(1.7, rel=1e-15) and l3 == pytest.approx(0.49, rel=1e-15)
 
 
 def test_solve_T_gd_first_adam_step():

@@ -448,6 +448,41 @@ def test_solve_T_long_rows(case, S):
             assert float(T[h]) == pytest.approx(closed, rel=2e-3)
 
 
+@pytest.mark.parametrize("solver", ["bisect", "gd"])
+def test_solve_T_long_rows_degenerate(solver):
+    """Streamed temperature searches on degenerate 65536-slot rows, against the oracle: no
+    candidates, k equal to the candidate count, k = 1 among tied maxima, every value equal
+    (the mass does not depend on T), and -inf values among the candidates."""
+    import paper_2606_28831_amd as hk
+    S, H = 65536, 5
+    rng = np.random.default_rng(77)
+    x = np.zeros((H, S), np.float32)
+    cand_len = np.array([0, S, S, S - 320, S], np.int32)
+    ks = np.array([5, S, 1, (S - 320) // 3, 100], np.int32)
+    tg = np.array([0.5, 0.9, 0.3, 0.5, 0.6], np.float32)
+    x[1] = rng.standard_normal(S)
+    x[2] = np.round(rng.standard_normal(S), 1)
+    x[2, rng.permutation(S)[:9]] = 9.0               # nine tied maxima, k = 1
+    x[4] = rng.standard_normal(S)
+    x[4, rng.permutation(S)[:S // 5]] = -np.inf
+    T = torch.empty(H, device=DEV)
+    args = (H, S, torch.tensor(cand_len, device=DEV), None, torch.tensor(x, device=DEV),
+            torch.tensor(ks, device=DEV), torch.tensor(tg, device=DEV))
+    if solver == "bisect":
+        hk.hk_calibrate_solve_T(*args, T)
+    else:
+        hk.hk_calibrate_solve_T_gd(*args, T, T_init=1.0, lr=0.05, iters=200)
+    torch.cuda.synchronize()
+    for h in range(H):
+        cand = np.arange(S) < cand_len[h]
+        if solver == "bisect":
+            want = O.solve_T_head(x[h].astype(np.float64), cand, int(ks[h]), float(tg[h]))
+        else:
+            want, _ = O.solve_T_gd_head(x[h].astype(np.float64), cand, int(ks[h]), float(tg[h]),
+                                        lr=0.05, iters=200)
+        assert float(T[h]) == pytest.approx(want, rel=2e-3), (solver, h, float(T[h]), want)
+
+
 @pytest.mark.parametrize("case", range(4))
 @pytest.mark.parametrize("S", [1024, 32768, 65536 + 64])
 def test_solve_T_gd(case, S):

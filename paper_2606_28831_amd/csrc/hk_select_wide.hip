@@ -633,14 +633,50 @@ __global__ __launch_bounds__(SW_FT) void sw_finish_kernel(
 
   // ties at v: the `take` with the largest slots, i.e. those at or after tie_from
   uint32_t tie_from = take >= f.ntie ? 0u : (uint32_t)S_max;
-  if (take > 0 && take < f.ntie) {
+  const auto slot = [](uint32_t p, int q) { return (uint32_t)q * SW_CH + (p & (SW_CH - 1)); };
+  if (take > 0 && take < f.ntie && S_max <= 32 * SW_FT) {
+    // rows of up to 32768 slots: one pass sets the ties' bits in a slot bitmap (one word per
+    // thread), a suffix count of the words from the top finds the word holding the cut, and
+    // the cut inside it comes from registers
+    uint32_t* tb = reinterpret_cast<uint32_t*>(hw2);     // [S_max / 32] words
+    tb[tid] = 0u;
+    __syncthreads();
+    const uint32_t v = f.v;
+    sw_for_each<true>(f, list, sh, [&](uint32_t kk, uint32_t, uint32_t p, int q) {
+      if (kk == v) {
+        const uint32_t j = slot(p, q);
+        atomicOr(&tb[j >> 5], 1u << (j & 31));
+      }
+    });
+    __syncthreads();
+    // thread t takes word W - 1 - t, so the words descend with the thread and "above" is a
+    // prefix over the threads
+    const int nwords = S_max / 32;
+    const int wd = nwords - 1 - tid;
+    const uint32_t word = wd >= 0 ? tb[wd] : 0u;
+    const uint32_t cnt = (uint32_t)__popc(word);
+    const unsigned long long incl = sw_wave_scan((unsigned long long)cnt);
+    if ((tid & 63) == 63) sh.rc[tid >> 6] = incl;
+    __syncthreads();
+    unsigned long long above = incl - cnt;
+#pragma unroll
+    for (int w = 0; w < SW_FW; ++w)
+      if (w < (tid >> 6)) above += sh.rc[w];
+    if (above < take && above + cnt >= take) {
+      // the (take - above)-th set bit from the top of this word
+      uint32_t x = word;
+      for (unsigned long long i = 1; i < take - above; ++i) x &= ~(0x80000000u >> __clz(x));
+      sh.tie_from = (uint32_t)wd * 32u + (uint32_t)(31 - __clz(x));
+    }
+    __syncthreads();
+    tie_from = sh.tie_from;
+  } else if (take > 0 && take < f.ntie) {
     uint32_t* th = reinterpret_cast<uint32_t*>(hw2);     // ties per 128-slot block (<= 2048)
     th[2 * tid] = 0u;
     th[2 * tid + 1] = 0u;
     if (tid < 4) sh.tmask[tid] = 0u;
     __syncthreads();
     const uint32_t v = f.v;
-    const auto slot = [](uint32_t p, int q) { return (uint32_t)q * SW_CH + (p & (SW_CH - 1)); };
     sw_for_each<true>(f, list, sh, [&](uint32_t kk, uint32_t, uint32_t p, int q) {
       if (kk == v) atomicAdd(&th[slot(p, q) >> SW_TSH], 1u);
     });

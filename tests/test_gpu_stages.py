@@ -679,6 +679,36 @@ def test_decode(name):
         check_lse(ln[s, kvh * G:(kvh + 1) * G], ref_l, rtol, f"lse head {h}")
 
 
+@pytest.mark.parametrize("G", [4, 7])
+def test_decode_long_rows(G):
+    """Decode attention over 131072-token rows (8192 pages per head, so many pages per
+    split and many splits merged), heads of unequal lengths -- the second of a single
+    page -- and masked slots, against the oracle's attention over the valid rows."""
+    import paper_2606_28831_amd as hk
+    import workload as WL
+    cfg = dict(L=1, B=1, Hq=2 * G, Hkv=2, D=128, N=131072, dtype="bf16", W=8, seed=17,
+               recipe="normal")
+    w = WL.make_workload(cfg, DEV, hole_prob=0.1, head_lens=[131072 - 37, 16])
+    kv = hk.PagedKV(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)
+    d = hk.dims(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"])
+    gen = torch.Generator(device=DEV).manual_seed(5)
+    q = (torch.randn(w.NS, cfg["Hq"], cfg["D"], generator=gen, device=DEV) * 2).to(torch.bfloat16)
+    o = torch.empty(w.NS, cfg["Hq"], cfg["D"], device=DEV)
+    lse = torch.empty(w.NS, cfg["Hq"], device=DEV)
+    scale = 1 / math.sqrt(cfg["D"])
+    hk.hk_decode_attn(d, q, kv, scale, o, lse, hk.workspace(hk.OP_DECODE, d, w.max_pages, DEV))
+    torch.cuda.synchronize()
+    host = HostCache(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)
+    qn, on, ln = np64(q), np64(o), np64(lse)
+    for h in range(w.n_heads):
+        K, valid = host.head(h)
+        V, _ = host.head_v(h)
+        ref_o, ref_l = O.decode_head(qn[0, h * G:(h + 1) * G], K, V, valid, scale)
+        for g in range(G):
+            check_prob(on[0, h * G + g], ref_o[g], 2e-3, f"o head {h} g {g}")
+        check_lse(ln[0, h * G:(h + 1) * G], ref_l, 2e-3, f"lse head {h}")
+
+
 def test_decode_after_compaction_equals_masked_original():
     """Tier equivalence (Sec. 3.3.1 HA-Max vs HA-Sparse): attention over the rewritten
     cache equals attention over the original pages restricted to the kept slots."""

@@ -48,7 +48,7 @@ __global__ __launch_bounds__(DEC_NT) void decode_split_kernel(
   const int n = n_pages_arr[h];
   // this head's pages are shared evenly by the launch's splits (at least DEC_PPS_MIN
   // each; pps bounds the share of a full row), so short rows are not left to few waves
-  const int per = min(pps, max((n + n_split - 1) / n_split, DEC_PPS_MIN));
+  const int per = min(min(pps, DEC_PPS), max((n + n_split - 1) / n_split, DEC_PPS_MIN));
   const int p_begin = split * per, p_end = min(p_begin + per, n);
   const int t = lane >> 2, c = lane & 3;
   const int kg = lane / LPR, dc = lane % LPR;
@@ -59,9 +59,20 @@ __global__ __launch_bounds__(DEC_NT) void decode_split_kernel(
     const uint4* src = reinterpret_cast<const uint4*>(q + ((size_t)s * Hq + kv * G) * D);
     for (int i = threadIdx.x; i < G * D * ES / 16; i += DEC_NT) s_q[i] = src[i];
   }
+  // the split's page ids and masks, staged once: a page's loads then wait on no global
+  // read of the table (the per-share bound above keeps the range within DEC_PPS)
+  const int32_t* trow = table + (size_t)h * max_pages;
+  const uint16_t* mrow = masks + (size_t)h * max_pages;
+  __shared__ int32_t s_pid[DEC_PPS];
+  __shared__ uint16_t s_pm[DEC_PPS];
+  for (int i = threadIdx.x; i < p_end - p_begin; i += DEC_NT) {
+    s_pid[i] = trow[p_begin + i];
+    s_pm[i] = mrow[p_begin + i];
+  }
   __syncthreads();
-  auto q_word = [&](int g, int i) -> uint32_t {
-    const uint4 u = s_q[(g * D * ES + c * DQ * ES) / 16 + i / 4];
+  const int q_lane = c * DQ * ES / 16;
+  auto q_word = [&](int qb, int g, int i) -> uint32_t {
+    const uint4 u = s_q[qb + g * D * ES / 16 + i / 4];
     return (i & 3) == 0 ? u.x : (i & 3) == 1 ? u.y : (i & 3) == 2 ? u.z : u.w;
   };
   float m_run[G], l_part[G], o[G][VEC];
@@ -72,17 +83,18 @@ __global__ __launch_bounds__(DEC_NT) void decode_split_kernel(
 #pragma unroll
     for (int e = 0; e < VEC; ++e) o[g][e] = 0.f;
   }
-  const int32_t* trow = table + (size_t)h * max_pages;
-  const uint16_t* mrow = masks + (size_t)h * max_pages;
-
   struct PageRegs {
     uint4 k[QW / 4];
     uint4 v[KPL];
     uint32_t m16;
   };
-  auto load_page = [&](PageRegs& r, int p) {
-    r.m16 = mrow[p];
-    const size_t page = (size_t)trow[p] * HK_PAGE;
+  // the wave's pages are p_begin + wave + DEC_NW * j, j < npg; load_page(r, j) reads
+  // page min(j, npg - 1) and gives it an empty mask when j >= npg
+  const int npg = p_begin + wave < p_end ? (p_end - 1 - p_begin - wave) / DEC_NW + 1 : 0;
+  auto load_page = [&](PageRegs& r, int j) {
+    const int li = wave + DEC_NW * min(j, npg - 1);
+    r.m16 = j < npg ? s_pm[li] : 0u;
+    const size_t page = (size_t)s_pid[li] * HK_PAGE;
     const uint4* ks = reinterpret_cast<const uint4*>(k_pool + (page + t) * D + c * DQ);
 #pragma unroll
     for (int i = 0; i < QW / 4; ++i) r.k[i] = ks[i];
@@ -92,7 +104,6 @@ __global__ __launch_bounds__(DEC_NT) void decode_split_kernel(
   };
   auto process_page = [&](const PageRegs& r) {
     const uint32_t m16 = r.m16;
-    if (m16 == 0u) return;
     uint32_t kw[QW];
 #pragma unroll
     for (int i = 0; i < QW / 4; ++i) {
@@ -102,6 +113,10 @@ __global__ __launch_bounds__(DEC_NT) void decode_split_kernel(
       kw[4 * i + 3] = r.k[i].w;
     }
     const bool valid = (m16 >> t) & 1u;
+    // the query words are read from LDS for every page (an opaque offset keeps the
+    // compiler from hoisting them into 64 more registers per lane)
+    int qb = q_lane;
+    asm volatile("" : "+v"(qb));
     float zl[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) {
@@ -110,11 +125,11 @@ __global__ __launch_bounds__(DEC_NT) void decode_split_kernel(
         typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 #pragma unroll
         for (int i = 0; i < QW; ++i)
-          z = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, q_word(g, i)),
+          z = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, q_word(qb, g, i)),
                                               __builtin_bit_cast(bf16x2, kw[i]), z, false);
       } else {
 #pragma unroll
-        for (int i = 0; i < QW; ++i) z = fmaf(__uint_as_float(q_word(g, i)), __uint_as_float(kw[i]), z);
+        for (int i = 0; i < QW; ++i) z = fmaf(__uint_as_float(q_word(qb, g, i)), __uint_as_float(kw[i]), z);
       }
       z += __shfl_xor(z, 1, 64);
       z += __shfl_xor(z, 2, 64);
@@ -128,9 +143,11 @@ __global__ __launch_bounds__(DEC_NT) void decode_split_kernel(
       pm = fmaxf(pm, __shfl_xor(pm, 8, 64));
       pm = fmaxf(pm, __shfl_xor(pm, 16, 64));
       pm = fmaxf(pm, __shfl_xor(pm, 32, 64));
-      const float mn = fmaxf(m_run[g], pm);     // finite: the page has a valid slot
-      alpha[g] = fast_exp2(m_run[g] - mn);
-      pr[g] = fast_exp2(zl[g] - mn);
+      // a page with no valid slot leaves the state as it is (alpha 1 or the state still
+      // empty, pr 0); the guards keep -inf - -inf out of the exponentials
+      const float mn = fmaxf(m_run[g], pm);
+      alpha[g] = m_run[g] == -INFINITY ? 0.f : fast_exp2(m_run[g] - mn);
+      pr[g] = valid ? fast_exp2(zl[g] - mn) : 0.f;
       m_run[g] = mn;
       l_part[g] = l_part[g] * alpha[g] + (c == 0 ? pr[g] : 0.f);
     }
@@ -163,20 +180,19 @@ __global__ __launch_bounds__(DEC_NT) void decode_split_kernel(
   };
 
   // the wave's next page is loaded (into the other register set) before the current one
-  // is processed; the loop is unrolled by two so both sets stay in registers
-  int p = p_begin + wave;
-  PageRegs ra, rb;
-  if (p < p_end) load_page(ra, p);
-  while (p < p_end) {
-    int pn = p + DEC_NW;
-    if (pn < p_end) load_page(rb, pn);
-    process_page(ra);
-    p = pn;
-    if (p >= p_end) break;
-    pn = p + DEC_NW;
-    if (pn < p_end) load_page(ra, pn);
-    process_page(rb);
-    p = pn;
+  // is processed; the loop is unrolled by two so both sets stay in registers.  Every
+  // trip issues both loads and processes both sets (a page past the wave's run is its
+  // last page again with an empty mask, which leaves the state as it is), so no load is
+  // moved behind the processing it should overlap.
+  if (npg > 0) {
+    PageRegs ra, rb;
+    load_page(ra, 0);
+    for (int j = 0; j < npg; j += 2) {
+      load_page(rb, j + 1);
+      process_page(ra);
+      load_page(ra, j + 2);
+      process_page(rb);
+    }
   }
   // reduce over slot groups (lanes with the same value chunk) and over all lanes for l
 #pragma unroll

@@ -26,6 +26,14 @@ constexpr int DEC_PPS = 128;                // most pages per split (one workgro
 constexpr int DEC_PPS_MIN = 16;             // fewest pages per split
 constexpr int DEC_TARGET_WG = 2048;         // workgroups a launch should offer the chip
 
+// Pages per split for a row of n pages: the row is shared evenly by the launch's n_split
+// splits, at least DEC_PPS_MIN pages each and at most pps (never above DEC_PPS).  Split i
+// covers pages [i * share, min((i + 1) * share, n)); the splits with i * share >= n hold
+// nothing, write nothing, and the merge reads only the ceil(n / share) splits before them.
+__device__ __forceinline__ int decode_share(int n, int n_split, int pps) {
+  return min(min(pps, DEC_PPS), max((n + n_split - 1) / n_split, DEC_PPS_MIN));
+}
+
 template <typename T, int D, int G>
 __global__ __launch_bounds__(DEC_NT) void decode_split_kernel(
     const T* __restrict__ q, const T* __restrict__ k_pool, const T* __restrict__ v_pool,
@@ -45,11 +53,12 @@ __global__ __launch_bounds__(DEC_NT) void decode_split_kernel(
   const int h = blockIdx.y, split = blockIdx.x;
   const int s = h / Hkv, kv = h % Hkv;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int n = n_pages_arr[h];
-  // this head's pages are shared evenly by the launch's splits (at least DEC_PPS_MIN
-  // each; pps bounds the share of a full row), so short rows are not left to few waves
-  const int per = min(min(pps, DEC_PPS), max((n + n_split - 1) / n_split, DEC_PPS_MIN));
+  const int n = min(n_pages_arr[h], max_pages);
+  // this head's pages are shared evenly by the launch's splits, so short rows are not left
+  // to few waves; a split past the row's end leaves at once (the merge skips it)
+  const int per = decode_share(n, n_split, pps);
   const int p_begin = split * per, p_end = min(p_begin + per, n);
+  if (p_begin >= n) return;
   const int t = lane >> 2, c = lane & 3;
   const int kg = lane / LPR, dc = lane % LPR;
 
@@ -237,15 +246,21 @@ __global__ __launch_bounds__(DEC_NT) void decode_split_kernel(
 // One workgroup per KV head merges the split states of its G query heads (App. F).  A
 // 32-lane group per query head finds the running maximum and the rescaled sum over the
 // splits; then each (query head, dim) thread sums its rescaled outputs with independent
-// loads.  Any number of splits.
+// loads.  Only the splits that held pages of the row are read (none for an empty row,
+// which gives o = 0, lse = -inf).
 template <int D>
-__global__ __launch_bounds__(256) void decode_merge_kernel(const float* __restrict__ part, int n_split,
+__global__ __launch_bounds__(256) void decode_merge_kernel(const float* __restrict__ part,
+                                                           const int32_t* __restrict__ n_pages_arr,
+                                                           int max_pages, int n_split_all, int pps,
                                                            int G, int Hq, int Hkv, float* __restrict__ o,
                                                            float* __restrict__ lse) {
   __shared__ float s_M[8], s_L[8];
   const int h = blockIdx.x, s = h / Hkv, kv = h % Hkv;
+  const int n = min(n_pages_arr[h], max_pages);
+  const int share = decode_share(n, n_split_all, pps);
+  const int n_split = n > 0 ? min(n_split_all, (n + share - 1) / share) : 0;
   const size_t stride = (size_t)G * (D + 2);
-  const float* base = part + (size_t)h * n_split * stride;
+  const float* base = part + (size_t)h * n_split_all * stride;
   {
     const int g = threadIdx.x >> 5, l32 = threadIdx.x & 31;
     float M = -INFINITY, L = 0.f;
@@ -486,11 +501,11 @@ hipError_t hk_launch_decode(int NS, int Hq, int Hkv, int D, const void* q, const
   if (!ok) return hipErrorInvalidValue;
   TimedLaunch t(timed ? HK_TK_DECODE_MERGE : -1, st);
   if (D == 128)
-    hipLaunchKernelGGL(decode_merge_kernel<128>, dim3(n_heads), dim3(256), 0, st, part, n_split, G,
-                       Hq, Hkv, o, lse);
+    hipLaunchKernelGGL(decode_merge_kernel<128>, dim3(n_heads), dim3(256), 0, st, part, kv->n_pages,
+                       kv->max_pages, n_split, pps, G, Hq, Hkv, o, lse);
   else
-    hipLaunchKernelGGL(decode_merge_kernel<64>, dim3(n_heads), dim3(256), 0, st, part, n_split, G,
-                       Hq, Hkv, o, lse);
+    hipLaunchKernelGGL(decode_merge_kernel<64>, dim3(n_heads), dim3(256), 0, st, part, kv->n_pages,
+                       kv->max_pages, n_split, pps, G, Hq, Hkv, o, lse);
   return hipGetLastError();
 }
 

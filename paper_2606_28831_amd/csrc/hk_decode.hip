@@ -244,17 +244,22 @@ __global__ __launch_bounds__(DEC_NT) void decode_split_kernel(
 }
 
 // One workgroup per KV head merges the split states of its G query heads (App. F).  A
-// 32-lane group per query head finds the running maximum and the rescaled sum over the
-// splits; then each (query head, dim) thread sums its rescaled outputs with independent
-// loads.  Only the splits that held pages of the row are read (none for an empty row,
-// which gives o = 0, lse = -inf).
+// 32-lane group per query head loads the (m, l) of up to DEC_MRG_CACHE splits once into
+// registers, finds the running maximum M and the rescaled sum L from them, and leaves each
+// split's factor exp2(m - M) in LDS; then each (query head, dim) thread sums its split
+// outputs times those factors with independent loads.  Only the splits that held pages of
+// the row are read (none for an empty row, which gives o = 0, lse = -inf); rows with more
+// splits than the cache holds read the rest from memory.
+constexpr int DEC_MRG_CACHE = 128;            // splits per query head kept in registers / LDS
 template <int D>
 __global__ __launch_bounds__(256) void decode_merge_kernel(const float* __restrict__ part,
                                                            const int32_t* __restrict__ n_pages_arr,
                                                            int max_pages, int n_split_all, int pps,
                                                            int G, int Hq, int Hkv, float* __restrict__ o,
                                                            float* __restrict__ lse) {
+  constexpr int KPL = DEC_MRG_CACHE / 32;     // cached splits per lane
   __shared__ float s_M[8], s_L[8];
+  __shared__ float s_a[8][DEC_MRG_CACHE];
   const int h = blockIdx.x, s = h / Hkv, kv = h % Hkv;
   const int n = min(n_pages_arr[h], max_pages);
   const int share = decode_share(n, n_split_all, pps);
@@ -263,15 +268,33 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(const float* __restri
   const float* base = part + (size_t)h * n_split_all * stride;
   {
     const int g = threadIdx.x >> 5, l32 = threadIdx.x & 31;
+    const float* pg = base + g * (D + 2);
+    float mv[KPL], lv[KPL];
     float M = -INFINITY, L = 0.f;
-    if (g < G) {
-      for (int i = l32; i < n_split; i += 32) M = fmaxf(M, base[i * stride + g * (D + 2) + D]);
+#pragma unroll
+    for (int k = 0; k < KPL; ++k) {
+      const int i = l32 + 32 * k;
+      mv[k] = -INFINITY;
+      lv[k] = 0.f;
+      if (g < G && i < n_split) {
+        mv[k] = pg[i * stride + D];
+        lv[k] = pg[i * stride + D + 1];
+      }
+      M = fmaxf(M, mv[k]);
     }
+    if (g < G)
+      for (int i = l32 + DEC_MRG_CACHE; i < n_split; i += 32) M = fmaxf(M, pg[i * stride + D]);
 #pragma unroll
     for (int x = 1; x < 32; x <<= 1) M = fmaxf(M, __shfl_xor(M, x, 32));
     if (g < G && M != -INFINITY) {
-      for (int i = l32; i < n_split; i += 32) {
-        const float* p = base + i * stride + g * (D + 2);
+#pragma unroll
+      for (int k = 0; k < KPL; ++k) {
+        const float a = exp2f(mv[k] - M);         // 0 for a split past n_split
+        L += lv[k] * a;
+        s_a[g][l32 + 32 * k] = a;
+      }
+      for (int i = l32 + DEC_MRG_CACHE; i < n_split; i += 32) {
+        const float* p = pg + i * stride;
         L += p[D + 1] * exp2f(p[D] - M);
       }
     }
@@ -287,18 +310,20 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(const float* __restri
     const int g = idx / D, d = idx % D;
     const float M = s_M[g], L = s_L[g];
     const float* p = base + g * (D + 2);
+    const float* a = s_a[g];
     float O0 = 0.f, O1 = 0.f, O2 = 0.f, O3 = 0.f;
     if (M != -INFINITY) {
+      const int nc = min(n_split, DEC_MRG_CACHE);
       int i = 0;
-      for (; i + 4 <= n_split; i += 4) {
+      for (; i + 4 <= nc; i += 4) {
         const float* q0 = p + i * stride;
-        const float m0 = q0[D], m1 = q0[stride + D], m2 = q0[2 * stride + D], m3 = q0[3 * stride + D];
         const float v0 = q0[d], v1 = q0[stride + d], v2 = q0[2 * stride + d], v3 = q0[3 * stride + d];
-        O0 = fmaf(v0, exp2f(m0 - M), O0);
-        O1 = fmaf(v1, exp2f(m1 - M), O1);
-        O2 = fmaf(v2, exp2f(m2 - M), O2);
-        O3 = fmaf(v3, exp2f(m3 - M), O3);
+        O0 = fmaf(v0, a[i], O0);
+        O1 = fmaf(v1, a[i + 1], O1);
+        O2 = fmaf(v2, a[i + 2], O2);
+        O3 = fmaf(v3, a[i + 3], O3);
       }
+      for (; i < nc; ++i) O0 = fmaf(p[i * stride + d], a[i], O0);
       for (; i < n_split; ++i) O0 = fmaf(p[i * stride + d], exp2f(p[i * stride + D] - M), O0);
     }
     const float O = (O0 + O1) + (O2 + O3);

@@ -210,3 +210,25 @@ def test_kernel_timing_host_side(hk):
     assert L.hk_timing_enable(C.c_uint32(0xFFFFFFFF)) == 0 and L.hk_timing_enable(C.c_uint32(0)) == 0
     text = open(HEADER).read()
     assert int(re.search(r"HK_TK_COUNT = (\d+)", text).group(1)) == len(hk.TIMED_KERNELS)
+
+
+def test_decode_split_plan_invariants():
+    """The decode split plan (host logic): pages per split a power of two in [16, 128], the
+    splits cover the table width, a launch offers at least 2048 workgroups unless its
+    splits are already the shortest, and the split states fit the workspace the library
+    asks for (sized for 16-page splits)."""
+    import paper_2606_28831_amd as hk
+    for NS, Hkv in ((1, 1), (1, 2), (2, 4), (64, 8), (2048, 8)):
+        for max_pages in (1, 15, 16, 17, 768, 8192, 16384):
+            d = hk.dims(NS, 4 * Hkv, Hkv, 128)
+            n_split, pps = hk.hk_decode_plan(d, max_pages)
+            heads = NS * Hkv
+            assert pps in (16, 32, 64, 128), (NS, Hkv, max_pages, pps)
+            assert n_split == -(-max_pages // pps)
+            assert heads * n_split >= 2048 or pps == 16
+            # the most pages one split can be given never exceeds pps (the kernel stages a
+            # split's page ids in an LDS array of 128)
+            share = min(pps, max(-(-max_pages // n_split), 16))
+            assert share <= pps and share * n_split >= max_pages
+            ws = hk.hk_workspace_size(hk.OP_DECODE, d, max_pages)
+            assert ws >= heads * n_split * 4 * 130 * 4

@@ -683,7 +683,10 @@ def test_decode(name):
 def test_decode_long_rows(G):
     """Decode attention over 131072-token rows (8192 pages per head, so many pages per
     split and many splits merged), heads of unequal lengths -- the second of a single
-    page -- and masked slots, against the oracle's attention over the valid rows."""
+    page -- and masked slots, against the oracle's attention over the valid rows.  The
+    long head spreads over more splits than the merge keeps in registers (128), so the
+    merge's read-from-memory path runs; the one-page head leaves all splits but its first
+    empty."""
     import paper_2606_28831_amd as hk
     import workload as WL
     cfg = dict(L=1, B=1, Hq=2 * G, Hkv=2, D=128, N=131072, dtype="bf16", W=8, seed=17,
@@ -696,6 +699,10 @@ def test_decode_long_rows(G):
     o = torch.empty(w.NS, cfg["Hq"], cfg["D"], device=DEV)
     lse = torch.empty(w.NS, cfg["Hq"], device=DEV)
     scale = 1 / math.sqrt(cfg["D"])
+    n_split, pps = hk.hk_decode_plan(d, w.max_pages)
+    n_long = int(w.n_pages[0].item())
+    share = min(pps, max(-(-n_long // n_split), 16))
+    assert -(-n_long // share) > 128, (n_split, pps)
     hk.hk_decode_attn(d, q, kv, scale, o, lse, hk.workspace(hk.OP_DECODE, d, w.max_pages, DEV))
     torch.cuda.synchronize()
     host = HostCache(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)

@@ -908,6 +908,70 @@ def summarize_pmc(a):
     return {"traffic_summary": path, "hbm_bytes_per_launch": hbm}
 
 
+# the score passes' MFMA: v_mfma_f32_32x32x16_bf16, 32 cycles of one SIMD each
+MFMA_CYCLES_PER_OP = 32
+MFMA_FLOP_PER_OP = 32 * 32 * 16 * 2
+N_SIMD = 256 * 4
+N_XCD = 8
+
+
+def _pmc_dispatches(run_dir, match):
+    """Per-dispatch counter values {counter: value, "ns": duration} of the kernels whose name
+    contains `match`, from a rocprofv3 --pmc output directory."""
+    import csv
+    import glob
+    per = {}
+    for f in glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True):
+        for row in csv.DictReader(open(f)):
+            if match not in row["Kernel_Name"]:
+                continue
+            d = per.setdefault((f, row["Dispatch_Id"]), {})
+            d[row["Counter_Name"]] = float(row["Counter_Value"])
+            if row.get("Start_Timestamp") and row.get("End_Timestamp"):
+                d["ns"] = float(row["End_Timestamp"]) - float(row["Start_Timestamp"])
+    if not per:
+        raise SystemExit(f"no dispatches of '{match}' under {run_dir}")
+    return list(per.values())
+
+
+def summarize_mfma(a):
+    """Write profiles/mfma_<kernel>_<workload>.txt from one rocprofv3 --pmc run with
+    SQ_VALU_MFMA_BUSY_CYCLES (summed over every SIMD: 32 per 32x32x16 MFMA) and
+    GRBM_GUI_ACTIVE (GPU cycles, summed over the 8 XCDs): the MFMA work the counters saw,
+    the clock the kernel ran at, and the MFMA pipes' busy share of the SIMD cycles."""
+    sym = KERNEL_SYMBOL[a.kernel]
+    rows = _pmc_dispatches(a.summarize_mfma, sym)
+    def mean(k):
+        v = [r[k] for r in rows if k in r]
+        if not v:
+            raise SystemExit(f"no {k} for '{sym}' under {a.summarize_mfma}")
+        return sum(v) / len(v), len(v)
+    busy, n = mean("SQ_VALU_MFMA_BUSY_CYCLES")
+    grbm, _ = mean("GRBM_GUI_ACTIVE")
+    ns, _ = mean("ns")
+    ops = busy / MFMA_CYCLES_PER_OP
+    flop = ops * MFMA_FLOP_PER_OP
+    gpu_cycles = grbm / N_XCD
+    out = {"kernel": sym, "workload": a.workload, "dispatches": n,
+           "mfma_busy_cycles_per_dispatch": busy, "mfma_ops_per_dispatch": ops,
+           "mfma_flop_per_dispatch": flop, "duration_us": ns / 1e3,
+           "gpu_cycles_per_dispatch": gpu_cycles, "clock_ghz": gpu_cycles / ns,
+           "mfma_busy_frac_of_simd_cycles": busy / (gpu_cycles * N_SIMD),
+           "mfma_tflops": flop / ns / 1e3, "mfma_frac_bf16_peak": flop / ns / 1e3 / BF16_PEAK_TFLOPS}
+    path = os.path.join(ROOT, "profiles", f"mfma_{a.kernel}_{a.workload}.txt")
+    with open(path, "w") as f:
+        f.write(f"# MFMA work and utilisation of {sym} on workload {a.workload}, per dispatch\n")
+        f.write(f"# made by: {a.command}\n")
+        f.write("# SQ_VALU_MFMA_BUSY_CYCLES is summed over every SIMD (32 per 32x32x16 bf16 MFMA);\n")
+        f.write("# GRBM_GUI_ACTIVE over the 8 XCDs; durations are the dispatches' own timestamps.\n")
+        for k, v in out.items():
+            f.write(f"{k}: {v:.6g}\n" if isinstance(v, float) else f"{k}: {v}\n")
+        f.write(f"source: paper_2606_28831_amd/csrc/{KERNEL_SOURCE[a.kernel]} + hk_internal.h\n")
+        f.write(f"source_sha256: {_source_sha(a.kernel)}\n")
+    out["mfma_summary"] = path
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -937,12 +1001,18 @@ def main():
     ap.add_argument("--summarize-pmc", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "CAL_FETCH_DIR",
                                                           "CAL_WRITE_DIR"),
                     help="write a profiles/traffic_*.txt summary from rocprofv3 --pmc outputs")
+    ap.add_argument("--summarize-mfma", metavar="RUN_DIR", default=None,
+                    help="write a profiles/mfma_*.txt summary from a rocprofv3 --pmc run with "
+                         "SQ_VALU_MFMA_BUSY_CYCLES and GRBM_GUI_ACTIVE")
     ap.add_argument("--kernel", default="compact_gather", choices=sorted(KERNEL_SYMBOL))
     ap.add_argument("--workload", default=None)
     ap.add_argument("--command", default="", help="the profiling command, recorded in the summary")
     args = ap.parse_args()
     if args.summarize_pmc:
         print(json.dumps(summarize_pmc(args)), flush=True)
+        return
+    if args.summarize_mfma:
+        print(json.dumps(summarize_mfma(args)), flush=True)
         return
     args.steps_given = args.steps is not None
     if args.steps is None:

@@ -121,3 +121,50 @@ def test_workload_state_is_one_buffer_and_restores_whole():
     WL.restore_state(w, st)
     for k in names:
         assert torch.equal(getattr(w, k), before[k]), k
+
+
+def test_committed_mfma_summaries_match_the_sources(bench):
+    """Every committed MFMA counter summary was taken on the current kernel source."""
+    files = [f for f in os.listdir(os.path.join(ROOT, "profiles")) if f.startswith("mfma_")]
+    by_symbol = {v: k for k, v in bench.KERNEL_SYMBOL.items()}
+    for f in files:
+        kv = _summary(os.path.join(ROOT, "profiles", f))
+        kernel = by_symbol[kv["kernel"]]
+        assert f == f"mfma_{kernel}_{kv['workload']}.txt"
+        assert kv["source_sha256"] == bench._source_sha(kernel), f
+
+
+def test_summarize_mfma_normalisation(bench, tmp_path, monkeypatch):
+    """Busy cycles are 32 per MFMA summed over the SIMDs, GRBM_GUI_ACTIVE is summed over the
+    XCDs, and the duration comes from each dispatch's timestamps."""
+    root = tmp_path / "repo"
+    shutil.copytree(os.path.join(ROOT, "paper_2606_28831_amd", "csrc"),
+                    root / "paper_2606_28831_amd" / "csrc")
+    (root / "profiles").mkdir()
+    monkeypatch.setattr(bench, "ROOT", str(root))
+    sym = bench.KERNEL_SYMBOL["score_pass1"]
+    run = tmp_path / "pmc"
+    run.mkdir()
+    ops = 7 * 2 ** 20                           # MFMAs per dispatch
+    ns = 300e3                                  # 300 us
+    cycles = 2.0 * ns                           # 2 GHz
+    with open(run / "run_counter_collection.csv", "w", newline="") as fh:
+        w = csv.writer(fh)
+        w.writerow(["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value",
+                    "Start_Timestamp", "End_Timestamp"])
+        for i in range(2):
+            for name, value in (("SQ_VALU_MFMA_BUSY_CYCLES", 32 * ops),
+                                ("GRBM_GUI_ACTIVE", 8 * cycles)):
+                w.writerow([i, f"void hk::{sym}<128, 7>(...)", name, value, 1000, 1000 + ns])
+        w.writerow([9, "hk::other_kernel", "SQ_VALU_MFMA_BUSY_CYCLES", 1, 0, 10])
+    args = argparse.Namespace(summarize_mfma=str(run), kernel="score_pass1", workload="unit",
+                              command="test")
+    out = bench.summarize_mfma(args)
+    assert out["dispatches"] == 2
+    assert out["mfma_ops_per_dispatch"] == pytest.approx(ops)
+    assert out["mfma_flop_per_dispatch"] == pytest.approx(ops * 32768)
+    assert out["clock_ghz"] == pytest.approx(2.0)
+    assert out["mfma_busy_frac_of_simd_cycles"] == pytest.approx(32 * ops / (cycles * 1024))
+    assert out["mfma_tflops"] == pytest.approx(ops * 32768 / ns / 1e3)
+    kv = _summary(out["mfma_summary"])
+    assert kv["source_sha256"] == bench._source_sha("score_pass1")

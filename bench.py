@@ -114,6 +114,27 @@ def _traffic(kernel, workload):
         return None, "malformed counter summary"
 
 
+def _mfma_counters(kernel, workload):
+    """The stored MFMA counter summary of this kernel and workload (flop counted, clock,
+    busy share), or None when there is none or the kernel's source has changed since."""
+    path = os.path.join(ROOT, "profiles", f"mfma_{kernel}_{workload}.txt")
+    if not os.path.isfile(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("source_sha256") != _source_sha(kernel):
+        return None
+    try:
+        return {"flop_counted": float(kv["mfma_flop_per_dispatch"]), "clock_ghz": float(kv["clock_ghz"]),
+                "busy_frac_of_simd_cycles": float(kv["mfma_busy_frac_of_simd_cycles"]),
+                "source": os.path.relpath(path, ROOT)}
+    except (KeyError, ValueError):
+        return None
+
+
 def _roofline(ktime, per_launch, workload):
     """Roofline entry for the kernel with the largest share of the timed region."""
     timed = {k: v for k, v in ktime.items() if k in per_launch}
@@ -314,7 +335,8 @@ def run_compression(args):
         "score_mfma": {"pass1_tflops": per_launch["score_pass1"][1] / (st["score_pass1_merge"] * 1e-3) / 1e12,
                        "pass2_tflops": per_launch["score_pass2"][1] / (st["score_pass2"] * 1e-3) / 1e12,
                        "pass2_frac_bf16_peak": per_launch["score_pass2"][1] / (st["score_pass2"] * 1e-3)
-                       / 1e12 / BF16_PEAK_TFLOPS, "flops_per_pass": per_launch["score_pass2"][1]},
+                       / 1e12 / BF16_PEAK_TFLOPS, "flops_per_pass": per_launch["score_pass2"][1],
+                       "counters": {k: _mfma_counters(k, cfg["name"]) for k in ("score_pass1", "score_pass2")}},
         "ms_per_step_no_kernel_events": ms_per_step_plain,
         "kernel_ms_discovery_step": kernels_discovery,
         "budget": {"mean_kept": kept_mean, "min_frac": float(frac.min()),

@@ -168,3 +168,13 @@ def test_summarize_mfma_normalisation(bench, tmp_path, monkeypatch):
     assert out["mfma_tflops"] == pytest.approx(ops * 32768 / ns / 1e3)
     kv = _summary(out["mfma_summary"])
     assert kv["source_sha256"] == bench._source_sha("score_pass1")
+
+
+def test_bench_line_reads_the_committed_mfma_counters(bench):
+    w = "cfg3_l1_b32_h28x4_d128_n32768_bf16_tempered"
+    for k in ("score_pass1", "score_pass2"):
+        got = bench._mfma_counters(k, w)
+        assert got is not None, k
+        assert 0.0 < got["busy_frac_of_simd_cycles"] < 1.0
+        assert got["flop_counted"] == pytest.approx(2.405e11, rel=1e-3)
+    assert bench._mfma_counters("score_pass1", "no_such_workload") is None

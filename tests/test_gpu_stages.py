@@ -716,6 +716,45 @@ def test_decode_long_rows(G):
         check_lse(ln[0, h * G:(h + 1) * G], ref_l, 2e-3, f"lse head {h}")
 
 
+def test_decode_fully_masked_pages():
+    """Decode attention where whole pages inside a row hold no valid slot: a row's first
+    pages, every third page, and one split's whole range (so a wave and a split start, and
+    stay, with no valid key before the valid ones come), against the oracle."""
+    import paper_2606_28831_amd as hk
+    import workload as WL
+    cfg = dict(L=1, B=4, Hq=16, Hkv=4, D=128, N=4000, dtype="bf16", W=8, seed=23, recipe="normal")
+    w = WL.make_workload(cfg, DEV, hole_prob=0.05, head_lens=[4000, 3000, 2050, 1000] * 4)
+    n = w.n_pages.cpu().numpy()
+    m = w.page_mask.cpu().numpy().copy()
+    for h in range(w.n_heads):
+        m[h, :5] = 0                                   # the row starts with five empty pages
+        m[h, 5:n[h]:3] = 0                             # every third page after them
+        if h % 4 == 0:
+            m[h, 64:128] = 0                           # a whole split's range
+    m[7, :n[7]] = 0                                    # and one row with no valid slot at all
+    w.page_mask.copy_(torch.tensor(m, device=DEV))
+    kv = hk.PagedKV(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)
+    d = hk.dims(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"])
+    gen = torch.Generator(device=DEV).manual_seed(4)
+    q = (torch.randn(w.NS, cfg["Hq"], cfg["D"], generator=gen, device=DEV) * 2).to(torch.bfloat16)
+    o = torch.empty(w.NS, cfg["Hq"], cfg["D"], device=DEV)
+    lse = torch.empty(w.NS, cfg["Hq"], device=DEV)
+    scale = 1 / math.sqrt(cfg["D"])
+    hk.hk_decode_attn(d, q, kv, scale, o, lse, hk.workspace(hk.OP_DECODE, d, w.max_pages, DEV))
+    torch.cuda.synchronize()
+    host = HostCache(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)
+    qn, on, ln = np64(q), np64(o), np64(lse)
+    G = cfg["Hq"] // cfg["Hkv"]
+    for h in range(w.n_heads):
+        s, kvh = h // cfg["Hkv"], h % cfg["Hkv"]
+        K, valid = host.head(h)
+        V, _ = host.head_v(h)
+        ref_o, ref_l = O.decode_head(qn[s, kvh * G:(kvh + 1) * G], K, V, valid, scale)
+        for g in range(G):
+            check_prob(on[s, kvh * G + g], ref_o[g], 2e-3, f"o head {h} g {g}")
+        check_lse(ln[s, kvh * G:(kvh + 1) * G], ref_l, 2e-3, f"lse head {h}")
+
+
 def test_decode_after_compaction_equals_masked_original():
     """Tier equivalence (Sec. 3.3.1 HA-Max vs HA-Sparse): attention over the rewritten
     cache equals attention over the original pages restricted to the kept slots."""

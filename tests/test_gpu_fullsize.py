@@ -8,7 +8,8 @@ temperature and mixture).  Stages that consume the GPU's own outputs are also ch
 their defining properties: the temperature solves its equation on the GPU's inputs (and
 equals the oracle's bisection on them), the selection satisfies the Top-p rule on the GPU's
 probabilities, and the rewritten cache holds exactly the selected rows in order (bytes)
-with the sparse and dense pages in place.  Heads are sampled across the budget range.
+with the sparse and dense pages in place.  Eight heads are sampled across the budget range
+for the oracle comparisons; the Top-p rule is checked on every head.
 """
 import math
 
@@ -62,7 +63,7 @@ def test_full_size_sampled(c):
     torch.cuda.synchronize()
     b = comp.buf
     k_all = np_i(b.k)
-    heads = _sample_heads(k_all, 5)
+    heads = _sample_heads(k_all, 8)
     host = HostCache(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages, heads=heads)
     s_gpu = {h: np64(b.s_attn[h]) for h in heads}
     c_gpu = {h: b.c[h].cpu().numpy() for h in heads}
@@ -148,6 +149,19 @@ def test_full_size_sampled(c):
             assert np.array_equal(got, wk) and np.array_equal(gotv, wv), f"cfg{c} bytes head {h} page {i}"
         for i, (pid, m) in enumerate(sparse + dense):
             assert new_table[npc + i] == pid and new_mask[npc + i] == m, f"cfg{c} kept page head {h}"
+    # beyond the sampled heads: the Top-p rule on every head, each on the values its
+    # selection was made from
+    c_all = b.c.cpu().numpy()
+    sel_all = np_i(b.sel_bits)
+    for h in range(w.n_heads):
+        n = int(pre["n"][h])
+        nd = O.tier_pages(n, cfg["L_dense"], cfg["L_sparse"])[2]
+        m = pre["mask"][h][:n]
+        valid = ((m[:, None] >> np.arange(16)[None, :]) & 1).reshape(-1).astype(bool)
+        cand = np.zeros(S, bool)
+        cand[:len(valid)] = O.candidate_mask(valid, 16 * (n - nd))
+        check_topp_rule(c_all[h], unpack_bits(sel_all[h], S), int(k_all[h]), cand, cfg["p"],
+                        what=f"cfg{c} head {h} (all-heads rule)")
 
 
 @pytest.mark.timeout(900)

@@ -9,7 +9,8 @@ their defining properties: the temperature solves its equation on the GPU's inpu
 equals the oracle's bisection on them), the selection satisfies the Top-p rule on the GPU's
 probabilities, and the rewritten cache holds exactly the selected rows in order (bytes)
 with the sparse and dense pages in place.  Eight heads are sampled across the budget range
-for the oracle comparisons; the Top-p rule is checked on every head.
+for the oracle comparisons; the Top-p rule and the rewritten layout are checked on every
+head, and no physical page may be listed twice.
 """
 import math
 
@@ -150,18 +151,35 @@ def test_full_size_sampled(c):
         for i, (pid, m) in enumerate(sparse + dense):
             assert new_table[npc + i] == pid and new_mask[npc + i] == m, f"cfg{c} kept page head {h}"
     # beyond the sampled heads: the Top-p rule on every head, each on the values its
-    # selection was made from
+    # selection was made from, and the rewritten layout of every head (page counts, masks,
+    # the sparse and dense pages kept in place); no physical page is listed twice
     c_all = b.c.cpu().numpy()
     sel_all = np_i(b.sel_bits)
+    tab_all, n_all = np_i(w.page_table), np_i(w.n_pages)
+    msk_all = np_i(w.page_mask).astype(np.int64) & 0xFFFF
     for h in range(w.n_heads):
         n = int(pre["n"][h])
-        nd = O.tier_pages(n, cfg["L_dense"], cfg["L_sparse"])[2]
+        nc, ns, nd = O.tier_pages(n, cfg["L_dense"], cfg["L_sparse"])
         m = pre["mask"][h][:n]
         valid = ((m[:, None] >> np.arange(16)[None, :]) & 1).reshape(-1).astype(bool)
         cand = np.zeros(S, bool)
         cand[:len(valid)] = O.candidate_mask(valid, 16 * (n - nd))
-        check_topp_rule(c_all[h], unpack_bits(sel_all[h], S), int(k_all[h]), cand, cfg["p"],
+        sel = unpack_bits(sel_all[h], S)
+        check_topp_rule(c_all[h], sel, int(k_all[h]), cand, cfg["p"],
                         what=f"cfg{c} head {h} (all-heads rule)")
+        kept = int((sel[:16 * nc] & valid[:16 * nc]).sum())
+        npc = -(-kept // 16)
+        words = (sel[:16 * n].reshape(n, 16) << np.arange(16)).sum(1)
+        keep = [(int(pre["table"][h][pp]), int(m[pp] & words[pp])) for pp in range(nc, nc + ns)
+                if m[pp] & words[pp]]
+        keep += [(int(pre["table"][h][pp]), int(m[pp])) for pp in range(nc + ns, n)]
+        assert int(n_all[h]) == npc + len(keep), f"cfg{c} n_pages head {h} (all heads)"
+        full = [(1 << 16) - 1] * (npc - 1) + ([(1 << (kept - 16 * (npc - 1))) - 1] if npc else [])
+        assert list(msk_all[h][:npc]) == full, f"cfg{c} condensed masks head {h}"
+        assert [(int(tab_all[h][npc + i]), int(msk_all[h][npc + i])) for i in range(len(keep))] == keep, \
+            f"cfg{c} kept pages head {h}"
+    used = np.concatenate([tab_all[h][:n_all[h]] for h in range(w.n_heads)])
+    assert len(np.unique(used)) == len(used), f"cfg{c}: a physical page listed twice"
 
 
 @pytest.mark.timeout(900)

@@ -7,7 +7,8 @@ host replay with the oracle: decode outputs at sampled steps and LSEs at every s
 attention and merge), the single-pass scores over the decode LSEs at each compression, the
 selection by the Top-p rule on the GPU's own probabilities, and the rewritten cache rows
 byte for byte.  The decode launches must take the 128-page split that the chip-filling rule
-picks for 512 heads per layer over a 768-page table."""
+picks for 512 heads per layer over a 768-page table.  After each segment's appends and each
+rewrite, every page of the pool is listed once or free, never both (all 16384 heads)."""
 import math
 
 import numpy as np
@@ -19,6 +20,18 @@ from hk_testlib import DecodeReplay, check_lse, check_prob, np64, np_i
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
+
+
+def _check_pages_conserved(w, what):
+    """Every page of the pool is either listed once in some head's table (below its page
+    count) or on the free list below its top, never both and never twice."""
+    tab, n = np_i(w.page_table), np_i(w.n_pages)
+    used = tab[np.arange(tab.shape[1])[None, :] < n[:, None]]
+    free = np_i(w.free_ids)[:int(np_i(w.free_top).reshape(-1)[0])]
+    assert len(np.unique(used)) == len(used), f"{what}: a page listed twice"
+    assert len(np.unique(free)) == len(free), f"{what}: a page free twice"
+    assert len(np.intersect1d(used, free)) == 0, f"{what}: a listed page is also free"
+    assert len(used) + len(free) == w.k_pool.shape[0], f"{what}: pages lost"
 
 
 @pytest.mark.timeout(900)
@@ -82,6 +95,7 @@ def test_config5_two_segments_sampled_heads():
             check_lse(lse_gpu[ts, sidx[s], kvh * G:(kvh + 1) * G], ref_lse[h][ts], 2e-3,
                       f"lse seg {seg} head {h}")
         replay.check_cache(w, f"seg {seg} before compression")
+        _check_pages_conserved(w, f"seg {seg} after the appends")
         loop.compress(q_seg[T - W:], lse_seg[T - W:])
         torch.cuda.synchronize()
         b = loop.comp.buf
@@ -91,6 +105,7 @@ def test_config5_two_segments_sampled_heads():
                         {h: np64(b.s_attn[h]) for h in heads}, rows(b.c), rows(b.sel_bits),
                         np_i(b.k), L_dense, p, w.S_max, f"seg {seg}", sidx=sidx)
         replay.check_cache(w, f"seg {seg} after the rewrite")
+        _check_pages_conserved(w, f"seg {seg} after the rewrite")
         print(f"config 5: segment {seg} matches the oracle (kept {[replay.nr[h] for h in heads]})",
               flush=True)
         del q_seg, k_seg, v_seg, lse_seg

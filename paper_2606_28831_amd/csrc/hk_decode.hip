@@ -7,7 +7,10 @@
 // combines the ranges with the merge operator
 //   o(I u J) = (o(I) SE(I) + o(J) SE(J)) / (SE(I) + SE(J)),  SE(I u J) = SE(I) + SE(J).
 // Only pages below n_pages are visited and page masks drop invalid slots, so the work
-// follows each head's own budget.
+// follows each head's own budget: a row's pages are shared by the launch's splits, a split
+// past the row's end exits at once, and the merge reads only the splits that held pages.
+// Each split stages its page ids and masks in LDS, and every wave keeps the next page's
+// loads in flight while it computes the current one.
 //
 // Lane mapping inside a wave, for one 16-slot page:
 //   scores  lane = 4 * t + c: slot t, quarter c of the head dimension; partial dot

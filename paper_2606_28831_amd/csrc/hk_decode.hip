@@ -250,10 +250,15 @@ __global__ __launch_bounds__(DEC_NT) void decode_split_kernel(
 // 32-lane group per query head loads the (m, l) of up to DEC_MRG_CACHE splits once into
 // registers, finds the running maximum M and the rescaled sum L from them, and leaves each
 // split's factor exp2(m - M) in LDS; then each (query head, dim) thread sums its split
-// outputs times those factors with independent loads.  Only the splits that held pages of
-// the row are read (none for an empty row, which gives o = 0, lse = -inf); rows with more
-// splits than the cache holds read the rest from memory.
+// outputs times those factors.  Only the splits that held pages of the row count (none for
+// an empty row, which gives o = 0, lse = -inf).  When the launch has at most
+// DEC_MRG_SPEC splits, every load -- the row's page count, the split states, the thread's
+// split outputs -- is issued at once, before the count of splits that held pages is known,
+// and the states of the others are dropped unread (their memory holds an earlier call's
+// values); otherwise the outputs are loaded after the factors, and rows with more splits
+// than the register cache read the rest from memory.
 constexpr int DEC_MRG_CACHE = 128;            // splits per query head kept in registers / LDS
+constexpr int DEC_MRG_SPEC = 8;               // splits loaded before the split count is known
 template <int D>
 __global__ __launch_bounds__(256) void decode_merge_kernel(const float* __restrict__ part,
                                                            const int32_t* __restrict__ n_pages_arr,
@@ -261,27 +266,54 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(const float* __restri
                                                            int G, int Hq, int Hkv, float* __restrict__ o,
                                                            float* __restrict__ lse) {
   constexpr int KPL = DEC_MRG_CACHE / 32;     // cached splits per lane
+  constexpr int OPT = 8 * D / 256;            // outputs per thread at the largest group (8)
   __shared__ float s_M[8], s_L[8];
   __shared__ float s_a[8][DEC_MRG_CACHE];
   const int h = blockIdx.x, s = h / Hkv, kv = h % Hkv;
-  const int n = min(n_pages_arr[h], max_pages);
-  const int share = decode_share(n, n_split_all, pps);
-  const int n_split = n > 0 ? min(n_split_all, (n + share - 1) / share) : 0;
   const size_t stride = (size_t)G * (D + 2);
   const float* base = part + (size_t)h * n_split_all * stride;
+  const bool spec = n_split_all <= DEC_MRG_SPEC;
+  const int n = min(n_pages_arr[h], max_pages);
+  const int g = threadIdx.x >> 5, l32 = threadIdx.x & 31;
+  const float* pg = base + g * (D + 2);
+  // split states (speculatively up to n_split_all when spec) and the thread's split outputs
+  const int n_load = spec ? n_split_all : 0;
+  float mv[KPL], lv[KPL];
+#pragma unroll
+  for (int k = 0; k < KPL; ++k) {
+    const int i = l32 + 32 * k;
+    mv[k] = -INFINITY;
+    lv[k] = 0.f;
+    if (g < G && i < n_load) {
+      mv[k] = pg[i * stride + D];
+      lv[k] = pg[i * stride + D + 1];
+    }
+  }
+  float ov[OPT][DEC_MRG_SPEC];
+  if (spec) {
+#pragma unroll
+    for (int q = 0; q < OPT; ++q) {
+      const int idx = threadIdx.x + 256 * q;
+      const int gq = idx / D, d = idx % D;
+#pragma unroll
+      for (int i = 0; i < DEC_MRG_SPEC; ++i)
+        ov[q][i] = (idx < G * D && i < n_split_all) ? base[i * stride + gq * (D + 2) + d] : 0.f;
+    }
+  }
+  const int share = decode_share(n, n_split_all, pps);
+  const int n_split = n > 0 ? min(n_split_all, (n + share - 1) / share) : 0;
   {
-    const int g = threadIdx.x >> 5, l32 = threadIdx.x & 31;
-    const float* pg = base + g * (D + 2);
-    float mv[KPL], lv[KPL];
     float M = -INFINITY, L = 0.f;
 #pragma unroll
     for (int k = 0; k < KPL; ++k) {
       const int i = l32 + 32 * k;
-      mv[k] = -INFINITY;
-      lv[k] = 0.f;
-      if (g < G && i < n_split) {
+      if (g < G && i < n_split && !spec) {
         mv[k] = pg[i * stride + D];
         lv[k] = pg[i * stride + D + 1];
+      }
+      if (i >= n_split) {                       // a split that held no pages of this row
+        mv[k] = -INFINITY;
+        lv[k] = 0.f;
       }
       M = fmaxf(M, mv[k]);
     }
@@ -309,28 +341,46 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(const float* __restri
     }
   }
   __syncthreads();
-  for (int idx = threadIdx.x; idx < G * D; idx += blockDim.x) {
-    const int g = idx / D, d = idx % D;
-    const float M = s_M[g], L = s_L[g];
-    const float* p = base + g * (D + 2);
-    const float* a = s_a[g];
+#pragma unroll
+  for (int q = 0; q < OPT; ++q) {
+    const int idx = threadIdx.x + 256 * q;
+    if (idx >= G * D) break;
+    const int gq = idx / D, d = idx % D;
+    const float M = s_M[gq], L = s_L[gq];
+    const float* p = base + gq * (D + 2);
+    const float* a = s_a[gq];
     float O0 = 0.f, O1 = 0.f, O2 = 0.f, O3 = 0.f;
     if (M != -INFINITY) {
-      const int nc = min(n_split, DEC_MRG_CACHE);
-      int i = 0;
-      for (; i + 4 <= nc; i += 4) {
-        const float* q0 = p + i * stride;
-        const float v0 = q0[d], v1 = q0[stride + d], v2 = q0[2 * stride + d], v3 = q0[3 * stride + d];
-        O0 = fmaf(v0, a[i], O0);
-        O1 = fmaf(v1, a[i + 1], O1);
-        O2 = fmaf(v2, a[i + 2], O2);
-        O3 = fmaf(v3, a[i + 3], O3);
+      if (spec) {
+        // the same grouping as below: fours into O0..O3, the rest into O0, slot order
+#pragma unroll
+        for (int i = 0; i + 4 <= DEC_MRG_SPEC; i += 4)
+          if (i + 4 <= n_split) {
+            O0 = fmaf(ov[q][i], a[i], O0);
+            O1 = fmaf(ov[q][i + 1], a[i + 1], O1);
+            O2 = fmaf(ov[q][i + 2], a[i + 2], O2);
+            O3 = fmaf(ov[q][i + 3], a[i + 3], O3);
+          }
+#pragma unroll
+        for (int i = 0; i < DEC_MRG_SPEC; ++i)
+          if (i >= (n_split & ~3) && i < n_split) O0 = fmaf(ov[q][i], a[i], O0);
+      } else {
+        const int nc = min(n_split, DEC_MRG_CACHE);
+        int i = 0;
+        for (; i + 4 <= nc; i += 4) {
+          const float* q0 = p + i * stride;
+          const float v0 = q0[d], v1 = q0[stride + d], v2 = q0[2 * stride + d], v3 = q0[3 * stride + d];
+          O0 = fmaf(v0, a[i], O0);
+          O1 = fmaf(v1, a[i + 1], O1);
+          O2 = fmaf(v2, a[i + 2], O2);
+          O3 = fmaf(v3, a[i + 3], O3);
+        }
+        for (; i < nc; ++i) O0 = fmaf(p[i * stride + d], a[i], O0);
+        for (; i < n_split; ++i) O0 = fmaf(p[i * stride + d], exp2f(p[i * stride + D] - M), O0);
       }
-      for (; i < nc; ++i) O0 = fmaf(p[i * stride + d], a[i], O0);
-      for (; i < n_split; ++i) O0 = fmaf(p[i * stride + d], exp2f(p[i * stride + D] - M), O0);
     }
     const float O = (O0 + O1) + (O2 + O3);
-    const size_t row = (size_t)s * Hq + kv * G + g;
+    const size_t row = (size_t)s * Hq + kv * G + gq;
     o[row * D + d] = (L > 0.f) ? O / L : 0.f;
     if (d == 0) lse[row] = (L > 0.f) ? (M + __log2f(L)) * kLn2 : -INFINITY;
   }

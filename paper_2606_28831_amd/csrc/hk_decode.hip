@@ -150,9 +150,13 @@ __global__ __launch_bounds__(DEC_NT) void decode_split_kernel(
     float pr[G], alpha[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) {
+      // the 4 lanes of a slot hold the same value, so within a 16-lane row the half-row
+      // and row mirrors (lane l <-> 7 - l within 8, l <-> 15 - l) meet every slot of the row
       float pm = zl[g];
-      pm = fmaxf(pm, __shfl_xor(pm, 4, 64));
-      pm = fmaxf(pm, __shfl_xor(pm, 8, 64));
+      pm = fmaxf(pm, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
+                         0, __builtin_bit_cast(int, pm), 0x141, 0xf, 0xf, false)));
+      pm = fmaxf(pm, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
+                         0, __builtin_bit_cast(int, pm), 0x140, 0xf, 0xf, false)));
       pm = fmaxf(pm, __shfl_xor(pm, 16, 64));
       pm = fmaxf(pm, __shfl_xor(pm, 32, 64));
       // a page with no valid slot leaves the state as it is (alpha 1 or the state still

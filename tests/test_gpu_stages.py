@@ -755,6 +755,44 @@ def test_decode_fully_masked_pages():
         check_lse(ln[s, kvh * G:(kvh + 1) * G], ref_l, 2e-3, f"lse head {h}")
 
 
+@pytest.mark.parametrize("max_pages", [128, 144])
+def test_decode_merge_split_count_boundary(max_pages):
+    """The merge loads every split at once up to 8 splits per row and after the split count
+    otherwise: 128 pages at 16 per split make 8 splits, 144 make 9.  Ragged rows (empty,
+    one page, part of the table, all of it) against the oracle."""
+    import paper_2606_28831_amd as hk
+    import workload as WL
+    N = max_pages * 16
+    cfg = dict(L=1, B=2, Hq=8, Hkv=4, D=128, N=N, dtype="bf16", W=8, seed=29, recipe="normal")
+    lens = [N, N - 100, 16, 0, 700, N // 2 + 3, 2000, 1]
+    w = WL.make_workload(cfg, DEV, hole_prob=0.05, head_lens=lens, max_pages=max_pages)
+    kv = hk.PagedKV(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)
+    d = hk.dims(w.NS, cfg["Hq"], cfg["Hkv"], cfg["D"])
+    n_split, pps = hk.hk_decode_plan(d, w.max_pages)
+    assert (n_split, pps) == (max_pages // 16, 16)
+    gen = torch.Generator(device=DEV).manual_seed(6)
+    q = (torch.randn(w.NS, cfg["Hq"], cfg["D"], generator=gen, device=DEV) * 2).to(torch.bfloat16)
+    o = torch.empty(w.NS, cfg["Hq"], cfg["D"], device=DEV)
+    lse = torch.empty(w.NS, cfg["Hq"], device=DEV)
+    scale = 1 / math.sqrt(cfg["D"])
+    ws = hk.workspace(hk.OP_DECODE, d, w.max_pages, DEV)
+    ws.fill_(255)                 # all-ones bytes: every float NaN; split states of splits
+                                  # that held no pages must never be read
+    hk.hk_decode_attn(d, q, kv, scale, o, lse, ws)
+    torch.cuda.synchronize()
+    host = HostCache(w.k_pool, w.v_pool, w.page_table, w.page_mask, w.n_pages)
+    qn, on, ln = np64(q), np64(o), np64(lse)
+    G = cfg["Hq"] // cfg["Hkv"]
+    for h in range(w.n_heads):
+        s, kvh = h // cfg["Hkv"], h % cfg["Hkv"]
+        K, valid = host.head(h)
+        V, _ = host.head_v(h)
+        ref_o, ref_l = O.decode_head(qn[s, kvh * G:(kvh + 1) * G], K, V, valid, scale)
+        for g in range(G):
+            check_prob(on[s, kvh * G + g], ref_o[g], 2e-3, f"o head {h} g {g}")
+        check_lse(ln[s, kvh * G:(kvh + 1) * G], ref_l, 2e-3, f"lse head {h}")
+
+
 def test_decode_after_compaction_equals_masked_original():
     """Tier equivalence (Sec. 3.3.1 HA-Max vs HA-Sparse): attention over the rewritten
     cache equals attention over the original pages restricted to the kept slots."""
